@@ -1,0 +1,13 @@
+"""CPU oracle for the Mixture-of-Translators KV-cache translation.
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's
+CPU-baseline leg use it.  The GPU library never imports it, and it never
+imports the GPU library.  It follows the paper's Definition
+"Mixture-of-Translators" (Sec. 3, Eq. mot_definition) literally, in double
+precision; see ``mot_oracle.c`` for the step-by-step statement.
+"""
+from .oracle import (OracleDims, build_oracle, oracle_translate, oracle_rows,
+                     oracle_depth_ratio_map, oracle_lib_path)
+
+__all__ = ["OracleDims", "build_oracle", "oracle_translate", "oracle_rows",
+           "oracle_depth_ratio_map", "oracle_lib_path"]

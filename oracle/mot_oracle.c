@@ -1,0 +1,347 @@
+/*
+ * Plain CPU oracle for the Mixture-of-Translators (MoT) KV-cache translation.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the slow, obviously-correct
+ * definition that the HIP library is checked against.  Only the tests, the
+ * smoke check and the benchmark's CPU-baseline leg may load it.  It shares no
+ * code, header, table or helper with the GPU library, and it never imports it.
+ *
+ * What it computes (paper: Sec. 3 "Mixture-of-Translators", Definition
+ * "Mixture-of-Translators", Eq. (mot_definition); problem statement in
+ * Sec. 2.1 "Problem Setup", paragraphs "Translation" and "Communication"):
+ *
+ *   for every channel (source layer i -> target layer j), i = layer_map[j] >= 0,
+ *   for X in {K, V} (keys and values translated independently, App. C.2),
+ *   for every context token u = (b, t):
+ *     z_u            = the source cache row of token u in layer i, flattened
+ *                      head-major (index h*D_src + d)
+ *     l_m            = sum_c Wr[m][c] z_u[c] + br[m]              (gate logits)
+ *     g_m            = exp(l_m - max l) / sum_r exp(l_r - max l)  (nonnegative)
+ *     TopK(u)        = indices of the top_k largest g_m (ties: lower index)
+ *     gt_m           = g_m / sum_{r in TopK(u)} g_r,  m in TopK(u)
+ *     Tr_m(z)        = W2_m act(W1_m z + b1_m) + b2_m             (translator)
+ *     out_u          = sum_{m in TopK(u), ascending} gt_m Tr_m(z_u)
+ *     dst[j] row u   = out_u, un-flattened as (h', d') = (o / D_tgt, o % D_tgt)
+ *
+ *   Target layers with layer_map[j] < 0 are not written.
+ *
+ * act is the exact erf GELU, 0.5 a (1 + erf(a / sqrt 2)) (the paper's phi,
+ * App. C.2), or the identity (used by closed-form pins).
+ *
+ * Precision: inputs arrive as float (bf16 values are widened exactly by the
+ * caller); every sum, exp and erf is evaluated in double; outputs are double.
+ * Sums run in plain index order with no blocking or reordering.
+ *
+ * Parity pins (each checked by a CPU test, see tests/test_oracle_pins.py):
+ * one-hot gate == single translator; E = 1 identity translators pass the
+ * mapped source rows through; uniform gate == mean of the translators;
+ * identity activation == closed-form matrix product; GELU against tabulated
+ * normal-CDF values; brute-force scalar loops on 2-token, 2-dim shapes;
+ * token and expert permutation invariance; depth-ratio map properties.
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* Problem dimensions.  Independent of the GPU library's own struct. */
+typedef struct {
+    int32_t L_src, L_tgt;   /* source / target layer counts                 */
+    int32_t B, T;           /* batch, context tokens                        */
+    int32_t H_src, D_src;   /* source KV heads, head dim                    */
+    int32_t H_tgt, D_tgt;   /* target KV heads, head dim                    */
+    int32_t E;              /* number of translators N_Tr                   */
+    int32_t top_k;          /* translators used per token (1..E)            */
+    int32_t hidden;         /* translator hidden width                      */
+    int32_t src_layout;     /* 0: [L][B][T][H][D]   1: [L][B][H][T][D]      */
+    int32_t dst_layout;     /* same encoding for the target cache           */
+    int32_t act;            /* 0: exact-erf GELU    1: identity             */
+} mot_oracle_dims;
+
+enum { OR_OK = 0, OR_BAD_ARG = 1, OR_NO_MEM = 2 };
+
+/* ------------------------------------------------------------------ */
+/* index helpers                                                       */
+/* ------------------------------------------------------------------ */
+
+static size_t cache_index(const mot_oracle_dims* s, int layout, int32_t H, int32_t D,
+                          int32_t layer, int32_t b, int32_t t, int32_t h, int32_t d)
+{
+    size_t L_stride = (size_t)s->B * s->T * H * D;
+    if (layout == 0) /* [L][B][T][H][D] */
+        return (size_t)layer * L_stride + (((size_t)b * s->T + t) * H + h) * D + d;
+    /* [L][B][H][T][D] */
+    return (size_t)layer * L_stride + (((size_t)b * H + h) * s->T + t) * D + d;
+}
+
+static double act_fn(int act, double a)
+{
+    if (act == 1) return a;
+    return 0.5 * a * (1.0 + erf(a / sqrt(2.0)));
+}
+
+/* ------------------------------------------------------------------ */
+/* one token row of one channel, straight from the definition          */
+/* ------------------------------------------------------------------ */
+
+typedef struct {
+    const float *w1, *b1, *w2, *b2, *wr, *br;   /* b* may be NULL (zero)  */
+} oracle_weights;
+
+/* scratch: z[d_in], logits[E], g[E], sel[E], a[hidden], y[d_out] */
+static void translate_row(const mot_oracle_dims* s, const oracle_weights* w,
+                          int32_t j, int32_t x, const double* z,
+                          double* out, double* gates_out,
+                          double* logits, double* g, int* sel, double* hid, double* y)
+{
+    const int32_t d_in = s->H_src * s->D_src;
+    const int32_t d_out = s->H_tgt * s->D_tgt;
+    const int32_t E = s->E, Hd = s->hidden;
+    const size_t unit = (size_t)j * 2 + x;
+
+    /* gate logits l_m = Wr z + br */
+    for (int32_t m = 0; m < E; ++m) {
+        const float* wr = w->wr + (unit * E + m) * d_in;
+        double acc = 0.0;
+        for (int32_t c = 0; c < d_in; ++c) acc += (double)wr[c] * z[c];
+        if (w->br) acc += (double)w->br[unit * E + m];
+        logits[m] = acc;
+    }
+    /* softmax: nonnegative scores that sum to one */
+    double mx = logits[0];
+    for (int32_t m = 1; m < E; ++m) if (logits[m] > mx) mx = logits[m];
+    double den = 0.0;
+    for (int32_t m = 0; m < E; ++m) { g[m] = exp(logits[m] - mx); den += g[m]; }
+    for (int32_t m = 0; m < E; ++m) g[m] /= den;
+
+    /* Top-K selection: repeatedly take the largest remaining score; on a tie
+     * the lower index wins because the scan is ascending with strict '>'. */
+    for (int32_t m = 0; m < E; ++m) sel[m] = 0;
+    for (int32_t k = 0; k < s->top_k; ++k) {
+        int32_t best = -1;
+        for (int32_t m = 0; m < E; ++m)
+            if (!sel[m] && (best < 0 || g[m] > g[best])) best = m;
+        sel[best] = 1;
+    }
+    /* renormalise over the selected set */
+    double gsum = 0.0;
+    for (int32_t m = 0; m < E; ++m) if (sel[m]) gsum += g[m];
+
+    for (int32_t o = 0; o < d_out; ++o) out[o] = 0.0;
+    for (int32_t m = 0; m < E; ++m) {
+        double gt = sel[m] ? g[m] / gsum : 0.0;
+        if (gates_out) gates_out[m] = gt;
+        if (!sel[m]) continue;
+        const size_t em = unit * E + m;
+        /* hidden = act(W1 z + b1) */
+        for (int32_t k = 0; k < Hd; ++k) {
+            const float* w1 = w->w1 + (em * Hd + k) * d_in;
+            double acc = 0.0;
+            for (int32_t c = 0; c < d_in; ++c) acc += (double)w1[c] * z[c];
+            if (w->b1) acc += (double)w->b1[em * Hd + k];
+            hid[k] = act_fn(s->act, acc);
+        }
+        /* Tr_m(z) = W2 hidden + b2 */
+        for (int32_t o = 0; o < d_out; ++o) {
+            const float* w2 = w->w2 + (em * d_out + o) * Hd;
+            double acc = 0.0;
+            for (int32_t k = 0; k < Hd; ++k) acc += (double)w2[k] * hid[k];
+            if (w->b2) acc += (double)w->b2[em * d_out + o];
+            y[o] = acc;
+        }
+        /* gated sum, translators in ascending order */
+        for (int32_t o = 0; o < d_out; ++o) out[o] += gt * y[o];
+    }
+}
+
+static void gather_row(const mot_oracle_dims* s, const float* src, int32_t i,
+                       int32_t b, int32_t t, double* z)
+{
+    for (int32_t h = 0; h < s->H_src; ++h)
+        for (int32_t d = 0; d < s->D_src; ++d)
+            z[h * s->D_src + d] =
+                (double)src[cache_index(s, s->src_layout, s->H_src, s->D_src, i, b, t, h, d)];
+}
+
+/* ------------------------------------------------------------------ */
+/* work distribution: one item = (unit index, row index)               */
+/* ------------------------------------------------------------------ */
+
+typedef struct {
+    const mot_oracle_dims* s;
+    const oracle_weights* w;
+    const float *src_k, *src_v;
+    const int32_t* layer_map;
+    /* either a full run (dst_k/dst_v) or a sampled run (rows/out) */
+    double *dst_k, *dst_v;
+    const int32_t *unit_j, *unit_x;
+    int32_t n_units;
+    const int64_t* rows;
+    int64_t n_rows;
+    double* out;      /* [n_units][n_rows][d_out]  (sampled)  */
+    double* gates;    /* [n_units][n_rows][E] or NULL          */
+    int64_t n_items;
+    int64_t next;     /* shared counter */
+    pthread_mutex_t lock;
+    int failed;
+} oracle_job;
+
+static void* worker(void* arg)
+{
+    oracle_job* jb = (oracle_job*)arg;
+    const mot_oracle_dims* s = jb->s;
+    const int32_t d_in = s->H_src * s->D_src, d_out = s->H_tgt * s->D_tgt;
+    double* z = (double*)malloc(sizeof(double) * d_in);
+    double* lg = (double*)malloc(sizeof(double) * s->E);
+    double* g = (double*)malloc(sizeof(double) * s->E);
+    int* sel = (int*)malloc(sizeof(int) * s->E);
+    double* hid = (double*)malloc(sizeof(double) * s->hidden);
+    double* y = (double*)malloc(sizeof(double) * d_out);
+    double* row = (double*)malloc(sizeof(double) * d_out);
+    double* gt = (double*)malloc(sizeof(double) * s->E);
+    if (!z || !lg || !g || !sel || !hid || !y || !row || !gt) {
+        pthread_mutex_lock(&jb->lock);
+        jb->failed = 1;
+        pthread_mutex_unlock(&jb->lock);
+        goto done;
+    }
+    for (;;) {
+        int64_t item;
+        pthread_mutex_lock(&jb->lock);
+        item = jb->next++;
+        pthread_mutex_unlock(&jb->lock);
+        if (item >= jb->n_items) break;
+        int64_t ui = item / jb->n_rows, ri = item % jb->n_rows;
+        int32_t j = jb->unit_j[ui], x = jb->unit_x[ui];
+        int32_t i = jb->layer_map[j];
+        int64_t r = jb->rows ? jb->rows[ri] : ri;
+        int32_t b = (int32_t)(r / s->T), t = (int32_t)(r % s->T);
+        gather_row(s, x == 0 ? jb->src_k : jb->src_v, i, b, t, z);
+        translate_row(s, jb->w, j, x, z, row, gt, lg, g, sel, hid, y);
+        if (jb->out) {
+            double* o = jb->out + ((size_t)ui * jb->n_rows + ri) * d_out;
+            memcpy(o, row, sizeof(double) * d_out);
+            if (jb->gates)
+                memcpy(jb->gates + ((size_t)ui * jb->n_rows + ri) * s->E, gt,
+                       sizeof(double) * s->E);
+        } else {
+            double* dst = x == 0 ? jb->dst_k : jb->dst_v;
+            for (int32_t o = 0; o < d_out; ++o) {
+                int32_t hh = o / s->D_tgt, dd = o % s->D_tgt;
+                dst[cache_index(s, s->dst_layout, s->H_tgt, s->D_tgt, j, b, t, hh, dd)] = row[o];
+            }
+        }
+    }
+done:
+    free(z); free(lg); free(g); free(sel); free(hid); free(y); free(row); free(gt);
+    return NULL;
+}
+
+static int check_dims(const mot_oracle_dims* s, const int32_t* layer_map)
+{
+    if (!s || !layer_map) return OR_BAD_ARG;
+    if (s->L_src <= 0 || s->L_tgt <= 0 || s->B < 0 || s->T < 0 || s->H_src <= 0 ||
+        s->D_src <= 0 || s->H_tgt <= 0 || s->D_tgt <= 0 || s->E <= 0 || s->hidden <= 0)
+        return OR_BAD_ARG;
+    if (s->top_k < 1 || s->top_k > s->E) return OR_BAD_ARG;
+    if ((s->src_layout != 0 && s->src_layout != 1) || (s->dst_layout != 0 && s->dst_layout != 1))
+        return OR_BAD_ARG;
+    if (s->act != 0 && s->act != 1) return OR_BAD_ARG;
+    for (int32_t j = 0; j < s->L_tgt; ++j)
+        if (layer_map[j] >= s->L_src) return OR_BAD_ARG;
+    return OR_OK;
+}
+
+static int run_job(oracle_job* jb, int nthreads)
+{
+    if (jb->n_items == 0) return OR_OK;
+    if (nthreads < 1) nthreads = 1;
+    if (nthreads > 256) nthreads = 256;
+    pthread_t th[256];
+    pthread_mutex_init(&jb->lock, NULL);
+    int started = 0;
+    for (int k = 0; k < nthreads; ++k)
+        if (pthread_create(&th[k], NULL, worker, jb) == 0) ++started;
+    if (started == 0) worker(jb);
+    for (int k = 0; k < started; ++k) pthread_join(th[k], NULL);
+    pthread_mutex_destroy(&jb->lock);
+    return jb->failed ? OR_NO_MEM : OR_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* public entry points (C ABI, loaded by the test harness via ctypes)  */
+/* ------------------------------------------------------------------ */
+
+/* Full translation: writes every row of every target layer j with
+ * layer_map[j] >= 0 into dst_k / dst_v (double, laid out per dst_layout);
+ * other layers are left untouched. */
+int mot_oracle_translate(const float* src_k, const float* src_v, const int32_t* layer_map,
+                         const float* w1, const float* b1, const float* w2, const float* b2,
+                         const float* wr, const float* br,
+                         double* dst_k, double* dst_v, const mot_oracle_dims* s, int nthreads)
+{
+    int rc = check_dims(s, layer_map);
+    if (rc) return rc;
+    if (!src_k || !src_v || !w1 || !w2 || !wr || !dst_k || !dst_v) return OR_BAD_ARG;
+    oracle_weights w = {w1, b1, w2, b2, wr, br};
+    int32_t* uj = (int32_t*)malloc(sizeof(int32_t) * 2 * s->L_tgt);
+    int32_t* ux = (int32_t*)malloc(sizeof(int32_t) * 2 * s->L_tgt);
+    if (!uj || !ux) { free(uj); free(ux); return OR_NO_MEM; }
+    int32_t nu = 0;
+    for (int32_t j = 0; j < s->L_tgt; ++j)
+        if (layer_map[j] >= 0)
+            for (int32_t x = 0; x < 2; ++x) { uj[nu] = j; ux[nu] = x; ++nu; }
+    oracle_job jb;
+    memset(&jb, 0, sizeof jb);
+    jb.s = s; jb.w = &w; jb.src_k = src_k; jb.src_v = src_v; jb.layer_map = layer_map;
+    jb.dst_k = dst_k; jb.dst_v = dst_v; jb.unit_j = uj; jb.unit_x = ux; jb.n_units = nu;
+    jb.rows = NULL; jb.n_rows = (int64_t)s->B * s->T;
+    jb.n_items = (int64_t)nu * jb.n_rows;
+    rc = run_job(&jb, nthreads);
+    free(uj); free(ux);
+    return rc;
+}
+
+/* Sampled translation: for each listed unit (unit_j[u], unit_x[u]) and each
+ * listed flattened token row r = b*T + t, writes out[u][k][0..d_out) and,
+ * if gates != NULL, the renormalised gates gates[u][k][0..E) (zero for
+ * translators outside the Top-K set).  layer_map[unit_j[u]] must be >= 0. */
+int mot_oracle_rows(const float* src_k, const float* src_v, const int32_t* layer_map,
+                    const float* w1, const float* b1, const float* w2, const float* b2,
+                    const float* wr, const float* br, const mot_oracle_dims* s,
+                    const int32_t* unit_j, const int32_t* unit_x, int32_t n_units,
+                    const int64_t* rows, int64_t n_rows,
+                    double* out, double* gates, int nthreads)
+{
+    int rc = check_dims(s, layer_map);
+    if (rc) return rc;
+    if (!src_k || !src_v || !w1 || !w2 || !wr || !out || !unit_j || !unit_x || !rows)
+        return OR_BAD_ARG;
+    for (int32_t u = 0; u < n_units; ++u) {
+        if (unit_j[u] < 0 || unit_j[u] >= s->L_tgt || (unit_x[u] != 0 && unit_x[u] != 1))
+            return OR_BAD_ARG;
+        if (layer_map[unit_j[u]] < 0) return OR_BAD_ARG;
+    }
+    for (int64_t k = 0; k < n_rows; ++k)
+        if (rows[k] < 0 || rows[k] >= (int64_t)s->B * s->T) return OR_BAD_ARG;
+    oracle_weights w = {w1, b1, w2, b2, wr, br};
+    oracle_job jb;
+    memset(&jb, 0, sizeof jb);
+    jb.s = s; jb.w = &w; jb.src_k = src_k; jb.src_v = src_v; jb.layer_map = layer_map;
+    jb.unit_j = unit_j; jb.unit_x = unit_x; jb.n_units = n_units;
+    jb.rows = rows; jb.n_rows = n_rows; jb.out = out; jb.gates = gates;
+    jb.n_items = (int64_t)n_units * n_rows;
+    return run_job(&jb, nthreads);
+}
+
+/* Depth-ratio channel map (App. C.3, "Depth-Ratio Mapping"): target layer j
+ * reads the source layer at the same relative depth, i = floor(j * L_src / L_tgt),
+ * computed in exact integer arithmetic.  Lower target layers read lower source
+ * layers and the order is preserved. */
+int mot_oracle_depth_ratio_map(int32_t L_src, int32_t L_tgt, int32_t* out)
+{
+    if (L_src <= 0 || L_tgt <= 0 || !out) return OR_BAD_ARG;
+    for (int32_t j = 0; j < L_tgt; ++j) out[j] = (int32_t)(((int64_t)j * L_src) / L_tgt);
+    return OR_OK;
+}

@@ -1,0 +1,169 @@
+"""ctypes wrapper around ``mot_oracle.c`` (plain C, double precision).
+
+TEST INFRASTRUCTURE ONLY (tests, smoke check, CPU-baseline timing).
+
+Array conventions (all numpy, C-contiguous):
+  src_k, src_v : float32 [L_src][B][T][H_src][D_src]  (or [L][B][H][T][D])
+  w1 : float32 [L_tgt][2][E][hidden][d_in]     b1 : [L_tgt][2][E][hidden]
+  w2 : float32 [L_tgt][2][E][d_out][hidden]    b2 : [L_tgt][2][E][d_out]
+  wr : float32 [L_tgt][2][E][d_in]             br : [L_tgt][2][E]
+  index 1 of every weight is 0 = keys, 1 = values; biases may be None.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "mot_oracle.c")
+_LIB = os.path.join(_HERE, "libmot_oracle.so")
+
+
+def oracle_lib_path() -> str:
+    return _LIB
+
+
+def build_oracle(force: bool = True) -> str:
+    """Compile the oracle with gcc.  IEEE semantics: no fast-math, no FMA
+    contraction, so every sum is evaluated exactly as written."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math",
+               "-fPIC", "-shared", "-o", tmp, _SRC, "-lm", "-lpthread"]
+        subprocess.check_call(cmd)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Dims(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "L_src", "L_tgt", "B", "T", "H_src", "D_src", "H_tgt", "D_tgt", "E",
+        "top_k", "hidden", "src_layout", "dst_layout", "act")]
+
+
+@dataclass
+class OracleDims:
+    L_src: int
+    L_tgt: int
+    B: int
+    T: int
+    H_src: int
+    D_src: int
+    H_tgt: int
+    D_tgt: int
+    E: int
+    hidden: int
+    top_k: int = 0          # 0 means "all E translators"
+    src_layout: int = 0     # 0 = BTHD, 1 = BHTD
+    dst_layout: int = 0
+    act: int = 0            # 0 = exact-erf GELU, 1 = identity
+
+    @property
+    def d_in(self) -> int:
+        return self.H_src * self.D_src
+
+    @property
+    def d_out(self) -> int:
+        return self.H_tgt * self.D_tgt
+
+    def _c(self) -> _Dims:
+        return _Dims(self.L_src, self.L_tgt, self.B, self.T, self.H_src, self.D_src,
+                     self.H_tgt, self.D_tgt, self.E, self.top_k or self.E, self.hidden,
+                     self.src_layout, self.dst_layout, self.act)
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build_oracle(force=False)
+        _lib = ctypes.CDLL(_LIB)
+        for fn in (_lib.mot_oracle_translate, _lib.mot_oracle_rows,
+                   _lib.mot_oracle_depth_ratio_map):
+            fn.restype = ctypes.c_int
+    return _lib
+
+
+def _f32(a, name):
+    if a is None:
+        return None
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    return a
+
+
+def _ptr(a):
+    if a is None:
+        return None
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _threads(n):
+    if n is None or n <= 0:
+        n = os.cpu_count() or 1
+    return int(n)
+
+
+def oracle_translate(dims: OracleDims, src_k, src_v, layer_map, w1, b1, w2, b2, wr, br,
+                     dst_k=None, dst_v=None, nthreads=None):
+    """Full translation.  Returns (dst_k, dst_v) as float64 arrays in the
+    dst layout; target layers with layer_map[j] < 0 keep the given contents
+    (NaN when dst_k/dst_v are not supplied)."""
+    lib = _load()
+    arrs = [_f32(a, n) for a, n in ((src_k, "src_k"), (src_v, "src_v"), (w1, "w1"), (b1, "b1"),
+                                    (w2, "w2"), (b2, "b2"), (wr, "wr"), (br, "br"))]
+    lm = np.ascontiguousarray(layer_map, dtype=np.int32)
+    shape = ((dims.L_tgt, dims.B, dims.T, dims.H_tgt, dims.D_tgt) if dims.dst_layout == 0
+             else (dims.L_tgt, dims.B, dims.H_tgt, dims.T, dims.D_tgt))
+    if dst_k is None:
+        dst_k = np.full(shape, np.nan)
+    if dst_v is None:
+        dst_v = np.full(shape, np.nan)
+    dst_k = np.ascontiguousarray(dst_k, dtype=np.float64)
+    dst_v = np.ascontiguousarray(dst_v, dtype=np.float64)
+    c = dims._c()
+    rc = lib.mot_oracle_translate(*[_ptr(a) for a in arrs[:2]], _ptr(lm),
+                                  *[_ptr(a) for a in arrs[2:]], _ptr(dst_k), _ptr(dst_v),
+                                  ctypes.byref(c), _threads(nthreads))
+    if rc != 0:
+        raise ValueError("mot_oracle_translate failed with code %d" % rc)
+    return dst_k, dst_v
+
+
+def oracle_rows(dims: OracleDims, src_k, src_v, layer_map, w1, b1, w2, b2, wr, br,
+                units, rows, nthreads=None, want_gates=False):
+    """Sampled translation of the listed (j, x) units and flattened rows.
+    Returns out[n_units][n_rows][d_out] (and gates[n_units][n_rows][E])."""
+    lib = _load()
+    arrs = [_f32(a, n) for a, n in ((src_k, "src_k"), (src_v, "src_v"), (w1, "w1"), (b1, "b1"),
+                                    (w2, "w2"), (b2, "b2"), (wr, "wr"), (br, "br"))]
+    lm = np.ascontiguousarray(layer_map, dtype=np.int32)
+    uj = np.ascontiguousarray([u[0] for u in units], dtype=np.int32)
+    ux = np.ascontiguousarray([u[1] for u in units], dtype=np.int32)
+    rr = np.ascontiguousarray(rows, dtype=np.int64)
+    out = np.zeros((len(units), len(rr), dims.d_out))
+    gates = np.zeros((len(units), len(rr), dims.E)) if want_gates else None
+    c = dims._c()
+    rc = lib.mot_oracle_rows(*[_ptr(a) for a in arrs[:2]], _ptr(lm),
+                             *[_ptr(a) for a in arrs[2:]], ctypes.byref(c),
+                             _ptr(uj), _ptr(ux), ctypes.c_int32(len(units)),
+                             _ptr(rr), ctypes.c_int64(len(rr)), _ptr(out), _ptr(gates),
+                             _threads(nthreads))
+    if rc != 0:
+        raise ValueError("mot_oracle_rows failed with code %d" % rc)
+    return (out, gates) if want_gates else out
+
+
+def oracle_depth_ratio_map(L_src: int, L_tgt: int) -> np.ndarray:
+    lib = _load()
+    out = np.zeros(L_tgt, dtype=np.int32)
+    rc = lib.mot_oracle_depth_ratio_map(ctypes.c_int32(L_src), ctypes.c_int32(L_tgt), _ptr(out))
+    if rc != 0:
+        raise ValueError("mot_oracle_depth_ratio_map failed with code %d" % rc)
+    return out

@@ -1,0 +1,107 @@
+"""Synthetic workload shapes for the KV-cache translation hot path.
+
+Each workload is shaped like a source/target model pair whose context KV
+caches the paper translates (Sec. 4 "Experimental Setup"; the model pairs of
+Table "qwen25_combined" and App. E.2).  The translator body is a per-token
+Linear(d_in -> hidden) - GELU - Linear(hidden -> d_out) MLP, the router is
+Linear(d_in -> E) + softmax, and every token uses all E translators.
+
+Value recipes (consumed by ``inputs.py``):
+  key_sigma / val_sigma : per-(layer, channel) log-normal scale exp(sigma*N(0,1))
+  key_outlier_frac / key_outlier_mult : fraction of token positions per batch
+      row whose key rows are multiplied (attention-sink-like rows); position 0
+      is always one of them.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field, replace
+from typing import List, Optional
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    dtype: str              # "f32" or "bf16"
+    L_src: int
+    L_tgt: int
+    B: int
+    T: int
+    H_src: int
+    D_src: int
+    H_tgt: int
+    D_tgt: int
+    E: int
+    hidden: int
+    seed: int
+    layer_map: str = "identity"      # "identity" or "depth_ratio"
+    key_sigma: float = 0.0
+    val_sigma: float = 0.0
+    key_outlier_frac: float = 0.0
+    key_outlier_mult: float = 1.0
+    src_layout: int = 0
+    dst_layout: int = 0
+
+    @property
+    def d_in(self) -> int:
+        return self.H_src * self.D_src
+
+    @property
+    def d_out(self) -> int:
+        return self.H_tgt * self.D_tgt
+
+    @property
+    def n_tok(self) -> int:
+        return self.B * self.T
+
+    def units(self) -> int:
+        return 2 * self.L_tgt
+
+    def gemm_flops(self) -> float:
+        """Algorithmic multiply-add flops of one full translation: router,
+        first and second translator layers, for every unit and token."""
+        per_tok_unit = 2.0 * (self.d_in * self.E + self.d_in * self.E * self.hidden
+                              + self.E * self.hidden * self.d_out)
+        return per_tok_unit * self.n_tok * self.units()
+
+    def alg_bytes(self) -> float:
+        """Algorithmic HBM bytes: each distinct source layer read once, all
+        weights read once, the translated cache written once."""
+        es = 4 if self.dtype == "f32" else 2
+        n_src_layers = self.L_src if self.layer_map != "identity" else min(self.L_src, self.L_tgt)
+        src = 2 * n_src_layers * self.n_tok * self.d_in * es
+        w = self.units() * self.E * (self.hidden * self.d_in + self.hidden + self.d_out * self.hidden
+                                     + self.d_out + self.d_in + 1) * es
+        dst = self.units() * self.n_tok * self.d_out * es
+        return float(src + w + dst)
+
+    def with_(self, **kw) -> "Workload":
+        return replace(self, **kw)
+
+
+WORKLOADS: List[Workload] = [
+    Workload("gpt2-small->opt-125m", "f32", L_src=12, L_tgt=12, B=1, T=64, H_src=12, D_src=64,
+             H_tgt=12, D_tgt=64, E=2, hidden=256, seed=0),
+    Workload("qwen2.5-0.5b->qwen2.5-0.5b", "bf16", L_src=24, L_tgt=24, B=4, T=1024, H_src=2,
+             D_src=64, H_tgt=2, D_tgt=64, E=4, hidden=512, seed=1, key_sigma=0.5, val_sigma=0.5),
+    Workload("opt-1.3b->qwen2.5-1.5b", "bf16", L_src=24, L_tgt=28, B=8, T=2048, H_src=32,
+             D_src=64, H_tgt=2, D_tgt=128, E=4, hidden=1024, seed=2, layer_map="depth_ratio"),
+    Workload("qwen2.5-1.5b->qwen2.5-7b", "bf16", L_src=28, L_tgt=28, B=8, T=4096, H_src=2,
+             D_src=128, H_tgt=4, D_tgt=128, E=8, hidden=2048, seed=3, key_sigma=1.0),
+    Workload("qwen2.5-7b->qwen2.5-7b-32k", "bf16", L_src=28, L_tgt=28, B=1, T=32768, H_src=4,
+             D_src=128, H_tgt=4, D_tgt=128, E=8, hidden=2048, seed=4, key_sigma=1.0,
+             key_outlier_frac=0.01, key_outlier_mult=20.0),
+]
+
+BY_NAME = {w.name: w for w in WORKLOADS}
+
+# the headline workload: Qwen2.5-1.5B -> Qwen2.5-7B, B=8, T=4096
+HEADLINE = WORKLOADS[3]
+
+
+def small_variant(w: Workload, L_src: Optional[int] = None, L_tgt: Optional[int] = None,
+                  B: Optional[int] = None, T: Optional[int] = None,
+                  hidden: Optional[int] = None) -> Workload:
+    """Same row dimensions, experts and value recipe; fewer layers/tokens so
+    the oracle finishes in seconds.  Used by the parity tests."""
+    return replace(w, L_src=L_src or w.L_src, L_tgt=L_tgt or w.L_tgt, B=B or w.B,
+                   T=T or w.T, hidden=hidden or w.hidden)

@@ -1,0 +1,132 @@
+"""Seeded synthetic inputs for the KV-cache translation workloads.
+
+This module only draws random numbers and rounds them to the storage type.
+It holds none of the translation arithmetic; both the GPU library's callers
+and the CPU oracle receive exactly the arrays produced here.
+
+Draw order (numpy ``Generator(PCG64(seed))``), all float32:
+  1. source keys   [L_src][B][T][H_src][D_src] ~ N(0, 1)
+  2. source values  same shape                 ~ N(0, 1)
+  3. key channel scales   [L_src][d_in] = exp(key_sigma * N(0,1))   (if key_sigma > 0)
+  4. value channel scales [L_src][d_in] = exp(val_sigma * N(0,1))   (if val_sigma > 0)
+  5. key outlier rows: for each batch row b, ceil(frac*T) positions = {0} plus
+     ceil(frac*T)-1 positions drawn without replacement from 1..T-1; the same
+     positions in every layer; those key rows are multiplied by key_outlier_mult
+  6. weights, for j = 0..L_tgt-1, x = keys, values:
+       router W [E][d_in]  Xavier-uniform  U(+-sqrt(6/(d_in+E)))
+       router b [E]        U(+-1/sqrt(d_in))
+       for m = 0..E-1:
+         W1 [hidden][d_in]  Xavier-uniform U(+-sqrt(6/(d_in+hidden)))
+         b1 [hidden]        U(+-1/sqrt(d_in))
+         W2 [d_out][hidden] Xavier-uniform U(+-sqrt(6/(hidden+d_out)))
+         b2 [d_out]         U(+-1/sqrt(hidden))
+Then, for bf16 workloads, every array is rounded to bfloat16 (round to
+nearest even) and returned widened back to float32 (exact).
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+
+from .configs import Workload
+
+
+@dataclass
+class Inputs:
+    src_k: np.ndarray      # float32, layout per workload.src_layout
+    src_v: np.ndarray
+    w1: np.ndarray         # [L_tgt][2][E][hidden][d_in]
+    b1: np.ndarray         # [L_tgt][2][E][hidden]
+    w2: np.ndarray         # [L_tgt][2][E][d_out][hidden]
+    b2: np.ndarray         # [L_tgt][2][E][d_out]
+    wr: np.ndarray         # [L_tgt][2][E][d_in]
+    br: np.ndarray         # [L_tgt][2][E]
+    dtype: str             # "f32" or "bf16": the storage type the values fit
+
+
+def round_to_bf16(a: np.ndarray, chunk: int = 1 << 24) -> np.ndarray:
+    """Round float32 values to the nearest bfloat16 (ties to even), in place;
+    returns the array (still float32, now exactly bf16-representable)."""
+    flat = a.reshape(-1)
+    u = flat.view(np.uint32)
+    for s in range(0, u.size, chunk):
+        blk = u[s:s + chunk].astype(np.uint64)
+        blk = (blk + 0x7FFF + ((blk >> 16) & 1)) >> 16
+        u[s:s + chunk] = (blk << 16).astype(np.uint32)
+    return a
+
+
+def bf16_bits(a: np.ndarray) -> np.ndarray:
+    """uint16 bit patterns of a float32 array whose values are exactly
+    bf16-representable (as produced by ``round_to_bf16``)."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    if np.any(u & 0xFFFF):
+        raise ValueError("array holds values that are not bf16-representable")
+    return (u >> 16).astype(np.uint16)
+
+
+def _uniform(rng: np.random.Generator, out: np.ndarray, bound: float) -> None:
+    rng.random(out=out, dtype=np.float32)
+    out *= np.float32(2.0 * bound)
+    out -= np.float32(bound)
+
+
+def generate(w: Workload, with_bias: bool = True) -> Inputs:
+    rng = np.random.Generator(np.random.PCG64(w.seed))
+    shp = (w.L_src, w.B, w.T, w.H_src, w.D_src)
+    src_k = rng.standard_normal(shp, dtype=np.float32)
+    src_v = rng.standard_normal(shp, dtype=np.float32)
+    d_in, d_out, E, Hd = w.d_in, w.d_out, w.E, w.hidden
+    if w.key_sigma > 0:
+        s = np.exp(np.float32(w.key_sigma) * rng.standard_normal((w.L_src, d_in), dtype=np.float32))
+        src_k *= s.reshape(w.L_src, 1, 1, w.H_src, w.D_src)
+    if w.val_sigma > 0:
+        s = np.exp(np.float32(w.val_sigma) * rng.standard_normal((w.L_src, d_in), dtype=np.float32))
+        src_v *= s.reshape(w.L_src, 1, 1, w.H_src, w.D_src)
+    if w.key_outlier_frac > 0 and w.T > 0:
+        n_out = int(math.ceil(w.key_outlier_frac * w.T))
+        for b in range(w.B):
+            rest = rng.choice(np.arange(1, w.T), size=max(0, min(n_out - 1, w.T - 1)), replace=False)
+            pos = np.concatenate([[0], np.sort(rest)]).astype(np.int64)
+            src_k[:, b, pos] *= np.float32(w.key_outlier_mult)
+
+    L = w.L_tgt
+    w1 = np.empty((L, 2, E, Hd, d_in), np.float32)
+    b1 = np.empty((L, 2, E, Hd), np.float32)
+    w2 = np.empty((L, 2, E, d_out, Hd), np.float32)
+    b2 = np.empty((L, 2, E, d_out), np.float32)
+    wr = np.empty((L, 2, E, d_in), np.float32)
+    br = np.empty((L, 2, E), np.float32)
+    for j in range(L):
+        for x in range(2):
+            _uniform(rng, wr[j, x], math.sqrt(6.0 / (d_in + E)))
+            _uniform(rng, br[j, x], 1.0 / math.sqrt(d_in))
+            for m in range(E):
+                _uniform(rng, w1[j, x, m], math.sqrt(6.0 / (d_in + Hd)))
+                _uniform(rng, b1[j, x, m], 1.0 / math.sqrt(d_in))
+                _uniform(rng, w2[j, x, m], math.sqrt(6.0 / (Hd + d_out)))
+                _uniform(rng, b2[j, x, m], 1.0 / math.sqrt(Hd))
+    if not with_bias:
+        b1[:] = 0
+        b2[:] = 0
+        br[:] = 0
+    if w.src_layout == 1:
+        src_k = np.ascontiguousarray(src_k.transpose(0, 1, 3, 2, 4))
+        src_v = np.ascontiguousarray(src_v.transpose(0, 1, 3, 2, 4))
+    if w.dtype == "bf16":
+        for a in (src_k, src_v, w1, b1, w2, b2, wr, br):
+            round_to_bf16(a)
+    return Inputs(src_k, src_v, w1, b1, w2, b2, wr, br, w.dtype)
+
+
+def sample_rows(n_tok: int, n: int, seed: int) -> np.ndarray:
+    """A seeded sorted sample of flattened token rows that always includes
+    the first and the last row (the ragged tail of the last token tile)."""
+    if n >= n_tok:
+        return np.arange(n_tok, dtype=np.int64)
+    rng = np.random.Generator(np.random.PCG64(10_000 + seed))
+    mid = rng.choice(np.arange(1, n_tok - 1), size=max(0, n - 2), replace=False)
+    return np.unique(np.concatenate([[0, n_tok - 1], mid]).astype(np.int64))

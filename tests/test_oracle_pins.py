@@ -1,0 +1,345 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics.
+
+Each test reduces the Mixture-of-Translators definition (paper Sec. 3,
+Definition "Mixture-of-Translators", Eq. mot_definition) to a case whose
+answer is known independently of the oracle's own code:
+
+* brute force: pure-Python scalar loops on 2-token, 2-channel shapes;
+* one-hot gate == the single translator (proof of Proposition
+  "Translation-Shift Reduction", App. B): evaluated with numpy matmuls;
+* E = 1 identity translators pass the mapped source rows through exactly;
+  GELU(x) - GELU(-x) = x for an odd/even split translator;
+* uniform gate (MoT-Uni, Sec. 4 "MoT Architecture Ablation") == mean;
+* two-way router == logistic function of the logit difference;
+* exact GELU against tabulated normal-CDF values;
+* renormalised Top-K with a lower-index tie-break;
+* token and translator permutation invariance, layout permutations;
+* depth-ratio channel map (App. C.3) against exact rational arithmetic.
+
+Each case is built so that a dropped bias, a transposed weight, a wrong
+softmax sign or a wrong cache stride changes the answer.
+"""
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+from scipy.special import expit, erf as sp_erf
+
+from oracle import OracleDims, oracle_translate, oracle_rows, oracle_depth_ratio_map
+from oracle.brute import brute_translate
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rand_weights(rng, L_tgt, E, Hd, d_in, d_out, scale=0.5):
+    w1 = rng.standard_normal((L_tgt, 2, E, Hd, d_in)).astype(np.float32) * scale
+    b1 = rng.standard_normal((L_tgt, 2, E, Hd)).astype(np.float32) * scale
+    w2 = rng.standard_normal((L_tgt, 2, E, d_out, Hd)).astype(np.float32) * scale
+    b2 = rng.standard_normal((L_tgt, 2, E, d_out)).astype(np.float32) * scale
+    wr = rng.standard_normal((L_tgt, 2, E, d_in)).astype(np.float32)
+    br = rng.standard_normal((L_tgt, 2, E)).astype(np.float32)
+    return w1, b1, w2, b2, wr, br
+
+
+def _gelu_np(a):
+    return 0.5 * a * (1.0 + sp_erf(a / np.sqrt(2.0)))
+
+
+def _rows(src, dims, i):
+    """source rows of layer i as [B*T][d_in] float64 (layout-aware)."""
+    a = src[i].astype(np.float64)
+    if dims.src_layout == 1:
+        a = a.transpose(0, 2, 1, 3)
+    return a.reshape(dims.B * dims.T, dims.d_in)
+
+
+def _dst_rows(dst, dims, j):
+    a = dst[j]
+    if dims.dst_layout == 1:
+        a = a.transpose(0, 2, 1, 3)
+    return a.reshape(dims.B * dims.T, dims.d_out)
+
+
+def _single(w1, b1, w2, b2, j, x, m, Z, act="gelu"):
+    A = Z @ w1[j, x, m].astype(np.float64).T + b1[j, x, m]
+    U = _gelu_np(A) if act == "gelu" else A
+    return U @ w2[j, x, m].astype(np.float64).T + b2[j, x, m]
+
+
+# ---------------------------------------------------------------- brute force
+
+@pytest.mark.parametrize("top_k", [0, 1])
+@pytest.mark.parametrize("layouts", [(0, 0), (1, 1), (0, 1)])
+def test_brute_force_tiny(oracle_built, top_k, layouts):
+    rng = np.random.default_rng(7)
+    dims = OracleDims(L_src=3, L_tgt=3, B=1, T=2, H_src=1, D_src=2, H_tgt=1, D_tgt=2,
+                      E=2, hidden=2, top_k=top_k, src_layout=layouts[0], dst_layout=layouts[1])
+    if layouts == (0, 1):
+        dims.H_src, dims.D_src, dims.H_tgt, dims.D_tgt, dims.B = 2, 1, 2, 1, 2
+    shp = ((dims.L_src, dims.B, dims.T, dims.H_src, dims.D_src) if dims.src_layout == 0
+           else (dims.L_src, dims.B, dims.H_src, dims.T, dims.D_src))
+    src_k = rng.standard_normal(shp).astype(np.float32)
+    src_v = rng.standard_normal(shp).astype(np.float32)
+    ws = _rand_weights(rng, dims.L_tgt, dims.E, dims.hidden, dims.d_in, dims.d_out)
+    layer_map = np.array([2, -1, 0], np.int32)
+    dk, dv = oracle_translate(dims, src_k, src_v, layer_map, *ws, nthreads=2)
+    ref = brute_translate(dims, src_k, src_v, layer_map, *ws)
+    for (j, x), rows in ref.items():
+        got = _dst_rows(dk if x == 0 else dv, dims, j)
+        np.testing.assert_allclose(got, np.array(rows), rtol=1e-12, atol=1e-13)
+    # the unmapped target layer is untouched (NaN fill survives)
+    assert np.isnan(dk[1]).all() and np.isnan(dv[1]).all()
+
+
+# ---------------------------------------------------------------- one-hot gate
+
+@pytest.mark.parametrize("m0", [0, 2])
+def test_one_hot_gate_is_single_translator(oracle_built, m0):
+    rng = np.random.default_rng(11)
+    dims = OracleDims(L_src=2, L_tgt=2, B=2, T=5, H_src=2, D_src=4, H_tgt=3, D_tgt=2,
+                      E=3, hidden=6)
+    src_k = rng.standard_normal((2, 2, 5, 2, 4)).astype(np.float32)
+    src_v = rng.standard_normal((2, 2, 5, 2, 4)).astype(np.float32)
+    w1, b1, w2, b2, wr, br = _rand_weights(rng, 2, 3, 6, 8, 6)
+    wr[:] = 0
+    br[:] = 0
+    br[:, :, m0] = 1.0e4          # exp(-1e4) underflows to exactly 0 in double
+    layer_map = np.array([1, 0], np.int32)
+    dk, dv = oracle_translate(dims, src_k, src_v, layer_map, w1, b1, w2, b2, wr, br, nthreads=2)
+    for j in range(2):
+        for x, (src, dst) in enumerate(((src_k, dk), (src_v, dv))):
+            Z = _rows(src, dims, layer_map[j])
+            ref = _single(w1, b1, w2, b2, j, x, m0, Z)
+            np.testing.assert_allclose(_dst_rows(dst, dims, j), ref, rtol=1e-12, atol=1e-12)
+
+
+# ---------------------------------------------------------------- E = 1 pass-through
+
+def test_identity_translator_passes_through_exactly(oracle_built):
+    rng = np.random.default_rng(3)
+    d = 6
+    dims = OracleDims(L_src=3, L_tgt=4, B=2, T=3, H_src=2, D_src=3, H_tgt=3, D_tgt=2,
+                      E=1, hidden=d, act=1)
+    src_k = rng.standard_normal((3, 2, 3, 2, 3)).astype(np.float32)
+    src_v = rng.standard_normal((3, 2, 3, 2, 3)).astype(np.float32)
+    eye = np.eye(d, dtype=np.float32)
+    w1 = np.broadcast_to(eye, (4, 2, 1, d, d)).copy()
+    w2 = np.broadcast_to(eye, (4, 2, 1, d, d)).copy()
+    wr = rng.standard_normal((4, 2, 1, d)).astype(np.float32)   # any router: softmax of one logit is 1
+    z = np.zeros
+    layer_map = np.array([2, 0, 0, 1], np.int32)
+    dk, dv = oracle_translate(dims, src_k, src_v, layer_map, w1, z((4, 2, 1, d), np.float32), w2,
+                              z((4, 2, 1, d), np.float32), wr, None, nthreads=2)
+    for j in range(4):
+        for src, dst in ((src_k, dk), (src_v, dv)):
+            assert np.array_equal(_dst_rows(dst, dims, j), _rows(src, dims, layer_map[j]))
+
+
+def test_gelu_odd_split_passes_through(oracle_built):
+    # hidden = 2d, W1 = [I; -I], W2 = [I, -I]: GELU(x) - GELU(-x) = x*Phi(x) + x*Phi(-x) = x
+    rng = np.random.default_rng(5)
+    d = 4
+    dims = OracleDims(L_src=1, L_tgt=1, B=1, T=7, H_src=1, D_src=d, H_tgt=2, D_tgt=2,
+                      E=1, hidden=2 * d)
+    src = rng.standard_normal((1, 1, 7, 1, d)).astype(np.float32) * 3
+    eye = np.eye(d, dtype=np.float32)
+    w1 = np.concatenate([eye, -eye], 0).reshape(1, 1, 1, 2 * d, d)
+    w1 = np.concatenate([w1, w1], 1)
+    w2 = np.concatenate([eye, -eye], 1).reshape(1, 1, 1, d, 2 * d)
+    w2 = np.concatenate([w2, w2], 1)
+    wr = np.zeros((1, 2, 1, d), np.float32)
+    dk, dv = oracle_translate(dims, src, src, np.array([0], np.int32), w1, None, w2, None, wr, None)
+    np.testing.assert_allclose(_dst_rows(dk, dims, 0), _rows(src, dims, 0), rtol=1e-14, atol=1e-15)
+
+
+# ---------------------------------------------------------------- uniform and fixed gates
+
+def test_uniform_gate_is_mean_of_translators(oracle_built):
+    rng = np.random.default_rng(13)
+    E = 4
+    dims = OracleDims(L_src=1, L_tgt=1, B=3, T=4, H_src=1, D_src=5, H_tgt=1, D_tgt=3, E=E, hidden=7)
+    src_k = rng.standard_normal((1, 3, 4, 1, 5)).astype(np.float32)
+    src_v = rng.standard_normal((1, 3, 4, 1, 5)).astype(np.float32)
+    w1, b1, w2, b2, wr, br = _rand_weights(rng, 1, E, 7, 5, 3)
+    wr[:] = 0
+    br[:] = 0
+    dk, dv = oracle_translate(dims, src_k, src_v, np.array([0], np.int32), w1, b1, w2, b2, wr, br)
+    for x, (src, dst) in enumerate(((src_k, dk), (src_v, dv))):
+        Z = _rows(src, dims, 0)
+        ref = sum(_single(w1, b1, w2, b2, 0, x, m, Z) for m in range(E)) / E
+        np.testing.assert_allclose(_dst_rows(dst, dims, 0), ref, rtol=1e-12, atol=1e-13)
+
+
+def test_fixed_nonuniform_gate_linear_closed_form(oracle_built):
+    # Wr = 0, br = log p  =>  g = p exactly (softmax(log p) = p / sum p).
+    # With the identity activation each translator is affine, so the output is
+    # sum_m p_m (W2_m (W1_m z + b1_m) + b2_m), a closed-form matrix product.
+    rng = np.random.default_rng(17)
+    E = 3
+    p = np.array([0.5, 0.3, 0.2])
+    dims = OracleDims(L_src=2, L_tgt=1, B=1, T=6, H_src=2, D_src=2, H_tgt=1, D_tgt=5, E=E,
+                      hidden=3, act=1)
+    src = rng.standard_normal((2, 1, 6, 2, 2)).astype(np.float32)
+    w1, b1, w2, b2, wr, br = _rand_weights(rng, 1, E, 3, 4, 5)
+    wr[:] = 0
+    br[0, :, :] = np.log(p).astype(np.float32)
+    out = oracle_rows(dims, src, src, np.array([1], np.int32), w1, b1, w2, b2, wr, br,
+                      units=[(0, 1)], rows=np.arange(6))
+    Z = _rows(src, dims, 1)
+    pf = np.exp(br[0, 1].astype(np.float64))
+    pf /= pf.sum()
+    ref = sum(pf[m] * ((Z @ w1[0, 1, m].T.astype(np.float64) + b1[0, 1, m]) @ w2[0, 1, m].T.astype(np.float64)
+                       + b2[0, 1, m]) for m in range(E))
+    np.testing.assert_allclose(out[0], ref, rtol=1e-12, atol=1e-13)
+
+
+def test_router_two_way_is_logistic(oracle_built):
+    # E = 2 constant translators Tr_0 = e_0, Tr_1 = e_1 (W1 = W2 = 0, b2 = unit
+    # vectors): the output is the gate vector.  For two logits the softmax is
+    # the logistic function of their difference.
+    rng = np.random.default_rng(19)
+    dims = OracleDims(L_src=1, L_tgt=1, B=1, T=9, H_src=1, D_src=2, H_tgt=1, D_tgt=2, E=2,
+                      hidden=1, act=1)
+    src = rng.standard_normal((1, 1, 9, 1, 2)).astype(np.float32)
+    w1 = np.zeros((1, 2, 2, 1, 2), np.float32)
+    b1 = np.zeros((1, 2, 2, 1), np.float32)
+    w2 = np.zeros((1, 2, 2, 2, 1), np.float32)
+    b2 = np.zeros((1, 2, 2, 2), np.float32)
+    b2[0, :, 0, 0] = 1.0
+    b2[0, :, 1, 1] = 1.0
+    a, b, c, d = 1.5, -0.75, 0.25, 2.0            # deliberately not symmetric
+    wr = np.array([[a, b], [c, d]], np.float32).reshape(1, 1, 2, 2).repeat(2, 1)
+    br = np.array([0.4, -0.3], np.float32).reshape(1, 1, 2).repeat(2, 1)
+    out, gates = oracle_rows(dims, src, src, np.array([0], np.int32), w1, b1, w2, b2, wr, br,
+                             units=[(0, 0)], rows=np.arange(9), want_gates=True)
+    z = src[0, 0, :, 0, :].astype(np.float64)
+    bd = float(br[0, 0, 0]) - float(br[0, 0, 1])     # the float32-stored biases
+    g0 = expit((a - c) * z[:, 0] + (b - d) * z[:, 1] + bd)
+    np.testing.assert_allclose(out[0][:, 0], g0, rtol=1e-13, atol=1e-15)
+    np.testing.assert_allclose(out[0][:, 1], 1 - g0, rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(gates[0][:, 0], g0, rtol=1e-13, atol=1e-15)
+
+
+# ---------------------------------------------------------------- GELU values
+
+def test_gelu_matches_normal_cdf_table(oracle_built):
+    tab = np.loadtxt(os.path.join(GOLDEN, "normal_cdf.txt"))
+    xs = np.concatenate([tab[:, 0], -tab[:, 0]])
+    phis = np.concatenate([tab[:, 1], 1.0 - tab[:, 1]])
+    n = xs.size
+    dims = OracleDims(L_src=1, L_tgt=1, B=1, T=n, H_src=1, D_src=1, H_tgt=1, D_tgt=1, E=1, hidden=1)
+    src = xs.astype(np.float32).reshape(1, 1, n, 1, 1)      # table abscissae are exact in float32
+    one = np.ones((1, 2, 1, 1, 1), np.float32)
+    dk, _ = oracle_translate(dims, src, src, np.array([0], np.int32), one, None, one, None,
+                             np.zeros((1, 2, 1, 1), np.float32), None)
+    np.testing.assert_allclose(dk.reshape(-1), xs * phis, rtol=1e-14, atol=1e-16)
+
+
+# ---------------------------------------------------------------- Top-K
+
+def test_top_k_renormalises_and_breaks_ties_low(oracle_built):
+    rng = np.random.default_rng(23)
+    E = 4
+    dims = OracleDims(L_src=1, L_tgt=1, B=1, T=3, H_src=1, D_src=3, H_tgt=1, D_tgt=2, E=E,
+                      hidden=4, top_k=2)
+    src = rng.standard_normal((1, 1, 3, 1, 3)).astype(np.float32)
+    w1, b1, w2, b2, wr, br = _rand_weights(rng, 1, E, 4, 3, 2)
+    wr[:] = 0
+    p = np.array([0.1, 0.4, 0.2, 0.3])
+    br[0, 0] = np.log(p)
+    out, gates = oracle_rows(dims, src, src, np.array([0], np.int32), w1, b1, w2, b2, wr, br,
+                             units=[(0, 0)], rows=np.arange(3), want_gates=True)
+    pf = np.exp(br[0, 0].astype(np.float64))
+    pf /= pf.sum()
+    sel = [1, 3]                       # the two largest
+    Z = _rows(src, dims, 0)
+    ref = sum(pf[m] / pf[sel].sum() * _single(w1, b1, w2, b2, 0, 0, m, Z) for m in sel)
+    np.testing.assert_allclose(out[0], ref, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(gates[0][0], [0, pf[1] / pf[sel].sum(), 0, pf[3] / pf[sel].sum()],
+                               rtol=1e-13)
+    # ties: uniform scores with top_k = 1 pick translator 0
+    br[:] = 0
+    dims.top_k = 1
+    out, gates = oracle_rows(dims, src, src, np.array([0], np.int32), w1, b1, w2, b2, wr, br,
+                             units=[(0, 0)], rows=np.arange(3), want_gates=True)
+    np.testing.assert_array_equal(gates[0], np.tile([1.0, 0, 0, 0], (3, 1)))
+    np.testing.assert_allclose(out[0], _single(w1, b1, w2, b2, 0, 0, 0, Z), rtol=1e-12, atol=1e-13)
+
+
+# ---------------------------------------------------------------- invariances
+
+def test_identical_translators_equal_single(oracle_built):
+    rng = np.random.default_rng(29)
+    E = 5
+    dims = OracleDims(L_src=1, L_tgt=1, B=2, T=3, H_src=1, D_src=4, H_tgt=2, D_tgt=2, E=E, hidden=3)
+    src = rng.standard_normal((1, 2, 3, 1, 4)).astype(np.float32)
+    w1, b1, w2, b2, wr, br = _rand_weights(rng, 1, E, 3, 4, 4)
+    for a in (w1, b1, w2, b2):
+        a[:, :, 1:] = a[:, :, :1]
+    dk, _ = oracle_translate(dims, src, src, np.array([0], np.int32), w1, b1, w2, b2, wr, br)
+    ref = _single(w1, b1, w2, b2, 0, 0, 0, _rows(src, dims, 0))
+    np.testing.assert_allclose(_dst_rows(dk, dims, 0), ref, rtol=1e-13, atol=1e-14)
+
+
+def test_token_and_translator_permutations(oracle_built):
+    rng = np.random.default_rng(31)
+    E = 3
+    dims = OracleDims(L_src=1, L_tgt=1, B=1, T=8, H_src=1, D_src=4, H_tgt=1, D_tgt=3, E=E, hidden=5)
+    src = rng.standard_normal((1, 1, 8, 1, 4)).astype(np.float32)
+    ws = list(_rand_weights(rng, 1, E, 5, 4, 3))
+    lm = np.array([0], np.int32)
+    dk, _ = oracle_translate(dims, src, src, lm, *ws)
+    perm = rng.permutation(8)
+    dkp, _ = oracle_translate(dims, src[:, :, perm], src[:, :, perm], lm, *ws)
+    assert np.array_equal(dkp[0, 0], dk[0, 0][perm])          # token-level: exact
+    ep = np.array([2, 0, 1])
+    ws_p = [a[:, :, ep] for a in ws]
+    dke, _ = oracle_translate(dims, src, src, lm, *ws_p)
+    np.testing.assert_allclose(dke, dk, rtol=1e-13, atol=1e-14)
+
+
+def test_sampled_rows_equal_full(oracle_built):
+    rng = np.random.default_rng(37)
+    dims = OracleDims(L_src=2, L_tgt=3, B=2, T=5, H_src=2, D_src=2, H_tgt=1, D_tgt=3, E=2, hidden=4,
+                      dst_layout=1)
+    src_k = rng.standard_normal((2, 2, 5, 2, 2)).astype(np.float32)
+    src_v = rng.standard_normal((2, 2, 5, 2, 2)).astype(np.float32)
+    ws = _rand_weights(rng, 3, 2, 4, 4, 3)
+    lm = np.array([0, 1, 1], np.int32)
+    dk, dv = oracle_translate(dims, src_k, src_v, lm, *ws)
+    rows = np.array([9, 0, 4])
+    out = oracle_rows(dims, src_k, src_v, lm, *ws, units=[(2, 1), (0, 0)], rows=rows)
+    assert np.array_equal(out[0], _dst_rows(dv, dims, 2)[rows])
+    assert np.array_equal(out[1], _dst_rows(dk, dims, 0)[rows])
+
+
+def test_layouts_are_permutations(oracle_built):
+    rng = np.random.default_rng(41)
+    base = dict(L_src=2, L_tgt=2, B=2, T=3, H_src=2, D_src=2, H_tgt=2, D_tgt=3, E=2, hidden=3)
+    src = rng.standard_normal((2, 2, 3, 2, 2)).astype(np.float32)
+    ws = _rand_weights(rng, 2, 2, 3, 4, 6)
+    lm = np.array([1, 0], np.int32)
+    ref, _ = oracle_translate(OracleDims(**base), src, src, lm, *ws)
+    src_h = np.ascontiguousarray(src.transpose(0, 1, 3, 2, 4))
+    got, _ = oracle_translate(OracleDims(**base, src_layout=1, dst_layout=1), src_h, src_h, lm, *ws)
+    assert np.array_equal(got, ref.transpose(0, 1, 3, 2, 4))
+
+
+# ---------------------------------------------------------------- depth-ratio map
+
+@pytest.mark.parametrize("L_src,L_tgt", [(24, 28), (28, 28), (12, 12), (28, 24), (32, 24), (24, 32),
+                                         (1, 5), (7, 3)])
+def test_depth_ratio_map(oracle_built, L_src, L_tgt):
+    got = oracle_depth_ratio_map(L_src, L_tgt)
+    ref = np.array([math.floor(Fraction(j * L_src, L_tgt)) for j in range(L_tgt)])
+    assert np.array_equal(got, ref)
+    # same relative depth: i / L_src <= j / L_tgt < (i + 1) / L_src
+    for j, i in enumerate(got):
+        assert Fraction(int(i), L_src) <= Fraction(j, L_tgt) < Fraction(int(i) + 1, L_src)
+    assert got[0] == 0 and np.all(np.diff(got) >= 0) and got[-1] <= L_src - 1
+    if L_src == L_tgt:
+        assert np.array_equal(got, np.arange(L_tgt))
+    if L_tgt >= L_src:                 # every source layer feeds some target layer
+        assert set(got.tolist()) == set(range(L_src))
