@@ -1,0 +1,178 @@
+"""Benchmark: translated KV tokens/s for one full MoT cache translation.
+
+One step = one mot_translate call over every unit (target layer x {K, V})
+of the workload, inputs resident in HBM.  Default workload: Qwen2.5-1.5B ->
+Qwen2.5-7B shapes (28 layers, B=8, T=4096, source rows 2x128, target rows
+4x128, E=8 translators Linear(256->2048)-GELU-Linear(2048->512)), bf16.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "translated KV tokens/sec (all layers) Qwen2.5-1.5B→7B; MFMA util % of peak"
+PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}     # MI355X dense MFMA peaks (AMD spec)
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=3,
+                    help="index into the workload list (default 3: Qwen2.5-1.5B -> 7B)")
+    ap.add_argument("--algo", type=int, default=0, help="0 auto, 1 unfused, 2 fused")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample rows (0 = auto)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: the translation shards with no exchange (by unit or "
+              "by token), and this build runs on a single MI355X; --gpus must be 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_28979_amd import binding as mb
+    from paper_2607_28979_amd.configs import WORKLOADS
+    from paper_2607_28979_amd.inputs import generate, bf16_bits
+
+    w = WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    t0 = time.time()
+    inp = generate(w)
+    log("inputs generated in %.1f s" % (time.time() - t0))
+
+    def dev(a):
+        if w.dtype == "f32":
+            return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+        return torch.from_numpy(bf16_bits(a).view(np.int16)).cuda().view(torch.bfloat16)
+
+    d = {n: dev(getattr(inp, n)) for n in ("src_k", "src_v", "w1", "b1", "w2", "b2", "wr", "br")}
+    tdt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    shape = (w.L_tgt, w.B, w.T, w.H_tgt, w.D_tgt)
+    dk = torch.empty(shape, dtype=tdt, device="cuda")
+    dv = torch.empty(shape, dtype=tdt, device="cuda")
+    lm = (np.arange(w.L_tgt, dtype=np.int32) if w.layer_map == "identity"
+          else mb.depth_ratio_map(w.L_src, w.L_tgt))
+    shapes = mb.Shapes.from_workload(w, algo=args.algo)
+    ws_bytes = mb.workspace_bytes(shapes)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device="cuda") if ws_bytes else None
+
+    def step():
+        mb.translate(d["src_k"], d["src_v"], lm, d["w1"], d["b1"], d["w2"], d["b2"], d["wr"], d["br"],
+                     dk, dv, shapes, workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("warmup done (%d steps)" % args.warmup)
+
+    # timed region: K steps, HIP events on the stream the kernels run on
+    stream = torch.cuda.current_stream()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_begin = time.perf_counter()
+    for k in range(args.steps):
+        starts[k].record(stream)
+        step()
+        ends[k].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_begin
+    per_call_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    ms_per_step = wall * 1e3 / args.steps
+    avg_call_ms = float(np.mean(per_call_ms))
+    med_call_ms = float(np.median(per_call_ms))
+    log("timed %d steps: wall %.3f ms/step, event avg %.3f ms, median %.3f ms"
+        % (args.steps, ms_per_step, avg_call_ms, med_call_ms))
+
+    n_tok = w.n_tok
+    value = n_tok / (ms_per_step / 1e3)
+    flops = w.gemm_flops()
+    fused = args.algo == 2 or (args.algo == 0 and w.dtype == "bf16"
+                              and w.d_in in (128, 256, 512) and w.d_out in (128, 256, 512))
+    achieved_tflops = flops / (avg_call_ms / 1e3) / 1e12
+    peak = PEAK_TFLOPS[w.dtype]
+    roofline = {
+        "bound": "mfma",
+        "kernel": "k_bf16_fused" if fused else "mot_translate (router + gemm1 + gemm2)",
+        "achieved": round(achieved_tflops, 2),
+        "peak": peak,
+        "unit": "TFLOP/s",
+        "frac": round(achieved_tflops / peak, 4),
+        "traffic": None,
+        "alg_flops_per_launch": flops,
+        "alg_bytes_per_launch": w.alg_bytes(),
+        "hbm_gbs_alg": round(w.alg_bytes() / (avg_call_ms / 1e3) / 1e9, 1),
+    }
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, inp, lm, args.cpu_rows)
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded numpy; shapes and value recipe of the model pair)",
+        "config": {"workload": w.name, "L_src": w.L_src, "L_tgt": w.L_tgt, "B": w.B, "T": w.T,
+                   "d_in": w.d_in, "hidden": w.hidden, "d_out": w.d_out, "E": w.E,
+                   "units": w.units(), "parallelism": "single GPU"},
+        "mfma_util_pct": round(100 * achieved_tflops / peak, 2),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(w, inp, lm, rows):
+    """The CPU oracle, untuned, on a bounded sample: every unit for the first
+    `rows` tokens (each token translated through all layers, K and V)."""
+    from oracle import OracleDims, oracle_rows
+    threads = min(16, os.cpu_count() or 1)
+    od = OracleDims(L_src=w.L_src, L_tgt=w.L_tgt, B=w.B, T=w.T, H_src=w.H_src, D_src=w.D_src,
+                    H_tgt=w.H_tgt, D_tgt=w.D_tgt, E=w.E, hidden=w.hidden)
+    units = [(j, x) for j in range(w.L_tgt) if lm[j] >= 0 for x in (0, 1)]
+    per_row_flops = w.gemm_flops() / w.n_tok
+    if rows <= 0:
+        # about 15 s of work at ~1 GFLOP/s per thread
+        rows = int(max(1, min(w.n_tok, 15e9 * threads / per_row_flops)))
+    sample = np.arange(rows, dtype=np.int64)
+    t0 = time.perf_counter()
+    oracle_rows(od, inp.src_k, inp.src_v, lm, inp.w1, inp.b1, inp.w2, inp.b2, inp.wr, inp.br,
+                units=units, rows=sample, nthreads=threads)
+    dt = time.perf_counter() - t0
+    log("cpu oracle: %d rows x %d units in %.2f s on %d threads" % (rows, len(units), dt, threads))
+    return {"value": round(rows / dt, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": "first %d of %d tokens, all %d units (K and V of every layer), fp64"
+                      % (rows, w.n_tok, len(units)),
+            "seconds": round(dt, 2)}
+
+
+if __name__ == "__main__":
+    main()

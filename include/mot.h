@@ -1,0 +1,179 @@
+/*
+ * libmot — Mixture-of-Translators KV-cache translation on AMD Instinct MI355X
+ * (gfx950).  Plain C ABI: device pointers, host structs of sizes, status codes.
+ *
+ * Operation (paper Sec. 2.1 "Problem Setup", paragraphs "Translation" and
+ * "Communication"; Sec. 3, Definition "Mixture-of-Translators", Eq.
+ * mot_definition; translator activation phi = GELU, App. C.2):
+ *
+ *   A source model's context KV cache is translated into the target model's
+ *   cache space.  A channel (i, j) connects source layer i to target layer j;
+ *   layer_map[j] = i lists the channels (App. C.3 "Depth-Ratio Mapping" gives
+ *   the default map, mot_depth_ratio_map below).  For every channel, for keys
+ *   and for values separately, every context token row z (the source cache row
+ *   of one token, flattened head-major: index h*D_src + d) is translated as
+ *
+ *       g      = softmax(Wr z + br)                   (E nonnegative gates)
+ *       Tr_m z = W2_m GELU(W1_m z + b1_m) + b2_m     (m = 0..E-1)
+ *       out    = sum_m g_m Tr_m z                     (all E translators:
+ *                                                      Top-K with K = E)
+ *
+ *   and written into target layer j, un-flattened as (h', d') =
+ *   (o / D_tgt, o % D_tgt).  GELU is the exact-erf GELU, x * Phi(x).
+ *
+ * Terms.  d_in = H_src*D_src, d_out = H_tgt*D_tgt, N_tok = B*T.  A "unit" is
+ * one (target layer j, X in {K, V}) with layer_map[j] >= 0.
+ */
+#ifndef MOT_H
+#define MOT_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOT_ABI_VERSION 1
+#define MOT_MAX_LAYERS 256   /* L_src, L_tgt <= MOT_MAX_LAYERS               */
+#define MOT_MAX_EXPERTS 16   /* E <= MOT_MAX_EXPERTS                         */
+
+typedef enum {
+    MOT_OK = 0,
+    MOT_ERR_NULL_ARG = 1,            /* a required pointer is NULL                */
+    MOT_ERR_BAD_SHAPE = 2,           /* a size is <= 0, too large, or inconsistent */
+    MOT_ERR_BAD_LAYER_MAP = 3,       /* layer_map[j] >= L_src or < -1             */
+    MOT_ERR_UNSUPPORTED = 4,         /* valid but not implemented (see below)     */
+    MOT_ERR_MISALIGNED = 5,          /* a device pointer is not 16-byte aligned   */
+    MOT_ERR_WORKSPACE_TOO_SMALL = 6, /* caller workspace below the minimum        */
+    MOT_ERR_HIP = 7                  /* a HIP runtime call or launch failed       */
+} mot_status;
+
+typedef enum { MOT_F32 = 0, MOT_BF16 = 1 } mot_dtype;
+typedef enum { MOT_LAYOUT_BTHD = 0, MOT_LAYOUT_BHTD = 1 } mot_layout;
+typedef enum { MOT_ACT_GELU = 0, MOT_ACT_IDENTITY = 1 } mot_act;
+typedef enum { MOT_ALGO_AUTO = 0, MOT_ALGO_UNFUSED = 1, MOT_ALGO_FUSED = 2 } mot_algo;
+
+/*
+ * Problem sizes and options (host struct, read during the call only).
+ *   L_src, L_tgt   source / target layer counts (1..MOT_MAX_LAYERS)
+ *   B, T           batch and context tokens (B*T >= 0; 0 is a no-op)
+ *   H_src, D_src   source KV heads and head dim
+ *   H_tgt, D_tgt   target KV heads and head dim
+ *   E              translators per unit (1..MOT_MAX_EXPERTS)
+ *   top_k          translators used per token; must equal E (dense mixture)
+ *   hidden         translator hidden width
+ *   dtype          MOT_F32: fp32 storage and math (erf GELU, expf softmax).
+ *                  MOT_BF16: bf16 storage; fp32 accumulation; fp32 gates;
+ *                  the gate-scaled hidden activation is rounded to bf16
+ *                  before the second translator layer; outputs rounded to
+ *                  nearest even.
+ *   src_layout     layout of each source layer: BTHD [B][T][H][D] or BHTD
+ *   dst_layout     layout of each target layer, same encoding
+ *   act            MOT_ACT_GELU (the method) or MOT_ACT_IDENTITY (tests)
+ *   algo           kernel path: MOT_ALGO_AUTO picks; MOT_ALGO_FUSED = one
+ *                  kernel per token tile (bf16 only; d_in and d_out in
+ *                  {128, 256, 512}; no workspace); MOT_ALGO_UNFUSED = router,
+ *                  then two grouped GEMMs through a hidden-activation
+ *                  workspace.  Requesting an impossible path returns
+ *                  MOT_ERR_UNSUPPORTED.  All paths compute the same function.
+ *   workspace      optional device scratch; NULL = library-owned buffer
+ *   workspace_bytes size of `workspace` in bytes
+ *
+ * Supported sizes (others return MOT_ERR_UNSUPPORTED):
+ *   MOT_BF16: D_src, D_tgt multiples of 8; d_in multiple of 64;
+ *             hidden multiple of 64; d_out multiple of 32.
+ *   MOT_F32:  D_src, D_tgt multiples of 4; d_in, hidden multiples of 4.
+ */
+typedef struct {
+    int32_t L_src, L_tgt;
+    int32_t B, T;
+    int32_t H_src, D_src;
+    int32_t H_tgt, D_tgt;
+    int32_t E, top_k, hidden;
+    int32_t dtype, src_layout, dst_layout, act, algo;
+    void* workspace;
+    size_t workspace_bytes;
+} mot_shapes;
+
+/*
+ * Translator weights: host struct of device pointers, element type = dtype,
+ * nn.Linear layout ([out][in]); index 1 of every array is 0 = keys, 1 = values.
+ *   w1 [L_tgt][2][E][hidden][d_in]     b1 [L_tgt][2][E][hidden]   (may be NULL)
+ *   w2 [L_tgt][2][E][d_out][hidden]    b2 [L_tgt][2][E][d_out]    (may be NULL)
+ * Weights are indexed by TARGET layer: two target layers that read the same
+ * source layer still have their own translators.
+ */
+typedef struct {
+    const void* w1;
+    const void* b1;
+    const void* w2;
+    const void* b2;
+} mot_translator_weights;
+
+/* Router (gate) weights, element type = dtype:
+ *   w [L_tgt][2][E][d_in]    b [L_tgt][2][E] (may be NULL)                   */
+typedef struct {
+    const void* w;
+    const void* b;
+} mot_router_weights;
+
+/*
+ * mot_translate — translate the source context cache into the target layout.
+ *
+ *   src_k, src_v  device, [L_src] x (src_layout) of dtype
+ *   layer_map     HOST int32[L_tgt]; layer_map[j] in [0, L_src) reads that
+ *                 source layer, -1 leaves target layer j untouched
+ *   tw, rw        translator / router weights (above)
+ *   dst_k, dst_v  device, [L_tgt] x (dst_layout) of dtype; only mapped layers
+ *                 are written
+ *   shapes        sizes and options (above)
+ *   stream        HIP stream the work is enqueued on (0 = default stream)
+ *
+ * B*T == 0 is a valid no-op that inspects no pointer.
+ *
+ * Asynchronous with respect to the host; results are ready when `stream`
+ * reaches this point.  All argument checks run before anything is enqueued:
+ * on any error nothing is launched and the outputs are untouched.  Device
+ * pointers must be 16-byte aligned; dst must not overlap src, weights or the
+ * workspace.  With workspace == NULL the library uses a per-device buffer it
+ * owns (grown with hipMalloc on first need, kept until process exit); calls
+ * that overlap in time on different streams of one device must then pass
+ * their own workspaces.  No call retains any pointer after it returns.
+ */
+mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* layer_map,
+                         const mot_translator_weights* tw, const mot_router_weights* rw,
+                         void* dst_k, void* dst_v, const mot_shapes* shapes,
+                         hipStream_t stream);
+
+/*
+ * Workspace bytes mot_translate needs for `shapes` (its dtype, sizes and
+ * options; the workspace fields are ignored).  0 when the chosen kernels need
+ * none.  A smaller caller workspace that is still >= the per-unit minimum is
+ * accepted and processed in smaller unit groups.  Returns SIZE_MAX when the
+ * shapes are invalid or unsupported (mot_last_error() says why).
+ */
+size_t mot_workspace_bytes(const mot_shapes* shapes);
+
+/*
+ * Depth-ratio channel map (paper App. C.3, "Depth-Ratio Mapping"): target
+ * layer j reads source layer floor(j * L_src / L_tgt), in exact integer
+ * arithmetic.  out: host int32[L_tgt].
+ */
+mot_status mot_depth_ratio_map(int32_t L_src, int32_t L_tgt, int32_t* out);
+
+/* Static text for a status code. */
+const char* mot_status_string(mot_status status);
+
+/* Detail of the last error raised on the calling thread ("" if none). */
+const char* mot_last_error(void);
+
+/* MOT_ABI_VERSION of the loaded library. */
+int mot_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOT_H */

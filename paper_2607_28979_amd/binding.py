@@ -1,0 +1,191 @@
+"""Thin ctypes binding of libmot (argument marshalling only).
+
+Every step of the translation runs in the HIP kernels of ``csrc/libmot.so``.
+This module turns torch tensors into device pointers and the current torch
+stream into a ``hipStream_t``; it has no compute path of its own and raises
+``MotError`` when the library is missing or a call fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(HERE, "csrc", "libmot.so")
+
+MOT_F32, MOT_BF16 = 0, 1
+LAYOUT_BTHD, LAYOUT_BHTD = 0, 1
+ACT_GELU, ACT_IDENTITY = 0, 1
+ALGO_AUTO, ALGO_UNFUSED, ALGO_FUSED = 0, 1, 2
+
+STATUS = {0: "MOT_OK", 1: "MOT_ERR_NULL_ARG", 2: "MOT_ERR_BAD_SHAPE", 3: "MOT_ERR_BAD_LAYER_MAP",
+          4: "MOT_ERR_UNSUPPORTED", 5: "MOT_ERR_MISALIGNED", 6: "MOT_ERR_WORKSPACE_TOO_SMALL",
+          7: "MOT_ERR_HIP"}
+
+EXPORTED = ("mot_translate", "mot_workspace_bytes", "mot_depth_ratio_map", "mot_status_string",
+            "mot_last_error", "mot_abi_version")
+
+
+class MotError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        self.status = status
+        self.name = STATUS.get(status, "MOT_ERR_%d" % status)
+        super().__init__("%s: %s" % (self.name, detail))
+
+
+class _Shapes(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "L_src", "L_tgt", "B", "T", "H_src", "D_src", "H_tgt", "D_tgt", "E", "top_k", "hidden",
+        "dtype", "src_layout", "dst_layout", "act", "algo")] + [
+        ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
+
+
+class _TW(ctypes.Structure):
+    _fields_ = [("w1", ctypes.c_void_p), ("b1", ctypes.c_void_p), ("w2", ctypes.c_void_p),
+                ("b2", ctypes.c_void_p)]
+
+
+class _RW(ctypes.Structure):
+    _fields_ = [("w", ctypes.c_void_p), ("b", ctypes.c_void_p)]
+
+
+@dataclass
+class Shapes:
+    L_src: int
+    L_tgt: int
+    B: int
+    T: int
+    H_src: int
+    D_src: int
+    H_tgt: int
+    D_tgt: int
+    E: int
+    hidden: int
+    dtype: int = MOT_BF16
+    top_k: int = 0            # 0 = E
+    src_layout: int = LAYOUT_BTHD
+    dst_layout: int = LAYOUT_BTHD
+    act: int = ACT_GELU
+    algo: int = ALGO_AUTO
+
+    def c(self, workspace=None, workspace_bytes=0) -> _Shapes:
+        return _Shapes(self.L_src, self.L_tgt, self.B, self.T, self.H_src, self.D_src, self.H_tgt,
+                       self.D_tgt, self.E, self.top_k or self.E, self.hidden, self.dtype,
+                       self.src_layout, self.dst_layout, self.act, self.algo, workspace,
+                       workspace_bytes)
+
+    @classmethod
+    def from_workload(cls, w, **kw) -> "Shapes":
+        return cls(w.L_src, w.L_tgt, w.B, w.T, w.H_src, w.D_src, w.H_tgt, w.D_tgt, w.E, w.hidden,
+                   dtype=MOT_F32 if w.dtype == "f32" else MOT_BF16, src_layout=w.src_layout,
+                   dst_layout=w.dst_layout, **kw)
+
+
+_lib = None
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def load_library():
+    """Load libmot.so; raises if it has not been built (no fallback exists)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise MotError(-1, "libmot.so not found at %s; build it with "
+                               "`python -m paper_2607_28979_amd.build`" % _LIB_PATH)
+        lib = ctypes.CDLL(_LIB_PATH)
+        lib.mot_translate.restype = ctypes.c_int
+        lib.mot_translate.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.POINTER(_TW), ctypes.POINTER(_RW), ctypes.c_void_p,
+                                      ctypes.c_void_p, ctypes.POINTER(_Shapes), ctypes.c_void_p]
+        lib.mot_workspace_bytes.restype = ctypes.c_size_t
+        lib.mot_workspace_bytes.argtypes = [ctypes.POINTER(_Shapes)]
+        lib.mot_depth_ratio_map.restype = ctypes.c_int
+        lib.mot_depth_ratio_map.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p]
+        lib.mot_status_string.restype = ctypes.c_char_p
+        lib.mot_status_string.argtypes = [ctypes.c_int]
+        lib.mot_last_error.restype = ctypes.c_char_p
+        lib.mot_abi_version.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def abi_version() -> int:
+    return load_library().mot_abi_version()
+
+
+def status_string(status: int) -> str:
+    return load_library().mot_status_string(status).decode()
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise MotError(rc, load_library().mot_last_error().decode())
+
+
+def depth_ratio_map(L_src: int, L_tgt: int):
+    import numpy as np
+    out = np.zeros(L_tgt, dtype=np.int32)
+    _check(load_library().mot_depth_ratio_map(L_src, L_tgt, out.ctypes.data))
+    return out
+
+
+def workspace_bytes(shapes: Shapes) -> int:
+    c = shapes.c()
+    n = load_library().mot_workspace_bytes(ctypes.byref(c))
+    if n == ctypes.c_size_t(-1).value:
+        raise MotError(2, load_library().mot_last_error().decode())
+    return int(n)
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def translate_raw(src_k, src_v, layer_map, w1, b1, w2, b2, wr, br, dst_k, dst_v,
+                  shapes: Shapes, stream=None, workspace=None, workspace_bytes_=0) -> None:
+    """Call mot_translate with raw device addresses (ints) or tensors.  No
+    checks beyond the library's own (used by the ABI validation tests)."""
+    import numpy as np
+    lib = load_library()
+    lm = np.ascontiguousarray(layer_map, dtype=np.int32)
+    tw = _TW(_ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2))
+    rw = _RW(_ptr(wr), _ptr(br))
+    c = shapes.c(_ptr(workspace), workspace_bytes_)
+    _check(lib.mot_translate(_ptr(src_k), _ptr(src_v), lm.ctypes.data if lm.size else None,
+                             ctypes.byref(tw), ctypes.byref(rw), _ptr(dst_k), _ptr(dst_v),
+                             ctypes.byref(c), stream))
+
+
+def translate(src_k, src_v, layer_map: Sequence[int], w1, b1, w2, b2, wr, br, dst_k, dst_v,
+              shapes: Shapes, workspace=None) -> None:
+    """Translate on the current torch stream.  Tensors must live on the
+    current HIP device, be contiguous and have the dtype named by
+    ``shapes.dtype`` (torch.float32 or torch.bfloat16)."""
+    import torch
+    want = torch.float32 if shapes.dtype == MOT_F32 else torch.bfloat16
+    dev = torch.device("cuda", torch.cuda.current_device())
+    for name, t in (("src_k", src_k), ("src_v", src_v), ("w1", w1), ("b1", b1), ("w2", w2),
+                    ("b2", b2), ("wr", wr), ("br", br), ("dst_k", dst_k), ("dst_v", dst_v)):
+        if t is None:
+            continue
+        if t.device != dev:
+            raise MotError(1, "%s is on %s, expected %s" % (name, t.device, dev))
+        if t.dtype != want:
+            raise MotError(2, "%s has dtype %s, expected %s" % (name, t.dtype, want))
+        if not t.is_contiguous():
+            raise MotError(2, "%s is not contiguous" % name)
+    ws_bytes = 0
+    if workspace is not None:
+        ws_bytes = workspace.numel() * workspace.element_size()
+    stream = torch.cuda.current_stream().cuda_stream
+    translate_raw(src_k, src_v, layer_map, w1, b1, w2, b2, wr, br, dst_k, dst_v, shapes,
+                  stream=stream, workspace=workspace, workspace_bytes_=ws_bytes)

@@ -1,0 +1,322 @@
+// C-ABI entry points of libmot: argument validation, planning, workspace and
+// kernel dispatch.  Every check runs before the first enqueue; on error
+// nothing is launched and the outputs are untouched.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <mutex>
+
+#include "../../include/mot.h"
+#include "mot_internal.h"
+
+using namespace mot;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+mot_status fail(mot_status s, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+constexpr size_t kAlign = 256;
+constexpr size_t kDefaultHiddenCap = size_t(1) << 30;   // hidden buffer per group, bytes
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Plan {
+    bool bf16 = false;
+    bool fused = false;
+    int n_units = 0;
+    int32_t n_tok = 0, n_tok_pad = 0;
+    size_t gates_bytes = 0;    // all units
+    size_t hid_unit_bytes = 0; // one unit's hidden buffer
+    uint32_t codes[kMaxUnits];
+};
+
+Problem base_problem(const mot_shapes* s);
+
+mot_status check_shapes(const mot_shapes* s) {
+    if (!s) return fail(MOT_ERR_NULL_ARG, "shapes is NULL");
+    if (s->L_src < 1 || s->L_src > MOT_MAX_LAYERS || s->L_tgt < 1 || s->L_tgt > MOT_MAX_LAYERS)
+        return fail(MOT_ERR_BAD_SHAPE, "L_src=%d L_tgt=%d must be in [1, %d]", s->L_src, s->L_tgt,
+                    MOT_MAX_LAYERS);
+    if (s->B < 0 || s->T < 0)
+        return fail(MOT_ERR_BAD_SHAPE, "B=%d T=%d must be >= 0", s->B, s->T);
+    if ((int64_t)s->B * s->T > (int64_t)1 << 26)
+        return fail(MOT_ERR_BAD_SHAPE, "B*T=%lld exceeds 2^26 tokens", (long long)s->B * s->T);
+    if (s->H_src < 1 || s->D_src < 1 || s->H_tgt < 1 || s->D_tgt < 1 || s->hidden < 1)
+        return fail(MOT_ERR_BAD_SHAPE, "head counts, head dims and hidden must be >= 1");
+    if ((int64_t)s->H_src * s->D_src > 65536 || (int64_t)s->H_tgt * s->D_tgt > 65536 ||
+        s->hidden > 65536)
+        return fail(MOT_ERR_BAD_SHAPE, "row or hidden width above 65536");
+    if (s->E < 1 || s->E > MOT_MAX_EXPERTS)
+        return fail(MOT_ERR_BAD_SHAPE, "E=%d must be in [1, %d]", s->E, MOT_MAX_EXPERTS);
+    if (s->top_k < 1 || s->top_k > s->E)
+        return fail(MOT_ERR_BAD_SHAPE, "top_k=%d must be in [1, E=%d]", s->top_k, s->E);
+    if (s->top_k != s->E)
+        return fail(MOT_ERR_UNSUPPORTED, "top_k=%d < E=%d: only the dense mixture (top_k == E) is implemented",
+                    s->top_k, s->E);
+    if (s->dtype != MOT_F32 && s->dtype != MOT_BF16)
+        return fail(MOT_ERR_BAD_SHAPE, "dtype=%d is not MOT_F32 or MOT_BF16", s->dtype);
+    if ((s->src_layout != MOT_LAYOUT_BTHD && s->src_layout != MOT_LAYOUT_BHTD) ||
+        (s->dst_layout != MOT_LAYOUT_BTHD && s->dst_layout != MOT_LAYOUT_BHTD))
+        return fail(MOT_ERR_BAD_SHAPE, "layouts must be MOT_LAYOUT_BTHD or MOT_LAYOUT_BHTD");
+    if (s->act != MOT_ACT_GELU && s->act != MOT_ACT_IDENTITY)
+        return fail(MOT_ERR_BAD_SHAPE, "act=%d is not MOT_ACT_GELU or MOT_ACT_IDENTITY", s->act);
+    if (s->algo != MOT_ALGO_AUTO && s->algo != MOT_ALGO_UNFUSED && s->algo != MOT_ALGO_FUSED)
+        return fail(MOT_ERR_BAD_SHAPE, "algo=%d is not a mot_algo value", s->algo);
+    const int d_in = s->H_src * s->D_src, d_out = s->H_tgt * s->D_tgt;
+    if (s->algo == MOT_ALGO_FUSED) {
+        Problem p = base_problem(s);
+        if (s->dtype != MOT_BF16 || !fused_supported(p))
+            return fail(MOT_ERR_UNSUPPORTED,
+                        "the fused kernel needs bf16, d_in and d_out in {128, 256, 512}, hidden %% 32 == 0");
+    }
+    if (s->dtype == MOT_BF16) {
+        if (s->D_src % 8 || s->D_tgt % 8 || d_in % 64 || s->hidden % 64 || d_out % 32)
+            return fail(MOT_ERR_UNSUPPORTED,
+                        "bf16 needs D_src, D_tgt %% 8 == 0, d_in %% 64 == 0, hidden %% 64 == 0, d_out %% 32 == 0 "
+                        "(got D_src=%d D_tgt=%d d_in=%d hidden=%d d_out=%d)",
+                        s->D_src, s->D_tgt, d_in, s->hidden, d_out);
+    } else {
+        if (s->D_src % 4 || s->D_tgt % 4 || s->hidden % 4)
+            return fail(MOT_ERR_UNSUPPORTED,
+                        "fp32 needs D_src, D_tgt, hidden %% 4 == 0 (got D_src=%d D_tgt=%d hidden=%d)",
+                        s->D_src, s->D_tgt, s->hidden);
+    }
+    return MOT_OK;
+}
+
+Problem base_problem(const mot_shapes* s) {
+    Problem p;
+    memset(&p, 0, sizeof p);
+    p.B = s->B; p.T = s->T; p.H_src = s->H_src; p.D_src = s->D_src;
+    p.H_tgt = s->H_tgt; p.D_tgt = s->D_tgt; p.E = s->E; p.hidden = s->hidden;
+    p.d_in = s->H_src * s->D_src; p.d_out = s->H_tgt * s->D_tgt;
+    p.n_tok = s->B * s->T;
+    p.n_tok_pad = (int32_t)round_up((size_t)p.n_tok, 128);
+    p.src_layout = s->src_layout; p.dst_layout = s->dst_layout; p.act = s->act;
+    return p;
+}
+
+// Plan for the given layer map (or the worst case, all 2*L_tgt units).
+void make_plan(const mot_shapes* s, const int32_t* layer_map, Plan* pl) {
+    Problem p = base_problem(s);
+    pl->bf16 = s->dtype == MOT_BF16;
+    pl->fused = pl->bf16 && s->algo != MOT_ALGO_UNFUSED && fused_supported(p);
+    pl->n_tok = p.n_tok;
+    pl->n_tok_pad = p.n_tok_pad;
+    int n = 0;
+    for (int j = 0; j < s->L_tgt; ++j) {
+        const int i = layer_map ? layer_map[j] : 0;
+        if (i < 0) continue;
+        for (int x = 0; x < 2; ++x) {
+            pl->codes[n] = unit_code(j, x, i, n);
+            ++n;
+        }
+    }
+    pl->n_units = n;
+    if (pl->fused) {
+        pl->gates_bytes = 0;
+        pl->hid_unit_bytes = 0;
+    } else {
+        pl->gates_bytes = round_up((size_t)n * p.n_tok_pad * p.E * sizeof(float), kAlign);
+        pl->hid_unit_bytes =
+            round_up((size_t)p.n_tok_pad * p.E * p.hidden * (pl->bf16 ? 2 : 4), kAlign);
+    }
+}
+
+int default_group(const Plan& pl) {
+    if (pl.hid_unit_bytes == 0) return pl.n_units;
+    size_t g = kDefaultHiddenCap / pl.hid_unit_bytes;
+    if (g < 1) g = 1;
+    if (g > (size_t)pl.n_units) g = pl.n_units;
+    return (int)g;
+}
+
+size_t plan_bytes(const Plan& pl, int group) {
+    if (pl.fused || pl.n_units == 0) return 0;
+    return pl.gates_bytes + (size_t)group * pl.hid_unit_bytes;
+}
+
+// Library-owned workspace, one per device, grown on demand.
+struct OwnedBuf {
+    void* ptr = nullptr;
+    size_t bytes = 0;
+};
+std::mutex g_buf_mu;
+OwnedBuf g_bufs[64];
+
+mot_status owned_workspace(size_t need, void** out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return fail(MOT_ERR_HIP, "hipGetDevice failed");
+    std::lock_guard<std::mutex> lk(g_buf_mu);
+    OwnedBuf& b = g_bufs[dev];
+    if (b.bytes < need) {
+        if (b.ptr) {
+            hipError_t e = hipFree(b.ptr);
+            b.ptr = nullptr;
+            b.bytes = 0;
+            if (e != hipSuccess) return fail(MOT_ERR_HIP, "hipFree: %s", hipGetErrorString(e));
+        }
+        hipError_t e = hipMalloc(&b.ptr, need);
+        if (e != hipSuccess) {
+            b.ptr = nullptr;
+            return fail(MOT_ERR_HIP, "hipMalloc(%zu): %s", need, hipGetErrorString(e));
+        }
+        b.bytes = need;
+    }
+    *out = b.ptr;
+    return MOT_OK;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+    const uintptr_t pa = reinterpret_cast<uintptr_t>(a), pb = reinterpret_cast<uintptr_t>(b);
+    return na && nb && pa < pb + nb && pb < pa + na;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mot_abi_version(void) { return MOT_ABI_VERSION; }
+
+const char* mot_last_error(void) { return g_err; }
+
+const char* mot_status_string(mot_status s) {
+    switch (s) {
+        case MOT_OK: return "MOT_OK";
+        case MOT_ERR_NULL_ARG: return "MOT_ERR_NULL_ARG";
+        case MOT_ERR_BAD_SHAPE: return "MOT_ERR_BAD_SHAPE";
+        case MOT_ERR_BAD_LAYER_MAP: return "MOT_ERR_BAD_LAYER_MAP";
+        case MOT_ERR_UNSUPPORTED: return "MOT_ERR_UNSUPPORTED";
+        case MOT_ERR_MISALIGNED: return "MOT_ERR_MISALIGNED";
+        case MOT_ERR_WORKSPACE_TOO_SMALL: return "MOT_ERR_WORKSPACE_TOO_SMALL";
+        case MOT_ERR_HIP: return "MOT_ERR_HIP";
+    }
+    return "MOT_ERR_UNKNOWN";
+}
+
+mot_status mot_depth_ratio_map(int32_t L_src, int32_t L_tgt, int32_t* out) {
+    g_err[0] = 0;
+    if (!out) return fail(MOT_ERR_NULL_ARG, "out is NULL");
+    if (L_src < 1 || L_src > MOT_MAX_LAYERS || L_tgt < 1 || L_tgt > MOT_MAX_LAYERS)
+        return fail(MOT_ERR_BAD_SHAPE, "L_src=%d L_tgt=%d must be in [1, %d]", L_src, L_tgt, MOT_MAX_LAYERS);
+    for (int32_t j = 0; j < L_tgt; ++j) out[j] = (int32_t)(((int64_t)j * L_src) / L_tgt);
+    return MOT_OK;
+}
+
+size_t mot_workspace_bytes(const mot_shapes* shapes) {
+    g_err[0] = 0;
+    if (check_shapes(shapes) != MOT_OK) return SIZE_MAX;
+    static thread_local Plan pl;
+    make_plan(shapes, nullptr, &pl);
+    return plan_bytes(pl, default_group(pl));
+}
+
+mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* layer_map,
+                         const mot_translator_weights* tw, const mot_router_weights* rw,
+                         void* dst_k, void* dst_v, const mot_shapes* s, hipStream_t stream) {
+    g_err[0] = 0;
+    mot_status st = check_shapes(s);
+    if (st != MOT_OK) return st;
+    if ((int64_t)s->B * s->T == 0) return MOT_OK;   // empty context: nothing is read or written
+    if (!src_k || !src_v || !layer_map || !tw || !rw || !dst_k || !dst_v)
+        return fail(MOT_ERR_NULL_ARG, "a required argument is NULL");
+    if (!tw->w1 || !tw->w2 || !rw->w)
+        return fail(MOT_ERR_NULL_ARG, "w1, w2 and the router weight are required (biases may be NULL)");
+    for (int j = 0; j < s->L_tgt; ++j)
+        if (layer_map[j] < -1 || layer_map[j] >= s->L_src)
+            return fail(MOT_ERR_BAD_LAYER_MAP, "layer_map[%d]=%d outside [-1, %d)", j, layer_map[j], s->L_src);
+    const void* dev_ptrs[] = {src_k, src_v, dst_k, dst_v, tw->w1, tw->w2, rw->w};
+    for (const void* q : dev_ptrs)
+        if (!aligned16(q)) return fail(MOT_ERR_MISALIGNED, "device pointer %p is not 16-byte aligned", q);
+    const size_t es = s->dtype == MOT_BF16 ? 2 : 4;
+    const void* bias_ptrs[] = {tw->b1, tw->b2, rw->b};
+    for (const void* q : bias_ptrs)
+        if (q && (reinterpret_cast<uintptr_t>(q) % es))
+            return fail(MOT_ERR_MISALIGNED, "bias pointer %p is not %zu-byte aligned", q, es);
+
+    static thread_local Plan pl;
+    make_plan(s, layer_map, &pl);
+    const size_t n_tok = (size_t)pl.n_tok;
+    const int d_in = s->H_src * s->D_src, d_out = s->H_tgt * s->D_tgt;
+    const size_t src_bytes = (size_t)s->L_src * n_tok * d_in * es;
+    const size_t dst_bytes = (size_t)s->L_tgt * n_tok * d_out * es;
+    if (overlaps(dst_k, dst_bytes, dst_v, dst_bytes) || overlaps(dst_k, dst_bytes, src_k, src_bytes) ||
+        overlaps(dst_k, dst_bytes, src_v, src_bytes) || overlaps(dst_v, dst_bytes, src_k, src_bytes) ||
+        overlaps(dst_v, dst_bytes, src_v, src_bytes))
+        return fail(MOT_ERR_BAD_SHAPE, "destination caches overlap each other or the source caches");
+
+    // workspace
+    int group = default_group(pl);
+    void* ws = nullptr;
+    const size_t need_min = plan_bytes(pl, pl.n_units ? 1 : 0);
+    if (need_min > 0) {
+        if (s->workspace) {
+            if (!aligned16(s->workspace))
+                return fail(MOT_ERR_MISALIGNED, "workspace %p is not 16-byte aligned", s->workspace);
+            if (s->workspace_bytes < need_min)
+                return fail(MOT_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes, need at least %zu",
+                            s->workspace_bytes, need_min);
+            size_t g = (s->workspace_bytes - pl.gates_bytes) / pl.hid_unit_bytes;
+            group = (int)(g < (size_t)pl.n_units ? g : (size_t)pl.n_units);
+            ws = s->workspace;
+            if (overlaps(ws, s->workspace_bytes, dst_k, dst_bytes) ||
+                overlaps(ws, s->workspace_bytes, dst_v, dst_bytes))
+                return fail(MOT_ERR_BAD_SHAPE, "workspace overlaps a destination cache");
+        }
+    }
+    if (pl.n_units == 0 || n_tok == 0) return MOT_OK;   // nothing to translate
+    if (need_min > 0 && !s->workspace) {
+        st = owned_workspace(plan_bytes(pl, group), &ws);
+        if (st != MOT_OK) return st;
+    }
+
+    Problem p = base_problem(s);
+    p.src[0] = src_k; p.src[1] = src_v;
+    p.dst[0] = dst_k; p.dst[1] = dst_v;
+    p.w1 = tw->w1; p.b1 = tw->b1; p.w2 = tw->w2; p.b2 = tw->b2;
+    p.wr = rw->w; p.br = rw->b;
+    if (ws) {
+        p.gates = reinterpret_cast<float*>(ws);
+        p.hbuf = reinterpret_cast<char*>(ws) + pl.gates_bytes;
+    }
+
+    static thread_local UnitTab ut;
+    hipError_t e = hipSuccess;
+    if (pl.fused) {
+        ut.n = pl.n_units;
+        memcpy(ut.code, pl.codes, sizeof(uint32_t) * pl.n_units);
+        e = launch_bf16_fused(p, ut, stream);
+    } else {
+        ut.n = pl.n_units;
+        memcpy(ut.code, pl.codes, sizeof(uint32_t) * pl.n_units);
+        e = launch_router(p, ut, pl.bf16, stream);
+        for (int u0 = 0; e == hipSuccess && u0 < pl.n_units; u0 += group) {
+            const int n = pl.n_units - u0 < group ? pl.n_units - u0 : group;
+            ut.n = n;
+            memcpy(ut.code, pl.codes + u0, sizeof(uint32_t) * n);
+            if (pl.bf16) {
+                e = launch_bf16_gemm1(p, ut, stream);
+                if (e == hipSuccess) e = launch_bf16_gemm2(p, ut, stream);
+            } else {
+                e = launch_f32_gemm1(p, ut, stream);
+                if (e == hipSuccess) e = launch_f32_gemm2(p, ut, stream);
+            }
+        }
+    }
+    if (e != hipSuccess) return fail(MOT_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
+    return MOT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,57 @@
+// Internal launch descriptors shared by the host dispatcher and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace mot {
+
+// Up to 2 * MOT_MAX_LAYERS units can be launched together.
+constexpr int kMaxUnits = 512;
+
+// One unit = (target layer j, X in {K=0, V=1}) reading source layer i.
+// gslot indexes the gate buffer (all units of a call), the launch position
+// indexes the hidden buffer (units of one group).
+__host__ __device__ inline uint32_t unit_code(int j, int x, int i, int gslot) {
+    return (uint32_t)j | ((uint32_t)x << 8) | ((uint32_t)i << 9) | ((uint32_t)gslot << 17);
+}
+__host__ __device__ inline int unit_j(uint32_t c) { return (int)(c & 0xFF); }
+__host__ __device__ inline int unit_x(uint32_t c) { return (int)((c >> 8) & 1); }
+__host__ __device__ inline int unit_i(uint32_t c) { return (int)((c >> 9) & 0xFF); }
+__host__ __device__ inline int unit_gslot(uint32_t c) { return (int)((c >> 17) & 0x3FF); }
+
+struct UnitTab {
+    int32_t n;
+    uint32_t code[kMaxUnits];
+};
+
+// Problem description handed to every kernel by value.
+struct Problem {
+    const void* src[2];   // source K, V: [L_src] x layout
+    void* dst[2];         // target K, V: [L_tgt] x layout
+    const void* w1;       // [L_tgt][2][E][hidden][d_in]
+    const void* b1;       // [L_tgt][2][E][hidden] or null
+    const void* w2;       // [L_tgt][2][E][d_out][hidden]
+    const void* b2;       // [L_tgt][2][E][d_out] or null
+    const void* wr;       // [L_tgt][2][E][d_in]
+    const void* br;       // [L_tgt][2][E] or null
+    int32_t B, T, H_src, D_src, H_tgt, D_tgt, E, hidden;
+    int32_t d_in, d_out, n_tok, n_tok_pad;   // n_tok_pad: n_tok rounded up to 128
+    int32_t src_layout, dst_layout, act;
+    float* gates;         // workspace: [n_units_total][n_tok_pad][E] fp32
+    void* hbuf;           // workspace: [group][n_tok_pad][E*hidden] (layout per path)
+};
+
+// Kernel launchers (each enqueues on `stream`; return hipGetLastError()).
+hipError_t launch_router(const Problem& p, const UnitTab& ut, bool bf16, hipStream_t stream);
+hipError_t launch_f32_gemm1(const Problem& p, const UnitTab& ut, hipStream_t stream);
+hipError_t launch_f32_gemm2(const Problem& p, const UnitTab& ut, hipStream_t stream);
+hipError_t launch_bf16_gemm1(const Problem& p, const UnitTab& ut, hipStream_t stream);
+hipError_t launch_bf16_gemm2(const Problem& p, const UnitTab& ut, hipStream_t stream);
+// Fused single-kernel path (router + both layers + mix + store); returns
+// hipErrorNotSupported when the sizes have no fused instantiation.
+bool fused_supported(const Problem& p);
+hipError_t launch_bf16_fused(const Problem& p, const UnitTab& ut, hipStream_t stream);
+
+}  // namespace mot

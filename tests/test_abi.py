@@ -1,0 +1,141 @@
+"""CPU tests of the C-ABI boundary: the library loads, exports every symbol
+the header declares, and rejects bad arguments before touching the GPU
+(nothing here launches a kernel)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2607_28979_amd import binding as mb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mot.h")
+
+FAKE = 0x7F0000000000       # 16-byte aligned address that is never dereferenced
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(mb.lib_path()):
+        pytest.skip("libmot.so not built (run __graft_entry__.build())")
+    return mb.load_library()
+
+
+def _decls():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(mot_[a-z_]+)\s*\(", txt)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _decls()
+    assert set(mb.EXPORTED) == set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_abi_version(lib):
+    assert mb.abi_version() == 1
+
+
+def test_status_strings(lib):
+    for code, name in mb.STATUS.items():
+        assert mb.status_string(code) == name
+
+
+@pytest.mark.parametrize("L_src,L_tgt", [(24, 28), (28, 28), (12, 12), (28, 24), (1, 7), (256, 3)])
+def test_depth_ratio_map_bit_exact_vs_oracle(lib, oracle_built, L_src, L_tgt):
+    from oracle import oracle_depth_ratio_map
+    assert np.array_equal(mb.depth_ratio_map(L_src, L_tgt), oracle_depth_ratio_map(L_src, L_tgt))
+
+
+def test_depth_ratio_map_rejects(lib):
+    with pytest.raises(mb.MotError) as e:
+        mb.depth_ratio_map(0, 4)
+    assert e.value.name == "MOT_ERR_BAD_SHAPE"
+
+
+def _shapes(**kw):
+    base = dict(L_src=2, L_tgt=2, B=1, T=8, H_src=2, D_src=64, H_tgt=2, D_tgt=64, E=4, hidden=128,
+                dtype=mb.MOT_BF16)
+    base.update(kw)
+    return mb.Shapes(**base)
+
+
+def _call(shapes, layer_map=(0, 1), ptrs=None, ws=None, ws_bytes=0):
+    p = dict(src_k=FAKE, src_v=FAKE + (1 << 30), w1=FAKE + (2 << 30), b1=None, w2=FAKE + (3 << 30),
+             b2=None, wr=FAKE + (4 << 30), br=None, dst_k=FAKE + (5 << 30), dst_v=FAKE + (6 << 30))
+    p.update(ptrs or {})
+    mb.translate_raw(p["src_k"], p["src_v"], layer_map, p["w1"], p["b1"], p["w2"], p["b2"], p["wr"],
+                     p["br"], p["dst_k"], p["dst_v"], shapes, workspace=ws, workspace_bytes_=ws_bytes)
+
+
+def _expect(code, **kw):
+    with pytest.raises(mb.MotError) as e:
+        _call(**kw)
+    assert e.value.name == code, str(e.value)
+
+
+def test_null_pointers(lib):
+    _expect("MOT_ERR_NULL_ARG", shapes=_shapes(), ptrs={"src_k": None})
+    _expect("MOT_ERR_NULL_ARG", shapes=_shapes(), ptrs={"dst_v": None})
+    _expect("MOT_ERR_NULL_ARG", shapes=_shapes(), ptrs={"w1": None})
+    _expect("MOT_ERR_NULL_ARG", shapes=_shapes(), ptrs={"wr": None})
+
+
+@pytest.mark.parametrize("kw", [dict(L_src=0), dict(L_tgt=257), dict(B=-1), dict(E=0), dict(E=17),
+                                dict(hidden=0), dict(dtype=7), dict(src_layout=2), dict(act=5),
+                                dict(algo=9), dict(top_k=5)])
+def test_bad_shapes(lib, kw):
+    _expect("MOT_ERR_BAD_SHAPE", shapes=_shapes(**kw), layer_map=[0] * 300)
+
+
+@pytest.mark.parametrize("kw", [dict(top_k=1), dict(D_src=60), dict(hidden=96),
+                                dict(H_tgt=1, D_tgt=24), dict(dtype=mb.MOT_F32, D_src=6, H_src=2),
+                                dict(algo=mb.ALGO_FUSED, dtype=mb.MOT_F32),
+                                dict(algo=mb.ALGO_FUSED, H_src=12, D_src=64)])
+def test_unsupported(lib, kw):
+    _expect("MOT_ERR_UNSUPPORTED", shapes=_shapes(**kw))
+
+
+@pytest.mark.parametrize("lm", [(0, 2), (-2, 0), (5, 5)])
+def test_bad_layer_map(lib, lm):
+    _expect("MOT_ERR_BAD_LAYER_MAP", shapes=_shapes(), layer_map=lm)
+
+
+def test_misaligned(lib):
+    _expect("MOT_ERR_MISALIGNED", shapes=_shapes(), ptrs={"src_k": FAKE + 8})
+    _expect("MOT_ERR_MISALIGNED", shapes=_shapes(), ptrs={"w2": FAKE + 4})
+    _expect("MOT_ERR_MISALIGNED", shapes=_shapes(), ptrs={"b1": FAKE + 1})
+
+
+def test_overlapping_destinations(lib):
+    _expect("MOT_ERR_BAD_SHAPE", shapes=_shapes(), ptrs={"dst_v": FAKE + (5 << 30) + 64})
+    _expect("MOT_ERR_BAD_SHAPE", shapes=_shapes(), ptrs={"dst_k": FAKE})
+
+
+def test_workspace_too_small(lib):
+    s = _shapes(algo=mb.ALGO_UNFUSED)
+    need = mb.workspace_bytes(s)
+    assert need > 0
+    _expect("MOT_ERR_WORKSPACE_TOO_SMALL", shapes=s, ws=FAKE + (7 << 30), ws_bytes=1024)
+
+
+def test_workspace_bytes(lib):
+    assert mb.workspace_bytes(_shapes()) == 0                    # fused: none
+    s = _shapes(algo=mb.ALGO_UNFUSED)
+    n_pad = 128
+    gates = (4 * n_pad * 4 * 4 + 255) // 256 * 256                # 4 units, E=4, fp32
+    hid = n_pad * 4 * 128 * 2
+    assert mb.workspace_bytes(s) == gates + 4 * hid
+    with pytest.raises(mb.MotError):
+        mb.workspace_bytes(_shapes(E=0))
+
+
+def test_header_struct_layout_matches_binding():
+    # mot_shapes: 16 int32 fields, then a pointer and a size_t
+    assert ctypes.sizeof(mb._Shapes) == 16 * 4 + 8 + 8
+    txt = open(HEADER).read()
+    assert "int32_t dtype, src_layout, dst_layout, act, algo;" in txt
