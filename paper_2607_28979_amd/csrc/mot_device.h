@@ -57,4 +57,20 @@ __device__ __forceinline__ float gelu_fast(float x) {
     return 0.5f * x * (1.0f + erf_v);
 }
 
+// g * GELU(x) with hg = g / 2, for the fused bf16 kernel: erf from
+// Abramowitz & Stegun formula 7.1.25 (|error of erf| <= 2.5e-5, two orders
+// below the bf16 rounding the result gets next):
+//   erf(y) = 1 - (a1 t + a2 t^2 + a3 t^3) exp(-y^2),  t = 1 / (1 + p y),  y >= 0;
+// then hg*x*(1 + erf(x / sqrt 2)) = hx + hx*erf with hx = hg*x.
+__device__ __forceinline__ float gelu_half_scaled(float x, float hg) {
+    const float y = fabsf(x) * 0.70710678118654752f;
+    const float t = __builtin_amdgcn_rcpf(fmaf(0.47047f, y, 1.0f));
+    const float poly = fmaf(fmaf(0.7478556f, t, -0.0958798f), t, 0.3480242f) * t;
+    // exp(-y^2) = 2^(-x^2 * log2(e) / 2)
+    const float e = __builtin_amdgcn_exp2f((x * x) * -0.72134752044448170f);
+    const float erf_v = copysignf(fmaf(-poly, e, 1.0f), x);
+    const float hx = hg * x;
+    return fmaf(hx, erf_v, hx);
+}
+
 }  // namespace mot
