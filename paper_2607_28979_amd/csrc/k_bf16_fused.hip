@@ -391,7 +391,8 @@ void k_bf16_fused(Problem p, UnitTab ut) {
             s[8 + 2 * q + 1] = bf16_hi(bv[1][q]);
         }
         u32x4 a1[NL1], hA[2][TB], bW[2][C::NBW];
-        float h[16];
+        float h[16], gx[16], gt[16], gx2[16], gq[16], ge[16];
+        constexpr int GD = 2;   // slots between GELU stages
         // operand reads needed by slot k
         auto issue_reads = [&](auto kc) {
             constexpr int k = decltype(kc)::value;
@@ -425,12 +426,28 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                               nb = q % C::NBW;
                 acc[tb][nb] = mfma_32x32x16(hA[ks][tb], bW[ks][nb], acc[tb][nb]);
             }
+            // GELU of element e runs as three stages in slots g0(e), g0(e)+GD,
+            // g0(e)+2*GD, so several independent chains overlap in each slot
             static_for<0, 16>([&](auto ec) {
                 constexpr int e = decltype(ec)::value;
-                if constexpr ((e * NM) / 16 == k) {
+                constexpr int g0 = (e * (NM - 2 * GD - 1)) / 15;
+                if constexpr (ACT == MOT_ACT_GELU) {
+                    if constexpr (k == g0) {
+                        float v = sp[e];
+                        asm volatile("" : "+v"(v));
+                        gx[e] = v;
+                        gelu_stage1(v, gt[e], gx2[e]);
+                        asm volatile("" : "+v"(gt[e]), "+v"(gx2[e]));
+                    } else if constexpr (k == g0 + GD) {
+                        gelu_stage2(gt[e], gx2[e], gq[e], ge[e]);
+                        asm volatile("" : "+v"(gq[e]), "+v"(ge[e]));
+                    } else if constexpr (k == g0 + 2 * GD) {
+                        h[e] = gelu_stage3(gx[e], gt[e], gq[e], ge[e], hg);
+                    }
+                } else if constexpr (k == g0) {
                     float v = sp[e];
-                    asm volatile("" : "+v"(v));   // anchor this evaluation to its slot
-                    h[e] = ACT == MOT_ACT_GELU ? gelu_half_scaled(v, hg) : 2.0f * hg * v;
+                    asm volatile("" : "+v"(v));
+                    h[e] = 2.0f * hg * v;
                 }
             });
             __builtin_amdgcn_sched_barrier(0);

@@ -73,4 +73,21 @@ __device__ __forceinline__ float gelu_half_scaled(float x, float hg) {
     return fmaf(hx, erf_v, hx);
 }
 
+// The same function as gelu_half_scaled, split into three dependent stages
+// so a software pipeline can overlap the chains of several elements.
+__device__ __forceinline__ void gelu_stage1(float x, float& t, float& x2) {
+    // 1 + p*|x|/sqrt(2), folded into one fused multiply-add
+    t = __builtin_amdgcn_rcpf(fmaf(0.47047f * 0.70710678118654752f, fabsf(x), 1.0f));
+    x2 = x * x;
+}
+__device__ __forceinline__ void gelu_stage2(float t, float x2, float& q, float& e) {
+    q = fmaf(fmaf(0.7478556f, t, -0.0958798f), t, 0.3480242f);
+    e = __builtin_amdgcn_exp2f(x2 * -0.72134752044448170f);
+}
+__device__ __forceinline__ float gelu_stage3(float x, float t, float q, float e, float hg) {
+    const float erf_v = copysignf(fmaf(-(q * t), e, 1.0f), x);
+    const float hx = hg * x;
+    return fmaf(hx, erf_v, hx);
+}
+
 }  // namespace mot
