@@ -49,8 +49,6 @@ struct Cfg {
     static constexpr int W1_CH = 32 * CPR1;       // chunks per W1 stage
     static constexpr int W2_CH = D_OUT * 4;       // chunks per W2 stage (32 hidden = 4 chunks)
     static constexpr int H_CH = 4 * 128;          // chunks per hidden stage (4 blocks x 32 tokens x 32)
-    static constexpr int W1_ROUNDS = W1_CH / 256;
-    static constexpr int W2_ROUNDS = W2_CH / 256;
     static constexpr int GS = 4 * MOT_MAX_EXPERTS * 32;   // gate floats (4 token blocks)
     // LDS map in 16-byte units
     static constexpr int OFF_W1 = 0;
@@ -59,15 +57,18 @@ struct Cfg {
     static constexpr int OFF_G = OFF_H + 2 * H_CH;
     static constexpr int TOTAL = OFF_G + GS / 4;
     static_assert(W1_CH % 256 == 0 && W2_CH % 256 == 0 && NBW >= 1, "tile shape");
+    static_assert(TB * NBW * 16 <= 192, "layer-2 accumulators must leave VGPR room");
 };
 
-// Row r of a staged 32-row W1 block holds hidden row w1_perm(r) of the chunk,
-// so the layer-1 accumulator fragment (rows 8*i + 4*g + j of lane half g)
-// lists hidden values 8g..8g+7 (i < 2) and 16+8g..16+8g+7 (i >= 2): the two
-// 16-wide k-slices of the layer-2 A operand.
+// Row R of a staged 32-row W1 block holds hidden row w1_perm(R) of the chunk.
+// Layer 1 runs as 16x16 MFMA blocks over row halves hh = R / 16; lane group q
+// of a block's accumulator holds rows 4q + j, j = 0..3.  Mapping row
+// hh*16 + 4q + j to hidden 8q + 4hh + j gives each lane, for one token, the
+// eight consecutive hidden values 8q .. 8q+7: one 16-byte unit of the
+// layer-2 A-operand tile.
 __device__ __forceinline__ int w1_perm(int r) {
-    const int i = r >> 3, g = (r >> 2) & 1, jj = r & 3;
-    return ((i >> 1) << 4) | (g << 3) | ((i & 1) << 2) | jj;
+    const int hh = r >> 4, q = (r >> 2) & 3, jj = r & 3;
+    return 8 * q + 4 * hh + jj;
 }
 
 __device__ __forceinline__ void load_lds16(const void* gsrc, u32x4* lds_dst_wave_base) {
@@ -92,10 +93,13 @@ __device__ __forceinline__ void static_for(F&& f) {
 }
 
 template <int D_IN, int D_OUT, int ACT>
-__global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void k_bf16_fused(Problem p, UnitTab ut) {
+__global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
     using C = Cfg<D_IN, D_OUT>;
     constexpr int TB = C::TB;
+    // waves that issue the global -> LDS weight loads: wave 3 alone when it has
+    // no token block (TB = 3), else the four layer-2 waves
+    constexpr int NLD = TB == 3 ? 1 : 4;
+    constexpr int W1_RL = C::W1_CH / (64 * NLD), W2_RL = C::W2_CH / (64 * NLD);
     __shared__ u32x4 smem[C::TOTAL];
     u32x4* W1s = smem + C::OFF_W1;
     u32x4* W2s = smem + C::OFF_W2;
@@ -107,11 +111,15 @@ void k_bf16_fused(Problem p, UnitTab ut) {
     const int E = p.E, hidden = p.hidden, EH = E * hidden;
     const size_t unit = (size_t)j * 2 + x;
     const int tid = threadIdx.x, lane = tid & 63;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // 0..7
     const int g = lane >> 5, l32 = lane & 31;
     const uint32_t gmask = 0u - (uint32_t)g;   // all ones in the upper lane half
     const int tok0 = blockIdx.x * C::BM;
-    const int my_tok = tok0 + 32 * w + l32;
+    const bool is_l1 = w < TB;                 // layer-1 + GELU wave of token block w
+    const bool is_l2 = w >= 4;                 // layer-2 wave q = w - 4
+    const bool is_ld = NLD == 1 ? w == 3 : is_l2;
+    const int q2 = w - 4;                      // layer-2 column group
+    const int lw = NLD == 1 ? 0 : q2;          // index among the loading waves
 
     const uint16_t* W1u = reinterpret_cast<const uint16_t*>(p.w1) + unit * EH * D_IN;
     const uint16_t* W2u = reinterpret_cast<const uint16_t*>(p.w2) + unit * E * D_OUT * hidden;
@@ -121,229 +129,43 @@ void k_bf16_fused(Problem p, UnitTab ut) {
     const uint16_t* b2u = p.b2 ? reinterpret_cast<const uint16_t*>(p.b2) + unit * E * D_OUT : nullptr;
     const uint16_t* Wru = reinterpret_cast<const uint16_t*>(p.wr) + unit * E * D_IN;
 
-    // ---- loop-invariant per-lane offsets of the direct-to-LDS loads
-    uint32_t off_w1[C::W1_ROUNDS], off_w2[C::W2_ROUNDS];
-#pragma unroll
-    for (int r = 0; r < C::W1_ROUNDS; ++r) {
-        const int slot = r * 256 + w * 64 + lane;
+    // ---- global -> LDS weight loads (loading waves only)
+    // byte offset, within a chunk, of the 16 bytes this lane loads in round r
+    auto w1_off = [&](int r) -> uint32_t {
+        const int slot = r * 64 * NLD + lw * 64 + lane;
         const int row = slot / C::CPR1, pc = slot % C::CPR1, cl = pc ^ (row & 7);
-        off_w1[r] = (uint32_t)(w1_perm(row) * D_IN + cl * 8);
-    }
-#pragma unroll
-    for (int r = 0; r < C::W2_ROUNDS; ++r) {
-        const int slot = r * 256 + w * 64 + lane;
+        return (uint32_t)(w1_perm(row) * D_IN + cl * 8) * 2u;
+    };
+    auto w2_off = [&](int r) -> uint32_t {
+        const int slot = r * 64 * NLD + lw * 64 + lane;
         const int o = slot >> 2, pc = slot & 3, cl = pc ^ ((o >> 1) & 3);
-        off_w2[r] = (uint32_t)(o * hidden + cl * 8);
-    }
-    auto load_w1 = [&](int c, int st) {
-        const uint16_t* base = W1u + (size_t)c * 32 * D_IN;
-#pragma unroll
-        for (int r = 0; r < C::W1_ROUNDS; ++r)
-            load_lds16(base + off_w1[r], W1s + st * C::W1_CH + r * 256 + w * 64);
+        return (uint32_t)(o * hidden + cl * 8) * 2u;
     };
-    // W2 columns [kk, kk+32) of translator m into stage st
-    auto load_w2 = [&](int m, int kk, int st) {
-        const uint16_t* base = W2u + (size_t)m * D_OUT * hidden + kk;
-#pragma unroll
-        for (int r = 0; r < C::W2_ROUNDS; ++r)
-            load_lds16(base + off_w2[r], W2s + st * C::W2_CH + r * 256 + w * 64);
+    // chunk c of W1 (round r) into stage st; the chunk base is wave-uniform,
+    // so each load is a scalar base plus a per-lane offset
+    auto load_w1_round = [&](int c, int st, int r, uint32_t off) {
+        const char* base = reinterpret_cast<const char*>(W1u + (size_t)c * 32 * D_IN);
+        load_lds16(base + off, W1s + st * C::W1_CH + r * 64 * NLD + lw * 64);
     };
-    // the two 8-value pieces of b1 lane half g needs for chunk c
-    auto load_b1 = [&](int c, u32x4* bv) {
-        typedef const __attribute__((address_space(1))) u32x4* gvec;
-        const uint16_t* bp = b1u + c * 32;
-        bv[0] = *(gvec)(bp + 8 * g) & b1_mask;
-        bv[1] = *(gvec)(bp + 16 + 8 * g) & b1_mask;
+    // W2 columns [kk, kk+32) of translator m (round r) into stage st
+    auto load_w2_round = [&](int m, int kk, int st, int r, uint32_t off) {
+        const char* base = reinterpret_cast<const char*>(W2u + (size_t)m * D_OUT * hidden + kk);
+        load_lds16(base + off, W2s + st * C::W2_CH + r * 64 * NLD + lw * 64);
     };
-
-    // ---- source rows -> VGPRs (B operand of layer 1 and of the router)
-    u32x4 zf[C::KS1];
-    {
-        const bool ok = w < TB && my_tok < p.n_tok;
-        const uint16_t* src = reinterpret_cast<const uint16_t*>(p.src[x]) + (size_t)i * p.n_tok * D_IN;
-        const int b = ok ? my_tok / p.T : 0, t = ok ? my_tok % p.T : 0;
-#pragma unroll
-        for (int s = 0; s < C::KS1; ++s) {
-            const int k = 16 * s + 8 * g;
-            size_t off;
-            if (p.src_layout == MOT_LAYOUT_BTHD) {
-                off = (size_t)my_tok * D_IN + k;
-            } else {
-                const int hh = k / p.D_src, dd = k % p.D_src;
-                off = (((size_t)b * p.H_src + hh) * p.T + t) * p.D_src + dd;
-            }
-            const u32x4 zero = {0u, 0u, 0u, 0u};
-            zf[s] = ok ? *reinterpret_cast<const u32x4*>(src + off) : zero;
-        }
-    }
-
-    // ---- router on MFMA: stage Wr (rows >= E zero) in the second W1 stage
-    {
+    const int nch = EH / 32;   // >= 2
+    // The three roles run the same number of workgroup barriers: two around
+    // the router, then one per pipeline iteration c = 0 .. nch+1.  Iteration c
+    // runs layer 1 of chunk c, the GELU of chunk c-1 and layer 2 of chunk c-2;
+    // the loading wave(s) fetch W1 of chunk c+1 and W2 of chunk c-1.
+    // (m1, kk1) = translator and column offset of chunk c-1.
+    auto stage_router_weights = [&]() {   // waves 0..3
         u32x4* Rs = W1s + C::W1_CH;
 #pragma unroll
-        for (int r = 0; r < C::W1_ROUNDS; ++r) {
+        for (int r = 0; r < C::W1_CH / 256; ++r) {
             const int slot = r * 256 + tid;
             const int row = slot / C::CPR1, pc = slot % C::CPR1, cl = pc ^ (row & 7);
             const u32x4 zero = {0u, 0u, 0u, 0u};
             Rs[slot] = row < E ? *reinterpret_cast<const u32x4*>(Wru + (size_t)row * D_IN + cl * 8) : zero;
-        }
-    }
-    load_w1(0, 0);   // first W1 chunk in flight while the router runs
-    __syncthreads();
-    {
-        const u32x4* Rs = W1s + C::W1_CH;
-        f32x16 lg;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) lg[e] = 0.f;
-#pragma unroll
-        for (int s = 0; s < C::KS1; ++s) {
-            const u32x4 a = Rs[l32 * C::CPR1 + ((2 * s + g) ^ (l32 & 7))];
-            lg = mfma_32x32x16(a, zf[s], lg);
-        }
-        // lane half g holds experts 8*ii + 4*g + jj (ii = 0, 1) of token l32;
-        // fetch the other half's four-expert groups from lane ^ 32
-        float own[8], oth[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            own[e] = lg[e];
-            oth[e] = __shfl_xor(lg[e], 32, 64);
-        }
-        float logit[16];
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-            logit[jj] = pick(gmask, own[jj], oth[jj]);
-            logit[4 + jj] = pick(gmask, oth[jj], own[jj]);
-            logit[8 + jj] = pick(gmask, own[4 + jj], oth[4 + jj]);
-            logit[12 + jj] = pick(gmask, oth[4 + jj], own[4 + jj]);
-        }
-        const uint16_t* bru = p.br ? reinterpret_cast<const uint16_t*>(p.br) + unit * E : nullptr;
-        float mx = -INFINITY;
-#pragma unroll
-        for (int m = 0; m < MOT_MAX_EXPERTS; ++m) {
-            if (m < E) {
-                if (bru) logit[m] += bf16_to_f32(bru[m]);
-                mx = fmaxf(mx, logit[m]);
-            }
-        }
-        float gate_all[MOT_MAX_EXPERTS];
-        float den = 0.f;
-#pragma unroll
-        for (int m = 0; m < MOT_MAX_EXPERTS; ++m) {
-            gate_all[m] = m < E ? __expf(logit[m] - mx) : 0.f;
-            den += gate_all[m];
-        }
-        const float inv = 1.0f / den;
-        if (g == 0) {
-            float* Gw = Gs + w * (MOT_MAX_EXPERTS * 32);
-#pragma unroll
-            for (int m = 0; m < MOT_MAX_EXPERTS; ++m)
-                if (m < E) Gw[m * 32 + l32] = gate_all[m] * inv;
-        }
-    }
-    __syncthreads();   // all gates visible; router stage free again
-
-    // ---- output accumulators, seeded with sum_m g_m b2_m[o] on MFMA:
-    // A = gates of a token block (k = translator), B = b2 (k = translator).
-    // Gates are split into bf16 high + residual parts (two products) so the
-    // seed keeps ~16 mantissa bits of the fp32 gates.
-    // acc[tb][nb]: column o = w*OUTW + nb*32 + l32, rows = tokens
-    // tb*32 + 8*ii + 4*g + jj (element 4*ii + jj).
-    f32x16 acc[TB][C::NBW];
-#pragma unroll
-    for (int tb = 0; tb < TB; ++tb)
-#pragma unroll
-        for (int nb = 0; nb < C::NBW; ++nb)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[tb][nb][e] = 0.f;
-    if (b2u) {
-        u32x4 bv[C::NBW];
-#pragma unroll
-        for (int nb = 0; nb < C::NBW; ++nb) {
-            const int o = w * C::OUTW + nb * 32 + l32;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int m0 = 8 * g + 2 * q;
-                const uint32_t v0 = m0 < E ? b2u[(size_t)m0 * D_OUT + o] : 0u;
-                const uint32_t v1 = m0 + 1 < E ? b2u[(size_t)(m0 + 1) * D_OUT + o] : 0u;
-                bv[nb][q] = v0 | (v1 << 16);
-            }
-        }
-#pragma unroll
-        for (int tb = 0; tb < TB; ++tb) {
-            const float* Gt = Gs + tb * (MOT_MAX_EXPERTS * 32);
-            u32x4 ghi, glo;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int m0 = 8 * g + 2 * q;
-                const float g0 = m0 < E ? Gt[m0 * 32 + l32] : 0.f;
-                const float g1 = m0 + 1 < E ? Gt[(m0 + 1) * 32 + l32] : 0.f;
-                const uint32_t hi = pack_bf16x2(g0, g1);
-                ghi[q] = hi;
-                glo[q] = pack_bf16x2(g0 - bf16_lo(hi), g1 - bf16_hi(hi));
-            }
-#pragma unroll
-            for (int nb = 0; nb < C::NBW; ++nb) {
-                acc[tb][nb] = mfma_32x32x16(ghi, bv[nb], acc[tb][nb]);
-                acc[tb][nb] = mfma_32x32x16(glo, bv[nb], acc[tb][nb]);
-            }
-        }
-    }
-
-    // ---- pipeline stages
-    const float* Gw = Gs + w * (MOT_MAX_EXPERTS * 32);
-    // layer 1 of chunk c from W1 stage c&1, bias bv preloaded into the accumulator
-    auto layer1 = [&](int c, const u32x4* bv) -> f32x16 {
-        const u32x4* W1c = W1s + (c & 1) * C::W1_CH;
-        f32x16 s;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            s[2 * q] = bf16_lo(bv[0][q]);
-            s[2 * q + 1] = bf16_hi(bv[0][q]);
-            s[8 + 2 * q] = bf16_lo(bv[1][q]);
-            s[8 + 2 * q + 1] = bf16_hi(bv[1][q]);
-        }
-#pragma unroll
-        for (int k = 0; k < C::KS1; ++k) {
-            const u32x4 a = W1c[l32 * C::CPR1 + ((2 * k + g) ^ (l32 & 7))];
-            s = mfma_32x32x16(a, zf[k], s);
-        }
-        return s;
-    };
-    // gate-scaled GELU of chunk c (translator m), written to hidden stage c&1
-    // in fragment order [token block][k-slice][lane half][token]
-    auto gelu_store = [&](int c, int m, const f32x16& s) {
-        const float hg = 0.5f * Gw[m * 32 + l32];
-        float h[16];
-#pragma unroll
-        for (int e = 0; e < 16; ++e)
-            h[e] = ACT == MOT_ACT_GELU ? gelu_half_scaled(s[e], hg) : 2.0f * hg * s[e];
-        u32x4* Hc = Hs + (c & 1) * C::H_CH + w * 128;
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            u32x4 v;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) v[q] = pack_bf16x2(h[8 * ks + 2 * q], h[8 * ks + 2 * q + 1]);
-            Hc[ks * 64 + g * 32 + l32] = v;
-        }
-    };
-    // layer 2 of chunk c: all TB token blocks x this wave's output blocks
-    auto layer2 = [&](int c) {
-        const u32x4* Hc = Hs + (c & 1) * C::H_CH;
-        const u32x4* W2c = W2s + (c & 1) * C::W2_CH;
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            u32x4 bw[C::NBW];
-#pragma unroll
-            for (int nb = 0; nb < C::NBW; ++nb) {
-                const int o = w * C::OUTW + nb * 32 + l32;
-                bw[nb] = W2c[o * 4 + ((2 * ks + g) ^ ((o >> 1) & 3))];
-            }
-#pragma unroll
-            for (int tb = 0; tb < TB; ++tb) {
-                const u32x4 a = Hc[tb * 128 + ks * 64 + g * 32 + l32];
-#pragma unroll
-                for (int nb = 0; nb < C::NBW; ++nb) acc[tb][nb] = mfma_32x32x16(a, bw[nb], acc[tb][nb]);
-            }
         }
     };
     auto sync_stage = [&]() {
@@ -351,183 +173,407 @@ void k_bf16_fused(Problem p, UnitTab ut) {
         __syncthreads();
     };
 
-    // One steady-state iteration as a fixed slot schedule: layer-1 MFMAs of
-    // chunk c and layer-2 MFMAs of chunk c-2 are merged proportionally; every
-    // LDS operand read is issued LOOK slots before its MFMA; the 16 GELU
-    // evaluations of chunk c-1 are spread evenly over the slots; each slot is
-    // fenced so the compiler keeps this order.
-    auto steady_slots = [&](int c, int m, const u32x4* bv, const f32x16& sp, int cn, int m_w2,
-                            int kk_w2, u32x4* bnext_out) -> f32x16 {
-        constexpr int NL1 = C::KS1, NL2 = 2 * TB * C::NBW, NM = NL1 + NL2, LOOK = 3;
-        // global -> LDS loads of the next W1 chunk and of W2 for chunk c-1,
-        // plus the next b1 pieces, spread evenly over the slots
-        constexpr int NV = C::W1_ROUNDS + C::W2_ROUNDS + 2;
-        const uint16_t* w1_base = W1u + (size_t)cn * 32 * D_IN;
-        u32x4* w1_dst = W1s + ((c + 1) & 1) * C::W1_CH + w * 64;
-        const uint16_t* w2_base = W2u + (size_t)m_w2 * D_OUT * hidden + kk_w2;
-        u32x4* w2_dst = W2s + ((c - 1) & 1) * C::W2_CH + w * 64;
-        auto issue_vmem = [&](auto rc) {
-            constexpr int r = decltype(rc)::value;
-            if constexpr (r < C::W1_ROUNDS) {
-                load_lds16(w1_base + off_w1[r], w1_dst + r * 256);
-            } else if constexpr (r < C::W1_ROUNDS + C::W2_ROUNDS) {
-                constexpr int q = r - C::W1_ROUNDS;
-                load_lds16(w2_base + off_w2[q], w2_dst + q * 256);
-            } else if constexpr (r == NV - 2) {
-                load_b1(cn, bnext_out);
+    if (is_l1) {
+        // ---------------------------------------------------------- layer 1
+        // Layer 1 and the router use v_mfma_f32_16x16x32_bf16: the 32-token
+        // block is two 16-token halves th, the 32 staged W1 rows two 16-row
+        // halves hh, so the chunk's S block is four independent 16x16
+        // accumulators (no dependent MFMA chain).  Lane l = 16*q + l16 holds
+        // S rows 4q + j of each sub-block for token th*16 + l16.
+        constexpr int KS2 = D_IN / 32;
+        const int l16 = lane & 15, q4 = lane >> 4;
+        u32x4 zf[2][KS2];   // B operand: token th*16 + l16, k = 32s + 8*q4 .. +7
+        {
+            const uint16_t* src = reinterpret_cast<const uint16_t*>(p.src[x]) + (size_t)i * p.n_tok * D_IN;
+#pragma unroll
+            for (int th = 0; th < 2; ++th) {
+                const int my_tok = tok0 + 32 * w + 16 * th + l16;
+                const bool ok = my_tok < p.n_tok;
+                const int b = ok ? my_tok / p.T : 0, t = ok ? my_tok % p.T : 0;
+#pragma unroll
+                for (int s = 0; s < KS2; ++s) {
+                    const int k = 32 * s + 8 * q4;
+                    size_t off;
+                    if (p.src_layout == MOT_LAYOUT_BTHD) {
+                        off = (size_t)my_tok * D_IN + k;
+                    } else {
+                        const int hh = k / p.D_src, dd = k % p.D_src;
+                        off = (((size_t)b * p.H_src + hh) * p.T + t) * p.D_src + dd;
+                    }
+                    const u32x4 zero = {0u, 0u, 0u, 0u};
+                    zf[th][s] = ok ? *reinterpret_cast<const u32x4*>(src + off) : zero;
+                }
+            }
+        }
+        stage_router_weights();
+        __syncthreads();                                     // barrier A
+        {
+            // router on MFMA: logits[expert][token] = Wr z (Wr rows >= E zero)
+            const u32x4* Rs = W1s + C::W1_CH;
+            const uint16_t* bru = p.br ? reinterpret_cast<const uint16_t*>(p.br) + unit * E : nullptr;
+            float* Gw = Gs + w * (MOT_MAX_EXPERTS * 32);
+#pragma unroll
+            for (int th = 0; th < 2; ++th) {
+                f32x4 lg = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int s = 0; s < KS2; ++s) {
+                    const u32x4 a = Rs[l16 * C::CPR1 + ((4 * s + q4) ^ (l16 & 7))];
+                    lg = mfma_16x16x32(a, zf[th][s], lg);
+                }
+                // lane group q4 holds experts 4*q4 .. 4*q4+3 of token l16; the
+                // other three groups' experts come from lanes ^ 16, ^ 32, ^ 48
+                float src4[4][4];
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    src4[0][jj] = lg[jj];
+                    src4[1][jj] = __shfl_xor(lg[jj], 16, 64);
+                    src4[2][jj] = __shfl_xor(lg[jj], 32, 64);
+                    src4[3][jj] = __shfl_xor(lg[jj], 48, 64);
+                }
+                float logit[16];
+#pragma unroll
+                for (int kq = 0; kq < 4; ++kq) {
+                    // experts 4*kq.. live in the source with index q4 ^ kq
+                    const uint32_t m0 = 0u - (uint32_t)((q4 ^ kq) & 1), m1 = 0u - (uint32_t)(((q4 ^ kq) >> 1) & 1);
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj) {
+                        const float t0 = pick(m0, src4[0][jj], src4[1][jj]);
+                        const float t1 = pick(m0, src4[2][jj], src4[3][jj]);
+                        logit[4 * kq + jj] = pick(m1, t0, t1);
+                    }
+                }
+                float mx = -INFINITY;
+#pragma unroll
+                for (int m = 0; m < MOT_MAX_EXPERTS; ++m) {
+                    if (m < E) {
+                        if (bru) logit[m] += bf16_to_f32(bru[m]);
+                        mx = fmaxf(mx, logit[m]);
+                    }
+                }
+                float gate_all[MOT_MAX_EXPERTS];
+                float den = 0.f;
+#pragma unroll
+                for (int m = 0; m < MOT_MAX_EXPERTS; ++m) {
+                    gate_all[m] = m < E ? __expf(logit[m] - mx) : 0.f;
+                    den += gate_all[m];
+                }
+                const float inv = 1.0f / den;
+                if (q4 == 0) {
+#pragma unroll
+                    for (int m = 0; m < MOT_MAX_EXPERTS; ++m)
+                        if (m < E) Gw[m * 32 + th * 16 + l16] = gate_all[m] * inv;
+                }
+            }
+        }
+        __syncthreads();                                     // barrier B
+
+        const float* Gw = Gs + w * (MOT_MAX_EXPERTS * 32);
+        // layer-1 biases of the two staged rows this lane's A operand covers
+        // (rows l16 and 16 + l16), in the low half of lane group 0, else zero
+        const int prow0 = w1_perm(l16), prow1 = w1_perm(16 + l16);
+        const uint32_t grp0 = q4 == 0 ? 0xFFFFFFFFu : 0u;
+        auto load_b1 = [&](int c, uint32_t* bv) {
+            typedef const __attribute__((address_space(1))) uint16_t* gu16;
+            bv[0] = (uint32_t)(*(gu16)(b1u + c * 32 + prow0)) & b1_mask & grp0;
+            bv[1] = (uint32_t)(*(gu16)(b1u + c * 32 + prow1)) & b1_mask & grp0;
+        };
+        // "ones" B operand: k = 0 is 1.0 for every token column, all else 0
+        const u32x4 ones = {0x3F80u & grp0, 0u, 0u, 0u};
+        // One iteration as a slot schedule of 16x16x32 MFMAs: four bias MFMAs
+        // (S[row][t] = b1[row] * 1), then KS2 k-steps x 2 row halves x 2 token
+        // halves, all on independent accumulators; W1 operand reads run LOOK
+        // slots ahead; the three-stage GELU of chunk c-1 is spread over the
+        // slots (stage s of element e in slot g0(e) + s*GD).
+        auto l1_iter = [&](auto l1c, auto gc, int c, int m, const uint32_t* bv,
+                           const f32x4 (&sp)[2][2], uint32_t* bnext, int c_next,
+                           f32x4 (&s)[2][2]) {
+            constexpr bool do_l1 = decltype(l1c)::value, do_gelu = decltype(gc)::value;
+            constexpr int NM = 4 + 4 * KS2, LOOK = 4, GD = 3;
+            const u32x4* W1c = W1s + (c & 1) * C::W1_CH;
+            u32x4* Hw = Hs + ((c - 1) & 1) * C::H_CH + w * 128;
+            const float hg0 = 0.5f * Gw[m * 32 + l16], hg1 = 0.5f * Gw[m * 32 + 16 + l16];
+            if constexpr (do_l1) load_b1(c_next, bnext);
+            u32x4 a1[KS2][2];
+            float h[2][2][4], gx[16], gt[16], gx2[16], gq[16], ge[16];
+            // A operand of (k-step s, row half hh), first used in slot 4 + 4s + 2hh
+            auto read_a = [&](auto kc) {
+                constexpr int k = decltype(kc)::value;
+                if constexpr (k >= 4 && k < NM && ((k - 4) % 2) == 0) {
+                    constexpr int s = (k - 4) / 4, hh = ((k - 4) / 2) % 2;
+                    const int row = hh * 16 + l16;
+                    a1[s][hh] = W1c[row * C::CPR1 + ((4 * s + q4) ^ (row & 7))];
+                }
+            };
+            const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+            if constexpr (do_l1) static_for<0, LOOK>([&](auto kc) { read_a(kc); });
+            static_for<0, NM>([&](auto kc) {
+                constexpr int k = decltype(kc)::value;
+                if constexpr (do_l1) {
+                    read_a(std::integral_constant<int, k + LOOK>{});
+                    if constexpr (k < 4) {
+                        constexpr int hh = k / 2, th = k % 2;
+                        const u32x4 ba = {bv[hh], 0u, 0u, 0u};
+                        s[hh][th] = mfma_16x16x32(ba, ones, zero4);
+                    } else {
+                        constexpr int st = (k - 4) / 4, hh = ((k - 4) / 2) % 2, th = (k - 4) % 2;
+                        s[hh][th] = mfma_16x16x32(a1[st][hh], zf[th][st], s[hh][th]);
+                    }
+                }
+                if constexpr (do_gelu) {
+                    static_for<0, 16>([&](auto ec) {
+                        constexpr int e = decltype(ec)::value;
+                        constexpr int hh = e / 8, th = (e / 4) % 2, jj = e % 4;
+                        constexpr int g0 = (e * (NM - 2 * GD - 1)) / 15;
+                        if constexpr (ACT == MOT_ACT_GELU) {
+                            if constexpr (k == g0) {
+                                float v = sp[hh][th][jj];
+                                asm volatile("" : "+v"(v));
+                                gx[e] = v;
+                                gelu_stage1(v, gt[e], gx2[e]);
+                                asm volatile("" : "+v"(gt[e]), "+v"(gx2[e]));
+                            } else if constexpr (k == g0 + GD) {
+                                gelu_stage2(gt[e], gx2[e], gq[e], ge[e]);
+                                asm volatile("" : "+v"(gq[e]), "+v"(ge[e]));
+                            } else if constexpr (k == g0 + 2 * GD) {
+                                h[hh][th][jj] = gelu_stage3(gx[e], gt[e], gq[e], ge[e], th ? hg1 : hg0);
+                            }
+                        } else if constexpr (k == g0) {
+                            float v = sp[hh][th][jj];
+                            asm volatile("" : "+v"(v));
+                            h[hh][th][jj] = 2.0f * (th ? hg1 : hg0) * v;
+                        }
+                    });
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            });
+            if constexpr (do_gelu) {
+                // token th*16 + l16: hidden 8*q4 .. 8*q4+3 from row half 0 and
+                // 8*q4+4 .. 8*q4+7 from row half 1: one 16-byte fragment unit
+#pragma unroll
+                for (int th = 0; th < 2; ++th) {
+                    u32x4 v;
+                    v[0] = pack_bf16x2(h[0][th][0], h[0][th][1]);
+                    v[1] = pack_bf16x2(h[0][th][2], h[0][th][3]);
+                    v[2] = pack_bf16x2(h[1][th][0], h[1][th][1]);
+                    v[3] = pack_bf16x2(h[1][th][2], h[1][th][3]);
+                    Hw[(q4 >> 1) * 64 + (q4 & 1) * 32 + th * 16 + l16] = v;
+                }
             }
         };
-        const u32x4* W1c = W1s + (c & 1) * C::W1_CH;
-        const u32x4* Hc = Hs + (c & 1) * C::H_CH;          // chunk c-2 shares c's parity
-        const u32x4* W2c = W2s + (c & 1) * C::W2_CH;
-        u32x4* Hw = Hs + ((c - 1) & 1) * C::H_CH + w * 128;
-        const float hg = 0.5f * Gw[m * 32 + l32];
-        f32x16 s;
+
+        int m1 = 0, kk1 = 0;
+        uint32_t bcur[2], bnext[2] = {0u, 0u};
+        load_b1(0, bcur);
+        f32x4 s_prev[2][2], s_new[2][2];
+        auto advance = [&]() {          // (m1, kk1) -> the next chunk
+            kk1 += 32;
+            const bool wrap = kk1 == hidden;
+            kk1 = wrap ? 0 : kk1;
+            m1 = wrap ? m1 + 1 : m1;
+        };
+        auto rotate = [&]() {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            s[2 * q] = bf16_lo(bv[0][q]);
-            s[2 * q + 1] = bf16_hi(bv[0][q]);
-            s[8 + 2 * q] = bf16_lo(bv[1][q]);
-            s[8 + 2 * q + 1] = bf16_hi(bv[1][q]);
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+                for (int b = 0; b < 2; ++b) s_prev[a][b] = s_new[a][b];
+            bcur[0] = bnext[0]; bcur[1] = bnext[1];
+        };
+        const std::integral_constant<bool, true> yes{};
+        const std::integral_constant<bool, false> no{};
+        // c = 0: layer 1 only; 1 .. nch-1: layer 1 and GELU; nch: GELU only;
+        // nch+1: barrier only (layer 2 of the last chunk runs on other waves)
+        sync_stage();
+        l1_iter(yes, no, 0, m1, bcur, s_prev, bnext, 1, s_new);
+        rotate();
+        for (int c = 1; c < nch; ++c) {
+            sync_stage();
+            l1_iter(yes, yes, c, m1, bcur, s_prev, bnext, c + 1 < nch ? c + 1 : nch - 1, s_new);
+            rotate();
+            advance();
         }
-        u32x4 a1[NL1], hA[2][TB], bW[2][C::NBW];
-        float h[16], gx[16], gt[16], gx2[16], gq[16], ge[16];
-        constexpr int GD = 2;   // slots between GELU stages
-        // operand reads needed by slot k
-        auto issue_reads = [&](auto kc) {
-            constexpr int k = decltype(kc)::value;
-            if constexpr (k < NM) {
-                constexpr int n1 = (k * NL1) / NM;
-                if constexpr (((k + 1) * NL1) / NM > n1) {
-                    a1[n1] = W1c[l32 * C::CPR1 + ((2 * n1 + g) ^ (l32 & 7))];
-                } else {
-                    constexpr int q = k - n1, ks = q / (TB * C::NBW), tb = (q / C::NBW) % TB,
-                                  nb = q % C::NBW;
+        sync_stage();
+        l1_iter(no, yes, nch, m1, bcur, s_prev, bnext, nch - 1, s_new);
+        sync_stage();
+    } else if (NLD == 1 && w == 3) {
+        // ---------------------------------------------------------- loader
+        uint32_t ow1[W1_RL], ow2[W2_RL];
+#pragma unroll
+        for (int r = 0; r < W1_RL; ++r) ow1[r] = w1_off(r);
+#pragma unroll
+        for (int r = 0; r < W2_RL; ++r) ow2[r] = w2_off(r);
+        auto load_w1 = [&](int c, int st) {
+#pragma unroll
+            for (int r = 0; r < W1_RL; ++r) load_w1_round(c, st, r, ow1[r]);
+        };
+        auto load_w2 = [&](int m, int kk, int st) {
+#pragma unroll
+            for (int r = 0; r < W2_RL; ++r) load_w2_round(m, kk, st, r, ow2[r]);
+        };
+        stage_router_weights();
+        load_w1(0, 0);
+        __syncthreads();                                     // barrier A
+        __syncthreads();                                     // barrier B
+        int m1 = 0, kk1 = 0;
+        for (int c = 0; c <= nch + 1; ++c) {
+            sync_stage();
+            const bool has_prev = c >= 1 && c <= nch;
+            if (c + 1 < nch) load_w1(c + 1, (c + 1) & 1);
+            if (has_prev) {
+                load_w2(m1, kk1, (c - 1) & 1);
+                kk1 += 32;
+                const bool wrap = kk1 == hidden;
+                kk1 = wrap ? 0 : kk1;
+                m1 = wrap ? m1 + 1 : m1;
+            }
+        }
+    } else if (is_l2) {
+        // ---------------------------------------------------------- layer 2
+        uint32_t ow1[NLD == 4 ? W1_RL : 1], ow2[NLD == 4 ? W2_RL : 1];
+        if constexpr (NLD == 4) {
+#pragma unroll
+            for (int r = 0; r < W1_RL; ++r) ow1[r] = w1_off(r);
+#pragma unroll
+            for (int r = 0; r < W2_RL; ++r) ow2[r] = w2_off(r);
+#pragma unroll
+            for (int r = 0; r < W1_RL; ++r) load_w1_round(0, 0, r, ow1[r]);
+        }
+        __syncthreads();                                     // barrier A
+        __syncthreads();                                     // barrier B
+        // accumulators seeded with sum_m g_m b2_m[o] on MFMA: A = gates of a
+        // token block (k = translator), B = b2 (k = translator); gates split
+        // into bf16 high + residual parts keep ~16 mantissa bits.
+        // acc[tb][nb]: column o = q2*OUTW + nb*32 + l32, rows = tokens
+        // tb*32 + 8*ii + 4*g + jj (element 4*ii + jj).
+        f32x16 acc[TB][C::NBW];
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+            for (int nb = 0; nb < C::NBW; ++nb)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) acc[tb][nb][e] = 0.f;
+        if (b2u) {
+            u32x4 bv[C::NBW];
+#pragma unroll
+            for (int nb = 0; nb < C::NBW; ++nb) {
+                const int o = q2 * C::OUTW + nb * 32 + l32;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int m0 = 8 * g + 2 * q;
+                    const uint32_t v0 = m0 < E ? b2u[(size_t)m0 * D_OUT + o] : 0u;
+                    const uint32_t v1 = m0 + 1 < E ? b2u[(size_t)(m0 + 1) * D_OUT + o] : 0u;
+                    bv[nb][q] = v0 | (v1 << 16);
+                }
+            }
+#pragma unroll
+            for (int tb = 0; tb < TB; ++tb) {
+                const float* Gt = Gs + tb * (MOT_MAX_EXPERTS * 32);
+                u32x4 ghi, glo;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int m0 = 8 * g + 2 * q;
+                    const float g0 = m0 < E ? Gt[m0 * 32 + l32] : 0.f;
+                    const float g1 = m0 + 1 < E ? Gt[(m0 + 1) * 32 + l32] : 0.f;
+                    const uint32_t hi = pack_bf16x2(g0, g1);
+                    ghi[q] = hi;
+                    glo[q] = pack_bf16x2(g0 - bf16_lo(hi), g1 - bf16_hi(hi));
+                }
+#pragma unroll
+                for (int nb = 0; nb < C::NBW; ++nb) {
+                    acc[tb][nb] = mfma_32x32x16(ghi, bv[nb], acc[tb][nb]);
+                    acc[tb][nb] = mfma_32x32x16(glo, bv[nb], acc[tb][nb]);
+                }
+            }
+        }
+
+        // One iteration as a slot schedule over this wave's MFMAs, ordered
+        // (k-slice, output block, token block) so few operands are live; H and
+        // W2 operand reads run LOOK slots ahead; when the layer-2 waves are the
+        // loading waves, their weight loads are spread over the slots.
+        auto l2_iter = [&](int c, bool do_l2, int c_w1, int m_w2, int kk_w2, bool do_w1, bool do_w2) {
+            constexpr int NM = 2 * TB * C::NBW, LOOK = 3;
+            constexpr int NV = NLD == 4 ? W1_RL + W2_RL : 0;
+            const u32x4* Hc = Hs + (c & 1) * C::H_CH;          // chunk c-2 shares c's parity
+            const u32x4* W2c = W2s + (c & 1) * C::W2_CH;
+            u32x4 hA[2][TB], bW[2][C::NBW];
+            auto issue_reads = [&](auto kc) {
+                constexpr int k = decltype(kc)::value;
+                if constexpr (k < NM) {
+                    constexpr int ks = k / (TB * C::NBW), nb = (k / TB) % C::NBW, tb = k % TB;
                     if constexpr (nb == 0) hA[ks][tb] = Hc[tb * 128 + ks * 64 + g * 32 + l32];
                     if constexpr (tb == 0) {
-                        const int o = w * C::OUTW + nb * 32 + l32;
+                        const int o = q2 * C::OUTW + nb * 32 + l32;
                         bW[ks][nb] = W2c[o * 4 + ((2 * ks + g) ^ ((o >> 1) & 3))];
                     }
                 }
-            }
+            };
+            if (do_l2) static_for<0, LOOK>([&](auto kc) { issue_reads(kc); });
+            static_for<0, NM>([&](auto kc) {
+                constexpr int k = decltype(kc)::value;
+                if constexpr (NV > 0) {
+                    static_for<0, NV>([&](auto rc) {
+                        constexpr int r = decltype(rc)::value;
+                        if constexpr ((r * NM) / NV == k) {
+                            if constexpr (r < W1_RL) {
+                                if (do_w1) load_w1_round(c_w1, (c + 1) & 1, r, ow1[r]);
+                            } else {
+                                if (do_w2) load_w2_round(m_w2, kk_w2, (c - 1) & 1, r - W1_RL, ow2[r - W1_RL]);
+                            }
+                        }
+                    });
+                }
+                if (do_l2) {
+                    issue_reads(std::integral_constant<int, k + LOOK>{});
+                    constexpr int ks = k / (TB * C::NBW), nb = (k / TB) % C::NBW, tb = k % TB;
+                    acc[tb][nb] = mfma_32x32x16(hA[ks][tb], bW[ks][nb], acc[tb][nb]);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            });
         };
-        static_for<0, LOOK>([&](auto kc) { issue_reads(kc); });
-        static_for<0, NM>([&](auto kc) {
-            constexpr int k = decltype(kc)::value;
-            static_for<0, NV>([&](auto rc) {
-                if constexpr ((decltype(rc)::value * NM) / NV == k) issue_vmem(rc);
-            });
-            issue_reads(std::integral_constant<int, k + LOOK>{});
-            constexpr int n1 = (k * NL1) / NM;
-            if constexpr (((k + 1) * NL1) / NM > n1) {
-                s = mfma_32x32x16(a1[n1], zf[n1], s);
-            } else {
-                constexpr int q = k - n1, ks = q / (TB * C::NBW), tb = (q / C::NBW) % TB,
-                              nb = q % C::NBW;
-                acc[tb][nb] = mfma_32x32x16(hA[ks][tb], bW[ks][nb], acc[tb][nb]);
+
+        int m1 = 0, kk1 = 0;
+        for (int c = 0; c <= nch + 1; ++c) {
+            sync_stage();
+            const bool has_prev = c >= 1 && c <= nch;
+            l2_iter(c, c >= 2, c + 1, m1, kk1, c + 1 < nch, has_prev);
+            if (has_prev) {
+                kk1 += 32;
+                const bool wrap = kk1 == hidden;
+                kk1 = wrap ? 0 : kk1;
+                m1 = wrap ? m1 + 1 : m1;
             }
-            // GELU of element e runs as three stages in slots g0(e), g0(e)+GD,
-            // g0(e)+2*GD, so several independent chains overlap in each slot
-            static_for<0, 16>([&](auto ec) {
-                constexpr int e = decltype(ec)::value;
-                constexpr int g0 = (e * (NM - 2 * GD - 1)) / 15;
-                if constexpr (ACT == MOT_ACT_GELU) {
-                    if constexpr (k == g0) {
-                        float v = sp[e];
-                        asm volatile("" : "+v"(v));
-                        gx[e] = v;
-                        gelu_stage1(v, gt[e], gx2[e]);
-                        asm volatile("" : "+v"(gt[e]), "+v"(gx2[e]));
-                    } else if constexpr (k == g0 + GD) {
-                        gelu_stage2(gt[e], gx2[e], gq[e], ge[e]);
-                        asm volatile("" : "+v"(gq[e]), "+v"(ge[e]));
-                    } else if constexpr (k == g0 + 2 * GD) {
-                        h[e] = gelu_stage3(gx[e], gt[e], gq[e], ge[e], hg);
+        }
+
+        // epilogue: bf16 round and store in the target layout
+        {
+        uint16_t* dst = reinterpret_cast<uint16_t*>(p.dst[x]) + (size_t)j * p.n_tok * D_OUT;
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int tok = tok0 + tb * 32 + 8 * (e >> 2) + 4 * g + (e & 3);
+                if (tok >= p.n_tok) continue;
+                const int b = tok / p.T, t = tok % p.T;
+#pragma unroll
+                for (int nb = 0; nb < C::NBW; ++nb) {
+                    const int o = q2 * C::OUTW + nb * 32 + l32;
+                    size_t off;
+                    if (p.dst_layout == MOT_LAYOUT_BTHD) {
+                        off = (size_t)tok * D_OUT + o;
+                    } else {
+                        const int hh = o / p.D_tgt, dd = o % p.D_tgt;
+                        off = (((size_t)b * p.H_tgt + hh) * p.T + t) * p.D_tgt + dd;
                     }
-                } else if constexpr (k == g0) {
-                    float v = sp[e];
-                    asm volatile("" : "+v"(v));
-                    h[e] = 2.0f * hg * v;
+                    dst[off] = (uint16_t)(pack_bf16x2(acc[tb][nb][e], 0.f) & 0xFFFFu);
                 }
-            });
-            __builtin_amdgcn_sched_barrier(0);
-        });
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            u32x4 v;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) v[q] = pack_bf16x2(h[8 * ks + 2 * q], h[8 * ks + 2 * q + 1]);
-            Hw[ks * 64 + g * 32 + l32] = v;
-        }
-        return s;
-    };
-
-    // ---- prologue (chunks 0, 1), steady state, drain.  (m1, kk1) = the
-    // translator and column offset of chunk c-1, advanced by 32 per step.
-    const int nch = EH / 32;   // >= 2
-    int m1 = 0, kk1 = 0;
-    auto advance = [&]() {
-        kk1 += 32;
-        const bool wrap = kk1 == hidden;
-        kk1 = wrap ? 0 : kk1;
-        m1 = wrap ? m1 + 1 : m1;
-    };
-    u32x4 bcur[2], bnext[2];
-    load_b1(0, bcur);
-    f32x16 s_prev;
-    sync_stage();                          // iteration 0
-    load_w1(1, 1);
-    load_b1(1, bnext);
-    s_prev = layer1(0, bcur);
-    bcur[0] = bnext[0]; bcur[1] = bnext[1];
-    sync_stage();                          // iteration 1
-    load_w1(nch > 2 ? 2 : nch - 1, 0);
-    load_w2(m1, kk1, 0);
-    load_b1(nch > 2 ? 2 : nch - 1, bnext);
-    {
-        f32x16 s_new = layer1(1, bcur);
-        gelu_store(0, m1, s_prev);
-        s_prev = s_new;
-    }
-    advance();
-    bcur[0] = bnext[0]; bcur[1] = bnext[1];
-    for (int c = 2; c < nch; ++c) {        // steady state: one basic block
-        sync_stage();
-        const int cn = c + 1 < nch ? c + 1 : nch - 1;
-        f32x16 s_new = steady_slots(c, m1, bcur, s_prev, cn, m1, kk1, bnext);
-        s_prev = s_new;
-        advance();
-        bcur[0] = bnext[0]; bcur[1] = bnext[1];
-    }
-    sync_stage();                          // iteration nch
-    load_w2(m1, kk1, (nch - 1) & 1);
-    gelu_store(nch - 1, m1, s_prev);
-    layer2(nch - 2);
-    sync_stage();                          // iteration nch + 1
-    layer2(nch - 1);
-
-    // ---- epilogue: bf16 round and store in the target layout
-    uint16_t* dst = reinterpret_cast<uint16_t*>(p.dst[x]) + (size_t)j * p.n_tok * D_OUT;
-#pragma unroll
-    for (int tb = 0; tb < TB; ++tb) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const int tok = tok0 + tb * 32 + 8 * (e >> 2) + 4 * g + (e & 3);
-            if (tok >= p.n_tok) continue;
-            const int b = tok / p.T, t = tok % p.T;
-#pragma unroll
-            for (int nb = 0; nb < C::NBW; ++nb) {
-                const int o = w * C::OUTW + nb * 32 + l32;
-                size_t off;
-                if (p.dst_layout == MOT_LAYOUT_BTHD) {
-                    off = (size_t)tok * D_OUT + o;
-                } else {
-                    const int hh = o / p.D_tgt, dd = o % p.D_tgt;
-                    off = (((size_t)b * p.H_tgt + hh) * p.T + t) * p.D_tgt + dd;
-                }
-                dst[off] = (uint16_t)(pack_bf16x2(acc[tb][nb][e], 0.f) & 0xFFFFu);
             }
         }
+    }
+    } else {
+        // idle wave (TB = 3 and loads on the layer-2 waves never happens; kept
+        // for barrier parity): none
+        __syncthreads();
+        __syncthreads();
+        for (int c = 0; c <= nch + 1; ++c) sync_stage();
     }
 }
 
@@ -536,9 +582,9 @@ hipError_t launch_t(const Problem& p, const UnitTab& ut, hipStream_t stream) {
     using C = Cfg<D_IN, D_OUT>;
     dim3 grid((p.n_tok + C::BM - 1) / C::BM, ut.n);
     if (p.act == MOT_ACT_GELU)
-        hipLaunchKernelGGL((k_bf16_fused<D_IN, D_OUT, MOT_ACT_GELU>), grid, dim3(256), 0, stream, p, ut);
+        hipLaunchKernelGGL((k_bf16_fused<D_IN, D_OUT, MOT_ACT_GELU>), grid, dim3(512), 0, stream, p, ut);
     else
-        hipLaunchKernelGGL((k_bf16_fused<D_IN, D_OUT, MOT_ACT_IDENTITY>), grid, dim3(256), 0, stream, p, ut);
+        hipLaunchKernelGGL((k_bf16_fused<D_IN, D_OUT, MOT_ACT_IDENTITY>), grid, dim3(512), 0, stream, p, ut);
     return hipGetLastError();
 }
 
