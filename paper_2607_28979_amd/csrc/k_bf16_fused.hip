@@ -38,6 +38,11 @@ namespace {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+// Elements (of 16 per lane and chunk) whose GELU runs before the layer-1 MFMAs
+#ifndef MOT_FUSED_PHASE_A
+#define MOT_FUSED_PHASE_A 10
+#endif
+
 template <int D_IN, int D_OUT>
 struct Cfg {
     static constexpr int TB = D_OUT == 512 ? 3 : 4;   // token blocks per workgroup
@@ -48,12 +53,15 @@ struct Cfg {
     static constexpr int CPR1 = D_IN / 8;         // 16-byte chunks per W1 row
     static constexpr int W1_CH = 32 * CPR1;       // chunks per W1 stage
     static constexpr int W2_CH = D_OUT * 4;       // chunks per W2 stage (32 hidden = 4 chunks)
-    static constexpr int H_CH = 4 * 128;          // chunks per hidden stage (4 blocks x 32 tokens x 32)
-    static constexpr int GS = 4 * MOT_MAX_EXPERTS * 32;   // gate floats (4 token blocks)
+    static constexpr int H_CH = TB * 128;         // chunks per hidden stage (TB blocks x 32 tokens x 32)
+    static constexpr int GS = TB * MOT_MAX_EXPERTS * 32;  // gate floats
+    // W2 stages: three (each chunk fetched two iterations before its use)
+    // when they fit in the 160 KB of LDS, else two (one iteration ahead)
+    static constexpr int NW2 = (2 * W1_CH + 3 * W2_CH + 2 * H_CH + GS / 4) * 16 <= 160 * 1024 ? 3 : 2;
     // LDS map in 16-byte units
     static constexpr int OFF_W1 = 0;
     static constexpr int OFF_W2 = OFF_W1 + 2 * W1_CH;
-    static constexpr int OFF_H = OFF_W2 + 2 * W2_CH;
+    static constexpr int OFF_H = OFF_W2 + NW2 * W2_CH;
     static constexpr int OFF_G = OFF_H + 2 * H_CH;
     static constexpr int TOTAL = OFF_G + GS / 4;
     static_assert(W1_CH % 256 == 0 && W2_CH % 256 == 0 && NBW >= 1, "tile shape");
@@ -96,9 +104,8 @@ template <int D_IN, int D_OUT, int ACT>
 __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
     using C = Cfg<D_IN, D_OUT>;
     constexpr int TB = C::TB;
-    // waves that issue the global -> LDS weight loads: wave 3 alone when it has
-    // no token block (TB = 3), else the four layer-2 waves
-    constexpr int NLD = TB == 3 ? 1 : 4;
+    // the four layer-2 waves issue the global -> LDS weight loads
+    constexpr int NLD = 4;
     constexpr int W1_RL = C::W1_CH / (64 * NLD), W2_RL = C::W2_CH / (64 * NLD);
     __shared__ u32x4 smem[C::TOTAL];
     u32x4* W1s = smem + C::OFF_W1;
@@ -117,9 +124,8 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
     const int tok0 = blockIdx.x * C::BM;
     const bool is_l1 = w < TB;                 // layer-1 + GELU wave of token block w
     const bool is_l2 = w >= 4;                 // layer-2 wave q = w - 4
-    const bool is_ld = NLD == 1 ? w == 3 : is_l2;
     const int q2 = w - 4;                      // layer-2 column group
-    const int lw = NLD == 1 ? 0 : q2;          // index among the loading waves
+    const int lw = q2;                         // index among the loading waves
 
     const uint16_t* W1u = reinterpret_cast<const uint16_t*>(p.w1) + unit * EH * D_IN;
     const uint16_t* W2u = reinterpret_cast<const uint16_t*>(p.w2) + unit * E * D_OUT * hidden;
@@ -129,28 +135,32 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
     const uint16_t* b2u = p.b2 ? reinterpret_cast<const uint16_t*>(p.b2) + unit * E * D_OUT : nullptr;
     const uint16_t* Wru = reinterpret_cast<const uint16_t*>(p.wr) + unit * E * D_IN;
 
-    // ---- global -> LDS weight loads (loading waves only)
-    // byte offset, within a chunk, of the 16 bytes this lane loads in round r
-    auto w1_off = [&](int r) -> uint32_t {
-        const int slot = r * 64 * NLD + lw * 64 + lane;
-        const int row = slot / C::CPR1, pc = slot % C::CPR1, cl = pc ^ (row & 7);
-        return (uint32_t)(w1_perm(row) * D_IN + cl * 8) * 2u;
+    // ---- global -> LDS weight loads (the four layer-2 waves)
+    // Round r of a stage load fills LDS slots [r*256, r*256 + 256); this lane
+    // fills slot r*256 + t.  Its global byte offset is a per-lane part plus a
+    // part that depends on r only:
+    //   W1: staged row r*RS + u (RS = 256/CPR1, u = t/CPR1), chunk t % CPR1;
+    //       w1_perm and the (row & 15) swizzle act on the disjoint bits of
+    //       r*RS and u, so only (r*RS) & 15 (NV1 values) changes the lane part;
+    //   W2: output row 64r + t/4, swizzle ((row >> 2) & 3) the same for all r.
+    const int t_ld = lw * 64 + lane;
+    constexpr int RS = 256 / C::CPR1;
+    constexpr int NV1 = RS < 16 ? 16 / RS : 1;
+    auto w1_lane = [&](int v) -> uint32_t {
+        const int u = t_ld / C::CPR1, pc = t_ld % C::CPR1;
+        return (uint32_t)(w1_perm(u) * D_IN + ((pc ^ (u & 15)) ^ ((v * RS) & 15)) * 8) * 2u;
     };
-    auto w2_off = [&](int r) -> uint32_t {
-        const int slot = r * 64 * NLD + lw * 64 + lane;
-        const int o = slot >> 2, pc = slot & 3, cl = pc ^ ((o >> 1) & 3);
-        return (uint32_t)(o * hidden + cl * 8) * 2u;
-    };
+    const uint32_t w2_lane = (uint32_t)((t_ld >> 2) * hidden + ((t_ld & 3) ^ ((t_ld >> 4) & 3)) * 8) * 2u;
     // chunk c of W1 (round r) into stage st; the chunk base is wave-uniform,
     // so each load is a scalar base plus a per-lane offset
-    auto load_w1_round = [&](int c, int st, int r, uint32_t off) {
-        const char* base = reinterpret_cast<const char*>(W1u + (size_t)c * 32 * D_IN);
-        load_lds16(base + off, W1s + st * C::W1_CH + r * 64 * NLD + lw * 64);
+    auto load_w1_round = [&](int c, int st, int r, uint32_t lane_off) {
+        const char* base = reinterpret_cast<const char*>(W1u + (size_t)c * 32 * D_IN + w1_perm(r * RS) * D_IN);
+        load_lds16(base + lane_off, W1s + st * C::W1_CH + r * 64 * NLD + lw * 64);
     };
     // W2 columns [kk, kk+32) of translator m (round r) into stage st
-    auto load_w2_round = [&](int m, int kk, int st, int r, uint32_t off) {
-        const char* base = reinterpret_cast<const char*>(W2u + (size_t)m * D_OUT * hidden + kk);
-        load_lds16(base + off, W2s + st * C::W2_CH + r * 64 * NLD + lw * 64);
+    auto load_w2_round = [&](int m, int kk, int st, int r) {
+        const char* base = reinterpret_cast<const char*>(W2u + ((size_t)m * D_OUT + 64 * r) * hidden + kk);
+        load_lds16(base + w2_lane, W2s + st * C::W2_CH + r * 64 * NLD + lw * 64);
     };
     const int nch = EH / 32;   // >= 2
     // The three roles run the same number of workgroup barriers: two around
@@ -163,7 +173,7 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
 #pragma unroll
         for (int r = 0; r < C::W1_CH / 256; ++r) {
             const int slot = r * 256 + tid;
-            const int row = slot / C::CPR1, pc = slot % C::CPR1, cl = pc ^ (row & 7);
+            const int row = slot / C::CPR1, pc = slot % C::CPR1, cl = pc ^ (row & 15);
             const u32x4 zero = {0u, 0u, 0u, 0u};
             Rs[slot] = row < E ? *reinterpret_cast<const u32x4*>(Wru + (size_t)row * D_IN + cl * 8) : zero;
         }
@@ -217,7 +227,7 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
                 f32x4 lg = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int s = 0; s < KS2; ++s) {
-                    const u32x4 a = Rs[l16 * C::CPR1 + ((4 * s + q4) ^ (l16 & 7))];
+                    const u32x4 a = Rs[l16 * C::CPR1 + ((4 * s + q4) ^ l16)];
                     lg = mfma_16x16x32(a, zf[th][s], lg);
                 }
                 // lane group q4 holds experts 4*q4 .. 4*q4+3 of token l16; the
@@ -272,23 +282,36 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
         // (rows l16 and 16 + l16), in the low half of lane group 0, else zero
         const int prow0 = w1_perm(l16), prow1 = w1_perm(16 + l16);
         const uint32_t grp0 = q4 == 0 ? 0xFFFFFFFFu : 0u;
+        const uint32_t bsel = b1_mask & grp0;
+        // raw loads, one chunk ahead; the masks are applied only at the use in
+        // the next iteration, so nothing waits on these loads mid-iteration
         auto load_b1 = [&](int c, uint32_t* bv) {
             typedef const __attribute__((address_space(1))) uint16_t* gu16;
-            bv[0] = (uint32_t)(*(gu16)(b1u + c * 32 + prow0)) & b1_mask & grp0;
-            bv[1] = (uint32_t)(*(gu16)(b1u + c * 32 + prow1)) & b1_mask & grp0;
+            bv[0] = (uint32_t)(*(gu16)(b1u + c * 32 + prow0));
+            bv[1] = (uint32_t)(*(gu16)(b1u + c * 32 + prow1));
         };
         // "ones" B operand: k = 0 is 1.0 for every token column, all else 0
         const u32x4 ones = {0x3F80u & grp0, 0u, 0u, 0u};
-        // One iteration as a slot schedule of 16x16x32 MFMAs: four bias MFMAs
-        // (S[row][t] = b1[row] * 1), then KS2 k-steps x 2 row halves x 2 token
-        // halves, all on independent accumulators; W1 operand reads run LOOK
-        // slots ahead; the three-stage GELU of chunk c-1 is spread over the
-        // slots (stage s of element e in slot g0(e) + s*GD).
+        // W1 operand of (k-step s, row half hh) sits at W1c[abase[s & 3] +
+        // hh*16*CPR1 + 16*(s >> 2)]: the swizzled chunk (4s + q4) ^ l16 splits
+        // into a per-lane part and compile-time offsets
+        int abase[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) abase[b] = l16 * C::CPR1 + 4 * (b ^ (l16 >> 2)) + (q4 ^ (l16 & 3));
+        // One iteration in two phases.  Phase A: GELU of the first NEA of the
+        // lane's 16 elements of chunk c-1, vector work only, while the layer-2
+        // wave on this SIMD runs its MFMAs.  Phase B: a slot schedule of
+        // 16x16x32 MFMAs (four bias MFMAs S[row][t] = b1[row] * 1, then KS2
+        // k-steps x 2 row halves x 2 token halves, all on independent
+        // accumulators) with the three-stage GELU of the other elements spread
+        // over the slots (stage s of element e in slot g0(e) + s*GD); W1
+        // operand reads run LOOK slots ahead.
+        constexpr int NEA = MOT_FUSED_PHASE_A;
         auto l1_iter = [&](auto l1c, auto gc, int c, int m, const uint32_t* bv,
                            const f32x4 (&sp)[2][2], uint32_t* bnext, int c_next,
                            f32x4 (&s)[2][2]) {
             constexpr bool do_l1 = decltype(l1c)::value, do_gelu = decltype(gc)::value;
-            constexpr int NM = 4 + 4 * KS2, LOOK = 4, GD = 3;
+            constexpr int NM = 4 + 4 * KS2, LOOK = 4, GD = 3, NEB = 16 - NEA;
             const u32x4* W1c = W1s + (c & 1) * C::W1_CH;
             u32x4* Hw = Hs + ((c - 1) & 1) * C::H_CH + w * 128;
             const float hg0 = 0.5f * Gw[m * 32 + l16], hg1 = 0.5f * Gw[m * 32 + 16 + l16];
@@ -300,30 +323,51 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
                 constexpr int k = decltype(kc)::value;
                 if constexpr (k >= 4 && k < NM && ((k - 4) % 2) == 0) {
                     constexpr int s = (k - 4) / 4, hh = ((k - 4) / 2) % 2;
-                    const int row = hh * 16 + l16;
-                    a1[s][hh] = W1c[row * C::CPR1 + ((4 * s + q4) ^ (row & 7))];
+                    a1[s][hh] = W1c[abase[s & 3] + hh * 16 * C::CPR1 + 16 * (s >> 2)];
+                }
+            };
+            auto gelu_elem = [&](auto ec, auto stc) {
+                constexpr int e = decltype(ec)::value, st = decltype(stc)::value;
+                constexpr int hh = e / 8, th = (e / 4) % 2, jj = e % 4;
+                if constexpr (ACT == MOT_ACT_GELU) {
+                    if constexpr (st == 0) {
+                        gx[e] = sp[hh][th][jj];
+                        gelu_stage1(gx[e], gt[e], gx2[e]);
+                    } else if constexpr (st == 1) {
+                        gelu_stage2(gt[e], gx2[e], gq[e], ge[e]);
+                    } else {
+                        h[hh][th][jj] = gelu_stage3(gx[e], gt[e], gq[e], ge[e], th ? hg1 : hg0);
+                    }
+                } else if constexpr (st == 0) {
+                    h[hh][th][jj] = 2.0f * (th ? hg1 : hg0) * sp[hh][th][jj];
                 }
             };
             const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
             if constexpr (do_l1) static_for<0, LOOK>([&](auto kc) { read_a(kc); });
+            if constexpr (do_gelu) {
+                static_for<0, 3>([&](auto stc) {
+                    static_for<0, NEA>([&](auto ec) { gelu_elem(ec, stc); });
+                });
+            }
+            __builtin_amdgcn_sched_barrier(0);
             static_for<0, NM>([&](auto kc) {
                 constexpr int k = decltype(kc)::value;
                 if constexpr (do_l1) {
                     read_a(std::integral_constant<int, k + LOOK>{});
                     if constexpr (k < 4) {
                         constexpr int hh = k / 2, th = k % 2;
-                        const u32x4 ba = {bv[hh], 0u, 0u, 0u};
+                        const u32x4 ba = {bv[hh] & bsel, 0u, 0u, 0u};
                         s[hh][th] = mfma_16x16x32(ba, ones, zero4);
                     } else {
                         constexpr int st = (k - 4) / 4, hh = ((k - 4) / 2) % 2, th = (k - 4) % 2;
                         s[hh][th] = mfma_16x16x32(a1[st][hh], zf[th][st], s[hh][th]);
                     }
                 }
-                if constexpr (do_gelu) {
-                    static_for<0, 16>([&](auto ec) {
-                        constexpr int e = decltype(ec)::value;
+                if constexpr (do_gelu && NEB > 0) {
+                    static_for<0, NEB>([&](auto ec) {
+                        constexpr int eb = decltype(ec)::value, e = NEA + eb;
                         constexpr int hh = e / 8, th = (e / 4) % 2, jj = e % 4;
-                        constexpr int g0 = (e * (NM - 2 * GD - 1)) / 15;
+                        constexpr int g0 = NEB > 1 ? (eb * (NM - 2 * GD - 1)) / (NEB - 1) : 0;
                         if constexpr (ACT == MOT_ACT_GELU) {
                             if constexpr (k == g0) {
                                 float v = sp[hh][th][jj];
@@ -394,49 +438,13 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
         sync_stage();
         l1_iter(no, yes, nch, m1, bcur, s_prev, bnext, nch - 1, s_new);
         sync_stage();
-    } else if (NLD == 1 && w == 3) {
-        // ---------------------------------------------------------- loader
-        uint32_t ow1[W1_RL], ow2[W2_RL];
-#pragma unroll
-        for (int r = 0; r < W1_RL; ++r) ow1[r] = w1_off(r);
-#pragma unroll
-        for (int r = 0; r < W2_RL; ++r) ow2[r] = w2_off(r);
-        auto load_w1 = [&](int c, int st) {
-#pragma unroll
-            for (int r = 0; r < W1_RL; ++r) load_w1_round(c, st, r, ow1[r]);
-        };
-        auto load_w2 = [&](int m, int kk, int st) {
-#pragma unroll
-            for (int r = 0; r < W2_RL; ++r) load_w2_round(m, kk, st, r, ow2[r]);
-        };
-        stage_router_weights();
-        load_w1(0, 0);
-        __syncthreads();                                     // barrier A
-        __syncthreads();                                     // barrier B
-        int m1 = 0, kk1 = 0;
-        for (int c = 0; c <= nch + 1; ++c) {
-            sync_stage();
-            const bool has_prev = c >= 1 && c <= nch;
-            if (c + 1 < nch) load_w1(c + 1, (c + 1) & 1);
-            if (has_prev) {
-                load_w2(m1, kk1, (c - 1) & 1);
-                kk1 += 32;
-                const bool wrap = kk1 == hidden;
-                kk1 = wrap ? 0 : kk1;
-                m1 = wrap ? m1 + 1 : m1;
-            }
-        }
     } else if (is_l2) {
         // ---------------------------------------------------------- layer 2
-        uint32_t ow1[NLD == 4 ? W1_RL : 1], ow2[NLD == 4 ? W2_RL : 1];
-        if constexpr (NLD == 4) {
+        uint32_t ow1[NV1];
 #pragma unroll
-            for (int r = 0; r < W1_RL; ++r) ow1[r] = w1_off(r);
+        for (int v = 0; v < NV1; ++v) ow1[v] = w1_lane(v);
 #pragma unroll
-            for (int r = 0; r < W2_RL; ++r) ow2[r] = w2_off(r);
-#pragma unroll
-            for (int r = 0; r < W1_RL; ++r) load_w1_round(0, 0, r, ow1[r]);
-        }
+        for (int r = 0; r < W1_RL; ++r) load_w1_round(0, 0, r, ow1[r % NV1]);
         __syncthreads();                                     // barrier A
         __syncthreads();                                     // barrier B
         // accumulators seeded with sum_m g_m b2_m[o] on MFMA: A = gates of a
@@ -489,11 +497,13 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
         // (k-slice, output block, token block) so few operands are live; H and
         // W2 operand reads run LOOK slots ahead; when the layer-2 waves are the
         // loading waves, their weight loads are spread over the slots.
-        auto l2_iter = [&](int c, bool do_l2, int c_w1, int m_w2, int kk_w2, bool do_w1, bool do_w2) {
+        auto l2_iter = [&](auto l2c, auto w1c, auto w2c, int c, int c_w1, int m_w2, int kk_w2, int st_w2) {
+            constexpr bool do_l2 = decltype(l2c)::value, do_w1 = decltype(w1c)::value,
+                           do_w2 = decltype(w2c)::value;
             constexpr int NM = 2 * TB * C::NBW, LOOK = 3;
-            constexpr int NV = NLD == 4 ? W1_RL + W2_RL : 0;
+            constexpr int NV = W1_RL + W2_RL;
             const u32x4* Hc = Hs + (c & 1) * C::H_CH;          // chunk c-2 shares c's parity
-            const u32x4* W2c = W2s + (c & 1) * C::W2_CH;
+            const u32x4* W2c = W2s + ((c + C::NW2 - 2) % C::NW2) * C::W2_CH;
             u32x4 hA[2][TB], bW[2][C::NBW];
             auto issue_reads = [&](auto kc) {
                 constexpr int k = decltype(kc)::value;
@@ -502,11 +512,11 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
                     if constexpr (nb == 0) hA[ks][tb] = Hc[tb * 128 + ks * 64 + g * 32 + l32];
                     if constexpr (tb == 0) {
                         const int o = q2 * C::OUTW + nb * 32 + l32;
-                        bW[ks][nb] = W2c[o * 4 + ((2 * ks + g) ^ ((o >> 1) & 3))];
+                        bW[ks][nb] = W2c[o * 4 + ((2 * ks + g) ^ ((o >> 2) & 3))];
                     }
                 }
             };
-            if (do_l2) static_for<0, LOOK>([&](auto kc) { issue_reads(kc); });
+            if constexpr (do_l2) static_for<0, LOOK>([&](auto kc) { issue_reads(kc); });
             static_for<0, NM>([&](auto kc) {
                 constexpr int k = decltype(kc)::value;
                 if constexpr (NV > 0) {
@@ -514,14 +524,14 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
                         constexpr int r = decltype(rc)::value;
                         if constexpr ((r * NM) / NV == k) {
                             if constexpr (r < W1_RL) {
-                                if (do_w1) load_w1_round(c_w1, (c + 1) & 1, r, ow1[r]);
+                                if constexpr (do_w1) load_w1_round(c_w1, (c + 1) & 1, r, ow1[r % NV1]);
                             } else {
-                                if (do_w2) load_w2_round(m_w2, kk_w2, (c - 1) & 1, r - W1_RL, ow2[r - W1_RL]);
+                                if constexpr (do_w2) load_w2_round(m_w2, kk_w2, st_w2, r - W1_RL);
                             }
                         }
                     });
                 }
-                if (do_l2) {
+                if constexpr (do_l2) {
                     issue_reads(std::integral_constant<int, k + LOOK>{});
                     constexpr int ks = k / (TB * C::NBW), nb = (k / TB) % C::NBW, tb = k % TB;
                     acc[tb][nb] = mfma_32x32x16(hA[ks][tb], bW[ks][nb], acc[tb][nb]);
@@ -530,18 +540,46 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
             });
         };
 
+        // (m1, kk1): translator and column offset of W2 chunk kw, the one
+        // fetched in iteration c: kw = c with three W2 stages, else c - 1
         int m1 = 0, kk1 = 0;
-        for (int c = 0; c <= nch + 1; ++c) {
+        const std::integral_constant<bool, true> T{};
+        const std::integral_constant<bool, false> F{};
+        auto advance = [&]() {
+            kk1 += 32;
+            const bool wrap = kk1 == hidden;
+            kk1 = wrap ? 0 : kk1;
+            m1 = wrap ? m1 + 1 : m1;
+        };
+        // Iteration c runs layer 2 of chunk c-2 (c >= 2), fetches W1 of chunk
+        // c+1 (c+1 < nch) and W2 of chunk kw (0 <= kw < nch).  The pipeline
+        // fill and drain iterations are peeled with their stage flags fixed at
+        // compile time (nch >= 2); the steady state runs every stage.
+        constexpr bool W2_AT_C = C::NW2 == 3;   // kw = c, else kw = c - 1
+        const std::integral_constant<bool, W2_AT_C> W2_FIRST{};
+        const std::integral_constant<bool, !W2_AT_C> W2_LAST{};
+        auto w2_stage = [&](int c) { return (c - (W2_AT_C ? 0 : 1) + C::NW2) % C::NW2; };
+        sync_stage();                                                   // c = 0
+        l2_iter(F, T, W2_FIRST, 0, 1, m1, kk1, w2_stage(0));
+        if (W2_AT_C) advance();
+        sync_stage();                                                   // c = 1
+        if (nch > 2) l2_iter(F, T, T, 1, 2, m1, kk1, w2_stage(1));
+        else l2_iter(F, F, T, 1, 2, m1, kk1, w2_stage(1));
+        advance();
+        for (int c = 2; c + 1 < nch; ++c) {                             // steady state
             sync_stage();
-            const bool has_prev = c >= 1 && c <= nch;
-            l2_iter(c, c >= 2, c + 1, m1, kk1, c + 1 < nch, has_prev);
-            if (has_prev) {
-                kk1 += 32;
-                const bool wrap = kk1 == hidden;
-                kk1 = wrap ? 0 : kk1;
-                m1 = wrap ? m1 + 1 : m1;
-            }
+            l2_iter(T, T, T, c, c + 1, m1, kk1, w2_stage(c));
+            advance();
         }
+        if (nch >= 3) {                                                 // c = nch - 1
+            sync_stage();
+            l2_iter(T, F, T, nch - 1, nch, m1, kk1, w2_stage(nch - 1));
+            advance();
+        }
+        sync_stage();                                                   // c = nch
+        l2_iter(T, F, W2_LAST, nch, nch + 1, m1, kk1, w2_stage(nch));
+        sync_stage();                                                   // c = nch + 1
+        l2_iter(T, F, F, nch + 1, nch + 2, m1, kk1, w2_stage(nch + 1));
 
         // epilogue: bf16 round and store in the target layout
         {
@@ -569,8 +607,9 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
         }
     }
     } else {
-        // idle wave (TB = 3 and loads on the layer-2 waves never happens; kept
-        // for barrier parity): none
+        // wave 3 when TB = 3: no token block; it helps stage the router
+        // weights and joins every barrier
+        stage_router_weights();
         __syncthreads();
         __syncthreads();
         for (int c = 0; c <= nch + 1; ++c) sync_stage();
