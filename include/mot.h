@@ -62,7 +62,11 @@ typedef enum { MOT_ALGO_AUTO = 0, MOT_ALGO_UNFUSED = 1, MOT_ALGO_FUSED = 2 } mot
  *   H_src, D_src   source KV heads and head dim
  *   H_tgt, D_tgt   target KV heads and head dim
  *   E              translators per unit (1..MOT_MAX_EXPERTS)
- *   top_k          translators used per token; must equal E (dense mixture)
+ *   top_k          translators used per token, 1..E: the top_k largest softmax
+ *                  scores are kept and renormalised to sum to one, the others
+ *                  are zero (ties go to the lower translator index); top_k = E
+ *                  is the dense mixture.  The kernels still evaluate every
+ *                  translator: unselected ones contribute exactly zero.
  *   hidden         translator hidden width
  *   dtype          MOT_F32: fp32 storage and math (erf GELU, expf softmax).
  *                  MOT_BF16: bf16 storage; fp32 accumulation; fp32 gates;

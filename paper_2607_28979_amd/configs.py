@@ -40,6 +40,7 @@ class Workload:
     key_outlier_mult: float = 1.0
     src_layout: int = 0
     dst_layout: int = 0
+    top_k: int = 0                   # translators used per token; 0 = all E (dense)
 
     @property
     def d_in(self) -> int:

@@ -1,31 +1,28 @@
 // Fused bf16 translation kernel: router + translator layer 1 + GELU + gate +
-// translator layer 2 + gated mix + store, in one pass per token tile.  The
-// E*hidden activations of a token never leave the chip.
+// translator layer 2 + gated mix + store, in one pass per token tile (paper
+// Sec. 3, Definition "Mixture-of-Translators", with the Linear-GELU-Linear
+// translator body).  The E*hidden activations of a token never leave the chip.
 //
-// Workgroup = one unit (target layer, K or V) x TB token blocks of 32
-// (TB = 4, or 3 when d_out = 512 so the output accumulators leave AGPR room
-// for layer 1); four waves, one per SIMD.  Wave w:
-//   * holds the source rows of token block w (32 x d_in bf16) in VGPRs as
-//     MFMA B operands for the whole kernel (with TB = 3, wave 3 runs a
-//     discarded layer-1 block on zero rows: it keeps the loop branch-free and
-//     costs no time, since waves 0..2 set the pace);
-//   * router: logits = Wr z on MFMA (Wr zero-padded to 32 rows), fp32
-//     softmax -> gates (paper Sec. 3, Definition "Mixture-of-Translators");
-//   * owns output columns [w*d_out/4, (w+1)*d_out/4) for all TB blocks; its
-//     accumulators are seeded with sum_m g_m b2_m[o] by small MFMAs;
-//   * walks E*hidden in 32-wide chunks (each inside one translator m) as a
-//     three-stage software pipeline; iteration c runs, independently,
-//       layer 1 of chunk c:   S^T = W1_m[c] z^T + b1   (MFMA, A = W1 from LDS)
-//       GELU of chunk c-1:    H = bf16(g_m * GELU(S))  (VALU; written to LDS)
-//       layer 2 of chunk c-2: Y += H . W2_m[:, c]^T    (MFMA, A = H, B = W2)
-//     so matrix-core and vector work overlap; the expert reduction of the
-//     gated sum happens inside Y.
-//   W1's 32 rows are staged in a permuted order (w1_perm) that makes each
-//   lane's layer-1 accumulator fragment exactly the 16-byte A-operand pieces
-//   of layer 2.  Weight chunks move global -> LDS with direct-to-LDS 16-byte
-//   loads, one chunk ahead; LDS tiles are XOR-swizzled in 16-byte units so
-//   every fragment read is bank-conflict free.
-//   * Y is rounded to bf16 and stored in the target layout.
+// Workgroup = one unit (target layer, K or V) x TB token blocks of 32 (TB = 3
+// when d_out = 512, else 4); eight waves, two per SIMD, with fixed roles:
+//   * waves 0..TB-1: source rows of one token block in VGPRs (MFMA B operand)
+//     for the whole kernel; router logits on MFMA, fp32 softmax, Top-K; then
+//     per 32-wide chunk of E*hidden: layer 1 (S = W1_m[c] z^T + b1, four
+//     independent 16x16x32 accumulators) and g_m * GELU(S) -> bf16 hidden tile
+//     in LDS;
+//   * waves 4..7: d_out/4 output columns each, for all TB blocks; accumulators
+//     seeded with sum_m g_m b2_m; per chunk Y += H . W2_m[:, c]^T (32x32x16);
+//     they also issue every global -> LDS weight load (direct-to-LDS, no VGPR
+//     staging);
+//   * wave 3 when TB = 3: no block; joins the barriers.
+// Iteration c runs layer 1 of chunk c, the GELU of chunk c-1 and layer 2 of
+// chunk c-2, and fetches W1 of chunk c+1 and W2 of chunk c (three W2 stages)
+// or c-1 (two); one workgroup barrier per iteration.  W1's 32 rows are staged
+// in a permuted order (w1_perm) that leaves each lane, per token, 8
+// consecutive hidden values: exactly a 16-byte piece of the layer-2 A operand.
+// LDS tiles are XOR-swizzled in 16-byte units so every 16-lane group of a
+// fragment read hits distinct banks.  Y is rounded to bf16 and stored in the
+// target layout.
 #include <type_traits>
 
 #include "mot_device.h"
@@ -268,10 +265,13 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
                     den += gate_all[m];
                 }
                 const float inv = 1.0f / den;
+#pragma unroll
+                for (int m = 0; m < MOT_MAX_EXPERTS; ++m) gate_all[m] *= inv;
+                topk_renormalise(gate_all, E, p.top_k);
                 if (q4 == 0) {
 #pragma unroll
                     for (int m = 0; m < MOT_MAX_EXPERTS; ++m)
-                        if (m < E) Gw[m * 32 + th * 16 + l16] = gate_all[m] * inv;
+                        if (m < E) Gw[m * 32 + th * 16 + l16] = gate_all[m];
                 }
             }
         }

@@ -1,4 +1,5 @@
-// Router GEMV + softmax: gates[unit][token][m] = softmax_m(Wr_unit z + br_unit).
+// Router GEMV + softmax: gates[unit][token][m] = softmax_m(Wr_unit z + br_unit),
+// then Top-K: the top_k largest kept and renormalised, the rest zero.
 // Paper Sec. 3, Definition "Mixture-of-Translators": token-level nonnegative
 // gate scores; here softmax of a linear map of the source row.
 //
@@ -117,10 +118,13 @@ __global__ __launch_bounds__(256) void k_router(Problem p, UnitTab ut) {
         }
     }
     const float inv = 1.0f / den;
+#pragma unroll
+    for (int m = 0; m < MOT_MAX_EXPERTS; ++m) acc[m] = m < E ? acc[m] * inv : 0.f;
+    topk_renormalise(acc, E, p.top_k);
     float* g = p.gates + ((size_t)gs * p.n_tok_pad + tok) * E;
 #pragma unroll
     for (int m = 0; m < MOT_MAX_EXPERTS; ++m)
-        if (m < E) g[m] = acc[m] * inv;
+        if (m < E) g[m] = acc[m];
 }
 
 }  // namespace

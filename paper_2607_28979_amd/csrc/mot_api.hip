@@ -61,9 +61,6 @@ mot_status check_shapes(const mot_shapes* s) {
         return fail(MOT_ERR_BAD_SHAPE, "E=%d must be in [1, %d]", s->E, MOT_MAX_EXPERTS);
     if (s->top_k < 1 || s->top_k > s->E)
         return fail(MOT_ERR_BAD_SHAPE, "top_k=%d must be in [1, E=%d]", s->top_k, s->E);
-    if (s->top_k != s->E)
-        return fail(MOT_ERR_UNSUPPORTED, "top_k=%d < E=%d: only the dense mixture (top_k == E) is implemented",
-                    s->top_k, s->E);
     if (s->dtype != MOT_F32 && s->dtype != MOT_BF16)
         return fail(MOT_ERR_BAD_SHAPE, "dtype=%d is not MOT_F32 or MOT_BF16", s->dtype);
     if ((s->src_layout != MOT_LAYOUT_BTHD && s->src_layout != MOT_LAYOUT_BHTD) ||
@@ -99,7 +96,7 @@ Problem base_problem(const mot_shapes* s) {
     Problem p;
     memset(&p, 0, sizeof p);
     p.B = s->B; p.T = s->T; p.H_src = s->H_src; p.D_src = s->D_src;
-    p.H_tgt = s->H_tgt; p.D_tgt = s->D_tgt; p.E = s->E; p.hidden = s->hidden;
+    p.H_tgt = s->H_tgt; p.D_tgt = s->D_tgt; p.E = s->E; p.top_k = s->top_k; p.hidden = s->hidden;
     p.d_in = s->H_src * s->D_src; p.d_out = s->H_tgt * s->D_tgt;
     p.n_tok = s->B * s->T;
     p.n_tok_pad = (int32_t)round_up((size_t)p.n_tok, 128);

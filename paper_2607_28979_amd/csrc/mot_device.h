@@ -41,6 +41,35 @@ __device__ __forceinline__ f32x4 mfma_16x16x32(u32x4 a, u32x4 b, f32x4 c) {
                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+// Top-K of the E softmax scores g[0..E) (paper Sec. 3, Definition
+// "Mixture-of-Translators": the K largest scores, renormalised to sum to one
+// over the selected set; the others become zero).  K rounds each take the
+// largest score not yet taken; the scan is ascending with a strict '>', so
+// ties go to the lower index.  K >= E keeps every score unchanged (the dense
+// mixture).
+template <int EMAX>
+__device__ __forceinline__ void topk_renormalise(float (&g)[EMAX], int E, int K) {
+    if (K >= E) return;
+    uint32_t taken = 0;
+    float sum = 0.f;
+    for (int k = 0; k < K; ++k) {
+        int best = -1;
+        float bv = 0.f;
+#pragma unroll
+        for (int m = 0; m < EMAX; ++m) {
+            const bool cand = m < E && !((taken >> m) & 1u) && (best < 0 || g[m] > bv);
+            best = cand ? m : best;
+            bv = cand ? g[m] : bv;
+        }
+        if (best < 0) break;
+        taken |= 1u << best;
+        sum += bv;
+    }
+    const float inv = 1.0f / sum;
+#pragma unroll
+    for (int m = 0; m < EMAX; ++m) g[m] = ((taken >> m) & 1u) ? g[m] * inv : 0.f;
+}
+
 // Exact-erf GELU, x * Phi(x), with the device erff.
 __device__ __forceinline__ float gelu_erf(float x) {
     return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));

@@ -36,7 +36,7 @@ struct Problem {
     const void* b2;       // [L_tgt][2][E][d_out] or null
     const void* wr;       // [L_tgt][2][E][d_in]
     const void* br;       // [L_tgt][2][E] or null
-    int32_t B, T, H_src, D_src, H_tgt, D_tgt, E, hidden;
+    int32_t B, T, H_src, D_src, H_tgt, D_tgt, E, top_k, hidden;
     int32_t d_in, d_out, n_tok, n_tok_pad;   // n_tok_pad: n_tok rounded up to 128
     int32_t src_layout, dst_layout, act;
     float* gates;         // workspace: [n_units_total][n_tok_pad][E] fp32

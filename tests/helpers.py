@@ -50,7 +50,8 @@ def oracle_dims(w, act=0):
     from oracle import OracleDims
     return OracleDims(L_src=w.L_src, L_tgt=w.L_tgt, B=w.B, T=w.T, H_src=w.H_src, D_src=w.D_src,
                       H_tgt=w.H_tgt, D_tgt=w.D_tgt, E=w.E, hidden=w.hidden,
-                      src_layout=w.src_layout, dst_layout=w.dst_layout, act=act)
+                      src_layout=w.src_layout, dst_layout=w.dst_layout, act=act,
+                      top_k=w.top_k)
 
 
 def unit_rows(dst, w, j):

@@ -87,12 +87,12 @@ def test_null_pointers(lib):
 
 @pytest.mark.parametrize("kw", [dict(L_src=0), dict(L_tgt=257), dict(B=-1), dict(E=0), dict(E=17),
                                 dict(hidden=0), dict(dtype=7), dict(src_layout=2), dict(act=5),
-                                dict(algo=9), dict(top_k=5)])
+                                dict(algo=9), dict(top_k=5), dict(top_k=-1)])
 def test_bad_shapes(lib, kw):
     _expect("MOT_ERR_BAD_SHAPE", shapes=_shapes(**kw), layer_map=[0] * 300)
 
 
-@pytest.mark.parametrize("kw", [dict(top_k=1), dict(D_src=60), dict(hidden=96),
+@pytest.mark.parametrize("kw", [dict(D_src=60), dict(hidden=96),
                                 dict(H_tgt=1, D_tgt=24), dict(dtype=mb.MOT_F32, D_src=6, H_src=2),
                                 dict(algo=mb.ALGO_FUSED, dtype=mb.MOT_F32),
                                 dict(algo=mb.ALGO_FUSED, H_src=12, D_src=64)])
