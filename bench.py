@@ -61,7 +61,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=3,
                     help="index into the workload list (default 3: Qwen2.5-1.5B -> 7B)")
-    ap.add_argument("--algo", type=int, default=0, help="0 auto, 1 unfused, 2 fused")
+    ap.add_argument("--algo", type=int, default=0, help="0 auto, 1 unfused, 2 fused, 3 routed")
+    ap.add_argument("--top-k", type=int, default=0,
+                    help="translators per token (default: the workload's, i.e. all E); below E "
+                         "the auto path is the routed Top-K kernel")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample rows (0 = auto)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -81,6 +84,8 @@ def main():
     from paper_2607_28979_amd.inputs import generate, bf16_bits
 
     w = WORKLOADS[args.workload]
+    if args.top_k:
+        w = w.with_(top_k=args.top_k)
     torch.cuda.set_device(0)
     t0 = time.time()
     inp = generate(w)
@@ -144,19 +149,23 @@ def main():
     n_tok = w.n_tok
     value = n_tok / (ms_per_step / 1e3)
     flops = w.gemm_flops()
-    fused = args.algo == 2 or (args.algo == 0 and w.dtype == "bf16"
-                              and w.d_in in (128, 256, 512) and w.d_out in (128, 256, 512))
+    fusable = w.dtype == "bf16" and w.d_in in (128, 256, 512) and w.d_out in (128, 256, 512)
+    routed = args.algo == 3 or (args.algo == 0 and fusable and 0 < w.top_k < w.E)
+    fused = not routed and (args.algo == 2 or (args.algo == 0 and fusable))
     achieved_tflops = flops / (avg_call_ms / 1e3) / 1e12
     peak = PEAK_TFLOPS[w.dtype]
     roofline = {
         "bound": "mfma",
-        "kernel": "k_bf16_fused" if fused else "mot_translate (router + gemm1 + gemm2)",
+        "kernel": ("k_bf16_fused" if fused else
+                   "mot_translate routed (router lists + plan + k_bf16_fused tiles%s)"
+                   % (" + combine" if w.top_k > 1 else "") if routed
+                   else "mot_translate (router + gemm1 + gemm2)"),
         "achieved": round(achieved_tflops, 2),
         "peak": peak,
         "unit": "TFLOP/s",
         "frac": round(achieved_tflops / peak, 4),
         "traffic": (measured_traffic("k_bf16_fused.hip", "qwen2.5-1.5b-7b")
-                    if fused and args.workload == 3 else None),
+                    if fused and args.workload == 3 and not args.top_k else None),
         "alg_flops_per_launch": flops,
         "alg_bytes_per_launch": w.alg_bytes(),
         "hbm_gbs_alg": round(w.alg_bytes() / (avg_call_ms / 1e3) / 1e9, 1),
@@ -181,7 +190,7 @@ def main():
         "data": "synthetic (seeded numpy; shapes and value recipe of the model pair)",
         "config": {"workload": w.name, "L_src": w.L_src, "L_tgt": w.L_tgt, "B": w.B, "T": w.T,
                    "d_in": w.d_in, "hidden": w.hidden, "d_out": w.d_out, "E": w.E,
-                   "units": w.units(), "parallelism": "single GPU"},
+                   "top_k": w.top_k or w.E, "units": w.units(), "parallelism": "single GPU"},
         "mfma_util_pct": round(100 * achieved_tflops / peak, 2),
         "roofline": roofline,
         "cpu_baseline": cpu,
@@ -195,7 +204,7 @@ def cpu_baseline(w, inp, lm, rows):
     from oracle import OracleDims, oracle_rows
     threads = min(16, os.cpu_count() or 1)
     od = OracleDims(L_src=w.L_src, L_tgt=w.L_tgt, B=w.B, T=w.T, H_src=w.H_src, D_src=w.D_src,
-                    H_tgt=w.H_tgt, D_tgt=w.D_tgt, E=w.E, hidden=w.hidden)
+                    H_tgt=w.H_tgt, D_tgt=w.D_tgt, E=w.E, hidden=w.hidden, top_k=w.top_k)
     units = [(j, x) for j in range(w.L_tgt) if lm[j] >= 0 for x in (0, 1)]
     per_row_flops = w.gemm_flops() / w.n_tok
     if rows <= 0:

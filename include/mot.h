@@ -53,7 +53,7 @@ typedef enum {
 typedef enum { MOT_F32 = 0, MOT_BF16 = 1 } mot_dtype;
 typedef enum { MOT_LAYOUT_BTHD = 0, MOT_LAYOUT_BHTD = 1 } mot_layout;
 typedef enum { MOT_ACT_GELU = 0, MOT_ACT_IDENTITY = 1 } mot_act;
-typedef enum { MOT_ALGO_AUTO = 0, MOT_ALGO_UNFUSED = 1, MOT_ALGO_FUSED = 2 } mot_algo;
+typedef enum { MOT_ALGO_AUTO = 0, MOT_ALGO_UNFUSED = 1, MOT_ALGO_FUSED = 2, MOT_ALGO_ROUTED = 3 } mot_algo;
 
 /*
  * Problem sizes and options (host struct, read during the call only).
@@ -76,12 +76,20 @@ typedef enum { MOT_ALGO_AUTO = 0, MOT_ALGO_UNFUSED = 1, MOT_ALGO_FUSED = 2 } mot
  *   src_layout     layout of each source layer: BTHD [B][T][H][D] or BHTD
  *   dst_layout     layout of each target layer, same encoding
  *   act            MOT_ACT_GELU (the method) or MOT_ACT_IDENTITY (tests)
- *   algo           kernel path: MOT_ALGO_AUTO picks; MOT_ALGO_FUSED = one
- *                  kernel per token tile (bf16 only; d_in and d_out in
- *                  {128, 256, 512}; no workspace); MOT_ALGO_UNFUSED = router,
- *                  then two grouped GEMMs through a hidden-activation
- *                  workspace.  Requesting an impossible path returns
- *                  MOT_ERR_UNSUPPORTED.  All paths compute the same function.
+ *   algo           kernel path: MOT_ALGO_AUTO picks (ROUTED when top_k < E and
+ *                  the fused kernel fits, else FUSED when it fits, else
+ *                  UNFUSED); MOT_ALGO_FUSED = one kernel per token tile over
+ *                  every translator (bf16 only; d_in and d_out in
+ *                  {128, 256, 512}; no workspace); MOT_ALGO_ROUTED = the same
+ *                  shapes, Top-K sparse: a router pass writes each token's
+ *                  top_k translators, a per-unit counting sort groups the
+ *                  (token, translator) pairs by translator, the fused kernel
+ *                  runs each translator only on its tokens, and for top_k > 1
+ *                  a combine sums each token's top_k rows (workspace needed);
+ *                  MOT_ALGO_UNFUSED = router, then two grouped GEMMs through a
+ *                  hidden-activation workspace.  Requesting an impossible path
+ *                  returns MOT_ERR_UNSUPPORTED.  All paths compute the same
+ *                  function.
  *   workspace      optional device scratch; NULL = library-owned buffer
  *   workspace_bytes size of `workspace` in bytes
  *

@@ -18,7 +18,7 @@ _LIB_PATH = os.path.join(HERE, "csrc", "libmot.so")
 MOT_F32, MOT_BF16 = 0, 1
 LAYOUT_BTHD, LAYOUT_BHTD = 0, 1
 ACT_GELU, ACT_IDENTITY = 0, 1
-ALGO_AUTO, ALGO_UNFUSED, ALGO_FUSED = 0, 1, 2
+ALGO_AUTO, ALGO_UNFUSED, ALGO_FUSED, ALGO_ROUTED = 0, 1, 2, 3
 
 STATUS = {0: "MOT_OK", 1: "MOT_ERR_NULL_ARG", 2: "MOT_ERR_BAD_SHAPE", 3: "MOT_ERR_BAD_LAYER_MAP",
           4: "MOT_ERR_UNSUPPORTED", 5: "MOT_ERR_MISALIGNED", 6: "MOT_ERR_WORKSPACE_TOO_SMALL",

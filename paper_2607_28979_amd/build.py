@@ -18,7 +18,14 @@ CSRC = os.path.join(HERE, "csrc")
 ROOT = os.path.dirname(HERE)
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(CSRC, "libmot.so")
-SOURCES = ["mot_api.hip", "k_router.hip", "k_f32.hip", "k_bf16_unfused.hip", "k_bf16_fused.hip"]
+# (source, object name, preprocessor definitions); the fused kernel's
+# instantiation file is compiled once per (d_in, d_out) so they build in parallel
+SOURCES = [(f, os.path.splitext(f)[0], {}) for f in
+           ("mot_api.hip", "k_router.hip", "k_routed.hip", "k_f32.hip", "k_bf16_unfused.hip",
+            "k_bf16_fused.hip")]
+SOURCES += [("k_bf16_fused_inst.hip", "k_bf16_fused_%d_%d" % (a, b),
+             {"MOT_FUSED_D_IN": a, "MOT_FUSED_D_OUT": b})
+            for a in (128, 256, 512) for b in (128, 256, 512)]
 
 
 def hipcc() -> str:
@@ -35,9 +42,11 @@ def flags():
             "-I", os.path.join(ROOT, "include")]
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *flags(), "-c", os.path.join(CSRC, src), "-o", obj]
+def _compile(entry) -> str:
+    src, name, defs = entry
+    obj = os.path.join(BUILD, name + ".o")
+    cmd = [hipcc(), *flags(), *["-D%s=%s" % kv for kv in defs.items()], "-c", os.path.join(CSRC, src),
+           "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("compile failed: %s\n%s%s" % (" ".join(cmd), r.stdout, r.stderr))

@@ -59,9 +59,11 @@ class Workload:
 
     def gemm_flops(self) -> float:
         """Algorithmic multiply-add flops of one full translation: router,
-        first and second translator layers, for every unit and token."""
-        per_tok_unit = 2.0 * (self.d_in * self.E + self.d_in * self.E * self.hidden
-                              + self.E * self.hidden * self.d_out)
+        first and second translator layers of the translators each token
+        uses (all E, or its top_k), for every unit and token."""
+        used = self.top_k if 0 < self.top_k < self.E else self.E
+        per_tok_unit = 2.0 * (self.d_in * self.E + used * (self.d_in * self.hidden
+                                                            + self.hidden * self.d_out))
         return per_tok_unit * self.n_tok * self.units()
 
     def alg_bytes(self) -> float:

@@ -1,638 +1,31 @@
-// Fused bf16 translation kernel: router + translator layer 1 + GELU + gate +
-// translator layer 2 + gated mix + store, in one pass per token tile (paper
-// Sec. 3, Definition "Mixture-of-Translators", with the Linear-GELU-Linear
-// translator body).  The E*hidden activations of a token never leave the chip.
-//
-// Workgroup = one unit (target layer, K or V) x TB token blocks of 32 (TB = 3
-// when d_out = 512, else 4); eight waves, two per SIMD, with fixed roles:
-//   * waves 0..TB-1: source rows of one token block in VGPRs (MFMA B operand)
-//     for the whole kernel; router logits on MFMA, fp32 softmax, Top-K; then
-//     per 32-wide chunk of E*hidden: layer 1 (S = W1_m[c] z^T + b1, four
-//     independent 16x16x32 accumulators) and g_m * GELU(S) -> bf16 hidden tile
-//     in LDS;
-//   * waves 4..7: d_out/4 output columns each, for all TB blocks; accumulators
-//     seeded with sum_m g_m b2_m; per chunk Y += H . W2_m[:, c]^T (32x32x16);
-//     they also issue every global -> LDS weight load (direct-to-LDS, no VGPR
-//     staging);
-//   * wave 3 when TB = 3: no block; joins the barriers.
-// Iteration c runs layer 1 of chunk c, the GELU of chunk c-1 and layer 2 of
-// chunk c-2, and fetches W1 of chunk c+1 and W2 of chunk c (three W2 stages)
-// or c-1 (two); one workgroup barrier per iteration.  W1's 32 rows are staged
-// in a permuted order (w1_perm) that leaves each lane, per token, 8
-// consecutive hidden values: exactly a 16-byte piece of the layer-2 A operand.
-// LDS tiles are XOR-swizzled in 16-byte units so every 16-lane group of a
-// fragment read hits distinct banks.  Y is rounded to bf16 and stored in the
-// target layout.
-#include <type_traits>
-
-#include "mot_device.h"
-#include "mot_internal.h"
-#include "../../include/mot.h"
+// Host side of the fused kernel: shape support and dispatch to the
+// per-shape instantiations (k_bf16_fused_inst.hip, built once per shape).
+#include "k_bf16_fused_kernel.h"
 
 namespace mot {
 
+#define MOT_DECL(a, b) \
+    hipError_t launch_fused_##a##_##b(const Problem& p, const UnitTab& ut, bool routed, hipStream_t stream);
+MOT_DECL(128, 128) MOT_DECL(128, 256) MOT_DECL(128, 512)
+MOT_DECL(256, 128) MOT_DECL(256, 256) MOT_DECL(256, 512)
+MOT_DECL(512, 128) MOT_DECL(512, 256) MOT_DECL(512, 512)
+#undef MOT_DECL
+
 namespace {
 
-typedef __attribute__((address_space(3))) void lds_void;
-
-// Elements (of 16 per lane and chunk) whose GELU runs before the layer-1 MFMAs
-#ifndef MOT_FUSED_PHASE_A
-#define MOT_FUSED_PHASE_A 10
-#endif
-
-template <int D_IN, int D_OUT>
-struct Cfg {
-    static constexpr int TB = D_OUT == 512 ? 3 : 4;   // token blocks per workgroup
-    static constexpr int BM = 32 * TB;            // tokens per workgroup
-    static constexpr int KS1 = D_IN / 16;         // layer-1 k-steps
-    static constexpr int OUTW = D_OUT / 4;        // output columns per wave
-    static constexpr int NBW = OUTW / 32;         // output blocks per wave
-    static constexpr int CPR1 = D_IN / 8;         // 16-byte chunks per W1 row
-    static constexpr int W1_CH = 32 * CPR1;       // chunks per W1 stage
-    static constexpr int W2_CH = D_OUT * 4;       // chunks per W2 stage (32 hidden = 4 chunks)
-    static constexpr int H_CH = TB * 128;         // chunks per hidden stage (TB blocks x 32 tokens x 32)
-    static constexpr int GS = TB * MOT_MAX_EXPERTS * 32;  // gate floats
-    // W2 stages: three (each chunk fetched two iterations before its use)
-    // when they fit in the 160 KB of LDS, else two (one iteration ahead)
-    static constexpr int NW2 = (2 * W1_CH + 3 * W2_CH + 2 * H_CH + GS / 4) * 16 <= 160 * 1024 ? 3 : 2;
-    // LDS map in 16-byte units
-    static constexpr int OFF_W1 = 0;
-    static constexpr int OFF_W2 = OFF_W1 + 2 * W1_CH;
-    static constexpr int OFF_H = OFF_W2 + NW2 * W2_CH;
-    static constexpr int OFF_G = OFF_H + 2 * H_CH;
-    static constexpr int TOTAL = OFF_G + GS / 4;
-    static_assert(W1_CH % 256 == 0 && W2_CH % 256 == 0 && NBW >= 1, "tile shape");
-    static_assert(TB * NBW * 16 <= 192, "layer-2 accumulators must leave VGPR room");
-};
-
-// Row R of a staged 32-row W1 block holds hidden row w1_perm(R) of the chunk.
-// Layer 1 runs as 16x16 MFMA blocks over row halves hh = R / 16; lane group q
-// of a block's accumulator holds rows 4q + j, j = 0..3.  Mapping row
-// hh*16 + 4q + j to hidden 8q + 4hh + j gives each lane, for one token, the
-// eight consecutive hidden values 8q .. 8q+7: one 16-byte unit of the
-// layer-2 A-operand tile.
-__device__ __forceinline__ int w1_perm(int r) {
-    const int hh = r >> 4, q = (r >> 2) & 3, jj = r & 3;
-    return 8 * q + 4 * hh + jj;
-}
-
-__device__ __forceinline__ void load_lds16(const void* gsrc, u32x4* lds_dst_wave_base) {
-    __builtin_amdgcn_global_load_lds(gsrc, (lds_void*)lds_dst_wave_base, 16, 0, 0);
-}
-
-// Per-lane choice between two registers as a bitwise blend, so the compiler
-// cannot fold it into a dynamically indexed (scratch) array access.
-__device__ __forceinline__ float pick(uint32_t mask, float a, float b) {
-    return __uint_as_float((__float_as_uint(a) & ~mask) | (__float_as_uint(b) & mask));
-}
-
-__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-
-// Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E).
-template <int B, int E, class F>
-__device__ __forceinline__ void static_for(F&& f) {
-    if constexpr (B < E) {
-        f(std::integral_constant<int, B>{});
-        static_for<B + 1, E>(f);
-    }
-}
-
-template <int D_IN, int D_OUT, int ACT>
-__global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
-    using C = Cfg<D_IN, D_OUT>;
-    constexpr int TB = C::TB;
-    // the four layer-2 waves issue the global -> LDS weight loads
-    constexpr int NLD = 4;
-    constexpr int W1_RL = C::W1_CH / (64 * NLD), W2_RL = C::W2_CH / (64 * NLD);
-    __shared__ u32x4 smem[C::TOTAL];
-    u32x4* W1s = smem + C::OFF_W1;
-    u32x4* W2s = smem + C::OFF_W2;
-    u32x4* Hs = smem + C::OFF_H;
-    float* Gs = reinterpret_cast<float*>(smem + C::OFF_G);
-
-    const uint32_t code = ut.code[blockIdx.y];
-    const int j = unit_j(code), x = unit_x(code), i = unit_i(code);
-    const int E = p.E, hidden = p.hidden, EH = E * hidden;
-    const size_t unit = (size_t)j * 2 + x;
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // 0..7
-    const int g = lane >> 5, l32 = lane & 31;
-    const uint32_t gmask = 0u - (uint32_t)g;   // all ones in the upper lane half
-    const int tok0 = blockIdx.x * C::BM;
-    const bool is_l1 = w < TB;                 // layer-1 + GELU wave of token block w
-    const bool is_l2 = w >= 4;                 // layer-2 wave q = w - 4
-    const int q2 = w - 4;                      // layer-2 column group
-    const int lw = q2;                         // index among the loading waves
-
-    const uint16_t* W1u = reinterpret_cast<const uint16_t*>(p.w1) + unit * EH * D_IN;
-    const uint16_t* W2u = reinterpret_cast<const uint16_t*>(p.w2) + unit * E * D_OUT * hidden;
-    // layer-1 bias: without one, read W1 instead and mask the bits to zero
-    const uint16_t* b1u = p.b1 ? reinterpret_cast<const uint16_t*>(p.b1) + unit * EH : W1u;
-    const uint32_t b1_mask = p.b1 ? 0xFFFFFFFFu : 0u;
-    const uint16_t* b2u = p.b2 ? reinterpret_cast<const uint16_t*>(p.b2) + unit * E * D_OUT : nullptr;
-    const uint16_t* Wru = reinterpret_cast<const uint16_t*>(p.wr) + unit * E * D_IN;
-
-    // ---- global -> LDS weight loads (the four layer-2 waves)
-    // Round r of a stage load fills LDS slots [r*256, r*256 + 256); this lane
-    // fills slot r*256 + t.  Its global byte offset is a per-lane part plus a
-    // part that depends on r only:
-    //   W1: staged row r*RS + u (RS = 256/CPR1, u = t/CPR1), chunk t % CPR1;
-    //       w1_perm and the (row & 15) swizzle act on the disjoint bits of
-    //       r*RS and u, so only (r*RS) & 15 (NV1 values) changes the lane part;
-    //   W2: output row 64r + t/4, swizzle ((row >> 2) & 3) the same for all r.
-    const int t_ld = lw * 64 + lane;
-    constexpr int RS = 256 / C::CPR1;
-    constexpr int NV1 = RS < 16 ? 16 / RS : 1;
-    auto w1_lane = [&](int v) -> uint32_t {
-        const int u = t_ld / C::CPR1, pc = t_ld % C::CPR1;
-        return (uint32_t)(w1_perm(u) * D_IN + ((pc ^ (u & 15)) ^ ((v * RS) & 15)) * 8) * 2u;
-    };
-    const uint32_t w2_lane = (uint32_t)((t_ld >> 2) * hidden + ((t_ld & 3) ^ ((t_ld >> 4) & 3)) * 8) * 2u;
-    // chunk c of W1 (round r) into stage st; the chunk base is wave-uniform,
-    // so each load is a scalar base plus a per-lane offset
-    auto load_w1_round = [&](int c, int st, int r, uint32_t lane_off) {
-        const char* base = reinterpret_cast<const char*>(W1u + (size_t)c * 32 * D_IN + w1_perm(r * RS) * D_IN);
-        load_lds16(base + lane_off, W1s + st * C::W1_CH + r * 64 * NLD + lw * 64);
-    };
-    // W2 columns [kk, kk+32) of translator m (round r) into stage st
-    auto load_w2_round = [&](int m, int kk, int st, int r) {
-        const char* base = reinterpret_cast<const char*>(W2u + ((size_t)m * D_OUT + 64 * r) * hidden + kk);
-        load_lds16(base + w2_lane, W2s + st * C::W2_CH + r * 64 * NLD + lw * 64);
-    };
-    const int nch = EH / 32;   // >= 2
-    // The three roles run the same number of workgroup barriers: two around
-    // the router, then one per pipeline iteration c = 0 .. nch+1.  Iteration c
-    // runs layer 1 of chunk c, the GELU of chunk c-1 and layer 2 of chunk c-2;
-    // the loading wave(s) fetch W1 of chunk c+1 and W2 of chunk c-1.
-    // (m1, kk1) = translator and column offset of chunk c-1.
-    auto stage_router_weights = [&]() {   // waves 0..3
-        u32x4* Rs = W1s + C::W1_CH;
-#pragma unroll
-        for (int r = 0; r < C::W1_CH / 256; ++r) {
-            const int slot = r * 256 + tid;
-            const int row = slot / C::CPR1, pc = slot % C::CPR1, cl = pc ^ (row & 15);
-            const u32x4 zero = {0u, 0u, 0u, 0u};
-            Rs[slot] = row < E ? *reinterpret_cast<const u32x4*>(Wru + (size_t)row * D_IN + cl * 8) : zero;
-        }
-    };
-    auto sync_stage = [&]() {
-        wait_vm_all();
-        __syncthreads();
-    };
-
-    if (is_l1) {
-        // ---------------------------------------------------------- layer 1
-        // Layer 1 and the router use v_mfma_f32_16x16x32_bf16: the 32-token
-        // block is two 16-token halves th, the 32 staged W1 rows two 16-row
-        // halves hh, so the chunk's S block is four independent 16x16
-        // accumulators (no dependent MFMA chain).  Lane l = 16*q + l16 holds
-        // S rows 4q + j of each sub-block for token th*16 + l16.
-        constexpr int KS2 = D_IN / 32;
-        const int l16 = lane & 15, q4 = lane >> 4;
-        u32x4 zf[2][KS2];   // B operand: token th*16 + l16, k = 32s + 8*q4 .. +7
-        {
-            const uint16_t* src = reinterpret_cast<const uint16_t*>(p.src[x]) + (size_t)i * p.n_tok * D_IN;
-#pragma unroll
-            for (int th = 0; th < 2; ++th) {
-                const int my_tok = tok0 + 32 * w + 16 * th + l16;
-                const bool ok = my_tok < p.n_tok;
-                const int b = ok ? my_tok / p.T : 0, t = ok ? my_tok % p.T : 0;
-#pragma unroll
-                for (int s = 0; s < KS2; ++s) {
-                    const int k = 32 * s + 8 * q4;
-                    size_t off;
-                    if (p.src_layout == MOT_LAYOUT_BTHD) {
-                        off = (size_t)my_tok * D_IN + k;
-                    } else {
-                        const int hh = k / p.D_src, dd = k % p.D_src;
-                        off = (((size_t)b * p.H_src + hh) * p.T + t) * p.D_src + dd;
-                    }
-                    const u32x4 zero = {0u, 0u, 0u, 0u};
-                    zf[th][s] = ok ? *reinterpret_cast<const u32x4*>(src + off) : zero;
-                }
-            }
-        }
-        stage_router_weights();
-        __syncthreads();                                     // barrier A
-        {
-            // router on MFMA: logits[expert][token] = Wr z (Wr rows >= E zero)
-            const u32x4* Rs = W1s + C::W1_CH;
-            const uint16_t* bru = p.br ? reinterpret_cast<const uint16_t*>(p.br) + unit * E : nullptr;
-            float* Gw = Gs + w * (MOT_MAX_EXPERTS * 32);
-#pragma unroll
-            for (int th = 0; th < 2; ++th) {
-                f32x4 lg = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int s = 0; s < KS2; ++s) {
-                    const u32x4 a = Rs[l16 * C::CPR1 + ((4 * s + q4) ^ l16)];
-                    lg = mfma_16x16x32(a, zf[th][s], lg);
-                }
-                // lane group q4 holds experts 4*q4 .. 4*q4+3 of token l16; the
-                // other three groups' experts come from lanes ^ 16, ^ 32, ^ 48
-                float src4[4][4];
-#pragma unroll
-                for (int jj = 0; jj < 4; ++jj) {
-                    src4[0][jj] = lg[jj];
-                    src4[1][jj] = __shfl_xor(lg[jj], 16, 64);
-                    src4[2][jj] = __shfl_xor(lg[jj], 32, 64);
-                    src4[3][jj] = __shfl_xor(lg[jj], 48, 64);
-                }
-                float logit[16];
-#pragma unroll
-                for (int kq = 0; kq < 4; ++kq) {
-                    // experts 4*kq.. live in the source with index q4 ^ kq
-                    const uint32_t m0 = 0u - (uint32_t)((q4 ^ kq) & 1), m1 = 0u - (uint32_t)(((q4 ^ kq) >> 1) & 1);
-#pragma unroll
-                    for (int jj = 0; jj < 4; ++jj) {
-                        const float t0 = pick(m0, src4[0][jj], src4[1][jj]);
-                        const float t1 = pick(m0, src4[2][jj], src4[3][jj]);
-                        logit[4 * kq + jj] = pick(m1, t0, t1);
-                    }
-                }
-                float mx = -INFINITY;
-#pragma unroll
-                for (int m = 0; m < MOT_MAX_EXPERTS; ++m) {
-                    if (m < E) {
-                        if (bru) logit[m] += bf16_to_f32(bru[m]);
-                        mx = fmaxf(mx, logit[m]);
-                    }
-                }
-                float gate_all[MOT_MAX_EXPERTS];
-                float den = 0.f;
-#pragma unroll
-                for (int m = 0; m < MOT_MAX_EXPERTS; ++m) {
-                    gate_all[m] = m < E ? __expf(logit[m] - mx) : 0.f;
-                    den += gate_all[m];
-                }
-                const float inv = 1.0f / den;
-#pragma unroll
-                for (int m = 0; m < MOT_MAX_EXPERTS; ++m) gate_all[m] *= inv;
-                topk_renormalise(gate_all, E, p.top_k);
-                if (q4 == 0) {
-#pragma unroll
-                    for (int m = 0; m < MOT_MAX_EXPERTS; ++m)
-                        if (m < E) Gw[m * 32 + th * 16 + l16] = gate_all[m];
-                }
-            }
-        }
-        __syncthreads();                                     // barrier B
-
-        const float* Gw = Gs + w * (MOT_MAX_EXPERTS * 32);
-        // layer-1 biases of the two staged rows this lane's A operand covers
-        // (rows l16 and 16 + l16), in the low half of lane group 0, else zero
-        const int prow0 = w1_perm(l16), prow1 = w1_perm(16 + l16);
-        const uint32_t grp0 = q4 == 0 ? 0xFFFFFFFFu : 0u;
-        const uint32_t bsel = b1_mask & grp0;
-        // raw loads, one chunk ahead; the masks are applied only at the use in
-        // the next iteration, so nothing waits on these loads mid-iteration
-        auto load_b1 = [&](int c, uint32_t* bv) {
-            typedef const __attribute__((address_space(1))) uint16_t* gu16;
-            bv[0] = (uint32_t)(*(gu16)(b1u + c * 32 + prow0));
-            bv[1] = (uint32_t)(*(gu16)(b1u + c * 32 + prow1));
-        };
-        // "ones" B operand: k = 0 is 1.0 for every token column, all else 0
-        const u32x4 ones = {0x3F80u & grp0, 0u, 0u, 0u};
-        // W1 operand of (k-step s, row half hh) sits at W1c[abase[s & 3] +
-        // hh*16*CPR1 + 16*(s >> 2)]: the swizzled chunk (4s + q4) ^ l16 splits
-        // into a per-lane part and compile-time offsets
-        int abase[4];
-#pragma unroll
-        for (int b = 0; b < 4; ++b) abase[b] = l16 * C::CPR1 + 4 * (b ^ (l16 >> 2)) + (q4 ^ (l16 & 3));
-        // One iteration in two phases.  Phase A: GELU of the first NEA of the
-        // lane's 16 elements of chunk c-1, vector work only, while the layer-2
-        // wave on this SIMD runs its MFMAs.  Phase B: a slot schedule of
-        // 16x16x32 MFMAs (four bias MFMAs S[row][t] = b1[row] * 1, then KS2
-        // k-steps x 2 row halves x 2 token halves, all on independent
-        // accumulators) with the three-stage GELU of the other elements spread
-        // over the slots (stage s of element e in slot g0(e) + s*GD); W1
-        // operand reads run LOOK slots ahead.
-        constexpr int NEA = MOT_FUSED_PHASE_A;
-        auto l1_iter = [&](auto l1c, auto gc, int c, int m, const uint32_t* bv,
-                           const f32x4 (&sp)[2][2], uint32_t* bnext, int c_next,
-                           f32x4 (&s)[2][2]) {
-            constexpr bool do_l1 = decltype(l1c)::value, do_gelu = decltype(gc)::value;
-            constexpr int NM = 4 + 4 * KS2, LOOK = 4, GD = 3, NEB = 16 - NEA;
-            const u32x4* W1c = W1s + (c & 1) * C::W1_CH;
-            u32x4* Hw = Hs + ((c - 1) & 1) * C::H_CH + w * 128;
-            const float hg0 = 0.5f * Gw[m * 32 + l16], hg1 = 0.5f * Gw[m * 32 + 16 + l16];
-            if constexpr (do_l1) load_b1(c_next, bnext);
-            u32x4 a1[KS2][2];
-            float h[2][2][4], gx[16], gt[16], gx2[16], gq[16], ge[16];
-            // A operand of (k-step s, row half hh), first used in slot 4 + 4s + 2hh
-            auto read_a = [&](auto kc) {
-                constexpr int k = decltype(kc)::value;
-                if constexpr (k >= 4 && k < NM && ((k - 4) % 2) == 0) {
-                    constexpr int s = (k - 4) / 4, hh = ((k - 4) / 2) % 2;
-                    a1[s][hh] = W1c[abase[s & 3] + hh * 16 * C::CPR1 + 16 * (s >> 2)];
-                }
-            };
-            auto gelu_elem = [&](auto ec, auto stc) {
-                constexpr int e = decltype(ec)::value, st = decltype(stc)::value;
-                constexpr int hh = e / 8, th = (e / 4) % 2, jj = e % 4;
-                if constexpr (ACT == MOT_ACT_GELU) {
-                    if constexpr (st == 0) {
-                        gx[e] = sp[hh][th][jj];
-                        gelu_stage1(gx[e], gt[e], gx2[e]);
-                    } else if constexpr (st == 1) {
-                        gelu_stage2(gt[e], gx2[e], gq[e], ge[e]);
-                    } else {
-                        h[hh][th][jj] = gelu_stage3(gx[e], gt[e], gq[e], ge[e], th ? hg1 : hg0);
-                    }
-                } else if constexpr (st == 0) {
-                    h[hh][th][jj] = 2.0f * (th ? hg1 : hg0) * sp[hh][th][jj];
-                }
-            };
-            const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
-            if constexpr (do_l1) static_for<0, LOOK>([&](auto kc) { read_a(kc); });
-            if constexpr (do_gelu) {
-                static_for<0, 3>([&](auto stc) {
-                    static_for<0, NEA>([&](auto ec) { gelu_elem(ec, stc); });
-                });
-            }
-            __builtin_amdgcn_sched_barrier(0);
-            static_for<0, NM>([&](auto kc) {
-                constexpr int k = decltype(kc)::value;
-                if constexpr (do_l1) {
-                    read_a(std::integral_constant<int, k + LOOK>{});
-                    if constexpr (k < 4) {
-                        constexpr int hh = k / 2, th = k % 2;
-                        const u32x4 ba = {bv[hh] & bsel, 0u, 0u, 0u};
-                        s[hh][th] = mfma_16x16x32(ba, ones, zero4);
-                    } else {
-                        constexpr int st = (k - 4) / 4, hh = ((k - 4) / 2) % 2, th = (k - 4) % 2;
-                        s[hh][th] = mfma_16x16x32(a1[st][hh], zf[th][st], s[hh][th]);
-                    }
-                }
-                if constexpr (do_gelu && NEB > 0) {
-                    static_for<0, NEB>([&](auto ec) {
-                        constexpr int eb = decltype(ec)::value, e = NEA + eb;
-                        constexpr int hh = e / 8, th = (e / 4) % 2, jj = e % 4;
-                        constexpr int g0 = NEB > 1 ? (eb * (NM - 2 * GD - 1)) / (NEB - 1) : 0;
-                        if constexpr (ACT == MOT_ACT_GELU) {
-                            if constexpr (k == g0) {
-                                float v = sp[hh][th][jj];
-                                asm volatile("" : "+v"(v));
-                                gx[e] = v;
-                                gelu_stage1(v, gt[e], gx2[e]);
-                                asm volatile("" : "+v"(gt[e]), "+v"(gx2[e]));
-                            } else if constexpr (k == g0 + GD) {
-                                gelu_stage2(gt[e], gx2[e], gq[e], ge[e]);
-                                asm volatile("" : "+v"(gq[e]), "+v"(ge[e]));
-                            } else if constexpr (k == g0 + 2 * GD) {
-                                h[hh][th][jj] = gelu_stage3(gx[e], gt[e], gq[e], ge[e], th ? hg1 : hg0);
-                            }
-                        } else if constexpr (k == g0) {
-                            float v = sp[hh][th][jj];
-                            asm volatile("" : "+v"(v));
-                            h[hh][th][jj] = 2.0f * (th ? hg1 : hg0) * v;
-                        }
-                    });
-                }
-                __builtin_amdgcn_sched_barrier(0);
-            });
-            if constexpr (do_gelu) {
-                // token th*16 + l16: hidden 8*q4 .. 8*q4+3 from row half 0 and
-                // 8*q4+4 .. 8*q4+7 from row half 1: one 16-byte fragment unit
-#pragma unroll
-                for (int th = 0; th < 2; ++th) {
-                    u32x4 v;
-                    v[0] = pack_bf16x2(h[0][th][0], h[0][th][1]);
-                    v[1] = pack_bf16x2(h[0][th][2], h[0][th][3]);
-                    v[2] = pack_bf16x2(h[1][th][0], h[1][th][1]);
-                    v[3] = pack_bf16x2(h[1][th][2], h[1][th][3]);
-                    Hw[(q4 >> 1) * 64 + (q4 & 1) * 32 + th * 16 + l16] = v;
-                }
-            }
-        };
-
-        int m1 = 0, kk1 = 0;
-        uint32_t bcur[2], bnext[2] = {0u, 0u};
-        load_b1(0, bcur);
-        f32x4 s_prev[2][2], s_new[2][2];
-        auto advance = [&]() {          // (m1, kk1) -> the next chunk
-            kk1 += 32;
-            const bool wrap = kk1 == hidden;
-            kk1 = wrap ? 0 : kk1;
-            m1 = wrap ? m1 + 1 : m1;
-        };
-        auto rotate = [&]() {
-#pragma unroll
-            for (int a = 0; a < 2; ++a)
-#pragma unroll
-                for (int b = 0; b < 2; ++b) s_prev[a][b] = s_new[a][b];
-            bcur[0] = bnext[0]; bcur[1] = bnext[1];
-        };
-        const std::integral_constant<bool, true> yes{};
-        const std::integral_constant<bool, false> no{};
-        // c = 0: layer 1 only; 1 .. nch-1: layer 1 and GELU; nch: GELU only;
-        // nch+1: barrier only (layer 2 of the last chunk runs on other waves)
-        sync_stage();
-        l1_iter(yes, no, 0, m1, bcur, s_prev, bnext, 1, s_new);
-        rotate();
-        for (int c = 1; c < nch; ++c) {
-            sync_stage();
-            l1_iter(yes, yes, c, m1, bcur, s_prev, bnext, c + 1 < nch ? c + 1 : nch - 1, s_new);
-            rotate();
-            advance();
-        }
-        sync_stage();
-        l1_iter(no, yes, nch, m1, bcur, s_prev, bnext, nch - 1, s_new);
-        sync_stage();
-    } else if (is_l2) {
-        // ---------------------------------------------------------- layer 2
-        uint32_t ow1[NV1];
-#pragma unroll
-        for (int v = 0; v < NV1; ++v) ow1[v] = w1_lane(v);
-#pragma unroll
-        for (int r = 0; r < W1_RL; ++r) load_w1_round(0, 0, r, ow1[r % NV1]);
-        __syncthreads();                                     // barrier A
-        __syncthreads();                                     // barrier B
-        // accumulators seeded with sum_m g_m b2_m[o] on MFMA: A = gates of a
-        // token block (k = translator), B = b2 (k = translator); gates split
-        // into bf16 high + residual parts keep ~16 mantissa bits.
-        // acc[tb][nb]: column o = q2*OUTW + nb*32 + l32, rows = tokens
-        // tb*32 + 8*ii + 4*g + jj (element 4*ii + jj).
-        f32x16 acc[TB][C::NBW];
-#pragma unroll
-        for (int tb = 0; tb < TB; ++tb)
-#pragma unroll
-            for (int nb = 0; nb < C::NBW; ++nb)
-#pragma unroll
-                for (int e = 0; e < 16; ++e) acc[tb][nb][e] = 0.f;
-        if (b2u) {
-            u32x4 bv[C::NBW];
-#pragma unroll
-            for (int nb = 0; nb < C::NBW; ++nb) {
-                const int o = q2 * C::OUTW + nb * 32 + l32;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int m0 = 8 * g + 2 * q;
-                    const uint32_t v0 = m0 < E ? b2u[(size_t)m0 * D_OUT + o] : 0u;
-                    const uint32_t v1 = m0 + 1 < E ? b2u[(size_t)(m0 + 1) * D_OUT + o] : 0u;
-                    bv[nb][q] = v0 | (v1 << 16);
-                }
-            }
-#pragma unroll
-            for (int tb = 0; tb < TB; ++tb) {
-                const float* Gt = Gs + tb * (MOT_MAX_EXPERTS * 32);
-                u32x4 ghi, glo;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int m0 = 8 * g + 2 * q;
-                    const float g0 = m0 < E ? Gt[m0 * 32 + l32] : 0.f;
-                    const float g1 = m0 + 1 < E ? Gt[(m0 + 1) * 32 + l32] : 0.f;
-                    const uint32_t hi = pack_bf16x2(g0, g1);
-                    ghi[q] = hi;
-                    glo[q] = pack_bf16x2(g0 - bf16_lo(hi), g1 - bf16_hi(hi));
-                }
-#pragma unroll
-                for (int nb = 0; nb < C::NBW; ++nb) {
-                    acc[tb][nb] = mfma_32x32x16(ghi, bv[nb], acc[tb][nb]);
-                    acc[tb][nb] = mfma_32x32x16(glo, bv[nb], acc[tb][nb]);
-                }
-            }
-        }
-
-        // One iteration as a slot schedule over this wave's MFMAs, ordered
-        // (k-slice, output block, token block) so few operands are live; H and
-        // W2 operand reads run LOOK slots ahead; when the layer-2 waves are the
-        // loading waves, their weight loads are spread over the slots.
-        auto l2_iter = [&](auto l2c, auto w1c, auto w2c, int c, int c_w1, int m_w2, int kk_w2, int st_w2) {
-            constexpr bool do_l2 = decltype(l2c)::value, do_w1 = decltype(w1c)::value,
-                           do_w2 = decltype(w2c)::value;
-            constexpr int NM = 2 * TB * C::NBW, LOOK = 3;
-            constexpr int NV = W1_RL + W2_RL;
-            const u32x4* Hc = Hs + (c & 1) * C::H_CH;          // chunk c-2 shares c's parity
-            const u32x4* W2c = W2s + ((c + C::NW2 - 2) % C::NW2) * C::W2_CH;
-            u32x4 hA[2][TB], bW[2][C::NBW];
-            auto issue_reads = [&](auto kc) {
-                constexpr int k = decltype(kc)::value;
-                if constexpr (k < NM) {
-                    constexpr int ks = k / (TB * C::NBW), nb = (k / TB) % C::NBW, tb = k % TB;
-                    if constexpr (nb == 0) hA[ks][tb] = Hc[tb * 128 + ks * 64 + g * 32 + l32];
-                    if constexpr (tb == 0) {
-                        const int o = q2 * C::OUTW + nb * 32 + l32;
-                        bW[ks][nb] = W2c[o * 4 + ((2 * ks + g) ^ ((o >> 2) & 3))];
-                    }
-                }
-            };
-            if constexpr (do_l2) static_for<0, LOOK>([&](auto kc) { issue_reads(kc); });
-            static_for<0, NM>([&](auto kc) {
-                constexpr int k = decltype(kc)::value;
-                if constexpr (NV > 0) {
-                    static_for<0, NV>([&](auto rc) {
-                        constexpr int r = decltype(rc)::value;
-                        if constexpr ((r * NM) / NV == k) {
-                            if constexpr (r < W1_RL) {
-                                if constexpr (do_w1) load_w1_round(c_w1, (c + 1) & 1, r, ow1[r % NV1]);
-                            } else {
-                                if constexpr (do_w2) load_w2_round(m_w2, kk_w2, st_w2, r - W1_RL);
-                            }
-                        }
-                    });
-                }
-                if constexpr (do_l2) {
-                    issue_reads(std::integral_constant<int, k + LOOK>{});
-                    constexpr int ks = k / (TB * C::NBW), nb = (k / TB) % C::NBW, tb = k % TB;
-                    acc[tb][nb] = mfma_32x32x16(hA[ks][tb], bW[ks][nb], acc[tb][nb]);
-                }
-                __builtin_amdgcn_sched_barrier(0);
-            });
-        };
-
-        // (m1, kk1): translator and column offset of W2 chunk kw, the one
-        // fetched in iteration c: kw = c with three W2 stages, else c - 1
-        int m1 = 0, kk1 = 0;
-        const std::integral_constant<bool, true> T{};
-        const std::integral_constant<bool, false> F{};
-        auto advance = [&]() {
-            kk1 += 32;
-            const bool wrap = kk1 == hidden;
-            kk1 = wrap ? 0 : kk1;
-            m1 = wrap ? m1 + 1 : m1;
-        };
-        // Iteration c runs layer 2 of chunk c-2 (c >= 2), fetches W1 of chunk
-        // c+1 (c+1 < nch) and W2 of chunk kw (0 <= kw < nch).  The pipeline
-        // fill and drain iterations are peeled with their stage flags fixed at
-        // compile time (nch >= 2); the steady state runs every stage.
-        constexpr bool W2_AT_C = C::NW2 == 3;   // kw = c, else kw = c - 1
-        const std::integral_constant<bool, W2_AT_C> W2_FIRST{};
-        const std::integral_constant<bool, !W2_AT_C> W2_LAST{};
-        auto w2_stage = [&](int c) { return (c - (W2_AT_C ? 0 : 1) + C::NW2) % C::NW2; };
-        sync_stage();                                                   // c = 0
-        l2_iter(F, T, W2_FIRST, 0, 1, m1, kk1, w2_stage(0));
-        if (W2_AT_C) advance();
-        sync_stage();                                                   // c = 1
-        if (nch > 2) l2_iter(F, T, T, 1, 2, m1, kk1, w2_stage(1));
-        else l2_iter(F, F, T, 1, 2, m1, kk1, w2_stage(1));
-        advance();
-        for (int c = 2; c + 1 < nch; ++c) {                             // steady state
-            sync_stage();
-            l2_iter(T, T, T, c, c + 1, m1, kk1, w2_stage(c));
-            advance();
-        }
-        if (nch >= 3) {                                                 // c = nch - 1
-            sync_stage();
-            l2_iter(T, F, T, nch - 1, nch, m1, kk1, w2_stage(nch - 1));
-            advance();
-        }
-        sync_stage();                                                   // c = nch
-        l2_iter(T, F, W2_LAST, nch, nch + 1, m1, kk1, w2_stage(nch));
-        sync_stage();                                                   // c = nch + 1
-        l2_iter(T, F, F, nch + 1, nch + 2, m1, kk1, w2_stage(nch + 1));
-
-        // epilogue: bf16 round and store in the target layout
-        {
-        uint16_t* dst = reinterpret_cast<uint16_t*>(p.dst[x]) + (size_t)j * p.n_tok * D_OUT;
-#pragma unroll
-        for (int tb = 0; tb < TB; ++tb) {
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int tok = tok0 + tb * 32 + 8 * (e >> 2) + 4 * g + (e & 3);
-                if (tok >= p.n_tok) continue;
-                const int b = tok / p.T, t = tok % p.T;
-#pragma unroll
-                for (int nb = 0; nb < C::NBW; ++nb) {
-                    const int o = q2 * C::OUTW + nb * 32 + l32;
-                    size_t off;
-                    if (p.dst_layout == MOT_LAYOUT_BTHD) {
-                        off = (size_t)tok * D_OUT + o;
-                    } else {
-                        const int hh = o / p.D_tgt, dd = o % p.D_tgt;
-                        off = (((size_t)b * p.H_tgt + hh) * p.T + t) * p.D_tgt + dd;
-                    }
-                    dst[off] = (uint16_t)(pack_bf16x2(acc[tb][nb][e], 0.f) & 0xFFFFu);
-                }
-            }
-        }
-    }
-    } else {
-        // wave 3 when TB = 3: no token block; it helps stage the router
-        // weights and joins every barrier
-        stage_router_weights();
-        __syncthreads();
-        __syncthreads();
-        for (int c = 0; c <= nch + 1; ++c) sync_stage();
-    }
-}
-
-template <int D_IN, int D_OUT>
-hipError_t launch_t(const Problem& p, const UnitTab& ut, hipStream_t stream) {
-    using C = Cfg<D_IN, D_OUT>;
-    dim3 grid((p.n_tok + C::BM - 1) / C::BM, ut.n);
-    if (p.act == MOT_ACT_GELU)
-        hipLaunchKernelGGL((k_bf16_fused<D_IN, D_OUT, MOT_ACT_GELU>), grid, dim3(512), 0, stream, p, ut);
-    else
-        hipLaunchKernelGGL((k_bf16_fused<D_IN, D_OUT, MOT_ACT_IDENTITY>), grid, dim3(512), 0, stream, p, ut);
-    return hipGetLastError();
-}
-
-template <int D_IN>
-hipError_t launch_din(const Problem& p, const UnitTab& ut, hipStream_t stream) {
-    switch (p.d_out) {
-        case 128: return launch_t<D_IN, 128>(p, ut, stream);
-        case 256: return launch_t<D_IN, 256>(p, ut, stream);
-        case 512: return launch_t<D_IN, 512>(p, ut, stream);
+hipError_t launch_shape(const Problem& p, const UnitTab& ut, bool routed, hipStream_t stream) {
+    if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
+    const int key = p.d_in * 1000 + p.d_out;
+    switch (key) {
+        case 128128: return launch_fused_128_128(p, ut, routed, stream);
+        case 128256: return launch_fused_128_256(p, ut, routed, stream);
+        case 128512: return launch_fused_128_512(p, ut, routed, stream);
+        case 256128: return launch_fused_256_128(p, ut, routed, stream);
+        case 256256: return launch_fused_256_256(p, ut, routed, stream);
+        case 256512: return launch_fused_256_512(p, ut, routed, stream);
+        case 512128: return launch_fused_512_128(p, ut, routed, stream);
+        case 512256: return launch_fused_512_256(p, ut, routed, stream);
+        case 512512: return launch_fused_512_512(p, ut, routed, stream);
         default: return hipErrorNotSupported;
     }
 }
@@ -645,14 +38,14 @@ bool fused_supported(const Problem& p) {
     return din && dout && p.hidden % 32 == 0 && p.E * p.hidden >= 64 && p.E <= MOT_MAX_EXPERTS;
 }
 
+int fused_tile_rows(const Problem& p) { return p.d_out == 512 ? Cfg<128, 512>::BM : Cfg<128, 128>::BM; }
+
 hipError_t launch_bf16_fused(const Problem& p, const UnitTab& ut, hipStream_t stream) {
-    if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
-    switch (p.d_in) {
-        case 128: return launch_din<128>(p, ut, stream);
-        case 256: return launch_din<256>(p, ut, stream);
-        case 512: return launch_din<512>(p, ut, stream);
-        default: return hipErrorNotSupported;
-    }
+    return launch_shape(p, ut, false, stream);
+}
+
+hipError_t launch_bf16_fused_routed(const Problem& p, const UnitTab& ut, hipStream_t stream) {
+    return launch_shape(p, ut, true, stream);
 }
 
 }  // namespace mot

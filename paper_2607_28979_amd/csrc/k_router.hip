@@ -47,7 +47,9 @@ struct Vec<false> {  // 4 fp32 per 16-byte chunk
     }
 };
 
-template <bool BF16>
+// LISTS = false: dense gate rows p.gates[gslot][token][E] (zeros outside the
+// Top-K set); LISTS = true: the Top-K lists p.rt.sel / p.rt.gk of the routed path.
+template <bool BF16, bool LISTS>
 __global__ __launch_bounds__(256) void k_router(Problem p, UnitTab ut) {
     using V = Vec<BF16>;
     const uint32_t code = ut.code[blockIdx.y];
@@ -120,6 +122,11 @@ __global__ __launch_bounds__(256) void k_router(Problem p, UnitTab ut) {
     const float inv = 1.0f / den;
 #pragma unroll
     for (int m = 0; m < MOT_MAX_EXPERTS; ++m) acc[m] = m < E ? acc[m] * inv : 0.f;
+    if constexpr (LISTS) {
+        const size_t base = ((size_t)gs * p.n_tok + tok) * p.top_k;
+        topk_list(acc, E, p.top_k, p.rt.sel + base, p.rt.gk + base);
+        return;
+    }
     topk_renormalise(acc, E, p.top_k);
     float* g = p.gates + ((size_t)gs * p.n_tok_pad + tok) * E;
 #pragma unroll
@@ -133,9 +140,16 @@ hipError_t launch_router(const Problem& p, const UnitTab& ut, bool bf16, hipStre
     if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
     dim3 grid((p.n_tok + kTokPerBlock - 1) / kTokPerBlock, ut.n);
     if (bf16)
-        hipLaunchKernelGGL(k_router<true>, grid, dim3(256), 0, stream, p, ut);
+        hipLaunchKernelGGL((k_router<true, false>), grid, dim3(256), 0, stream, p, ut);
     else
-        hipLaunchKernelGGL(k_router<false>, grid, dim3(256), 0, stream, p, ut);
+        hipLaunchKernelGGL((k_router<false, false>), grid, dim3(256), 0, stream, p, ut);
+    return hipGetLastError();
+}
+
+hipError_t launch_router_lists(const Problem& p, const UnitTab& ut, hipStream_t stream) {
+    if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
+    dim3 grid((p.n_tok + kTokPerBlock - 1) / kTokPerBlock, ut.n);
+    hipLaunchKernelGGL((k_router<true, true>), grid, dim3(256), 0, stream, p, ut);
     return hipGetLastError();
 }
 

@@ -34,10 +34,12 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 struct Plan {
     bool bf16 = false;
     bool fused = false;
+    bool routed = false;       // Top-K sparse path (fused kernel over translator tiles)
     int n_units = 0;
     int32_t n_tok = 0, n_tok_pad = 0;
-    size_t gates_bytes = 0;    // all units
-    size_t hid_unit_bytes = 0; // one unit's hidden buffer
+    size_t fixed_bytes = 0;    // workspace for all units of the call
+    size_t unit_bytes = 0;     // workspace per unit of a launch group
+    int32_t max_tiles = 0, tile_rows = 0;
     uint32_t codes[kMaxUnits];
 };
 
@@ -68,10 +70,11 @@ mot_status check_shapes(const mot_shapes* s) {
         return fail(MOT_ERR_BAD_SHAPE, "layouts must be MOT_LAYOUT_BTHD or MOT_LAYOUT_BHTD");
     if (s->act != MOT_ACT_GELU && s->act != MOT_ACT_IDENTITY)
         return fail(MOT_ERR_BAD_SHAPE, "act=%d is not MOT_ACT_GELU or MOT_ACT_IDENTITY", s->act);
-    if (s->algo != MOT_ALGO_AUTO && s->algo != MOT_ALGO_UNFUSED && s->algo != MOT_ALGO_FUSED)
+    if (s->algo != MOT_ALGO_AUTO && s->algo != MOT_ALGO_UNFUSED && s->algo != MOT_ALGO_FUSED &&
+        s->algo != MOT_ALGO_ROUTED)
         return fail(MOT_ERR_BAD_SHAPE, "algo=%d is not a mot_algo value", s->algo);
     const int d_in = s->H_src * s->D_src, d_out = s->H_tgt * s->D_tgt;
-    if (s->algo == MOT_ALGO_FUSED) {
+    if (s->algo == MOT_ALGO_FUSED || s->algo == MOT_ALGO_ROUTED) {
         Problem p = base_problem(s);
         if (s->dtype != MOT_BF16 || !fused_supported(p))
             return fail(MOT_ERR_UNSUPPORTED,
@@ -109,6 +112,7 @@ void make_plan(const mot_shapes* s, const int32_t* layer_map, Plan* pl) {
     Problem p = base_problem(s);
     pl->bf16 = s->dtype == MOT_BF16;
     pl->fused = pl->bf16 && s->algo != MOT_ALGO_UNFUSED && fused_supported(p);
+    pl->routed = pl->fused && (s->algo == MOT_ALGO_ROUTED || (s->algo == MOT_ALGO_AUTO && s->top_k < s->E));
     pl->n_tok = p.n_tok;
     pl->n_tok_pad = p.n_tok_pad;
     int n = 0;
@@ -121,27 +125,51 @@ void make_plan(const mot_shapes* s, const int32_t* layer_map, Plan* pl) {
         }
     }
     pl->n_units = n;
-    if (pl->fused) {
-        pl->gates_bytes = 0;
-        pl->hid_unit_bytes = 0;
-    } else {
-        pl->gates_bytes = round_up((size_t)n * p.n_tok_pad * p.E * sizeof(float), kAlign);
-        pl->hid_unit_bytes =
-            round_up((size_t)p.n_tok_pad * p.E * p.hidden * (pl->bf16 ? 2 : 4), kAlign);
+    pl->fixed_bytes = 0;
+    pl->unit_bytes = 0;
+    pl->max_tiles = pl->tile_rows = 0;
+    if (pl->routed) {
+        const size_t nk = (size_t)p.n_tok * p.top_k;
+        pl->tile_rows = fused_tile_rows(p);
+        pl->max_tiles = (int32_t)((nk + pl->tile_rows - 1) / pl->tile_rows) + p.E;
+        const size_t per = round_up(nk * 4, kAlign);   // one int32 / fp32 per assignment
+        pl->fixed_bytes = (size_t)n * (5 * per + round_up((size_t)pl->max_tiles * 16, kAlign)) +
+                          round_up((size_t)n * 4, kAlign);
+        if (p.top_k > 1) pl->unit_bytes = round_up(nk * p.d_out * sizeof(float), kAlign);
+    } else if (!pl->fused) {
+        pl->fixed_bytes = round_up((size_t)n * p.n_tok_pad * p.E * sizeof(float), kAlign);
+        pl->unit_bytes = round_up((size_t)p.n_tok_pad * p.E * p.hidden * (pl->bf16 ? 2 : 4), kAlign);
     }
 }
 
 int default_group(const Plan& pl) {
-    if (pl.hid_unit_bytes == 0) return pl.n_units;
-    size_t g = kDefaultHiddenCap / pl.hid_unit_bytes;
+    if (pl.unit_bytes == 0) return pl.n_units;
+    size_t g = kDefaultHiddenCap / pl.unit_bytes;
     if (g < 1) g = 1;
     if (g > (size_t)pl.n_units) g = pl.n_units;
     return (int)g;
 }
 
 size_t plan_bytes(const Plan& pl, int group) {
-    if (pl.fused || pl.n_units == 0) return 0;
-    return pl.gates_bytes + (size_t)group * pl.hid_unit_bytes;
+    if (pl.n_units == 0) return 0;
+    return pl.fixed_bytes + (size_t)group * pl.unit_bytes;
+}
+
+// Carve the routed path's buffers out of the workspace (layout of make_plan).
+void carve_routing(const Plan& pl, const Problem& p, void* ws, Routing* rt) {
+    const size_t nk = (size_t)p.n_tok * p.top_k, per = round_up(nk * 4, kAlign);
+    const size_t U = (size_t)pl.n_units;
+    char* c = reinterpret_cast<char*>(ws);
+    rt->sel = reinterpret_cast<int32_t*>(c); c += U * per;
+    rt->gk = reinterpret_cast<float*>(c); c += U * per;
+    rt->list = reinterpret_cast<int32_t*>(c); c += U * per;
+    rt->agate = reinterpret_cast<float*>(c); c += U * per;
+    rt->slot = p.top_k > 1 ? reinterpret_cast<int32_t*>(c) : nullptr; c += U * per;
+    rt->tiles = reinterpret_cast<int4*>(c); c += U * round_up((size_t)pl.max_tiles * 16, kAlign);
+    rt->ntiles = reinterpret_cast<int32_t*>(c); c += round_up(U * 4, kAlign);
+    rt->part = p.top_k > 1 ? reinterpret_cast<float*>(c) : nullptr;
+    rt->max_tiles = pl.max_tiles;
+    rt->tile_rows = pl.tile_rows;
 }
 
 // Library-owned workspace, one per device, grown on demand.
@@ -265,8 +293,10 @@ mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* la
             if (s->workspace_bytes < need_min)
                 return fail(MOT_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes, need at least %zu",
                             s->workspace_bytes, need_min);
-            size_t g = (s->workspace_bytes - pl.gates_bytes) / pl.hid_unit_bytes;
-            group = (int)(g < (size_t)pl.n_units ? g : (size_t)pl.n_units);
+            if (pl.unit_bytes) {
+                size_t g = (s->workspace_bytes - pl.fixed_bytes) / pl.unit_bytes;
+                group = (int)(g < (size_t)pl.n_units ? g : (size_t)pl.n_units);
+            }
             ws = s->workspace;
             if (overlaps(ws, s->workspace_bytes, dst_k, dst_bytes) ||
                 overlaps(ws, s->workspace_bytes, dst_v, dst_bytes))
@@ -284,14 +314,28 @@ mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* la
     p.dst[0] = dst_k; p.dst[1] = dst_v;
     p.w1 = tw->w1; p.b1 = tw->b1; p.w2 = tw->w2; p.b2 = tw->b2;
     p.wr = rw->w; p.br = rw->b;
-    if (ws) {
+    if (ws && pl.routed) {
+        carve_routing(pl, p, ws, &p.rt);
+    } else if (ws) {
         p.gates = reinterpret_cast<float*>(ws);
-        p.hbuf = reinterpret_cast<char*>(ws) + pl.gates_bytes;
+        p.hbuf = reinterpret_cast<char*>(ws) + pl.fixed_bytes;
     }
 
     static thread_local UnitTab ut;
     hipError_t e = hipSuccess;
-    if (pl.fused) {
+    if (pl.routed) {
+        ut.n = pl.n_units;
+        memcpy(ut.code, pl.codes, sizeof(uint32_t) * pl.n_units);
+        e = launch_router_lists(p, ut, stream);
+        if (e == hipSuccess) e = launch_route_plan(p, ut, stream);
+        for (int u0 = 0; e == hipSuccess && u0 < pl.n_units; u0 += group) {
+            const int n = pl.n_units - u0 < group ? pl.n_units - u0 : group;
+            ut.n = n;
+            memcpy(ut.code, pl.codes + u0, sizeof(uint32_t) * n);
+            e = launch_bf16_fused_routed(p, ut, stream);
+            if (e == hipSuccess && p.top_k > 1) e = launch_routed_combine(p, ut, stream);
+        }
+    } else if (pl.fused) {
         ut.n = pl.n_units;
         memcpy(ut.code, pl.codes, sizeof(uint32_t) * pl.n_units);
         e = launch_bf16_fused(p, ut, stream);

@@ -70,6 +70,33 @@ __device__ __forceinline__ void topk_renormalise(float (&g)[EMAX], int E, int K)
     for (int m = 0; m < EMAX; ++m) g[m] = ((taken >> m) & 1u) ? g[m] * inv : 0.f;
 }
 
+// The same Top-K as topk_renormalise, emitted as a list: sel[k], gk[k] for
+// k < K in selection order (largest score first, ties to the lower index),
+// gates renormalised over the list.  K <= E.
+template <int EMAX>
+__device__ __forceinline__ void topk_list(const float (&g)[EMAX], int E, int K, int32_t* sel,
+                                          float* gk) {
+    uint32_t taken = 0;
+    float sum = 0.f;
+    for (int k = 0; k < K; ++k) {
+        int best = -1;
+        float bv = 0.f;
+#pragma unroll
+        for (int m = 0; m < EMAX; ++m) {
+            const bool cand = m < E && !((taken >> m) & 1u) && (best < 0 || g[m] > bv);
+            best = cand ? m : best;
+            bv = cand ? g[m] : bv;
+        }
+        if (best < 0) best = 0;   // not reached for finite scores
+        taken |= 1u << best;
+        sum += bv;
+        sel[k] = best;
+        gk[k] = bv;
+    }
+    const float inv = 1.0f / sum;
+    for (int k = 0; k < K; ++k) gk[k] *= inv;
+}
+
 // Exact-erf GELU, x * Phi(x), with the device erff.
 __device__ __forceinline__ float gelu_erf(float x) {
     return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));

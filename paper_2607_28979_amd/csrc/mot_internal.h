@@ -26,6 +26,22 @@ struct UnitTab {
     uint32_t code[kMaxUnits];
 };
 
+// Buffers of the routed (Top-K sparse) path, all in the workspace.  Arrays
+// marked [units] are indexed by the unit's gslot; part by the launch position
+// of the unit within its group.
+struct Routing {
+    int32_t* sel;       // [units][n_tok][top_k] selected translators, best first
+    float* gk;          // [units][n_tok][top_k] their renormalised gates
+    int32_t* list;      // [units][n_tok*top_k] token of each assignment, grouped by translator
+    float* agate;       // [units][n_tok*top_k] gate of each assignment
+    int32_t* slot;      // [units][n_tok][top_k] assignment index of (token, k)
+    int4* tiles;        // [units][max_tiles] {translator, first assignment, rows, 0}
+    int32_t* ntiles;    // [units]
+    float* part;        // [group][n_tok*top_k][d_out] fp32 per-assignment outputs (top_k > 1)
+    int32_t max_tiles;  // tiles per unit the launch grid covers
+    int32_t tile_rows;  // assignments per tile
+};
+
 // Problem description handed to every kernel by value.
 struct Problem {
     const void* src[2];   // source K, V: [L_src] x layout
@@ -41,6 +57,7 @@ struct Problem {
     int32_t src_layout, dst_layout, act;
     float* gates;         // workspace: [n_units_total][n_tok_pad][E] fp32
     void* hbuf;           // workspace: [group][n_tok_pad][E*hidden] (layout per path)
+    Routing rt;           // routed path only
 };
 
 // Kernel launchers (each enqueues on `stream`; return hipGetLastError()).
@@ -53,5 +70,14 @@ hipError_t launch_bf16_gemm2(const Problem& p, const UnitTab& ut, hipStream_t st
 // hipErrorNotSupported when the sizes have no fused instantiation.
 bool fused_supported(const Problem& p);
 hipError_t launch_bf16_fused(const Problem& p, const UnitTab& ut, hipStream_t stream);
+// Routed path: router -> per-token Top-K lists; per-unit counting sort of the
+// (token, translator) assignments into translator-contiguous lists and row
+// tiles; the fused kernel over tiles (one translator each); for top_k > 1, a
+// combine of the top_k per-assignment rows of every token.
+int fused_tile_rows(const Problem& p);
+hipError_t launch_router_lists(const Problem& p, const UnitTab& ut, hipStream_t stream);
+hipError_t launch_route_plan(const Problem& p, const UnitTab& ut, hipStream_t stream);
+hipError_t launch_bf16_fused_routed(const Problem& p, const UnitTab& ut, hipStream_t stream);
+hipError_t launch_routed_combine(const Problem& p, const UnitTab& ut, hipStream_t stream);
 
 }  // namespace mot

@@ -55,7 +55,7 @@ def _algos(w):
     if w.dtype == "f32":
         return [mb.ALGO_AUTO]
     if w.d_in in (128, 256, 512) and w.d_out in (128, 256, 512):
-        return [mb.ALGO_FUSED, mb.ALGO_UNFUSED]
+        return [mb.ALGO_FUSED, mb.ALGO_ROUTED, mb.ALGO_UNFUSED]
     return [mb.ALGO_UNFUSED]
 
 
@@ -196,6 +196,44 @@ def test_one_hot_and_uniform_gates(algo, oracle_built):
     rk, rv = _oracle_full(w, inp, lm)
     gk, gv = run_gpu(w, inp, lm, algo=algo)
     assert max_unit_error(gk, gv, rk, rv, w, lm) <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("k", [1, 2])
+def test_routed_skewed_routing(k, oracle_built):
+    """Routed path with every token sent to the same translators (router bias
+    +64 on translator 2, +32 on 5): one translator holds every assignment,
+    the others are empty; a ragged token count leaves a partial last tile."""
+    w = small_variant(WORKLOADS[3], L_src=2, L_tgt=2, B=1, T=230).with_(top_k=k)
+    inp = generate(w)
+    lm = _layer_map(w)
+    inp.br[:, :, 2] = 64.0
+    inp.br[:, :, 5] = 32.0
+    rk, rv = _oracle_full(w, inp, lm)
+    for algo in (mb.ALGO_ROUTED, mb.ALGO_FUSED):
+        gk, gv = run_gpu(w, inp, lm, algo=algo)
+        err = max_unit_error(gk, gv, rk, rv, w, lm)
+        print("case skewed top_k", k, "algo", algo, "max unit error %.3e" % err, flush=True)
+        assert err <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("k", [1, 3])
+def test_routed_deterministic_and_sub_batch(k):
+    """The routed path's counting sort and combine use no atomics: two runs
+    are bit-identical, and translating a prefix of the tokens gives the same
+    rows as the full run (each row's arithmetic does not depend on which
+    other rows share its tile)."""
+    w = small_variant(WORKLOADS[1], L_src=2, L_tgt=2, B=2, T=300).with_(top_k=k)
+    inp = generate(w)
+    lm = _layer_map(w)
+    a = run_gpu(w, inp, lm, algo=mb.ALGO_ROUTED)
+    b = run_gpu(w, inp, lm, algo=mb.ALGO_ROUTED)
+    assert all(np.array_equal(x, y) for x, y in zip(a, b))
+    ws = w.with_(B=1)
+    inps = generate(w)
+    inps.src_k = inps.src_k[:, :1].copy()
+    inps.src_v = inps.src_v[:, :1].copy()
+    c = run_gpu(ws, inps, lm, algo=mb.ALGO_ROUTED)
+    assert np.array_equal(a[0][:, :1], c[0]) and np.array_equal(a[1][:, :1], c[1])
 
 
 @pytest.mark.parametrize("algo", [mb.ALGO_FUSED, mb.ALGO_UNFUSED])
