@@ -124,8 +124,13 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
     int4 tile = make_int4(0, 0, 0, 0);
     if constexpr (ROUTED) {
         const int gs = unit_gslot(code);
-        if ((int)blockIdx.x >= p.rt.ntiles[gs]) return;
-        tile = p.rt.tiles[(size_t)gs * p.rt.max_tiles + blockIdx.x];
+        // Workgroups go to the 8 XCDs round-robin by linear id, and the tiles
+        // of one translator are consecutive: give each XCD a contiguous run
+        // of tiles (max_tiles is a multiple of 8), so the workgroups an XCD
+        // runs together share one translator's weights in its L2.
+        const int t = (int)(blockIdx.x % 8) * (p.rt.max_tiles / 8) + (int)(blockIdx.x / 8);
+        if (t >= p.rt.ntiles[gs]) return;
+        tile = p.rt.tiles[(size_t)gs * p.rt.max_tiles + t];
     }
     const int E = ROUTED ? 1 : p.E, hidden = p.hidden, EH = E * hidden;
     const size_t um = unit * p.E + (ROUTED ? tile.x : 0);   // first translator walked

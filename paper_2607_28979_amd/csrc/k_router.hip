@@ -6,7 +6,7 @@
 // Eight lanes share one token row: lane q reads 16-byte chunks q, q+8, ...
 // (coalesced 128-byte runs), accumulates E partial dot products in fp32, and
 // the eight partials are combined with cross-lane shuffles.  256 threads =
-// 32 tokens per workgroup; grid.y enumerates the units.
+// 32 tokens per pass, 8 passes per workgroup; grid.y enumerates the units.
 #include "mot_device.h"
 #include "mot_internal.h"
 #include "../../include/mot.h"
@@ -16,49 +16,77 @@ namespace mot {
 namespace {
 
 constexpr int kLanesPerTok = 8;
-constexpr int kTokPerBlock = 256 / kLanesPerTok;
+constexpr int kTokPerBlock = 256 / kLanesPerTok;   // tokens per pass of a workgroup
+constexpr int kGroups = 8;                          // passes per workgroup
 
 template <bool BF16>
 struct Vec;
 template <>
 struct Vec<true> {  // 8 bf16 per 16-byte chunk
     static constexpr int n = 8;
-    __device__ static void load(const void* base, size_t elem, float* out) {
-        u32x4 w = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(base) + elem);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            out[2 * q] = bf16_lo(w[q]);
-            out[2 * q + 1] = bf16_hi(w[q]);
-        }
-    }
     __device__ static float scalar(const void* base, size_t elem) {
         return bf16_to_f32(reinterpret_cast<const uint16_t*>(base)[elem]);
+    }
+    typedef u32x4 Raw;
+    __device__ static Raw raw(const void* base, size_t elem) {
+        return *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(base) + elem);
+    }
+    // acc + w . z over the 8 values, on packed bf16 dot products (exact
+    // products, fp32 sums)
+    __device__ static float dot2(uint32_t w, uint32_t z, float acc) {
+        return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), __builtin_bit_cast(bf16x2, z), acc,
+                                               false);
+    }
+    __device__ static float dot(Raw w, Raw z, float acc) {
+        acc = dot2(w.x, z.x, acc);
+        acc = dot2(w.y, z.y, acc);
+        acc = dot2(w.z, z.z, acc);
+        return dot2(w.w, z.w, acc);
     }
 };
 template <>
 struct Vec<false> {  // 4 fp32 per 16-byte chunk
     static constexpr int n = 4;
-    __device__ static void load(const void* base, size_t elem, float* out) {
-        f32x4 w = *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(base) + elem);
-        out[0] = w[0]; out[1] = w[1]; out[2] = w[2]; out[3] = w[3];
-    }
     __device__ static float scalar(const void* base, size_t elem) {
         return reinterpret_cast<const float*>(base)[elem];
+    }
+    typedef f32x4 Raw;
+    __device__ static Raw raw(const void* base, size_t elem) {
+        return *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(base) + elem);
+    }
+    __device__ static float dot(const Raw& w, const Raw& z, float acc) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc = fmaf(w[e], z[e], acc);
+        return acc;
     }
 };
 
 // LISTS = false: dense gate rows p.gates[gslot][token][E] (zeros outside the
 // Top-K set); LISTS = true: the Top-K lists p.rt.sel / p.rt.gk of the routed path.
-template <bool BF16, bool LISTS>
+// WLDS: the unit's router rows (E x d_in) are staged once in LDS (dynamic
+// shared memory, when they fit) instead of being re-read per token.
+template <bool BF16, bool LISTS, bool WLDS>
 __global__ __launch_bounds__(256) void k_router(Problem p, UnitTab ut) {
     using V = Vec<BF16>;
+    extern __shared__ u32x4 s_wr[];
     const uint32_t code = ut.code[blockIdx.y];
     const int j = unit_j(code), x = unit_x(code), i = unit_i(code), gs = unit_gslot(code);
-    const int tok = blockIdx.x * kTokPerBlock + threadIdx.x / kLanesPerTok;
     const int q = threadIdx.x % kLanesPerTok;
+    const void* wr = p.wr;
+    size_t wr_base = ((size_t)j * 2 + x) * p.E * p.d_in;
+    if constexpr (WLDS) {
+        const int n16 = p.E * p.d_in / V::n;   // 16-byte chunks
+        const u32x4* g = reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(p.wr) +
+                                                        wr_base * (BF16 ? 2 : 4));
+        for (int c = threadIdx.x; c < n16; c += 256) s_wr[c] = g[c];
+        __syncthreads();
+        wr = s_wr;
+        wr_base = 0;
+    }
+    for (int grp = 0; grp < kGroups; ++grp) {
+    const int tok = (blockIdx.x * kGroups + grp) * kTokPerBlock + threadIdx.x / kLanesPerTok;
     const int E = p.E, d_in = p.d_in;
     const size_t unit = (size_t)j * 2 + x;
-    const size_t wr_base = unit * E * d_in;
 
     float acc[MOT_MAX_EXPERTS];
 #pragma unroll
@@ -67,25 +95,30 @@ __global__ __launch_bounds__(256) void k_router(Problem p, UnitTab ut) {
     if (tok < p.n_tok) {
         const size_t layer = (size_t)i * p.n_tok * d_in;
         const int b = tok / p.T, t = tok % p.T;
-        for (int c0 = q * V::n; c0 < d_in; c0 += kLanesPerTok * V::n) {
-            size_t off;
-            if (p.src_layout == MOT_LAYOUT_BTHD) {
-                off = layer + (size_t)tok * d_in + c0;
-            } else {
-                const int hh = c0 / p.D_src, dd = c0 % p.D_src;
-                off = layer + (((size_t)b * p.H_src + hh) * p.T + t) * p.D_src + dd;
+        // four 16-byte source chunks in flight per lane before they are used
+        constexpr int kStep = kLanesPerTok * V::n;
+        for (int c0 = q * V::n; c0 < d_in; c0 += 4 * kStep) {
+            typename V::Raw zr[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int c = c0 + u * kStep;
+                const int cc = c < d_in ? c : c0;   // in range; unused when c >= d_in
+                size_t off;
+                if (p.src_layout == MOT_LAYOUT_BTHD) {
+                    off = layer + (size_t)tok * d_in + cc;
+                } else {
+                    const int hh = cc / p.D_src, dd = cc % p.D_src;
+                    off = layer + (((size_t)b * p.H_src + hh) * p.T + t) * p.D_src + dd;
+                }
+                zr[u] = V::raw(p.src[x], off);
             }
-            float z[V::n];
-            V::load(p.src[x], off, z);
 #pragma unroll
-            for (int m = 0; m < MOT_MAX_EXPERTS; ++m) {
-                if (m < E) {
-                    float w[V::n];
-                    V::load(p.wr, wr_base + (size_t)m * d_in + c0, w);
-                    float s = acc[m];
+            for (int u = 0; u < 4; ++u) {
+                const int c = c0 + u * kStep;
+                if (c < d_in) {
 #pragma unroll
-                    for (int e = 0; e < V::n; ++e) s = fmaf(w[e], z[e], s);
-                    acc[m] = s;
+                    for (int m = 0; m < MOT_MAX_EXPERTS; ++m)
+                        if (m < E) acc[m] = V::dot(V::raw(wr, wr_base + (size_t)m * d_in + c), zr[u], acc[m]);
                 }
             }
         }
@@ -102,7 +135,7 @@ __global__ __launch_bounds__(256) void k_router(Problem p, UnitTab ut) {
             acc[m] = v;
         }
     }
-    if (tok >= p.n_tok || q != 0) return;
+    if (tok >= p.n_tok || q != 0) continue;
     float mx = -INFINITY;
 #pragma unroll
     for (int m = 0; m < MOT_MAX_EXPERTS; ++m) {
@@ -125,32 +158,38 @@ __global__ __launch_bounds__(256) void k_router(Problem p, UnitTab ut) {
     if constexpr (LISTS) {
         const size_t base = ((size_t)gs * p.n_tok + tok) * p.top_k;
         topk_list(acc, E, p.top_k, p.rt.sel + base, p.rt.gk + base);
-        return;
+        continue;
     }
     topk_renormalise(acc, E, p.top_k);
     float* g = p.gates + ((size_t)gs * p.n_tok_pad + tok) * E;
 #pragma unroll
     for (int m = 0; m < MOT_MAX_EXPERTS; ++m)
         if (m < E) g[m] = acc[m];
+    }
+}
+
+constexpr size_t kWrLdsMax = 64 * 1024;   // router rows staged in LDS up to this size
+
+template <bool BF16, bool LISTS>
+hipError_t launch_k(const Problem& p, const UnitTab& ut, hipStream_t stream) {
+    if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
+    dim3 grid((p.n_tok + kTokPerBlock * kGroups - 1) / (kTokPerBlock * kGroups), ut.n);
+    const size_t wr_bytes = (size_t)p.E * p.d_in * (BF16 ? 2 : 4);
+    if (wr_bytes <= kWrLdsMax)
+        hipLaunchKernelGGL((k_router<BF16, LISTS, true>), grid, dim3(256), wr_bytes, stream, p, ut);
+    else
+        hipLaunchKernelGGL((k_router<BF16, LISTS, false>), grid, dim3(256), 0, stream, p, ut);
+    return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_router(const Problem& p, const UnitTab& ut, bool bf16, hipStream_t stream) {
-    if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
-    dim3 grid((p.n_tok + kTokPerBlock - 1) / kTokPerBlock, ut.n);
-    if (bf16)
-        hipLaunchKernelGGL((k_router<true, false>), grid, dim3(256), 0, stream, p, ut);
-    else
-        hipLaunchKernelGGL((k_router<false, false>), grid, dim3(256), 0, stream, p, ut);
-    return hipGetLastError();
+    return bf16 ? launch_k<true, false>(p, ut, stream) : launch_k<false, false>(p, ut, stream);
 }
 
 hipError_t launch_router_lists(const Problem& p, const UnitTab& ut, hipStream_t stream) {
-    if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
-    dim3 grid((p.n_tok + kTokPerBlock - 1) / kTokPerBlock, ut.n);
-    hipLaunchKernelGGL((k_router<true, true>), grid, dim3(256), 0, stream, p, ut);
-    return hipGetLastError();
+    return launch_k<true, true>(p, ut, stream);
 }
 
 }  // namespace mot

@@ -131,7 +131,7 @@ void make_plan(const mot_shapes* s, const int32_t* layer_map, Plan* pl) {
     if (pl->routed) {
         const size_t nk = (size_t)p.n_tok * p.top_k;
         pl->tile_rows = fused_tile_rows(p);
-        pl->max_tiles = (int32_t)((nk + pl->tile_rows - 1) / pl->tile_rows) + p.E;
+        pl->max_tiles = (int32_t)round_up((nk + pl->tile_rows - 1) / pl->tile_rows + p.E, 8);
         const size_t per = round_up(nk * 4, kAlign);   // one int32 / fp32 per assignment
         pl->fixed_bytes = (size_t)n * (5 * per + round_up((size_t)pl->max_tiles * 16, kAlign)) +
                           round_up((size_t)n * 4, kAlign);

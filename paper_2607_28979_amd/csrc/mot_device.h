@@ -72,29 +72,34 @@ __device__ __forceinline__ void topk_renormalise(float (&g)[EMAX], int E, int K)
 
 // The same Top-K as topk_renormalise, emitted as a list: sel[k], gk[k] for
 // k < K in selection order (largest score first, ties to the lower index),
-// gates renormalised over the list.  K <= E.
+// gates renormalised over the list.  K <= E.  The selection runs twice (sum,
+// then emit) so nothing is read back from the output arrays.
 template <int EMAX>
 __device__ __forceinline__ void topk_list(const float (&g)[EMAX], int E, int K, int32_t* sel,
                                           float* gk) {
-    uint32_t taken = 0;
-    float sum = 0.f;
-    for (int k = 0; k < K; ++k) {
-        int best = -1;
-        float bv = 0.f;
+    float inv = 0.f;
+    for (int pass = 0; pass < 2; ++pass) {
+        uint32_t taken = 0;
+        float sum = 0.f;
+        for (int k = 0; k < K; ++k) {
+            int best = -1;
+            float bv = 0.f;
 #pragma unroll
-        for (int m = 0; m < EMAX; ++m) {
-            const bool cand = m < E && !((taken >> m) & 1u) && (best < 0 || g[m] > bv);
-            best = cand ? m : best;
-            bv = cand ? g[m] : bv;
+            for (int m = 0; m < EMAX; ++m) {
+                const bool cand = m < E && !((taken >> m) & 1u) && (best < 0 || g[m] > bv);
+                best = cand ? m : best;
+                bv = cand ? g[m] : bv;
+            }
+            if (best < 0) best = 0;   // not reached for finite scores
+            taken |= 1u << best;
+            sum += bv;
+            if (pass == 1) {
+                sel[k] = best;
+                gk[k] = bv * inv;
+            }
         }
-        if (best < 0) best = 0;   // not reached for finite scores
-        taken |= 1u << best;
-        sum += bv;
-        sel[k] = best;
-        gk[k] = bv;
+        inv = 1.0f / sum;
     }
-    const float inv = 1.0f / sum;
-    for (int k = 0; k < K; ++k) gk[k] *= inv;
 }
 
 // Exact-erf GELU, x * Phi(x), with the device erff.
