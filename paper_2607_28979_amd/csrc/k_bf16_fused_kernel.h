@@ -14,7 +14,8 @@
 //     seeded with sum_m g_m b2_m; per chunk Y += H . W2_m[:, c]^T (32x32x16);
 //     they also issue every global -> LDS weight load (direct-to-LDS, no VGPR
 //     staging);
-//   * wave 3 when TB = 3: no block; joins the barriers.
+//   * wave 3 when TB = 3: no block; evaluates part of the layer-1 waves'
+//     GELU (fp32 values handed over through LDS).
 // Iteration c runs layer 1 of chunk c, the GELU of chunk c-1 and layer 2 of
 // chunk c-2, and fetches W1 of chunk c+1 and W2 of chunk c (three W2 stages)
 // or c-1 (two); one workgroup barrier per iteration.  W1's 32 rows are staged
@@ -39,7 +40,13 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 // Elements (of 16 per lane and chunk) whose GELU runs before the layer-1 MFMAs
 #ifndef MOT_FUSED_PHASE_A
-#define MOT_FUSED_PHASE_A 10
+#define MOT_FUSED_PHASE_A 6
+#endif
+// With TB = 3, wave 3 has no token block: it evaluates the GELU of this many
+// of each layer-1 lane's 16 elements (0, 4 or 8: row half 1 of token half 1,
+// or of both token halves), handed over through LDS in fp32.
+#ifndef MOT_FUSED_OFFLOAD
+#define MOT_FUSED_OFFLOAD 8
 #endif
 
 template <int D_IN, int D_OUT>
@@ -54,15 +61,21 @@ struct Cfg {
     static constexpr int W2_CH = D_OUT * 4;       // chunks per W2 stage (32 hidden = 4 chunks)
     static constexpr int H_CH = TB * 128;         // chunks per hidden stage (TB blocks x 32 tokens x 32)
     static constexpr int GS = TB * MOT_MAX_EXPERTS * 32;  // gate floats
+    static constexpr int NOFF = TB == 3 ? MOT_FUSED_OFFLOAD : 0;   // GELU elements on wave 3
+    static constexpr int X_CH = TB * (NOFF / 4) * 64;   // hand-over stage: f32x4 per lane
     // W2 stages: three (each chunk fetched two iterations before its use)
     // when they fit in the 160 KB of LDS, else two (one iteration ahead)
-    static constexpr int NW2 = (2 * W1_CH + 3 * W2_CH + 2 * H_CH + GS / 4) * 16 <= 160 * 1024 ? 3 : 2;
+    static constexpr int NW2 =
+        (2 * W1_CH + 3 * W2_CH + 2 * H_CH + GS / 4 + 2 * X_CH) * 16 <= 160 * 1024 ? 3 : 2;
     // LDS map in 16-byte units
     static constexpr int OFF_W1 = 0;
     static constexpr int OFF_W2 = OFF_W1 + 2 * W1_CH;
     static constexpr int OFF_H = OFF_W2 + NW2 * W2_CH;
     static constexpr int OFF_G = OFF_H + 2 * H_CH;
-    static constexpr int TOTAL = OFF_G + GS / 4;
+    static constexpr int OFF_X = OFF_G + GS / 4;
+    static constexpr int TOTAL = OFF_X + 2 * X_CH;
+    static_assert(NOFF == 0 || NOFF == 4 || NOFF == 8, "offloaded GELU elements");
+    static_assert(TOTAL * 16 <= 160 * 1024, "LDS");
     static_assert(W1_CH % 256 == 0 && W2_CH % 256 == 0 && NBW >= 1, "tile shape");
     static_assert(TB * NBW * 16 <= 192, "layer-2 accumulators must leave VGPR room");
 };
@@ -115,6 +128,7 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
     u32x4* W2s = smem + C::OFF_W2;
     u32x4* Hs = smem + C::OFF_H;
     float* Gs = reinterpret_cast<float*>(smem + C::OFF_G);
+    u32x4* Xs = smem + C::OFF_X;   // fp32 layer-1 results handed to wave 3
 
     const uint32_t code = ut.code[blockIdx.y];
     const int j = unit_j(code), x = unit_x(code), i = unit_i(code);
@@ -195,10 +209,21 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
             Rs[slot] = row < E ? *reinterpret_cast<const u32x4*>(Wru + (size_t)row * D_IN + cl * 8) : zero;
         }
     };
-    auto sync_stage = [&]() {
-        wait_vm_all();
-        __syncthreads();
+    // Pipeline barrier.  Each wave first waits for its own LDS traffic and for
+    // its global loads except the newest `keep` (LDS data produced by direct
+    // loads is written when the load completes), then all waves meet.  No
+    // fence: the waits above are all the ordering the pipeline needs, and a
+    // fence would drain every outstanding load.
+    auto sync_keep = [&](auto keepc) {
+        constexpr int keep = decltype(keepc)::value;
+        static_assert(keep >= 0 && keep < 64, "vmcnt range");
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" :: "n"(keep) : "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
     };
+    auto sync_stage = [&]() { sync_keep(std::integral_constant<int, 0>{}); };
 
     if (is_l1) {
         // ---------------------------------------------------------- layer 1
@@ -344,7 +369,8 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
                            const f32x4 (&sp)[2][2], uint32_t* bnext, int c_next,
                            f32x4 (&s)[2][2]) {
             constexpr bool do_l1 = decltype(l1c)::value, do_gelu = decltype(gc)::value;
-            constexpr int NM = 4 + 4 * KS2, LOOK = 4, GD = 3, NEB = 16 - NEA;
+            constexpr int NM = 4 + 4 * KS2, LOOK = 4, GD = 3, NEB = 16 - C::NOFF - NEA;
+            static_assert(NEB >= 0, "phase split");
             const u32x4* W1c = W1s + (c & 1) * C::W1_CH;
             u32x4* Hw = Hs + ((c - 1) & 1) * C::H_CH + w * 128;
             const float hg0 = 0.5f * Gw[m * 32 + l16], hg1 = 0.5f * Gw[m * 32 + 16 + l16];
@@ -426,15 +452,31 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
             if constexpr (do_gelu) {
                 // token th*16 + l16: hidden 8*q4 .. 8*q4+3 from row half 0 and
                 // 8*q4+4 .. 8*q4+7 from row half 1: one 16-byte fragment unit
+                // (the row-half-1 part of token halves >= TH_OFF comes from wave 3)
+                constexpr int TH_OFF = 2 - C::NOFF / 4;
 #pragma unroll
                 for (int th = 0; th < 2; ++th) {
-                    u32x4 v;
-                    v[0] = pack_bf16x2(h[0][th][0], h[0][th][1]);
-                    v[1] = pack_bf16x2(h[0][th][2], h[0][th][3]);
-                    v[2] = pack_bf16x2(h[1][th][0], h[1][th][1]);
-                    v[3] = pack_bf16x2(h[1][th][2], h[1][th][3]);
-                    Hw[(q4 >> 1) * 64 + (q4 & 1) * 32 + th * 16 + l16] = v;
+                    u32x4* dst = &Hw[(q4 >> 1) * 64 + (q4 & 1) * 32 + th * 16 + l16];
+                    if (th >= TH_OFF) {
+                        const u32x2 v = {pack_bf16x2(h[0][th][0], h[0][th][1]), pack_bf16x2(h[0][th][2], h[0][th][3])};
+                        *reinterpret_cast<u32x2*>(dst) = v;
+                    } else {
+                        u32x4 v;
+                        v[0] = pack_bf16x2(h[0][th][0], h[0][th][1]);
+                        v[1] = pack_bf16x2(h[0][th][2], h[0][th][3]);
+                        v[2] = pack_bf16x2(h[1][th][0], h[1][th][1]);
+                        v[3] = pack_bf16x2(h[1][th][2], h[1][th][3]);
+                        *dst = v;
+                    }
                 }
+            }
+            if constexpr (do_l1 && C::NOFF > 0) {
+                // hand row half 1 of the offloaded token halves of chunk c to wave 3
+                constexpr int TH_OFF = 2 - C::NOFF / 4;
+#pragma unroll
+                for (int th = TH_OFF; th < 2; ++th)
+                    Xs[(c & 1) * C::X_CH + (w * (C::NOFF / 4) + th - TH_OFF) * 64 + lane] =
+                        __builtin_bit_cast(u32x4, s[1][th]);
             }
         };
 
@@ -600,7 +642,10 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
         else l2_iter(F, F, T, 1, 2, m1, kk1, w2_stage(1));
         advance();
         for (int c = 2; c + 1 < nch; ++c) {                             // steady state
-            sync_stage();
+            // after a steady iteration, whose last loads are W2 rounds of a
+            // chunk used two iterations later, those stay in flight
+            if (C::NW2 == 3 && c > 2) sync_keep(std::integral_constant<int, C::NW2 == 3 ? W2_RL : 0>{});
+            else sync_stage();
             l2_iter(T, T, T, c, c + 1, m1, kk1, w2_stage(c));
             advance();
         }
@@ -657,11 +702,49 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
     }
     } else {
         // wave 3 when TB = 3: no token block; it helps stage the router
-        // weights and joins every barrier
+        // weights, then (NOFF > 0) evaluates the GELU of the row-half-1
+        // elements of the offloaded token halves of every layer-1 wave:
+        // iteration c reads chunk c-1's fp32 values from the hand-over stage
+        // and writes the upper 8 bytes of those hidden-tile units
         if constexpr (!ROUTED) stage_router_weights();
         __syncthreads();
         __syncthreads();
-        for (int c = 0; c <= nch + 1; ++c) sync_stage();
+        const int l16 = lane & 15, q4 = lane >> 4;
+        constexpr int NX = C::NOFF / 4, TH_OFF = 2 - NX;
+        int m3 = 0, kk3 = 0;
+        for (int c = 0; c <= nch + 1; ++c) {
+            sync_stage();
+            if (C::NOFF > 0 && c >= 1 && c <= nch) {
+                const u32x4* Xc = Xs + ((c - 1) & 1) * C::X_CH;
+                u32x4* Hc = Hs + ((c - 1) & 1) * C::H_CH;
+                f32x4 sv[TB][NX];
+                float hg[TB][NX];
+#pragma unroll
+                for (int wb = 0; wb < TB; ++wb)
+#pragma unroll
+                    for (int f = 0; f < NX; ++f) {
+                        sv[wb][f] = __builtin_bit_cast(f32x4, Xc[(wb * NX + f) * 64 + lane]);
+                        hg[wb][f] = 0.5f * Gs[wb * (MOT_MAX_EXPERTS * 32) + m3 * 32 + (TH_OFF + f) * 16 + l16];
+                    }
+#pragma unroll
+                for (int wb = 0; wb < TB; ++wb)
+#pragma unroll
+                    for (int f = 0; f < NX; ++f) {
+                        float hv[4];
+#pragma unroll
+                        for (int jj = 0; jj < 4; ++jj)
+                            hv[jj] = ACT == MOT_ACT_GELU ? gelu_half_scaled(sv[wb][f][jj], hg[wb][f])
+                                                         : 2.0f * hg[wb][f] * sv[wb][f][jj];
+                        const u32x2 v = {pack_bf16x2(hv[0], hv[1]), pack_bf16x2(hv[2], hv[3])};
+                        u32x4* unit16 = &Hc[wb * 128 + (q4 >> 1) * 64 + (q4 & 1) * 32 + (TH_OFF + f) * 16 + l16];
+                        reinterpret_cast<u32x2*>(unit16)[1] = v;
+                    }
+                kk3 += 32;
+                const bool wrap = kk3 == hidden;
+                kk3 = wrap ? 0 : kk3;
+                m3 = wrap ? m3 + 1 : m3;
+            }
+        }
     }
 }
 
