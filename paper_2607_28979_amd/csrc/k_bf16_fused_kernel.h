@@ -46,7 +46,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 // of each layer-1 lane's 16 elements (0, 4 or 8: row half 1 of token half 1,
 // or of both token halves), handed over through LDS in fp32.
 #ifndef MOT_FUSED_OFFLOAD
-#define MOT_FUSED_OFFLOAD 8
+#define MOT_FUSED_OFFLOAD 4
 #endif
 
 template <int D_IN, int D_OUT>
