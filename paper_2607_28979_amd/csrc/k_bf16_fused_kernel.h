@@ -38,9 +38,18 @@ namespace {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Elements (of 16 per lane and chunk) whose GELU runs before the layer-1 MFMAs
+// Elements (of 16 per lane and chunk) whose GELU runs as vector-only work
+// outside the layer-1 MFMA slots: before them (MOT_FUSED_A_LAST = 0) or after
+// them (1)
 #ifndef MOT_FUSED_PHASE_A
 #define MOT_FUSED_PHASE_A 6
+#endif
+#ifndef MOT_FUSED_A_LAST
+#define MOT_FUSED_A_LAST 0
+#endif
+// 0: layer-1 waves are the older waves of each SIMD pair; 4: layer-2 waves are
+#ifndef MOT_FUSED_ROLE_SHIFT
+#define MOT_FUSED_ROLE_SHIFT 0
 #endif
 // With TB = 3, wave 3 has no token block: it evaluates the GELU of this many
 // of each layer-1 lane's 16 elements (0, 4 or 8: row half 1 of token half 1,
@@ -148,8 +157,11 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
     }
     const int E = ROUTED ? 1 : p.E, hidden = p.hidden, EH = E * hidden;
     const size_t um = unit * p.E + (ROUTED ? tile.x : 0);   // first translator walked
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // 0..7
+    const int lane = threadIdx.x & 63;
+    // logical wave index: hardware wave h plays role (h + MOT_FUSED_ROLE_SHIFT) & 7
+    // (waves h and h + 4 share a SIMD either way)
+    const int w = __builtin_amdgcn_readfirstlane(((threadIdx.x >> 6) + MOT_FUSED_ROLE_SHIFT) & 7);
+    const int tid = w * 64 + lane;   // logical thread index
     const int g = lane >> 5, l32 = lane & 31;
     const uint32_t gmask = 0u - (uint32_t)g;   // all ones in the upper lane half
     const int tok0 = blockIdx.x * C::BM;
@@ -403,7 +415,7 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
             };
             const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
             if constexpr (do_l1) static_for<0, LOOK>([&](auto kc) { read_a(kc); });
-            if constexpr (do_gelu) {
+            if constexpr (do_gelu && !MOT_FUSED_A_LAST) {
                 static_for<0, 3>([&](auto stc) {
                     static_for<0, NEA>([&](auto ec) { gelu_elem(ec, stc); });
                 });
@@ -449,6 +461,11 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
                 }
                 __builtin_amdgcn_sched_barrier(0);
             });
+            if constexpr (do_gelu && MOT_FUSED_A_LAST) {
+                static_for<0, 3>([&](auto stc) {
+                    static_for<0, NEA>([&](auto ec) { gelu_elem(ec, stc); });
+                });
+            }
             if constexpr (do_gelu) {
                 // token th*16 + l16: hidden 8*q4 .. 8*q4+3 from row half 0 and
                 // 8*q4+4 .. 8*q4+7 from row half 1: one 16-byte fragment unit
