@@ -33,10 +33,10 @@ def log(*a):
 def measured_traffic(kernel_file: str, workload_tag: str):
     """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
     summary, or None when that summary was taken on a different kernel source
-    (its recorded source hash no longer matches)."""
+    (its recorded hash of the kernel's source file no longer matches)."""
     import hashlib
     src = os.path.join(ROOT, "paper_2607_28979_amd", "csrc", kernel_file)
-    prof = os.path.join(ROOT, "profiles", "%s_%s_hbm_traffic.md" % (kernel_file.split(".")[0],
+    prof = os.path.join(ROOT, "profiles", "%s_%s_hbm_traffic.md" % (kernel_file.split(".")[0].replace("_kernel", ""),
                                                                     workload_tag))
     if not (os.path.exists(src) and os.path.exists(prof)):
         return None
@@ -164,7 +164,7 @@ def main():
         "peak": peak,
         "unit": "TFLOP/s",
         "frac": round(achieved_tflops / peak, 4),
-        "traffic": (measured_traffic("k_bf16_fused.hip", "qwen2.5-1.5b-7b")
+        "traffic": (measured_traffic("k_bf16_fused_kernel.h", "qwen2.5-1.5b-7b")
                     if fused and args.workload == 3 and not args.top_k else None),
         "alg_flops_per_launch": flops,
         "alg_bytes_per_launch": w.alg_bytes(),

@@ -8,7 +8,9 @@ fp32 <= 1e-5, bf16 <= 2e-2; layer mapping and untouched layers bit-exact.
   oracle, both kernel paths where both exist;
 * every workload at full size in the benchmark's launch configuration,
   checked on sampled rows (first, last and seeded random rows) that the
-  oracle computes one by one;
+  oracle computes one by one, and the routed Top-K path at full size;
+* Top-K < E routing on every path (dense-masked and routed), skewed
+  routing (one translator takes every token), routed determinism;
 * invariants on the GPU: E = 1 identity pass-through (bit-exact), one-hot
   gate = single translator, uniform gate = mean, untouched layers, empty
   input, sub-batch invariance, run-to-run determinism, layouts.
@@ -143,6 +145,37 @@ def test_full_size_sampled(w, oracle_built):
         worst = max(worst, rel_frob(got, ref[u]))
     print("  max unit rel-Frobenius error on sampled rows %.3e" % worst, flush=True)
     assert worst <= TOL[w.dtype]
+    assert np.isfinite(gk).all() and np.isfinite(gv).all()
+
+
+ROUTED_FULL = [(WORKLOADS[3], 1), (WORKLOADS[3], 2), (WORKLOADS[4], 2)]
+
+
+@pytest.mark.parametrize("w,k", ROUTED_FULL, ids=["%s-top%d" % (w.name, k) for w, k in ROUTED_FULL])
+def test_full_size_routed_sampled(w, k, oracle_built):
+    """The routed Top-K path at full size (the launch `bench.py --top-k K`
+    times), on sampled rows the oracle computes one by one; rows whose K-th
+    and (K+1)-th scores are within 1e-3 (relative) are left out."""
+    from oracle import oracle_rows
+    w = w.with_(top_k=k)
+    print("case", w.name, "top_k", k, "full size routed", flush=True)
+    inp = generate(w)
+    lm = _layer_map(w)
+    gk, gv = run_gpu(w, inp, lm, algo=mb.ALGO_AUTO)
+    rows = sample_rows(w.n_tok, 24, w.seed)
+    units = [(j, x) for j in range(w.L_tgt) if lm[j] >= 0 for x in (0, 1)]
+    ref = oracle_rows(oracle_dims(w), inp.src_k, inp.src_v, lm, inp.w1, inp.b1, inp.w2, inp.b2,
+                      inp.wr, inp.br, units=units, rows=rows)
+    worst, n_skip = 0.0, 0
+    for u, (j, x) in enumerate(units):
+        keep = _topk_margin(w, inp, lm, j, x)[rows] >= 1e-3
+        n_skip += int((~keep).sum())
+        got = unit_rows(gk if x == 0 else gv, w, j)[rows]
+        worst = max(worst, rel_frob(got[keep], ref[u][keep]))
+    print("  max unit rel-Frobenius error on sampled rows %.3e (%d near-tie rows left out)"
+          % (worst, n_skip), flush=True)
+    assert worst <= TOL[w.dtype]
+    assert n_skip <= max(2, len(rows) * len(units) // 100)
     assert np.isfinite(gk).all() and np.isfinite(gv).all()
 
 
