@@ -38,7 +38,20 @@ bool fused_supported(const Problem& p) {
     return din && dout && p.hidden % 32 == 0 && p.E * p.hidden >= 64 && p.E <= MOT_MAX_EXPERTS;
 }
 
-int fused_tile_rows(const Problem& p) { return p.d_out == 512 ? Cfg<128, 512>::BM : Cfg<128, 128>::BM; }
+int fused_tile_rows(const Problem& p) {
+    switch (p.d_in * 1000 + p.d_out) {
+        case 128128: return Cfg<128, 128>::BM;
+        case 128256: return Cfg<128, 256>::BM;
+        case 128512: return Cfg<128, 512>::BM;
+        case 256128: return Cfg<256, 128>::BM;
+        case 256256: return Cfg<256, 256>::BM;
+        case 256512: return Cfg<256, 512>::BM;
+        case 512128: return Cfg<512, 128>::BM;
+        case 512256: return Cfg<512, 256>::BM;
+        case 512512: return Cfg<512, 512>::BM;
+        default: return 0;
+    }
+}
 
 hipError_t launch_bf16_fused(const Problem& p, const UnitTab& ut, hipStream_t stream) {
     return launch_shape(p, ut, false, stream);

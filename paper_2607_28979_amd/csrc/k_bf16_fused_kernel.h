@@ -51,6 +51,12 @@ typedef __attribute__((address_space(3))) void lds_void;
 #ifndef MOT_FUSED_ROLE_SHIFT
 #define MOT_FUSED_ROLE_SHIFT 0
 #endif
+// Layer-2 waves per workgroup when d_out >= 256 and d_in <= 256: 4 (one per
+// SIMD; d_out = 512 then takes 3 token blocks) or 8 (two per SIMD, each with
+// half the output columns, which leaves room for 4 token blocks)
+#ifndef MOT_FUSED_L2W
+#define MOT_FUSED_L2W 8
+#endif
 // With TB = 3, wave 3 has no token block: it evaluates the GELU of this many
 // of each layer-1 lane's 16 elements (0, 4 or 8: row half 1 of token half 1,
 // or of both token halves), handed over through LDS in fp32.
@@ -60,10 +66,12 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 template <int D_IN, int D_OUT>
 struct Cfg {
-    static constexpr int TB = D_OUT == 512 ? 3 : 4;   // token blocks per workgroup
+    static constexpr int L2W = (D_OUT >= 256 && D_IN <= 256) ? MOT_FUSED_L2W : 4;   // layer-2 waves
+    static constexpr int NW = 4 + L2W;                     // waves per workgroup
+    static constexpr int TB = (D_OUT == 512 && L2W == 4) ? 3 : 4;   // token blocks per workgroup
     static constexpr int BM = 32 * TB;            // tokens per workgroup
     static constexpr int KS1 = D_IN / 16;         // layer-1 k-steps
-    static constexpr int OUTW = D_OUT / 4;        // output columns per wave
+    static constexpr int OUTW = D_OUT / L2W;      // output columns per layer-2 wave
     static constexpr int NBW = OUTW / 32;         // output blocks per wave
     static constexpr int CPR1 = D_IN / 8;         // 16-byte chunks per W1 row
     static constexpr int W1_CH = 32 * CPR1;       // chunks per W1 stage
@@ -126,11 +134,12 @@ __device__ __forceinline__ void static_for(F&& f) {
 // the router is skipped (the gates come with the assignments) and the E*hidden
 // walk covers that translator's hidden only.
 template <int D_IN, int D_OUT, int ACT, bool ROUTED>
-__global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * Cfg<D_IN, D_OUT>::NW, 64 * Cfg<D_IN, D_OUT>::NW)))
+void k_bf16_fused(Problem p, UnitTab ut) {
     using C = Cfg<D_IN, D_OUT>;
     constexpr int TB = C::TB;
     // the four layer-2 waves issue the global -> LDS weight loads
-    constexpr int NLD = 4;
+    constexpr int NLD = C::L2W;
     constexpr int W1_RL = C::W1_CH / (64 * NLD), W2_RL = C::W2_CH / (64 * NLD);
     __shared__ u32x4 smem[C::TOTAL];
     u32x4* W1s = smem + C::OFF_W1;
@@ -160,7 +169,7 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
     const int lane = threadIdx.x & 63;
     // logical wave index: hardware wave h plays role (h + MOT_FUSED_ROLE_SHIFT) & 7
     // (waves h and h + 4 share a SIMD either way)
-    const int w = __builtin_amdgcn_readfirstlane(((threadIdx.x >> 6) + MOT_FUSED_ROLE_SHIFT) & 7);
+    const int w = __builtin_amdgcn_readfirstlane(((threadIdx.x >> 6) + MOT_FUSED_ROLE_SHIFT) % C::NW);
     const int tid = w * 64 + lane;   // logical thread index
     const int g = lane >> 5, l32 = lane & 31;
     const uint32_t gmask = 0u - (uint32_t)g;   // all ones in the upper lane half
@@ -187,7 +196,7 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
     //       r*RS and u, so only (r*RS) & 15 (NV1 values) changes the lane part;
     //   W2: output row 64r + t/4, swizzle ((row >> 2) & 3) the same for all r.
     const int t_ld = lw * 64 + lane;
-    constexpr int RS = 256 / C::CPR1;
+    constexpr int RS = 64 * NLD / C::CPR1;
     constexpr int NV1 = RS < 16 ? 16 / RS : 1;
     auto w1_lane = [&](int v) -> uint32_t {
         const int u = t_ld / C::CPR1, pc = t_ld % C::CPR1;
@@ -202,7 +211,7 @@ __global__ __launch_bounds__(512, 1) void k_bf16_fused(Problem p, UnitTab ut) {
     };
     // W2 columns [kk, kk+32) of translator m (round r) into stage st
     auto load_w2_round = [&](int m, int kk, int st, int r) {
-        const char* base = reinterpret_cast<const char*>(W2u + ((size_t)m * D_OUT + 64 * r) * hidden + kk);
+        const char* base = reinterpret_cast<const char*>(W2u + ((size_t)m * D_OUT + 16 * NLD * r) * hidden + kk);
         load_lds16(base + w2_lane, W2s + st * C::W2_CH + r * 64 * NLD + lw * 64);
     };
     const int nch = EH / 32;   // >= 2
@@ -770,9 +779,10 @@ hipError_t launch_t(const Problem& p, const UnitTab& ut, hipStream_t stream) {
     using C = Cfg<D_IN, D_OUT>;
     dim3 grid(ROUTED ? p.rt.max_tiles : (p.n_tok + C::BM - 1) / C::BM, ut.n);
     if (p.act == MOT_ACT_GELU)
-        hipLaunchKernelGGL((k_bf16_fused<D_IN, D_OUT, MOT_ACT_GELU, ROUTED>), grid, dim3(512), 0, stream, p, ut);
+        hipLaunchKernelGGL((k_bf16_fused<D_IN, D_OUT, MOT_ACT_GELU, ROUTED>), grid, dim3(64 * C::NW), 0, stream, p,
+                           ut);
     else
-        hipLaunchKernelGGL((k_bf16_fused<D_IN, D_OUT, MOT_ACT_IDENTITY, ROUTED>), grid, dim3(512), 0, stream,
+        hipLaunchKernelGGL((k_bf16_fused<D_IN, D_OUT, MOT_ACT_IDENTITY, ROUTED>), grid, dim3(64 * C::NW), 0, stream,
                            p, ut);
     return hipGetLastError();
 }
