@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define MOT_ABI_VERSION 1
+#define MOT_ABI_VERSION 2
 #define MOT_MAX_LAYERS 256   /* L_src, L_tgt <= MOT_MAX_LAYERS               */
 #define MOT_MAX_EXPERTS 16   /* E <= MOT_MAX_EXPERTS                         */
 
@@ -90,6 +90,11 @@ typedef enum { MOT_ALGO_AUTO = 0, MOT_ALGO_UNFUSED = 1, MOT_ALGO_FUSED = 2, MOT_
  *                  hidden-activation workspace.  Requesting an impossible path
  *                  returns MOT_ERR_UNSUPPORTED.  All paths compute the same
  *                  function.
+ *   streams        2 (or 0): keys and values, each with its own translators;
+ *                  1: one activation stream per layer (the MoT-h variant,
+ *                  paper App. C.5): src_k -> dst_k with translators indexed
+ *                  [L_tgt][1][E]...; src_v and dst_v are ignored (may be
+ *                  NULL).  mot_restore_kv then forms K and V from it.
  *   workspace      optional device scratch; NULL = library-owned buffer
  *   workspace_bytes size of `workspace` in bytes
  *
@@ -105,6 +110,7 @@ typedef struct {
     int32_t H_tgt, D_tgt;
     int32_t E, top_k, hidden;
     int32_t dtype, src_layout, dst_layout, act, algo;
+    int32_t streams;
     void* workspace;
     size_t workspace_bytes;
 } mot_shapes;
@@ -180,6 +186,33 @@ const char* mot_status_string(mot_status status);
 
 /* Detail of the last error raised on the calling thread ("" if none). */
 const char* mot_last_error(void);
+
+/*
+ * Key/value restoration for the activation-translation variant MoT-h (paper
+ * App. C.5): the target's key and value projections applied to a translated
+ * intermediate activation a (as written by mot_translate with streams = 1):
+ *     K[l][t] = W^K[l] a[l][t] + b^K[l],    V[l][t] = W^V[l] a[l][t] + b^V[l]
+ * for every layer l with layer_map[l] >= 0 (NULL: every layer).
+ *
+ *   act        device bf16 [L][B][T][d_act]
+ *   wk, wv     device bf16 [L][d_kv][d_act], d_kv = H_tgt * D_tgt (nn.Linear layout)
+ *   bk, bv     device bf16 [L][d_kv] or NULL (zero)
+ *   dst_k/v    device bf16 [L] x dst_layout ([B][T][H_tgt][D_tgt] or [B][H_tgt][T][D_tgt])
+ *   layer_map  HOST int32[L] or NULL; layers with a negative entry are not written
+ * Requires dtype MOT_BF16, d_act a multiple of 64, D_tgt a multiple of 8
+ * (MOT_ERR_UNSUPPORTED otherwise).  Same error discipline as mot_translate:
+ * every check runs before anything is enqueued.
+ */
+typedef struct {
+    int32_t L, B, T;
+    int32_t d_act;
+    int32_t H_tgt, D_tgt;
+    int32_t dtype, dst_layout;
+} mot_restore_shapes;
+
+mot_status mot_restore_kv(const void* act, const int32_t* layer_map, const void* wk, const void* bk,
+                          const void* wv, const void* bv, void* dst_k, void* dst_v,
+                          const mot_restore_shapes* shapes, hipStream_t stream);
 
 /* MOT_ABI_VERSION of the loaded library. */
 int mot_abi_version(void);

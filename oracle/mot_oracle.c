@@ -38,6 +38,10 @@
  * identity activation == closed-form matrix product; GELU against tabulated
  * normal-CDF values; brute-force scalar loops on 2-token, 2-dim shapes;
  * token and expert permutation invariance; depth-ratio map properties.
+ *
+ * Also here: the key/value restoration of the activation-translation variant
+ * MoT-h (App. C.5), pinned by hand-computed values, the identity projection,
+ * a float64 matrix product and an identity-translator chain.
  */
 #include <math.h>
 #include <pthread.h>
@@ -343,5 +347,51 @@ int mot_oracle_depth_ratio_map(int32_t L_src, int32_t L_tgt, int32_t* out)
 {
     if (L_src <= 0 || L_tgt <= 0 || !out) return OR_BAD_ARG;
     for (int32_t j = 0; j < L_tgt; ++j) out[j] = (int32_t)(((int64_t)j * L_src) / L_tgt);
+    return OR_OK;
+}
+
+/* Key/value restoration of the activation-translation variant MoT-h
+ * (App. C.5, "Hidden States Translation"): the target's fixed key and value
+ * projections applied to a translated intermediate activation,
+ *     K[l][u] = W^K[l] a[l][u] + b^K[l],    V[l][u] = W^V[l] a[l][u] + b^V[l],
+ * for every layer l with layer_map[l] >= 0 (layer_map NULL: every layer).
+ *   act   [L][B][T][d_act]        wk, wv [L][d_kv][d_act], d_kv = H_tgt*D_tgt
+ *   bk,bv [L][d_kv] or NULL        dst_k, dst_v [L] x dst_layout, double
+ * Sums run over c = 0..d_act-1 in order, in double; the bias is added last.
+ * Layers that are not restored are left untouched. */
+int mot_oracle_restore_kv(const float* act, const int32_t* layer_map,
+                          const float* wk, const float* bk, const float* wv, const float* bv,
+                          double* dst_k, double* dst_v, int32_t L, int32_t B, int32_t T,
+                          int32_t d_act, int32_t H_tgt, int32_t D_tgt, int32_t dst_layout)
+{
+    if (!act || !wk || !wv || !dst_k || !dst_v) return OR_BAD_ARG;
+    if (L <= 0 || B < 0 || T < 0 || d_act <= 0 || H_tgt <= 0 || D_tgt <= 0) return OR_BAD_ARG;
+    if (dst_layout != 0 && dst_layout != 1) return OR_BAD_ARG;
+    const size_t d_kv = (size_t)H_tgt * D_tgt, n_tok = (size_t)B * T;
+    for (int32_t l = 0; l < L; ++l) {
+        if (layer_map && layer_map[l] < 0) continue;
+        for (int32_t b = 0; b < B; ++b)
+            for (int32_t t = 0; t < T; ++t) {
+                const float* a = act + ((size_t)l * n_tok + (size_t)b * T + t) * d_act;
+                for (int32_t h = 0; h < H_tgt; ++h)
+                    for (int32_t d = 0; d < D_tgt; ++d) {
+                        const size_t o = (size_t)h * D_tgt + d;
+                        const float* rk = wk + ((size_t)l * d_kv + o) * d_act;
+                        const float* rv = wv + ((size_t)l * d_kv + o) * d_act;
+                        double sk = 0.0, sv = 0.0;
+                        for (int32_t c = 0; c < d_act; ++c) {
+                            sk += (double)rk[c] * (double)a[c];
+                            sv += (double)rv[c] * (double)a[c];
+                        }
+                        if (bk) sk += (double)bk[(size_t)l * d_kv + o];
+                        if (bv) sv += (double)bv[(size_t)l * d_kv + o];
+                        size_t idx = (size_t)l * n_tok * d_kv;
+                        idx += dst_layout == 0 ? (((size_t)b * T + t) * H_tgt + h) * D_tgt + d
+                                               : (((size_t)b * H_tgt + h) * T + t) * D_tgt + d;
+                        dst_k[idx] = sk;
+                        dst_v[idx] = sv;
+                    }
+            }
+    }
     return OR_OK;
 }

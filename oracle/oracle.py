@@ -86,7 +86,7 @@ def _load():
             build_oracle(force=False)
         _lib = ctypes.CDLL(_LIB)
         for fn in (_lib.mot_oracle_translate, _lib.mot_oracle_rows,
-                   _lib.mot_oracle_depth_ratio_map):
+                   _lib.mot_oracle_depth_ratio_map, _lib.mot_oracle_restore_kv):
             fn.restype = ctypes.c_int
     return _lib
 
@@ -167,3 +167,27 @@ def oracle_depth_ratio_map(L_src: int, L_tgt: int) -> np.ndarray:
     if rc != 0:
         raise ValueError("mot_oracle_depth_ratio_map failed with code %d" % rc)
     return out
+
+
+def oracle_restore_kv(act, layer_map, wk, bk, wv, bv, B, T, H_tgt, D_tgt, dst_layout=0,
+                      dst_k=None, dst_v=None):
+    """MoT-h key/value restoration (App. C.5): K = W^K a + b^K, V = W^V a + b^V
+    per restored layer.  act [L][B][T][d_act]; wk, wv [L][d_kv][d_act];
+    bk, bv [L][d_kv] or None; layer_map int[L] or None (every layer).
+    Returns (dst_k, dst_v) as float64 in the dst layout; layers that are not
+    restored keep the given contents (NaN when dst_k/dst_v are not supplied)."""
+    lib = _load()
+    act = _f32(act, "act")
+    L, d_act = act.shape[0], act.shape[-1]
+    arrs = [_f32(a, n) for a, n in ((wk, "wk"), (bk, "bk"), (wv, "wv"), (bv, "bv"))]
+    lm = None if layer_map is None else np.ascontiguousarray(layer_map, dtype=np.int32)
+    shape = (L, B, T, H_tgt, D_tgt) if dst_layout == 0 else (L, B, H_tgt, T, D_tgt)
+    dst_k = np.full(shape, np.nan) if dst_k is None else np.array(dst_k, dtype=np.float64)
+    dst_v = np.full(shape, np.nan) if dst_v is None else np.array(dst_v, dtype=np.float64)
+    i32 = ctypes.c_int32
+    rc = lib.mot_oracle_restore_kv(_ptr(act), _ptr(lm), *[_ptr(a) for a in arrs],
+                                   _ptr(dst_k), _ptr(dst_v), i32(L), i32(B), i32(T), i32(d_act),
+                                   i32(H_tgt), i32(D_tgt), i32(dst_layout))
+    if rc != 0:
+        raise ValueError("mot_oracle_restore_kv failed with code %d" % rc)
+    return dst_k, dst_v

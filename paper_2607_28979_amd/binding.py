@@ -25,7 +25,7 @@ STATUS = {0: "MOT_OK", 1: "MOT_ERR_NULL_ARG", 2: "MOT_ERR_BAD_SHAPE", 3: "MOT_ER
           7: "MOT_ERR_HIP"}
 
 EXPORTED = ("mot_translate", "mot_workspace_bytes", "mot_depth_ratio_map", "mot_status_string",
-            "mot_last_error", "mot_abi_version")
+            "mot_last_error", "mot_abi_version", "mot_restore_kv")
 
 
 class MotError(RuntimeError):
@@ -38,8 +38,13 @@ class MotError(RuntimeError):
 class _Shapes(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "L_src", "L_tgt", "B", "T", "H_src", "D_src", "H_tgt", "D_tgt", "E", "top_k", "hidden",
-        "dtype", "src_layout", "dst_layout", "act", "algo")] + [
+        "dtype", "src_layout", "dst_layout", "act", "algo", "streams")] + [
         ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
+
+
+class _RestoreShapes(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("L", "B", "T", "d_act", "H_tgt", "D_tgt", "dtype",
+                                             "dst_layout")]
 
 
 class _TW(ctypes.Structure):
@@ -69,12 +74,13 @@ class Shapes:
     dst_layout: int = LAYOUT_BTHD
     act: int = ACT_GELU
     algo: int = ALGO_AUTO
+    streams: int = 2          # 2 = keys and values; 1 = one activation stream (MoT-h)
 
     def c(self, workspace=None, workspace_bytes=0) -> _Shapes:
         return _Shapes(self.L_src, self.L_tgt, self.B, self.T, self.H_src, self.D_src, self.H_tgt,
                        self.D_tgt, self.E, self.top_k or self.E, self.hidden, self.dtype,
-                       self.src_layout, self.dst_layout, self.act, self.algo, workspace,
-                       workspace_bytes)
+                       self.src_layout, self.dst_layout, self.act, self.algo, self.streams,
+                       workspace, workspace_bytes)
 
     @classmethod
     def from_workload(cls, w, **kw) -> "Shapes":
@@ -90,6 +96,16 @@ def lib_path() -> str:
     return _LIB_PATH
 
 
+def _hip_runtimes() -> set:
+    """Distinct files of the HIP runtime mapped into this process (Linux)."""
+    try:
+        with open("/proc/self/maps") as f:
+            return {os.path.realpath(ln.split()[-1]) for ln in f
+                    if "libamdhip64.so" in ln and ln.split()[-1].startswith("/")}
+    except OSError:
+        return set()
+
+
 def load_library():
     """Load libmot.so; raises if it has not been built (no fallback exists)."""
     global _lib
@@ -97,7 +113,20 @@ def load_library():
         if not os.path.exists(_LIB_PATH):
             raise MotError(-1, "libmot.so not found at %s; build it with "
                                "`python -m paper_2607_28979_amd.build`" % _LIB_PATH)
+        # PyTorch for ROCm ships its own HIP runtime.  Loading torch first lets
+        # libmot bind to that same runtime (the dynamic linker matches its
+        # soname), so streams and device pointers from torch are valid here;
+        # loading libmot first would bring a second, separate runtime into
+        # the process.
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         lib = ctypes.CDLL(_LIB_PATH)
+        runtimes = _hip_runtimes()
+        if len(runtimes) > 1:
+            raise MotError(-1, "two HIP runtimes are loaded in this process (%s); import torch "
+                               "before loading libmot" % ", ".join(sorted(runtimes)))
         lib.mot_translate.restype = ctypes.c_int
         lib.mot_translate.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                       ctypes.POINTER(_TW), ctypes.POINTER(_RW), ctypes.c_void_p,
@@ -110,6 +139,9 @@ def load_library():
         lib.mot_status_string.argtypes = [ctypes.c_int]
         lib.mot_last_error.restype = ctypes.c_char_p
         lib.mot_abi_version.restype = ctypes.c_int
+        lib.mot_restore_kv.restype = ctypes.c_int
+        lib.mot_restore_kv.argtypes = [ctypes.c_void_p] * 8 + [ctypes.POINTER(_RestoreShapes),
+                                                               ctypes.c_void_p]
         _lib = lib
     return _lib
 
@@ -189,3 +221,23 @@ def translate(src_k, src_v, layer_map: Sequence[int], w1, b1, w2, b2, wr, br, ds
     stream = torch.cuda.current_stream().cuda_stream
     translate_raw(src_k, src_v, layer_map, w1, b1, w2, b2, wr, br, dst_k, dst_v, shapes,
                   stream=stream, workspace=workspace, workspace_bytes_=ws_bytes)
+
+
+def restore_kv(act, layer_map, wk, bk, wv, bv, dst_k, dst_v, L: int, B: int, T: int, d_act: int,
+               H_tgt: int, D_tgt: int, dst_layout: int = LAYOUT_BTHD) -> None:
+    """mot_restore_kv on the current torch stream (bf16 tensors on the
+    current device): K = W^K a + b^K and V = W^V a + b^V for every layer with
+    layer_map[l] >= 0 (layer_map None = all layers)."""
+    import numpy as np
+    import torch
+    lib = load_library()
+    for name, t in (("act", act), ("wk", wk), ("bk", bk), ("wv", wv), ("bv", bv), ("dst_k", dst_k),
+                    ("dst_v", dst_v)):
+        if t is not None and (t.dtype != torch.bfloat16 or not t.is_contiguous()):
+            raise MotError(2, "%s must be a contiguous bfloat16 tensor" % name)
+    lm = None if layer_map is None else np.ascontiguousarray(layer_map, dtype=np.int32)
+    c = _RestoreShapes(L, B, T, d_act, H_tgt, D_tgt, MOT_BF16, dst_layout)
+    stream = torch.cuda.current_stream().cuda_stream
+    _check(lib.mot_restore_kv(_ptr(act), lm.ctypes.data if lm is not None else None, _ptr(wk),
+                              _ptr(bk), _ptr(wv), _ptr(bv), _ptr(dst_k), _ptr(dst_v),
+                              ctypes.byref(c), stream))

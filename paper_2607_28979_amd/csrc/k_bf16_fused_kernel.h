@@ -150,7 +150,7 @@ void k_bf16_fused(Problem p, UnitTab ut) {
 
     const uint32_t code = ut.code[blockIdx.y];
     const int j = unit_j(code), x = unit_x(code), i = unit_i(code);
-    const size_t unit = (size_t)j * 2 + x;
+    const size_t unit = (size_t)j * p.streams + x;
     // routed tile: {translator, first assignment, rows}; tiles beyond the
     // unit's count leave at once (uniform over the workgroup, before any barrier)
     int4 tile = make_int4(0, 0, 0, 0);

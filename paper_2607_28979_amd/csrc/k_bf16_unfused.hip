@@ -57,7 +57,7 @@ __global__ __launch_bounds__(256) void k_bf16_gemm1(Problem p, UnitTab ut) {
     const int j = unit_j(code), x = unit_x(code), i = unit_i(code), gs = unit_gslot(code);
     const int EH = p.E * p.hidden;
     const int tok0 = blockIdx.x * BN, hid0 = blockIdx.y * BM;
-    const size_t unit = (size_t)j * 2 + x;
+    const size_t unit = (size_t)j * p.streams + x;
     const uint16_t* W1 = reinterpret_cast<const uint16_t*>(p.w1) + unit * EH * p.d_in;
     const uint16_t* src = reinterpret_cast<const uint16_t*>(p.src[x]);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -165,7 +165,7 @@ __global__ __launch_bounds__(256) void k_bf16_gemm2(Problem p, UnitTab ut) {
     const int j = unit_j(code), x = unit_x(code), gs = unit_gslot(code);
     const int EH = p.E * p.hidden;
     const int tok0 = blockIdx.x * BM, out0 = blockIdx.y * BN;
-    const size_t unit = (size_t)j * 2 + x;
+    const size_t unit = (size_t)j * p.streams + x;
     const uint16_t* W2 = reinterpret_cast<const uint16_t*>(p.w2) + unit * p.E * p.d_out * p.hidden;
     const uint16_t* H = reinterpret_cast<const uint16_t*>(p.hbuf) + (size_t)blockIdx.z * p.n_tok_pad * EH;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;

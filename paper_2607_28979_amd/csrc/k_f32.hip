@@ -41,7 +41,7 @@ __global__ __launch_bounds__(256) void k_f32_gemm1(Problem p, UnitTab ut) {
     const int j = unit_j(code), x = unit_x(code), i = unit_i(code), gs = unit_gslot(code);
     const int EH = p.E * p.hidden;
     const int tok0 = blockIdx.x * TM, hid0 = blockIdx.y * TN;
-    const size_t unit = (size_t)j * 2 + x;
+    const size_t unit = (size_t)j * p.streams + x;
     const float* W1 = reinterpret_cast<const float*>(p.w1) + unit * EH * p.d_in;
     const float* src = reinterpret_cast<const float*>(p.src[x]);
     const int tid = threadIdx.x, tx = tid % 16, ty = tid / 16;
@@ -96,7 +96,7 @@ __global__ __launch_bounds__(256) void k_f32_gemm2(Problem p, UnitTab ut) {
     const int j = unit_j(code), x = unit_x(code), gs = unit_gslot(code);
     const int EH = p.E * p.hidden;
     const int tok0 = blockIdx.x * TM, out0 = blockIdx.y * TN;
-    const size_t unit = (size_t)j * 2 + x;
+    const size_t unit = (size_t)j * p.streams + x;
     const float* W2 = reinterpret_cast<const float*>(p.w2) + unit * p.E * p.d_out * p.hidden;
     const float* H = reinterpret_cast<const float*>(p.hbuf) + (size_t)blockIdx.z * p.n_tok_pad * EH;
     const int tid = threadIdx.x, tx = tid % 16, ty = tid / 16;

@@ -73,7 +73,7 @@ __global__ __launch_bounds__(256) void k_router(Problem p, UnitTab ut) {
     const int j = unit_j(code), x = unit_x(code), i = unit_i(code), gs = unit_gslot(code);
     const int q = threadIdx.x % kLanesPerTok;
     const void* wr = p.wr;
-    size_t wr_base = ((size_t)j * 2 + x) * p.E * p.d_in;
+    size_t wr_base = ((size_t)j * p.streams + x) * p.E * p.d_in;
     if constexpr (WLDS) {
         const int n16 = p.E * p.d_in / V::n;   // 16-byte chunks
         const u32x4* g = reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(p.wr) +
@@ -86,7 +86,7 @@ __global__ __launch_bounds__(256) void k_router(Problem p, UnitTab ut) {
     for (int grp = 0; grp < kGroups; ++grp) {
     const int tok = (blockIdx.x * kGroups + grp) * kTokPerBlock + threadIdx.x / kLanesPerTok;
     const int E = p.E, d_in = p.d_in;
-    const size_t unit = (size_t)j * 2 + x;
+    const size_t unit = (size_t)j * p.streams + x;
 
     float acc[MOT_MAX_EXPERTS];
 #pragma unroll

@@ -70,6 +70,9 @@ mot_status check_shapes(const mot_shapes* s) {
         return fail(MOT_ERR_BAD_SHAPE, "layouts must be MOT_LAYOUT_BTHD or MOT_LAYOUT_BHTD");
     if (s->act != MOT_ACT_GELU && s->act != MOT_ACT_IDENTITY)
         return fail(MOT_ERR_BAD_SHAPE, "act=%d is not MOT_ACT_GELU or MOT_ACT_IDENTITY", s->act);
+    if (s->streams < 0 || s->streams > 2)
+        return fail(MOT_ERR_BAD_SHAPE, "streams=%d must be 1 (one activation stream) or 2 (keys and values; 0 = 2)",
+                    s->streams);
     if (s->algo != MOT_ALGO_AUTO && s->algo != MOT_ALGO_UNFUSED && s->algo != MOT_ALGO_FUSED &&
         s->algo != MOT_ALGO_ROUTED)
         return fail(MOT_ERR_BAD_SHAPE, "algo=%d is not a mot_algo value", s->algo);
@@ -104,6 +107,7 @@ Problem base_problem(const mot_shapes* s) {
     p.n_tok = s->B * s->T;
     p.n_tok_pad = (int32_t)round_up((size_t)p.n_tok, 128);
     p.src_layout = s->src_layout; p.dst_layout = s->dst_layout; p.act = s->act;
+    p.streams = s->streams == 1 ? 1 : 2;
     return p;
 }
 
@@ -119,7 +123,7 @@ void make_plan(const mot_shapes* s, const int32_t* layer_map, Plan* pl) {
     for (int j = 0; j < s->L_tgt; ++j) {
         const int i = layer_map ? layer_map[j] : 0;
         if (i < 0) continue;
-        for (int x = 0; x < 2; ++x) {
+        for (int x = 0; x < p.streams; ++x) {
             pl->codes[n] = unit_code(j, x, i, n);
             ++n;
         }
@@ -255,16 +259,21 @@ mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* la
     mot_status st = check_shapes(s);
     if (st != MOT_OK) return st;
     if ((int64_t)s->B * s->T == 0) return MOT_OK;   // empty context: nothing is read or written
-    if (!src_k || !src_v || !layer_map || !tw || !rw || !dst_k || !dst_v)
+    const bool two = s->streams != 1;   // keys and values, or one activation stream
+    if (!src_k || !layer_map || !tw || !rw || !dst_k || (two && (!src_v || !dst_v)))
         return fail(MOT_ERR_NULL_ARG, "a required argument is NULL");
     if (!tw->w1 || !tw->w2 || !rw->w)
         return fail(MOT_ERR_NULL_ARG, "w1, w2 and the router weight are required (biases may be NULL)");
     for (int j = 0; j < s->L_tgt; ++j)
         if (layer_map[j] < -1 || layer_map[j] >= s->L_src)
             return fail(MOT_ERR_BAD_LAYER_MAP, "layer_map[%d]=%d outside [-1, %d)", j, layer_map[j], s->L_src);
-    const void* dev_ptrs[] = {src_k, src_v, dst_k, dst_v, tw->w1, tw->w2, rw->w};
+    const void* dev_ptrs[] = {src_k, dst_k, tw->w1, tw->w2, rw->w, two ? src_v : src_k, two ? dst_v : dst_k};
     for (const void* q : dev_ptrs)
         if (!aligned16(q)) return fail(MOT_ERR_MISALIGNED, "device pointer %p is not 16-byte aligned", q);
+    if (!two) {
+        src_v = nullptr;
+        dst_v = nullptr;
+    }
     const size_t es = s->dtype == MOT_BF16 ? 2 : 4;
     const void* bias_ptrs[] = {tw->b1, tw->b2, rw->b};
     for (const void* q : bias_ptrs)
@@ -277,9 +286,9 @@ mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* la
     const int d_in = s->H_src * s->D_src, d_out = s->H_tgt * s->D_tgt;
     const size_t src_bytes = (size_t)s->L_src * n_tok * d_in * es;
     const size_t dst_bytes = (size_t)s->L_tgt * n_tok * d_out * es;
-    if (overlaps(dst_k, dst_bytes, dst_v, dst_bytes) || overlaps(dst_k, dst_bytes, src_k, src_bytes) ||
-        overlaps(dst_k, dst_bytes, src_v, src_bytes) || overlaps(dst_v, dst_bytes, src_k, src_bytes) ||
-        overlaps(dst_v, dst_bytes, src_v, src_bytes))
+    if (overlaps(dst_k, dst_bytes, src_k, src_bytes) ||
+        (two && (overlaps(dst_k, dst_bytes, dst_v, dst_bytes) || overlaps(dst_k, dst_bytes, src_v, src_bytes) ||
+                 overlaps(dst_v, dst_bytes, src_k, src_bytes) || overlaps(dst_v, dst_bytes, src_v, src_bytes))))
         return fail(MOT_ERR_BAD_SHAPE, "destination caches overlap each other or the source caches");
 
     // workspace
@@ -299,7 +308,7 @@ mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* la
             }
             ws = s->workspace;
             if (overlaps(ws, s->workspace_bytes, dst_k, dst_bytes) ||
-                overlaps(ws, s->workspace_bytes, dst_v, dst_bytes))
+                (two && overlaps(ws, s->workspace_bytes, dst_v, dst_bytes)))
                 return fail(MOT_ERR_BAD_SHAPE, "workspace overlaps a destination cache");
         }
     }
@@ -356,6 +365,50 @@ mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* la
             }
         }
     }
+    if (e != hipSuccess) return fail(MOT_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
+    return MOT_OK;
+}
+
+mot_status mot_restore_kv(const void* act, const int32_t* layer_map, const void* wk, const void* bk,
+                          const void* wv, const void* bv, void* dst_k, void* dst_v,
+                          const mot_restore_shapes* s, hipStream_t stream) {
+    g_err[0] = 0;
+    if (!s) return fail(MOT_ERR_NULL_ARG, "shapes is NULL");
+    if (s->L < 1 || s->L > MOT_MAX_LAYERS)
+        return fail(MOT_ERR_BAD_SHAPE, "L=%d must be in [1, %d]", s->L, MOT_MAX_LAYERS);
+    if (s->B < 0 || s->T < 0 || (int64_t)s->B * s->T > (int64_t)1 << 26)
+        return fail(MOT_ERR_BAD_SHAPE, "B=%d T=%d: need B, T >= 0 and B*T <= 2^26", s->B, s->T);
+    if (s->d_act < 1 || s->d_act > 65536 || s->H_tgt < 1 || s->D_tgt < 1 || (int64_t)s->H_tgt * s->D_tgt > 65536)
+        return fail(MOT_ERR_BAD_SHAPE, "d_act, H_tgt, D_tgt must be >= 1 and rows at most 65536 wide");
+    if (s->dtype != MOT_F32 && s->dtype != MOT_BF16)
+        return fail(MOT_ERR_BAD_SHAPE, "dtype=%d is not MOT_F32 or MOT_BF16", s->dtype);
+    if (s->dst_layout != MOT_LAYOUT_BTHD && s->dst_layout != MOT_LAYOUT_BHTD)
+        return fail(MOT_ERR_BAD_SHAPE, "dst_layout must be MOT_LAYOUT_BTHD or MOT_LAYOUT_BHTD");
+    if (s->dtype != MOT_BF16 || s->d_act % 64 || s->D_tgt % 8)
+        return fail(MOT_ERR_UNSUPPORTED, "restore needs bf16, d_act %% 64 == 0 and D_tgt %% 8 == 0 "
+                    "(got dtype=%d d_act=%d D_tgt=%d)", s->dtype, s->d_act, s->D_tgt);
+    if ((int64_t)s->B * s->T == 0) return MOT_OK;
+    if (!act || !wk || !wv || !dst_k || !dst_v)
+        return fail(MOT_ERR_NULL_ARG, "act, wk, wv, dst_k and dst_v are required (biases may be NULL)");
+    const void* dev_ptrs[] = {act, wk, wv, dst_k, dst_v};
+    for (const void* q : dev_ptrs)
+        if (!aligned16(q)) return fail(MOT_ERR_MISALIGNED, "device pointer %p is not 16-byte aligned", q);
+    if ((bk && (reinterpret_cast<uintptr_t>(bk) & 1)) || (bv && (reinterpret_cast<uintptr_t>(bv) & 1)))
+        return fail(MOT_ERR_MISALIGNED, "bias pointers must be 2-byte aligned");
+    const size_t n_tok = (size_t)s->B * s->T, d_kv = (size_t)s->H_tgt * s->D_tgt;
+    const size_t act_bytes = (size_t)s->L * n_tok * s->d_act * 2, kv_bytes = (size_t)s->L * n_tok * d_kv * 2;
+    if (overlaps(dst_k, kv_bytes, dst_v, kv_bytes) || overlaps(dst_k, kv_bytes, act, act_bytes) ||
+        overlaps(dst_v, kv_bytes, act, act_bytes))
+        return fail(MOT_ERR_BAD_SHAPE, "destination caches overlap each other or the activation");
+    static thread_local ProjProblem p;
+    memset(&p, 0, sizeof p);
+    p.act = act; p.wk = wk; p.bk = bk; p.wv = wv; p.bv = bv; p.dst_k = dst_k; p.dst_v = dst_v;
+    p.B = s->B; p.T = s->T; p.n_tok = (int32_t)n_tok; p.d_act = s->d_act; p.d_kv = (int32_t)d_kv;
+    p.H_tgt = s->H_tgt; p.D_tgt = s->D_tgt; p.dst_layout = s->dst_layout;
+    int n = 0;
+    for (int l = 0; l < s->L; ++l)
+        if (!layer_map || layer_map[l] >= 0) p.layers[n++] = l;
+    hipError_t e = launch_bf16_project(p, n, stream);
     if (e != hipSuccess) return fail(MOT_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
     return MOT_OK;
 }

@@ -55,10 +55,25 @@ struct Problem {
     int32_t B, T, H_src, D_src, H_tgt, D_tgt, E, top_k, hidden;
     int32_t d_in, d_out, n_tok, n_tok_pad;   // n_tok_pad: n_tok rounded up to 128
     int32_t src_layout, dst_layout, act;
+    int32_t streams;      // 2: keys and values; 1: one activation stream (src[0] -> dst[0])
     float* gates;         // workspace: [n_units_total][n_tok_pad][E] fp32
     void* hbuf;           // workspace: [group][n_tok_pad][E*hidden] (layout per path)
     Routing rt;           // routed path only
 };
+
+// Key/value restoration (MoT-h): K and V caches from a translated activation.
+struct ProjProblem {
+    const void* act;      // [L][B*T][d_act]
+    const void* wk;       // [L][d_kv][d_act]
+    const void* bk;       // [L][d_kv] or null
+    const void* wv;
+    const void* bv;
+    void* dst_k;          // [L] x dst layout, d_kv = H_tgt * D_tgt per token
+    void* dst_v;
+    int32_t B, T, n_tok, d_act, d_kv, H_tgt, D_tgt, dst_layout;
+    int32_t layers[kMaxUnits];   // layers to restore, in launch order
+};
+hipError_t launch_bf16_project(const ProjProblem& p, int n_layers, hipStream_t stream);
 
 // Kernel launchers (each enqueues on `stream`; return hipGetLastError()).
 hipError_t launch_router(const Problem& p, const UnitTab& ut, bool bf16, hipStream_t stream);

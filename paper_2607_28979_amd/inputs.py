@@ -130,3 +130,34 @@ def sample_rows(n_tok: int, n: int, seed: int) -> np.ndarray:
     rng = np.random.Generator(np.random.PCG64(10_000 + seed))
     mid = rng.choice(np.arange(1, n_tok - 1), size=max(0, n - 2), replace=False)
     return np.unique(np.concatenate([[0, n_tok - 1], mid]).astype(np.int64))
+
+
+def projection_weights(L: int, d_act: int, d_kv: int, seed: int, dtype: str = "bf16"):
+    """Stand-in target key/value projections for the activation variant:
+    W^K, W^V [L][d_kv][d_act] Xavier-uniform U(+-sqrt(6/(d_act+d_kv))) and
+    b^K, b^V [L][d_kv] U(+-1/sqrt(d_act)), drawn in that order per layer
+    (W^K, b^K, W^V, b^V), from PCG64(20_000 + seed); rounded like generate()."""
+    rng = np.random.Generator(np.random.PCG64(20_000 + seed))
+    wk = np.empty((L, d_kv, d_act), np.float32)
+    wv = np.empty((L, d_kv, d_act), np.float32)
+    bk = np.empty((L, d_kv), np.float32)
+    bv = np.empty((L, d_kv), np.float32)
+    for l in range(L):
+        _uniform(rng, wk[l], math.sqrt(6.0 / (d_act + d_kv)))
+        _uniform(rng, bk[l], 1.0 / math.sqrt(d_act))
+        _uniform(rng, wv[l], math.sqrt(6.0 / (d_act + d_kv)))
+        _uniform(rng, bv[l], 1.0 / math.sqrt(d_act))
+    if dtype == "bf16":
+        for a in (wk, bk, wv, bv):
+            round_to_bf16(a)
+    return wk, bk, wv, bv
+
+
+def activations(L: int, B: int, T: int, d_act: int, seed: int, dtype: str = "bf16") -> np.ndarray:
+    """Intermediate activation rows [L][B][T][d_act] ~ N(0, 1) from
+    PCG64(30_000 + seed), rounded like generate()."""
+    rng = np.random.Generator(np.random.PCG64(30_000 + seed))
+    a = rng.standard_normal((L, B, T, d_act), dtype=np.float32)
+    if dtype == "bf16":
+        round_to_bf16(a)
+    return a

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert mb.abi_version() == 1
+    assert mb.abi_version() == 2
 
 
 def test_status_strings(lib):
@@ -134,8 +134,75 @@ def test_workspace_bytes(lib):
         mb.workspace_bytes(_shapes(E=0))
 
 
-def test_header_struct_layout_matches_binding():
-    # mot_shapes: 16 int32 fields, then a pointer and a size_t
-    assert ctypes.sizeof(mb._Shapes) == 16 * 4 + 8 + 8
-    txt = open(HEADER).read()
-    assert "int32_t dtype, src_layout, dst_layout, act, algo;" in txt
+def test_streams_field(lib):
+    """streams selects one activation stream (MoT-h) or keys and values."""
+    _expect("MOT_ERR_BAD_SHAPE", shapes=_shapes(streams=3))
+    _expect("MOT_ERR_BAD_SHAPE", shapes=_shapes(streams=-1))
+    one, two = (mb.workspace_bytes(_shapes(algo=mb.ALGO_UNFUSED, streams=n)) for n in (1, 2))
+    assert 0 < one < two
+    _expect("MOT_ERR_NULL_ARG", shapes=_shapes(streams=2), ptrs={"src_v": None})
+
+
+def _restore(ptrs=None, lm=None, **kw):
+    base = dict(L=2, B=1, T=8, d_act=128, H_tgt=2, D_tgt=64, dtype=mb.MOT_BF16, dst_layout=0)
+    base.update(kw)
+    p = dict(act=FAKE, wk=FAKE + (1 << 30), bk=None, wv=FAKE + (2 << 30), bv=None,
+             dst_k=FAKE + (3 << 30), dst_v=FAKE + (4 << 30))
+    p.update(ptrs or {})
+    c = mb._RestoreShapes(*[base[k] for k in ("L", "B", "T", "d_act", "H_tgt", "D_tgt", "dtype",
+                                              "dst_layout")])
+    arr = None if lm is None else np.ascontiguousarray(lm, dtype=np.int32)
+    mb._check(mb.load_library().mot_restore_kv(p["act"], None if arr is None else arr.ctypes.data,
+                                               p["wk"], p["bk"], p["wv"], p["bv"], p["dst_k"], p["dst_v"],
+                                               ctypes.byref(c), None))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(L=0), "MOT_ERR_BAD_SHAPE"), (dict(L=257), "MOT_ERR_BAD_SHAPE"), (dict(T=-1), "MOT_ERR_BAD_SHAPE"),
+    (dict(d_act=0), "MOT_ERR_BAD_SHAPE"), (dict(dst_layout=2), "MOT_ERR_BAD_SHAPE"),
+    (dict(dtype=5), "MOT_ERR_BAD_SHAPE"), (dict(dtype=mb.MOT_F32), "MOT_ERR_UNSUPPORTED"),
+    (dict(d_act=96), "MOT_ERR_UNSUPPORTED"), (dict(D_tgt=12), "MOT_ERR_UNSUPPORTED")])
+def test_restore_rejects_shapes(lib, kw, code):
+    with pytest.raises(mb.MotError) as e:
+        _restore(**kw)
+    assert e.value.name == code, str(e.value)
+
+
+@pytest.mark.parametrize("ptrs,code", [
+    (dict(act=None), "MOT_ERR_NULL_ARG"), (dict(dst_v=None), "MOT_ERR_NULL_ARG"),
+    (dict(wk=FAKE + (1 << 30) + 8), "MOT_ERR_MISALIGNED"), (dict(bv=FAKE + 1), "MOT_ERR_MISALIGNED"),
+    (dict(dst_v=FAKE + (3 << 30) + 256), "MOT_ERR_BAD_SHAPE"),      # dst_v inside dst_k
+    (dict(dst_k=FAKE + 64), "MOT_ERR_BAD_SHAPE")])                  # dst_k inside act
+def test_restore_rejects_pointers(lib, ptrs, code):
+    with pytest.raises(mb.MotError) as e:
+        _restore(ptrs=ptrs)
+    assert e.value.name == code, str(e.value)
+
+
+def test_restore_empty_is_a_no_op(lib):
+    _restore(T=0, ptrs=dict(act=None, dst_k=None))     # nothing to do: no pointer is read
+
+
+def test_header_struct_layout_matches_binding(tmp_path):
+    """sizeof and every field offset of the header's structs, as a C compiler
+    lays them out, equal the ctypes mirrors in the binding."""
+    import subprocess
+    structs = {"mot_shapes": mb._Shapes, "mot_restore_shapes": mb._RestoreShapes,
+               "mot_translator_weights": mb._TW, "mot_router_weights": mb._RW}
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "mot.h"', "int main(void) {"]
+    for cname, cls in structs.items():
+        lines.append('printf("%s size %%zu\\n", sizeof(%s));' % (cname, cname))
+        for f, _ in cls._fields_:
+            lines.append('printf("%s %s %%zu\\n", offsetof(%s, %s));' % (cname, f, cname, f))
+    lines.append("return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-D__HIP_PLATFORM_AMD__", "-I", os.path.dirname(HEADER),
+                    "-I", "/opt/rocm/include", str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out if l.strip()}
+    for cname, cls in structs.items():
+        assert got[(cname, "size")] == ctypes.sizeof(cls), cname
+        for f, _ in cls._fields_:
+            assert got[(cname, f)] == getattr(cls, f).offset, (cname, f)

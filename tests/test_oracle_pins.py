@@ -14,7 +14,9 @@ answer is known independently of the oracle's own code:
 * exact GELU against tabulated normal-CDF values;
 * renormalised Top-K with a lower-index tie-break;
 * token and translator permutation invariance, layout permutations;
-* depth-ratio channel map (App. C.3) against exact rational arithmetic.
+* depth-ratio channel map (App. C.3) against exact rational arithmetic;
+* MoT-h key/value restoration (App. C.5): hand-computed values, identity
+  projection = head split, float64 matrix product, identity-translator chain.
 
 Each case is built so that a dropped bias, a transposed weight, a wrong
 softmax sign or a wrong cache stride changes the answer.
@@ -343,3 +345,100 @@ def test_depth_ratio_map(oracle_built, L_src, L_tgt):
         assert np.array_equal(got, np.arange(L_tgt))
     if L_tgt >= L_src:                 # every source layer feeds some target layer
         assert set(got.tolist()) == set(range(L_src))
+
+
+# ---------------------------------------------------------------------------
+# MoT-h key/value restoration (App. C.5): K = W^K a + b^K, V = W^V a + b^V
+# ---------------------------------------------------------------------------
+
+def test_restore_hand_computed_values(oracle_built):
+    """Two tokens, two channels, values worked out by hand:
+    W^K = [[1, 2], [3, 4]], b^K = [1, -1]; W^V swaps the channels, b^V = [0.5, 0].
+    a = (5, 6): K = (18, 38), V = (6.5, 5);   a = (-1, 2): K = (4, 4), V = (2.5, -1)."""
+    from oracle import oracle_restore_kv
+    act = np.array([[[[5, 6], [-1, 2]]]], np.float32)          # [L=1][B=1][T=2][2]
+    wk = np.array([[[1, 2], [3, 4]]], np.float32)
+    bk = np.array([[1, -1]], np.float32)
+    wv = np.array([[[0, 1], [1, 0]]], np.float32)
+    bv = np.array([[0.5, 0]], np.float32)
+    k, v = oracle_restore_kv(act, None, wk, bk, wv, bv, B=1, T=2, H_tgt=1, D_tgt=2)
+    assert k.reshape(2, 2).tolist() == [[18, 38], [4, 4]]
+    assert v.reshape(2, 2).tolist() == [[6.5, 5], [2.5, -1]]
+    # two heads of one channel each, head-major target layout: the same numbers
+    # land at [b][h][t][0]
+    k2, v2 = oracle_restore_kv(act, None, wk, bk, wv, bv, B=1, T=2, H_tgt=2, D_tgt=1, dst_layout=1)
+    assert k2.reshape(2, 2).tolist() == [[18, 4], [38, 4]]
+    assert v2.reshape(2, 2).tolist() == [[6.5, 2.5], [5, -1]]
+
+
+@pytest.mark.parametrize("layout", [0, 1])
+def test_restore_identity_projection_is_head_split(oracle_built, layout):
+    """W^K = W^V = I and no bias: K and V are the activation rows cut into
+    heads, exactly, in the requested layout."""
+    from oracle import oracle_restore_kv
+    rng = np.random.default_rng(5)
+    L, B, T, H, D = 2, 2, 3, 4, 8
+    act = rng.standard_normal((L, B, T, H * D)).astype(np.float32)
+    eye = np.broadcast_to(np.eye(H * D, dtype=np.float32), (L, H * D, H * D))
+    k, v = oracle_restore_kv(act, None, eye, None, eye, None, B=B, T=T, H_tgt=H, D_tgt=D,
+                             dst_layout=layout)
+    want = act.astype(np.float64).reshape(L, B, T, H, D)
+    if layout == 1:
+        want = want.transpose(0, 1, 3, 2, 4)
+    assert np.array_equal(k, want) and np.array_equal(v, want)
+
+
+def test_restore_matches_matmul_and_skips_unmapped_layers(oracle_built):
+    """Against numpy's float64 matrix product; layers with a negative map
+    entry keep what the destination held."""
+    from oracle import oracle_restore_kv
+    rng = np.random.default_rng(11)
+    L, B, T, d_act, H, D = 3, 2, 5, 24, 2, 4
+    act = rng.standard_normal((L, B, T, d_act)).astype(np.float32)
+    wk = rng.standard_normal((L, H * D, d_act)).astype(np.float32)
+    wv = rng.standard_normal((L, H * D, d_act)).astype(np.float32)
+    bk = rng.standard_normal((L, H * D)).astype(np.float32)
+    bv = rng.standard_normal((L, H * D)).astype(np.float32)
+    lm = np.array([0, -1, 2], np.int32)
+    keep = np.full((L, B, T, H, D), 7.0)
+    k, v = oracle_restore_kv(act, lm, wk, bk, wv, bv, B=B, T=T, H_tgt=H, D_tgt=D,
+                             dst_k=keep, dst_v=keep)
+    a64 = act.astype(np.float64)
+    for l in range(L):
+        if lm[l] < 0:
+            assert (k[l] == 7.0).all() and (v[l] == 7.0).all()
+            continue
+        rk = np.einsum("btc,oc->bto", a64[l], wk[l].astype(np.float64)) + bk[l]
+        rv = np.einsum("btc,oc->bto", a64[l], wv[l].astype(np.float64)) + bv[l]
+        np.testing.assert_allclose(k[l].reshape(B, T, H * D), rk, rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(v[l].reshape(B, T, H * D), rv, rtol=1e-12, atol=1e-12)
+
+
+def test_moth_chain_with_identity_translator(oracle_built):
+    """MoT-h end to end with one identity translator over the activation
+    (E = 1, W1 = W2 = I, identity activation, no bias): restoring from the
+    translated activation equals projecting the mapped source activation,
+    K[j] = W^K[j] a_src[map(j)] (depth-ratio map 2 -> 3)."""
+    from oracle import oracle_restore_kv
+    rng = np.random.default_rng(17)
+    L_src, L_tgt, B, T, d = 2, 3, 1, 4, 8
+    H, D = 2, 2
+    a_src = rng.standard_normal((L_src, B, T, 1, d)).astype(np.float32)
+    eye = np.eye(d, dtype=np.float32)
+    w1 = np.broadcast_to(eye, (L_tgt, 2, 1, d, d)).copy()
+    w2 = w1.copy()
+    wr = np.zeros((L_tgt, 2, 1, d), np.float32)
+    dims = OracleDims(L_src=L_src, L_tgt=L_tgt, B=B, T=T, H_src=1, D_src=d, H_tgt=1, D_tgt=d,
+                      E=1, hidden=d, act=1)
+    lm = oracle_depth_ratio_map(L_src, L_tgt)
+    a_tgt, _ = oracle_translate(dims, a_src, a_src, lm, w1, None, w2, None, wr, None)
+    wk = rng.standard_normal((L_tgt, H * D, d)).astype(np.float32)
+    wv = rng.standard_normal((L_tgt, H * D, d)).astype(np.float32)
+    k, v = oracle_restore_kv(a_tgt.reshape(L_tgt, B, T, d), None, wk, None, wv, None,
+                             B=B, T=T, H_tgt=H, D_tgt=D)
+    for j in range(L_tgt):
+        a = a_src[lm[j]].reshape(B * T, d).astype(np.float64)
+        np.testing.assert_allclose(k[j].reshape(B * T, H * D), a @ wk[j].T.astype(np.float64),
+                                   rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(v[j].reshape(B * T, H * D), a @ wv[j].T.astype(np.float64),
+                                   rtol=1e-12, atol=1e-12)
