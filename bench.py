@@ -67,6 +67,10 @@ def main():
                          "the auto path is the routed Top-K kernel")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample rows (0 = auto)")
+    ap.add_argument("--moth", action="store_true",
+                    help="time the activation variant MoT-h instead: one activation stream per "
+                         "layer translated (Qwen2.5-1.5B -> 7B widths 1536 -> 3584), then the "
+                         "target K/V restored through its key/value projections")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain device copy of MIB MiB (a known-size "
                          "reference for the HBM byte counters of a profiler run)")
@@ -77,6 +81,9 @@ def main():
               "by token), and this build runs on a single MI355X; --gpus must be 1.",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.moth:
+        return bench_moth(args)
 
     import torch
     from paper_2607_28979_amd import binding as mb
@@ -218,6 +225,126 @@ def cpu_baseline(w, inp, lm, rows):
     log("cpu oracle: %d rows x %d units in %.2f s on %d threads" % (rows, len(units), dt, threads))
     return {"value": round(rows / dt, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": "first %d of %d tokens, all %d units (K and V of every layer), fp64"
+                      % (rows, w.n_tok, len(units)),
+            "seconds": round(dt, 2)}
+
+
+def bench_moth(args):
+    """MoT-h (App. C.5): one step = mot_translate over the activation stream of
+    every layer, then mot_restore_kv of every layer's keys and values."""
+    import torch
+    from paper_2607_28979_amd import binding as mb
+    from paper_2607_28979_amd.configs import MOTH
+    from paper_2607_28979_amd.inputs import bf16_bits, generate, projection_weights
+
+    w = MOTH.act
+    if args.top_k:
+        w = w.with_(top_k=args.top_k)
+    torch.cuda.set_device(0)
+    t0 = time.time()
+    inp = generate(w)
+    wk, bk, wv, bv = projection_weights(w.L_tgt, w.d_out, MOTH.d_kv, seed=w.seed)
+    log("inputs generated in %.1f s" % (time.time() - t0))
+
+    def dev(a):
+        return torch.from_numpy(bf16_bits(a).view(np.int16)).cuda().view(torch.bfloat16)
+
+    d = {n: dev(getattr(inp, n)) for n in ("src_k", "w1", "b1", "w2", "b2", "wr", "br")}
+    p = {n: dev(a) for n, a in (("wk", wk), ("bk", bk), ("wv", wv), ("bv", bv))}
+    act = torch.empty((w.L_tgt, w.B, w.T, 1, w.d_out), dtype=torch.bfloat16, device="cuda")
+    kv_shape = (w.L_tgt, w.B, w.T, MOTH.kv_heads, MOTH.head_dim)
+    dk = torch.empty(kv_shape, dtype=torch.bfloat16, device="cuda")
+    dv = torch.empty(kv_shape, dtype=torch.bfloat16, device="cuda")
+    lm = (np.arange(w.L_tgt, dtype=np.int32) if w.layer_map == "identity"
+          else mb.depth_ratio_map(w.L_src, w.L_tgt))
+    shapes = mb.Shapes.from_workload(w, algo=args.algo)
+    ws_bytes = mb.workspace_bytes(shapes)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device="cuda") if ws_bytes else None
+    log("workspace %.2f GB" % (ws_bytes / 1e9))
+
+    def translate():
+        mb.translate(d["src_k"], None, lm, d["w1"], d["b1"], d["w2"], d["b2"], d["wr"], d["br"],
+                     act, None, shapes, workspace=ws)
+
+    def restore():
+        mb.restore_kv(act, None, p["wk"], p["bk"], p["wv"], p["bv"], dk, dv, L=w.L_tgt, B=w.B,
+                      T=w.T, d_act=w.d_out, H_tgt=MOTH.kv_heads, D_tgt=MOTH.head_dim)
+
+    for _ in range(args.warmup):
+        translate()
+        restore()
+    torch.cuda.synchronize()
+    log("warmup done (%d steps)" % args.warmup)
+    stream = torch.cuda.current_stream()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_begin = time.perf_counter()
+    for k in range(args.steps):
+        ev[k][0].record(stream)
+        translate()
+        ev[k][1].record(stream)
+        restore()
+        ev[k][2].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_begin
+    tr_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    rs_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    ms_per_step = wall * 1e3 / args.steps
+    log("timed %d steps: wall %.3f ms/step, translate %.3f ms, restore %.3f ms"
+        % (args.steps, ms_per_step, tr_ms, rs_ms))
+    tr_flops = w.gemm_flops()
+    rs_flops = MOTH.restore_flops()
+    peak = PEAK_TFLOPS["bf16"]
+    tr_tf = tr_flops / (tr_ms / 1e3) / 1e12
+    rs_tf = rs_flops / (rs_ms / 1e3) / 1e12
+    cpu = None if args.no_cpu_baseline else cpu_baseline_moth(w, inp, lm, (wk, bk, wv, bv),
+                                                              args.cpu_rows)
+    out = {
+        "metric": "translated and restored KV tokens/sec (all layers, MoT-h) Qwen2.5-1.5B→7B",
+        "value": round(w.n_tok / (ms_per_step / 1e3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded numpy; activation widths of the model pair)",
+        "config": {"workload": w.name, "L_src": w.L_src, "L_tgt": w.L_tgt, "B": w.B, "T": w.T,
+                   "d_act_src": w.d_in, "hidden": w.hidden, "d_act_tgt": w.d_out, "E": w.E,
+                   "top_k": w.top_k or w.E, "kv_heads": MOTH.kv_heads,
+                   "head_dim": MOTH.head_dim, "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "kernel": "mot_translate (streams = 1)",
+                     "achieved": round(tr_tf, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(tr_tf / peak, 4), "traffic": None,
+                     "alg_flops_per_launch": tr_flops, "ms": round(tr_ms, 3)},
+        "restore": {"kernel": "k_bf16_project", "achieved": round(rs_tf, 2), "peak": peak,
+                    "unit": "TFLOP/s", "frac": round(rs_tf / peak, 4), "ms": round(rs_ms, 3),
+                    "alg_flops_per_launch": rs_flops},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline_moth(w, inp, lm, proj, rows):
+    """The CPU oracle on the first `rows` tokens of every layer: translation of
+    the activation stream, then the key/value restoration of those rows."""
+    from oracle import OracleDims, oracle_restore_kv, oracle_rows
+    wk, bk, wv, bv = proj
+    threads = min(16, os.cpu_count() or 1)
+    od = OracleDims(L_src=w.L_src, L_tgt=w.L_tgt, B=w.B, T=w.T, H_src=w.H_src, D_src=w.D_src,
+                    H_tgt=w.H_tgt, D_tgt=w.D_tgt, E=w.E, hidden=w.hidden, top_k=w.top_k,
+                    streams=1)
+    units = [(j, 0) for j in range(w.L_tgt) if lm[j] >= 0]
+    if rows <= 0:
+        rows = int(max(1, min(w.n_tok, 60e9 * threads / (w.gemm_flops() / w.n_tok))))
+    t0 = time.perf_counter()
+    a = oracle_rows(od, inp.src_k, None, lm, inp.w1, inp.b1, inp.w2, inp.b2, inp.wr, inp.br,
+                    units=units, rows=np.arange(rows, dtype=np.int64), nthreads=threads)
+    from paper_2607_28979_amd.configs import MOTH
+    oracle_restore_kv(a.reshape(len(units), 1, rows, w.d_out), None, wk, bk, wv, bv, B=1, T=rows,
+                      H_tgt=MOTH.kv_heads, D_tgt=MOTH.head_dim)
+    dt = time.perf_counter() - t0
+    log("cpu oracle: %d rows x %d layers in %.2f s on %d threads" % (rows, len(units), dt, threads))
+    return {"value": round(rows / dt, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": "first %d of %d tokens, all %d layers (translation + K/V restoration), fp64"
                       % (rows, w.n_tok, len(units)),
             "seconds": round(dt, 2)}
 

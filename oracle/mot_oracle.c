@@ -11,7 +11,9 @@
  * Sec. 2.1 "Problem Setup", paragraphs "Translation" and "Communication"):
  *
  *   for every channel (source layer i -> target layer j), i = layer_map[j] >= 0,
- *   for X in {K, V} (keys and values translated independently, App. C.2),
+ *   for X in {K, V} (keys and values translated independently, App. C.2;
+ *                   streams = 1: the single intermediate-activation stream
+ *                   of the MoT-h variant, App. C.5),
  *   for every context token u = (b, t):
  *     z_u            = the source cache row of token u in layer i, flattened
  *                      head-major (index h*D_src + d)
@@ -61,6 +63,8 @@ typedef struct {
     int32_t src_layout;     /* 0: [L][B][T][H][D]   1: [L][B][H][T][D]      */
     int32_t dst_layout;     /* same encoding for the target cache           */
     int32_t act;            /* 0: exact-erf GELU    1: identity             */
+    int32_t streams;        /* 2: keys and values; 1: one activation stream
+                               (MoT-h, App. C.5): weights [L_tgt][streams][E] */
 } mot_oracle_dims;
 
 enum { OR_OK = 0, OR_BAD_ARG = 1, OR_NO_MEM = 2 };
@@ -102,7 +106,7 @@ static void translate_row(const mot_oracle_dims* s, const oracle_weights* w,
     const int32_t d_in = s->H_src * s->D_src;
     const int32_t d_out = s->H_tgt * s->D_tgt;
     const int32_t E = s->E, Hd = s->hidden;
-    const size_t unit = (size_t)j * 2 + x;
+    const size_t unit = (size_t)j * s->streams + x;
 
     /* gate logits l_m = Wr z + br */
     for (int32_t m = 0; m < E; ++m) {
@@ -252,6 +256,7 @@ static int check_dims(const mot_oracle_dims* s, const int32_t* layer_map)
     if ((s->src_layout != 0 && s->src_layout != 1) || (s->dst_layout != 0 && s->dst_layout != 1))
         return OR_BAD_ARG;
     if (s->act != 0 && s->act != 1) return OR_BAD_ARG;
+    if (s->streams != 1 && s->streams != 2) return OR_BAD_ARG;
     for (int32_t j = 0; j < s->L_tgt; ++j)
         if (layer_map[j] >= s->L_src) return OR_BAD_ARG;
     return OR_OK;
@@ -287,7 +292,8 @@ int mot_oracle_translate(const float* src_k, const float* src_v, const int32_t* 
 {
     int rc = check_dims(s, layer_map);
     if (rc) return rc;
-    if (!src_k || !src_v || !w1 || !w2 || !wr || !dst_k || !dst_v) return OR_BAD_ARG;
+    if (!src_k || !w1 || !w2 || !wr || !dst_k) return OR_BAD_ARG;
+    if (s->streams == 2 && (!src_v || !dst_v)) return OR_BAD_ARG;
     oracle_weights w = {w1, b1, w2, b2, wr, br};
     int32_t* uj = (int32_t*)malloc(sizeof(int32_t) * 2 * s->L_tgt);
     int32_t* ux = (int32_t*)malloc(sizeof(int32_t) * 2 * s->L_tgt);
@@ -295,7 +301,7 @@ int mot_oracle_translate(const float* src_k, const float* src_v, const int32_t* 
     int32_t nu = 0;
     for (int32_t j = 0; j < s->L_tgt; ++j)
         if (layer_map[j] >= 0)
-            for (int32_t x = 0; x < 2; ++x) { uj[nu] = j; ux[nu] = x; ++nu; }
+            for (int32_t x = 0; x < s->streams; ++x) { uj[nu] = j; ux[nu] = x; ++nu; }
     oracle_job jb;
     memset(&jb, 0, sizeof jb);
     jb.s = s; jb.w = &w; jb.src_k = src_k; jb.src_v = src_v; jb.layer_map = layer_map;
@@ -320,10 +326,10 @@ int mot_oracle_rows(const float* src_k, const float* src_v, const int32_t* layer
 {
     int rc = check_dims(s, layer_map);
     if (rc) return rc;
-    if (!src_k || !src_v || !w1 || !w2 || !wr || !out || !unit_j || !unit_x || !rows)
-        return OR_BAD_ARG;
+    if (!src_k || !w1 || !w2 || !wr || !out || !unit_j || !unit_x || !rows) return OR_BAD_ARG;
+    if (s->streams == 2 && !src_v) return OR_BAD_ARG;
     for (int32_t u = 0; u < n_units; ++u) {
-        if (unit_j[u] < 0 || unit_j[u] >= s->L_tgt || (unit_x[u] != 0 && unit_x[u] != 1))
+        if (unit_j[u] < 0 || unit_j[u] >= s->L_tgt || unit_x[u] < 0 || unit_x[u] >= s->streams)
             return OR_BAD_ARG;
         if (layer_map[unit_j[u]] < 0) return OR_BAD_ARG;
     }

@@ -8,6 +8,8 @@ Array conventions (all numpy, C-contiguous):
   w2 : float32 [L_tgt][2][E][d_out][hidden]    b2 : [L_tgt][2][E][d_out]
   wr : float32 [L_tgt][2][E][d_in]             br : [L_tgt][2][E]
   index 1 of every weight is 0 = keys, 1 = values; biases may be None.
+  With dims.streams = 1 (the MoT-h activation stream) index 1 has size 1,
+  src_v may be None and the returned dst_v is None.
 """
 from __future__ import annotations
 
@@ -42,7 +44,7 @@ def build_oracle(force: bool = True) -> str:
 class _Dims(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "L_src", "L_tgt", "B", "T", "H_src", "D_src", "H_tgt", "D_tgt", "E",
-        "top_k", "hidden", "src_layout", "dst_layout", "act")]
+        "top_k", "hidden", "src_layout", "dst_layout", "act", "streams")]
 
 
 @dataclass
@@ -61,6 +63,7 @@ class OracleDims:
     src_layout: int = 0     # 0 = BTHD, 1 = BHTD
     dst_layout: int = 0
     act: int = 0            # 0 = exact-erf GELU, 1 = identity
+    streams: int = 2        # 2 = keys and values; 1 = one activation stream (MoT-h)
 
     @property
     def d_in(self) -> int:
@@ -73,7 +76,7 @@ class OracleDims:
     def _c(self) -> _Dims:
         return _Dims(self.L_src, self.L_tgt, self.B, self.T, self.H_src, self.D_src,
                      self.H_tgt, self.D_tgt, self.E, self.top_k or self.E, self.hidden,
-                     self.src_layout, self.dst_layout, self.act)
+                     self.src_layout, self.dst_layout, self.act, self.streams)
 
 
 _lib = None
@@ -127,6 +130,8 @@ def oracle_translate(dims: OracleDims, src_k, src_v, layer_map, w1, b1, w2, b2, 
         dst_v = np.full(shape, np.nan)
     dst_k = np.ascontiguousarray(dst_k, dtype=np.float64)
     dst_v = np.ascontiguousarray(dst_v, dtype=np.float64)
+    if dims.streams == 1:
+        dst_v = None
     c = dims._c()
     rc = lib.mot_oracle_translate(*[_ptr(a) for a in arrs[:2]], _ptr(lm),
                                   *[_ptr(a) for a in arrs[2:]], _ptr(dst_k), _ptr(dst_v),

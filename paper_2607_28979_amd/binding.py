@@ -86,7 +86,7 @@ class Shapes:
     def from_workload(cls, w, **kw) -> "Shapes":
         return cls(w.L_src, w.L_tgt, w.B, w.T, w.H_src, w.D_src, w.H_tgt, w.D_tgt, w.E, w.hidden,
                    dtype=MOT_F32 if w.dtype == "f32" else MOT_BF16, src_layout=w.src_layout,
-                   dst_layout=w.dst_layout, **{"top_k": w.top_k, **kw})
+                   dst_layout=w.dst_layout, **{"top_k": w.top_k, "streams": w.streams, **kw})
 
 
 _lib = None

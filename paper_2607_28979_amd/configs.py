@@ -41,6 +41,7 @@ class Workload:
     src_layout: int = 0
     dst_layout: int = 0
     top_k: int = 0                   # translators used per token; 0 = all E (dense)
+    streams: int = 2                 # 2 = keys and values; 1 = one activation stream (MoT-h)
 
     @property
     def d_in(self) -> int:
@@ -55,7 +56,7 @@ class Workload:
         return self.B * self.T
 
     def units(self) -> int:
-        return 2 * self.L_tgt
+        return self.streams * self.L_tgt
 
     def gemm_flops(self) -> float:
         """Algorithmic multiply-add flops of one full translation: router,
@@ -71,7 +72,7 @@ class Workload:
         weights read once, the translated cache written once."""
         es = 4 if self.dtype == "f32" else 2
         n_src_layers = self.L_src if self.layer_map != "identity" else min(self.L_src, self.L_tgt)
-        src = 2 * n_src_layers * self.n_tok * self.d_in * es
+        src = self.streams * n_src_layers * self.n_tok * self.d_in * es
         w = self.units() * self.E * (self.hidden * self.d_in + self.hidden + self.d_out * self.hidden
                                      + self.d_out + self.d_in + 1) * es
         dst = self.units() * self.n_tok * self.d_out * es
@@ -99,6 +100,31 @@ BY_NAME = {w.name: w for w in WORKLOADS}
 
 # the headline workload: Qwen2.5-1.5B -> Qwen2.5-7B, B=8, T=4096
 HEADLINE = WORKLOADS[3]
+
+
+@dataclass(frozen=True)
+class MothWorkload:
+    """The activation variant MoT-h (App. C.5): each layer's intermediate
+    activation (width d_model) is translated as one stream, then the target's
+    key and value projections (kv_heads x head_dim each) restore its cache."""
+    act: Workload
+    kv_heads: int
+    head_dim: int
+
+    @property
+    def d_kv(self) -> int:
+        return self.kv_heads * self.head_dim
+
+    def restore_flops(self) -> float:
+        return 2.0 * 2 * self.d_kv * self.act.d_out * self.act.n_tok * self.act.L_tgt
+
+
+# Qwen2.5-1.5B (d_model 1536) -> Qwen2.5-7B (d_model 3584, 4 KV heads of 128),
+# 28 -> 28 layers, B=8, T=4096; translator width and experts as the headline
+MOTH = MothWorkload(
+    Workload("qwen2.5-1.5b->qwen2.5-7b activations", "bf16", L_src=28, L_tgt=28, B=8, T=4096,
+             H_src=1, D_src=1536, H_tgt=1, D_tgt=3584, E=8, hidden=2048, seed=5, streams=1),
+    kv_heads=4, head_dim=128)
 
 
 def small_variant(w: Workload, L_src: Optional[int] = None, L_tgt: Optional[int] = None,

@@ -37,7 +37,7 @@ from .configs import Workload
 @dataclass
 class Inputs:
     src_k: np.ndarray      # float32, layout per workload.src_layout
-    src_v: np.ndarray
+    src_v: Optional[np.ndarray]   # None for a single activation stream
     w1: np.ndarray         # [L_tgt][2][E][hidden][d_in]
     b1: np.ndarray         # [L_tgt][2][E][hidden]
     w2: np.ndarray         # [L_tgt][2][E][d_out][hidden]
@@ -74,16 +74,21 @@ def _uniform(rng: np.random.Generator, out: np.ndarray, bound: float) -> None:
     out -= np.float32(bound)
 
 
-def generate(w: Workload, with_bias: bool = True) -> Inputs:
+def generate(w: Workload, with_bias: bool = True, streams: Optional[int] = None) -> Inputs:
+    """streams (default: the workload's) = 1 draws only the key-side arrays
+    (the one activation stream of the MoT-h variant): src_v is None, weights
+    have size 1 on axis 1, and the value-side draws (items 2 and 4, the
+    x = values weights) are skipped."""
+    streams = streams or w.streams
     rng = np.random.Generator(np.random.PCG64(w.seed))
     shp = (w.L_src, w.B, w.T, w.H_src, w.D_src)
     src_k = rng.standard_normal(shp, dtype=np.float32)
-    src_v = rng.standard_normal(shp, dtype=np.float32)
+    src_v = rng.standard_normal(shp, dtype=np.float32) if streams == 2 else None
     d_in, d_out, E, Hd = w.d_in, w.d_out, w.E, w.hidden
     if w.key_sigma > 0:
         s = np.exp(np.float32(w.key_sigma) * rng.standard_normal((w.L_src, d_in), dtype=np.float32))
         src_k *= s.reshape(w.L_src, 1, 1, w.H_src, w.D_src)
-    if w.val_sigma > 0:
+    if w.val_sigma > 0 and streams == 2:
         s = np.exp(np.float32(w.val_sigma) * rng.standard_normal((w.L_src, d_in), dtype=np.float32))
         src_v *= s.reshape(w.L_src, 1, 1, w.H_src, w.D_src)
     if w.key_outlier_frac > 0 and w.T > 0:
@@ -94,14 +99,14 @@ def generate(w: Workload, with_bias: bool = True) -> Inputs:
             src_k[:, b, pos] *= np.float32(w.key_outlier_mult)
 
     L = w.L_tgt
-    w1 = np.empty((L, 2, E, Hd, d_in), np.float32)
-    b1 = np.empty((L, 2, E, Hd), np.float32)
-    w2 = np.empty((L, 2, E, d_out, Hd), np.float32)
-    b2 = np.empty((L, 2, E, d_out), np.float32)
-    wr = np.empty((L, 2, E, d_in), np.float32)
-    br = np.empty((L, 2, E), np.float32)
+    w1 = np.empty((L, streams, E, Hd, d_in), np.float32)
+    b1 = np.empty((L, streams, E, Hd), np.float32)
+    w2 = np.empty((L, streams, E, d_out, Hd), np.float32)
+    b2 = np.empty((L, streams, E, d_out), np.float32)
+    wr = np.empty((L, streams, E, d_in), np.float32)
+    br = np.empty((L, streams, E), np.float32)
     for j in range(L):
-        for x in range(2):
+        for x in range(streams):
             _uniform(rng, wr[j, x], math.sqrt(6.0 / (d_in + E)))
             _uniform(rng, br[j, x], 1.0 / math.sqrt(d_in))
             for m in range(E):
@@ -115,10 +120,12 @@ def generate(w: Workload, with_bias: bool = True) -> Inputs:
         br[:] = 0
     if w.src_layout == 1:
         src_k = np.ascontiguousarray(src_k.transpose(0, 1, 3, 2, 4))
-        src_v = np.ascontiguousarray(src_v.transpose(0, 1, 3, 2, 4))
+        if src_v is not None:
+            src_v = np.ascontiguousarray(src_v.transpose(0, 1, 3, 2, 4))
     if w.dtype == "bf16":
         for a in (src_k, src_v, w1, b1, w2, b2, wr, br):
-            round_to_bf16(a)
+            if a is not None:
+                round_to_bf16(a)
     return Inputs(src_k, src_v, w1, b1, w2, b2, wr, br, w.dtype)
 
 

@@ -51,7 +51,7 @@ def oracle_dims(w, act=0):
     return OracleDims(L_src=w.L_src, L_tgt=w.L_tgt, B=w.B, T=w.T, H_src=w.H_src, D_src=w.D_src,
                       H_tgt=w.H_tgt, D_tgt=w.D_tgt, E=w.E, hidden=w.hidden,
                       src_layout=w.src_layout, dst_layout=w.dst_layout, act=act,
-                      top_k=w.top_k)
+                      top_k=w.top_k, streams=w.streams)
 
 
 def unit_rows(dst, w, j):

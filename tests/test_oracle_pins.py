@@ -442,3 +442,31 @@ def test_moth_chain_with_identity_translator(oracle_built):
                                    rtol=1e-12, atol=1e-12)
         np.testing.assert_allclose(v[j].reshape(B * T, H * D), a @ wv[j].T.astype(np.float64),
                                    rtol=1e-12, atol=1e-12)
+
+
+def test_single_stream_indexing(oracle_built):
+    """streams = 1 (one activation stream, weights [L_tgt][1][E]) gives
+    exactly the key stream of a two-stream run whose index-0 weights are the
+    same: the per-unit weight offset j*streams + x and the optional value
+    arrays are honoured (a stride of 2 would read the wrong translators)."""
+    rng = np.random.default_rng(23)
+    L_src, L_tgt, B, T, H, D, E, Hd = 2, 3, 1, 5, 2, 4, 3, 6
+    src = rng.standard_normal((L_src, B, T, H, D)).astype(np.float32)
+    w1, b1, w2, b2, wr, br = _rand_weights(rng, L_tgt, E, Hd, H * D, H * D)
+    dims2 = OracleDims(L_src=L_src, L_tgt=L_tgt, B=B, T=T, H_src=H, D_src=D, H_tgt=H, D_tgt=D,
+                       E=E, hidden=Hd, top_k=2)
+    dims1 = OracleDims(**{**dims2.__dict__, "streams": 1})
+    lm = oracle_depth_ratio_map(L_src, L_tgt)
+    k2, _ = oracle_translate(dims2, src, src * 2, lm, w1, b1, w2, b2, wr, br)
+    one = lambda a: np.ascontiguousarray(a[:, :1])
+    k1, v1 = oracle_translate(dims1, src, None, lm, one(w1), one(b1), one(w2), one(b2), one(wr),
+                              one(br))
+    assert v1 is None
+    assert np.array_equal(k1, k2)
+    r = oracle_rows(dims1, src, None, lm, one(w1), one(b1), one(w2), one(b2), one(wr), one(br),
+                    units=[(j, 0) for j in range(L_tgt)], rows=[0, T - 1])
+    for j in range(L_tgt):
+        assert np.array_equal(r[j], _dst_rows(k2, dims2, j)[[0, T - 1]])
+    with pytest.raises(ValueError):
+        oracle_rows(dims1, src, None, lm, one(w1), one(b1), one(w2), one(b2), one(wr), one(br),
+                    units=[(0, 1)], rows=[0])
