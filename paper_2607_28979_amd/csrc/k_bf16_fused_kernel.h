@@ -595,13 +595,16 @@ void k_bf16_fused(Problem p, UnitTab ut) {
         }
 
         // One iteration as a slot schedule over this wave's MFMAs, ordered
-        // (k-slice, output block, token block) so few operands are live; H and
-        // W2 operand reads run LOOK slots ahead; when the layer-2 waves are the
-        // loading waves, their weight loads are spread over the slots.
+        // (k-slice, token block, output block): a k-slice's W2 fragments stay
+        // live while each H fragment is used by consecutive MFMAs, which keeps
+        // the operand registers few enough for the 128 accumulators of
+        // TB = 4, NBW = 2 to fit 168 VGPRs without spilling; H and W2 operand
+        // reads run LOOK slots ahead, and the weight loads are spread over
+        // the slots.
         auto l2_iter = [&](auto l2c, auto w1c, auto w2c, int c, int c_w1, int m_w2, int kk_w2, int st_w2) {
             constexpr bool do_l2 = decltype(l2c)::value, do_w1 = decltype(w1c)::value,
                            do_w2 = decltype(w2c)::value;
-            constexpr int NM = 2 * TB * C::NBW, LOOK = 3;
+            constexpr int NM = 2 * TB * C::NBW, LOOK = 2;
             constexpr int NV = W1_RL + W2_RL;
             const u32x4* Hc = Hs + (c & 1) * C::H_CH;          // chunk c-2 shares c's parity
             const u32x4* W2c = W2s + ((c + C::NW2 - 2) % C::NW2) * C::W2_CH;
@@ -609,7 +612,7 @@ void k_bf16_fused(Problem p, UnitTab ut) {
             auto issue_reads = [&](auto kc) {
                 constexpr int k = decltype(kc)::value;
                 if constexpr (k < NM) {
-                    constexpr int ks = k / (TB * C::NBW), nb = (k / TB) % C::NBW, tb = k % TB;
+                    constexpr int ks = k / (TB * C::NBW), nb = k % C::NBW, tb = (k / C::NBW) % TB;
                     if constexpr (nb == 0) hA[ks][tb] = Hc[tb * 128 + ks * 64 + g * 32 + l32];
                     if constexpr (tb == 0) {
                         const int o = q2 * C::OUTW + nb * 32 + l32;
@@ -634,7 +637,7 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                 }
                 if constexpr (do_l2) {
                     issue_reads(std::integral_constant<int, k + LOOK>{});
-                    constexpr int ks = k / (TB * C::NBW), nb = (k / TB) % C::NBW, tb = k % TB;
+                    constexpr int ks = k / (TB * C::NBW), nb = k % C::NBW, tb = (k / C::NBW) % TB;
                     acc[tb][nb] = mfma_32x32x16(hA[ks][tb], bW[ks][nb], acc[tb][nb]);
                 }
                 __builtin_amdgcn_sched_barrier(0);
