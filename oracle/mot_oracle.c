@@ -43,7 +43,11 @@
  *
  * Also here: the key/value restoration of the activation-translation variant
  * MoT-h (App. C.5), pinned by hand-computed values, the identity projection,
- * a float64 matrix product and an identity-translator chain.
+ * a float64 matrix product and an identity-translator chain; and the context
+ * replay step after translation (App. C.4): Top-S source-guided key
+ * selection and attention over the selected (or the full causal) key set,
+ * pinned by worked examples, sorting, single-key and uniform-score cases and
+ * numpy softmax attention.
  */
 #include <math.h>
 #include <pthread.h>
@@ -399,5 +403,103 @@ int mot_oracle_restore_kv(const float* act, const int32_t* layer_map,
                     }
             }
     }
+    return OR_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* Context replay with Top-S source-guided sparse attention (App. C.4, */
+/* "Post-Translation Phase: Cache Replay")                             */
+/* ------------------------------------------------------------------ */
+
+/* Selection: for each batch row b and context query position u, the key
+ * set N(u) holds the S positions v in 0..u with the largest head-averaged
+ * source attention A[b][u][v] (all of 0..u when u + 1 <= S).  Order of
+ * preference: larger A first, then the lower position.  The set is written
+ * in ascending position order to idx[b][u][0..S), padded with -1.
+ * A: [B][T][T] (entries v > u are never read). */
+int mot_oracle_topS_select(const float* A, int32_t B, int32_t T, int32_t S, int32_t* idx)
+{
+    if (!A || !idx || B < 0 || T < 0 || S < 1) return OR_BAD_ARG;
+    char* take = (char*)malloc(T > 0 ? T : 1);
+    if (!take) return OR_NO_MEM;
+    for (int32_t b = 0; b < B; ++b)
+        for (int32_t u = 0; u < T; ++u) {
+            const float* row = A + ((size_t)b * T + u) * T;
+            const int32_t n = u + 1;
+            int32_t* out = idx + ((size_t)b * T + u) * S;
+            for (int32_t v = 0; v < n; ++v) take[v] = 0;
+            /* S rounds of "the best position not yet taken" (ties: lower v) */
+            const int32_t k = n < S ? n : S;
+            for (int32_t r = 0; r < k; ++r) {
+                int32_t best = -1;
+                for (int32_t v = 0; v < n; ++v)
+                    if (!take[v] && (best < 0 || row[v] > row[best])) best = v;
+                take[best] = 1;
+            }
+            int32_t c = 0;
+            for (int32_t v = 0; v < n; ++v)
+                if (take[v]) out[c++] = v;
+            for (; c < S; ++c) out[c] = -1;
+        }
+    free(take);
+    return OR_OK;
+}
+
+/* Replay attention of one target layer: for batch row b, query position u
+ * and query head h (KV head h / (H_q / H_kv)), over the key set N(u):
+ *     o[b][u][h] = sum_{v in N(u)} p_v V[v],  p = softmax_v(Q[b][u][h] . K[v] / sqrt(D))
+ * N(u) = idx[b][u][0..S) without the -1 entries, or, when idx is NULL, the
+ * full causal set 0..u (the bottom L_Full layers).
+ *   q, o: [B][T][H_q][D];  k, v: [B][T][H_kv][D] (kv_layout 0) or [B][H_kv][T][D] (1).
+ * Dot products, exponentials and sums in double, in index order. */
+int mot_oracle_replay_attention(const float* q, const float* k, const float* v, const int32_t* idx,
+                                double* o, int32_t B, int32_t T, int32_t H_q, int32_t H_kv, int32_t D,
+                                int32_t S, int32_t kv_layout)
+{
+    if (!q || !k || !v || !o || B < 0 || T < 0 || H_q < 1 || H_kv < 1 || D < 1) return OR_BAD_ARG;
+    if (H_q % H_kv || (idx && S < 1) || (kv_layout != 0 && kv_layout != 1)) return OR_BAD_ARG;
+    const int32_t G = H_q / H_kv;
+    const double scale = 1.0 / sqrt((double)D);
+    double* sc = (double*)malloc(sizeof(double) * (T > 0 ? T : 1));
+    int32_t* keys = (int32_t*)malloc(sizeof(int32_t) * (T > 0 ? T : 1));
+    if (!sc || !keys) { free(sc); free(keys); return OR_NO_MEM; }
+    for (int32_t b = 0; b < B; ++b)
+        for (int32_t u = 0; u < T; ++u) {
+            int32_t n = 0;
+            if (idx) {
+                const int32_t* row = idx + ((size_t)b * T + u) * S;
+                for (int32_t c = 0; c < S; ++c)
+                    if (row[c] >= 0) {
+                        if (row[c] > u) { free(sc); free(keys); return OR_BAD_ARG; }
+                        keys[n++] = row[c];
+                    }
+            } else {
+                for (int32_t t = 0; t <= u; ++t) keys[n++] = t;
+            }
+            for (int32_t h = 0; h < H_q; ++h) {
+                const int32_t hk = h / G;
+                const float* qr = q + (((size_t)b * T + u) * H_q + h) * D;
+                double* orow = o + (((size_t)b * T + u) * H_q + h) * D;
+                double mx = -INFINITY;
+                for (int32_t c = 0; c < n; ++c) {
+                    const size_t kr = kv_layout == 0 ? (((size_t)b * T + keys[c]) * H_kv + hk) * D
+                                                     : (((size_t)b * H_kv + hk) * T + keys[c]) * D;
+                    double acc = 0.0;
+                    for (int32_t d = 0; d < D; ++d) acc += (double)qr[d] * (double)k[kr + d];
+                    sc[c] = acc * scale;
+                    if (sc[c] > mx) mx = sc[c];
+                }
+                double den = 0.0;
+                for (int32_t c = 0; c < n; ++c) { sc[c] = exp(sc[c] - mx); den += sc[c]; }
+                for (int32_t d = 0; d < D; ++d) orow[d] = 0.0;
+                for (int32_t c = 0; c < n; ++c) {
+                    const size_t vr = kv_layout == 0 ? (((size_t)b * T + keys[c]) * H_kv + hk) * D
+                                                     : (((size_t)b * H_kv + hk) * T + keys[c]) * D;
+                    const double p = sc[c] / den;
+                    for (int32_t d = 0; d < D; ++d) orow[d] += p * (double)v[vr + d];
+                }
+            }
+        }
+    free(sc); free(keys);
     return OR_OK;
 }

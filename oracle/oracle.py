@@ -89,7 +89,8 @@ def _load():
             build_oracle(force=False)
         _lib = ctypes.CDLL(_LIB)
         for fn in (_lib.mot_oracle_translate, _lib.mot_oracle_rows,
-                   _lib.mot_oracle_depth_ratio_map, _lib.mot_oracle_restore_kv):
+                   _lib.mot_oracle_depth_ratio_map, _lib.mot_oracle_restore_kv,
+                   _lib.mot_oracle_topS_select, _lib.mot_oracle_replay_attention):
             fn.restype = ctypes.c_int
     return _lib
 
@@ -196,3 +197,40 @@ def oracle_restore_kv(act, layer_map, wk, bk, wv, bv, B, T, H_tgt, D_tgt, dst_la
     if rc != 0:
         raise ValueError("mot_oracle_restore_kv failed with code %d" % rc)
     return dst_k, dst_v
+
+
+def oracle_topS_select(A, S: int) -> np.ndarray:
+    """Top-S source-guided key sets (App. C.4): A [B][T][T] head-averaged
+    source attention; returns int32 [B][T][S], each row the S positions
+    v <= u with the largest A[b][u][v] (ties: lower v), ascending, padded -1."""
+    lib = _load()
+    A = _f32(A, "A")
+    B, T = A.shape[0], A.shape[1]
+    idx = np.zeros((B, T, S), dtype=np.int32)
+    rc = lib.mot_oracle_topS_select(_ptr(A), ctypes.c_int32(B), ctypes.c_int32(T), ctypes.c_int32(S),
+                                    _ptr(idx))
+    if rc != 0:
+        raise ValueError("mot_oracle_topS_select failed with code %d" % rc)
+    return idx
+
+
+def oracle_replay_attention(q, k, v, idx=None, kv_layout: int = 0) -> np.ndarray:
+    """Replay attention of one target layer over the key sets idx [B][T][S]
+    (-1 padded), or the full causal set when idx is None (App. C.4).
+    q [B][T][H_q][D]; k, v [B][T][H_kv][D] (kv_layout 0) or [B][H_kv][T][D] (1).
+    Returns float64 [B][T][H_q][D]."""
+    lib = _load()
+    q = _f32(q, "q"); k = _f32(k, "k"); v = _f32(v, "v")
+    B, T, H_q, D = q.shape
+    H_kv = k.shape[2] if kv_layout == 0 else k.shape[1]
+    S = 0
+    if idx is not None:
+        idx = np.ascontiguousarray(idx, dtype=np.int32)
+        S = idx.shape[2]
+    o = np.zeros((B, T, H_q, D))
+    i32 = ctypes.c_int32
+    rc = lib.mot_oracle_replay_attention(_ptr(q), _ptr(k), _ptr(v), _ptr(idx), _ptr(o), i32(B), i32(T),
+                                         i32(H_q), i32(H_kv), i32(D), i32(S), i32(kv_layout))
+    if rc != 0:
+        raise ValueError("mot_oracle_replay_attention failed with code %d" % rc)
+    return o

@@ -470,3 +470,111 @@ def test_single_stream_indexing(oracle_built):
     with pytest.raises(ValueError):
         oracle_rows(dims1, src, None, lm, one(w1), one(b1), one(w2), one(b2), one(wr), one(br),
                     units=[(0, 1)], rows=[0])
+
+
+# ---------------------------------------------------------------------------
+# Context replay (App. C.4): Top-S source-guided selection and attention
+# ---------------------------------------------------------------------------
+
+def test_topS_worked_example(oracle_built):
+    """Rows of a causal head-averaged attention map, S = 2, sets by hand:
+    u=0 -> {0}; u=1 [.5,.5] -> {0,1}; u=2 [.2,.5,.3] -> {1,2};
+    u=3 [.1,.4,.1,.4] -> {1,3} (tie at .4 keeps both, tie at .1 drops both);
+    u=4 [.25]*4 + [0] -> {0,1} (four-way tie: the lower positions)."""
+    from oracle import oracle_topS_select
+    A = np.zeros((1, 5, 5), np.float32)
+    A[0, 0, :1] = [1]
+    A[0, 1, :2] = [.5, .5]
+    A[0, 2, :3] = [.2, .5, .3]
+    A[0, 3, :4] = [.1, .4, .1, .4]
+    A[0, 4, :5] = [.25, .25, .25, .25, 0]
+    got = oracle_topS_select(A, 2)[0].tolist()
+    assert got == [[0, -1], [0, 1], [1, 2], [1, 3], [0, 1]]
+
+
+def test_topS_matches_sorting_and_ignores_future(oracle_built):
+    """Against Python's stable sort on (-A, v) with many ties (values rounded
+    to a coarse grid); entries above the diagonal (NaN here) are never read;
+    S >= T gives every row 0..u."""
+    from oracle import oracle_topS_select
+    rng = np.random.default_rng(29)
+    B, T, S = 2, 11, 4
+    A = np.round(rng.random((B, T, T)) * 4).astype(np.float32) / 4
+    A[:, np.triu_indices(T, 1)[0], np.triu_indices(T, 1)[1]] = np.nan
+    got = oracle_topS_select(A, S)
+    for b in range(B):
+        for u in range(T):
+            best = sorted(range(u + 1), key=lambda v: (-float(A[b, u, v]), v))[:S]
+            want = sorted(best) + [-1] * (S - len(best))
+            assert got[b, u].tolist() == want, (b, u)
+    full = oracle_topS_select(np.nan_to_num(A), T + 3)
+    for u in range(T):
+        assert full[0, u].tolist() == list(range(u + 1)) + [-1] * (T + 3 - u - 1)
+
+
+def _np_attention(q, k, v, sets, G):
+    """softmax(q.K^T / sqrt(D)) V over each key set, numpy float64."""
+    B, T, Hq, D = q.shape
+    o = np.zeros((B, T, Hq, D))
+    for b in range(B):
+        for u in range(T):
+            ks = np.array(sets(b, u))
+            for h in range(Hq):
+                s = k[b, ks, h // G].astype(np.float64) @ q[b, u, h].astype(np.float64) / np.sqrt(D)
+                p = np.exp(s - s.max())
+                p /= p.sum()
+                o[b, u, h] = p @ v[b, ks, h // G].astype(np.float64)
+    return o
+
+
+def test_replay_attention_matches_numpy(oracle_built):
+    """Sparse (Top-S key sets) and full causal attention with GQA (4 query
+    heads on 2 KV heads) against numpy softmax attention, both KV layouts."""
+    from oracle import oracle_replay_attention, oracle_topS_select
+    rng = np.random.default_rng(31)
+    B, T, Hq, Hkv, D, S = 2, 9, 4, 2, 8, 3
+    q = rng.standard_normal((B, T, Hq, D)).astype(np.float32)
+    k = rng.standard_normal((B, T, Hkv, D)).astype(np.float32)
+    v = rng.standard_normal((B, T, Hkv, D)).astype(np.float32)
+    A = rng.random((B, T, T)).astype(np.float32)
+    idx = oracle_topS_select(A, S)
+    sparse = oracle_replay_attention(q, k, v, idx)
+    want = _np_attention(q, k, v, lambda b, u: [c for c in idx[b, u] if c >= 0], Hq // Hkv)
+    np.testing.assert_allclose(sparse, want, rtol=1e-12, atol=1e-12)
+    full = oracle_replay_attention(q, k, v, None)
+    np.testing.assert_allclose(full, _np_attention(q, k, v, lambda b, u: range(u + 1), Hq // Hkv),
+                               rtol=1e-12, atol=1e-12)
+    kt, vt = (np.ascontiguousarray(a.transpose(0, 2, 1, 3)) for a in (k, v))
+    assert np.array_equal(oracle_replay_attention(q, kt, vt, idx, kv_layout=1), sparse)
+
+
+def test_replay_attention_special_cases(oracle_built):
+    """One key: the output is that key's value row exactly.  Zero query: the
+    scores are uniform and the output is the mean of the set's values.  The
+    order of a key set does not matter.  Query head h reads KV head
+    h // (H_q / H_kv)."""
+    from oracle import oracle_replay_attention
+    rng = np.random.default_rng(37)
+    B, T, Hq, Hkv, D = 1, 6, 4, 2, 4
+    q = rng.standard_normal((B, T, Hq, D)).astype(np.float32)
+    k = rng.standard_normal((B, T, Hkv, D)).astype(np.float32)
+    v = rng.standard_normal((B, T, Hkv, D)).astype(np.float32)
+    one = np.full((B, T, 2), -1, np.int32)
+    one[0, :, 0] = np.arange(T) // 2                         # v = floor(u / 2) <= u
+    o = oracle_replay_attention(q, k, v, one)
+    for u in range(T):
+        for h in range(Hq):
+            assert np.array_equal(o[0, u, h], v[0, u // 2, h // 2].astype(np.float64))
+    zq = np.zeros_like(q)
+    sets = np.array([[[0, -1, -1], [1, 0, -1], [0, 1, 2], [3, 1, 0], [4, 2, 3], [5, 0, 1]]], np.int32)
+    oz = oracle_replay_attention(zq, k, v, sets)
+    for u in range(T):
+        ks = [c for c in sets[0, u] if c >= 0]
+        for h in range(Hq):
+            np.testing.assert_allclose(oz[0, u, h], v[0, ks, h // 2].astype(np.float64).mean(axis=0),
+                                       rtol=1e-12, atol=1e-14)
+    perm = sets[:, :, ::-1].copy()
+    np.testing.assert_allclose(oracle_replay_attention(q, k, v, perm), oracle_replay_attention(q, k, v, sets),
+                               rtol=1e-13, atol=1e-15)
+    with pytest.raises(ValueError):   # a key after the query position
+        oracle_replay_attention(q, k, v, np.full((B, T, 1), T - 1, np.int32))
