@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define MOT_ABI_VERSION 2
+#define MOT_ABI_VERSION 3
 #define MOT_MAX_LAYERS 256   /* L_src, L_tgt <= MOT_MAX_LAYERS               */
 #define MOT_MAX_EXPERTS 16   /* E <= MOT_MAX_EXPERTS                         */
 
@@ -213,6 +213,51 @@ typedef struct {
 mot_status mot_restore_kv(const void* act, const int32_t* layer_map, const void* wk, const void* bk,
                           const void* wv, const void* bv, void* dst_k, void* dst_v,
                           const mot_restore_shapes* shapes, hipStream_t stream);
+
+/*
+ * Context replay after translation (paper App. C.4, "Post-Translation Phase:
+ * Cache Replay", Top-S source-guided sparse attention).  Query position u of
+ * a target layer attends only to the S context positions that the source
+ * model attended to most at the guiding source layer (head-averaged map A),
+ * or, in the bottom L_Full layers, to every position 0..u.
+ *
+ *   B, T       batch rows, context tokens
+ *   H_q, H_kv  target query heads and KV heads (H_q a multiple of H_kv; query
+ *              head h reads KV head h / (H_q / H_kv), at most 16 per KV head)
+ *   D          head dim: 64 or 128
+ *   S          Top-S budget: a multiple of 32, 32 .. 256 (at most 192 when
+ *              D = 128); the paper uses 128
+ *   kv_layout  K and V in MOT_LAYOUT_BTHD ([B][T][H_kv][D]) or MOT_LAYOUT_BHTD
+ */
+typedef struct {
+    int32_t B, T;
+    int32_t H_q, H_kv, D;
+    int32_t S;
+    int32_t kv_layout;
+} mot_replay_shapes;
+
+/*
+ * Top-S key sets (App. C.4, N(u) = Top-S of A[u, 1:u]): for every b and u,
+ * the S positions v <= u with the largest A[b][u][v] (ties: lower v), written
+ * in ascending order to idx[b][u][0..S) and padded with -1 (all of 0..u when
+ * u < S).  A: device fp32 [B][T][T] head-averaged source attention (entries
+ * v > u are not read); idx: device int32 [B][T][S].  Only B, T and S of
+ * `shapes` are used.  Both pointers 4-byte aligned and non-overlapping.
+ */
+mot_status mot_topS_select(const float* A, int32_t* idx, const mot_replay_shapes* shapes, hipStream_t stream);
+
+/*
+ * Replay attention of one target layer: for every b, u and query head h,
+ *     o[b][u][h] = sum_{v in N(u)} softmax_v(q[b][u][h] . k[v] / sqrt(D)) v[v]
+ * with N(u) = the entries of idx[b][u] that lie in 0..u (others, such as the
+ * -1 padding, are skipped; a set with none gives zeros), or the full causal
+ * set 0..u when idx is NULL.  q, o: device bf16 [B][T][H_q][D]; k, v: device
+ * bf16 in kv_layout; idx: device int32 [B][T][S] or NULL.  Softmax and
+ * accumulation in fp32; o rounded to bf16.  All pointers 16-byte aligned; o
+ * must not overlap an input.
+ */
+mot_status mot_replay_attention(const void* q, const void* k, const void* v, const int32_t* idx, void* o,
+                                const mot_replay_shapes* shapes, hipStream_t stream);
 
 /* MOT_ABI_VERSION of the loaded library. */
 int mot_abi_version(void);

@@ -452,54 +452,124 @@ int mot_oracle_topS_select(const float* A, int32_t B, int32_t T, int32_t S, int3
  * full causal set 0..u (the bottom L_Full layers).
  *   q, o: [B][T][H_q][D];  k, v: [B][T][H_kv][D] (kv_layout 0) or [B][H_kv][T][D] (1).
  * Dot products, exponentials and sums in double, in index order. */
+typedef struct {
+    const float *q, *k, *v;
+    const int32_t* idx;
+    int32_t B, T, H_q, H_kv, D, S, kv_layout;
+} replay_args;
+
+/* all heads of (b, u) into orow[H_q][D]; sc, keys: scratch of T entries */
+static int replay_row(const replay_args* a, int32_t b, int32_t u, double* orow, double* sc, int32_t* keys)
+{
+    const int32_t G = a->H_q / a->H_kv, D = a->D, T = a->T;
+    const double scale = 1.0 / sqrt((double)D);
+    int32_t n = 0;
+    if (a->idx) {
+        const int32_t* row = a->idx + ((size_t)b * T + u) * a->S;
+        for (int32_t c = 0; c < a->S; ++c)
+            if (row[c] >= 0) {
+                if (row[c] > u) return OR_BAD_ARG;
+                keys[n++] = row[c];
+            }
+    } else {
+        for (int32_t t = 0; t <= u; ++t) keys[n++] = t;
+    }
+    for (int32_t h = 0; h < a->H_q; ++h) {
+        const int32_t hk = h / G;
+        const float* qr = a->q + (((size_t)b * T + u) * a->H_q + h) * D;
+        double* oh = orow + (size_t)h * D;
+        double mx = -INFINITY;
+        for (int32_t c = 0; c < n; ++c) {
+            const size_t kr = a->kv_layout == 0 ? (((size_t)b * T + keys[c]) * a->H_kv + hk) * D
+                                                : (((size_t)b * a->H_kv + hk) * T + keys[c]) * D;
+            double acc = 0.0;
+            for (int32_t d = 0; d < D; ++d) acc += (double)qr[d] * (double)a->k[kr + d];
+            sc[c] = acc * scale;
+            if (sc[c] > mx) mx = sc[c];
+        }
+        double den = 0.0;
+        for (int32_t c = 0; c < n; ++c) { sc[c] = exp(sc[c] - mx); den += sc[c]; }
+        for (int32_t d = 0; d < D; ++d) oh[d] = 0.0;
+        for (int32_t c = 0; c < n; ++c) {
+            const size_t vr = a->kv_layout == 0 ? (((size_t)b * T + keys[c]) * a->H_kv + hk) * D
+                                                : (((size_t)b * a->H_kv + hk) * T + keys[c]) * D;
+            const double pr = sc[c] / den;
+            for (int32_t d = 0; d < D; ++d) oh[d] += pr * (double)a->v[vr + d];
+        }
+    }
+    return OR_OK;
+}
+
+static int replay_check(const replay_args* a)
+{
+    if (!a->q || !a->k || !a->v || a->B < 0 || a->T < 0 || a->H_q < 1 || a->H_kv < 1 || a->D < 1) return OR_BAD_ARG;
+    if (a->H_q % a->H_kv || (a->idx && a->S < 1) || (a->kv_layout != 0 && a->kv_layout != 1)) return OR_BAD_ARG;
+    return OR_OK;
+}
+
 int mot_oracle_replay_attention(const float* q, const float* k, const float* v, const int32_t* idx,
                                 double* o, int32_t B, int32_t T, int32_t H_q, int32_t H_kv, int32_t D,
                                 int32_t S, int32_t kv_layout)
 {
-    if (!q || !k || !v || !o || B < 0 || T < 0 || H_q < 1 || H_kv < 1 || D < 1) return OR_BAD_ARG;
-    if (H_q % H_kv || (idx && S < 1) || (kv_layout != 0 && kv_layout != 1)) return OR_BAD_ARG;
-    const int32_t G = H_q / H_kv;
-    const double scale = 1.0 / sqrt((double)D);
+    replay_args a = {q, k, v, idx, B, T, H_q, H_kv, D, S, kv_layout};
+    int rc = replay_check(&a);
+    if (rc || !o) return rc ? rc : OR_BAD_ARG;
     double* sc = (double*)malloc(sizeof(double) * (T > 0 ? T : 1));
     int32_t* keys = (int32_t*)malloc(sizeof(int32_t) * (T > 0 ? T : 1));
     if (!sc || !keys) { free(sc); free(keys); return OR_NO_MEM; }
-    for (int32_t b = 0; b < B; ++b)
-        for (int32_t u = 0; u < T; ++u) {
-            int32_t n = 0;
-            if (idx) {
-                const int32_t* row = idx + ((size_t)b * T + u) * S;
-                for (int32_t c = 0; c < S; ++c)
-                    if (row[c] >= 0) {
-                        if (row[c] > u) { free(sc); free(keys); return OR_BAD_ARG; }
-                        keys[n++] = row[c];
-                    }
-            } else {
-                for (int32_t t = 0; t <= u; ++t) keys[n++] = t;
-            }
-            for (int32_t h = 0; h < H_q; ++h) {
-                const int32_t hk = h / G;
-                const float* qr = q + (((size_t)b * T + u) * H_q + h) * D;
-                double* orow = o + (((size_t)b * T + u) * H_q + h) * D;
-                double mx = -INFINITY;
-                for (int32_t c = 0; c < n; ++c) {
-                    const size_t kr = kv_layout == 0 ? (((size_t)b * T + keys[c]) * H_kv + hk) * D
-                                                     : (((size_t)b * H_kv + hk) * T + keys[c]) * D;
-                    double acc = 0.0;
-                    for (int32_t d = 0; d < D; ++d) acc += (double)qr[d] * (double)k[kr + d];
-                    sc[c] = acc * scale;
-                    if (sc[c] > mx) mx = sc[c];
-                }
-                double den = 0.0;
-                for (int32_t c = 0; c < n; ++c) { sc[c] = exp(sc[c] - mx); den += sc[c]; }
-                for (int32_t d = 0; d < D; ++d) orow[d] = 0.0;
-                for (int32_t c = 0; c < n; ++c) {
-                    const size_t vr = kv_layout == 0 ? (((size_t)b * T + keys[c]) * H_kv + hk) * D
-                                                     : (((size_t)b * H_kv + hk) * T + keys[c]) * D;
-                    const double p = sc[c] / den;
-                    for (int32_t d = 0; d < D; ++d) orow[d] += p * (double)v[vr + d];
-                }
-            }
-        }
+    for (int32_t b = 0; b < B && rc == OR_OK; ++b)
+        for (int32_t u = 0; u < T && rc == OR_OK; ++u)
+            rc = replay_row(&a, b, u, o + ((size_t)b * T + u) * H_q * D, sc, keys);
     free(sc); free(keys);
+    return rc;
+}
+
+/* The same for listed positions (rb[i], ru[i]) only: out[i][H_q][D]. */
+int mot_oracle_replay_attention_rows(const float* q, const float* k, const float* v, const int32_t* idx,
+                                     int32_t B, int32_t T, int32_t H_q, int32_t H_kv, int32_t D,
+                                     int32_t S, int32_t kv_layout, const int32_t* rb, const int32_t* ru,
+                                     int32_t n_rows, double* out)
+{
+    replay_args a = {q, k, v, idx, B, T, H_q, H_kv, D, S, kv_layout};
+    int rc = replay_check(&a);
+    if (rc || !out || !rb || !ru || n_rows < 0) return rc ? rc : OR_BAD_ARG;
+    for (int32_t i = 0; i < n_rows; ++i)
+        if (rb[i] < 0 || rb[i] >= B || ru[i] < 0 || ru[i] >= T) return OR_BAD_ARG;
+    double* sc = (double*)malloc(sizeof(double) * (T > 0 ? T : 1));
+    int32_t* keys = (int32_t*)malloc(sizeof(int32_t) * (T > 0 ? T : 1));
+    if (!sc || !keys) { free(sc); free(keys); return OR_NO_MEM; }
+    for (int32_t i = 0; i < n_rows && rc == OR_OK; ++i)
+        rc = replay_row(&a, rb[i], ru[i], out + (size_t)i * H_q * D, sc, keys);
+    free(sc); free(keys);
+    return rc;
+}
+
+/* Top-S sets of listed rows (rb[i], ru[i]) only: out[i][S] (see
+ * mot_oracle_topS_select). */
+int mot_oracle_topS_rows(const float* A, int32_t B, int32_t T, int32_t S, const int32_t* rb,
+                         const int32_t* ru, int32_t n_rows, int32_t* out)
+{
+    if (!A || !out || !rb || !ru || B < 0 || T < 0 || S < 1 || n_rows < 0) return OR_BAD_ARG;
+    char* take = (char*)malloc(T > 0 ? T : 1);
+    if (!take) return OR_NO_MEM;
+    for (int32_t i = 0; i < n_rows; ++i) {
+        const int32_t b = rb[i], u = ru[i];
+        if (b < 0 || b >= B || u < 0 || u >= T) { free(take); return OR_BAD_ARG; }
+        const float* row = A + ((size_t)b * T + u) * T;
+        const int32_t n = u + 1, k = n < S ? n : S;
+        int32_t* o = out + (size_t)i * S;
+        for (int32_t v = 0; v < n; ++v) take[v] = 0;
+        for (int32_t r = 0; r < k; ++r) {
+            int32_t best = -1;
+            for (int32_t v = 0; v < n; ++v)
+                if (!take[v] && (best < 0 || row[v] > row[best])) best = v;
+            take[best] = 1;
+        }
+        int32_t c = 0;
+        for (int32_t v = 0; v < n; ++v)
+            if (take[v]) o[c++] = v;
+        for (; c < S; ++c) o[c] = -1;
+    }
+    free(take);
     return OR_OK;
 }

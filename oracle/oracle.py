@@ -90,7 +90,8 @@ def _load():
         _lib = ctypes.CDLL(_LIB)
         for fn in (_lib.mot_oracle_translate, _lib.mot_oracle_rows,
                    _lib.mot_oracle_depth_ratio_map, _lib.mot_oracle_restore_kv,
-                   _lib.mot_oracle_topS_select, _lib.mot_oracle_replay_attention):
+                   _lib.mot_oracle_topS_select, _lib.mot_oracle_replay_attention,
+                   _lib.mot_oracle_replay_attention_rows, _lib.mot_oracle_topS_rows):
             fn.restype = ctypes.c_int
     return _lib
 
@@ -234,3 +235,40 @@ def oracle_replay_attention(q, k, v, idx=None, kv_layout: int = 0) -> np.ndarray
     if rc != 0:
         raise ValueError("mot_oracle_replay_attention failed with code %d" % rc)
     return o
+
+
+def oracle_topS_rows(A, S: int, rows) -> np.ndarray:
+    """Top-S sets of the listed (b, u) rows only: int32 [n][S]."""
+    lib = _load()
+    A = _f32(A, "A")
+    B, T = A.shape[0], A.shape[1]
+    rb = np.ascontiguousarray([r[0] for r in rows], dtype=np.int32)
+    ru = np.ascontiguousarray([r[1] for r in rows], dtype=np.int32)
+    out = np.zeros((len(rows), S), dtype=np.int32)
+    i32 = ctypes.c_int32
+    rc = lib.mot_oracle_topS_rows(_ptr(A), i32(B), i32(T), i32(S), _ptr(rb), _ptr(ru), i32(len(rows)), _ptr(out))
+    if rc != 0:
+        raise ValueError("mot_oracle_topS_rows failed with code %d" % rc)
+    return out
+
+
+def oracle_replay_attention_rows(q, k, v, idx, rows, kv_layout: int = 0) -> np.ndarray:
+    """oracle_replay_attention for the listed (b, u) rows only: float64 [n][H_q][D]."""
+    lib = _load()
+    q = _f32(q, "q"); k = _f32(k, "k"); v = _f32(v, "v")
+    B, T, H_q, D = q.shape
+    H_kv = k.shape[2] if kv_layout == 0 else k.shape[1]
+    S = 0
+    if idx is not None:
+        idx = np.ascontiguousarray(idx, dtype=np.int32)
+        S = idx.shape[2]
+    rb = np.ascontiguousarray([r[0] for r in rows], dtype=np.int32)
+    ru = np.ascontiguousarray([r[1] for r in rows], dtype=np.int32)
+    out = np.zeros((len(rows), H_q, D))
+    i32 = ctypes.c_int32
+    rc = lib.mot_oracle_replay_attention_rows(_ptr(q), _ptr(k), _ptr(v), _ptr(idx), i32(B), i32(T), i32(H_q),
+                                              i32(H_kv), i32(D), i32(S), i32(kv_layout), _ptr(rb), _ptr(ru),
+                                              i32(len(rows)), _ptr(out))
+    if rc != 0:
+        raise ValueError("mot_oracle_replay_attention_rows failed with code %d" % rc)
+    return out

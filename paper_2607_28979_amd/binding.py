@@ -25,7 +25,8 @@ STATUS = {0: "MOT_OK", 1: "MOT_ERR_NULL_ARG", 2: "MOT_ERR_BAD_SHAPE", 3: "MOT_ER
           7: "MOT_ERR_HIP"}
 
 EXPORTED = ("mot_translate", "mot_workspace_bytes", "mot_depth_ratio_map", "mot_status_string",
-            "mot_last_error", "mot_abi_version", "mot_restore_kv")
+            "mot_last_error", "mot_abi_version", "mot_restore_kv", "mot_topS_select",
+            "mot_replay_attention")
 
 
 class MotError(RuntimeError):
@@ -45,6 +46,10 @@ class _Shapes(ctypes.Structure):
 class _RestoreShapes(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("L", "B", "T", "d_act", "H_tgt", "D_tgt", "dtype",
                                              "dst_layout")]
+
+
+class _ReplayShapes(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("B", "T", "H_q", "H_kv", "D", "S", "kv_layout")]
 
 
 class _TW(ctypes.Structure):
@@ -142,6 +147,12 @@ def load_library():
         lib.mot_restore_kv.restype = ctypes.c_int
         lib.mot_restore_kv.argtypes = [ctypes.c_void_p] * 8 + [ctypes.POINTER(_RestoreShapes),
                                                                ctypes.c_void_p]
+        lib.mot_topS_select.restype = ctypes.c_int
+        lib.mot_topS_select.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(_ReplayShapes),
+                                        ctypes.c_void_p]
+        lib.mot_replay_attention.restype = ctypes.c_int
+        lib.mot_replay_attention.argtypes = [ctypes.c_void_p] * 5 + [ctypes.POINTER(_ReplayShapes),
+                                                                     ctypes.c_void_p]
         _lib = lib
     return _lib
 
@@ -241,3 +252,32 @@ def restore_kv(act, layer_map, wk, bk, wv, bv, dst_k, dst_v, L: int, B: int, T: 
     _check(lib.mot_restore_kv(_ptr(act), lm.ctypes.data if lm is not None else None, _ptr(wk),
                               _ptr(bk), _ptr(wv), _ptr(bv), _ptr(dst_k), _ptr(dst_v),
                               ctypes.byref(c), stream))
+
+
+def topS_select(A, idx, B: int, T: int, S: int) -> None:
+    """mot_topS_select on the current torch stream: A fp32 [B][T][T] (head-
+    averaged source attention), idx int32 [B][T][S] (output)."""
+    import torch
+    lib = load_library()
+    for name, t, dt in (("A", A, torch.float32), ("idx", idx, torch.int32)):
+        if t is not None and (t.dtype != dt or not t.is_contiguous()):
+            raise MotError(2, "%s must be a contiguous %s tensor" % (name, dt))
+    c = _ReplayShapes(B, T, 1, 1, 128, S, LAYOUT_BTHD)
+    _check(lib.mot_topS_select(_ptr(A), _ptr(idx), ctypes.byref(c),
+                               torch.cuda.current_stream().cuda_stream))
+
+
+def replay_attention(q, k, v, idx, o, B: int, T: int, H_q: int, H_kv: int, D: int, S: int = 0,
+                     kv_layout: int = LAYOUT_BTHD) -> None:
+    """mot_replay_attention on the current torch stream (bf16 q, k, v, o;
+    int32 idx [B][T][S], or None for the full causal set)."""
+    import torch
+    lib = load_library()
+    for name, t in (("q", q), ("k", k), ("v", v), ("o", o)):
+        if t.dtype != torch.bfloat16 or not t.is_contiguous():
+            raise MotError(2, "%s must be a contiguous bfloat16 tensor" % name)
+    if idx is not None and (idx.dtype != torch.int32 or not idx.is_contiguous()):
+        raise MotError(2, "idx must be a contiguous int32 tensor")
+    c = _ReplayShapes(B, T, H_q, H_kv, D, S if idx is not None else 0, kv_layout)
+    _check(lib.mot_replay_attention(_ptr(q), _ptr(k), _ptr(v), _ptr(idx), _ptr(o), ctypes.byref(c),
+                                    torch.cuda.current_stream().cuda_stream))

@@ -134,3 +134,35 @@ def small_variant(w: Workload, L_src: Optional[int] = None, L_tgt: Optional[int]
     the oracle finishes in seconds.  Used by the parity tests."""
     return replace(w, L_src=L_src or w.L_src, L_tgt=L_tgt or w.L_tgt, B=B or w.B,
                    T=T or w.T, hidden=hidden or w.hidden)
+
+
+@dataclass(frozen=True)
+class ReplayWorkload:
+    """Context replay after translation (App. C.4): every target layer
+    attends over the context; the bottom L_full layers over the full causal
+    prefix, the others over their Top-S source-guided key sets, chosen from
+    the head-averaged attention map of the source layer the depth-ratio map
+    pairs with them."""
+    name: str
+    L_src: int
+    L_tgt: int
+    B: int
+    T: int
+    H_q: int
+    H_kv: int
+    D: int
+    S: int
+    L_full: int
+    seed: int
+
+    def attention_flops(self) -> float:
+        """2 (scores) + 2 (values) flops per (query head, key, head dim)."""
+        sparse = (self.L_tgt - self.L_full) * self.B * sum(min(u + 1, self.S) for u in range(self.T))
+        full = self.L_full * self.B * self.T * (self.T + 1) / 2
+        return 4.0 * self.H_q * self.D * (sparse + full)
+
+
+# Qwen2.5-1.5B source -> Qwen2.5-7B target (28 query heads on 4 KV heads of
+# 128), one 8K-token context, S = 128, L_full = 2
+REPLAY = ReplayWorkload("qwen2.5-1.5b->qwen2.5-7b replay, 8K context", L_src=28, L_tgt=28, B=1, T=8192,
+                        H_q=28, H_kv=4, D=128, S=128, L_full=2, seed=6)

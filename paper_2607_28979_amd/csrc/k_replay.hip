@@ -1,0 +1,429 @@
+// Context replay after translation (paper App. C.4, "Post-Translation Phase:
+// Cache Replay"): Top-S source-guided sparse attention.
+//
+// * k_topS_select: for each query position u, the S key positions v <= u
+//   with the largest head-averaged source attention A[b][u][v] (ties to the
+//   lower position), in ascending position order, padded with -1.  Radix
+//   select over order-preserving 32-bit keys: four 8-bit histogram passes
+//   find the S-th largest key, then one ordered pass keeps every larger key
+//   and the lowest-positioned equal ones.
+// * k_sparse_attn: attention of every query head of (b, u) over its key set
+//   (grouped-query: query head h reads KV head h / G).  Per KV head the
+//   workgroup computes scores^T = K_sel . Q^T on v_mfma_f32_16x16x32_bf16 with
+//   the gathered key rows loaded straight into A operands, a softmax over the
+//   set, and O^T = V_sel^T . P^T with V_sel staged transposed in LDS.
+// * k_causal_attn: the full causal attention of the bottom layers, tiled
+//   (64 query positions of one head per workgroup, 64-key chunks staged in
+//   LDS, online softmax).
+// Scores, softmax and accumulation are fp32; Q, K, V, O are bf16.
+#include "mot_device.h"
+#include "mot_internal.h"
+#include "../../include/mot.h"
+
+namespace mot {
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// Monotone map float -> uint32 (a < b  <=>  key(a) < key(b) for non-NaN).
+__device__ __forceinline__ uint32_t order_key(float a) {
+    const uint32_t b = __float_as_uint(a);
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+// Exclusive rank of a per-thread flag in thread order over the 256-thread
+// workgroup, and the workgroup's total.  s_cnt: 4 ints of LDS.
+__device__ __forceinline__ int block_rank(bool f, int* s_cnt, int& total) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const unsigned long long bal = __ballot(f);
+    const int in_wave = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) s_cnt[w] = __popcll(bal);
+    __syncthreads();
+    int base = 0;
+    total = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int c = s_cnt[i];
+        base += i < w ? c : 0;
+        total += c;
+    }
+    __syncthreads();
+    return base + in_wave;
+}
+
+// grid (T, B), 256 threads; CACHE: the row's keys live in dynamic LDS (T words)
+template <bool CACHE>
+__global__ __launch_bounds__(256) void k_topS_select(const float* A, int32_t* idx, int T, int S) {
+    extern __shared__ uint32_t s_key[];
+    __shared__ uint32_t hist[256];
+    __shared__ int s_cnt[4];
+    __shared__ uint32_t s_sel[2];
+    const int u = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    const int n = u + 1;
+    int32_t* out = idx + ((size_t)b * T + u) * S;
+    if (n <= S) {   // every causal position is kept (uniform exit, before any barrier)
+        for (int c = tid; c < S; c += 256) out[c] = c < n ? c : -1;
+        return;
+    }
+    const float* row = A + ((size_t)b * T + u) * T;
+    if constexpr (CACHE) {
+        for (int v = tid; v < n; v += 256) s_key[v] = order_key(row[v]);
+        __syncthreads();
+    }
+    auto key_at = [&](int v) -> uint32_t {
+        if constexpr (CACHE) return s_key[v];
+        else return order_key(row[v]);
+    };
+    uint32_t prefix = 0, mask = 0;
+    int rem = S;   // keys still to choose among those matching the prefix
+    for (int shift = 24; shift >= 0; shift -= 8) {
+        hist[tid] = 0;
+        __syncthreads();
+        for (int v = tid; v < n; v += 256) {
+            const uint32_t k = key_at(v);
+            if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+        }
+        __syncthreads();
+        if (tid < 64) {
+            // lane l holds bins 4l .. 4l+3; suffix sums over lanes find the
+            // bin holding the rem-th largest remaining key
+            const uint32_t h0 = hist[4 * tid], h1 = hist[4 * tid + 1], h2 = hist[4 * tid + 2],
+                           h3 = hist[4 * tid + 3];
+            const uint32_t c = h0 + h1 + h2 + h3;
+            uint32_t suf = c;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const uint32_t t = __shfl_down(suf, off, 64);
+                if (tid + off < 64) suf += t;
+            }
+            const unsigned long long bal = __ballot(suf >= (uint32_t)rem);   // lanes 0 .. L
+            const int L = 63 - __clzll(bal);
+            if (tid == L) {
+                uint32_t cum = suf - c;   // keys in bins above 4L+3
+                int d = 4 * L;
+                const uint32_t hb[4] = {h0, h1, h2, h3};
+#pragma unroll
+                for (int q = 3; q >= 0; --q) {
+                    if (cum + hb[q] >= (uint32_t)rem) {
+                        d = 4 * L + q;
+                        break;
+                    }
+                    cum += hb[q];
+                }
+                s_sel[0] = (uint32_t)d;
+                s_sel[1] = cum;
+            }
+        }
+        __syncthreads();
+        const uint32_t d = s_sel[0];
+        rem -= (int)s_sel[1];
+        prefix |= d << shift;
+        mask |= 255u << shift;
+        __syncthreads();
+    }
+    // prefix is the S-th largest key; take all larger keys and the first rem
+    // equal ones in position order
+    int out_base = 0, eq_base = 0;
+    for (int c0 = 0; c0 < n; c0 += 256) {
+        const int v = c0 + tid;
+        const uint32_t k = v < n ? key_at(v) : 0u;
+        const bool gt = v < n && k > prefix, eq = v < n && k == prefix;
+        int eq_tot, tk_tot;
+        const int eq_rank = block_rank(eq, s_cnt, eq_tot);
+        const bool take = gt || (eq && eq_base + eq_rank < rem);
+        const int pos = block_rank(take, s_cnt, tk_tot);
+        if (take && out_base + pos < S) out[out_base + pos] = v;
+        out_base += tk_tot;
+        eq_base += eq_tot;
+    }
+}
+
+__device__ __forceinline__ size_t kv_row(const ReplayProblem& p, int b, int t, int kvh) {
+    return p.kv_layout == MOT_LAYOUT_BTHD ? (((size_t)b * p.T + t) * p.H_kv + kvh) * p.D
+                                          : (((size_t)b * p.H_kv + kvh) * p.T + t) * p.D;
+}
+
+__device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// 8 bf16 of chunk a (keys k0) and c (key k0+1) interleaved into 8 words:
+// word i = (a[i], c[i]) for d = 8*chunk + i
+__device__ __forceinline__ uint32_t pair_word(const u32x4& a, const u32x4& c, int i) {
+    const uint32_t wa = a[i >> 1], wc = c[i >> 1];
+    return (i & 1) ? ((wa >> 16) | (wc & 0xFFFF0000u)) : ((wa & 0xFFFFu) | (wc << 16));
+}
+
+// grid (T, B), 256 threads; dynamic LDS: V^T [D][S] + P [16][S] (bf16) + 128 floats
+template <int D>
+__global__ __launch_bounds__(256) void k_sparse_attn(ReplayProblem p) {
+    extern __shared__ u32x4 s_dyn[];
+    constexpr int DC = D / 8;               // 16-byte chunks per row of D
+    const int S = p.S, SC = S / 8;          // 16-byte chunks per row of S keys
+    const int swm = (SC < 16 ? SC : 16) - 1;
+    u32x4* Vt = s_dyn;                      // row d: SC chunks, chunk c at (c ^ (d & swm))
+    u32x4* Pl = s_dyn + D * SC;             // row = query head slot
+    float* red = reinterpret_cast<float*>(Pl + 16 * SC);   // [4 waves][16]: max, then sum
+    const int u = blockIdx.x, b = blockIdx.y;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, q4 = lane >> 4;
+    const int G = p.H_q / p.H_kv, KB = S / 16;
+    const int32_t* keys = p.idx + ((size_t)b * p.T + u) * S;
+    const uint16_t* Q = reinterpret_cast<const uint16_t*>(p.q);
+    const uint16_t* K = reinterpret_cast<const uint16_t*>(p.k);
+    const uint16_t* V = reinterpret_cast<const uint16_t*>(p.v);
+    uint16_t* O = reinterpret_cast<uint16_t*>(p.o);
+    const float sl2 = kLog2e / sqrtf((float)D);
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    // a key entry outside 0..u (the -1 padding) is not attended
+    auto key_ok = [&](int kv) { return kv >= 0 && kv <= u; };
+
+    for (int kvh = 0; kvh < p.H_kv; ++kvh) {
+        // (a) V_sel^T into LDS: item = (key pair, d chunk)
+        uint32_t* Vw = reinterpret_cast<uint32_t*>(Vt);
+        for (int it = tid; it < (S / 2) * DC; it += 256) {
+            const int pr = it % (S / 2), dc = it / (S / 2), k0 = 2 * pr;
+            const int v0 = keys[k0], v1 = keys[k0 + 1];
+            const u32x4 a = key_ok(v0) ? *reinterpret_cast<const u32x4*>(V + kv_row(p, b, v0, kvh) + 8 * dc) : zero;
+            const u32x4 c = key_ok(v1) ? *reinterpret_cast<const u32x4*>(V + kv_row(p, b, v1, kvh) + 8 * dc) : zero;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int d = 8 * dc + i;
+                Vw[(d * SC + ((k0 >> 3) ^ (d & swm))) * 4 + ((k0 & 7) >> 1)] = pair_word(a, c, i);
+            }
+        }
+        // (b) scores^T[key][head] for key blocks kb = w, w+4, ...
+        const int hq = kvh * G + l16;
+        u32x4 qop[D / 32];
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks)
+            qop[ks] = l16 < G ? *reinterpret_cast<const u32x4*>(Q + (((size_t)b * p.T + u) * p.H_q + hq) * D + 32 * ks + 8 * q4)
+                              : zero;
+        f32x4 sc[4];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int kb = w + 4 * i;
+            sc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (kb < KB) {
+                const int kr = keys[kb * 16 + l16];
+                const uint16_t* krow = K + (key_ok(kr) ? kv_row(p, b, kr, kvh) : 0);
+#pragma unroll
+                for (int ks = 0; ks < D / 32; ++ks) {
+                    const u32x4 a = key_ok(kr) ? *reinterpret_cast<const u32x4*>(krow + 32 * ks + 8 * q4) : zero;
+                    sc[i] = mfma_16x16x32(a, qop[ks], sc[i]);
+                }
+                const int4 kk = *reinterpret_cast<const int4*>(keys + kb * 16 + 4 * q4);
+                const int kv4[4] = {kk.x, kk.y, kk.z, kk.w};
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    sc[i][j] = key_ok(kv4[j]) ? sc[i][j] : -INFINITY;
+                    mx = fmaxf(mx, sc[i][j]);
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) sc[i][j] = -INFINITY;
+            }
+        }
+        // (c) softmax over the set, per head (lane column l16)
+        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        if (q4 == 0) red[w * 16 + l16] = mx;
+        __syncthreads();
+        mx = fmaxf(fmaxf(red[l16], red[16 + l16]), fmaxf(red[32 + l16], red[48 + l16]));
+        float sum = 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float e = sc[i][j] == -INFINITY ? 0.f : exp2f((sc[i][j] - mx) * sl2);
+                sc[i][j] = e;
+                sum += e;
+            }
+        sum += __shfl_xor(sum, 16, 64);
+        sum += __shfl_xor(sum, 32, 64);
+        __syncthreads();   // every wave has read the maxima
+        if (q4 == 0) red[w * 16 + l16] = sum;
+        __syncthreads();
+        sum = red[l16] + red[16 + l16] + red[32 + l16] + red[48 + l16];
+        const float inv = sum > 0.f ? 1.0f / sum : 0.f;
+        uint32_t* Pw = reinterpret_cast<uint32_t*>(Pl);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int kb = w + 4 * i;
+            if (kb < KB) {
+                const int ch = (2 * kb + (q4 >> 1)) ^ (l16 & swm);
+                const int base = (l16 * SC + ch) * 4 + 2 * (q4 & 1);
+                Pw[base] = pack_bf16x2(sc[i][0] * inv, sc[i][1] * inv);
+                Pw[base + 1] = pack_bf16x2(sc[i][2] * inv, sc[i][3] * inv);
+            }
+        }
+        __syncthreads();
+        // (d) O^T[d][head] = V_sel^T . P^T, d blocks db = w, w+4, ...
+#pragma unroll
+        for (int i = 0; i < D / 64; ++i) {
+            const int db = w + 4 * i;
+            const int dr = 16 * db + l16;
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            for (int ks = 0; ks < S / 32; ++ks) {
+                const u32x4 a = Vt[dr * SC + ((4 * ks + q4) ^ (dr & swm))];
+                const u32x4 bb = Pl[l16 * SC + ((4 * ks + q4) ^ (l16 & swm))];
+                acc = mfma_16x16x32(a, bb, acc);
+            }
+            if (l16 < G) {
+                const u32x2 o2 = {pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3])};
+                *reinterpret_cast<u32x2*>(O + (((size_t)b * p.T + u) * p.H_q + hq) * D + 16 * db + 4 * q4) = o2;
+            }
+        }
+        __syncthreads();   // V^T and P are rewritten for the next KV head
+    }
+}
+
+// grid (ceil(T/64), H_q, B), 256 threads: query positions u0 + 16w + l16 of
+// head hq; 64-key chunks up to the tile's last position.  LDS: K chunk
+// [64][D], V^T chunk [D][64], P per wave [16][64] (bf16).
+template <int D>
+__global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
+    constexpr int DC = D / 8;
+    constexpr int KSW = (DC < 16 ? DC : 16) - 1;
+    __shared__ u32x4 Kl[64 * DC];          // row key: chunk c at (c ^ (key & KSW))
+    __shared__ u32x4 Vt[D * 8];            // row d: 8 chunks of 8 keys, chunk c at (c ^ (d & 7))
+    __shared__ u32x4 Pl[4][16 * 8];        // per wave, row = position: chunk c at (c ^ (pos & 7))
+    const int u0 = blockIdx.x * 64, hq = blockIdx.y, b = blockIdx.z;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, q4 = lane >> 4;
+    const int G = p.H_q / p.H_kv, kvh = hq / G;
+    const int u = u0 + 16 * w + l16;       // this lane's query column
+    const uint16_t* Q = reinterpret_cast<const uint16_t*>(p.q);
+    const uint16_t* K = reinterpret_cast<const uint16_t*>(p.k);
+    const uint16_t* V = reinterpret_cast<const uint16_t*>(p.v);
+    uint16_t* O = reinterpret_cast<uint16_t*>(p.o);
+    const float sl2 = kLog2e / sqrtf((float)D);
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    u32x4 qop[D / 32];
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks)
+        qop[ks] = u < p.T ? *reinterpret_cast<const u32x4*>(Q + (((size_t)b * p.T + u) * p.H_q + hq) * D + 32 * ks + 8 * q4)
+                          : zero;
+    f32x4 acc[D / 16];
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m = -INFINITY, l = 0.f;
+    const int last = (u0 + 63 < p.T ? u0 + 63 : p.T - 1);
+    for (int kc0 = 0; kc0 <= last; kc0 += 64) {
+        __syncthreads();   // the previous chunk's K and V^T are consumed
+        for (int it = tid; it < 64 * DC; it += 256) {
+            const int kr = it / DC, c = it % DC, t = kc0 + kr;
+            Kl[kr * DC + (c ^ (kr & KSW))] =
+                t < p.T ? *reinterpret_cast<const u32x4*>(K + kv_row(p, b, t, kvh) + 8 * c) : zero;
+        }
+        uint32_t* Vw = reinterpret_cast<uint32_t*>(Vt);
+        for (int it = tid; it < 32 * DC; it += 256) {
+            const int pr = it % 32, c = it / 32, k0 = 2 * pr, t = kc0 + k0;
+            const u32x4 a = t < p.T ? *reinterpret_cast<const u32x4*>(V + kv_row(p, b, t, kvh) + 8 * c) : zero;
+            const u32x4 cc = t + 1 < p.T ? *reinterpret_cast<const u32x4*>(V + kv_row(p, b, t + 1, kvh) + 8 * c) : zero;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int d = 8 * c + i;
+                Vw[(d * 8 + ((k0 >> 3) ^ (d & 7))) * 4 + ((k0 & 7) >> 1)] = pair_word(a, cc, i);
+            }
+        }
+        __syncthreads();
+        // scores^T[key][position] for 4 key blocks of 16
+        f32x4 sc[4];
+        float cm = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+            sc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            const int kr = kb * 16 + l16;
+#pragma unroll
+            for (int ks = 0; ks < D / 32; ++ks)
+                sc[kb] = mfma_16x16x32(Kl[kr * DC + ((4 * ks + q4) ^ (kr & KSW))], qop[ks], sc[kb]);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int key = kc0 + kb * 16 + 4 * q4 + j;
+                sc[kb][j] = key <= u ? sc[kb][j] : -INFINITY;
+                cm = fmaxf(cm, sc[kb][j]);
+            }
+        }
+        cm = fmaxf(cm, __shfl_xor(cm, 16, 64));
+        cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
+        const float mn = fmaxf(m, cm);   // finite: chunk 0 holds key 0 <= u
+        const float alpha = exp2f((m - mn) * sl2);
+        float rs = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float e = sc[kb][j] == -INFINITY ? 0.f : exp2f((sc[kb][j] - mn) * sl2);
+                sc[kb][j] = e;
+                rs += e;
+            }
+        rs += __shfl_xor(rs, 16, 64);
+        rs += __shfl_xor(rs, 32, 64);
+        l = l * alpha + rs;
+        m = mn;
+#pragma unroll
+        for (int db = 0; db < D / 16; ++db)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[db][j] *= alpha;
+        uint32_t* Pw = reinterpret_cast<uint32_t*>(Pl[w]);
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+            const int ch = (2 * kb + (q4 >> 1)) ^ (l16 & 7);
+            const int base = (l16 * 8 + ch) * 4 + 2 * (q4 & 1);
+            Pw[base] = pack_bf16x2(sc[kb][0], sc[kb][1]);
+            Pw[base + 1] = pack_bf16x2(sc[kb][2], sc[kb][3]);
+        }
+        wave_lds_sync();
+        // O^T[d][position] += V^T . P^T
+#pragma unroll
+        for (int db = 0; db < D / 16; ++db) {
+            const int dr = 16 * db + l16;
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks)
+                acc[db] = mfma_16x16x32(Vt[dr * 8 + ((4 * ks + q4) ^ (dr & 7))],
+                                        Pl[w][l16 * 8 + ((4 * ks + q4) ^ (l16 & 7))], acc[db]);
+        }
+        wave_lds_sync();   // this wave's P row is rewritten next chunk
+    }
+    if (u < p.T) {
+        const float inv = 1.0f / l;
+#pragma unroll
+        for (int db = 0; db < D / 16; ++db) {
+            const u32x2 o2 = {pack_bf16x2(acc[db][0] * inv, acc[db][1] * inv),
+                              pack_bf16x2(acc[db][2] * inv, acc[db][3] * inv)};
+            *reinterpret_cast<u32x2*>(O + (((size_t)b * p.T + u) * p.H_q + hq) * D + 16 * db + 4 * q4) = o2;
+        }
+    }
+}
+
+constexpr int kSelCacheMax = 16384;   // rows up to this length keep their keys in LDS
+
+}  // namespace
+
+size_t replay_sparse_lds_bytes(int D, int S) { return (size_t)(D * S + 16 * S) * 2 + 128 * sizeof(float); }
+
+hipError_t launch_topS_select(const float* A, int32_t* idx, int B, int T, int S, hipStream_t stream) {
+    if (B == 0 || T == 0) return hipSuccess;
+    const dim3 grid(T, B);
+    if (T <= kSelCacheMax)
+        hipLaunchKernelGGL(k_topS_select<true>, grid, dim3(256), (size_t)T * 4, stream, A, idx, T, S);
+    else
+        hipLaunchKernelGGL(k_topS_select<false>, grid, dim3(256), 0, stream, A, idx, T, S);
+    return hipGetLastError();
+}
+
+hipError_t launch_replay_attention(const ReplayProblem& p, hipStream_t stream) {
+    if (p.B == 0 || p.T == 0) return hipSuccess;
+    if (p.idx) {
+        const dim3 grid(p.T, p.B);
+        const size_t lds = replay_sparse_lds_bytes(p.D, p.S);
+        if (p.D == 128) hipLaunchKernelGGL(k_sparse_attn<128>, grid, dim3(256), lds, stream, p);
+        else hipLaunchKernelGGL(k_sparse_attn<64>, grid, dim3(256), lds, stream, p);
+    } else {
+        const dim3 grid((p.T + 63) / 64, p.H_q, p.B);
+        if (p.D == 128) hipLaunchKernelGGL(k_causal_attn<128>, grid, dim3(256), 0, stream, p);
+        else hipLaunchKernelGGL(k_causal_attn<64>, grid, dim3(256), 0, stream, p);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace mot

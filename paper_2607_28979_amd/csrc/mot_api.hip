@@ -413,4 +413,64 @@ mot_status mot_restore_kv(const void* act, const int32_t* layer_map, const void*
     return MOT_OK;
 }
 
+namespace {
+mot_status check_replay(const mot_replay_shapes* s, bool need_s) {
+    if (!s) return fail(MOT_ERR_NULL_ARG, "shapes is NULL");
+    if (s->B < 0 || s->T < 0 || (int64_t)s->B * s->T > (int64_t)1 << 26)
+        return fail(MOT_ERR_BAD_SHAPE, "B=%d T=%d: need B, T >= 0 and B*T <= 2^26", s->B, s->T);
+    if (s->H_q < 1 || s->H_kv < 1 || s->H_q % s->H_kv || s->D < 1)
+        return fail(MOT_ERR_BAD_SHAPE, "H_q=%d H_kv=%d D=%d: need H_q a positive multiple of H_kv and D >= 1",
+                    s->H_q, s->H_kv, s->D);
+    if (s->kv_layout != MOT_LAYOUT_BTHD && s->kv_layout != MOT_LAYOUT_BHTD)
+        return fail(MOT_ERR_BAD_SHAPE, "kv_layout must be MOT_LAYOUT_BTHD or MOT_LAYOUT_BHTD");
+    if (need_s && s->S < 1) return fail(MOT_ERR_BAD_SHAPE, "S=%d must be >= 1", s->S);
+    if (s->D != 64 && s->D != 128)
+        return fail(MOT_ERR_UNSUPPORTED, "D=%d: replay attention supports head dims 64 and 128", s->D);
+    if (s->H_q / s->H_kv > 16)
+        return fail(MOT_ERR_UNSUPPORTED, "%d query heads per KV head (at most 16)", s->H_q / s->H_kv);
+    if (need_s && (s->S % 32 || s->S > 256 || replay_sparse_lds_bytes(s->D, s->S) > 65536))
+        return fail(MOT_ERR_UNSUPPORTED, "S=%d: need a multiple of 32, at most 256 (192 when D = 128)", s->S);
+    return MOT_OK;
+}
+}  // namespace
+
+mot_status mot_topS_select(const float* A, int32_t* idx, const mot_replay_shapes* s, hipStream_t stream) {
+    g_err[0] = 0;
+    if (!s) return fail(MOT_ERR_NULL_ARG, "shapes is NULL");
+    if (s->B < 0 || s->T < 0 || (int64_t)s->B * s->T > (int64_t)1 << 26 || s->S < 1)
+        return fail(MOT_ERR_BAD_SHAPE, "B=%d T=%d S=%d: need B, T >= 0, B*T <= 2^26, S >= 1", s->B, s->T, s->S);
+    if ((int64_t)s->B * s->T == 0) return MOT_OK;
+    if (!A || !idx) return fail(MOT_ERR_NULL_ARG, "A and idx are required");
+    if ((reinterpret_cast<uintptr_t>(A) & 3) || (reinterpret_cast<uintptr_t>(idx) & 3))
+        return fail(MOT_ERR_MISALIGNED, "A and idx must be 4-byte aligned");
+    if (overlaps(A, (size_t)s->B * s->T * s->T * 4, idx, (size_t)s->B * s->T * s->S * 4))
+        return fail(MOT_ERR_BAD_SHAPE, "idx overlaps A");
+    hipError_t e = launch_topS_select(A, idx, s->B, s->T, s->S, stream);
+    if (e != hipSuccess) return fail(MOT_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
+    return MOT_OK;
+}
+
+mot_status mot_replay_attention(const void* q, const void* k, const void* v, const int32_t* idx, void* o,
+                                const mot_replay_shapes* s, hipStream_t stream) {
+    g_err[0] = 0;
+    mot_status st = check_replay(s, idx != nullptr);
+    if (st != MOT_OK) return st;
+    if ((int64_t)s->B * s->T == 0) return MOT_OK;
+    if (!q || !k || !v || !o) return fail(MOT_ERR_NULL_ARG, "q, k, v and o are required");
+    const void* ptrs[] = {q, k, v, o, idx ? static_cast<const void*>(idx) : q};
+    for (const void* x : ptrs)
+        if (!aligned16(x)) return fail(MOT_ERR_MISALIGNED, "device pointer %p is not 16-byte aligned", x);
+    const size_t qo = (size_t)s->B * s->T * s->H_q * s->D * 2, kv = (size_t)s->B * s->T * s->H_kv * s->D * 2;
+    if (overlaps(o, qo, q, qo) || overlaps(o, qo, k, kv) || overlaps(o, qo, v, kv) ||
+        (idx && overlaps(o, qo, idx, (size_t)s->B * s->T * s->S * 4)))
+        return fail(MOT_ERR_BAD_SHAPE, "o overlaps an input");
+    ReplayProblem p;
+    p.q = q; p.k = k; p.v = v; p.idx = idx; p.o = o;
+    p.B = s->B; p.T = s->T; p.H_q = s->H_q; p.H_kv = s->H_kv; p.D = s->D; p.S = idx ? s->S : 0;
+    p.kv_layout = s->kv_layout;
+    hipError_t e = launch_replay_attention(p, stream);
+    if (e != hipSuccess) return fail(MOT_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
+    return MOT_OK;
+}
+
 }  // extern "C"

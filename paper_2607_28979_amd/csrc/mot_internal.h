@@ -75,6 +75,20 @@ struct ProjProblem {
 };
 hipError_t launch_bf16_project(const ProjProblem& p, int n_layers, hipStream_t stream);
 
+// Context replay attention (Top-S sparse, or full causal when idx == nullptr).
+struct ReplayProblem {
+    const void* q;        // bf16 [B][T][H_q][D]
+    const void* k;        // bf16 [B][T][H_kv][D] (BTHD) or [B][H_kv][T][D] (BHTD)
+    const void* v;
+    const int32_t* idx;   // [B][T][S] key sets, -1 padded; nullptr = full causal
+    void* o;              // bf16 [B][T][H_q][D]
+    int32_t B, T, H_q, H_kv, D, S, kv_layout;
+};
+
+size_t replay_sparse_lds_bytes(int D, int S);
+hipError_t launch_topS_select(const float* A, int32_t* idx, int B, int T, int S, hipStream_t stream);
+hipError_t launch_replay_attention(const ReplayProblem& p, hipStream_t stream);
+
 // Kernel launchers (each enqueues on `stream`; return hipGetLastError()).
 hipError_t launch_router(const Problem& p, const UnitTab& ut, bool bf16, hipStream_t stream);
 hipError_t launch_f32_gemm1(const Problem& p, const UnitTab& ut, hipStream_t stream);

@@ -168,3 +168,55 @@ def activations(L: int, B: int, T: int, d_act: int, seed: int, dtype: str = "bf1
     if dtype == "bf16":
         round_to_bf16(a)
     return a
+
+
+def replay_inputs(B: int, T: int, H_q: int, H_kv: int, D: int, seed: int, kv_layout: int = 0):
+    """Replay-attention operands from PCG64(40_000 + seed), drawn in the order
+    q [B][T][H_q][D], k, v [B][T][H_kv][D], all N(0, 1) and rounded to bf16;
+    k and v are returned transposed to [B][H_kv][T][D] when kv_layout = 1."""
+    rng = np.random.Generator(np.random.PCG64(40_000 + seed))
+    q = round_to_bf16(rng.standard_normal((B, T, H_q, D), dtype=np.float32))
+    k = round_to_bf16(rng.standard_normal((B, T, H_kv, D), dtype=np.float32))
+    v = round_to_bf16(rng.standard_normal((B, T, H_kv, D), dtype=np.float32))
+    if kv_layout == 1:
+        k = np.ascontiguousarray(k.transpose(0, 2, 1, 3))
+        v = np.ascontiguousarray(v.transpose(0, 2, 1, 3))
+    return q, k, v
+
+
+def source_attention(B: int, T: int, seed: int, window: float = 64.0, sink: float = 4.0,
+                     hitters: float = 2.0, noise: float = 0.5) -> np.ndarray:
+    """Stand-in for a source model's head-averaged causal attention map,
+    fp32 [B][T][T] from PCG64(50_000 + seed): row u is a softmax over v <= u
+    of  -|u - v|/window + sink*[v = 0] + hitters*h[b][v] + noise*eps[b][u][v]
+    (locality, an attention sink at position 0, per-position heavy hitters
+    h ~ N(0, 1), entry noise eps ~ N(0, 1)); entries v > u are 0.  Drawn:
+    h [B][T], then eps row block by row block."""
+    rng = np.random.Generator(np.random.PCG64(50_000 + seed))
+    h = rng.standard_normal((B, T), dtype=np.float32)
+    A = np.empty((B, T, T), np.float32)
+    pos = np.arange(T, dtype=np.float32)
+    blk = max(1, min(T, (1 << 22) // max(T, 1)))
+    lg = np.empty((blk, T), np.float32)
+    eps = np.empty((blk, T), np.float32)
+    fut = np.empty((blk, T), bool)
+    for b in range(B):
+        col = hitters * h[b]
+        col[0] += sink
+        for u0 in range(0, T, blk):
+            n = min(T, u0 + blk) - u0
+            g, e, f = lg[:n], eps[:n], fut[:n]
+            rng.standard_normal(out=e, dtype=np.float32)
+            np.subtract(pos[u0:u0 + n, None], pos[None, :], out=g)
+            np.abs(g, out=g)
+            g *= np.float32(-1.0 / window)
+            g += col[None, :]
+            e *= np.float32(noise)
+            g += e
+            np.greater(pos[None, :], pos[u0:u0 + n, None], out=f)
+            g[f] = -np.inf
+            g -= g.max(axis=1, keepdims=True)
+            np.exp(g, out=g)
+            g /= g.sum(axis=1, keepdims=True)
+            A[b, u0:u0 + n] = g
+    return A

@@ -26,7 +26,7 @@ def lib():
 def _decls():
     txt = open(HEADER).read()
     txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
-    return sorted(set(re.findall(r"\b(mot_[a-z_]+)\s*\(", txt)))
+    return sorted(set(re.findall(r"\b(mot_[A-Za-z_]+)\s*\(", txt)))
 
 
 def test_exports_every_declared_symbol(lib):
@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert mb.abi_version() == 2
+    assert mb.abi_version() == 3
 
 
 def test_status_strings(lib):
@@ -188,7 +188,8 @@ def test_header_struct_layout_matches_binding(tmp_path):
     lays them out, equal the ctypes mirrors in the binding."""
     import subprocess
     structs = {"mot_shapes": mb._Shapes, "mot_restore_shapes": mb._RestoreShapes,
-               "mot_translator_weights": mb._TW, "mot_router_weights": mb._RW}
+               "mot_translator_weights": mb._TW, "mot_router_weights": mb._RW,
+               "mot_replay_shapes": mb._ReplayShapes}
     lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "mot.h"', "int main(void) {"]
     for cname, cls in structs.items():
         lines.append('printf("%s size %%zu\\n", sizeof(%s));' % (cname, cname))

@@ -1,0 +1,187 @@
+"""GPU parity of the context-replay step (paper App. C.4): Top-S source-guided
+key selection and replay attention, through the C ABI, against the oracle.
+
+* selection (mot_topS_select): bit-exact key sets on maps with many ties,
+  ragged row lengths (rows shorter than S, rows across 256-element chunks),
+  and a 16500-token map (rows too long for the LDS-cached kernel) on sampled
+  rows;
+* sparse attention over the selected sets (grouped-query heads, both KV
+  layouts, head dims 64 and 128, S = 32 .. 128), sets with padding and
+  out-of-range entries, an all-empty set (zeros);
+* full causal attention (the bottom L_Full layers) with a ragged last tile;
+* the replay benchmark's layer shape (Qwen2.5-7B target heads, T = 8192,
+  S = 128) on sampled rows.
+Bar: key sets bit-exact; attention outputs (bf16) within a relative
+Frobenius error of 2e-2 of the fp64 oracle.
+"""
+import numpy as np
+import pytest
+
+from paper_2607_28979_amd import binding as mb
+from paper_2607_28979_amd.inputs import replay_inputs, source_attention
+
+from helpers import TOL, rel_frob, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu_select(A, S):
+    import torch
+    B, T = A.shape[0], A.shape[1]
+    a = torch.from_numpy(np.ascontiguousarray(A, dtype=np.float32)).cuda()
+    idx = torch.full((B, T, S), -7, dtype=torch.int32, device="cuda")
+    mb.topS_select(a, idx, B, T, S)
+    torch.cuda.synchronize()
+    return idx
+
+
+def _gpu_attention(q, k, v, idx, kv_layout=0):
+    """idx: None, or a device / numpy int32 [B][T][S] array."""
+    import torch
+    B, T, Hq, D = q.shape
+    Hkv = k.shape[2] if kv_layout == 0 else k.shape[1]
+    o = torch.full((B, T, Hq, D), 9.0, dtype=torch.bfloat16, device="cuda")
+    ii = idx
+    if isinstance(idx, np.ndarray):
+        ii = torch.from_numpy(np.ascontiguousarray(idx, dtype=np.int32)).cuda()
+    S = 0 if idx is None else idx.shape[2]
+    mb.replay_attention(to_dev(q, "bf16"), to_dev(k, "bf16"), to_dev(v, "bf16"), ii, o, B=B, T=T, H_q=Hq,
+                        H_kv=Hkv, D=D, S=S, kv_layout=kv_layout)
+    torch.cuda.synchronize()
+    return o.float().cpu().numpy().astype(np.float64)
+
+
+@pytest.mark.parametrize("B,T,S", [(2, 300, 32), (1, 517, 128), (3, 70, 64)])
+def test_topS_select_bit_exact(B, T, S, oracle_built):
+    """Coarsely quantised maps (many equal values) so the lower-position tie
+    rule decides many sets."""
+    from oracle import oracle_topS_select
+    print("case select", B, T, S, flush=True)
+    rng = np.random.default_rng(T + S)
+    A = (np.round(rng.random((B, T, T)) * 16) / 16).astype(np.float32)
+    got = _gpu_select(A, S).cpu().numpy()
+    want = oracle_topS_select(A, S)
+    assert np.array_equal(got, want), int((got != want).sum())
+
+
+def test_topS_select_structured_map(oracle_built):
+    from oracle import oracle_topS_select
+    A = source_attention(2, 600, seed=1)
+    got = _gpu_select(A, 128).cpu().numpy()
+    assert np.array_equal(got, oracle_topS_select(A, 128))
+
+
+def test_topS_select_long_rows_sampled(oracle_built):
+    """T = 16500 exceeds the LDS row cache: the uncached kernel, on sampled
+    rows (first, last, and around the 16384 boundary)."""
+    from oracle import oracle_topS_rows
+    T, S = 16500, 128
+    print("case select long T", T, flush=True)
+    A = source_attention(1, T, seed=2)
+    got = _gpu_select(A, S).cpu().numpy()
+    rows = [(0, u) for u in (0, 127, 128, 5000, 16383, 16384, 16385, T - 1)]
+    want = oracle_topS_rows(A, S, rows)
+    for i, (b, u) in enumerate(rows):
+        assert np.array_equal(got[b, u], want[i]), u
+
+
+ATTN = [  # B, T, H_q, H_kv, D, S, kv_layout
+    (2, 200, 8, 2, 128, 64, 0),
+    (1, 260, 28, 4, 128, 128, 1),     # Qwen2.5-7B heads (7 per KV head)
+    (2, 150, 4, 4, 64, 32, 0),        # one query head per KV head, 2 of 4 waves without key blocks
+    (1, 300, 12, 2, 64, 128, 1),      # Qwen2.5-1.5B heads
+]
+
+
+@pytest.mark.parametrize("case", ATTN, ids=["B%d-T%d-Hq%d-Hkv%d-D%d-S%d-l%d" % c for c in ATTN])
+def test_sparse_attention_parity(case, oracle_built):
+    from oracle import oracle_replay_attention, oracle_topS_select
+    B, T, Hq, Hkv, D, S, lay = case
+    print("case sparse", case, flush=True)
+    q, k, v = replay_inputs(B, T, Hq, Hkv, D, seed=T + D, kv_layout=lay)
+    A = source_attention(B, T, seed=T)
+    idx = oracle_topS_select(A, S)
+    got = _gpu_attention(q, k, v, idx, lay)
+    want = oracle_replay_attention(q, k, v, idx, kv_layout=lay)
+    err = rel_frob(got, want)
+    print("  rel-Frobenius %.3e" % err, flush=True)
+    assert err <= TOL["bf16"]
+    # per position too: no row may be off even when the total is fine
+    worst = max(rel_frob(got[b, u], want[b, u]) for b in range(B) for u in range(T))
+    assert worst <= 2 * TOL["bf16"], worst
+
+
+def test_sparse_attention_padding_and_invalid_entries(oracle_built):
+    """Entries that are -1 or lie after the query position are skipped; a set
+    with no valid entry gives zeros."""
+    from oracle import oracle_replay_attention
+    B, T, Hq, Hkv, D, S = 1, 96, 4, 2, 128, 32
+    q, k, v = replay_inputs(B, T, Hq, Hkv, D, seed=5)
+    rng = np.random.default_rng(5)
+    idx = np.full((B, T, S), -1, np.int32)
+    for u in range(T):
+        n = int(rng.integers(1, min(u + 1, S - 1) + 1))
+        idx[0, u, :n] = np.sort(rng.choice(u + 1, size=n, replace=False))
+    bad = idx.copy()
+    bad[0, :, S - 1] = np.minimum(np.arange(T) + 5, T + 100)   # after u (or past T): skipped
+    bad[0, 10] = -1                                             # empty set
+    got = _gpu_attention(q, k, v, bad)
+    want = oracle_replay_attention(q, k, v, idx)
+    assert np.array_equal(got[0, 10], np.zeros((Hq, D)))
+    keep = np.ones(T, bool)
+    keep[10] = False
+    assert rel_frob(got[0, keep], want[0, keep]) <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("B,T,Hq,Hkv,D,lay", [(1, 200, 4, 2, 128, 0), (2, 130, 6, 1, 64, 1), (1, 64, 2, 2, 128, 0)])
+def test_causal_attention_parity(B, T, Hq, Hkv, D, lay, oracle_built):
+    from oracle import oracle_replay_attention
+    print("case causal", B, T, Hq, Hkv, D, lay, flush=True)
+    q, k, v = replay_inputs(B, T, Hq, Hkv, D, seed=3 * T + D, kv_layout=lay)
+    got = _gpu_attention(q, k, v, None, lay)
+    want = oracle_replay_attention(q, k, v, None, kv_layout=lay)
+    err = rel_frob(got, want)
+    print("  rel-Frobenius %.3e" % err, flush=True)
+    assert err <= TOL["bf16"]
+    worst = max(rel_frob(got[b, u], want[b, u]) for b in range(B) for u in range(T))
+    assert worst <= 2 * TOL["bf16"], worst
+
+
+def test_sparse_with_full_sets_equals_causal(oracle_built):
+    """With S >= T every set is the whole causal prefix, so the sparse kernel
+    and the causal kernel compute the same attention."""
+    B, T, Hq, Hkv, D = 1, 120, 4, 2, 64
+    q, k, v = replay_inputs(B, T, Hq, Hkv, D, seed=9)
+    A = source_attention(B, T, seed=9)
+    idx = _gpu_select(A, 128)
+    sp = _gpu_attention(q, k, v, idx)
+    fu = _gpu_attention(q, k, v, None)
+    assert rel_frob(sp, fu) <= 1e-2
+
+
+def test_replay_layer_full_size_sampled(oracle_built):
+    """The replay benchmark's layer: Qwen2.5-7B target (28 query heads on 4
+    KV heads of 128), T = 8192, S = 128: selection and sparse attention over
+    the whole layer on the GPU, sampled rows checked against the oracle; the
+    causal kernel on the same layer, sampled rows."""
+    from oracle import oracle_replay_attention_rows, oracle_topS_rows
+    from paper_2607_28979_amd.configs import REPLAY
+    w = REPLAY
+    print("case replay layer full size", flush=True)
+    q, k, v = replay_inputs(w.B, w.T, w.H_q, w.H_kv, w.D, seed=w.seed)
+    A = source_attention(w.B, w.T, seed=w.seed)
+    idx = _gpu_select(A, w.S)
+    rows = [(0, u) for u in (0, 1, 127, 128, 129, 4095, 6000, w.T - 1)]
+    want_idx = oracle_topS_rows(A, w.S, rows)
+    idx_h = idx.cpu().numpy()
+    for i, (b, u) in enumerate(rows):
+        assert np.array_equal(idx_h[b, u], want_idx[i]), u
+    got = _gpu_attention(q, k, v, idx)
+    want = oracle_replay_attention_rows(q, k, v, idx_h, rows)
+    for i, (b, u) in enumerate(rows):
+        assert rel_frob(got[b, u], want[i]) <= TOL["bf16"], u
+    got_c = _gpu_attention(q, k, v, None)
+    rows_c = [(0, u) for u in (0, 63, 64, 3000, w.T - 1)]
+    want_c = oracle_replay_attention_rows(q, k, v, None, rows_c)
+    for i, (b, u) in enumerate(rows_c):
+        assert rel_frob(got_c[b, u], want_c[i]) <= TOL["bf16"], u

@@ -578,3 +578,22 @@ def test_replay_attention_special_cases(oracle_built):
                                rtol=1e-13, atol=1e-15)
     with pytest.raises(ValueError):   # a key after the query position
         oracle_replay_attention(q, k, v, np.full((B, T, 1), T - 1, np.int32))
+
+
+def test_replay_sampled_rows_equal_full(oracle_built):
+    """The sampled-row entry points return exactly the rows of the full ones."""
+    from oracle import (oracle_replay_attention, oracle_replay_attention_rows, oracle_topS_rows,
+                        oracle_topS_select)
+    rng = np.random.default_rng(41)
+    B, T, Hq, Hkv, D, S = 2, 10, 4, 1, 8, 3
+    q = rng.standard_normal((B, T, Hq, D)).astype(np.float32)
+    k = rng.standard_normal((B, T, Hkv, D)).astype(np.float32)
+    v = rng.standard_normal((B, T, Hkv, D)).astype(np.float32)
+    A = rng.random((B, T, T)).astype(np.float32)
+    rows = [(0, 0), (1, 9), (0, 4), (1, 2)]
+    idx = oracle_topS_select(A, S)
+    assert np.array_equal(oracle_topS_rows(A, S, rows), np.stack([idx[b, u] for b, u in rows]))
+    for sets in (idx, None):
+        full = oracle_replay_attention(q, k, v, sets)
+        assert np.array_equal(oracle_replay_attention_rows(q, k, v, sets, rows),
+                              np.stack([full[b, u] for b, u in rows]))
