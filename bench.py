@@ -71,6 +71,10 @@ def main():
                     help="time the activation variant MoT-h instead: one activation stream per "
                          "layer translated (Qwen2.5-1.5B -> 7B widths 1536 -> 3584), then the "
                          "target K/V restored through its key/value projections")
+    ap.add_argument("--replay", action="store_true",
+                    help="time the context replay after translation instead: Top-S source-guided "
+                         "sparse attention over every Qwen2.5-7B target layer of an 8K context "
+                         "(the bottom two layers with full causal attention)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain device copy of MIB MiB (a known-size "
                          "reference for the HBM byte counters of a profiler run)")
@@ -84,6 +88,8 @@ def main():
 
     if args.moth:
         return bench_moth(args)
+    if args.replay:
+        return bench_replay(args)
 
     import torch
     from paper_2607_28979_amd import binding as mb
@@ -347,6 +353,153 @@ def cpu_baseline_moth(w, inp, lm, proj, rows):
             "sample": "first %d of %d tokens, all %d layers (translation + K/V restoration), fp64"
                       % (rows, w.n_tok, len(units)),
             "seconds": round(dt, 2)}
+
+
+def bench_replay(args):
+    """Context replay (App. C.4): one step = for every target layer, either
+    the full causal attention (bottom L_full layers) or mot_topS_select on
+    the paired source layer's head-averaged attention map followed by
+    mot_replay_attention over the selected sets."""
+    import torch
+    from paper_2607_28979_amd import binding as mb
+    from paper_2607_28979_amd.configs import REPLAY
+    from paper_2607_28979_amd.inputs import bf16_bits, replay_inputs, source_attention
+
+    w = REPLAY
+    torch.cuda.set_device(0)
+    pi = mb.depth_ratio_map(w.L_src, w.L_tgt)
+    t0 = time.time()
+
+    def dev(a):
+        return torch.from_numpy(bf16_bits(a).view(np.int16)).cuda().view(torch.bfloat16)
+
+    layers = []
+    for l in range(w.L_tgt):
+        q, k, v = replay_inputs(w.B, w.T, w.H_q, w.H_kv, w.D, seed=w.seed + 100 * l)
+        layers.append((dev(q), dev(k), dev(v)))
+    maps = {}
+    for l in range(w.L_full, w.L_tgt):
+        i = int(pi[l])
+        if i not in maps:
+            maps[i] = torch.from_numpy(source_attention(w.B, w.T, seed=w.seed + 1000 * i)).cuda()
+    log("inputs generated in %.1f s (%d source maps)" % (time.time() - t0, len(maps)))
+    idx = torch.empty((w.B, w.T, w.S), dtype=torch.int32, device="cuda")
+    out = torch.empty((w.B, w.T, w.H_q, w.D), dtype=torch.bfloat16, device="cuda")
+    stream = torch.cuda.current_stream()
+    ev = {"select": [], "sparse": [], "causal": []}
+
+    def step(record):
+        for l in range(w.L_tgt):
+            q, k, v = layers[l]
+            if l < w.L_full:
+                e0 = torch.cuda.Event(enable_timing=True) if record else None
+                e1 = torch.cuda.Event(enable_timing=True) if record else None
+                if record: e0.record(stream)
+                mb.replay_attention(q, k, v, None, out, B=w.B, T=w.T, H_q=w.H_q, H_kv=w.H_kv, D=w.D)
+                if record:
+                    e1.record(stream)
+                    ev["causal"].append((e0, e1))
+            else:
+                es = [torch.cuda.Event(enable_timing=True) for _ in range(3)] if record else None
+                if record: es[0].record(stream)
+                mb.topS_select(maps[int(pi[l])], idx, w.B, w.T, w.S)
+                if record: es[1].record(stream)
+                mb.replay_attention(q, k, v, idx, out, B=w.B, T=w.T, H_q=w.H_q, H_kv=w.H_kv, D=w.D, S=w.S)
+                if record:
+                    es[2].record(stream)
+                    ev["select"].append((es[0], es[1]))
+                    ev["sparse"].append((es[1], es[2]))
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    log("warmup done (%d steps)" % args.warmup)
+    torch.cuda.synchronize()
+    t_begin = time.perf_counter()
+    for _ in range(args.steps):
+        step(True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_begin
+    ms_per_step = wall * 1e3 / args.steps
+    avg = {kk: float(np.mean([a.elapsed_time(b) for a, b in vv])) for kk, vv in ev.items()}
+    log("timed %d steps: wall %.3f ms/step; per launch: select %.3f ms, sparse %.3f ms, causal %.3f ms"
+        % (args.steps, ms_per_step, avg["select"], avg["sparse"], avg["causal"]))
+    # per-launch algorithmic figures
+    n_tok = w.B * w.T
+    sp_flops = 4.0 * w.H_q * w.D * w.B * sum(min(u + 1, w.S) for u in range(w.T))
+    ca_flops = 4.0 * w.H_q * w.D * w.B * w.T * (w.T + 1) / 2
+    sel_bytes = 4.0 * w.B * w.T * (w.T + 1) / 2 + 4.0 * n_tok * w.S        # causal half of A once, idx
+    # sparse attention: q and o once, idx once, each selected K and V row once per (query, KV head)
+    sp_gather = 2.0 * 2 * w.D * w.H_kv * w.B * sum(min(u + 1, w.S) for u in range(w.T))
+    sp_bytes = 2.0 * 2 * n_tok * w.H_q * w.D + 4.0 * n_tok * w.S + sp_gather
+    peak_bf16 = PEAK_TFLOPS["bf16"]
+    rows = {
+        "select": {"bound": "hbm", "achieved": sel_bytes / (avg["select"] / 1e3) / 1e9, "peak": PEAK_HBM_GBS,
+                   "unit": "GB/s", "alg_bytes_per_launch": sel_bytes, "ms": avg["select"]},
+        "sparse": {"bound": "hbm", "achieved": sp_bytes / (avg["sparse"] / 1e3) / 1e9, "peak": PEAK_HBM_GBS,
+                   "unit": "GB/s", "alg_bytes_per_launch": sp_bytes, "ms": avg["sparse"],
+                   "tflops": sp_flops / (avg["sparse"] / 1e3) / 1e12},
+        "causal": {"bound": "mfma", "achieved": ca_flops / (avg["causal"] / 1e3) / 1e12, "peak": peak_bf16,
+                   "unit": "TFLOP/s", "alg_flops_per_launch": ca_flops, "ms": avg["causal"]},
+    }
+    for r in rows.values():
+        r["achieved"] = round(r["achieved"], 2)
+        r["frac"] = round(r["achieved"] / r["peak"], 4)
+        r["ms"] = round(r["ms"], 4)
+    share = {"select": avg["select"] * (w.L_tgt - w.L_full), "sparse": avg["sparse"] * (w.L_tgt - w.L_full),
+             "causal": avg["causal"] * w.L_full}
+    dom = max(share, key=share.get)
+    kname = {"select": "k_topS_select", "sparse": "k_sparse_attn", "causal": "k_causal_attn"}
+    roof = dict(rows[dom], kernel=kname[dom], traffic=None)
+    cpu = None if args.no_cpu_baseline else cpu_baseline_replay(w, args.cpu_rows)
+    out_line = {
+        "metric": "replayed context tokens/sec (all target layers, Top-S source-guided sparse attention)",
+        "value": round(n_tok / (ms_per_step / 1e3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded numpy; Qwen2.5-7B head shapes, structured source attention maps)",
+        "config": {"workload": w.name, "L_tgt": w.L_tgt, "L_full": w.L_full, "B": w.B, "T": w.T,
+                   "H_q": w.H_q, "H_kv": w.H_kv, "D": w.D, "S": w.S, "parallelism": "single GPU"},
+        "roofline": roof,
+        "kernels": {kname[k_]: rows[k_] for k_ in rows},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out_line), flush=True)
+
+
+def cpu_baseline_replay(w, rows):
+    """The CPU oracle on the first `rows` query positions of every target
+    layer: selection and attention (sparse layers), or full causal attention."""
+    from oracle import oracle_replay_attention_rows, oracle_topS_rows
+    from paper_2607_28979_amd import binding as mb
+    from paper_2607_28979_amd.inputs import replay_inputs, source_attention
+    rows = rows if rows > 0 else 256
+    pi = mb.depth_ratio_map(w.L_src, w.L_tgt)
+    sample = [(0, u) for u in range(rows)]
+    dt = 0.0
+    maps = {}
+    for l in range(w.L_tgt):
+        q, k, v = replay_inputs(w.B, w.T, w.H_q, w.H_kv, w.D, seed=w.seed + 100 * l)
+        if l < w.L_full:
+            t0 = time.perf_counter()
+            oracle_replay_attention_rows(q, k, v, None, sample)
+            dt += time.perf_counter() - t0
+            continue
+        i = int(pi[l])
+        if i not in maps:
+            maps = {i: source_attention(w.B, w.T, seed=w.seed + 1000 * i)}
+        t0 = time.perf_counter()
+        sets = oracle_topS_rows(maps[i], w.S, sample)
+        idx = np.full((w.B, w.T, w.S), -1, np.int32)
+        idx[0, :rows] = sets
+        oracle_replay_attention_rows(q, k, v, idx, sample)
+        dt += time.perf_counter() - t0
+    log("cpu oracle: %d positions x %d layers in %.2f s (1 thread)" % (rows, w.L_tgt, dt))
+    return {"value": round(rows / dt, 3), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": "first %d of %d query positions, all %d target layers (selection + attention), fp64"
+                      % (rows, w.T, w.L_tgt), "seconds": round(dt, 2)}
 
 
 if __name__ == "__main__":
