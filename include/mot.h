@@ -242,7 +242,8 @@ typedef struct {
  * in ascending order to idx[b][u][0..S) and padded with -1 (all of 0..u when
  * u < S).  A: device fp32 [B][T][T] head-averaged source attention (entries
  * v > u are not read); idx: device int32 [B][T][S].  Only B, T and S of
- * `shapes` are used.  Both pointers 4-byte aligned and non-overlapping.
+ * `shapes` are used (T at most 65536).  Both pointers 4-byte aligned and
+ * non-overlapping.
  */
 mot_status mot_topS_select(const float* A, int32_t* idx, const mot_replay_shapes* shapes, hipStream_t stream);
 

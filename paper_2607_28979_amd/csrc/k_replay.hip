@@ -14,7 +14,7 @@
 //   set, and O^T = V_sel^T . P^T with V_sel staged transposed in LDS.
 // * k_causal_attn: the full causal attention of the bottom layers, tiled
 //   (64 query positions of one head per workgroup, 64-key chunks staged in
-//   LDS, online softmax).
+//   LDS with the next chunk prefetched into registers, online softmax).
 // Scores, softmax and accumulation are fp32; Q, K, V, O are bf16.
 #include "mot_device.h"
 #include "mot_internal.h"
@@ -32,32 +32,12 @@ __device__ __forceinline__ uint32_t order_key(float a) {
     return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
-// Exclusive rank of a per-thread flag in thread order over the 256-thread
-// workgroup, and the workgroup's total.  s_cnt: 4 ints of LDS.
-__device__ __forceinline__ int block_rank(bool f, int* s_cnt, int& total) {
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const unsigned long long bal = __ballot(f);
-    const int in_wave = __popcll(bal & ((1ull << lane) - 1ull));
-    if (lane == 0) s_cnt[w] = __popcll(bal);
-    __syncthreads();
-    int base = 0;
-    total = 0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int c = s_cnt[i];
-        base += i < w ? c : 0;
-        total += c;
-    }
-    __syncthreads();
-    return base + in_wave;
-}
-
 // grid (T, B), 256 threads; CACHE: the row's keys live in dynamic LDS (T words)
+// ahead of the per-chunk counts
 template <bool CACHE>
 __global__ __launch_bounds__(256) void k_topS_select(const float* A, int32_t* idx, int T, int S) {
     extern __shared__ uint32_t s_key[];
     __shared__ uint32_t hist[256];
-    __shared__ int s_cnt[4];
     __shared__ uint32_t s_sel[2];
     const int u = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
     const int n = u + 1;
@@ -67,6 +47,9 @@ __global__ __launch_bounds__(256) void k_topS_select(const float* A, int32_t* id
         return;
     }
     const float* row = A + ((size_t)b * T + u) * T;
+    // dynamic LDS: [CACHE: T keys] then per-chunk counts s_gt, s_eq (T/64 + 1 each)
+    int* s_gt = reinterpret_cast<int*>(s_key + (CACHE ? T : 0));
+    int* s_eq = s_gt + (T >> 6) + 1;
     if constexpr (CACHE) {
         for (int v = tid; v < n; v += 256) s_key[v] = order_key(row[v]);
         __syncthreads();
@@ -123,19 +106,67 @@ __global__ __launch_bounds__(256) void k_topS_select(const float* A, int32_t* id
         __syncthreads();
     }
     // prefix is the S-th largest key; take all larger keys and the first rem
-    // equal ones in position order
-    int out_base = 0, eq_base = 0;
-    for (int c0 = 0; c0 < n; c0 += 256) {
-        const int v = c0 + tid;
+    // equal ones in position order.  Rows are cut into 64-position chunks
+    // (chunk c: positions 64c + lane, wave c % 4): per-chunk counts of larger
+    // and equal keys, one scan over the chunks, then each chunk writes its
+    // picks at its offset in ballot order.
+    const int lane = tid & 63, wv = tid >> 6, nch = (n + 63) >> 6;
+    for (int c = wv; c < nch; c += 4) {
+        const int v = 64 * c + lane;
         const uint32_t k = v < n ? key_at(v) : 0u;
-        const bool gt = v < n && k > prefix, eq = v < n && k == prefix;
-        int eq_tot, tk_tot;
-        const int eq_rank = block_rank(eq, s_cnt, eq_tot);
-        const bool take = gt || (eq && eq_base + eq_rank < rem);
-        const int pos = block_rank(take, s_cnt, tk_tot);
-        if (take && out_base + pos < S) out[out_base + pos] = v;
-        out_base += tk_tot;
-        eq_base += eq_tot;
+        const unsigned long long bg = __ballot(v < n && k > prefix), be = __ballot(v < n && k == prefix);
+        if (lane == 0) {
+            s_gt[c] = __popcll(bg);
+            s_eq[c] = __popcll(be);
+        }
+    }
+    __syncthreads();
+    if (tid < 64) {
+        // exclusive scans over chunks: lane l owns chunks [l*cpl, l*cpl + cpl)
+        const int cpl = (nch + 63) >> 6, c0 = tid * cpl, c1 = min(c0 + cpl, nch);
+        int eq_l = 0;
+        for (int c = c0; c < c1; ++c) eq_l += s_eq[c];
+        int eq_pre = eq_l;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int t = __shfl_up(eq_pre, off, 64);
+            if (tid >= off) eq_pre += t;
+        }
+        eq_pre -= eq_l;   // equal keys before this lane's chunks
+        int take_l = 0;
+        for (int c = c0; c < c1; ++c) {
+            const int e = s_eq[c];
+            const int left = rem - eq_pre;   // equal keys still to take when chunk c starts
+            const int tk = s_gt[c] + (left <= 0 ? 0 : (left < e ? left : e));
+            s_eq[c] = eq_pre;                // now: equal keys before chunk c
+            s_gt[c] = tk;                    // now: picks in chunk c
+            eq_pre += e;
+            take_l += tk;
+        }
+        int tk_pre = take_l;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int t = __shfl_up(tk_pre, off, 64);
+            if (tid >= off) tk_pre += t;
+        }
+        tk_pre -= take_l;
+        for (int c = c0; c < c1; ++c) {
+            const int tk = s_gt[c];
+            s_gt[c] = tk_pre;                // now: picks before chunk c
+            tk_pre += tk;
+        }
+    }
+    __syncthreads();
+    for (int c = wv; c < nch; c += 4) {
+        const int v = 64 * c + lane;
+        const uint32_t k = v < n ? key_at(v) : 0u;
+        const bool eq = v < n && k == prefix;
+        const unsigned long long be = __ballot(eq);
+        const int eq_rank = s_eq[c] + __popcll(be & ((1ull << lane) - 1ull));
+        const bool take = (v < n && k > prefix) || (eq && eq_rank < rem);
+        const unsigned long long bt = __ballot(take);
+        const int pos = s_gt[c] + __popcll(bt & ((1ull << lane) - 1ull));
+        if (take && pos < S) out[pos] = v;
     }
 }
 
@@ -307,25 +338,43 @@ __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
     for (int db = 0; db < D / 16; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
     float m = -INFINITY, l = 0.f;
     const int last = (u0 + 63 < p.T ? u0 + 63 : p.T - 1);
+    // the next chunk's K and V rows are fetched into registers while the
+    // current one is computed: K items (key, d chunk), V items (key pair, d chunk)
+    constexpr int NKI = 64 * DC / 256, NVI = 32 * DC / 256;
+    u32x4 kreg[NKI], va[NVI], vb[NVI];
+    auto fetch = [&](int kc0) {
+#pragma unroll
+        for (int i = 0; i < NKI; ++i) {
+            const int it = tid + 256 * i, kr = it / DC, c = it % DC, t = kc0 + kr;
+            kreg[i] = t < p.T ? *reinterpret_cast<const u32x4*>(K + kv_row(p, b, t, kvh) + 8 * c) : zero;
+        }
+#pragma unroll
+        for (int i = 0; i < NVI; ++i) {
+            const int it = tid + 256 * i, c = it / 32, t = kc0 + 2 * (it % 32);
+            va[i] = t < p.T ? *reinterpret_cast<const u32x4*>(V + kv_row(p, b, t, kvh) + 8 * c) : zero;
+            vb[i] = t + 1 < p.T ? *reinterpret_cast<const u32x4*>(V + kv_row(p, b, t + 1, kvh) + 8 * c) : zero;
+        }
+    };
+    fetch(0);
     for (int kc0 = 0; kc0 <= last; kc0 += 64) {
         __syncthreads();   // the previous chunk's K and V^T are consumed
-        for (int it = tid; it < 64 * DC; it += 256) {
-            const int kr = it / DC, c = it % DC, t = kc0 + kr;
-            Kl[kr * DC + (c ^ (kr & KSW))] =
-                t < p.T ? *reinterpret_cast<const u32x4*>(K + kv_row(p, b, t, kvh) + 8 * c) : zero;
+#pragma unroll
+        for (int i = 0; i < NKI; ++i) {
+            const int it = tid + 256 * i, kr = it / DC, c = it % DC;
+            Kl[kr * DC + (c ^ (kr & KSW))] = kreg[i];
         }
         uint32_t* Vw = reinterpret_cast<uint32_t*>(Vt);
-        for (int it = tid; it < 32 * DC; it += 256) {
-            const int pr = it % 32, c = it / 32, k0 = 2 * pr, t = kc0 + k0;
-            const u32x4 a = t < p.T ? *reinterpret_cast<const u32x4*>(V + kv_row(p, b, t, kvh) + 8 * c) : zero;
-            const u32x4 cc = t + 1 < p.T ? *reinterpret_cast<const u32x4*>(V + kv_row(p, b, t + 1, kvh) + 8 * c) : zero;
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int d = 8 * c + i;
-                Vw[(d * 8 + ((k0 >> 3) ^ (d & 7))) * 4 + ((k0 & 7) >> 1)] = pair_word(a, cc, i);
+        for (int i = 0; i < NVI; ++i) {
+            const int it = tid + 256 * i, c = it / 32, k0 = 2 * (it % 32);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int d = 8 * c + e;
+                Vw[(d * 8 + ((k0 >> 3) ^ (d & 7))) * 4 + ((k0 & 7) >> 1)] = pair_word(va[i], vb[i], e);
             }
         }
         __syncthreads();
+        if (kc0 + 64 <= last) fetch(kc0 + 64);
         // scores^T[key][position] for 4 key blocks of 16
         f32x4 sc[4];
         float cm = -INFINITY;
@@ -395,7 +444,7 @@ __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
     }
 }
 
-constexpr int kSelCacheMax = 16384;   // rows up to this length keep their keys in LDS
+constexpr int kSelCacheMax = 15872;   // rows up to this length keep their keys in LDS (<= 64 KB with the counts)
 
 }  // namespace
 
@@ -404,10 +453,11 @@ size_t replay_sparse_lds_bytes(int D, int S) { return (size_t)(D * S + 16 * S) *
 hipError_t launch_topS_select(const float* A, int32_t* idx, int B, int T, int S, hipStream_t stream) {
     if (B == 0 || T == 0) return hipSuccess;
     const dim3 grid(T, B);
+    const size_t counts = (size_t)2 * ((T >> 6) + 1) * 4;
     if (T <= kSelCacheMax)
-        hipLaunchKernelGGL(k_topS_select<true>, grid, dim3(256), (size_t)T * 4, stream, A, idx, T, S);
+        hipLaunchKernelGGL(k_topS_select<true>, grid, dim3(256), (size_t)T * 4 + counts, stream, A, idx, T, S);
     else
-        hipLaunchKernelGGL(k_topS_select<false>, grid, dim3(256), 0, stream, A, idx, T, S);
+        hipLaunchKernelGGL(k_topS_select<false>, grid, dim3(256), counts, stream, A, idx, T, S);
     return hipGetLastError();
 }
 

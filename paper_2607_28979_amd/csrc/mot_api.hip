@@ -439,6 +439,7 @@ mot_status mot_topS_select(const float* A, int32_t* idx, const mot_replay_shapes
     if (!s) return fail(MOT_ERR_NULL_ARG, "shapes is NULL");
     if (s->B < 0 || s->T < 0 || (int64_t)s->B * s->T > (int64_t)1 << 26 || s->S < 1)
         return fail(MOT_ERR_BAD_SHAPE, "B=%d T=%d S=%d: need B, T >= 0, B*T <= 2^26, S >= 1", s->B, s->T, s->S);
+    if (s->T > 65536) return fail(MOT_ERR_UNSUPPORTED, "T=%d: selection supports rows of up to 65536 positions", s->T);
     if ((int64_t)s->B * s->T == 0) return MOT_OK;
     if (!A || !idx) return fail(MOT_ERR_NULL_ARG, "A and idx are required");
     if ((reinterpret_cast<uintptr_t>(A) & 3) || (reinterpret_cast<uintptr_t>(idx) & 3))

@@ -3,7 +3,7 @@ key selection and replay attention, through the C ABI, against the oracle.
 
 * selection (mot_topS_select): bit-exact key sets on maps with many ties,
   ragged row lengths (rows shorter than S, rows across 256-element chunks),
-  and a 16500-token map (rows too long for the LDS-cached kernel) on sampled
+  and a 16500-token map (rows longer than the LDS row cache) on sampled
   rows;
 * sparse attention over the selected sets (grouped-query heads, both KV
   layouts, head dims 64 and 128, S = 32 .. 128), sets with padding and
@@ -73,7 +73,7 @@ def test_topS_select_structured_map(oracle_built):
 
 def test_topS_select_long_rows_sampled(oracle_built):
     """T = 16500 exceeds the LDS row cache: the uncached kernel, on sampled
-    rows (first, last, and around the 16384 boundary)."""
+    rows (first, last, and around 16384)."""
     from oracle import oracle_topS_rows
     T, S = 16500, 128
     print("case select long T", T, flush=True)
