@@ -54,6 +54,23 @@ def measured_traffic(kernel_file: str, workload_tag: str):
         return None
 
 
+def calibration_copy(mib: int) -> None:
+    """One plain device copy of `mib` MiB: a known-size reference for the HBM
+    byte counters of a profiler run."""
+    if mib <= 0:
+        return
+    import torch
+    n = mib << 20
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    log("calibration copy of %d MiB done" % mib)
+    del a, b
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -124,16 +141,7 @@ def main():
         mb.translate(d["src_k"], d["src_v"], lm, d["w1"], d["b1"], d["w2"], d["b2"], d["wr"], d["br"],
                      dk, dv, shapes, workspace=ws)
 
-    if args.calibrate_copy > 0:
-        n = args.calibrate_copy << 20
-        a = torch.empty(n, dtype=torch.uint8, device="cuda")
-        b = torch.empty(n, dtype=torch.uint8, device="cuda")
-        a.fill_(1)
-        torch.cuda.synchronize()
-        b.copy_(a)
-        torch.cuda.synchronize()
-        log("calibration copy of %d MiB done" % args.calibrate_copy)
-        del a, b
+    calibration_copy(args.calibrate_copy)
 
     for _ in range(args.warmup):
         step()
@@ -276,6 +284,7 @@ def bench_moth(args):
         mb.restore_kv(act, None, p["wk"], p["bk"], p["wv"], p["bv"], dk, dv, L=w.L_tgt, B=w.B,
                       T=w.T, d_act=w.d_out, H_tgt=MOTH.kv_heads, D_tgt=MOTH.head_dim)
 
+    calibration_copy(args.calibrate_copy)
     for _ in range(args.warmup):
         translate()
         restore()
@@ -410,6 +419,7 @@ def bench_replay(args):
                     ev["select"].append((es[0], es[1]))
                     ev["sparse"].append((es[1], es[2]))
 
+    calibration_copy(args.calibrate_copy)
     for _ in range(args.warmup):
         step(False)
     torch.cuda.synchronize()
@@ -429,16 +439,19 @@ def bench_replay(args):
     sp_flops = 4.0 * w.H_q * w.D * w.B * sum(min(u + 1, w.S) for u in range(w.T))
     ca_flops = 4.0 * w.H_q * w.D * w.B * w.T * (w.T + 1) / 2
     sel_bytes = 4.0 * w.B * w.T * (w.T + 1) / 2 + 4.0 * n_tok * w.S        # causal half of A once, idx
-    # sparse attention: q and o once, idx once, each selected K and V row once per (query, KV head)
+    # sparse attention: q and o once, idx once, the layer's K and V once; the
+    # selected K and V rows it gathers per (query, KV head) are reported beside
     sp_gather = 2.0 * 2 * w.D * w.H_kv * w.B * sum(min(u + 1, w.S) for u in range(w.T))
-    sp_bytes = 2.0 * 2 * n_tok * w.H_q * w.D + 4.0 * n_tok * w.S + sp_gather
+    sp_bytes = 2.0 * 2 * n_tok * w.H_q * w.D + 4.0 * n_tok * w.S + 2.0 * 2 * n_tok * w.H_kv * w.D
     peak_bf16 = PEAK_TFLOPS["bf16"]
     rows = {
         "select": {"bound": "hbm", "achieved": sel_bytes / (avg["select"] / 1e3) / 1e9, "peak": PEAK_HBM_GBS,
                    "unit": "GB/s", "alg_bytes_per_launch": sel_bytes, "ms": avg["select"]},
         "sparse": {"bound": "hbm", "achieved": sp_bytes / (avg["sparse"] / 1e3) / 1e9, "peak": PEAK_HBM_GBS,
                    "unit": "GB/s", "alg_bytes_per_launch": sp_bytes, "ms": avg["sparse"],
-                   "tflops": sp_flops / (avg["sparse"] / 1e3) / 1e12},
+                   "gathered_bytes_per_launch": sp_gather,
+                   "gather_gbs": round(sp_gather / (avg["sparse"] / 1e3) / 1e9, 1),
+                   "tflops": round(sp_flops / (avg["sparse"] / 1e3) / 1e12, 2)},
         "causal": {"bound": "mfma", "achieved": ca_flops / (avg["causal"] / 1e3) / 1e12, "peak": peak_bf16,
                    "unit": "TFLOP/s", "alg_flops_per_launch": ca_flops, "ms": avg["causal"]},
     }
@@ -450,7 +463,8 @@ def bench_replay(args):
              "causal": avg["causal"] * w.L_full}
     dom = max(share, key=share.get)
     kname = {"select": "k_topS_select", "sparse": "k_sparse_attn", "causal": "k_causal_attn"}
-    roof = dict(rows[dom], kernel=kname[dom], traffic=None)
+    roof = dict(rows[dom], kernel=kname[dom],
+                traffic=measured_traffic("k_replay.hip", "qwen2.5-7b-replay-8k") if dom == "sparse" else None)
     cpu = None if args.no_cpu_baseline else cpu_baseline_replay(w, args.cpu_rows)
     out_line = {
         "metric": "replayed context tokens/sec (all target layers, Top-S source-guided sparse attention)",
