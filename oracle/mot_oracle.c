@@ -47,7 +47,9 @@
  * replay step after translation (App. C.4): Top-S source-guided key
  * selection and attention over the selected (or the full causal) key set,
  * pinned by worked examples, sorting, single-key and uniform-score cases and
- * numpy softmax attention.
+ * numpy softmax attention; and the backbone translator body (App. C.2) as
+ * the experts of the mixture, pinned by a numpy implementation, a closed
+ * form (zero output weights), causality and batch-row independence.
  */
 #include <math.h>
 #include <pthread.h>
@@ -572,4 +574,200 @@ int mot_oracle_topS_rows(const float* A, int32_t B, int32_t T, int32_t S, const 
     }
     free(take);
     return OR_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* Backbone translator body (App. C.2, "Backbone Translator")          */
+/* ------------------------------------------------------------------ */
+
+/* One channel-window slot per unit (target layer j, K or V, source layer
+ * i = layer_map[j]): for every batch row b, over the context positions t,
+ *   x_t  = source row (d_in)
+ *   z_t  = GELU(W_in LN_in(x_t) + b_in)                     (d_h)
+ *   h0   = z                                                (h_0 = z_1)
+ *   a    = CrossAttn(LN_Q(h0), LN_C(z), LN_C(z)):  n_heads heads of width
+ *          d_h / n_heads, Q = Wq . + bq, K = Wk . + bk, V = Wv . + bv,
+ *          causal softmax(Q_t . K_s / sqrt(width)) over s <= t, Wo . + bo
+ *   h1   = h0 + a
+ *   h2   = h1 + W_f2 GELU(W_f1 LN_F(h1) + b_f1) + b_f2       (FFN)
+ *   y_t  = GELU(W_out LN_out(h2_t) + b_out)                  (d_out)
+ * and the mixture out_t = sum over the Top-K experts m of g~_m y_t^(m), with
+ * the gates of the translation (softmax of Wr x_t + br, renormalised Top-K).
+ * LN(v) = (v - mean) / sqrt(var + 1e-5) * gamma + beta, population variance.
+ *
+ * Parameters of (unit u = 2j + x, expert m), packed in this order at
+ * params + (u * E + m) * P (P = mot_oracle_backbone_param_count):
+ *   ln_in_g[d_in] ln_in_b[d_in] w_in[d_h][d_in] b_in[d_h]
+ *   ln_q_g[d_h] ln_q_b[d_h] ln_c_g[d_h] ln_c_b[d_h]
+ *   wq[d_h][d_h] bq[d_h] wk[d_h][d_h] bk[d_h] wv[d_h][d_h] bv[d_h] wo[d_h][d_h] bo[d_h]
+ *   ln_f_g[d_h] ln_f_b[d_h] w_f1[d_ff][d_h] b_f1[d_ff] w_f2[d_h][d_ff] b_f2[d_h]
+ *   ln_out_g[d_h] ln_out_b[d_h] w_out[d_out][d_h] b_out[d_out]
+ * Everything in double; dst in the dst layout (double), layers with
+ * layer_map[j] < 0 untouched. */
+size_t mot_oracle_backbone_param_count(int32_t d_in, int32_t d_h, int32_t d_ff, int32_t d_out)
+{
+    return (size_t)2 * d_in + (size_t)d_h * d_in + d_h + 4 * (size_t)d_h +
+           4 * ((size_t)d_h * d_h + d_h) + 2 * (size_t)d_h + (size_t)d_ff * d_h + d_ff +
+           (size_t)d_h * d_ff + d_h + 2 * (size_t)d_h + (size_t)d_out * d_h + d_out;
+}
+
+static void bb_layernorm(const double* v, int32_t w, const float* g, const float* b, double* out)
+{
+    double mean = 0.0, var = 0.0;
+    for (int32_t c = 0; c < w; ++c) mean += v[c];
+    mean /= w;
+    for (int32_t c = 0; c < w; ++c) var += (v[c] - mean) * (v[c] - mean);
+    var /= w;
+    const double inv = 1.0 / sqrt(var + 1e-5);
+    for (int32_t c = 0; c < w; ++c) out[c] = (v[c] - mean) * inv * (double)g[c] + (double)b[c];
+}
+
+/* out[o] = W[o][:] . v + b[o] (+ act) */
+static void bb_linear(const double* v, int32_t n_in, const float* W, const float* b, int32_t n_out, int gelu,
+                      double* out)
+{
+    for (int32_t o = 0; o < n_out; ++o) {
+        double acc = 0.0;
+        for (int32_t c = 0; c < n_in; ++c) acc += (double)W[(size_t)o * n_in + c] * v[c];
+        acc += (double)b[o];
+        out[o] = gelu ? act_fn(0, acc) : acc;
+    }
+}
+
+int mot_oracle_backbone_translate(const float* src_k, const float* src_v, const int32_t* layer_map,
+                                  const float* params, const float* wr, const float* br,
+                                  double* dst_k, double* dst_v, const mot_oracle_dims* s,
+                                  int32_t d_h, int32_t n_heads, int32_t d_ff)
+{
+    int rc = check_dims(s, layer_map);
+    if (rc) return rc;
+    if (!src_k || !src_v || !params || !wr || !dst_k || !dst_v || s->streams != 2) return OR_BAD_ARG;
+    if (d_h < 1 || n_heads < 1 || d_h % n_heads || d_ff < 1) return OR_BAD_ARG;
+    const int32_t d_in = s->H_src * s->D_src, d_out = s->H_tgt * s->D_tgt, E = s->E, T = s->T;
+    const int32_t hw = d_h / n_heads;
+    const size_t P = mot_oracle_backbone_param_count(d_in, d_h, d_ff, d_out);
+    const size_t TT = T > 0 ? (size_t)T : 1;
+    double* x = (double*)malloc(sizeof(double) * TT * d_in);
+    double* z = (double*)malloc(sizeof(double) * TT * d_h);
+    double* Q = (double*)malloc(sizeof(double) * TT * d_h);
+    double* K = (double*)malloc(sizeof(double) * TT * d_h);
+    double* V = (double*)malloc(sizeof(double) * TT * d_h);
+    double* h2 = (double*)malloc(sizeof(double) * TT * d_h);
+    double* out = (double*)malloc(sizeof(double) * TT * d_out);
+    double* gt = (double*)malloc(sizeof(double) * TT * E);
+    double* t1 = (double*)malloc(sizeof(double) * (d_in > d_h ? d_in : d_h));
+    double* t2 = (double*)malloc(sizeof(double) * d_h);
+    double* att = (double*)malloc(sizeof(double) * d_h);
+    double* f = (double*)malloc(sizeof(double) * d_ff);
+    double* y = (double*)malloc(sizeof(double) * d_out);
+    double* sc = (double*)malloc(sizeof(double) * TT);
+    double* lg = (double*)malloc(sizeof(double) * E);
+    int* sel = (int*)malloc(sizeof(int) * E);
+    if (!x || !z || !Q || !K || !V || !h2 || !out || !gt || !t1 || !t2 || !att || !f || !y || !sc || !lg || !sel) {
+        rc = OR_NO_MEM;
+        goto done;
+    }
+    for (int32_t j = 0; j < s->L_tgt; ++j) {
+        const int32_t i = layer_map[j];
+        if (i < 0) continue;
+        for (int32_t xk = 0; xk < 2; ++xk) {
+            const size_t unit = (size_t)j * 2 + xk;
+            const float* src = xk == 0 ? src_k : src_v;
+            double* dst = xk == 0 ? dst_k : dst_v;
+            for (int32_t b = 0; b < s->B; ++b) {
+                /* source rows and gates */
+                for (int32_t t = 0; t < T; ++t) {
+                    gather_row(s, src, i, b, t, x + (size_t)t * d_in);
+                    const double* xt = x + (size_t)t * d_in;
+                    double mx = -INFINITY;
+                    for (int32_t m = 0; m < E; ++m) {
+                        double acc = 0.0;
+                        for (int32_t c = 0; c < d_in; ++c) acc += (double)wr[(unit * E + m) * d_in + c] * xt[c];
+                        if (br) acc += (double)br[unit * E + m];
+                        lg[m] = acc;
+                        if (acc > mx) mx = acc;
+                    }
+                    double den = 0.0;
+                    for (int32_t m = 0; m < E; ++m) { lg[m] = exp(lg[m] - mx); den += lg[m]; }
+                    for (int32_t m = 0; m < E; ++m) { lg[m] /= den; sel[m] = 0; }
+                    for (int32_t k = 0; k < s->top_k; ++k) {
+                        int32_t best = -1;
+                        for (int32_t m = 0; m < E; ++m)
+                            if (!sel[m] && (best < 0 || lg[m] > lg[best])) best = m;
+                        sel[best] = 1;
+                    }
+                    double gs = 0.0;
+                    for (int32_t m = 0; m < E; ++m) if (sel[m]) gs += lg[m];
+                    for (int32_t m = 0; m < E; ++m) gt[(size_t)t * E + m] = sel[m] ? lg[m] / gs : 0.0;
+                }
+                for (size_t c = 0; c < (size_t)T * d_out; ++c) out[c] = 0.0;
+                for (int32_t m = 0; m < E; ++m) {
+                    int used = 0;
+                    for (int32_t t = 0; t < T; ++t) used |= gt[(size_t)t * E + m] != 0.0;
+                    if (!used) continue;
+                    const float* pp = params + (unit * E + m) * P;
+                    const float *ln_in_g = pp, *ln_in_b = ln_in_g + d_in, *w_in = ln_in_b + d_in,
+                                *b_in = w_in + (size_t)d_h * d_in, *ln_q_g = b_in + d_h, *ln_q_b = ln_q_g + d_h,
+                                *ln_c_g = ln_q_b + d_h, *ln_c_b = ln_c_g + d_h, *wq = ln_c_b + d_h,
+                                *bq = wq + (size_t)d_h * d_h, *wk = bq + d_h, *bk = wk + (size_t)d_h * d_h,
+                                *wv = bk + d_h, *bv = wv + (size_t)d_h * d_h, *wo = bv + d_h,
+                                *bo = wo + (size_t)d_h * d_h, *ln_f_g = bo + d_h, *ln_f_b = ln_f_g + d_h,
+                                *w_f1 = ln_f_b + d_h, *b_f1 = w_f1 + (size_t)d_ff * d_h, *w_f2 = b_f1 + d_ff,
+                                *b_f2 = w_f2 + (size_t)d_h * d_ff, *ln_out_g = b_f2 + d_h,
+                                *ln_out_b = ln_out_g + d_h, *w_out = ln_out_b + d_h,
+                                *b_out = w_out + (size_t)d_out * d_h;
+                    /* z, then Q (from LN_Q(z)), K and V (from LN_C(z)) */
+                    for (int32_t t = 0; t < T; ++t) {
+                        bb_layernorm(x + (size_t)t * d_in, d_in, ln_in_g, ln_in_b, t1);
+                        bb_linear(t1, d_in, w_in, b_in, d_h, 1, z + (size_t)t * d_h);
+                        bb_layernorm(z + (size_t)t * d_h, d_h, ln_q_g, ln_q_b, t1);
+                        bb_linear(t1, d_h, wq, bq, d_h, 0, Q + (size_t)t * d_h);
+                        bb_layernorm(z + (size_t)t * d_h, d_h, ln_c_g, ln_c_b, t1);
+                        bb_linear(t1, d_h, wk, bk, d_h, 0, K + (size_t)t * d_h);
+                        bb_linear(t1, d_h, wv, bv, d_h, 0, V + (size_t)t * d_h);
+                    }
+                    for (int32_t t = 0; t < T; ++t) {
+                        /* causal multi-head attention of position t */
+                        for (int32_t hh = 0; hh < n_heads; ++hh) {
+                            const double* qt = Q + (size_t)t * d_h + hh * hw;
+                            double mx = -INFINITY;
+                            for (int32_t u = 0; u <= t; ++u) {
+                                const double* ku = K + (size_t)u * d_h + hh * hw;
+                                double acc = 0.0;
+                                for (int32_t d = 0; d < hw; ++d) acc += qt[d] * ku[d];
+                                sc[u] = acc / sqrt((double)hw);
+                                if (sc[u] > mx) mx = sc[u];
+                            }
+                            double den = 0.0;
+                            for (int32_t u = 0; u <= t; ++u) { sc[u] = exp(sc[u] - mx); den += sc[u]; }
+                            for (int32_t d = 0; d < hw; ++d) att[hh * hw + d] = 0.0;
+                            for (int32_t u = 0; u <= t; ++u) {
+                                const double* vu = V + (size_t)u * d_h + hh * hw;
+                                for (int32_t d = 0; d < hw; ++d) att[hh * hw + d] += sc[u] / den * vu[d];
+                            }
+                        }
+                        /* h1 = z + Wo a + bo;  h2 = h1 + FFN(LN_F(h1)) */
+                        bb_linear(att, d_h, wo, bo, d_h, 0, t2);
+                        for (int32_t c = 0; c < d_h; ++c) t2[c] += z[(size_t)t * d_h + c];
+                        bb_layernorm(t2, d_h, ln_f_g, ln_f_b, t1);
+                        bb_linear(t1, d_h, w_f1, b_f1, d_ff, 1, f);
+                        bb_linear(f, d_ff, w_f2, b_f2, d_h, 0, h2 + (size_t)t * d_h);
+                        for (int32_t c = 0; c < d_h; ++c) h2[(size_t)t * d_h + c] += t2[c];
+                        bb_layernorm(h2 + (size_t)t * d_h, d_h, ln_out_g, ln_out_b, t1);
+                        bb_linear(t1, d_h, w_out, b_out, d_out, 1, y);
+                        const double g = gt[(size_t)t * E + m];
+                        for (int32_t o = 0; o < d_out; ++o) out[(size_t)t * d_out + o] += g * y[o];
+                    }
+                }
+                for (int32_t t = 0; t < T; ++t)
+                    for (int32_t o = 0; o < d_out; ++o)
+                        dst[cache_index(s, s->dst_layout, s->H_tgt, s->D_tgt, j, b, t, o / s->D_tgt, o % s->D_tgt)] =
+                            out[(size_t)t * d_out + o];
+            }
+        }
+    }
+done:
+    free(x); free(z); free(Q); free(K); free(V); free(h2); free(out); free(gt); free(t1); free(t2);
+    free(att); free(f); free(y); free(sc); free(lg); free(sel);
+    return rc;
 }

@@ -88,10 +88,13 @@ def _load():
         if not os.path.exists(_LIB):
             build_oracle(force=False)
         _lib = ctypes.CDLL(_LIB)
+        _lib.mot_oracle_backbone_param_count.restype = ctypes.c_size_t
+        _lib.mot_oracle_backbone_param_count.argtypes = [ctypes.c_int32] * 4
         for fn in (_lib.mot_oracle_translate, _lib.mot_oracle_rows,
                    _lib.mot_oracle_depth_ratio_map, _lib.mot_oracle_restore_kv,
                    _lib.mot_oracle_topS_select, _lib.mot_oracle_replay_attention,
-                   _lib.mot_oracle_replay_attention_rows, _lib.mot_oracle_topS_rows):
+                   _lib.mot_oracle_replay_attention_rows, _lib.mot_oracle_topS_rows,
+                   _lib.mot_oracle_backbone_translate):
             fn.restype = ctypes.c_int
     return _lib
 
@@ -272,3 +275,32 @@ def oracle_replay_attention_rows(q, k, v, idx, rows, kv_layout: int = 0) -> np.n
     if rc != 0:
         raise ValueError("mot_oracle_replay_attention_rows failed with code %d" % rc)
     return out
+
+
+def oracle_backbone_param_count(d_in: int, d_h: int, d_ff: int, d_out: int) -> int:
+    """Parameters per (unit, expert) of the backbone translator body."""
+    return int(_load().mot_oracle_backbone_param_count(d_in, d_h, d_ff, d_out))
+
+
+def oracle_backbone_translate(dims: OracleDims, src_k, src_v, layer_map, params, wr, br,
+                              d_h: int, n_heads: int, d_ff: int):
+    """Mixture of backbone translators (App. C.2, one channel-window slot per
+    unit): params float32 [L_tgt][2][E][P] packed as documented in
+    mot_oracle.c.  Returns (dst_k, dst_v) float64 in the dst layout (NaN in
+    layers with layer_map[j] < 0)."""
+    lib = _load()
+    arrs = [_f32(a, n) for a, n in ((src_k, "src_k"), (src_v, "src_v"), (params, "params"), (wr, "wr"),
+                                    (br, "br"))]
+    lm = np.ascontiguousarray(layer_map, dtype=np.int32)
+    shape = ((dims.L_tgt, dims.B, dims.T, dims.H_tgt, dims.D_tgt) if dims.dst_layout == 0
+             else (dims.L_tgt, dims.B, dims.H_tgt, dims.T, dims.D_tgt))
+    dst_k = np.full(shape, np.nan)
+    dst_v = np.full(shape, np.nan)
+    c = dims._c()
+    i32 = ctypes.c_int32
+    rc = lib.mot_oracle_backbone_translate(_ptr(arrs[0]), _ptr(arrs[1]), _ptr(lm), _ptr(arrs[2]), _ptr(arrs[3]),
+                                           _ptr(arrs[4]), _ptr(dst_k), _ptr(dst_v), ctypes.byref(c),
+                                           i32(d_h), i32(n_heads), i32(d_ff))
+    if rc != 0:
+        raise ValueError("mot_oracle_backbone_translate failed with code %d" % rc)
+    return dst_k, dst_v

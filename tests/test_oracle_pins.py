@@ -597,3 +597,120 @@ def test_replay_sampled_rows_equal_full(oracle_built):
         full = oracle_replay_attention(q, k, v, sets)
         assert np.array_equal(oracle_replay_attention_rows(q, k, v, sets, rows),
                               np.stack([full[b, u] for b, u in rows]))
+
+
+# ---------------------------------------------------------------------------
+# Backbone translator body (App. C.2), one channel-window slot per unit
+# ---------------------------------------------------------------------------
+
+def _bb_unpack(p, d_in, d_h, d_ff, d_out):
+    sizes = [("ln_in_g", d_in), ("ln_in_b", d_in), ("w_in", d_h * d_in), ("b_in", d_h), ("ln_q_g", d_h),
+             ("ln_q_b", d_h), ("ln_c_g", d_h), ("ln_c_b", d_h), ("wq", d_h * d_h), ("bq", d_h),
+             ("wk", d_h * d_h), ("bk", d_h), ("wv", d_h * d_h), ("bv", d_h), ("wo", d_h * d_h), ("bo", d_h),
+             ("ln_f_g", d_h), ("ln_f_b", d_h), ("w_f1", d_ff * d_h), ("b_f1", d_ff), ("w_f2", d_h * d_ff),
+             ("b_f2", d_h), ("ln_out_g", d_h), ("ln_out_b", d_h), ("w_out", d_out * d_h), ("b_out", d_out)]
+    out, o = {}, 0
+    for name, n in sizes:
+        out[name] = p[o:o + n].astype(np.float64)
+        o += n
+    assert o == p.size
+    out["w_in"] = out["w_in"].reshape(d_h, d_in)
+    for k_ in ("wq", "wk", "wv", "wo"):
+        out[k_] = out[k_].reshape(d_h, d_h)
+    out["w_f1"] = out["w_f1"].reshape(d_ff, d_h)
+    out["w_f2"] = out["w_f2"].reshape(d_h, d_ff)
+    out["w_out"] = out["w_out"].reshape(d_out, d_h)
+    return out
+
+
+def _np_backbone(x, P, n_heads):
+    """One expert on rows x [T][d_in] of one batch row, numpy float64."""
+    def ln(v, g, b):
+        mu = v.mean(axis=-1, keepdims=True)
+        var = ((v - mu) ** 2).mean(axis=-1, keepdims=True)
+        return (v - mu) / np.sqrt(var + 1e-5) * g + b
+    gelu = lambda a: 0.5 * a * (1.0 + sp_erf(a / np.sqrt(2.0)))
+    z = gelu(ln(x, P["ln_in_g"], P["ln_in_b"]) @ P["w_in"].T + P["b_in"])
+    q = ln(z, P["ln_q_g"], P["ln_q_b"]) @ P["wq"].T + P["bq"]
+    c = ln(z, P["ln_c_g"], P["ln_c_b"])
+    k = c @ P["wk"].T + P["bk"]
+    v = c @ P["wv"].T + P["bv"]
+    T, d_h = z.shape
+    hw = d_h // n_heads
+    a = np.zeros_like(z)
+    mask = np.tril(np.ones((T, T), bool))
+    for h in range(n_heads):
+        sl = slice(h * hw, (h + 1) * hw)
+        s = q[:, sl] @ k[:, sl].T / np.sqrt(hw)
+        s = np.where(mask, s, -np.inf)
+        p = np.exp(s - s.max(axis=1, keepdims=True))
+        p /= p.sum(axis=1, keepdims=True)
+        a[:, sl] = p @ v[:, sl]
+    h1 = z + a @ P["wo"].T + P["bo"]
+    h2 = h1 + gelu(ln(h1, P["ln_f_g"], P["ln_f_b"]) @ P["w_f1"].T + P["b_f1"]) @ P["w_f2"].T + P["b_f2"]
+    return gelu(ln(h2, P["ln_out_g"], P["ln_out_b"]) @ P["w_out"].T + P["b_out"])
+
+
+def _bb_case(rng, E=2, top_k=2, T=7, B=2, d=(8, 8, 16, 8), n_heads=2):
+    from oracle import oracle_backbone_param_count
+    d_in, d_h, d_ff, d_out = d
+    dims = OracleDims(L_src=2, L_tgt=2, B=B, T=T, H_src=1, D_src=d_in, H_tgt=2, D_tgt=d_out // 2, E=E,
+                      hidden=d_h, top_k=top_k)
+    Pn = oracle_backbone_param_count(d_in, d_h, d_ff, d_out)
+    params = (rng.standard_normal((2, 2, E, Pn)) * 0.4).astype(np.float32)
+    src_k = rng.standard_normal((2, B, T, 1, d_in)).astype(np.float32)
+    src_v = rng.standard_normal((2, B, T, 1, d_in)).astype(np.float32)
+    wr = rng.standard_normal((2, 2, E, d_in)).astype(np.float32)
+    br = rng.standard_normal((2, 2, E)).astype(np.float32)
+    return dims, params, src_k, src_v, wr, br
+
+
+def test_backbone_matches_numpy(oracle_built):
+    """Mixture of two backbone experts against a numpy implementation (layer
+    norms, causal multi-head attention, FFN, output GELU, softmax gates),
+    depth map [1, -1]: layer 1 untouched."""
+    from oracle import oracle_backbone_translate
+    rng = np.random.default_rng(43)
+    d_in, d_h, d_ff, d_out, nh = 8, 8, 16, 8, 2
+    dims, params, src_k, src_v, wr, br = _bb_case(rng)
+    lm = np.array([1, -1], np.int32)
+    gk, gv = oracle_backbone_translate(dims, src_k, src_v, lm, params, wr, br, d_h, nh, d_ff)
+    assert np.isnan(gk[1]).all()
+    for x, (src, got) in enumerate(((src_k, gk), (src_v, gv))):
+        for b in range(dims.B):
+            xs = src[1, b, :, 0].astype(np.float64)
+            lg = xs @ wr[0, x].astype(np.float64).T + br[0, x]
+            g = np.exp(lg - lg.max(axis=1, keepdims=True))
+            g /= g.sum(axis=1, keepdims=True)
+            want = sum(g[:, m:m + 1] * _np_backbone(xs, _bb_unpack(params[0, x, m], d_in, d_h, d_ff, d_out), nh)
+                       for m in range(dims.E))
+            np.testing.assert_allclose(got[0, b].reshape(dims.T, d_out), want, rtol=1e-10, atol=1e-12)
+
+
+def test_backbone_closed_form_and_causality(oracle_built):
+    """W_out = 0: every row is GELU(b_out) (one expert), whatever the source.
+    Changing the source rows of the last positions leaves earlier outputs
+    unchanged (causal attention, per-token elsewhere); batch rows are
+    independent."""
+    from oracle import oracle_backbone_translate
+    rng = np.random.default_rng(47)
+    d_in, d_h, d_ff, d_out, nh = 8, 8, 16, 8, 2
+    dims, params, src_k, src_v, wr, br = _bb_case(rng, E=1, top_k=1)
+    lm = np.array([0, 1], np.int32)
+    p0 = params.copy()
+    off = p0.shape[-1] - d_out - d_out * d_h
+    p0[..., off:off + d_out * d_h] = 0.0
+    gk, _ = oracle_backbone_translate(dims, src_k, src_v, lm, p0, wr, br, d_h, nh, d_ff)
+    bo = p0[..., -d_out:].astype(np.float64)
+    for j in range(2):
+        want = 0.5 * bo[j, 0, 0] * (1 + sp_erf(bo[j, 0, 0] / np.sqrt(2)))
+        np.testing.assert_allclose(gk[j].reshape(-1, d_out), np.broadcast_to(want, (dims.B * dims.T, d_out)),
+                                   rtol=1e-13, atol=1e-15)
+    a, _ = oracle_backbone_translate(dims, src_k, src_v, lm, params, wr, br, d_h, nh, d_ff)
+    sk2 = src_k.copy()
+    sk2[:, :, 4:] = rng.standard_normal(sk2[:, :, 4:].shape)
+    b2, _ = oracle_backbone_translate(dims, sk2, src_v, lm, params, wr, br, d_h, nh, d_ff)
+    assert np.array_equal(a[:, :, :4], b2[:, :, :4]) and not np.allclose(a[:, :, 4:], b2[:, :, 4:])
+    sk3 = src_k[:, ::-1].copy()
+    c3, _ = oracle_backbone_translate(dims, sk3, src_v, lm, params, wr, br, d_h, nh, d_ff)
+    assert np.array_equal(c3, a[:, ::-1])
