@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define MOT_ABI_VERSION 3
+#define MOT_ABI_VERSION 4
 #define MOT_MAX_LAYERS 256   /* L_src, L_tgt <= MOT_MAX_LAYERS               */
 #define MOT_MAX_EXPERTS 16   /* E <= MOT_MAX_EXPERTS                         */
 
@@ -259,6 +259,48 @@ mot_status mot_topS_select(const float* A, int32_t* idx, const mot_replay_shapes
  */
 mot_status mot_replay_attention(const void* q, const void* k, const void* v, const int32_t* idx, void* o,
                                 const mot_replay_shapes* shapes, hipStream_t stream);
+
+/*
+ * The backbone translator body (paper App. C.2, "Backbone Translator") as the
+ * experts of the mixture, with a channel window of one slot per unit (target
+ * layer j, K or V, source layer layer_map[j]).  For each batch row, over the
+ * context positions t, expert m computes
+ *     z   = GELU(W_in LN_in(x_t) + b_in)                       (d_h)
+ *     h1  = z + Wo CausalMHA(Wq LN_Q(z) + bq, Wk LN_C(z) + bk, Wv LN_C(z) + bv) + bo
+ *     h2  = h1 + W_f2 GELU(W_f1 LN_F(h1) + b_f1) + b_f2
+ *     y_t = GELU(W_out LN_out(h2) + b_out)                     (d_out)
+ * (n_heads heads of width d_h / n_heads, softmax(q.k / sqrt(width)) over the
+ * positions s <= t of the same batch row; LN with population variance,
+ * eps 1e-5) and the output row is sum_m g~_m y_t^(m) with the Top-K gates of
+ * mot_translate's router.
+ *
+ *   params   device bf16 [L_tgt][2][E][P], P = mot_backbone_param_count():
+ *            per expert, in order: ln_in_g[d_in] ln_in_b[d_in] w_in[d_h][d_in]
+ *            b_in[d_h] ln_q_g[d_h] ln_q_b[d_h] ln_c_g[d_h] ln_c_b[d_h]
+ *            wq[d_h][d_h] bq[d_h] wk[d_h][d_h] bk[d_h] wv[d_h][d_h] bv[d_h]
+ *            wo[d_h][d_h] bo[d_h] ln_f_g[d_h] ln_f_b[d_h] w_f1[d_ff][d_h]
+ *            b_f1[d_ff] w_f2[d_h][d_ff] b_f2[d_h] ln_out_g[d_h] ln_out_b[d_h]
+ *            w_out[d_out][d_h] b_out[d_out]
+ *   router   as for mot_translate (bias optional)
+ *   shapes   as for mot_translate; dtype MOT_BF16, both layouts
+ *            MOT_LAYOUT_BTHD, streams 2; hidden, act, algo and the workspace
+ *            fields are not used (the library owns the scratch it needs)
+ * Requires d_in and d_h multiples of 64 up to 4096, d_ff a multiple of 64,
+ * D_tgt a multiple of 8, head width d_h / n_heads of 64 or 128
+ * (MOT_ERR_UNSUPPORTED otherwise).  Every check runs before any enqueue.
+ */
+typedef struct {
+    int32_t d_h;       /* translator width          */
+    int32_t n_heads;   /* attention heads           */
+    int32_t d_ff;      /* feed-forward width        */
+} mot_backbone_dims;
+
+/* Elements per expert of the packed parameters (0 for invalid arguments). */
+size_t mot_backbone_param_count(const mot_shapes* shapes, const mot_backbone_dims* dims);
+
+mot_status mot_backbone_translate(const void* src_k, const void* src_v, const int32_t* layer_map,
+                                  const void* params, const mot_router_weights* router, void* dst_k, void* dst_v,
+                                  const mot_shapes* shapes, const mot_backbone_dims* dims, hipStream_t stream);
 
 /* MOT_ABI_VERSION of the loaded library. */
 int mot_abi_version(void);

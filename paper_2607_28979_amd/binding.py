@@ -26,7 +26,7 @@ STATUS = {0: "MOT_OK", 1: "MOT_ERR_NULL_ARG", 2: "MOT_ERR_BAD_SHAPE", 3: "MOT_ER
 
 EXPORTED = ("mot_translate", "mot_workspace_bytes", "mot_depth_ratio_map", "mot_status_string",
             "mot_last_error", "mot_abi_version", "mot_restore_kv", "mot_topS_select",
-            "mot_replay_attention")
+            "mot_replay_attention", "mot_backbone_param_count", "mot_backbone_translate")
 
 
 class MotError(RuntimeError):
@@ -46,6 +46,10 @@ class _Shapes(ctypes.Structure):
 class _RestoreShapes(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("L", "B", "T", "d_act", "H_tgt", "D_tgt", "dtype",
                                              "dst_layout")]
+
+
+class _BackboneDims(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("d_h", "n_heads", "d_ff")]
 
 
 class _ReplayShapes(ctypes.Structure):
@@ -150,6 +154,12 @@ def load_library():
         lib.mot_topS_select.restype = ctypes.c_int
         lib.mot_topS_select.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(_ReplayShapes),
                                         ctypes.c_void_p]
+        lib.mot_backbone_param_count.restype = ctypes.c_size_t
+        lib.mot_backbone_param_count.argtypes = [ctypes.POINTER(_Shapes), ctypes.POINTER(_BackboneDims)]
+        lib.mot_backbone_translate.restype = ctypes.c_int
+        lib.mot_backbone_translate.argtypes = [ctypes.c_void_p] * 4 + [ctypes.POINTER(_RW), ctypes.c_void_p,
+                                                                       ctypes.c_void_p, ctypes.POINTER(_Shapes),
+                                                                       ctypes.POINTER(_BackboneDims), ctypes.c_void_p]
         lib.mot_replay_attention.restype = ctypes.c_int
         lib.mot_replay_attention.argtypes = [ctypes.c_void_p] * 5 + [ctypes.POINTER(_ReplayShapes),
                                                                      ctypes.c_void_p]
@@ -281,3 +291,28 @@ def replay_attention(q, k, v, idx, o, B: int, T: int, H_q: int, H_kv: int, D: in
     c = _ReplayShapes(B, T, H_q, H_kv, D, S if idx is not None else 0, kv_layout)
     _check(lib.mot_replay_attention(_ptr(q), _ptr(k), _ptr(v), _ptr(idx), _ptr(o), ctypes.byref(c),
                                     torch.cuda.current_stream().cuda_stream))
+
+
+def backbone_param_count(shapes: Shapes, d_h: int, n_heads: int, d_ff: int) -> int:
+    """Elements per expert of the packed backbone parameters."""
+    c = shapes.c()
+    return int(load_library().mot_backbone_param_count(ctypes.byref(c), ctypes.byref(_BackboneDims(d_h, n_heads, d_ff))))
+
+
+def backbone_translate(src_k, src_v, layer_map, params, wr, br, dst_k, dst_v, shapes: Shapes, d_h: int,
+                       n_heads: int, d_ff: int) -> None:
+    """mot_backbone_translate on the current torch stream (bf16 tensors)."""
+    import numpy as np
+    import torch
+    lib = load_library()
+    for name, t in (("src_k", src_k), ("src_v", src_v), ("params", params), ("wr", wr), ("br", br),
+                    ("dst_k", dst_k), ("dst_v", dst_v)):
+        if t is not None and (t.dtype != torch.bfloat16 or not t.is_contiguous()):
+            raise MotError(2, "%s must be a contiguous bfloat16 tensor" % name)
+    lm = np.ascontiguousarray(layer_map, dtype=np.int32)
+    rw = _RW(_ptr(wr), _ptr(br))
+    c = shapes.c()
+    _check(lib.mot_backbone_translate(_ptr(src_k), _ptr(src_v), lm.ctypes.data, _ptr(params), ctypes.byref(rw),
+                                      _ptr(dst_k), _ptr(dst_v), ctypes.byref(c),
+                                      ctypes.byref(_BackboneDims(d_h, n_heads, d_ff)),
+                                      torch.cuda.current_stream().cuda_stream))

@@ -414,6 +414,27 @@ mot_status mot_restore_kv(const void* act, const int32_t* layer_map, const void*
 }
 
 namespace {
+// Offsets (elements) of one expert's packed backbone parameters, in the
+// order the header documents.
+struct BackboneOffsets {
+    size_t ln_in_g, ln_in_b, w_in, b_in, ln_q_g, ln_q_b, ln_c_g, ln_c_b, wq, bq, wk, bk, wv, bv, wo, bo,
+        ln_f_g, ln_f_b, w_f1, b_f1, w_f2, b_f2, ln_out_g, ln_out_b, w_out, b_out, total;
+};
+BackboneOffsets backbone_offsets(size_t d_in, size_t d_h, size_t d_ff, size_t d_out) {
+    BackboneOffsets o;
+    size_t at = 0;
+    auto take = [&](size_t n) { const size_t r = at; at += n; return r; };
+    o.ln_in_g = take(d_in); o.ln_in_b = take(d_in); o.w_in = take(d_h * d_in); o.b_in = take(d_h);
+    o.ln_q_g = take(d_h); o.ln_q_b = take(d_h); o.ln_c_g = take(d_h); o.ln_c_b = take(d_h);
+    o.wq = take(d_h * d_h); o.bq = take(d_h); o.wk = take(d_h * d_h); o.bk = take(d_h);
+    o.wv = take(d_h * d_h); o.bv = take(d_h); o.wo = take(d_h * d_h); o.bo = take(d_h);
+    o.ln_f_g = take(d_h); o.ln_f_b = take(d_h); o.w_f1 = take(d_ff * d_h); o.b_f1 = take(d_ff);
+    o.w_f2 = take(d_h * d_ff); o.b_f2 = take(d_h); o.ln_out_g = take(d_h); o.ln_out_b = take(d_h);
+    o.w_out = take(d_out * d_h); o.b_out = take(d_out);
+    o.total = at;
+    return o;
+}
+
 mot_status check_replay(const mot_replay_shapes* s, bool need_s) {
     if (!s) return fail(MOT_ERR_NULL_ARG, "shapes is NULL");
     if (s->B < 0 || s->T < 0 || (int64_t)s->B * s->T > (int64_t)1 << 26)
@@ -470,6 +491,142 @@ mot_status mot_replay_attention(const void* q, const void* k, const void* v, con
     p.B = s->B; p.T = s->T; p.H_q = s->H_q; p.H_kv = s->H_kv; p.D = s->D; p.S = idx ? s->S : 0;
     p.kv_layout = s->kv_layout;
     hipError_t e = launch_replay_attention(p, stream);
+    if (e != hipSuccess) return fail(MOT_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
+    return MOT_OK;
+}
+
+size_t mot_backbone_param_count(const mot_shapes* s, const mot_backbone_dims* bd) {
+    if (!s || !bd || s->H_src < 1 || s->D_src < 1 || s->H_tgt < 1 || s->D_tgt < 1 || bd->d_h < 1 || bd->d_ff < 1)
+        return 0;
+    return backbone_offsets((size_t)s->H_src * s->D_src, bd->d_h, bd->d_ff, (size_t)s->H_tgt * s->D_tgt).total;
+}
+
+mot_status mot_backbone_translate(const void* src_k, const void* src_v, const int32_t* layer_map, const void* params,
+                                  const mot_router_weights* rw, void* dst_k, void* dst_v, const mot_shapes* s,
+                                  const mot_backbone_dims* bd, hipStream_t stream) {
+    g_err[0] = 0;
+    mot_status st = check_shapes(s);
+    if (st != MOT_OK) return st;
+    if (!bd) return fail(MOT_ERR_NULL_ARG, "backbone dims are NULL");
+    const int d_in = s->H_src * s->D_src, d_out = s->H_tgt * s->D_tgt, d_h = bd->d_h, nh = bd->n_heads,
+              d_ff = bd->d_ff;
+    if (d_h < 1 || nh < 1 || d_ff < 1 || d_h % nh)
+        return fail(MOT_ERR_BAD_SHAPE, "d_h=%d n_heads=%d d_ff=%d: need positive sizes, d_h a multiple of n_heads",
+                    d_h, nh, d_ff);
+    if (s->dtype != MOT_BF16 || s->src_layout != MOT_LAYOUT_BTHD || s->dst_layout != MOT_LAYOUT_BTHD ||
+        s->streams == 1)
+        return fail(MOT_ERR_UNSUPPORTED, "the backbone translator needs bf16, BTHD source and target layouts, "
+                    "keys and values (streams = 2)");
+    if (d_in % 64 || d_in > 4096 || d_h % 64 || d_h > 4096 || d_ff % 64 || d_out % 8 ||
+        (d_h / nh != 64 && d_h / nh != 128))
+        return fail(MOT_ERR_UNSUPPORTED, "backbone sizes: d_in, d_h multiples of 64 up to 4096, d_ff a multiple of "
+                    "64, d_out of 8, head width d_h / n_heads 64 or 128 (got d_in=%d d_h=%d n_heads=%d d_ff=%d "
+                    "d_out=%d)", d_in, d_h, nh, d_ff, d_out);
+    if ((int64_t)s->B * s->T == 0) return MOT_OK;
+    if (!src_k || !src_v || !layer_map || !params || !rw || !rw->w || !dst_k || !dst_v)
+        return fail(MOT_ERR_NULL_ARG, "a required argument is NULL");
+    for (int j = 0; j < s->L_tgt; ++j)
+        if (layer_map[j] < -1 || layer_map[j] >= s->L_src)
+            return fail(MOT_ERR_BAD_LAYER_MAP, "layer_map[%d]=%d outside [-1, %d)", j, layer_map[j], s->L_src);
+    const void* dev_ptrs[] = {src_k, src_v, params, rw->w, dst_k, dst_v};
+    for (const void* q : dev_ptrs)
+        if (!aligned16(q)) return fail(MOT_ERR_MISALIGNED, "device pointer %p is not 16-byte aligned", q);
+    if (rw->b && (reinterpret_cast<uintptr_t>(rw->b) & 1)) return fail(MOT_ERR_MISALIGNED, "router bias misaligned");
+    const size_t n = (size_t)s->B * s->T;
+    const size_t dst_bytes = (size_t)s->L_tgt * n * d_out * 2, src_bytes = (size_t)s->L_src * n * d_in * 2;
+    if (overlaps(dst_k, dst_bytes, dst_v, dst_bytes) || overlaps(dst_k, dst_bytes, src_k, src_bytes) ||
+        overlaps(dst_k, dst_bytes, src_v, src_bytes) || overlaps(dst_v, dst_bytes, src_k, src_bytes) ||
+        overlaps(dst_v, dst_bytes, src_v, src_bytes))
+        return fail(MOT_ERR_BAD_SHAPE, "destination caches overlap each other or the source caches");
+
+    const BackboneOffsets off = backbone_offsets(d_in, d_h, d_ff, d_out);
+    Problem p = base_problem(s);
+    static thread_local UnitTab ut;
+    int nu = 0;
+    for (int j = 0; j < s->L_tgt; ++j)
+        if (layer_map[j] >= 0)
+            for (int x = 0; x < 2; ++x) { ut.code[nu] = unit_code(j, x, layer_map[j], nu); ++nu; }
+    ut.n = nu;
+    if (nu == 0) return MOT_OK;
+    // workspace: gates, then one unit's activations
+    const size_t gates_b = round_up((size_t)nu * p.n_tok_pad * s->E * 4, kAlign);
+    const size_t row_b[] = {(size_t)d_in * 2, (size_t)d_h * 2, (size_t)d_h * 2, (size_t)d_h * 2, (size_t)d_h * 2,
+                            (size_t)d_h * 2, (size_t)d_h * 2, (size_t)d_h * 2, (size_t)d_h * 2, (size_t)d_h * 2,
+                            (size_t)d_ff * 2, (size_t)d_h * 2, (size_t)d_h * 2, (size_t)d_out * 4};
+    constexpr int NB = sizeof(row_b) / sizeof(row_b[0]);
+    size_t need = gates_b, at[NB];
+    for (int k = 0; k < NB; ++k) { at[k] = need; need += round_up(n * row_b[k], kAlign); }
+    void* ws = nullptr;
+    st = owned_workspace(need, &ws);
+    if (st != MOT_OK) return st;
+    char* w8 = reinterpret_cast<char*>(ws);
+    uint16_t* xn = reinterpret_cast<uint16_t*>(w8 + at[0]);
+    uint16_t* z = reinterpret_cast<uint16_t*>(w8 + at[1]);
+    uint16_t* qn = reinterpret_cast<uint16_t*>(w8 + at[2]);
+    uint16_t* cn = reinterpret_cast<uint16_t*>(w8 + at[3]);
+    uint16_t* Q = reinterpret_cast<uint16_t*>(w8 + at[4]);
+    uint16_t* K = reinterpret_cast<uint16_t*>(w8 + at[5]);
+    uint16_t* V = reinterpret_cast<uint16_t*>(w8 + at[6]);
+    uint16_t* att = reinterpret_cast<uint16_t*>(w8 + at[7]);
+    uint16_t* h1 = reinterpret_cast<uint16_t*>(w8 + at[8]);
+    uint16_t* fn = reinterpret_cast<uint16_t*>(w8 + at[9]);
+    uint16_t* f1 = reinterpret_cast<uint16_t*>(w8 + at[10]);
+    uint16_t* h2 = reinterpret_cast<uint16_t*>(w8 + at[11]);
+    uint16_t* on = reinterpret_cast<uint16_t*>(w8 + at[12]);
+    float* mix = reinterpret_cast<float*>(w8 + at[13]);
+
+    p.src[0] = src_k; p.src[1] = src_v; p.wr = rw->w; p.br = rw->b;
+    p.gates = reinterpret_cast<float*>(ws);
+    hipError_t e = launch_router(p, ut, true, stream);
+    const uint16_t* P0 = reinterpret_cast<const uint16_t*>(params);
+    const int n_i = (int)n;
+    for (int u = 0; u < nu && e == hipSuccess; ++u) {
+        const uint32_t code = ut.code[u];
+        const int j = unit_j(code), x = unit_x(code), i = unit_i(code), gs = unit_gslot(code);
+        const uint16_t* src = reinterpret_cast<const uint16_t*>(x ? src_v : src_k) + (size_t)i * n * d_in;
+        uint16_t* dst = reinterpret_cast<uint16_t*>(x ? dst_v : dst_k) + (size_t)j * n * d_out;
+        for (int m = 0; m < s->E && e == hipSuccess; ++m) {
+            const uint16_t* Pm = P0 + (((size_t)j * 2 + x) * s->E + m) * off.total;
+            auto lin = [&](const uint16_t* in, int K_, const uint16_t* W, const uint16_t* bias, int N_, int gelu,
+                           const uint16_t* res, uint16_t* out) {
+                LinearProblem lp;
+                memset(&lp, 0, sizeof lp);
+                lp.in = in; lp.ld_in = (size_t)K_; lp.W = W; lp.bias = bias; lp.res = res; lp.out = out;
+                lp.n = n_i; lp.K = K_; lp.N = N_; lp.gelu = gelu;
+                return launch_linear(lp, stream);
+            };
+            e = launch_ln_rows(src, d_in, Pm + off.ln_in_g, Pm + off.ln_in_b, xn, n_i, d_in, stream);
+            if (e == hipSuccess) e = lin(xn, d_in, Pm + off.w_in, Pm + off.b_in, d_h, 1, nullptr, z);
+            if (e == hipSuccess) e = launch_ln_rows(z, d_h, Pm + off.ln_q_g, Pm + off.ln_q_b, qn, n_i, d_h, stream);
+            if (e == hipSuccess) e = launch_ln_rows(z, d_h, Pm + off.ln_c_g, Pm + off.ln_c_b, cn, n_i, d_h, stream);
+            if (e == hipSuccess) e = lin(qn, d_h, Pm + off.wq, Pm + off.bq, d_h, 0, nullptr, Q);
+            if (e == hipSuccess) e = lin(cn, d_h, Pm + off.wk, Pm + off.bk, d_h, 0, nullptr, K);
+            if (e == hipSuccess) e = lin(cn, d_h, Pm + off.wv, Pm + off.bv, d_h, 0, nullptr, V);
+            if (e == hipSuccess) {
+                ReplayProblem rp;
+                rp.q = Q; rp.k = K; rp.v = V; rp.idx = nullptr; rp.o = att;
+                rp.B = s->B; rp.T = s->T; rp.H_q = nh; rp.H_kv = nh; rp.D = d_h / nh; rp.S = 0;
+                rp.kv_layout = MOT_LAYOUT_BTHD;
+                e = launch_replay_attention(rp, stream);
+            }
+            if (e == hipSuccess) e = lin(att, d_h, Pm + off.wo, Pm + off.bo, d_h, 0, z, h1);
+            if (e == hipSuccess) e = launch_ln_rows(h1, d_h, Pm + off.ln_f_g, Pm + off.ln_f_b, fn, n_i, d_h, stream);
+            if (e == hipSuccess) e = lin(fn, d_h, Pm + off.w_f1, Pm + off.b_f1, d_ff, 1, nullptr, f1);
+            if (e == hipSuccess) e = lin(f1, d_ff, Pm + off.w_f2, Pm + off.b_f2, d_h, 0, h1, h2);
+            if (e == hipSuccess)
+                e = launch_ln_rows(h2, d_h, Pm + off.ln_out_g, Pm + off.ln_out_b, on, n_i, d_h, stream);
+            if (e == hipSuccess) {
+                LinearProblem lp;
+                memset(&lp, 0, sizeof lp);
+                lp.in = on; lp.ld_in = (size_t)d_h; lp.W = Pm + off.w_out; lp.bias = Pm + off.b_out;
+                lp.out = dst; lp.mix_acc = mix;
+                lp.gates = p.gates + (size_t)gs * p.n_tok_pad * s->E; lp.gate_ld = s->E; lp.expert = m;
+                lp.n = n_i; lp.K = d_h; lp.N = d_out; lp.gelu = 1; lp.mix = 1;
+                lp.first = m == 0; lp.last = m == s->E - 1;
+                e = launch_linear(lp, stream);
+            }
+        }
+    }
     if (e != hipSuccess) return fail(MOT_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
     return MOT_OK;
 }

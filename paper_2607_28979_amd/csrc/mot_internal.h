@@ -86,6 +86,25 @@ struct ReplayProblem {
 };
 
 size_t replay_sparse_lds_bytes(int D, int S);
+
+// Generic bf16 linear layer of the backbone translator body.
+struct LinearProblem {
+    const uint16_t* in;   // [n] rows of K inputs, row stride ld_in elements
+    size_t ld_in;
+    const uint16_t* W;    // [N][K]
+    const uint16_t* bias; // [N]
+    const uint16_t* res;  // [n][N] residual added after the activation, or nullptr
+    uint16_t* out;        // [n][N] bf16 (plain output, or the mixture when last)
+    float* mix_acc;       // [n][N] fp32 mixture accumulator (mix)
+    const float* gates;   // gate of row t, expert e: gates[t * gate_ld + e] (mix)
+    int32_t gate_ld, expert;
+    int32_t n, K, N;
+    int32_t gelu, mix, first, last;
+};
+
+hipError_t launch_ln_rows(const uint16_t* in, size_t ld_in, const uint16_t* g, const uint16_t* b, uint16_t* out,
+                          int n, int w, hipStream_t stream);
+hipError_t launch_linear(const LinearProblem& p, hipStream_t stream);
 hipError_t launch_topS_select(const float* A, int32_t* idx, int B, int T, int S, hipStream_t stream);
 hipError_t launch_replay_attention(const ReplayProblem& p, hipStream_t stream);
 

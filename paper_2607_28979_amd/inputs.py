@@ -220,3 +220,38 @@ def source_attention(B: int, T: int, seed: int, window: float = 64.0, sink: floa
             g /= g.sum(axis=1, keepdims=True)
             A[b, u0:u0 + n] = g
     return A
+
+
+def backbone_params(w: Workload, d_h: int, d_ff: int, seed: int) -> np.ndarray:
+    """Packed parameters of the backbone experts, float32 [L_tgt][2][E][P]
+    (bf16-representable), from PCG64(60_000 + seed): for each (j, x, m), in
+    the packed order, LayerNorm gains U(0.8, 1.2) and shifts U(+-0.1), weight
+    matrices Xavier-uniform U(+-sqrt(6/(fan_in+fan_out))), biases
+    U(+-1/sqrt(fan_in))."""
+    d_in, d_out = w.d_in, w.d_out
+    parts = [("ln", d_in), ("w", (d_h, d_in)), ("b", (d_h, d_in)), ("ln", d_h), ("ln", d_h),
+             ("w", (d_h, d_h)), ("b", (d_h, d_h)), ("w", (d_h, d_h)), ("b", (d_h, d_h)),
+             ("w", (d_h, d_h)), ("b", (d_h, d_h)), ("w", (d_h, d_h)), ("b", (d_h, d_h)), ("ln", d_h),
+             ("w", (d_ff, d_h)), ("b", (d_ff, d_h)), ("w", (d_h, d_ff)), ("b", (d_h, d_ff)), ("ln", d_h),
+             ("w", (d_out, d_h)), ("b", (d_out, d_h))]
+    P = sum(2 * a if k == "ln" else (a[0] * a[1] if k == "w" else a[0]) for k, a in parts)
+    rng = np.random.Generator(np.random.PCG64(60_000 + seed))
+    out = np.empty((w.L_tgt, 2, w.E, P), np.float32)
+    for j in range(w.L_tgt):
+        for x in range(2):
+            for m in range(w.E):
+                dst = out[j, x, m]
+                o = 0
+                for k, a in parts:
+                    if k == "ln":
+                        dst[o:o + a] = rng.uniform(0.8, 1.2, a).astype(np.float32)
+                        dst[o + a:o + 2 * a] = rng.uniform(-0.1, 0.1, a).astype(np.float32)
+                        o += 2 * a
+                    elif k == "w":
+                        n = a[0] * a[1]
+                        _uniform(rng, dst[o:o + n], math.sqrt(6.0 / (a[0] + a[1])))
+                        o += n
+                    else:
+                        _uniform(rng, dst[o:o + a[0]], 1.0 / math.sqrt(a[1]))
+                        o += a[0]
+    return round_to_bf16(out)

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert mb.abi_version() == 3
+    assert mb.abi_version() == 4
 
 
 def test_status_strings(lib):
@@ -183,13 +183,40 @@ def test_restore_empty_is_a_no_op(lib):
     _restore(T=0, ptrs=dict(act=None, dst_k=None))     # nothing to do: no pointer is read
 
 
+def _bb_raw(shapes, d_h, n_heads, d_ff):
+    lm = np.array([0, 1], np.int32)
+    rw = mb._RW(None, None)
+    c = shapes.c()
+    mb._check(mb.load_library().mot_backbone_translate(None, None, lm.ctypes.data, None, ctypes.byref(rw), None,
+                                                       None, ctypes.byref(c),
+                                                       ctypes.byref(mb._BackboneDims(d_h, n_heads, d_ff)), None))
+
+
+def test_backbone_rejects(lib):
+    """Shape checks of mot_backbone_translate run before any pointer is used."""
+    s = _shapes(H_tgt=2, D_tgt=64)
+    for sh, dh, nh, code in ((mb.Shapes(**{**s.__dict__, "dst_layout": 1}), 128, 2, "MOT_ERR_UNSUPPORTED"),
+                             (s, 128, 4, "MOT_ERR_UNSUPPORTED"),          # head width 32
+                             (s, 96, 1, "MOT_ERR_UNSUPPORTED"),           # d_h not a multiple of 64
+                             (s, 128, 3, "MOT_ERR_BAD_SHAPE"),            # d_h not a multiple of n_heads
+                             (mb.Shapes(**{**s.__dict__, "dtype": mb.MOT_F32, "D_src": 64}), 128, 2,
+                              "MOT_ERR_UNSUPPORTED")):
+        with pytest.raises(mb.MotError) as e:
+            _bb_raw(sh, dh, nh, 256)
+        assert e.value.name == code, (code, str(e.value))
+    with pytest.raises(mb.MotError) as e:
+        _bb_raw(s, 128, 2, 256)
+    assert e.value.name == "MOT_ERR_NULL_ARG"
+    assert mb.backbone_param_count(s, 128, 2, 256) > 0
+
+
 def test_header_struct_layout_matches_binding(tmp_path):
     """sizeof and every field offset of the header's structs, as a C compiler
     lays them out, equal the ctypes mirrors in the binding."""
     import subprocess
     structs = {"mot_shapes": mb._Shapes, "mot_restore_shapes": mb._RestoreShapes,
                "mot_translator_weights": mb._TW, "mot_router_weights": mb._RW,
-               "mot_replay_shapes": mb._ReplayShapes}
+               "mot_replay_shapes": mb._ReplayShapes, "mot_backbone_dims": mb._BackboneDims}
     lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "mot.h"', "int main(void) {"]
     for cname, cls in structs.items():
         lines.append('printf("%s size %%zu\\n", sizeof(%s));' % (cname, cname))

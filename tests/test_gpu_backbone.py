@@ -1,0 +1,69 @@
+"""GPU parity of the backbone translator body (paper App. C.2) as the experts
+of the mixture, through mot_backbone_translate, against the oracle.
+
+Cases: two experts dense and Top-1, one head of width 128 and two of 64,
+ragged token counts (not multiples of the 64-position attention tiles or the
+128-row linear tiles), a depth-ratio map with a skipped (-1) layer whose
+sentinel must survive bit for bit, and the benchmark's widths on sampled
+rows.  Bar: relative Frobenius error per unit <= 2e-2 (bf16).
+"""
+import numpy as np
+import pytest
+
+from paper_2607_28979_amd import binding as mb
+from paper_2607_28979_amd.configs import Workload
+from paper_2607_28979_amd.inputs import backbone_params, generate
+
+from helpers import SENTINEL, TOL, dst_shape, oracle_dims, rel_frob, to_dev, unit_rows
+
+pytestmark = pytest.mark.gpu
+
+CASES = [  # workload, d_h, n_heads, d_ff
+    (Workload("bb-a", "bf16", L_src=2, L_tgt=2, B=2, T=100, H_src=2, D_src=64, H_tgt=2, D_tgt=64, E=2,
+              hidden=128, seed=81), 128, 2, 256),
+    (Workload("bb-b", "bf16", L_src=3, L_tgt=3, B=1, T=150, H_src=2, D_src=64, H_tgt=4, D_tgt=32, E=2,
+              hidden=128, seed=82, top_k=1, layer_map="depth_ratio"), 128, 1, 128),
+    (Workload("bb-c", "bf16", L_src=1, L_tgt=1, B=3, T=70, H_src=4, D_src=64, H_tgt=2, D_tgt=128, E=3,
+              hidden=256, seed=83), 256, 2, 512),
+    # the benchmark's widths (Qwen2.5-1.5B -> 7B rows, d_h 256, two heads of 128, d_ff 512, E = 2)
+    # on one layer of 520 tokens
+    (Workload("bb-bench-widths", "bf16", L_src=1, L_tgt=1, B=1, T=520, H_src=2, D_src=128, H_tgt=4, D_tgt=128,
+              E=2, hidden=256, seed=84, key_sigma=1.0), 256, 2, 512),
+]
+
+
+def _run(w, d_h, nh, d_ff, lm, params, inp):
+    import torch
+    dev = {n: to_dev(getattr(inp, n), "bf16") for n in ("src_k", "src_v", "wr", "br")}
+    pr = to_dev(params, "bf16")
+    dk = torch.full(dst_shape(w), SENTINEL, dtype=torch.bfloat16, device="cuda")
+    dv = torch.full(dst_shape(w), SENTINEL, dtype=torch.bfloat16, device="cuda")
+    mb.backbone_translate(dev["src_k"], dev["src_v"], lm, pr, dev["wr"], dev["br"], dk, dv,
+                          mb.Shapes.from_workload(w), d_h, nh, d_ff)
+    torch.cuda.synchronize()
+    return (dk.float().cpu().numpy().astype(np.float64), dv.float().cpu().numpy().astype(np.float64))
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0].name for c in CASES])
+def test_backbone_parity(case, oracle_built):
+    from oracle import oracle_backbone_translate
+    w, d_h, nh, d_ff = case
+    print("case", w.name, "d_h", d_h, "heads", nh, "d_ff", d_ff, "top_k", w.top_k or w.E, flush=True)
+    inp = generate(w)
+    params = backbone_params(w, d_h, d_ff, seed=w.seed)
+    lm = (np.arange(w.L_tgt, dtype=np.int32) if w.layer_map == "identity"
+          else mb.depth_ratio_map(w.L_src, w.L_tgt))
+    if w.L_tgt == 3:
+        lm[1] = -1
+    gk, gv = _run(w, d_h, nh, d_ff, lm, params, inp)
+    rk, rv = oracle_backbone_translate(oracle_dims(w), inp.src_k, inp.src_v, lm, params, inp.wr, inp.br,
+                                       d_h, nh, d_ff)
+    worst = 0.0
+    for j in range(w.L_tgt):
+        if lm[j] < 0:
+            assert (gk[j] == SENTINEL).all() and (gv[j] == SENTINEL).all()
+            continue
+        for g, r in ((gk, rk), (gv, rv)):
+            worst = max(worst, rel_frob(unit_rows(g, w, j), unit_rows(r, w, j)))
+    print("  max unit rel-Frobenius error %.3e" % worst, flush=True)
+    assert worst <= TOL["bf16"]
