@@ -92,6 +92,9 @@ def main():
                     help="time the context replay after translation instead: Top-S source-guided "
                          "sparse attention over every Qwen2.5-7B target layer of an 8K context "
                          "(the bottom two layers with full causal attention)")
+    ap.add_argument("--backbone", action="store_true",
+                    help="time the mixture with the backbone translator body (App. C.2) as its experts "
+                         "on the Qwen2.5-1.5B -> 7B cache rows")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain device copy of MIB MiB (a known-size "
                          "reference for the HBM byte counters of a profiler run)")
@@ -107,6 +110,8 @@ def main():
         return bench_moth(args)
     if args.replay:
         return bench_replay(args)
+    if args.backbone:
+        return bench_backbone(args)
 
     import torch
     from paper_2607_28979_amd import binding as mb
@@ -514,6 +519,74 @@ def cpu_baseline_replay(w, rows):
     return {"value": round(rows / dt, 3), "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "sample": "first %d of %d query positions, all %d target layers (selection + attention), fp64"
                       % (rows, w.T, w.L_tgt), "seconds": round(dt, 2)}
+
+
+def bench_backbone(args):
+    """One step = one mot_backbone_translate call over every unit."""
+    import torch
+    from paper_2607_28979_amd import binding as mb
+    from paper_2607_28979_amd.configs import BACKBONE
+    from paper_2607_28979_amd.inputs import backbone_params, bf16_bits, generate
+
+    bw = BACKBONE
+    w = bw.kv
+    torch.cuda.set_device(0)
+    t0 = time.time()
+    inp = generate(w)
+    params = backbone_params(w, bw.d_h, bw.d_ff, seed=w.seed)
+    log("inputs generated in %.1f s" % (time.time() - t0))
+
+    def dev(a):
+        return torch.from_numpy(bf16_bits(a).view(np.int16)).cuda().view(torch.bfloat16)
+
+    d = {n: dev(getattr(inp, n)) for n in ("src_k", "src_v", "wr", "br")}
+    pr = dev(params)
+    shape = (w.L_tgt, w.B, w.T, w.H_tgt, w.D_tgt)
+    dk = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+    dv = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+    lm = np.arange(w.L_tgt, dtype=np.int32)
+    shapes = mb.Shapes.from_workload(w)
+
+    def step():
+        mb.backbone_translate(d["src_k"], d["src_v"], lm, pr, d["wr"], d["br"], dk, dv, shapes, bw.d_h,
+                              bw.n_heads, bw.d_ff)
+
+    calibration_copy(args.calibrate_copy)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("warmup done (%d steps)" % args.warmup)
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_begin = time.perf_counter()
+    for a, b in ev:
+        a.record(stream)
+        step()
+        b.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_begin
+    ms_per_step = wall * 1e3 / args.steps
+    call_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    log("timed %d steps: wall %.3f ms/step, event avg %.3f ms" % (args.steps, ms_per_step, call_ms))
+    flops = bw.flops()
+    tf = flops / (call_ms / 1e3) / 1e12
+    out = {
+        "metric": "translated KV tokens/sec (all layers, backbone-translator experts) Qwen2.5-1.5B→7B",
+        "value": round(w.n_tok / (ms_per_step / 1e3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded numpy; shapes of the model pair, random backbone parameters)",
+        "config": {"workload": w.name, "L_tgt": w.L_tgt, "B": w.B, "T": w.T, "d_in": w.d_in, "d_out": w.d_out,
+                   "E": w.E, "d_h": bw.d_h, "n_heads": bw.n_heads, "d_ff": bw.d_ff, "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "kernel": "mot_backbone_translate (LayerNorm + linear + causal attention chain)",
+                     "achieved": round(tf, 2), "peak": PEAK_TFLOPS["bf16"], "unit": "TFLOP/s",
+                     "frac": round(tf / PEAK_TFLOPS["bf16"], 4), "traffic": None, "alg_flops_per_launch": flops},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(out), flush=True)
 
 
 if __name__ == "__main__":

@@ -166,3 +166,32 @@ class ReplayWorkload:
 # 128), one 8K-token context, S = 128, L_full = 2
 REPLAY = ReplayWorkload("qwen2.5-1.5b->qwen2.5-7b replay, 8K context", L_src=28, L_tgt=28, B=1, T=8192,
                         H_q=28, H_kv=4, D=128, S=128, L_full=2, seed=6)
+
+
+@dataclass(frozen=True)
+class BackboneWorkload:
+    """The Mixture-of-Translators with the backbone translator body (App.
+    C.2) as its experts: the headline model pair's cache rows, translator
+    width d_h, n_heads attention heads, FFN width d_ff, E experts."""
+    kv: Workload
+    d_h: int
+    n_heads: int
+    d_ff: int
+
+    def flops(self) -> float:
+        """Matrix flops of one call: per unit and expert the input, Q, K, V,
+        output, FFN and target projections, and causal attention (scores and
+        values) within each batch row; every expert runs on every token."""
+        w = self.kv
+        per_tok = 2.0 * (w.d_in * self.d_h + 4 * self.d_h * self.d_h + 2 * self.d_h * self.d_ff
+                         + self.d_h * w.d_out)
+        attn = 4.0 * self.d_h * w.B * w.T * (w.T + 1) / 2
+        return w.units() * w.E * (per_tok * w.n_tok + attn)
+
+
+# Qwen2.5-1.5B -> Qwen2.5-7B cache rows (256 -> 512), B = 8, T = 4096, two
+# backbone experts (the paper's N_Tr = 2), both used per token
+BACKBONE = BackboneWorkload(
+    Workload("qwen2.5-1.5b->qwen2.5-7b backbone experts", "bf16", L_src=28, L_tgt=28, B=8, T=4096, H_src=2,
+             D_src=128, H_tgt=4, D_tgt=128, E=2, hidden=256, seed=7, key_sigma=1.0),
+    d_h=256, n_heads=2, d_ff=512)
