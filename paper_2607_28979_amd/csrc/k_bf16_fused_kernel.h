@@ -357,20 +357,15 @@ void k_bf16_fused(Problem p, UnitTab ut) {
         __syncthreads();                                     // barrier B
 
         const float* Gw = Gs + w * (MOT_MAX_EXPERTS * 32);
-        // layer-1 biases of the two staged rows this lane's A operand covers
-        // (rows l16 and 16 + l16), in the low half of lane group 0, else zero
-        const int prow0 = w1_perm(l16), prow1 = w1_perm(16 + l16);
-        const uint32_t grp0 = q4 == 0 ? 0xFFFFFFFFu : 0u;
-        const uint32_t bsel = b1_mask & grp0;
-        // raw loads, one chunk ahead; the masks are applied only at the use in
-        // the next iteration, so nothing waits on these loads mid-iteration
-        auto load_b1 = [&](int c, uint32_t* bv) {
-            typedef const __attribute__((address_space(1))) uint16_t* gu16;
-            bv[0] = (uint32_t)(*(gu16)(b1u + c * 32 + prow0));
-            bv[1] = (uint32_t)(*(gu16)(b1u + c * 32 + prow1));
+        // layer-1 biases enter as the accumulators' initial values: this lane's
+        // rows 4*q4 + j of row half hh are hidden 8*q4 + 4*hh + j of the chunk
+        // (w1_perm), i.e. the 16 bytes at hidden 8*q4 of the chunk's b1.  Raw
+        // loads one chunk ahead; the mask (no bias) is applied only at the use
+        // in the next iteration, so nothing waits on these loads mid-iteration.
+        auto load_b1 = [&](int c, u32x4& bv) {
+            typedef const __attribute__((address_space(1))) u32x4* gu128;
+            bv = *(gu128)(b1u + c * 32 + 8 * q4);
         };
-        // "ones" B operand: k = 0 is 1.0 for every token column, all else 0
-        const u32x4 ones = {0x3F80u & grp0, 0u, 0u, 0u};
         // W1 operand of (k-step s, row half hh) sits at W1c[abase[s & 3] +
         // hh*16*CPR1 + 16*(s >> 2)]: the swizzled chunk (4s + q4) ^ l16 splits
         // into a per-lane part and compile-time offsets
@@ -380,17 +375,17 @@ void k_bf16_fused(Problem p, UnitTab ut) {
         // One iteration in two phases.  Phase A: GELU of the first NEA of the
         // lane's 16 elements of chunk c-1, vector work only, while the layer-2
         // wave on this SIMD runs its MFMAs.  Phase B: a slot schedule of
-        // 16x16x32 MFMAs (four bias MFMAs S[row][t] = b1[row] * 1, then KS2
-        // k-steps x 2 row halves x 2 token halves, all on independent
-        // accumulators) with the three-stage GELU of the other elements spread
+        // 16x16x32 MFMAs (KS2 k-steps x 2 row halves x 2 token halves, all on
+        // independent accumulators; the first k-step starts from the bias)
+        // with the three-stage GELU of the other elements spread
         // over the slots (stage s of element e in slot g0(e) + s*GD); W1
         // operand reads run LOOK slots ahead.
         constexpr int NEA = MOT_FUSED_PHASE_A;
-        auto l1_iter = [&](auto l1c, auto gc, int c, int m, const uint32_t* bv,
-                           const f32x4 (&sp)[2][2], uint32_t* bnext, int c_next,
+        auto l1_iter = [&](auto l1c, auto gc, int c, int m, const u32x4& bv,
+                           const f32x4 (&sp)[2][2], u32x4& bnext, int c_next,
                            f32x4 (&s)[2][2]) {
             constexpr bool do_l1 = decltype(l1c)::value, do_gelu = decltype(gc)::value;
-            constexpr int NM = 4 + 4 * KS2, LOOK = 4, GD = 3, NEB = 16 - C::NOFF - NEA;
+            constexpr int NM = 4 * KS2, LOOK = 4, GD = 3, NEB = 16 - C::NOFF - NEA;
             static_assert(NEB >= 0, "phase split");
             const u32x4* W1c = W1s + (c & 1) * C::W1_CH;
             u32x4* Hw = Hs + ((c - 1) & 1) * C::H_CH + w * 128;
@@ -398,11 +393,11 @@ void k_bf16_fused(Problem p, UnitTab ut) {
             if constexpr (do_l1) load_b1(c_next, bnext);
             u32x4 a1[KS2][2];
             float h[2][2][4], gx[16], gt[16], gx2[16], gq[16], ge[16];
-            // A operand of (k-step s, row half hh), first used in slot 4 + 4s + 2hh
+            // A operand of (k-step s, row half hh), first used in slot 4s + 2hh
             auto read_a = [&](auto kc) {
                 constexpr int k = decltype(kc)::value;
-                if constexpr (k >= 4 && k < NM && ((k - 4) % 2) == 0) {
-                    constexpr int s = (k - 4) / 4, hh = ((k - 4) / 2) % 2;
+                if constexpr (k < NM && (k % 2) == 0) {
+                    constexpr int s = k / 4, hh = (k / 2) % 2;
                     a1[s][hh] = W1c[abase[s & 3] + hh * 16 * C::CPR1 + 16 * (s >> 2)];
                 }
             };
@@ -422,7 +417,13 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                     h[hh][th][jj] = 2.0f * (th ? hg1 : hg0) * sp[hh][th][jj];
                 }
             };
-            const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+            // bias of rows 4*q4 + j of row half hh (zero without a bias)
+            f32x4 binit[2];
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+                const uint32_t w0 = bv[2 * hh] & b1_mask, w1 = bv[2 * hh + 1] & b1_mask;
+                binit[hh] = f32x4{bf16_lo(w0), bf16_hi(w0), bf16_lo(w1), bf16_hi(w1)};
+            }
             if constexpr (do_l1) static_for<0, LOOK>([&](auto kc) { read_a(kc); });
             if constexpr (do_gelu && !MOT_FUSED_A_LAST) {
                 static_for<0, 3>([&](auto stc) {
@@ -434,14 +435,8 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                 constexpr int k = decltype(kc)::value;
                 if constexpr (do_l1) {
                     read_a(std::integral_constant<int, k + LOOK>{});
-                    if constexpr (k < 4) {
-                        constexpr int hh = k / 2, th = k % 2;
-                        const u32x4 ba = {bv[hh] & bsel, 0u, 0u, 0u};
-                        s[hh][th] = mfma_16x16x32(ba, ones, zero4);
-                    } else {
-                        constexpr int st = (k - 4) / 4, hh = ((k - 4) / 2) % 2, th = (k - 4) % 2;
-                        s[hh][th] = mfma_16x16x32(a1[st][hh], zf[th][st], s[hh][th]);
-                    }
+                    constexpr int st = k / 4, hh = (k / 2) % 2, th = k % 2;
+                    s[hh][th] = mfma_16x16x32(a1[st][hh], zf[th][st], st == 0 ? binit[hh] : s[hh][th]);
                 }
                 if constexpr (do_gelu && NEB > 0) {
                     static_for<0, NEB>([&](auto ec) {
@@ -507,7 +502,7 @@ void k_bf16_fused(Problem p, UnitTab ut) {
         };
 
         int m1 = 0, kk1 = 0;
-        uint32_t bcur[2], bnext[2] = {0u, 0u};
+        u32x4 bcur, bnext = {0u, 0u, 0u, 0u};
         load_b1(0, bcur);
         f32x4 s_prev[2][2], s_new[2][2];
         auto advance = [&]() {          // (m1, kk1) -> the next chunk
@@ -521,7 +516,7 @@ void k_bf16_fused(Problem p, UnitTab ut) {
             for (int a = 0; a < 2; ++a)
 #pragma unroll
                 for (int b = 0; b < 2; ++b) s_prev[a][b] = s_new[a][b];
-            bcur[0] = bnext[0]; bcur[1] = bnext[1];
+            bcur = bnext;
         };
         const std::integral_constant<bool, true> yes{};
         const std::integral_constant<bool, false> no{};

@@ -277,8 +277,8 @@ mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* la
     const size_t es = s->dtype == MOT_BF16 ? 2 : 4;
     const void* bias_ptrs[] = {tw->b1, tw->b2, rw->b};
     for (const void* q : bias_ptrs)
-        if (q && (reinterpret_cast<uintptr_t>(q) % es))
-            return fail(MOT_ERR_MISALIGNED, "bias pointer %p is not %zu-byte aligned", q, es);
+        if (q && !aligned16(q))   // the fused kernel reads b1 in 16-byte pieces
+            return fail(MOT_ERR_MISALIGNED, "bias pointer %p is not 16-byte aligned", q);
 
     static thread_local Plan pl;
     make_plan(s, layer_map, &pl);
