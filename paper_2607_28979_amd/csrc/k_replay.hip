@@ -51,7 +51,22 @@ __global__ __launch_bounds__(256) void k_topS_select(const float* A, int32_t* id
     int* s_gt = reinterpret_cast<int*>(s_key + (CACHE ? T : 0));
     int* s_eq = s_gt + (T >> 6) + 1;
     if constexpr (CACHE) {
-        for (int v = tid; v < n; v += 256) s_key[v] = order_key(row[v]);
+        // fill the key cache with 16-byte loads, several in flight per thread
+        // (rows are 16-byte aligned when T % 4 == 0; the last piece may read
+        // positions past u, still inside the row, and they are never used)
+        if ((T & 3) == 0) {
+            const f32x4* row4 = reinterpret_cast<const f32x4*>(row);
+            u32x4* key4 = reinterpret_cast<u32x4*>(s_key);
+            const int n4 = (n + 3) >> 2;
+#pragma unroll 4
+            for (int v = tid; v < n4; v += 256) {
+                const f32x4 a = row4[v];
+                key4[v] = u32x4{order_key(a.x), order_key(a.y), order_key(a.z), order_key(a.w)};
+            }
+        } else {
+#pragma unroll 8
+            for (int v = tid; v < n; v += 256) s_key[v] = order_key(row[v]);
+        }
         __syncthreads();
     }
     auto key_at = [&](int v) -> uint32_t {
