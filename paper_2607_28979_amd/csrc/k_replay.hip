@@ -13,8 +13,9 @@
 //   the gathered key rows loaded straight into A operands, a softmax over the
 //   set, and O^T = V_sel^T . P^T with V_sel staged transposed in LDS.
 // * k_causal_attn: the full causal attention of the bottom layers, tiled
-//   (64 query positions of one head per workgroup, 64-key chunks staged in
-//   LDS with the next chunk prefetched into registers, online softmax).
+//   (64 query positions of one head, two tiles per workgroup paired short
+//   with long, 64-key chunks staged in LDS with the next chunk prefetched
+//   into registers, online softmax).
 // Scores, softmax and accumulation are fp32; Q, K, V, O are bf16.
 #include "mot_device.h"
 #include "mot_internal.h"
@@ -323,8 +324,9 @@ __global__ __launch_bounds__(256) void k_sparse_attn(ReplayProblem p) {
     }
 }
 
-// grid (ceil(T/64), H_q, B), 256 threads: query positions u0 + 16w + l16 of
-// head hq; 64-key chunks up to the tile's last position.  LDS: K chunk
+// grid (ceil(ceil(T/64) / 2), H_q, B), 256 threads: query positions
+// u0 + 16w + l16 of head hq for two query tiles (a short and a long one);
+// 64-key chunks up to the tile's last position.  LDS: K chunk
 // [64][D], V^T chunk [D][64], P per wave [16][64] (bf16).
 template <int D>
 __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
@@ -333,7 +335,13 @@ __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
     __shared__ u32x4 Kl[64 * DC];          // row key: chunk c at (c ^ (key & KSW))
     __shared__ u32x4 Vt[D * 8];            // row d: 8 chunks of 8 keys, chunk c at (c ^ (d & 7))
     __shared__ u32x4 Pl[4][16 * 8];        // per wave, row = position: chunk c at (c ^ (pos & 7))
-    const int u0 = blockIdx.x * 64, hq = blockIdx.y, b = blockIdx.z;
+    // workgroup x runs query tile x and tile ntiles-1-x: every workgroup
+    // walks about the same number of key chunks
+    const int ntiles = (p.T + 63) / 64;
+    for (int pass = 0; pass < 2; ++pass) {
+    const int tile = pass == 0 ? (int)blockIdx.x : ntiles - 1 - (int)blockIdx.x;
+    if (pass == 1 && tile <= (int)blockIdx.x) break;   // uniform over the workgroup
+    const int u0 = tile * 64, hq = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, q4 = lane >> 4;
     const int G = p.H_q / p.H_kv, kvh = hq / G;
     const int u = u0 + 16 * w + l16;       // this lane's query column
@@ -457,6 +465,7 @@ __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
             *reinterpret_cast<u32x2*>(O + (((size_t)b * p.T + u) * p.H_q + hq) * D + 16 * db + 4 * q4) = o2;
         }
     }
+    }
 }
 
 constexpr int kSelCacheMax = 15872;   // rows up to this length keep their keys in LDS (<= 64 KB with the counts)
@@ -484,7 +493,7 @@ hipError_t launch_replay_attention(const ReplayProblem& p, hipStream_t stream) {
         if (p.D == 128) hipLaunchKernelGGL(k_sparse_attn<128>, grid, dim3(256), lds, stream, p);
         else hipLaunchKernelGGL(k_sparse_attn<64>, grid, dim3(256), lds, stream, p);
     } else {
-        const dim3 grid((p.T + 63) / 64, p.H_q, p.B);
+        const dim3 grid(((p.T + 63) / 64 + 1) / 2, p.H_q, p.B);
         if (p.D == 128) hipLaunchKernelGGL(k_causal_attn<128>, grid, dim3(256), 0, stream, p);
         else hipLaunchKernelGGL(k_causal_attn<64>, grid, dim3(256), 0, stream, p);
     }
