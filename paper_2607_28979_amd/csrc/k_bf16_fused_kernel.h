@@ -3,19 +3,21 @@
 // Sec. 3, Definition "Mixture-of-Translators", with the Linear-GELU-Linear
 // translator body).  The E*hidden activations of a token never leave the chip.
 //
-// Workgroup = one unit (target layer, K or V) x TB token blocks of 32 (TB = 3
-// when d_out = 512, else 4); eight waves, two per SIMD, with fixed roles:
+// Workgroup = one unit (target layer, K or V) x TB token blocks of 32, with
+// fixed wave roles:
 //   * waves 0..TB-1: source rows of one token block in VGPRs (MFMA B operand)
 //     for the whole kernel; router logits on MFMA, fp32 softmax, Top-K; then
-//     per 32-wide chunk of E*hidden: layer 1 (S = W1_m[c] z^T + b1, four
-//     independent 16x16x32 accumulators) and g_m * GELU(S) -> bf16 hidden tile
-//     in LDS;
-//   * waves 4..7: d_out/4 output columns each, for all TB blocks; accumulators
-//     seeded with sum_m g_m b2_m; per chunk Y += H . W2_m[:, c]^T (32x32x16);
-//     they also issue every global -> LDS weight load (direct-to-LDS, no VGPR
-//     staging);
-//   * wave 3 when TB = 3: no block; evaluates part of the layer-1 waves'
-//     GELU (fp32 values handed over through LDS).
+//     per 32-wide chunk of E*hidden: layer 1 (S = W1_m[c] z^T, four
+//     independent 16x16x32 accumulators started from the bias) and
+//     g_m * GELU(S) -> bf16 hidden tile in LDS;
+//   * waves 4..4+L2W-1: d_out/L2W output columns each, for all TB blocks;
+//     accumulators seeded with sum_m g_m b2_m; per chunk
+//     Y += H . W2_m[:, c]^T (32x32x16); they also issue every global -> LDS
+//     weight load (direct-to-LDS, no VGPR staging).  L2W = 8 (two layer-2
+//     waves per SIMD, TB = 4, 12 waves) when d_in <= 256 and d_out >= 256,
+//     else 4 (8 waves);
+//   * wave 3 when TB = 3 (d_in = d_out = 512): no block; evaluates part of
+//     the layer-1 waves' GELU (fp32 values handed over through LDS).
 // Iteration c runs layer 1 of chunk c, the GELU of chunk c-1 and layer 2 of
 // chunk c-2, and fetches W1 of chunk c+1 and W2 of chunk c (three W2 stages)
 // or c-1 (two); one workgroup barrier per iteration.  W1's 32 rows are staged
@@ -138,7 +140,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64 * Cfg<D_IN, D_OUT>::NW,
 void k_bf16_fused(Problem p, UnitTab ut) {
     using C = Cfg<D_IN, D_OUT>;
     constexpr int TB = C::TB;
-    // the four layer-2 waves issue the global -> LDS weight loads
+    // the layer-2 waves issue the global -> LDS weight loads
     constexpr int NLD = C::L2W;
     constexpr int W1_RL = C::W1_CH / (64 * NLD), W2_RL = C::W2_CH / (64 * NLD);
     __shared__ u32x4 smem[C::TOTAL];
@@ -167,8 +169,8 @@ void k_bf16_fused(Problem p, UnitTab ut) {
     const int E = ROUTED ? 1 : p.E, hidden = p.hidden, EH = E * hidden;
     const size_t um = unit * p.E + (ROUTED ? tile.x : 0);   // first translator walked
     const int lane = threadIdx.x & 63;
-    // logical wave index: hardware wave h plays role (h + MOT_FUSED_ROLE_SHIFT) & 7
-    // (waves h and h + 4 share a SIMD either way)
+    // logical wave index: hardware wave h plays role (h + MOT_FUSED_ROLE_SHIFT) % NW
+    // (hardware waves h, h + 4, h + 8 share a SIMD)
     const int w = __builtin_amdgcn_readfirstlane(((threadIdx.x >> 6) + MOT_FUSED_ROLE_SHIFT) % C::NW);
     const int tid = w * 64 + lane;   // logical thread index
     const int g = lane >> 5, l32 = lane & 31;
@@ -187,7 +189,7 @@ void k_bf16_fused(Problem p, UnitTab ut) {
     const uint16_t* b2u = p.b2 ? reinterpret_cast<const uint16_t*>(p.b2) + um * D_OUT : nullptr;
     const uint16_t* Wru = reinterpret_cast<const uint16_t*>(p.wr) + unit * E * D_IN;
 
-    // ---- global -> LDS weight loads (the four layer-2 waves)
+    // ---- global -> LDS weight loads (the layer-2 waves)
     // Round r of a stage load fills LDS slots [r*256, r*256 + 256); this lane
     // fills slot r*256 + t.  Its global byte offset is a per-lane part plus a
     // part that depends on r only:
