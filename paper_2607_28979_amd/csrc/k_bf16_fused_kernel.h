@@ -65,6 +65,12 @@ typedef __attribute__((address_space(3))) void lds_void;
 #ifndef MOT_FUSED_OFFLOAD
 #define MOT_FUSED_OFFLOAD 4
 #endif
+// Split iteration (12-wave form): the layer-1 waves evaluate all their GELU
+// elements while the layer-2 waves run their MFMAs, then, after a
+// mid-iteration barrier, the layer-1 waves run their MFMAs alone
+#ifndef MOT_FUSED_SPLIT
+#define MOT_FUSED_SPLIT 1
+#endif
 
 template <int D_IN, int D_OUT>
 struct Cfg {
@@ -97,6 +103,7 @@ struct Cfg {
     static_assert(TOTAL * 16 <= 160 * 1024, "LDS");
     static_assert(W1_CH % 256 == 0 && W2_CH % 256 == 0 && NBW >= 1, "tile shape");
     static_assert(TB * NBW * 16 <= 192, "layer-2 accumulators must leave VGPR room");
+    static constexpr bool SPLIT = MOT_FUSED_SPLIT && L2W == 8 && NOFF == 0;
 };
 
 // Row R of a staged 32-row W1 block holds hidden row w1_perm(R) of the chunk.
@@ -247,6 +254,14 @@ void k_bf16_fused(Problem p, UnitTab ut) {
         __builtin_amdgcn_sched_barrier(0);
     };
     auto sync_stage = [&]() { sync_keep(std::integral_constant<int, 0>{}); };
+    // mid-iteration barrier of the split form: timing only, no data crosses it
+    auto mid_barrier = [&]() {
+        if constexpr (C::SPLIT) {
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
 
     if (is_l1) {
         // ---------------------------------------------------------- layer 1
@@ -387,7 +402,8 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                            const f32x4 (&sp)[2][2], u32x4& bnext, int c_next,
                            f32x4 (&s)[2][2]) {
             constexpr bool do_l1 = decltype(l1c)::value, do_gelu = decltype(gc)::value;
-            constexpr int NM = 4 * KS2, LOOK = 4, GD = 3, NEB = 16 - C::NOFF - NEA;
+            constexpr int NEAx = C::SPLIT ? 16 : NEA;
+            constexpr int NM = 4 * KS2, LOOK = 4, GD = 3, NEB = 16 - C::NOFF - NEAx;
             static_assert(NEB >= 0, "phase split");
             const u32x4* W1c = W1s + (c & 1) * C::W1_CH;
             u32x4* Hw = Hs + ((c - 1) & 1) * C::H_CH + w * 128;
@@ -426,12 +442,46 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                 const uint32_t w0 = bv[2 * hh] & b1_mask, w1 = bv[2 * hh + 1] & b1_mask;
                 binit[hh] = f32x4{bf16_lo(w0), bf16_hi(w0), bf16_lo(w1), bf16_hi(w1)};
             }
+            // the GELU results of chunk c-1 into this wave's hidden tile
+            auto write_h = [&]() {
+                // token th*16 + l16: hidden 8*q4 .. 8*q4+3 from row half 0 and
+                // 8*q4+4 .. 8*q4+7 from row half 1: one 16-byte fragment unit
+                // (the row-half-1 part of token halves >= TH_OFF comes from wave 3)
+                constexpr int TH_OFF = 2 - C::NOFF / 4;
+#pragma unroll
+                for (int th = 0; th < 2; ++th) {
+                    u32x4* dst = &Hw[(q4 >> 1) * 64 + (q4 & 1) * 32 + th * 16 + l16];
+                    if (th >= TH_OFF) {
+                        const u32x2 v = {pack_bf16x2(h[0][th][0], h[0][th][1]), pack_bf16x2(h[0][th][2], h[0][th][3])};
+                        *reinterpret_cast<u32x2*>(dst) = v;
+                    } else {
+                        u32x4 v;
+                        v[0] = pack_bf16x2(h[0][th][0], h[0][th][1]);
+                        v[1] = pack_bf16x2(h[0][th][2], h[0][th][3]);
+                        v[2] = pack_bf16x2(h[1][th][0], h[1][th][1]);
+                        v[3] = pack_bf16x2(h[1][th][2], h[1][th][3]);
+                        *dst = v;
+                    }
+                }
+            };
             if constexpr (do_l1) static_for<0, LOOK>([&](auto kc) { read_a(kc); });
-            if constexpr (do_gelu && !MOT_FUSED_A_LAST) {
+            if constexpr (do_gelu && C::SPLIT) {
+                // all 16 elements, four at a time through the three stages
+                static_for<0, 4>([&](auto gc4) {
+                    constexpr int g4 = decltype(gc4)::value;
+                    static_for<0, 3>([&](auto stc) {
+                        static_for<0, 4>([&](auto ec) {
+                            gelu_elem(std::integral_constant<int, 4 * g4 + decltype(ec)::value>{}, stc);
+                        });
+                    });
+                });
+                write_h();
+            } else if constexpr (do_gelu && !MOT_FUSED_A_LAST) {
                 static_for<0, 3>([&](auto stc) {
                     static_for<0, NEA>([&](auto ec) { gelu_elem(ec, stc); });
                 });
             }
+            mid_barrier();
             __builtin_amdgcn_sched_barrier(0);
             static_for<0, NM>([&](auto kc) {
                 constexpr int k = decltype(kc)::value;
@@ -467,32 +517,12 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                 }
                 __builtin_amdgcn_sched_barrier(0);
             });
-            if constexpr (do_gelu && MOT_FUSED_A_LAST) {
+            if constexpr (do_gelu && MOT_FUSED_A_LAST && !C::SPLIT) {
                 static_for<0, 3>([&](auto stc) {
                     static_for<0, NEA>([&](auto ec) { gelu_elem(ec, stc); });
                 });
             }
-            if constexpr (do_gelu) {
-                // token th*16 + l16: hidden 8*q4 .. 8*q4+3 from row half 0 and
-                // 8*q4+4 .. 8*q4+7 from row half 1: one 16-byte fragment unit
-                // (the row-half-1 part of token halves >= TH_OFF comes from wave 3)
-                constexpr int TH_OFF = 2 - C::NOFF / 4;
-#pragma unroll
-                for (int th = 0; th < 2; ++th) {
-                    u32x4* dst = &Hw[(q4 >> 1) * 64 + (q4 & 1) * 32 + th * 16 + l16];
-                    if (th >= TH_OFF) {
-                        const u32x2 v = {pack_bf16x2(h[0][th][0], h[0][th][1]), pack_bf16x2(h[0][th][2], h[0][th][3])};
-                        *reinterpret_cast<u32x2*>(dst) = v;
-                    } else {
-                        u32x4 v;
-                        v[0] = pack_bf16x2(h[0][th][0], h[0][th][1]);
-                        v[1] = pack_bf16x2(h[0][th][2], h[0][th][3]);
-                        v[2] = pack_bf16x2(h[1][th][0], h[1][th][1]);
-                        v[3] = pack_bf16x2(h[1][th][2], h[1][th][3]);
-                        *dst = v;
-                    }
-                }
-            }
+            if constexpr (do_gelu && !C::SPLIT) write_h();
             if constexpr (do_l1 && C::NOFF > 0) {
                 // hand row half 1 of the offloaded token halves of chunk c to wave 3
                 constexpr int TH_OFF = 2 - C::NOFF / 4;
@@ -536,6 +566,7 @@ void k_bf16_fused(Problem p, UnitTab ut) {
         sync_stage();
         l1_iter(no, yes, nch, m1, bcur, s_prev, bnext, nch - 1, s_new);
         sync_stage();
+        mid_barrier();   // the layer-2 waves' last iteration
     } else if (is_l2) {
         // ---------------------------------------------------------- layer 2
         uint32_t ow1[NV1];
@@ -639,6 +670,7 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                 }
                 __builtin_amdgcn_sched_barrier(0);
             });
+            mid_barrier();
         };
 
         // (m1, kk1): translator and column offset of W2 chunk kw, the one
