@@ -284,7 +284,9 @@ mot_status mot_replay_attention(const void* q, const void* k, const void* v, con
  *   router   as for mot_translate (bias optional)
  *   shapes   as for mot_translate; dtype MOT_BF16, both layouts
  *            MOT_LAYOUT_BTHD, streams 2; hidden, act, algo and the workspace
- *            fields are not used (the library owns the scratch it needs)
+ *            fields are not used (the library owns the scratch it needs:
+ *            the per-device buffer mot_translate uses without a workspace,
+ *            so calls of either that overlap in time on one device race)
  * Requires d_in and d_h multiples of 64 up to 4096, d_ff a multiple of 64,
  * D_tgt a multiple of 8, head width d_h / n_heads of 64 or 128
  * (MOT_ERR_UNSUPPORTED otherwise).  Every check runs before any enqueue.
