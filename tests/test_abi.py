@@ -244,3 +244,41 @@ def test_bench_refuses_several_gpus():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr or "single" in r.stderr
+
+
+def test_empty_contexts_are_no_ops(lib):
+    """B*T == 0 returns MOT_OK without reading any pointer, for every entry point."""
+    c = mb._ReplayShapes(1, 0, 4, 2, 128, 32, 0)
+    mb._check(mb.load_library().mot_topS_select(None, None, ctypes.byref(c), None))
+    mb._check(mb.load_library().mot_replay_attention(None, None, None, None, None, ctypes.byref(c), None))
+    mb._check(mb.load_library().mot_replay_attention(None, None, None, FAKE, None, ctypes.byref(c), None))
+    _bb_raw(_shapes(H_tgt=2, D_tgt=64, T=0), 128, 2, 256)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(S=48), "MOT_ERR_UNSUPPORTED"), (dict(S=256), "MOT_ERR_UNSUPPORTED"),    # D = 128: at most 192
+    (dict(D=96), "MOT_ERR_UNSUPPORTED"), (dict(H_q=6, H_kv=4), "MOT_ERR_BAD_SHAPE"),
+    (dict(H_q=34, H_kv=2), "MOT_ERR_UNSUPPORTED"), (dict(kv_layout=3), "MOT_ERR_BAD_SHAPE"),
+    (dict(T=-1), "MOT_ERR_BAD_SHAPE")])
+def test_replay_rejects(lib, kw, code):
+    base = dict(B=1, T=8, H_q=4, H_kv=2, D=128, S=32, kv_layout=0)
+    base.update(kw)
+    c = mb._ReplayShapes(*[base[k] for k in ("B", "T", "H_q", "H_kv", "D", "S", "kv_layout")])
+    with pytest.raises(mb.MotError) as e:
+        mb._check(mb.load_library().mot_replay_attention(FAKE, FAKE + (1 << 30), FAKE + (2 << 30), FAKE + (3 << 30),
+                                                         FAKE + (4 << 30), ctypes.byref(c), None))
+    assert e.value.name == code, str(e.value)
+
+
+def test_topS_rejects(lib):
+    c = mb._ReplayShapes(1, 70000, 1, 1, 128, 32, 0)
+    with pytest.raises(mb.MotError) as e:
+        mb._check(mb.load_library().mot_topS_select(FAKE, FAKE + (1 << 40), ctypes.byref(c), None))
+    assert e.value.name == "MOT_ERR_UNSUPPORTED"
+    c = mb._ReplayShapes(1, 64, 1, 1, 128, 32, 0)
+    with pytest.raises(mb.MotError) as e:
+        mb._check(mb.load_library().mot_topS_select(FAKE + 2, FAKE + (1 << 40), ctypes.byref(c), None))
+    assert e.value.name == "MOT_ERR_MISALIGNED"
+    with pytest.raises(mb.MotError) as e:
+        mb._check(mb.load_library().mot_topS_select(FAKE, FAKE + 64, ctypes.byref(c), None))   # idx inside A
+    assert e.value.name == "MOT_ERR_BAD_SHAPE"
