@@ -587,21 +587,55 @@ mot_status mot_backbone_translate(const void* src_k, const void* src_v, const in
         uint16_t* dst = reinterpret_cast<uint16_t*>(x ? dst_v : dst_k) + (size_t)j * n * d_out;
         for (int m = 0; m < s->E && e == hipSuccess; ++m) {
             const uint16_t* Pm = P0 + (((size_t)j * 2 + x) * s->E + m) * off.total;
-            auto lin = [&](const uint16_t* in, int K_, const uint16_t* W, const uint16_t* bias, int N_, int gelu,
-                           const uint16_t* res, uint16_t* out) {
+            // one linear launch over up to three parts sharing the input rows;
+            // the LayerNorm of a part's input is fused when K <= kLinearLnMaxK,
+            // otherwise it runs as its own pass into the workspace first
+            auto part = [&](const uint16_t* W, const uint16_t* bias, int N_, uint16_t* out,
+                            const uint16_t* g = nullptr, const uint16_t* b = nullptr) {
+                LinearPart q;
+                q.W = W; q.bias = bias; q.ln_g = g; q.ln_b = b; q.out = out; q.N = N_;
+                return q;
+            };
+            auto lin = [&](const uint16_t* in, int K_, int gelu, const uint16_t* res, int np, const LinearPart* ps) {
                 LinearProblem lp;
                 memset(&lp, 0, sizeof lp);
-                lp.in = in; lp.ld_in = (size_t)K_; lp.W = W; lp.bias = bias; lp.res = res; lp.out = out;
-                lp.n = n_i; lp.K = K_; lp.N = N_; lp.gelu = gelu;
+                lp.in = in; lp.ld_in = (size_t)K_; lp.res = res; lp.n = n_i; lp.K = K_; lp.gelu = gelu;
+                lp.nparts = np;
+                for (int q = 0; q < np; ++q) lp.part[q] = ps[q];
                 return launch_linear(lp, stream);
             };
-            e = launch_ln_rows(src, d_in, Pm + off.ln_in_g, Pm + off.ln_in_b, xn, n_i, d_in, stream);
-            if (e == hipSuccess) e = lin(xn, d_in, Pm + off.w_in, Pm + off.b_in, d_h, 1, nullptr, z);
-            if (e == hipSuccess) e = launch_ln_rows(z, d_h, Pm + off.ln_q_g, Pm + off.ln_q_b, qn, n_i, d_h, stream);
-            if (e == hipSuccess) e = launch_ln_rows(z, d_h, Pm + off.ln_c_g, Pm + off.ln_c_b, cn, n_i, d_h, stream);
-            if (e == hipSuccess) e = lin(qn, d_h, Pm + off.wq, Pm + off.bq, d_h, 0, nullptr, Q);
-            if (e == hipSuccess) e = lin(cn, d_h, Pm + off.wk, Pm + off.bk, d_h, 0, nullptr, K);
-            if (e == hipSuccess) e = lin(cn, d_h, Pm + off.wv, Pm + off.bv, d_h, 0, nullptr, V);
+            auto ln = [&](const uint16_t* in, int w, const uint16_t* g, const uint16_t* b, uint16_t* out,
+                          const uint16_t* g2, const uint16_t* b2, uint16_t* out2) {
+                LnProblem q;
+                q.in = in; q.ld_in = (size_t)w; q.g = g; q.b = b; q.out = out;
+                q.g2 = g2; q.b2 = b2; q.out2 = out2; q.n = n_i; q.w = w;
+                return launch_ln_rows(q, stream);
+            };
+            const bool fuse_in = d_in <= kLinearLnMaxK, fuse_h = d_h <= kLinearLnMaxK;
+            // z = GELU(W_in LN_in(src) + b_in)
+            if (fuse_in) {
+                const LinearPart q = part(Pm + off.w_in, Pm + off.b_in, d_h, z, Pm + off.ln_in_g, Pm + off.ln_in_b);
+                e = lin(src, d_in, 1, nullptr, 1, &q);
+            } else {
+                e = ln(src, d_in, Pm + off.ln_in_g, Pm + off.ln_in_b, xn, nullptr, nullptr, nullptr);
+                const LinearPart q = part(Pm + off.w_in, Pm + off.b_in, d_h, z);
+                if (e == hipSuccess) e = lin(xn, d_in, 1, nullptr, 1, &q);
+            }
+            // Q = Wq LN_Q(z) + bq; K, V = Wk, Wv LN_C(z) + bk, bv
+            if (e == hipSuccess) {
+                if (fuse_h) {
+                    const LinearPart q[3] = {part(Pm + off.wq, Pm + off.bq, d_h, Q, Pm + off.ln_q_g, Pm + off.ln_q_b),
+                                             part(Pm + off.wk, Pm + off.bk, d_h, K, Pm + off.ln_c_g, Pm + off.ln_c_b),
+                                             part(Pm + off.wv, Pm + off.bv, d_h, V, Pm + off.ln_c_g, Pm + off.ln_c_b)};
+                    e = lin(z, d_h, 0, nullptr, 3, q);
+                } else {
+                    e = ln(z, d_h, Pm + off.ln_q_g, Pm + off.ln_q_b, qn, Pm + off.ln_c_g, Pm + off.ln_c_b, cn);
+                    const LinearPart q = part(Pm + off.wq, Pm + off.bq, d_h, Q);
+                    const LinearPart kv[2] = {part(Pm + off.wk, Pm + off.bk, d_h, K), part(Pm + off.wv, Pm + off.bv, d_h, V)};
+                    if (e == hipSuccess) e = lin(qn, d_h, 0, nullptr, 1, &q);
+                    if (e == hipSuccess) e = lin(cn, d_h, 0, nullptr, 2, kv);
+                }
+            }
             if (e == hipSuccess) {
                 ReplayProblem rp;
                 rp.q = Q; rp.k = K; rp.v = V; rp.idx = nullptr; rp.o = att;
@@ -609,19 +643,42 @@ mot_status mot_backbone_translate(const void* src_k, const void* src_v, const in
                 rp.kv_layout = MOT_LAYOUT_BTHD;
                 e = launch_replay_attention(rp, stream);
             }
-            if (e == hipSuccess) e = lin(att, d_h, Pm + off.wo, Pm + off.bo, d_h, 0, z, h1);
-            if (e == hipSuccess) e = launch_ln_rows(h1, d_h, Pm + off.ln_f_g, Pm + off.ln_f_b, fn, n_i, d_h, stream);
-            if (e == hipSuccess) e = lin(fn, d_h, Pm + off.w_f1, Pm + off.b_f1, d_ff, 1, nullptr, f1);
-            if (e == hipSuccess) e = lin(f1, d_ff, Pm + off.w_f2, Pm + off.b_f2, d_h, 0, h1, h2);
-            if (e == hipSuccess)
-                e = launch_ln_rows(h2, d_h, Pm + off.ln_out_g, Pm + off.ln_out_b, on, n_i, d_h, stream);
+            // h1 = Wo att + bo + z
+            if (e == hipSuccess) {
+                const LinearPart q = part(Pm + off.wo, Pm + off.bo, d_h, h1);
+                e = lin(att, d_h, 0, z, 1, &q);
+            }
+            // f1 = GELU(W_f1 LN_F(h1) + b_f1)
+            if (e == hipSuccess) {
+                if (fuse_h) {
+                    const LinearPart q = part(Pm + off.w_f1, Pm + off.b_f1, d_ff, f1, Pm + off.ln_f_g, Pm + off.ln_f_b);
+                    e = lin(h1, d_h, 1, nullptr, 1, &q);
+                } else {
+                    e = ln(h1, d_h, Pm + off.ln_f_g, Pm + off.ln_f_b, fn, nullptr, nullptr, nullptr);
+                    const LinearPart q = part(Pm + off.w_f1, Pm + off.b_f1, d_ff, f1);
+                    if (e == hipSuccess) e = lin(fn, d_h, 1, nullptr, 1, &q);
+                }
+            }
+            // h2 = W_f2 f1 + b_f2 + h1
+            if (e == hipSuccess) {
+                const LinearPart q = part(Pm + off.w_f2, Pm + off.b_f2, d_h, h2);
+                e = lin(f1, d_ff, 0, h1, 1, &q);
+            }
+            // mixture += gate_m * GELU(W_out LN_out(h2) + b_out)
+            const uint16_t* out_in = h2;
+            if (e == hipSuccess && !fuse_h) {
+                e = ln(h2, d_h, Pm + off.ln_out_g, Pm + off.ln_out_b, on, nullptr, nullptr, nullptr);
+                out_in = on;
+            }
             if (e == hipSuccess) {
                 LinearProblem lp;
                 memset(&lp, 0, sizeof lp);
-                lp.in = on; lp.ld_in = (size_t)d_h; lp.W = Pm + off.w_out; lp.bias = Pm + off.b_out;
-                lp.out = dst; lp.mix_acc = mix;
+                lp.in = out_in; lp.ld_in = (size_t)d_h; lp.nparts = 1;
+                lp.part[0] = fuse_h ? part(Pm + off.w_out, Pm + off.b_out, d_out, dst, Pm + off.ln_out_g, Pm + off.ln_out_b)
+                                    : part(Pm + off.w_out, Pm + off.b_out, d_out, dst);
+                lp.mix_acc = mix;
                 lp.gates = p.gates + (size_t)gs * p.n_tok_pad * s->E; lp.gate_ld = s->E; lp.expert = m;
-                lp.n = n_i; lp.K = d_h; lp.N = d_out; lp.gelu = 1; lp.mix = 1;
+                lp.n = n_i; lp.K = d_h; lp.gelu = 1; lp.mix = 1;
                 lp.first = m == 0; lp.last = m == s->E - 1;
                 e = launch_linear(lp, stream);
             }

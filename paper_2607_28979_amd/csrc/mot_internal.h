@@ -87,23 +87,45 @@ struct ReplayProblem {
 
 size_t replay_sparse_lds_bytes(int D, int S);
 
-// Generic bf16 linear layer of the backbone translator body.
+// Generic bf16 linear layer of the backbone translator body.  One launch
+// computes up to three output blocks ("parts") that share the input rows:
+// part q writes out_q[t][o] = act(sum_k x_q[t][k] W_q[o][k] + b_q[o]), where
+// x_q is the input row, or its LayerNorm with (ln_g, ln_b) when ln_g is set
+// (then K <= kLinearLnMaxK).
+struct LinearPart {
+    const uint16_t* W;      // [N][K]
+    const uint16_t* bias;   // [N]
+    const uint16_t* ln_g;   // [K] or nullptr
+    const uint16_t* ln_b;   // [K]
+    uint16_t* out;          // [n][N] bf16 (plain output, or the mixture when last)
+    int32_t N;
+};
+constexpr int kLinearLnMaxK = 256;
 struct LinearProblem {
     const uint16_t* in;   // [n] rows of K inputs, row stride ld_in elements
     size_t ld_in;
-    const uint16_t* W;    // [N][K]
-    const uint16_t* bias; // [N]
+    LinearPart part[3];
+    int32_t nparts;
+    // residual and mixture apply to a single part
     const uint16_t* res;  // [n][N] residual added after the activation, or nullptr
-    uint16_t* out;        // [n][N] bf16 (plain output, or the mixture when last)
     float* mix_acc;       // [n][N] fp32 mixture accumulator (mix)
     const float* gates;   // gate of row t, expert e: gates[t * gate_ld + e] (mix)
     int32_t gate_ld, expert;
-    int32_t n, K, N;
+    int32_t n, K;
     int32_t gelu, mix, first, last;
 };
 
-hipError_t launch_ln_rows(const uint16_t* in, size_t ld_in, const uint16_t* g, const uint16_t* b, uint16_t* out,
-                          int n, int w, hipStream_t stream);
+// LayerNorm of n bf16 rows of width w (w % 8 == 0, w <= 4096): out = LN(in; g, b)
+// and, when out2 is set, out2 = LN(in; g2, b2) on the same statistics.
+struct LnProblem {
+    const uint16_t* in;   // [n] rows, row stride ld_in elements
+    size_t ld_in;
+    const uint16_t *g, *b, *g2, *b2;   // [w] each
+    uint16_t *out, *out2;              // [n][w]
+    int32_t n, w;
+};
+
+hipError_t launch_ln_rows(const LnProblem& p, hipStream_t stream);
 hipError_t launch_linear(const LinearProblem& p, hipStream_t stream);
 hipError_t launch_topS_select(const float* A, int32_t* idx, int B, int T, int S, hipStream_t stream);
 hipError_t launch_replay_attention(const ReplayProblem& p, hipStream_t stream);

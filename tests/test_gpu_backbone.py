@@ -1,8 +1,8 @@
 """GPU parity of the backbone translator body (paper App. C.2) as the experts
 of the mixture, through mot_backbone_translate, against the oracle.
 
-Cases: two experts dense and Top-1, one head of width 128 and two of 64,
-ragged token counts (not multiples of the 64-position attention tiles or the
+Cases: two experts dense and Top-1, three experts, one head of width 128,
+two of 64 and three of 128, rows of up to and wider than 256, ragged token counts (not multiples of the 64-position attention tiles or the
 128-row linear tiles), a depth-ratio map with a skipped (-1) layer whose
 sentinel must survive bit for bit, and the benchmark's widths on sampled
 rows.  Bar: relative Frobenius error per unit <= 2e-2 (bf16).
@@ -25,6 +25,9 @@ CASES = [  # workload, d_h, n_heads, d_ff
               hidden=128, seed=82, top_k=1, layer_map="depth_ratio"), 128, 1, 128),
     (Workload("bb-c", "bf16", L_src=1, L_tgt=1, B=3, T=70, H_src=4, D_src=64, H_tgt=2, D_tgt=128, E=3,
               hidden=256, seed=83), 256, 2, 512),
+    # rows wider than 256 (LayerNorm on whole waves), three heads, an output tile count of 3
+    (Workload("bb-d", "bf16", L_src=1, L_tgt=1, B=1, T=90, H_src=4, D_src=128, H_tgt=2, D_tgt=96, E=2,
+              hidden=128, seed=85), 384, 3, 256),
     # the benchmark's widths (Qwen2.5-1.5B -> 7B rows, d_h 256, two heads of 128, d_ff 512, E = 2)
     # on one layer of 520 tokens
     (Workload("bb-bench-widths", "bf16", L_src=1, L_tgt=1, B=1, T=520, H_src=2, D_src=128, H_tgt=4, D_tgt=128,
