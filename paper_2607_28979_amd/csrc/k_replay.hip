@@ -398,7 +398,10 @@ __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
         }
         __syncthreads();
         if (kc0 + 64 <= last) fetch(kc0 + 64);
-        // scores^T[key][position] for 4 key blocks of 16
+        // scores^T[key][position] for 4 key blocks of 16.  Only the diagonal
+        // chunk (kc0 == u0, which also holds any keys past T) needs the mask:
+        // every key of an earlier chunk precedes every position of the tile.
+        const bool diag = kc0 == u0;
         f32x4 sc[4];
         float cm = -INFINITY;
 #pragma unroll
@@ -408,34 +411,42 @@ __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
 #pragma unroll
             for (int ks = 0; ks < D / 32; ++ks)
                 sc[kb] = mfma_16x16x32(Kl[kr * DC + ((4 * ks + q4) ^ (kr & KSW))], qop[ks], sc[kb]);
+            if (diag) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int key = kc0 + kb * 16 + 4 * q4 + j;
-                sc[kb][j] = key <= u ? sc[kb][j] : -INFINITY;
-                cm = fmaxf(cm, sc[kb][j]);
+                for (int j = 0; j < 4; ++j) {
+                    const int key = kc0 + kb * 16 + 4 * q4 + j;
+                    sc[kb][j] = key <= u ? sc[kb][j] : -INFINITY;
+                }
             }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) cm = fmaxf(cm, sc[kb][j]);
         }
         cm = fmaxf(cm, __shfl_xor(cm, 16, 64));
         cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
         const float mn = fmaxf(m, cm);   // finite: chunk 0 holds key 0 <= u
         const float alpha = exp2f((m - mn) * sl2);
+        const float mo = mn * sl2;       // e = 2^(s sl2 - mn sl2); exp2(-inf) = 0 for masked keys
         float rs = 0.f;
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const float e = sc[kb][j] == -INFINITY ? 0.f : exp2f((sc[kb][j] - mn) * sl2);
+                const float e = exp2f(fmaf(sc[kb][j], sl2, -mo));
                 sc[kb][j] = e;
                 rs += e;
             }
         rs += __shfl_xor(rs, 16, 64);
         rs += __shfl_xor(rs, 32, 64);
         l = l * alpha + rs;
+        // alpha is exactly 1 where the running maximum did not move: the
+        // accumulators are rescaled only when some position's maximum rose
+        if (__builtin_amdgcn_ballot_w64(mn != m)) {
+#pragma unroll
+            for (int db = 0; db < D / 16; ++db)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[db][j] *= alpha;
+        }
         m = mn;
-#pragma unroll
-        for (int db = 0; db < D / 16; ++db)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) acc[db][j] *= alpha;
         uint32_t* Pw = reinterpret_cast<uint32_t*>(Pl[w]);
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) {
