@@ -26,6 +26,10 @@ SOURCES = [(f, os.path.splitext(f)[0], {}) for f in
 SOURCES += [("k_bf16_fused_inst.hip", "k_bf16_fused_%d_%d" % (a, b),
              {"MOT_FUSED_D_IN": a, "MOT_FUSED_D_OUT": b})
             for a in (128, 256, 512) for b in (128, 256, 512)]
+# per-source device-compiler options: the attention kernels keep their MFMA
+# accumulators in VGPRs (the softmax rescales them in place; the AGPR form
+# copies them in and out around every product)
+EXTRA = {"k_replay.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def hipcc() -> str:
@@ -45,7 +49,7 @@ def flags():
 def _compile(entry) -> str:
     src, name, defs = entry
     obj = os.path.join(BUILD, name + ".o")
-    cmd = [hipcc(), *flags(), *["-D%s=%s" % kv for kv in defs.items()], "-c", os.path.join(CSRC, src),
+    cmd = [hipcc(), *flags(), *EXTRA.get(src, []), *["-D%s=%s" % kv for kv in defs.items()], "-c", os.path.join(CSRC, src),
            "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:

@@ -365,17 +365,25 @@ __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
     // current one is computed: K items (key, d chunk), V items (key pair, d chunk)
     constexpr int NKI = 64 * DC / 256, NVI = 32 * DC / 256;
     u32x4 kreg[NKI], va[NVI], vb[NVI];
+    // key t of this batch row and KV head sits at row0 + t * ts in either
+    // layout; per chunk the base is scalar and each item adds a 32-bit offset
+    // (H_kv * D < 2^20 is checked on the host)
+    const uint32_t ts = p.kv_layout == MOT_LAYOUT_BTHD ? (uint32_t)(p.H_kv * D) : (uint32_t)D;
+    const size_t row0 = kv_row(p, b, 0, kvh);
     auto fetch = [&](int kc0) {
+        const uint16_t* Kc = K + row0 + (size_t)kc0 * ts;
+        const uint16_t* Vc = V + row0 + (size_t)kc0 * ts;
 #pragma unroll
         for (int i = 0; i < NKI; ++i) {
-            const int it = tid + 256 * i, kr = it / DC, c = it % DC, t = kc0 + kr;
-            kreg[i] = t < p.T ? *reinterpret_cast<const u32x4*>(K + kv_row(p, b, t, kvh) + 8 * c) : zero;
+            const int it = tid + 256 * i, kr = it / DC, c = it % DC;
+            kreg[i] = kc0 + kr < p.T ? *reinterpret_cast<const u32x4*>(Kc + ((uint32_t)kr * ts + 8 * c)) : zero;
         }
 #pragma unroll
         for (int i = 0; i < NVI; ++i) {
-            const int it = tid + 256 * i, c = it / 32, t = kc0 + 2 * (it % 32);
-            va[i] = t < p.T ? *reinterpret_cast<const u32x4*>(V + kv_row(p, b, t, kvh) + 8 * c) : zero;
-            vb[i] = t + 1 < p.T ? *reinterpret_cast<const u32x4*>(V + kv_row(p, b, t + 1, kvh) + 8 * c) : zero;
+            const int it = tid + 256 * i, c = it / 32, kr = 2 * (it % 32);
+            va[i] = kc0 + kr < p.T ? *reinterpret_cast<const u32x4*>(Vc + ((uint32_t)kr * ts + 8 * c)) : zero;
+            vb[i] = kc0 + kr + 1 < p.T ? *reinterpret_cast<const u32x4*>(Vc + ((uint32_t)(kr + 1) * ts + 8 * c))
+                                       : zero;
         }
     };
     fetch(0);
@@ -424,14 +432,16 @@ __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
         cm = fmaxf(cm, __shfl_xor(cm, 16, 64));
         cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
         const float mn = fmaxf(m, cm);   // finite: chunk 0 holds key 0 <= u
-        const float alpha = exp2f((m - mn) * sl2);
-        const float mo = mn * sl2;       // e = 2^(s sl2 - mn sl2); exp2(-inf) = 0 for masked keys
+        // v_exp_f32 directly: results below 2^-126 flush to 0, far below the
+        // bf16 resolution of P; exp2(-inf) = 0 for masked keys and the first chunk
+        const float alpha = __builtin_amdgcn_exp2f((m - mn) * sl2);
+        const float mo = mn * sl2;       // e = 2^(s sl2 - mn sl2)
         float rs = 0.f;
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const float e = exp2f(fmaf(sc[kb][j], sl2, -mo));
+                const float e = __builtin_amdgcn_exp2f(fmaf(sc[kb][j], sl2, -mo));
                 sc[kb][j] = e;
                 rs += e;
             }

@@ -447,6 +447,8 @@ mot_status check_replay(const mot_replay_shapes* s, bool need_s) {
     if (need_s && s->S < 1) return fail(MOT_ERR_BAD_SHAPE, "S=%d must be >= 1", s->S);
     if (s->D != 64 && s->D != 128)
         return fail(MOT_ERR_UNSUPPORTED, "D=%d: replay attention supports head dims 64 and 128", s->D);
+    if ((int64_t)s->H_kv * s->D >= (1 << 20))
+        return fail(MOT_ERR_UNSUPPORTED, "H_kv * D = %lld: at most 2^20 - 1", (long long)s->H_kv * s->D);
     if (s->H_q / s->H_kv > 16)
         return fail(MOT_ERR_UNSUPPORTED, "%d query heads per KV head (at most 16)", s->H_q / s->H_kv);
     if (need_s && (s->S % 32 || s->S > 256 || replay_sparse_lds_bytes(s->D, s->S) > 65536))

@@ -259,7 +259,7 @@ def test_empty_contexts_are_no_ops(lib):
     (dict(S=48), "MOT_ERR_UNSUPPORTED"), (dict(S=256), "MOT_ERR_UNSUPPORTED"),    # D = 128: at most 192
     (dict(D=96), "MOT_ERR_UNSUPPORTED"), (dict(H_q=6, H_kv=4), "MOT_ERR_BAD_SHAPE"),
     (dict(H_q=34, H_kv=2), "MOT_ERR_UNSUPPORTED"), (dict(kv_layout=3), "MOT_ERR_BAD_SHAPE"),
-    (dict(T=-1), "MOT_ERR_BAD_SHAPE")])
+    (dict(T=-1), "MOT_ERR_BAD_SHAPE"), (dict(H_q=8192, H_kv=8192), "MOT_ERR_UNSUPPORTED")])
 def test_replay_rejects(lib, kw, code):
     base = dict(B=1, T=8, H_q=4, H_kv=2, D=128, S=32, kv_layout=0)
     base.update(kw)
