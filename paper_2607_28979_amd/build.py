@@ -26,10 +26,11 @@ SOURCES = [(f, os.path.splitext(f)[0], {}) for f in
 SOURCES += [("k_bf16_fused_inst.hip", "k_bf16_fused_%d_%d" % (a, b),
              {"MOT_FUSED_D_IN": a, "MOT_FUSED_D_OUT": b})
             for a in (128, 256, 512) for b in (128, 256, 512)]
-# per-source device-compiler options: the attention kernels keep their MFMA
-# accumulators in VGPRs (the softmax rescales them in place; the AGPR form
-# copies them in and out around every product)
-EXTRA = {"k_replay.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+# per-source device-compiler options: these kernels keep their MFMA
+# accumulators in VGPRs (the attention softmax rescales them in place and the
+# GEMM epilogues read them; the AGPR form copies them in and out)
+_VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
+EXTRA = {f: _VGPR_FORM for f in ("k_replay.hip", "k_backbone.hip", "k_project.hip", "k_bf16_unfused.hip")}
 
 
 def hipcc() -> str:
