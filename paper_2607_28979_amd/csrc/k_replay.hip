@@ -191,6 +191,14 @@ __device__ __forceinline__ size_t kv_row(const ReplayProblem& p, int b, int t, i
                                           : (((size_t)b * p.H_kv + kvh) * p.T + t) * p.D;
 }
 
+// Workgroups are dispatched round-robin over the 8 XCDs, each with its own
+// L2.  A grid of 8 * ceil(n / 8) workgroups is remapped so that XCD k walks
+// the contiguous range [k * per, (k + 1) * per) of the n work items: items
+// that share K/V rows (neighbouring positions, the heads of one KV group)
+// meet in one L2.  Items >= n return at once.
+__device__ __forceinline__ int xcd_item(int id, int n) { return (id & 7) * ((n + 7) >> 3) + (id >> 3); }
+inline int xcd_grid(int n) { return 8 * ((n + 7) / 8); }
+
 __device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 // 8 bf16 of chunk a (keys k0) and c (key k0+1) interleaved into 8 words:
@@ -200,7 +208,7 @@ __device__ __forceinline__ uint32_t pair_word(const u32x4& a, const u32x4& c, in
     return (i & 1) ? ((wa >> 16) | (wc & 0xFFFF0000u)) : ((wa & 0xFFFFu) | (wc << 16));
 }
 
-// grid (T, B), 256 threads; dynamic LDS: V^T [D][S] + P [16][S] (bf16) + 128 floats
+// grid (xcd_grid(T), B), 256 threads; dynamic LDS: V^T [D][S] + P [16][S] (bf16) + 128 floats
 template <int D>
 __global__ __launch_bounds__(256) void k_sparse_attn(ReplayProblem p) {
     extern __shared__ u32x4 s_dyn[];
@@ -210,7 +218,8 @@ __global__ __launch_bounds__(256) void k_sparse_attn(ReplayProblem p) {
     u32x4* Vt = s_dyn;                      // row d: SC chunks, chunk c at (c ^ (d & swm))
     u32x4* Pl = s_dyn + D * SC;             // row = query head slot
     float* red = reinterpret_cast<float*>(Pl + 16 * SC);   // [4 waves][16]: max, then sum
-    const int u = blockIdx.x, b = blockIdx.y;
+    const int u = xcd_item(blockIdx.x, p.T), b = blockIdx.y;
+    if (u >= p.T) return;   // uniform over the workgroup
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, q4 = lane >> 4;
     const int G = p.H_q / p.H_kv, KB = S / 16;
     const int32_t* keys = p.idx + ((size_t)b * p.T + u) * S;
@@ -324,7 +333,8 @@ __global__ __launch_bounds__(256) void k_sparse_attn(ReplayProblem p) {
     }
 }
 
-// grid (ceil(ceil(T/64) / 2), H_q, B), 256 threads: query positions
+// grid xcd_grid(npairs * H_q * B) with npairs = ceil(ceil(T/64) / 2), items
+// ordered (pair, head, batch row) pair fastest; 256 threads: query positions
 // u0 + 16w + l16 of head hq for two query tiles (a short and a long one);
 // 64-key chunks up to the tile's last position.  LDS: K chunk
 // [64][D], V^T chunk [D][64], P per wave [16][64] (bf16).
@@ -337,11 +347,14 @@ __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
     __shared__ u32x4 Pl[4][16 * 8];        // per wave, row = position: chunk c at (c ^ (pos & 7))
     // workgroup x runs query tile x and tile ntiles-1-x: every workgroup
     // walks about the same number of key chunks
-    const int ntiles = (p.T + 63) / 64;
+    const int ntiles = (p.T + 63) / 64, npairs = (ntiles + 1) / 2;
+    const int item = xcd_item(blockIdx.x, npairs * p.H_q * p.B);
+    if (item >= npairs * p.H_q * p.B) return;   // uniform over the workgroup
+    const int px = item % npairs, hq = (item / npairs) % p.H_q, b = item / (npairs * p.H_q);
     for (int pass = 0; pass < 2; ++pass) {
-    const int tile = pass == 0 ? (int)blockIdx.x : ntiles - 1 - (int)blockIdx.x;
-    if (pass == 1 && tile <= (int)blockIdx.x) break;   // uniform over the workgroup
-    const int u0 = tile * 64, hq = blockIdx.y, b = blockIdx.z;
+    const int tile = pass == 0 ? px : ntiles - 1 - px;
+    if (pass == 1 && tile <= px) break;   // uniform over the workgroup
+    const int u0 = tile * 64;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, q4 = lane >> 4;
     const int G = p.H_q / p.H_kv, kvh = hq / G;
     const int u = u0 + 16 * w + l16;       // this lane's query column
@@ -509,12 +522,13 @@ hipError_t launch_topS_select(const float* A, int32_t* idx, int B, int T, int S,
 hipError_t launch_replay_attention(const ReplayProblem& p, hipStream_t stream) {
     if (p.B == 0 || p.T == 0) return hipSuccess;
     if (p.idx) {
-        const dim3 grid(p.T, p.B);
+        const dim3 grid(xcd_grid(p.T), p.B);
         const size_t lds = replay_sparse_lds_bytes(p.D, p.S);
         if (p.D == 128) hipLaunchKernelGGL(k_sparse_attn<128>, grid, dim3(256), lds, stream, p);
         else hipLaunchKernelGGL(k_sparse_attn<64>, grid, dim3(256), lds, stream, p);
     } else {
-        const dim3 grid(((p.T + 63) / 64 + 1) / 2, p.H_q, p.B);
+        const int npairs = ((p.T + 63) / 64 + 1) / 2;
+        const dim3 grid(xcd_grid(npairs * p.H_q * p.B));
         if (p.D == 128) hipLaunchKernelGGL(k_causal_attn<128>, grid, dim3(256), 0, stream, p);
         else hipLaunchKernelGGL(k_causal_attn<64>, grid, dim3(256), 0, stream, p);
     }
