@@ -209,12 +209,14 @@ __device__ __forceinline__ uint32_t pair_word(const u32x4& a, const u32x4& c, in
 }
 
 // grid (xcd_grid(T), B), 256 threads; dynamic LDS: V^T [D][S] + P [16][S] (bf16) + 128 floats
-template <int D>
+template <int D, int SMAX>
 __global__ __launch_bounds__(256) void k_sparse_attn(ReplayProblem p) {
     extern __shared__ u32x4 s_dyn[];
     constexpr int DC = D / 8;               // 16-byte chunks per row of D
     const int S = p.S, SC = S / 8;          // 16-byte chunks per row of S keys
-    const int swm = (SC < 16 ? SC : 16) - 1;
+    // XOR swizzle within aligned groups of the largest power of two (<= 16)
+    // dividing SC, so that a permuted chunk stays inside its row
+    const int swm = ((SC & -SC) < 16 ? (SC & -SC) : 16) - 1;
     u32x4* Vt = s_dyn;                      // row d: SC chunks, chunk c at (c ^ (d & swm))
     u32x4* Pl = s_dyn + D * SC;             // row = query head slot
     float* red = reinterpret_cast<float*>(Pl + 16 * SC);   // [4 waves][16]: max, then sum
@@ -231,47 +233,74 @@ __global__ __launch_bounds__(256) void k_sparse_attn(ReplayProblem p) {
     const u32x4 zero = {0u, 0u, 0u, 0u};
     // a key entry outside 0..u (the -1 padding) is not attended
     auto key_ok = [&](int kv) { return kv >= 0 && kv <= u; };
+    // the set is the same for every KV head: read it once
+    __shared__ int s_keys[256];
+    for (int i = tid; i < S; i += 256) s_keys[i] = keys[i];
+    __syncthreads();
+    // per-thread item counts for sets of up to SMAX keys
+    constexpr int MAXR = SMAX / 2 * DC / 256;   // V key-pair items
+    constexpr int MAXB = SMAX / 16 / 4;         // key blocks per wave
 
     for (int kvh = 0; kvh < p.H_kv; ++kvh) {
-        // (a) V_sel^T into LDS: item = (key pair, d chunk)
-        uint32_t* Vw = reinterpret_cast<uint32_t*>(Vt);
-        for (int it = tid; it < (S / 2) * DC; it += 256) {
-            const int pr = it % (S / 2), dc = it / (S / 2), k0 = 2 * pr;
-            const int v0 = keys[k0], v1 = keys[k0 + 1];
-            const u32x4 a = key_ok(v0) ? *reinterpret_cast<const u32x4*>(V + kv_row(p, b, v0, kvh) + 8 * dc) : zero;
-            const u32x4 c = key_ok(v1) ? *reinterpret_cast<const u32x4*>(V + kv_row(p, b, v1, kvh) + 8 * dc) : zero;
+        // every gather of this KV head is issued before the first is used:
+        // (a) V rows, item = (key pair, d chunk); (b) K rows of this wave's
+        // key blocks kb = w, w+4, ...; then the query heads of the group
+        u32x4 va[MAXR], vc[MAXR];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int d = 8 * dc + i;
-                Vw[(d * SC + ((k0 >> 3) ^ (d & swm))) * 4 + ((k0 & 7) >> 1)] = pair_word(a, c, i);
+        for (int r = 0; r < MAXR; ++r) {
+            const int it = tid + 256 * r;
+            va[r] = zero;
+            vc[r] = zero;
+            if (it < (S / 2) * DC) {
+                const int pr = it % (S / 2), dc = it / (S / 2), k0 = 2 * pr;
+                const int v0 = s_keys[k0], v1 = s_keys[k0 + 1];
+                if (key_ok(v0)) va[r] = *reinterpret_cast<const u32x4*>(V + kv_row(p, b, v0, kvh) + 8 * dc);
+                if (key_ok(v1)) vc[r] = *reinterpret_cast<const u32x4*>(V + kv_row(p, b, v1, kvh) + 8 * dc);
             }
         }
-        // (b) scores^T[key][head] for key blocks kb = w, w+4, ...
+        u32x4 ka[MAXB][D / 32];
+#pragma unroll
+        for (int i = 0; i < MAXB; ++i) {
+            const int kb = w + 4 * i;
+            const int kr = kb < KB ? s_keys[kb * 16 + l16] : -1;
+            const uint16_t* krow = K + (key_ok(kr) ? kv_row(p, b, kr, kvh) : 0);
+#pragma unroll
+            for (int ks = 0; ks < D / 32; ++ks)
+                ka[i][ks] = key_ok(kr) ? *reinterpret_cast<const u32x4*>(krow + 32 * ks + 8 * q4) : zero;
+        }
         const int hq = kvh * G + l16;
         u32x4 qop[D / 32];
 #pragma unroll
         for (int ks = 0; ks < D / 32; ++ks)
             qop[ks] = l16 < G ? *reinterpret_cast<const u32x4*>(Q + (((size_t)b * p.T + u) * p.H_q + hq) * D + 32 * ks + 8 * q4)
                               : zero;
-        f32x4 sc[4];
+        // V_sel^T into LDS
+        uint32_t* Vw = reinterpret_cast<uint32_t*>(Vt);
+#pragma unroll
+        for (int r = 0; r < MAXR; ++r) {
+            const int it = tid + 256 * r;
+            if (it < (S / 2) * DC) {
+                const int pr = it % (S / 2), dc = it / (S / 2), k0 = 2 * pr;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const int d = 8 * dc + i;
+                    Vw[(d * SC + ((k0 >> 3) ^ (d & swm))) * 4 + ((k0 & 7) >> 1)] = pair_word(va[r], vc[r], i);
+                }
+            }
+        }
+        // scores^T[key][head]
+        f32x4 sc[MAXB];
         float mx = -INFINITY;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < MAXB; ++i) {
             const int kb = w + 4 * i;
             sc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
             if (kb < KB) {
-                const int kr = keys[kb * 16 + l16];
-                const uint16_t* krow = K + (key_ok(kr) ? kv_row(p, b, kr, kvh) : 0);
 #pragma unroll
-                for (int ks = 0; ks < D / 32; ++ks) {
-                    const u32x4 a = key_ok(kr) ? *reinterpret_cast<const u32x4*>(krow + 32 * ks + 8 * q4) : zero;
-                    sc[i] = mfma_16x16x32(a, qop[ks], sc[i]);
-                }
-                const int4 kk = *reinterpret_cast<const int4*>(keys + kb * 16 + 4 * q4);
-                const int kv4[4] = {kk.x, kk.y, kk.z, kk.w};
+                for (int ks = 0; ks < D / 32; ++ks) sc[i] = mfma_16x16x32(ka[i][ks], qop[ks], sc[i]);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    sc[i][j] = key_ok(kv4[j]) ? sc[i][j] : -INFINITY;
+                    sc[i][j] = key_ok(s_keys[kb * 16 + 4 * q4 + j]) ? sc[i][j] : -INFINITY;
                     mx = fmaxf(mx, sc[i][j]);
                 }
             } else {
@@ -287,7 +316,7 @@ __global__ __launch_bounds__(256) void k_sparse_attn(ReplayProblem p) {
         mx = fmaxf(fmaxf(red[l16], red[16 + l16]), fmaxf(red[32 + l16], red[48 + l16]));
         float sum = 0.f;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < MAXB; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const float e = sc[i][j] == -INFINITY ? 0.f : exp2f((sc[i][j] - mx) * sl2);
@@ -303,7 +332,7 @@ __global__ __launch_bounds__(256) void k_sparse_attn(ReplayProblem p) {
         const float inv = sum > 0.f ? 1.0f / sum : 0.f;
         uint32_t* Pw = reinterpret_cast<uint32_t*>(Pl);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < MAXB; ++i) {
             const int kb = w + 4 * i;
             if (kb < KB) {
                 const int ch = (2 * kb + (q4 >> 1)) ^ (l16 & swm);
@@ -524,8 +553,14 @@ hipError_t launch_replay_attention(const ReplayProblem& p, hipStream_t stream) {
     if (p.idx) {
         const dim3 grid(xcd_grid(p.T), p.B);
         const size_t lds = replay_sparse_lds_bytes(p.D, p.S);
-        if (p.D == 128) hipLaunchKernelGGL(k_sparse_attn<128>, grid, dim3(256), lds, stream, p);
-        else hipLaunchKernelGGL(k_sparse_attn<64>, grid, dim3(256), lds, stream, p);
+        // register arrays sized for S <= 128, or for the largest S the LDS allows
+        if (p.D == 128) {
+            if (p.S <= 128) hipLaunchKernelGGL((k_sparse_attn<128, 128>), grid, dim3(256), lds, stream, p);
+            else hipLaunchKernelGGL((k_sparse_attn<128, 192>), grid, dim3(256), lds, stream, p);
+        } else {
+            if (p.S <= 128) hipLaunchKernelGGL((k_sparse_attn<64, 128>), grid, dim3(256), lds, stream, p);
+            else hipLaunchKernelGGL((k_sparse_attn<64, 256>), grid, dim3(256), lds, stream, p);
+        }
     } else {
         const int npairs = ((p.T + 63) / 64 + 1) / 2;
         const dim3 grid(xcd_grid(npairs * p.H_q * p.B));

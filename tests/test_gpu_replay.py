@@ -6,7 +6,7 @@ key selection and replay attention, through the C ABI, against the oracle.
   and a 16500-token map (rows longer than the LDS row cache) on sampled
   rows;
 * sparse attention over the selected sets (grouped-query heads, both KV
-  layouts, head dims 64 and 128, S = 32 .. 128), sets with padding and
+  layouts, head dims 64 and 128, S = 32 .. 256), sets with padding and
   out-of-range entries, an all-empty set (zeros);
 * full causal attention (the bottom L_Full layers) with a ragged last tile;
 * the replay benchmark's layer shape (Qwen2.5-7B target heads, T = 8192,
@@ -90,6 +90,10 @@ ATTN = [  # B, T, H_q, H_kv, D, S, kv_layout
     (1, 260, 28, 4, 128, 128, 1),     # Qwen2.5-7B heads (7 per KV head)
     (2, 150, 4, 4, 64, 32, 0),        # one query head per KV head, 2 of 4 waves without key blocks
     (1, 300, 12, 2, 64, 128, 1),      # Qwen2.5-1.5B heads
+    # sets above 128 keys: the larger register-array instantiations
+    (1, 280, 14, 2, 128, 192, 0),     # the largest S at D = 128
+    (1, 230, 7, 1, 128, 160, 0),      # 10 key blocks: waves with 3 and with 2
+    (1, 270, 8, 4, 64, 256, 1),       # the largest S at D = 64
 ]
 
 
