@@ -223,7 +223,8 @@ mot_status mot_restore_kv(const void* act, const int32_t* layer_map, const void*
  *
  *   B, T       batch rows, context tokens
  *   H_q, H_kv  target query heads and KV heads (H_q a multiple of H_kv; query
- *              head h reads KV head h / (H_q / H_kv), at most 16 per KV head)
+ *              head h reads KV head h / (H_q / H_kv), at most 16 per KV head;
+ *              H_kv * D below 2^20)
  *   D          head dim: 64 or 128
  *   S          Top-S budget: a multiple of 32, 32 .. 256 (at most 192 when
  *              D = 128); the paper uses 128
