@@ -256,7 +256,11 @@ mot_status mot_topS_select(const float* A, int32_t* idx, const mot_replay_shapes
  * set 0..u when idx is NULL.  q, o: device bf16 [B][T][H_q][D]; k, v: device
  * bf16 in kv_layout; idx: device int32 [B][T][S] or NULL.  Softmax and
  * accumulation in fp32; o rounded to bf16.  All pointers 16-byte aligned; o
- * must not overlap an input.
+ * must not overlap an input.  With idx NULL the call stages V transposed
+ * (B * H_kv * D * T rounded up to 64, bf16) in the per-device buffer that
+ * mot_translate uses without a workspace, so such calls and those of
+ * mot_translate or mot_backbone_translate that overlap in time on one device
+ * race.
  */
 mot_status mot_replay_attention(const void* q, const void* k, const void* v, const int32_t* idx, void* o,
                                 const mot_replay_shapes* shapes, hipStream_t stream);

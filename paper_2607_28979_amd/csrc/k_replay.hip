@@ -362,6 +362,34 @@ __global__ __launch_bounds__(256) void k_sparse_attn(ReplayProblem p) {
     }
 }
 
+// V transposed for the causal kernel: vt[b][kvh][d][t] (t < replay_tpad(T),
+// zero past T).  grid (replay_tpad(T) / 64, H_kv, B), 256 threads: one
+// 64-key chunk through LDS (rows padded by 8 elements against bank conflicts).
+template <int D>
+__global__ __launch_bounds__(256) void k_transpose_v(ReplayProblem p) {
+    constexpr int DC = D / 8;
+    __shared__ __align__(16) uint16_t tl[64][D + 8];
+    const int t0 = blockIdx.x * 64, kvh = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+    const uint16_t* V = reinterpret_cast<const uint16_t*>(p.v);
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    for (int it = tid; it < 64 * DC; it += 256) {
+        const int kr = it / DC, c = it % DC, t = t0 + kr;
+        const u32x4 x = t < p.T ? *reinterpret_cast<const u32x4*>(V + kv_row(p, b, t, kvh) + 8 * c) : zero;
+        *reinterpret_cast<u32x4*>(&tl[kr][8 * c]) = x;
+    }
+    __syncthreads();
+    const int64_t tpad = replay_tpad(p.T);
+    uint16_t* out = p.vt + ((size_t)b * p.H_kv + kvh) * D * tpad + t0;
+    for (int it = tid; it < D * 8; it += 256) {
+        const int d = it >> 3, c = it & 7;
+        u32x4 w;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            w[j] = (uint32_t)tl[8 * c + 2 * j][d] | ((uint32_t)tl[8 * c + 2 * j + 1][d] << 16);
+        *reinterpret_cast<u32x4*>(out + (size_t)d * tpad + 8 * c) = w;
+    }
+}
+
 // grid xcd_grid(npairs * H_q * B) with npairs = ceil(ceil(T/64) / 2), items
 // ordered (pair, head, batch row) pair fastest; 256 threads: query positions
 // u0 + 16w + l16 of head hq for two query tiles (a short and a long one);
@@ -389,7 +417,6 @@ __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
     const int u = u0 + 16 * w + l16;       // this lane's query column
     const uint16_t* Q = reinterpret_cast<const uint16_t*>(p.q);
     const uint16_t* K = reinterpret_cast<const uint16_t*>(p.k);
-    const uint16_t* V = reinterpret_cast<const uint16_t*>(p.v);
     uint16_t* O = reinterpret_cast<uint16_t*>(p.o);
     const float sl2 = kLog2e / sqrtf((float)D);
     const u32x4 zero = {0u, 0u, 0u, 0u};
@@ -403,10 +430,13 @@ __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
     for (int db = 0; db < D / 16; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
     float m = -INFINITY, l = 0.f;
     const int last = (u0 + 63 < p.T ? u0 + 63 : p.T - 1);
-    // the next chunk's K and V rows are fetched into registers while the
-    // current one is computed: K items (key, d chunk), V items (key pair, d chunk)
-    constexpr int NKI = 64 * DC / 256, NVI = 32 * DC / 256;
-    u32x4 kreg[NKI], va[NVI], vb[NVI];
+    // the next chunk's K rows and V^T rows are fetched into registers while
+    // the current one is computed: K items (key, d chunk), V^T items (d, 8-key
+    // chunk) from the transposed copy, whose keys past T are zero
+    constexpr int NKI = 64 * DC / 256, NVI = D * 8 / 256;
+    u32x4 kreg[NKI], vreg[NVI];
+    const int64_t tpad = replay_tpad(p.T);
+    const uint16_t* VT = p.vt + ((size_t)b * p.H_kv + kvh) * D * tpad;
     // key t of this batch row and KV head sits at row0 + t * ts in either
     // layout; per chunk the base is scalar and each item adds a 32-bit offset
     // (H_kv * D < 2^20 is checked on the host)
@@ -414,7 +444,6 @@ __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
     const size_t row0 = kv_row(p, b, 0, kvh);
     auto fetch = [&](int kc0) {
         const uint16_t* Kc = K + row0 + (size_t)kc0 * ts;
-        const uint16_t* Vc = V + row0 + (size_t)kc0 * ts;
 #pragma unroll
         for (int i = 0; i < NKI; ++i) {
             const int it = tid + 256 * i, kr = it / DC, c = it % DC;
@@ -422,10 +451,8 @@ __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
         }
 #pragma unroll
         for (int i = 0; i < NVI; ++i) {
-            const int it = tid + 256 * i, c = it / 32, kr = 2 * (it % 32);
-            va[i] = kc0 + kr < p.T ? *reinterpret_cast<const u32x4*>(Vc + ((uint32_t)kr * ts + 8 * c)) : zero;
-            vb[i] = kc0 + kr + 1 < p.T ? *reinterpret_cast<const u32x4*>(Vc + ((uint32_t)(kr + 1) * ts + 8 * c))
-                                       : zero;
+            const int it = tid + 256 * i, d = it >> 3, c = it & 7;
+            vreg[i] = *reinterpret_cast<const u32x4*>(VT + (size_t)d * tpad + kc0 + 8 * c);
         }
     };
     fetch(0);
@@ -436,15 +463,10 @@ __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
             const int it = tid + 256 * i, kr = it / DC, c = it % DC;
             Kl[kr * DC + (c ^ (kr & KSW))] = kreg[i];
         }
-        uint32_t* Vw = reinterpret_cast<uint32_t*>(Vt);
 #pragma unroll
         for (int i = 0; i < NVI; ++i) {
-            const int it = tid + 256 * i, c = it / 32, k0 = 2 * (it % 32);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int d = 8 * c + e;
-                Vw[(d * 8 + ((k0 >> 3) ^ (d & 7))) * 4 + ((k0 & 7) >> 1)] = pair_word(va[i], vb[i], e);
-            }
+            const int it = tid + 256 * i, d = it >> 3, c = it & 7;
+            Vt[d * 8 + (c ^ (d & 7))] = vreg[i];
         }
         __syncthreads();
         if (kc0 + 64 <= last) fetch(kc0 + 64);
@@ -562,6 +584,10 @@ hipError_t launch_replay_attention(const ReplayProblem& p, hipStream_t stream) {
             else hipLaunchKernelGGL((k_sparse_attn<64, 256>), grid, dim3(256), lds, stream, p);
         }
     } else {
+        if (!p.vt) return hipErrorInvalidValue;
+        const dim3 tgrid((unsigned)(replay_tpad(p.T) / 64), p.H_kv, p.B);
+        if (p.D == 128) hipLaunchKernelGGL(k_transpose_v<128>, tgrid, dim3(256), 0, stream, p);
+        else hipLaunchKernelGGL(k_transpose_v<64>, tgrid, dim3(256), 0, stream, p);
         const int npairs = ((p.T + 63) / 64 + 1) / 2;
         const dim3 grid(xcd_grid(npairs * p.H_q * p.B));
         if (p.D == 128) hipLaunchKernelGGL(k_causal_attn<128>, grid, dim3(256), 0, stream, p);

@@ -489,9 +489,15 @@ mot_status mot_replay_attention(const void* q, const void* k, const void* v, con
         (idx && overlaps(o, qo, idx, (size_t)s->B * s->T * s->S * 4)))
         return fail(MOT_ERR_BAD_SHAPE, "o overlaps an input");
     ReplayProblem p;
-    p.q = q; p.k = k; p.v = v; p.idx = idx; p.o = o;
+    p.q = q; p.k = k; p.v = v; p.idx = idx; p.o = o; p.vt = nullptr;
     p.B = s->B; p.T = s->T; p.H_q = s->H_q; p.H_kv = s->H_kv; p.D = s->D; p.S = idx ? s->S : 0;
     p.kv_layout = s->kv_layout;
+    if (!idx) {   // the full causal path stages V transposed through the library's buffer
+        void* ws = nullptr;
+        st = owned_workspace(replay_vt_bytes(s->B, s->T, s->H_kv, s->D), &ws);
+        if (st != MOT_OK) return st;
+        p.vt = reinterpret_cast<uint16_t*>(ws);
+    }
     hipError_t e = launch_replay_attention(p, stream);
     if (e != hipSuccess) return fail(MOT_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
     return MOT_OK;
@@ -558,6 +564,8 @@ mot_status mot_backbone_translate(const void* src_k, const void* src_v, const in
     constexpr int NB = sizeof(row_b) / sizeof(row_b[0]);
     size_t need = gates_b, at[NB];
     for (int k = 0; k < NB; ++k) { at[k] = need; need += round_up(n * row_b[k], kAlign); }
+    const size_t at_vt = need;   // V transposed for the attention
+    need += round_up(replay_vt_bytes(s->B, s->T, nh, d_h / nh), kAlign);
     void* ws = nullptr;
     st = owned_workspace(need, &ws);
     if (st != MOT_OK) return st;
@@ -576,6 +584,7 @@ mot_status mot_backbone_translate(const void* src_k, const void* src_v, const in
     uint16_t* h2 = reinterpret_cast<uint16_t*>(w8 + at[11]);
     uint16_t* on = reinterpret_cast<uint16_t*>(w8 + at[12]);
     float* mix = reinterpret_cast<float*>(w8 + at[13]);
+    uint16_t* vt = reinterpret_cast<uint16_t*>(w8 + at_vt);
 
     p.src[0] = src_k; p.src[1] = src_v; p.wr = rw->w; p.br = rw->b;
     p.gates = reinterpret_cast<float*>(ws);
@@ -640,7 +649,7 @@ mot_status mot_backbone_translate(const void* src_k, const void* src_v, const in
             }
             if (e == hipSuccess) {
                 ReplayProblem rp;
-                rp.q = Q; rp.k = K; rp.v = V; rp.idx = nullptr; rp.o = att;
+                rp.q = Q; rp.k = K; rp.v = V; rp.idx = nullptr; rp.o = att; rp.vt = vt;
                 rp.B = s->B; rp.T = s->T; rp.H_q = nh; rp.H_kv = nh; rp.D = d_h / nh; rp.S = 0;
                 rp.kv_layout = MOT_LAYOUT_BTHD;
                 e = launch_replay_attention(rp, stream);

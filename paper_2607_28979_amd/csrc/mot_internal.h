@@ -82,8 +82,15 @@ struct ReplayProblem {
     const void* v;
     const int32_t* idx;   // [B][T][S] key sets, -1 padded; nullptr = full causal
     void* o;              // bf16 [B][T][H_q][D]
+    // full causal path only: scratch for V transposed, bf16
+    // [B][H_kv][D][replay_tpad(T)], written by the launch before use
+    uint16_t* vt;
     int32_t B, T, H_q, H_kv, D, S, kv_layout;
 };
+__host__ __device__ inline int64_t replay_tpad(int64_t T) { return (T + 63) / 64 * 64; }
+inline size_t replay_vt_bytes(int B, int T, int H_kv, int D) {
+    return (size_t)B * H_kv * D * (size_t)replay_tpad(T) * 2;
+}
 
 size_t replay_sparse_lds_bytes(int D, int S);
 
