@@ -39,7 +39,7 @@ template <bool CACHE>
 __global__ __launch_bounds__(256) void k_topS_select(const float* A, int32_t* idx, int T, int S) {
     extern __shared__ uint32_t s_key[];
     __shared__ uint32_t hist[256];
-    __shared__ uint32_t s_sel[2];
+    __shared__ uint32_t s_sel[3];
     const int u = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
     const int n = u + 1;
     int32_t* out = idx + ((size_t)b * T + u) * S;
@@ -101,35 +101,41 @@ __global__ __launch_bounds__(256) void k_topS_select(const float* A, int32_t* id
             if (tid == L) {
                 uint32_t cum = suf - c;   // keys in bins above 4L+3
                 int d = 4 * L;
+                uint32_t cnt = h0;
                 const uint32_t hb[4] = {h0, h1, h2, h3};
 #pragma unroll
                 for (int q = 3; q >= 0; --q) {
                     if (cum + hb[q] >= (uint32_t)rem) {
                         d = 4 * L + q;
+                        cnt = hb[q];
                         break;
                     }
                     cum += hb[q];
                 }
                 s_sel[0] = (uint32_t)d;
                 s_sel[1] = cum;
+                s_sel[2] = cnt;
             }
         }
         __syncthreads();
-        const uint32_t d = s_sel[0];
+        const uint32_t d = s_sel[0], cnt = s_sel[2];
         rem -= (int)s_sel[1];
         prefix |= d << shift;
         mask |= 255u << shift;
         __syncthreads();
+        // every key of the boundary bin is taken: the digits below decide nothing
+        if (cnt == (uint32_t)rem) break;
     }
-    // prefix is the S-th largest key; take all larger keys and the first rem
-    // equal ones in position order.  Rows are cut into 64-position chunks
-    // (chunk c: positions 64c + lane, wave c % 4): per-chunk counts of larger
-    // and equal keys, one scan over the chunks, then each chunk writes its
-    // picks at its offset in ballot order.
+    // prefix is the S-th largest key on the resolved digits (k & mask): take
+    // every key larger under the mask and the first rem equal ones in
+    // position order (all of them after an early stop).  Rows are cut into
+    // 64-position chunks (chunk c: positions 64c + lane, wave c % 4):
+    // per-chunk counts of larger and equal keys, one scan over the chunks,
+    // then each chunk writes its picks at its offset in ballot order.
     const int lane = tid & 63, wv = tid >> 6, nch = (n + 63) >> 6;
     for (int c = wv; c < nch; c += 4) {
         const int v = 64 * c + lane;
-        const uint32_t k = v < n ? key_at(v) : 0u;
+        const uint32_t k = v < n ? key_at(v) & mask : 0u;
         const unsigned long long bg = __ballot(v < n && k > prefix), be = __ballot(v < n && k == prefix);
         if (lane == 0) {
             s_gt[c] = __popcll(bg);
@@ -175,7 +181,7 @@ __global__ __launch_bounds__(256) void k_topS_select(const float* A, int32_t* id
     __syncthreads();
     for (int c = wv; c < nch; c += 4) {
         const int v = 64 * c + lane;
-        const uint32_t k = v < n ? key_at(v) : 0u;
+        const uint32_t k = v < n ? key_at(v) & mask : 0u;
         const bool eq = v < n && k == prefix;
         const unsigned long long be = __ballot(eq);
         const int eq_rank = s_eq[c] + __popcll(be & ((1ull << lane) - 1ull));
