@@ -157,14 +157,20 @@ __global__ __launch_bounds__(256) void k_bf16_gemm1(Problem p, UnitTab ut) {
 // ---------------------------------------------------------------------------
 // gemm2: Y[token][out] = Hs[token][:] . W2cat[out][:]  (+ gate-mixed b2)
 //   MFMA A operand = hidden rows (tokens), B operand = W2 rows (outputs).
-// grid: x = token tiles, y = output tiles (d_out / 128, ragged), z = unit
+// grid: x = token tiles, y = output tiles (d_out / 128, ragged), z = unit;
+// the (x, y) workgroup id is remapped so that y varies fastest
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_bf16_gemm2(Problem p, UnitTab ut) {
     __shared__ u32x4 lds[2][2][kChunks];   // [stage][0 = Hs, 1 = W2]
     const uint32_t code = ut.code[blockIdx.z];
     const int j = unit_j(code), x = unit_x(code), gs = unit_gslot(code);
     const int EH = p.E * p.hidden;
-    const int tok0 = blockIdx.x * BM, out0 = blockIdx.y * BN;
+    // output tiles fastest in dispatch order: the workgroups sharing one token
+    // tile's A rows (128 tokens x E*hidden, re-read by every output tile) run
+    // together and find them on chip, instead of A streaming from HBM once per
+    // output tile
+    const int lin = blockIdx.x + gridDim.x * blockIdx.y;
+    const int tok0 = (lin / gridDim.y) * BM, out0 = (lin % gridDim.y) * BN;
     const size_t unit = (size_t)j * p.streams + x;
     const uint16_t* W2 = reinterpret_cast<const uint16_t*>(p.w2) + unit * p.E * p.d_out * p.hidden;
     const uint16_t* H = reinterpret_cast<const uint16_t*>(p.hbuf) + (size_t)blockIdx.z * p.n_tok_pad * EH;
