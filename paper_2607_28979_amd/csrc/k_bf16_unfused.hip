@@ -49,14 +49,20 @@ __device__ __forceinline__ size_t dst_offset(const Problem& p, int j, int tok, i
 // gemm1: S^T[hidden][token] = W1[hidden][:] . Z[token][:]
 //   MFMA A operand = W1 rows (hidden), B operand = source rows (tokens), so
 //   each lane ends with 4 consecutive hidden values of one token per group.
-// grid: x = token tiles, y = hidden tiles (E*hidden / 128), z = unit
+// grid: x = token tiles, y = hidden tiles (E*hidden / 128), z = unit; the
+// (x, y) workgroup id is remapped to a grouped order (below)
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_bf16_gemm1(Problem p, UnitTab ut) {
     __shared__ u32x4 lds[2][2][kChunks];   // [stage][0 = W1, 1 = Z]
     const uint32_t code = ut.code[blockIdx.z];
     const int j = unit_j(code), x = unit_x(code), i = unit_i(code), gs = unit_gslot(code);
     const int EH = p.E * p.hidden;
-    const int tok0 = blockIdx.x * BN, hid0 = blockIdx.y * BM;
+    // grouped dispatch order as in gemm2: 8 token tiles inner, hidden tiles
+    // outer, so each XCD keeps one token tile's source rows in its L2 and a W1
+    // tile is fetched once per group
+    const int lin = blockIdx.x + gridDim.x * blockIdx.y, ny = gridDim.y;
+    const int grp = lin / (8 * ny), gsz = min(8, (int)gridDim.x - 8 * grp), r = lin - grp * 8 * ny;
+    const int tok0 = (8 * grp + r % gsz) * BN, hid0 = (r / gsz) * BM;
     const size_t unit = (size_t)j * p.streams + x;
     const uint16_t* W1 = reinterpret_cast<const uint16_t*>(p.w1) + unit * EH * p.d_in;
     const uint16_t* src = reinterpret_cast<const uint16_t*>(p.src[x]);
@@ -158,19 +164,21 @@ __global__ __launch_bounds__(256) void k_bf16_gemm1(Problem p, UnitTab ut) {
 // gemm2: Y[token][out] = Hs[token][:] . W2cat[out][:]  (+ gate-mixed b2)
 //   MFMA A operand = hidden rows (tokens), B operand = W2 rows (outputs).
 // grid: x = token tiles, y = output tiles (d_out / 128, ragged), z = unit;
-// the (x, y) workgroup id is remapped so that y varies fastest
+// the (x, y) workgroup id is remapped to a grouped order (below)
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_bf16_gemm2(Problem p, UnitTab ut) {
     __shared__ u32x4 lds[2][2][kChunks];   // [stage][0 = Hs, 1 = W2]
     const uint32_t code = ut.code[blockIdx.z];
     const int j = unit_j(code), x = unit_x(code), gs = unit_gslot(code);
     const int EH = p.E * p.hidden;
-    // output tiles fastest in dispatch order: the workgroups sharing one token
-    // tile's A rows (128 tokens x E*hidden, re-read by every output tile) run
-    // together and find them on chip, instead of A streaming from HBM once per
-    // output tile
-    const int lin = blockIdx.x + gridDim.x * blockIdx.y;
-    const int tok0 = (lin / gridDim.y) * BM, out0 = (lin % gridDim.y) * BN;
+    // dispatch order in groups of 8 token tiles: output tiles outer, the
+    // group's token tiles inner.  Workgroups are dealt round-robin to the 8
+    // XCDs, so each XCD keeps one token tile (its A rows, re-read by every
+    // output tile) in its L2, and a W2 tile is fetched once per group instead
+    // of once per token tile.
+    const int lin = blockIdx.x + gridDim.x * blockIdx.y, ny = gridDim.y;
+    const int grp = lin / (8 * ny), gsz = min(8, (int)gridDim.x - 8 * grp), r = lin - grp * 8 * ny;
+    const int tok0 = (8 * grp + r % gsz) * BM, out0 = (r / gsz) * BN;
     const size_t unit = (size_t)j * p.streams + x;
     const uint16_t* W2 = reinterpret_cast<const uint16_t*>(p.w2) + unit * p.E * p.d_out * p.hidden;
     const uint16_t* H = reinterpret_cast<const uint16_t*>(p.hbuf) + (size_t)blockIdx.z * p.n_tok_pad * EH;
