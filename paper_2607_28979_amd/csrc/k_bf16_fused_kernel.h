@@ -410,7 +410,7 @@ void k_bf16_fused(Problem p, UnitTab ut) {
             const float hg0 = 0.5f * Gw[m * 32 + l16], hg1 = 0.5f * Gw[m * 32 + 16 + l16];
             if constexpr (do_l1) load_b1(c_next, bnext);
             u32x4 a1[KS2][2];
-            float h[2][2][4], gx[16], gt[16], gx2[16], gq[16], ge[16];
+            float h[2][2][4], gx[16], gt[16], gq[16];
             // A operand of (k-step s, row half hh), first used in slot 4s + 2hh
             auto read_a = [&](auto kc) {
                 constexpr int k = decltype(kc)::value;
@@ -425,11 +425,11 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                 if constexpr (ACT == MOT_ACT_GELU) {
                     if constexpr (st == 0) {
                         gx[e] = sp[hh][th][jj];
-                        gelu_stage1(gx[e], gt[e], gx2[e]);
+                        gelu_stage1(gx[e], gt[e]);
                     } else if constexpr (st == 1) {
-                        gelu_stage2(gt[e], gx2[e], gq[e], ge[e]);
+                        gelu_stage2(gt[e], gq[e]);
                     } else {
-                        h[hh][th][jj] = gelu_stage3(gx[e], gt[e], gq[e], ge[e], th ? hg1 : hg0);
+                        h[hh][th][jj] = gelu_stage3(gx[e], gq[e], th ? hg1 : hg0);
                     }
                 } else if constexpr (st == 0) {
                     h[hh][th][jj] = 2.0f * (th ? hg1 : hg0) * sp[hh][th][jj];
@@ -500,13 +500,13 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                                 float v = sp[hh][th][jj];
                                 asm volatile("" : "+v"(v));
                                 gx[e] = v;
-                                gelu_stage1(v, gt[e], gx2[e]);
-                                asm volatile("" : "+v"(gt[e]), "+v"(gx2[e]));
+                                gelu_stage1(v, gt[e]);
+                                asm volatile("" : "+v"(gt[e]));
                             } else if constexpr (k == g0 + GD) {
-                                gelu_stage2(gt[e], gx2[e], gq[e], ge[e]);
-                                asm volatile("" : "+v"(gq[e]), "+v"(ge[e]));
+                                gelu_stage2(gt[e], gq[e]);
+                                asm volatile("" : "+v"(gq[e]));
                             } else if constexpr (k == g0 + 2 * GD) {
-                                h[hh][th][jj] = gelu_stage3(gx[e], gt[e], gq[e], ge[e], th ? hg1 : hg0);
+                                h[hh][th][jj] = gelu_stage3(gx[e], gq[e], th ? hg1 : hg0);
                             }
                         } else if constexpr (k == g0) {
                             float v = sp[hh][th][jj];

@@ -126,37 +126,29 @@ __device__ __forceinline__ float gelu_fast(float x) {
     return 0.5f * x * (1.0f + erf_v);
 }
 
-// g * GELU(x) with hg = g / 2, for the fused bf16 kernel: erf from
-// Abramowitz & Stegun formula 7.1.25 (|error of erf| <= 2.5e-5, two orders
-// below the bf16 rounding the result gets next):
-//   erf(y) = 1 - (a1 t + a2 t^2 + a3 t^3) exp(-y^2),  t = 1 / (1 + p y),  y >= 0;
-// then hg*x*(1 + erf(x / sqrt 2)) = hx + hx*erf with hx = hg*x.
+// g * GELU(x) with hg = g / 2, for the fused bf16 kernel, in the tanh form
+// of GELU (Hendrycks & Gimpel): GELU(x) ~ x * sigmoid(2u),
+// u = sqrt(2/pi) * (x + 0.044715 x^3).  Its largest deviation from the erf
+// form is 4.7e-4 (at x ~ 2.7, 1.8e-4 relative), an order below the bf16
+// rounding the result gets next.  With e = 2^(x * (K1 + K3 x^2)) =
+// exp(-2u):  g * GELU(x) = hg * x * 2 / (1 + e).
+#define MOT_GELU_K1 (-2.3022082f)      // -2 sqrt(2/pi) log2(e)
+#define MOT_GELU_K3 (-0.10294324f)     // K1 * 0.044715
 __device__ __forceinline__ float gelu_half_scaled(float x, float hg) {
-    const float y = fabsf(x) * 0.70710678118654752f;
-    const float t = __builtin_amdgcn_rcpf(fmaf(0.47047f, y, 1.0f));
-    const float poly = fmaf(fmaf(0.7478556f, t, -0.0958798f), t, 0.3480242f) * t;
-    // exp(-y^2) = 2^(-x^2 * log2(e) / 2)
-    const float e = __builtin_amdgcn_exp2f((x * x) * -0.72134752044448170f);
-    const float erf_v = copysignf(fmaf(-poly, e, 1.0f), x);
-    const float hx = hg * x;
-    return fmaf(hx, erf_v, hx);
+    const float e = __builtin_amdgcn_exp2f(x * fmaf(x * x, MOT_GELU_K3, MOT_GELU_K1));
+    return (hg * x) * __builtin_amdgcn_rcpf(fmaf(e, 0.5f, 0.5f));
 }
 
 // The same function as gelu_half_scaled, split into three dependent stages
 // so a software pipeline can overlap the chains of several elements.
-__device__ __forceinline__ void gelu_stage1(float x, float& t, float& x2) {
-    // 1 + p*|x|/sqrt(2), folded into one fused multiply-add
-    t = __builtin_amdgcn_rcpf(fmaf(0.47047f * 0.70710678118654752f, fabsf(x), 1.0f));
-    x2 = x * x;
+__device__ __forceinline__ void gelu_stage1(float x, float& e) {
+    e = __builtin_amdgcn_exp2f(x * fmaf(x * x, MOT_GELU_K3, MOT_GELU_K1));
 }
-__device__ __forceinline__ void gelu_stage2(float t, float x2, float& q, float& e) {
-    q = fmaf(fmaf(0.7478556f, t, -0.0958798f), t, 0.3480242f);
-    e = __builtin_amdgcn_exp2f(x2 * -0.72134752044448170f);
+__device__ __forceinline__ void gelu_stage2(float e, float& r) {
+    r = __builtin_amdgcn_rcpf(fmaf(e, 0.5f, 0.5f));   // 2 / (1 + e)
 }
-__device__ __forceinline__ float gelu_stage3(float x, float t, float q, float e, float hg) {
-    const float erf_v = copysignf(fmaf(-(q * t), e, 1.0f), x);
-    const float hx = hg * x;
-    return fmaf(hx, erf_v, hx);
+__device__ __forceinline__ float gelu_stage3(float x, float r, float hg) {
+    return (hg * x) * r;
 }
 
 }  // namespace mot
