@@ -46,6 +46,10 @@ typedef __attribute__((address_space(3))) void lds_void;
 #ifndef MOT_FUSED_PHASE_A
 #define MOT_FUSED_PHASE_A 6
 #endif
+// The same count for the 12-wave form (two layer-2 waves per SIMD)
+#ifndef MOT_FUSED_PHASE_A12
+#define MOT_FUSED_PHASE_A12 14
+#endif
 #ifndef MOT_FUSED_A_LAST
 #define MOT_FUSED_A_LAST 0
 #endif
@@ -65,11 +69,11 @@ typedef __attribute__((address_space(3))) void lds_void;
 #ifndef MOT_FUSED_OFFLOAD
 #define MOT_FUSED_OFFLOAD 4
 #endif
-// Split iteration (12-wave form): the layer-1 waves evaluate all their GELU
-// elements while the layer-2 waves run their MFMAs, then, after a
-// mid-iteration barrier, the layer-1 waves run their MFMAs alone
+// Split iteration (12-wave form, off by default): the layer-1 waves evaluate
+// all their GELU elements while the layer-2 waves run their MFMAs, then,
+// after a mid-iteration barrier, the layer-1 waves run their MFMAs alone
 #ifndef MOT_FUSED_SPLIT
-#define MOT_FUSED_SPLIT 1
+#define MOT_FUSED_SPLIT 0
 #endif
 
 template <int D_IN, int D_OUT>
@@ -397,7 +401,8 @@ void k_bf16_fused(Problem p, UnitTab ut) {
         // with the three-stage GELU of the other elements spread
         // over the slots (stage s of element e in slot g0(e) + s*GD); W1
         // operand reads run LOOK slots ahead.
-        constexpr int NEA = MOT_FUSED_PHASE_A;
+        constexpr int NEA0 = C::L2W == 8 ? MOT_FUSED_PHASE_A12 : MOT_FUSED_PHASE_A;
+        constexpr int NEA = NEA0 < 16 - C::NOFF ? NEA0 : 16 - C::NOFF;
         auto l1_iter = [&](auto l1c, auto gc, int c, int m, const u32x4& bv,
                            const f32x4 (&sp)[2][2], u32x4& bnext, int c_next,
                            f32x4 (&s)[2][2]) {
