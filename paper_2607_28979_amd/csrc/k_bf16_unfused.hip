@@ -150,7 +150,7 @@ __global__ __launch_bounds__(256) void k_bf16_gemm1(Problem p, UnitTab ut) {
                 for (int jj = 0; jj < 4; ++jj) {
                     const int hr = hbase + 8 * ii + 4 * g + jj;
                     float a = acc[bm][bn][4 * ii + jj] + (b1 ? bf16_to_f32(b1[hr]) : 0.f);
-                    a = p.act == MOT_ACT_GELU ? gelu_fast(a) : a;
+                    a = p.act == MOT_ACT_GELU ? gelu_tanh(a) : a;
                     v[jj] = gate * a;
                 }
                 u32x2 w = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};

@@ -140,6 +140,13 @@ __device__ __forceinline__ float gelu_half_scaled(float x, float hg) {
     return (hg * x) * __builtin_amdgcn_rcpf(fmaf(e, 0.5f, 0.5f));
 }
 
+// GELU(x) in the same tanh form, x / (1 + e), for the two-GEMM bf16 path's
+// layer-1 epilogue.
+__device__ __forceinline__ float gelu_tanh(float x) {
+    const float e = __builtin_amdgcn_exp2f(x * fmaf(x * x, MOT_GELU_K3, MOT_GELU_K1));
+    return x * __builtin_amdgcn_rcpf(1.0f + e);
+}
+
 // The same function as gelu_half_scaled, split into three dependent stages
 // so a software pipeline can overlap the chains of several elements.
 __device__ __forceinline__ void gelu_stage1(float x, float& e) {

@@ -1,7 +1,8 @@
-"""CPU checks of the GELU form the fused bf16 kernel evaluates.
+"""CPU checks of the GELU form the bf16 translation kernels evaluate.
 
-The kernel computes g * GELU(x) as g * x / (1 + 2^(x (K1 + K3 x^2))), the tanh
-form of GELU written as a logistic, with K1 and K3 defined in the device
+The fused kernel computes g * GELU(x) as g * x / (1 + 2^(x (K1 + K3 x^2))), the tanh
+form of GELU written as a logistic (the two-GEMM path's epilogue x / (1 + 2^(...)),
+the same form without the gate), with K1 and K3 defined in the device
 header.  These tests read those two constants from the source and check, in
 float64, that they are the tanh form's (K1 = -2 sqrt(2/pi) log2 e,
 K3 = 0.044715 K1), that the form stays within 4.7e-4 of the exact erf GELU
