@@ -283,7 +283,7 @@ __global__ __launch_bounds__(256) void k_linear(LinearProblem p) {
                 for (int jj = 0; jj < 4; ++jj) {
                     const float bj = (jj & 1) ? bf16_hi(bw[bm][ii][jj >> 1]) : bf16_lo(bw[bm][ii][jj >> 1]);
                     const float x = acc[bm][bn][4 * ii + jj] + bj;
-                    v[jj] = p.gelu ? gelu_fast(x) : x;
+                    v[jj] = p.gelu ? gelu_tanh(x) : x;
                 }
                 stg[tl * 32 + (c ^ (tl & 31))] = v;
             }

@@ -107,25 +107,6 @@ __device__ __forceinline__ float gelu_erf(float x) {
     return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
 }
 
-// GELU for the bf16 path: x * Phi(x) with erf from Abramowitz & Stegun
-// formula 7.1.26 (|error of erf| <= 1.5e-7, far below bf16 resolution):
-//   erf(y) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-y^2),
-//   t = 1 / (1 + p y), y >= 0, erf odd.
-__device__ __forceinline__ float gelu_fast(float x) {
-    const float y = fabsf(x) * 0.70710678118654752f;
-    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, y, 1.0f));
-    float poly = fmaf(1.061405429f, t, -1.453152027f);
-    poly = fmaf(poly, t, 1.421413741f);
-    poly = fmaf(poly, t, -0.284496736f);
-    poly = fmaf(poly, t, 0.254829592f);
-    poly *= t;
-    // exp(-y^2) = 2^(-y^2 * log2(e))
-    const float e = __builtin_amdgcn_exp2f(-(y * y) * 1.44269504088896341f);
-    const float erf_abs = fmaf(-poly, e, 1.0f);
-    const float erf_v = copysignf(erf_abs, x);
-    return 0.5f * x * (1.0f + erf_v);
-}
-
 // g * GELU(x) with hg = g / 2, for the fused bf16 kernel, in the tanh form
 // of GELU (Hendrycks & Gimpel): GELU(x) ~ x * sigmoid(2u),
 // u = sqrt(2/pi) * (x + 0.044715 x^3).  Its largest deviation from the erf
@@ -141,7 +122,7 @@ __device__ __forceinline__ float gelu_half_scaled(float x, float hg) {
 }
 
 // GELU(x) in the same tanh form, x / (1 + e), for the two-GEMM bf16 path's
-// layer-1 epilogue.
+// layer-1 epilogue and the backbone experts' linear epilogue.
 __device__ __forceinline__ float gelu_tanh(float x) {
     const float e = __builtin_amdgcn_exp2f(x * fmaf(x * x, MOT_GELU_K3, MOT_GELU_K1));
     return x * __builtin_amdgcn_rcpf(1.0f + e);
