@@ -54,6 +54,25 @@ def measured_traffic(kernel_file: str, workload_tag: str):
         return None
 
 
+def host_cpu() -> dict:
+    """The host the CPU baseline ran on: its logical CPU count and model
+    name.  The oracle uses at most 16 of those threads, the CPU share a
+    single-GPU job gets on these machines."""
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"host_cpus": os.cpu_count() or 1, "cpu_model": model}
+
+
+def oracle_threads() -> int:
+    return min(16, os.cpu_count() or 1)
+
+
 def calibration_copy(mib: int) -> None:
     """One plain device copy of `mib` MiB: a known-size reference for the HBM
     byte counters of a profiler run."""
@@ -228,7 +247,7 @@ def cpu_baseline(w, inp, lm, rows):
     """The CPU oracle, untuned, on a bounded sample: every unit for the first
     `rows` tokens (each token translated through all layers, K and V)."""
     from oracle import OracleDims, oracle_rows
-    threads = min(16, os.cpu_count() or 1)
+    threads = oracle_threads()
     od = OracleDims(L_src=w.L_src, L_tgt=w.L_tgt, B=w.B, T=w.T, H_src=w.H_src, D_src=w.D_src,
                     H_tgt=w.H_tgt, D_tgt=w.D_tgt, E=w.E, hidden=w.hidden, top_k=w.top_k)
     units = [(j, x) for j in range(w.L_tgt) if lm[j] >= 0 for x in (0, 1)]
@@ -242,7 +261,7 @@ def cpu_baseline(w, inp, lm, rows):
                 units=units, rows=sample, nthreads=threads)
     dt = time.perf_counter() - t0
     log("cpu oracle: %d rows x %d units in %.2f s on %d threads" % (rows, len(units), dt, threads))
-    return {"value": round(rows / dt, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+    return {"value": round(rows / dt, 3), "unit": "tokens/s", "cores": threads, **host_cpu(), "kind": "oracle",
             "sample": "first %d of %d tokens, all %d units (K and V of every layer), fp64"
                       % (rows, w.n_tok, len(units)),
             "seconds": round(dt, 2)}
@@ -348,7 +367,7 @@ def cpu_baseline_moth(w, inp, lm, proj, rows):
     the activation stream, then the key/value restoration of those rows."""
     from oracle import OracleDims, oracle_restore_kv, oracle_rows
     wk, bk, wv, bv = proj
-    threads = min(16, os.cpu_count() or 1)
+    threads = oracle_threads()
     od = OracleDims(L_src=w.L_src, L_tgt=w.L_tgt, B=w.B, T=w.T, H_src=w.H_src, D_src=w.D_src,
                     H_tgt=w.H_tgt, D_tgt=w.D_tgt, E=w.E, hidden=w.hidden, top_k=w.top_k,
                     streams=1)
@@ -363,7 +382,7 @@ def cpu_baseline_moth(w, inp, lm, proj, rows):
                       H_tgt=MOTH.kv_heads, D_tgt=MOTH.head_dim)
     dt = time.perf_counter() - t0
     log("cpu oracle: %d rows x %d layers in %.2f s on %d threads" % (rows, len(units), dt, threads))
-    return {"value": round(rows / dt, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+    return {"value": round(rows / dt, 3), "unit": "tokens/s", "cores": threads, **host_cpu(), "kind": "oracle",
             "sample": "first %d of %d tokens, all %d layers (translation + K/V restoration), fp64"
                       % (rows, w.n_tok, len(units)),
             "seconds": round(dt, 2)}
@@ -516,7 +535,7 @@ def cpu_baseline_replay(w, rows):
         oracle_replay_attention_rows(q, k, v, idx, sample)
         dt += time.perf_counter() - t0
     log("cpu oracle: %d positions x %d layers in %.2f s (1 thread)" % (rows, w.L_tgt, dt))
-    return {"value": round(rows / dt, 3), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+    return {"value": round(rows / dt, 3), "unit": "tokens/s", "cores": 1, **host_cpu(), "kind": "oracle",
             "sample": "first %d of %d query positions, all %d target layers (selection + attention), fp64"
                       % (rows, w.T, w.L_tgt), "seconds": round(dt, 2)}
 

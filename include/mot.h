@@ -15,11 +15,15 @@
  *
  *       g      = softmax(Wr z + br)                   (E nonnegative gates)
  *       Tr_m z = W2_m GELU(W1_m z + b1_m) + b2_m     (m = 0..E-1)
- *       out    = sum_m g_m Tr_m z                     (all E translators:
- *                                                      Top-K with K = E)
+ *       S      = the top_k largest g_m (ties: lower index), 1 <= top_k <= E
+ *       out    = sum_{m in S} (g_m / sum_{r in S} g_r) Tr_m z
  *
  *   and written into target layer j, un-flattened as (h', d') =
- *   (o / D_tgt, o % D_tgt).  GELU is the exact-erf GELU, x * Phi(x).
+ *   (o / D_tgt, o % D_tgt).  top_k = E is the dense mixture.  GELU is
+ *   x * Phi(x) with the exact erf in MOT_F32; every MOT_BF16 kernel evaluates
+ *   the tanh form of GELU (Hendrycks & Gimpel), whose largest deviation from
+ *   the erf form is 4.7e-4 absolute (at |x| ~ 2.7), well below the bf16
+ *   rounding of the hidden activation that follows it.
  *
  * Terms.  d_in = H_src*D_src, d_out = H_tgt*D_tgt, N_tok = B*T.  A "unit" is
  * one (target layer j, X in {K, V}) with layer_map[j] >= 0.
@@ -65,11 +69,14 @@ typedef enum { MOT_ALGO_AUTO = 0, MOT_ALGO_UNFUSED = 1, MOT_ALGO_FUSED = 2, MOT_
  *   top_k          translators used per token, 1..E: the top_k largest softmax
  *                  scores are kept and renormalised to sum to one, the others
  *                  are zero (ties go to the lower translator index); top_k = E
- *                  is the dense mixture.  The kernels still evaluate every
- *                  translator: unselected ones contribute exactly zero.
+ *                  is the dense mixture.  MOT_ALGO_ROUTED runs each translator
+ *                  only on the tokens that selected it; MOT_ALGO_FUSED and
+ *                  MOT_ALGO_UNFUSED evaluate every translator and give the
+ *                  unselected ones a gate of exactly zero.
  *   hidden         translator hidden width
  *   dtype          MOT_F32: fp32 storage and math (erf GELU, expf softmax).
  *                  MOT_BF16: bf16 storage; fp32 accumulation; fp32 gates;
+ *                  tanh-form GELU (within 4.7e-4 absolute of the erf form);
  *                  the gate-scaled hidden activation is rounded to bf16
  *                  before the second translator layer; outputs rounded to
  *                  nearest even.

@@ -85,9 +85,12 @@ _lib = None
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB):
+        # MOT_ORACLE_LIB: a mutated build of this oracle, used only by the
+        # mutation tests to show that the pins fail on planted mistakes
+        path = os.environ.get("MOT_ORACLE_LIB") or _LIB
+        if path == _LIB and not os.path.exists(_LIB):
             build_oracle(force=False)
-        _lib = ctypes.CDLL(_LIB)
+        _lib = ctypes.CDLL(path)
         _lib.mot_oracle_backbone_param_count.restype = ctypes.c_size_t
         _lib.mot_oracle_backbone_param_count.argtypes = [ctypes.c_int32] * 4
         for fn in (_lib.mot_oracle_translate, _lib.mot_oracle_rows,

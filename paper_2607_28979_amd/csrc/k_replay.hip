@@ -222,7 +222,7 @@ __global__ __launch_bounds__(256) void k_sparse_attn(ReplayProblem p) {
     const int S = p.S, SC = S / 8;          // 16-byte chunks per row of S keys
     // XOR swizzle within aligned groups of the largest power of two (<= 16)
     // dividing SC, so that a permuted chunk stays inside its row
-    const int swm = ((SC & -SC) < 16 ? (SC & -SC) : 16) - 1;
+    const int swm = replay_swizzle_mask(SC);
     u32x4* Vt = s_dyn;                      // row d: SC chunks, chunk c at (c ^ (d & swm))
     u32x4* Pl = s_dyn + D * SC;             // row = query head slot
     float* red = reinterpret_cast<float*>(Pl + 16 * SC);   // [4 waves][16]: max, then sum
@@ -244,8 +244,9 @@ __global__ __launch_bounds__(256) void k_sparse_attn(ReplayProblem p) {
     for (int i = tid; i < S; i += 256) s_keys[i] = keys[i];
     __syncthreads();
     // per-thread item counts for sets of up to SMAX keys
-    constexpr int MAXR = SMAX / 2 * DC / 256;   // V key-pair items
-    constexpr int MAXB = SMAX / 16 / 4;         // key blocks per wave
+    constexpr int MAXR = replay_sparse_v_items(D, SMAX);   // V key-pair items
+    constexpr int MAXB = replay_sparse_key_blocks(SMAX);   // key blocks per wave
+    static_assert(replay_sparse_supported(D, SMAX), "instantiated set size");
 
     for (int kvh = 0; kvh < p.H_kv; ++kvh) {
         // every gather of this KV head is issued before the first is used:
@@ -563,8 +564,6 @@ constexpr int kSelCacheMax = 15872;   // rows up to this length keep their keys 
 
 }  // namespace
 
-size_t replay_sparse_lds_bytes(int D, int S) { return (size_t)(D * S + 16 * S) * 2 + 128 * sizeof(float); }
-
 hipError_t launch_topS_select(const float* A, int32_t* idx, int B, int T, int S, hipStream_t stream) {
     if (B == 0 || T == 0) return hipSuccess;
     const dim3 grid(T, B);
@@ -579,15 +578,20 @@ hipError_t launch_topS_select(const float* A, int32_t* idx, int B, int T, int S,
 hipError_t launch_replay_attention(const ReplayProblem& p, hipStream_t stream) {
     if (p.B == 0 || p.T == 0) return hipSuccess;
     if (p.idx) {
+        // the caller's check admits only these sizes; the register arrays of
+        // the instantiation below cover every admitted S
+        if (!replay_sparse_supported(p.D, p.S)) return hipErrorInvalidValue;
         const dim3 grid(xcd_grid(p.T), p.B);
         const size_t lds = replay_sparse_lds_bytes(p.D, p.S);
         // register arrays sized for S <= 128, or for the largest S the LDS allows
         if (p.D == 128) {
-            if (p.S <= 128) hipLaunchKernelGGL((k_sparse_attn<128, 128>), grid, dim3(256), lds, stream, p);
-            else hipLaunchKernelGGL((k_sparse_attn<128, 192>), grid, dim3(256), lds, stream, p);
+            if (replay_sparse_instance(128, p.S) == 128)
+                hipLaunchKernelGGL((k_sparse_attn<128, 128>), grid, dim3(256), lds, stream, p);
+            else hipLaunchKernelGGL((k_sparse_attn<128, replay_sparse_smax(128)>), grid, dim3(256), lds, stream, p);
         } else {
-            if (p.S <= 128) hipLaunchKernelGGL((k_sparse_attn<64, 128>), grid, dim3(256), lds, stream, p);
-            else hipLaunchKernelGGL((k_sparse_attn<64, 256>), grid, dim3(256), lds, stream, p);
+            if (replay_sparse_instance(64, p.S) == 128)
+                hipLaunchKernelGGL((k_sparse_attn<64, 128>), grid, dim3(256), lds, stream, p);
+            else hipLaunchKernelGGL((k_sparse_attn<64, replay_sparse_smax(64)>), grid, dim3(256), lds, stream, p);
         }
     } else {
         if (!p.vt) return hipErrorInvalidValue;

@@ -451,8 +451,9 @@ mot_status check_replay(const mot_replay_shapes* s, bool need_s) {
         return fail(MOT_ERR_UNSUPPORTED, "H_kv * D = %lld: at most 2^20 - 1", (long long)s->H_kv * s->D);
     if (s->H_q / s->H_kv > 16)
         return fail(MOT_ERR_UNSUPPORTED, "%d query heads per KV head (at most 16)", s->H_q / s->H_kv);
-    if (need_s && (s->S % 32 || s->S > 256 || replay_sparse_lds_bytes(s->D, s->S) > 65536))
-        return fail(MOT_ERR_UNSUPPORTED, "S=%d: need a multiple of 32, at most 256 (192 when D = 128)", s->S);
+    if (need_s && !replay_sparse_supported(s->D, s->S))
+        return fail(MOT_ERR_UNSUPPORTED, "S=%d: need a multiple of 32 from 32 to %d for D = %d", s->S,
+                    replay_sparse_smax(s->D), s->D);
     return MOT_OK;
 }
 }  // namespace

@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "replay_limits.h"
+
 namespace mot {
 
 // Up to 2 * MOT_MAX_LAYERS units can be launched together.
@@ -91,8 +93,6 @@ __host__ __device__ inline int64_t replay_tpad(int64_t T) { return (T + 63) / 64
 inline size_t replay_vt_bytes(int B, int T, int H_kv, int D) {
     return (size_t)B * H_kv * D * (size_t)replay_tpad(T) * 2;
 }
-
-size_t replay_sparse_lds_bytes(int D, int S);
 
 // Generic bf16 linear layer of the backbone translator body.  One launch
 // computes up to three output blocks ("parts") that share the input rows:

@@ -257,6 +257,7 @@ def test_empty_contexts_are_no_ops(lib):
 
 @pytest.mark.parametrize("kw,code", [
     (dict(S=48), "MOT_ERR_UNSUPPORTED"), (dict(S=256), "MOT_ERR_UNSUPPORTED"),    # D = 128: at most 192
+    (dict(S=224), "MOT_ERR_UNSUPPORTED"), (dict(D=64, S=288), "MOT_ERR_UNSUPPORTED"),
     (dict(D=96), "MOT_ERR_UNSUPPORTED"), (dict(H_q=6, H_kv=4), "MOT_ERR_BAD_SHAPE"),
     (dict(H_q=34, H_kv=2), "MOT_ERR_UNSUPPORTED"), (dict(kv_layout=3), "MOT_ERR_BAD_SHAPE"),
     (dict(T=-1), "MOT_ERR_BAD_SHAPE"), (dict(H_q=8192, H_kv=8192), "MOT_ERR_UNSUPPORTED")])
@@ -282,3 +283,66 @@ def test_topS_rejects(lib):
     with pytest.raises(mb.MotError) as e:
         mb._check(mb.load_library().mot_topS_select(FAKE, FAKE + 64, ctypes.byref(c), None))   # idx inside A
     assert e.value.name == "MOT_ERR_BAD_SHAPE"
+
+
+_ENUM_SRC = r"""
+#include <stdio.h>
+#include "replay_limits.h"
+using namespace mot;
+int main() {
+    for (int D = 64; D <= 128; D += 64)
+        for (int S = 1; S <= 320; ++S) {
+            const int sc = S / 8, m = replay_swizzle_mask(sc > 0 ? sc : 1);
+            int perm = S % 8 == 0;                 /* every row: c -> c ^ (d & m) permutes 0..sc-1 */
+            for (int d = 0; perm && d < D; ++d) {
+                unsigned char seen[64] = {0};
+                for (int c = 0; c < sc; ++c) {
+                    const int t = c ^ (d & m);
+                    if (t < 0 || t >= sc || seen[t]) { perm = 0; break; }
+                    seen[t] = 1;
+                }
+            }
+            const int inst = replay_sparse_instance(D, S);
+            const int cover = replay_sparse_v_items(D, inst) * 256 >= (S / 2) * (D / 8) &&
+                              replay_sparse_key_blocks(inst) * 4 >= (S + 15) / 16 && S <= inst;
+            printf("%d %d %d %d %d %d\n", D, S, (int)replay_sparse_supported(D, S), perm, cover,
+                   (int)replay_sparse_lds_bytes(D, S));
+        }
+    return 0;
+}
+"""
+
+
+def test_replay_set_sizes_and_swizzle(lib, tmp_path):
+    """Every (D, S) that mot_replay_attention admits with a key set has (i)
+    an LDS swizzle that permutes the 16-byte chunks inside each row of S keys,
+    (ii) register arrays in the dispatched instantiation that cover all S
+    keys, and (iii) LDS within 64 KB.  The limits are read from the header the
+    kernel and the host check share, compiled here as host-only C++; the
+    admitted set comes from the library itself (the argument check runs
+    before any device access, so NULL buffers give MOT_ERR_NULL_ARG exactly
+    when the sizes are admitted).  Regression: a mask of SC - 1 moved chunks
+    into the neighbouring row for S = 96, 160, 192, 224."""
+    import subprocess
+    src = tmp_path / "enum.cpp"
+    exe = tmp_path / "enum"
+    src.write_text(_ENUM_SRC)
+    subprocess.run(["g++", "-std=c++17", "-O1", "-I", os.path.join(ROOT, "paper_2607_28979_amd", "csrc"),
+                    str(src), "-o", str(exe)], check=True)
+    rows = [tuple(int(v) for v in l.split()) for l in
+            subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n") if l.strip()]
+    admitted = set()
+    for D, S, supported, perm, cover, lds in rows:
+        c = mb._ReplayShapes(1, 4, 2, 1, D, S, 0)
+        st = mb.load_library().mot_replay_attention(None, None, None, FAKE, None, ctypes.byref(c), None)
+        name = mb.STATUS[st]
+        assert name in ("MOT_ERR_NULL_ARG", "MOT_ERR_UNSUPPORTED", "MOT_ERR_BAD_SHAPE"), (D, S, name)
+        assert (name == "MOT_ERR_NULL_ARG") == bool(supported), (D, S, name)
+        if supported:
+            admitted.add((D, S))
+            assert perm and cover and lds <= 65536, (D, S, perm, cover, lds)
+    assert admitted == {(64, s) for s in range(32, 257, 32)} | {(128, s) for s in range(32, 193, 32)}
+    # the old mask (SC - 1) is not a row permutation for these sizes: the test has teeth
+    for S in (96, 160, 192, 224):
+        sc = S // 8
+        assert any(sorted(c ^ (d & (sc - 1)) for c in range(sc)) != list(range(sc)) for d in range(64))

@@ -14,7 +14,7 @@ from paper_2607_28979_amd import binding as mb
 from paper_2607_28979_amd.configs import Workload
 from paper_2607_28979_amd.inputs import backbone_params, generate
 
-from helpers import SENTINEL, TOL, dst_shape, oracle_dims, rel_frob, to_dev, unit_rows
+from helpers import SENTINEL, TOL, dst_shape, oracle_dims, rel_frob, row_errors, to_dev, unit_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -61,12 +61,16 @@ def test_backbone_parity(case, oracle_built):
     gk, gv = _run(w, d_h, nh, d_ff, lm, params, inp)
     rk, rv = oracle_backbone_translate(oracle_dims(w), inp.src_k, inp.src_v, lm, params, inp.wr, inp.br,
                                        d_h, nh, d_ff)
-    worst = 0.0
+    worst, worst_row = 0.0, 0.0
     for j in range(w.L_tgt):
         if lm[j] < 0:
             assert (gk[j] == SENTINEL).all() and (gv[j] == SENTINEL).all()
             continue
         for g, r in ((gk, rk), (gv, rv)):
             worst = max(worst, rel_frob(unit_rows(g, w, j), unit_rows(r, w, j)))
-    print("  max unit rel-Frobenius error %.3e" % worst, flush=True)
+            worst_row = max(worst_row, float(row_errors(unit_rows(g, w, j), unit_rows(r, w, j)).max()))
+    print("  max unit rel-Frobenius error %.3e, max row error %.3e" % (worst, worst_row), flush=True)
     assert worst <= TOL["bf16"]
+    # every row runs a chain of seven bf16 stages (three LayerNorms, attention),
+    # so single rows get twice the unit bar, as replay positions do
+    assert worst_row <= 2 * TOL["bf16"]

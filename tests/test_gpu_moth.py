@@ -21,7 +21,7 @@ from paper_2607_28979_amd import binding as mb
 from paper_2607_28979_amd.configs import Workload
 from paper_2607_28979_amd.inputs import activations, generate, projection_weights
 
-from helpers import SENTINEL, TOL, oracle_dims, rel_frob, to_dev
+from helpers import ROW_TOL, SENTINEL, TOL, oracle_dims, rel_frob, row_errors, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -74,8 +74,11 @@ def test_activation_translation_streams1(w, oracle_built):
         _, got = _translate_act(w, inp, lm, algo)
         worst = max(rel_frob(got[j].reshape(w.n_tok, -1), ref[j].reshape(w.n_tok, -1))
                     for j in range(w.L_tgt))
-        print("  max layer rel-Frobenius error %.3e" % worst, flush=True)
+        worst_row = max(float(row_errors(got[j].reshape(w.n_tok, -1), ref[j].reshape(w.n_tok, -1)).max())
+                        for j in range(w.L_tgt))
+        print("  max layer rel-Frobenius error %.3e, max row error %.3e" % (worst, worst_row), flush=True)
         assert worst <= TOL["bf16"], (w.name, algo, worst)
+        assert worst_row <= ROW_TOL["bf16"], (w.name, algo, worst_row)
 
 
 def _restore_gpu(act, lm, wk, bk, wv, bv, L, B, T, H, D, layout):
@@ -184,6 +187,7 @@ def test_moth_full_width_sampled(oracle_built):
                                B=1, T=len(rows), H_tgt=MOTH.kv_heads, D_tgt=MOTH.head_dim)
     for j in range(w.L_tgt):
         ea = rel_frob(a_got[j].reshape(w.n_tok, -1)[rows], ref[j])
+        assert float(row_errors(a_got[j].reshape(w.n_tok, -1)[rows], ref[j]).max()) <= ROW_TOL["bf16"], j
         ek = rel_frob(gk[j].reshape(w.n_tok, -1)[rows], rk[j].reshape(len(rows), -1))
         ev = rel_frob(gv[j].reshape(w.n_tok, -1)[rows], rv[j].reshape(len(rows), -1))
         print("  layer %d rel-Frobenius act %.3e K %.3e V %.3e" % (j, ea, ek, ev), flush=True)

@@ -22,8 +22,8 @@ from paper_2607_28979_amd import binding as mb
 from paper_2607_28979_amd.configs import WORKLOADS, small_variant
 from paper_2607_28979_amd.inputs import generate, sample_rows
 
-from helpers import (SENTINEL, TOL, max_unit_error, oracle_dims, rel_frob, run_gpu, to_dev,
-                     unit_rows)
+from helpers import (ROW_TOL, SENTINEL, TOL, check_topk_rows, max_unit_error, oracle_dims, rel_frob,
+                     row_errors, run_gpu, to_dev, unit_rows)
 
 pytestmark = pytest.mark.gpu
 
@@ -70,29 +70,21 @@ def test_small_parity(w, oracle_built):
         print("case", w.name, "algo", algo, flush=True)
         gk, gv = run_gpu(w, inp, lm, algo=algo)
         err = max_unit_error(gk, gv, rk, rv, w, lm)
-        print("  max unit rel-Frobenius error %.3e" % err, flush=True)
+        rows_worst = _max_row_error(gk, gv, rk, rv, w, lm)
+        print("  max unit rel-Frobenius error %.3e, max row error %.3e" % (err, rows_worst), flush=True)
         assert err <= TOL[w.dtype], (w.name, algo, err)
+        assert rows_worst <= ROW_TOL[w.dtype], (w.name, algo, rows_worst)
         assert np.isfinite(gk).all() and np.isfinite(gv).all()
 
 
-def _src_rows(w, inp, x, i):
-    """Source layer i of K (x = 0) or V (x = 1) as [B*T][d_in] float64."""
-    a = (inp.src_k, inp.src_v)[x][i].astype(np.float64)
-    if w.src_layout == 1:
-        a = a.transpose(0, 2, 1, 3)
-    return a.reshape(w.B * w.T, w.d_in)
-
-
-def _topk_margin(w, inp, lm, j, x):
-    """Per token: relative gap between the softmax scores of the K-th and the
-    (K+1)-th best translator, from float64 logits.  Rows with a gap below the
-    fp32 resolution of the scores may pick a different (equally valid) set."""
-    z = _src_rows(w, inp, x, lm[j])
-    logits = z @ inp.wr[j, x].astype(np.float64).T + inp.br[j, x].astype(np.float64)
-    g = np.exp(logits - logits.max(axis=1, keepdims=True))
-    g /= g.sum(axis=1, keepdims=True)
-    gs = -np.sort(-g, axis=1)
-    return (gs[:, w.top_k - 1] - gs[:, w.top_k]) / gs[:, w.top_k - 1]
+def _max_row_error(gk, gv, rk, rv, w, lm):
+    worst = 0.0
+    for j in range(w.L_tgt):
+        if lm[j] < 0:
+            continue
+        for g, r in ((gk, rk), (gv, rv)):
+            worst = max(worst, float(row_errors(unit_rows(g, w, j), unit_rows(r, w, j)).max()))
+    return worst
 
 
 TOPK = [(SMALL[0], 1), (SMALL[1], 1), (SMALL[1], 2), (SMALL[2], 2), (SMALL[3], 1), (SMALL[3], 2),
@@ -102,10 +94,11 @@ TOPK = [(SMALL[0], 1), (SMALL[1], 1), (SMALL[1], 2), (SMALL[2], 2), (SMALL[3], 1
 @pytest.mark.parametrize("w,k", TOPK, ids=["%s-top%d" % (w.name, k) for w, k in TOPK])
 def test_topk_parity(w, k, oracle_built):
     """Top-K < E routing (the K largest softmax scores, renormalised, ties to
-    the lower index) against the oracle, every kernel path.  Rows whose K-th
-    and (K+1)-th scores differ by less than 1e-3 of the K-th are left out of
-    the comparison (their selection is decided near the precision of the fp32
-    scores); they must be rare and finite."""
+    the lower index) against the oracle, every kernel path.  Every row meets
+    the per-row bar.  A row whose K-th and (K+1)-th scores differ by less than
+    1e-3 of the K-th has several valid sets at the precision of the fp32
+    scores: it must match the oracle row of one of them (each computed with a
+    router bias that forces that set), and such rows stay rare."""
     w = w.with_(top_k=k)
     inp = generate(w)
     lm = _layer_map(w)
@@ -113,19 +106,20 @@ def test_topk_parity(w, k, oracle_built):
     for algo in _algos(w):
         print("case", w.name, "top_k", k, "algo", algo, flush=True)
         gk, gv = run_gpu(w, inp, lm, algo=algo)
-        worst, n_skip, n_all = 0.0, 0, 0
+        worst, worst_row, n_tie, n_all = 0.0, 0.0, 0, 0
         for j in range(w.L_tgt):
             for x, (g, r) in enumerate(((gk, rk), (gv, rv))):
-                keep = _topk_margin(w, inp, lm, j, x) >= 1e-3
-                n_skip += int((~keep).sum())
-                n_all += keep.size
                 gr, rr = unit_rows(g, w, j), unit_rows(r, w, j)
                 assert np.isfinite(gr).all()
+                keep, wr_, nt = check_topk_rows(w, inp, lm, j, x, gr, rr)
+                n_tie += nt
+                n_all += keep.size
+                worst_row = max(worst_row, wr_)
                 worst = max(worst, rel_frob(gr[keep], rr[keep]))
-        print("  max unit rel-Frobenius error %.3e (%d of %d near-tie rows left out)"
-              % (worst, n_skip, n_all), flush=True)
+        print("  max unit rel-Frobenius error %.3e, max row error %.3e (%d of %d near-tie rows, each "
+              "matched to an admissible set)" % (worst, worst_row, n_tie, n_all), flush=True)
         assert worst <= TOL[w.dtype], (w.name, k, algo, worst)
-        assert n_skip <= max(2, n_all // 100)
+        assert n_tie <= max(2, n_all // 100)
 
 
 @pytest.mark.parametrize("w", WORKLOADS, ids=[w.name for w in WORKLOADS])
@@ -139,12 +133,15 @@ def test_full_size_sampled(w, oracle_built):
     units = [(j, x) for j in range(w.L_tgt) if lm[j] >= 0 for x in (0, 1)]
     ref = oracle_rows(oracle_dims(w), inp.src_k, inp.src_v, lm, inp.w1, inp.b1, inp.w2, inp.b2,
                       inp.wr, inp.br, units=units, rows=rows)
-    worst = 0.0
+    worst, worst_row = 0.0, 0.0
     for u, (j, x) in enumerate(units):
         got = unit_rows(gk if x == 0 else gv, w, j)[rows]
         worst = max(worst, rel_frob(got, ref[u]))
-    print("  max unit rel-Frobenius error on sampled rows %.3e" % worst, flush=True)
+        worst_row = max(worst_row, float(row_errors(got, ref[u]).max()))
+    print("  max unit rel-Frobenius error on sampled rows %.3e, max row error %.3e" % (worst, worst_row),
+          flush=True)
     assert worst <= TOL[w.dtype]
+    assert worst_row <= ROW_TOL[w.dtype]
     assert np.isfinite(gk).all() and np.isfinite(gv).all()
 
 
@@ -154,8 +151,9 @@ ROUTED_FULL = [(WORKLOADS[3], 1), (WORKLOADS[3], 2), (WORKLOADS[4], 2)]
 @pytest.mark.parametrize("w,k", ROUTED_FULL, ids=["%s-top%d" % (w.name, k) for w, k in ROUTED_FULL])
 def test_full_size_routed_sampled(w, k, oracle_built):
     """The routed Top-K path at full size (the launch `bench.py --top-k K`
-    times), on sampled rows the oracle computes one by one; rows whose K-th
-    and (K+1)-th scores are within 1e-3 (relative) are left out."""
+    times), on sampled rows the oracle computes one by one; a row whose K-th
+    and (K+1)-th scores are within 1e-3 (relative) must match the oracle row
+    of one of its admissible sets."""
     from oracle import oracle_rows
     w = w.with_(top_k=k)
     print("case", w.name, "top_k", k, "full size routed", flush=True)
@@ -166,16 +164,17 @@ def test_full_size_routed_sampled(w, k, oracle_built):
     units = [(j, x) for j in range(w.L_tgt) if lm[j] >= 0 for x in (0, 1)]
     ref = oracle_rows(oracle_dims(w), inp.src_k, inp.src_v, lm, inp.w1, inp.b1, inp.w2, inp.b2,
                       inp.wr, inp.br, units=units, rows=rows)
-    worst, n_skip = 0.0, 0
+    worst, worst_row, n_tie = 0.0, 0.0, 0
     for u, (j, x) in enumerate(units):
-        keep = _topk_margin(w, inp, lm, j, x)[rows] >= 1e-3
-        n_skip += int((~keep).sum())
         got = unit_rows(gk if x == 0 else gv, w, j)[rows]
+        keep, wr_, nt = check_topk_rows(w, inp, lm, j, x, got, ref[u], rows=rows)
+        n_tie += nt
+        worst_row = max(worst_row, wr_)
         worst = max(worst, rel_frob(got[keep], ref[u][keep]))
-    print("  max unit rel-Frobenius error on sampled rows %.3e (%d near-tie rows left out)"
-          % (worst, n_skip), flush=True)
+    print("  max unit rel-Frobenius error on sampled rows %.3e, max row error %.3e (%d near-tie rows, "
+          "each matched to an admissible set)" % (worst, worst_row, n_tie), flush=True)
     assert worst <= TOL[w.dtype]
-    assert n_skip <= max(2, len(rows) * len(units) // 100)
+    assert n_tie <= max(2, len(rows) * len(units) // 100)
     assert np.isfinite(gk).all() and np.isfinite(gv).all()
 
 

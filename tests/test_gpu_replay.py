@@ -94,6 +94,10 @@ ATTN = [  # B, T, H_q, H_kv, D, S, kv_layout
     (1, 280, 14, 2, 128, 192, 0),     # the largest S at D = 128
     (1, 230, 7, 1, 128, 160, 0),      # 10 key blocks: waves with 3 and with 2
     (1, 270, 8, 4, 64, 256, 1),       # the largest S at D = 64
+    # set sizes whose chunk count per row is not a power of two (a row-local
+    # LDS swizzle is needed): 12 and 28 chunks
+    (1, 240, 6, 2, 64, 96, 0),
+    (1, 300, 4, 1, 64, 224, 1),
 ]
 
 
