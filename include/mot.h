@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define MOT_ABI_VERSION 4
+#define MOT_ABI_VERSION 5
 #define MOT_MAX_LAYERS 256   /* L_src, L_tgt <= MOT_MAX_LAYERS               */
 #define MOT_MAX_EXPERTS 16   /* E <= MOT_MAX_EXPERTS                         */
 
@@ -104,6 +104,17 @@ typedef enum { MOT_ALGO_AUTO = 0, MOT_ALGO_UNFUSED = 1, MOT_ALGO_FUSED = 2, MOT_
  *                  NULL).  mot_restore_kv then forms K and V from it.
  *   workspace      optional device scratch; NULL = library-owned buffer
  *   workspace_bytes size of `workspace` in bytes
+ *   usage          optional device uint32 [L_tgt][streams][E], 4-byte aligned:
+ *                  translator usage (paper Sec. 4, "MoT Architecture
+ *                  Ablation": I_m, the cumulative selection count of
+ *                  translator m).  For every mapped unit (j, x) and every
+ *                  context token, usage[j][x][m] is incremented once for each
+ *                  translator m of the token's Top-K set, so each call adds
+ *                  top_k * B * T to a unit's row (B * T per translator when
+ *                  top_k = E).  Counts accumulate over calls (zero the array
+ *                  to start; they wrap at 2^32); rows of unmapped layers are
+ *                  not touched; NULL = not counted.  mot_usage_stats turns
+ *                  the counts into the paper's usage imbalance and entropy.
  *
  * Supported sizes (others return MOT_ERR_UNSUPPORTED):
  *   MOT_BF16: D_src, D_tgt multiples of 8; d_in multiple of 64;
@@ -120,6 +131,7 @@ typedef struct {
     int32_t streams;
     void* workspace;
     size_t workspace_bytes;
+    uint32_t* usage;
 } mot_shapes;
 
 /*
@@ -188,6 +200,22 @@ size_t mot_workspace_bytes(const mot_shapes* shapes);
  */
 mot_status mot_depth_ratio_map(int32_t L_src, int32_t L_tgt, int32_t* out);
 
+/*
+ * Translator usage statistics (paper Sec. 4, "MoT Architecture Ablation",
+ * Table "mot_analysis") of n rows of selection counts I[n][E] (as written
+ * by mot_translate's usage output; device uint32):
+ *     cv2[r]     = Var_m(I[r][m]) / Mean_m(I[r][m])^2   (population variance
+ *                  over the E translators: the usage imbalance CV^2)
+ *     entropy[r] = -sum_m p_m ln p_m,  p_m = I[r][m] / sum_m I[r][m]
+ *                  (natural log, 0 ln 0 = 0: the usage entropy)
+ * in double precision; both are NaN for a row of zeros.  cv2 and entropy:
+ * device double [n], 8-byte aligned, not overlapping the counts.  1 <= E <=
+ * MOT_MAX_EXPERTS; n = 0 is a no-op.  Asynchronous on `stream`; every check
+ * runs before the launch.
+ */
+mot_status mot_usage_stats(const uint32_t* counts, int32_t n, int32_t E, double* cv2, double* entropy,
+                           hipStream_t stream);
+
 /* Static text for a status code. */
 const char* mot_status_string(mot_status status);
 
@@ -236,13 +264,24 @@ mot_status mot_restore_kv(const void* act, const int32_t* layer_map, const void*
  *   S          Top-S budget: a multiple of 32, 32 .. 256 (at most 192 when
  *              D = 128); the paper uses 128
  *   kv_layout  K and V in MOT_LAYOUT_BTHD ([B][T][H_kv][D]) or MOT_LAYOUT_BHTD
+ *   workspace, workspace_bytes
+ *              optional device scratch of mot_replay_attention without key
+ *              sets (16-byte aligned, at least mot_replay_workspace_bytes);
+ *              NULL = the library's per-device buffer (see below)
  */
 typedef struct {
     int32_t B, T;
     int32_t H_q, H_kv, D;
     int32_t S;
     int32_t kv_layout;
+    void* workspace;
+    size_t workspace_bytes;
 } mot_replay_shapes;
+
+/* Scratch bytes mot_replay_attention needs for `shapes` with idx = NULL (V
+ * staged transposed: B * H_kv * D * T rounded up to 64, bf16); 0 with key
+ * sets; SIZE_MAX for invalid or unsupported shapes. */
+size_t mot_replay_workspace_bytes(const mot_replay_shapes* shapes, int with_sets);
 
 /*
  * Top-S key sets (App. C.4, N(u) = Top-S of A[u, 1:u]): for every b and u,
@@ -264,10 +303,12 @@ mot_status mot_topS_select(const float* A, int32_t* idx, const mot_replay_shapes
  * bf16 in kv_layout; idx: device int32 [B][T][S] or NULL.  Softmax and
  * accumulation in fp32; o rounded to bf16.  All pointers 16-byte aligned; o
  * must not overlap an input.  With idx NULL the call stages V transposed
- * (B * H_kv * D * T rounded up to 64, bf16) in the per-device buffer that
- * mot_translate uses without a workspace, so such calls and those of
- * mot_translate or mot_backbone_translate that overlap in time on one device
- * race.
+ * (mot_replay_workspace_bytes) in shapes->workspace, or, when that is NULL,
+ * in the per-device buffer that mot_translate uses without a workspace (so
+ * such calls and those of mot_translate or mot_backbone_translate without
+ * workspaces that overlap in time on one device race; calls with their own
+ * workspaces do not).  A workspace below the need returns
+ * MOT_ERR_WORKSPACE_TOO_SMALL; it must not overlap q, k, v or o.
  */
 mot_status mot_replay_attention(const void* q, const void* k, const void* v, const int32_t* idx, void* o,
                                 const mot_replay_shapes* shapes, hipStream_t stream);
@@ -294,11 +335,14 @@ mot_status mot_replay_attention(const void* q, const void* k, const void* v, con
  *            b_f1[d_ff] w_f2[d_h][d_ff] b_f2[d_h] ln_out_g[d_h] ln_out_b[d_h]
  *            w_out[d_out][d_h] b_out[d_out]
  *   router   as for mot_translate (bias optional)
- *   shapes   as for mot_translate; dtype MOT_BF16, both layouts
- *            MOT_LAYOUT_BTHD, streams 2; hidden, act, algo and the workspace
- *            fields are not used (the library owns the scratch it needs:
- *            the per-device buffer mot_translate uses without a workspace,
- *            so calls of either that overlap in time on one device race)
+ *   shapes   as for mot_translate (including the optional usage counts of
+ *            the Top-K selections); dtype MOT_BF16, both layouts
+ *            MOT_LAYOUT_BTHD, streams 2; hidden, act and algo are not used.
+ *            workspace: device scratch of at least
+ *            mot_backbone_workspace_bytes (16-byte aligned, not overlapping
+ *            any other argument), or NULL for the per-device buffer that
+ *            mot_translate uses without a workspace (calls of either that
+ *            overlap in time on one device then race)
  * Requires d_in and d_h multiples of 64 up to 4096, d_ff a multiple of 64,
  * D_tgt a multiple of 8, head width d_h / n_heads of 64 or 128
  * (MOT_ERR_UNSUPPORTED otherwise).  Every check runs before any enqueue.
@@ -311,6 +355,11 @@ typedef struct {
 
 /* Elements per expert of the packed parameters (0 for invalid arguments). */
 size_t mot_backbone_param_count(const mot_shapes* shapes, const mot_backbone_dims* dims);
+
+/* Scratch bytes mot_backbone_translate needs (the router's gates for every
+ * unit, one unit's activations and the attention's staged V); SIZE_MAX for
+ * invalid or unsupported arguments. */
+size_t mot_backbone_workspace_bytes(const mot_shapes* shapes, const mot_backbone_dims* dims);
 
 mot_status mot_backbone_translate(const void* src_k, const void* src_v, const int32_t* layer_map,
                                   const void* params, const mot_router_weights* router, void* dst_k, void* dst_v,

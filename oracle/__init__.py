@@ -9,9 +9,11 @@ precision; see ``mot_oracle.c`` for the step-by-step statement.
 from .oracle import (OracleDims, build_oracle, oracle_translate, oracle_rows,
                      oracle_depth_ratio_map, oracle_lib_path, oracle_restore_kv,
                      oracle_topS_select, oracle_replay_attention, oracle_topS_rows,
-                     oracle_replay_attention_rows, oracle_backbone_translate, oracle_backbone_param_count)
+                     oracle_replay_attention_rows, oracle_backbone_translate, oracle_backbone_param_count,
+                     oracle_usage, oracle_usage_stats)
 
 __all__ = ["OracleDims", "build_oracle", "oracle_translate", "oracle_rows",
            "oracle_depth_ratio_map", "oracle_lib_path", "oracle_restore_kv",
            "oracle_topS_select", "oracle_replay_attention", "oracle_topS_rows",
-           "oracle_replay_attention_rows", "oracle_backbone_translate", "oracle_backbone_param_count"]
+           "oracle_replay_attention_rows", "oracle_backbone_translate", "oracle_backbone_param_count",
+           "oracle_usage", "oracle_usage_stats"]

@@ -771,3 +771,85 @@ done:
     free(att); free(f); free(y); free(sc); free(lg); free(sel);
     return rc;
 }
+
+/* ------------------------------------------------------------------ */
+/* translator usage (paper Sec. 4, "MoT Architecture Ablation",        */
+/* Table "mot_analysis")                                               */
+/* ------------------------------------------------------------------ */
+
+/* Selection counts: counts[(j * streams + x) * E + m] += the number of
+ * context tokens whose Top-K set (Definition "Mixture-of-Translators": the
+ * top_k largest softmax scores, ties to the lower index) holds translator m,
+ * for every unit (j, x) with layer_map[j] >= 0.  Counts accumulate: the
+ * caller zeroes them to start. */
+int mot_oracle_usage(const float* src_k, const float* src_v, const int32_t* layer_map,
+                     const float* wr, const float* br, const mot_oracle_dims* s, int64_t* counts)
+{
+    int rc = check_dims(s, layer_map);
+    if (rc) return rc;
+    if (!src_k || !wr || !counts || (s->streams == 2 && !src_v)) return OR_BAD_ARG;
+    const int32_t d_in = s->H_src * s->D_src, E = s->E;
+    double* z = (double*)malloc(sizeof(double) * d_in);
+    double* g = (double*)malloc(sizeof(double) * E);
+    int* sel = (int*)malloc(sizeof(int) * E);
+    if (!z || !g || !sel) { free(z); free(g); free(sel); return OR_NO_MEM; }
+    for (int32_t j = 0; j < s->L_tgt; ++j) {
+        const int32_t i = layer_map[j];
+        if (i < 0) continue;
+        for (int32_t x = 0; x < s->streams; ++x) {
+            const size_t unit = (size_t)j * s->streams + x;
+            for (int32_t b = 0; b < s->B; ++b)
+                for (int32_t t = 0; t < s->T; ++t) {
+                    gather_row(s, x == 0 ? src_k : src_v, i, b, t, z);
+                    /* gate logits, softmax */
+                    double mx = -INFINITY;
+                    for (int32_t m = 0; m < E; ++m) {
+                        double acc = 0.0;
+                        for (int32_t c = 0; c < d_in; ++c) acc += (double)wr[(unit * E + m) * d_in + c] * z[c];
+                        if (br) acc += (double)br[unit * E + m];
+                        g[m] = acc;
+                        if (acc > mx) mx = acc;
+                    }
+                    double den = 0.0;
+                    for (int32_t m = 0; m < E; ++m) { g[m] = exp(g[m] - mx); den += g[m]; }
+                    for (int32_t m = 0; m < E; ++m) { g[m] /= den; sel[m] = 0; }
+                    /* Top-K: the largest remaining score, top_k times; a tie
+                     * keeps the lower index (ascending scan, strict '>') */
+                    for (int32_t k = 0; k < s->top_k; ++k) {
+                        int32_t best = -1;
+                        for (int32_t m = 0; m < E; ++m)
+                            if (!sel[m] && (best < 0 || g[m] > g[best])) best = m;
+                        sel[best] = 1;
+                    }
+                    for (int32_t m = 0; m < E; ++m) counts[unit * E + m] += sel[m];
+                }
+        }
+    }
+    free(z); free(g); free(sel);
+    return OR_OK;
+}
+
+/* Usage imbalance and entropy of one unit's counts I[0..E):
+ *   CV^2    = Var_m(I_m) / Mean_m(I_m)^2   (population variance: the mean of
+ *             the squared deviations over the E translators)
+ *   entropy = -sum_m p_m ln p_m,  p_m = I_m / sum_r I_r  (0 ln 0 = 0)
+ * Both are NaN when every count is zero. */
+int mot_oracle_usage_stats(const int64_t* counts, int32_t E, double* cv2, double* entropy)
+{
+    if (!counts || E < 1 || !cv2 || !entropy) return OR_BAD_ARG;
+    double total = 0.0;
+    for (int32_t m = 0; m < E; ++m) total += (double)counts[m];
+    const double mean = total / E;
+    double var = 0.0;
+    for (int32_t m = 0; m < E; ++m) var += ((double)counts[m] - mean) * ((double)counts[m] - mean);
+    var /= E;
+    *cv2 = var / (mean * mean);
+    double h = 0.0;
+    for (int32_t m = 0; m < E; ++m) {
+        if (counts[m] == 0) continue;
+        const double p = (double)counts[m] / total;
+        h -= p * log(p);
+    }
+    *entropy = total > 0.0 ? h : NAN;
+    return OR_OK;
+}

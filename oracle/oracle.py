@@ -97,7 +97,8 @@ def _load():
                    _lib.mot_oracle_depth_ratio_map, _lib.mot_oracle_restore_kv,
                    _lib.mot_oracle_topS_select, _lib.mot_oracle_replay_attention,
                    _lib.mot_oracle_replay_attention_rows, _lib.mot_oracle_topS_rows,
-                   _lib.mot_oracle_backbone_translate):
+                   _lib.mot_oracle_backbone_translate, _lib.mot_oracle_usage,
+                   _lib.mot_oracle_usage_stats):
             fn.restype = ctypes.c_int
     return _lib
 
@@ -307,3 +308,30 @@ def oracle_backbone_translate(dims: OracleDims, src_k, src_v, layer_map, params,
     if rc != 0:
         raise ValueError("mot_oracle_backbone_translate failed with code %d" % rc)
     return dst_k, dst_v
+
+
+def oracle_usage(dims: OracleDims, src_k, src_v, layer_map, wr, br) -> np.ndarray:
+    """Translator selection counts per unit (paper Sec. 4, "MoT Architecture
+    Ablation"): int64 [L_tgt][streams][E]; units of unmapped layers stay 0."""
+    lib = _load()
+    arrs = [_f32(a, n) for a, n in ((src_k, "src_k"), (src_v, "src_v"), (wr, "wr"), (br, "br"))]
+    lm = np.ascontiguousarray(layer_map, dtype=np.int32)
+    counts = np.zeros((dims.L_tgt, dims.streams, dims.E), np.int64)
+    c = dims._c()
+    rc = lib.mot_oracle_usage(_ptr(arrs[0]), _ptr(arrs[1]), _ptr(lm), _ptr(arrs[2]), _ptr(arrs[3]),
+                              ctypes.byref(c), _ptr(counts))
+    if rc != 0:
+        raise ValueError("mot_oracle_usage failed with code %d" % rc)
+    return counts
+
+
+def oracle_usage_stats(counts) -> tuple:
+    """(CV^2, entropy) of one unit's counts I[0..E): population variance over
+    the squared mean, and -sum p ln p with p = I / sum I."""
+    lib = _load()
+    cnt = np.ascontiguousarray(counts, dtype=np.int64).ravel()
+    cv2, ent = ctypes.c_double(), ctypes.c_double()
+    rc = lib.mot_oracle_usage_stats(_ptr(cnt), ctypes.c_int32(cnt.size), ctypes.byref(cv2), ctypes.byref(ent))
+    if rc != 0:
+        raise ValueError("mot_oracle_usage_stats failed with code %d" % rc)
+    return cv2.value, ent.value

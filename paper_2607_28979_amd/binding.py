@@ -26,7 +26,8 @@ STATUS = {0: "MOT_OK", 1: "MOT_ERR_NULL_ARG", 2: "MOT_ERR_BAD_SHAPE", 3: "MOT_ER
 
 EXPORTED = ("mot_translate", "mot_workspace_bytes", "mot_depth_ratio_map", "mot_status_string",
             "mot_last_error", "mot_abi_version", "mot_restore_kv", "mot_topS_select",
-            "mot_replay_attention", "mot_backbone_param_count", "mot_backbone_translate")
+            "mot_replay_attention", "mot_backbone_param_count", "mot_backbone_translate",
+            "mot_usage_stats", "mot_replay_workspace_bytes", "mot_backbone_workspace_bytes")
 
 
 class MotError(RuntimeError):
@@ -40,7 +41,7 @@ class _Shapes(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "L_src", "L_tgt", "B", "T", "H_src", "D_src", "H_tgt", "D_tgt", "E", "top_k", "hidden",
         "dtype", "src_layout", "dst_layout", "act", "algo", "streams")] + [
-        ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
+        ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t), ("usage", ctypes.c_void_p)]
 
 
 class _RestoreShapes(ctypes.Structure):
@@ -53,7 +54,8 @@ class _BackboneDims(ctypes.Structure):
 
 
 class _ReplayShapes(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_int32) for n in ("B", "T", "H_q", "H_kv", "D", "S", "kv_layout")]
+    _fields_ = [(n, ctypes.c_int32) for n in ("B", "T", "H_q", "H_kv", "D", "S", "kv_layout")] + [
+        ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
 
 
 class _TW(ctypes.Structure):
@@ -85,11 +87,11 @@ class Shapes:
     algo: int = ALGO_AUTO
     streams: int = 2          # 2 = keys and values; 1 = one activation stream (MoT-h)
 
-    def c(self, workspace=None, workspace_bytes=0) -> _Shapes:
+    def c(self, workspace=None, workspace_bytes=0, usage=None) -> _Shapes:
         return _Shapes(self.L_src, self.L_tgt, self.B, self.T, self.H_src, self.D_src, self.H_tgt,
                        self.D_tgt, self.E, self.top_k or self.E, self.hidden, self.dtype,
                        self.src_layout, self.dst_layout, self.act, self.algo, self.streams,
-                       workspace, workspace_bytes)
+                       workspace, workspace_bytes, usage)
 
     @classmethod
     def from_workload(cls, w, **kw) -> "Shapes":
@@ -160,6 +162,13 @@ def load_library():
         lib.mot_backbone_translate.argtypes = [ctypes.c_void_p] * 4 + [ctypes.POINTER(_RW), ctypes.c_void_p,
                                                                        ctypes.c_void_p, ctypes.POINTER(_Shapes),
                                                                        ctypes.POINTER(_BackboneDims), ctypes.c_void_p]
+        lib.mot_replay_workspace_bytes.restype = ctypes.c_size_t
+        lib.mot_replay_workspace_bytes.argtypes = [ctypes.POINTER(_ReplayShapes), ctypes.c_int]
+        lib.mot_backbone_workspace_bytes.restype = ctypes.c_size_t
+        lib.mot_backbone_workspace_bytes.argtypes = [ctypes.POINTER(_Shapes), ctypes.POINTER(_BackboneDims)]
+        lib.mot_usage_stats.restype = ctypes.c_int
+        lib.mot_usage_stats.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                        ctypes.c_void_p, ctypes.c_void_p]
         lib.mot_replay_attention.restype = ctypes.c_int
         lib.mot_replay_attention.argtypes = [ctypes.c_void_p] * 5 + [ctypes.POINTER(_ReplayShapes),
                                                                      ctypes.c_void_p]
@@ -204,7 +213,7 @@ def _ptr(t) -> Optional[int]:
 
 
 def translate_raw(src_k, src_v, layer_map, w1, b1, w2, b2, wr, br, dst_k, dst_v,
-                  shapes: Shapes, stream=None, workspace=None, workspace_bytes_=0) -> None:
+                  shapes: Shapes, stream=None, workspace=None, workspace_bytes_=0, usage=None) -> None:
     """Call mot_translate with raw device addresses (ints) or tensors.  No
     checks beyond the library's own (used by the ABI validation tests)."""
     import numpy as np
@@ -212,17 +221,19 @@ def translate_raw(src_k, src_v, layer_map, w1, b1, w2, b2, wr, br, dst_k, dst_v,
     lm = np.ascontiguousarray(layer_map, dtype=np.int32)
     tw = _TW(_ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2))
     rw = _RW(_ptr(wr), _ptr(br))
-    c = shapes.c(_ptr(workspace), workspace_bytes_)
+    c = shapes.c(_ptr(workspace), workspace_bytes_, _ptr(usage))
     _check(lib.mot_translate(_ptr(src_k), _ptr(src_v), lm.ctypes.data if lm.size else None,
                              ctypes.byref(tw), ctypes.byref(rw), _ptr(dst_k), _ptr(dst_v),
                              ctypes.byref(c), stream))
 
 
 def translate(src_k, src_v, layer_map: Sequence[int], w1, b1, w2, b2, wr, br, dst_k, dst_v,
-              shapes: Shapes, workspace=None) -> None:
+              shapes: Shapes, workspace=None, usage=None) -> None:
     """Translate on the current torch stream.  Tensors must live on the
     current HIP device, be contiguous and have the dtype named by
-    ``shapes.dtype`` (torch.float32 or torch.bfloat16)."""
+    ``shapes.dtype`` (torch.float32 or torch.bfloat16).  ``usage``: optional
+    int32 tensor [L_tgt][streams][E] of translator selection counts that the
+    call adds to (the library treats it as uint32)."""
     import torch
     want = torch.float32 if shapes.dtype == MOT_F32 else torch.bfloat16
     dev = torch.device("cuda", torch.cuda.current_device())
@@ -239,9 +250,24 @@ def translate(src_k, src_v, layer_map: Sequence[int], w1, b1, w2, b2, wr, br, ds
     ws_bytes = 0
     if workspace is not None:
         ws_bytes = workspace.numel() * workspace.element_size()
+    if usage is not None and (usage.device != dev or usage.dtype != torch.int32 or not usage.is_contiguous()):
+        raise MotError(2, "usage must be a contiguous int32 tensor on %s" % dev)
     stream = torch.cuda.current_stream().cuda_stream
     translate_raw(src_k, src_v, layer_map, w1, b1, w2, b2, wr, br, dst_k, dst_v, shapes,
-                  stream=stream, workspace=workspace, workspace_bytes_=ws_bytes)
+                  stream=stream, workspace=workspace, workspace_bytes_=ws_bytes, usage=usage)
+
+
+def usage_stats(counts, cv2, entropy) -> None:
+    """mot_usage_stats on the current torch stream: counts int32 [n][E]
+    (read as uint32), cv2 and entropy float64 [n] (outputs)."""
+    import torch
+    for name, t, dt in (("counts", counts, torch.int32), ("cv2", cv2, torch.float64),
+                        ("entropy", entropy, torch.float64)):
+        if t.dtype != dt or not t.is_contiguous():
+            raise MotError(2, "%s must be a contiguous %s tensor" % (name, dt))
+    n, E = counts.shape
+    _check(load_library().mot_usage_stats(_ptr(counts), n, E, _ptr(cv2), _ptr(entropy),
+                                          torch.cuda.current_stream().cuda_stream))
 
 
 def restore_kv(act, layer_map, wk, bk, wv, bv, dst_k, dst_v, L: int, B: int, T: int, d_act: int,
@@ -277,10 +303,19 @@ def topS_select(A, idx, B: int, T: int, S: int) -> None:
                                torch.cuda.current_stream().cuda_stream))
 
 
+def replay_workspace_bytes(B: int, T: int, H_q: int, H_kv: int, D: int, S: int = 0, with_sets: bool = False) -> int:
+    c = _ReplayShapes(B, T, H_q, H_kv, D, S, LAYOUT_BTHD)
+    n = load_library().mot_replay_workspace_bytes(ctypes.byref(c), int(with_sets))
+    if n == ctypes.c_size_t(-1).value:
+        raise MotError(2, load_library().mot_last_error().decode())
+    return int(n)
+
+
 def replay_attention(q, k, v, idx, o, B: int, T: int, H_q: int, H_kv: int, D: int, S: int = 0,
-                     kv_layout: int = LAYOUT_BTHD) -> None:
+                     kv_layout: int = LAYOUT_BTHD, workspace=None) -> None:
     """mot_replay_attention on the current torch stream (bf16 q, k, v, o;
-    int32 idx [B][T][S], or None for the full causal set)."""
+    int32 idx [B][T][S], or None for the full causal set; optional device
+    workspace tensor for the full causal set's staging)."""
     import torch
     lib = load_library()
     for name, t in (("q", q), ("k", k), ("v", v), ("o", o)):
@@ -288,7 +323,8 @@ def replay_attention(q, k, v, idx, o, B: int, T: int, H_q: int, H_kv: int, D: in
             raise MotError(2, "%s must be a contiguous bfloat16 tensor" % name)
     if idx is not None and (idx.dtype != torch.int32 or not idx.is_contiguous()):
         raise MotError(2, "idx must be a contiguous int32 tensor")
-    c = _ReplayShapes(B, T, H_q, H_kv, D, S if idx is not None else 0, kv_layout)
+    c = _ReplayShapes(B, T, H_q, H_kv, D, S if idx is not None else 0, kv_layout, _ptr(workspace),
+                      workspace.numel() * workspace.element_size() if workspace is not None else 0)
     _check(lib.mot_replay_attention(_ptr(q), _ptr(k), _ptr(v), _ptr(idx), _ptr(o), ctypes.byref(c),
                                     torch.cuda.current_stream().cuda_stream))
 
@@ -299,8 +335,16 @@ def backbone_param_count(shapes: Shapes, d_h: int, n_heads: int, d_ff: int) -> i
     return int(load_library().mot_backbone_param_count(ctypes.byref(c), ctypes.byref(_BackboneDims(d_h, n_heads, d_ff))))
 
 
+def backbone_workspace_bytes(shapes: Shapes, d_h: int, n_heads: int, d_ff: int) -> int:
+    c = shapes.c()
+    n = load_library().mot_backbone_workspace_bytes(ctypes.byref(c), ctypes.byref(_BackboneDims(d_h, n_heads, d_ff)))
+    if n == ctypes.c_size_t(-1).value:
+        raise MotError(2, load_library().mot_last_error().decode())
+    return int(n)
+
+
 def backbone_translate(src_k, src_v, layer_map, params, wr, br, dst_k, dst_v, shapes: Shapes, d_h: int,
-                       n_heads: int, d_ff: int) -> None:
+                       n_heads: int, d_ff: int, usage=None, workspace=None) -> None:
     """mot_backbone_translate on the current torch stream (bf16 tensors)."""
     import numpy as np
     import torch
@@ -311,7 +355,8 @@ def backbone_translate(src_k, src_v, layer_map, params, wr, br, dst_k, dst_v, sh
             raise MotError(2, "%s must be a contiguous bfloat16 tensor" % name)
     lm = np.ascontiguousarray(layer_map, dtype=np.int32)
     rw = _RW(_ptr(wr), _ptr(br))
-    c = shapes.c()
+    c = shapes.c(_ptr(workspace), workspace.numel() * workspace.element_size() if workspace is not None else 0,
+                 _ptr(usage))
     _check(lib.mot_backbone_translate(_ptr(src_k), _ptr(src_v), lm.ctypes.data, _ptr(params), ctypes.byref(rw),
                                       _ptr(dst_k), _ptr(dst_v), ctypes.byref(c),
                                       ctypes.byref(_BackboneDims(d_h, n_heads, d_ff)),

@@ -75,6 +75,17 @@ typedef __attribute__((address_space(3))) void lds_void;
 #ifndef MOT_FUSED_SPLIT
 #define MOT_FUSED_SPLIT 0
 #endif
+// Slots of the layer-2 waves' global -> LDS weight loads within an
+// iteration: spread evenly over the MFMA slots (1) or issued in the first
+// slots (0)
+#ifndef MOT_FUSED_LOAD_SPREAD
+#define MOT_FUSED_LOAD_SPREAD 1
+#endif
+// Wave priority (s_setprio) of the layer-1 waves during their MFMA slots
+// (0: the default priority throughout)
+#ifndef MOT_FUSED_L1_PRIO
+#define MOT_FUSED_L1_PRIO 0
+#endif
 
 template <int D_IN, int D_OUT>
 struct Cfg {
@@ -160,6 +171,14 @@ void k_bf16_fused(Problem p, UnitTab ut) {
     u32x4* Hs = smem + C::OFF_H;
     float* Gs = reinterpret_cast<float*>(smem + C::OFF_G);
     u32x4* Xs = smem + C::OFF_X;   // fp32 layer-1 results handed to wave 3
+    // Translator usage of the tile (non-routed mode): MOT_MAX_EXPERTS
+    // counters in the last 64 bytes of W1 stage 1, which holds the router
+    // rows during the router and is zeroed there for rows >= E (these words
+    // are in row 31); W1 chunk 1 overwrites it only after the counters are
+    // flushed.  Kept inside smem: a second LDS object would make the
+    // compiler wait for every direct-to-LDS load before each LDS read.
+    uint32_t* s_usage = reinterpret_cast<uint32_t*>(W1s + 2 * C::W1_CH) - MOT_MAX_EXPERTS;
+    static_assert(C::W1_CH / C::CPR1 == 32 && C::CPR1 * 16 >= MOT_MAX_EXPERTS * 4, "usage counters in row 31");
 
     const uint32_t code = ut.code[blockIdx.y];
     const int j = unit_j(code), x = unit_x(code), i = unit_i(code);
@@ -367,7 +386,11 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                 const float inv = 1.0f / den;
 #pragma unroll
                 for (int m = 0; m < MOT_MAX_EXPERTS; ++m) gate_all[m] *= inv;
-                topk_renormalise(gate_all, E, p.top_k);
+                const uint32_t taken = topk_renormalise(gate_all, E, p.top_k);
+                // translator usage: lanes 0..15 hold this token half's tokens
+                if (p.usage && q4 == 0 && tok0 + 32 * w + 16 * th + l16 < p.n_tok) {
+                    for (uint32_t t = taken; t; t &= t - 1) atomicAdd(&s_usage[__builtin_ctz(t)], 1u);
+                }
                 if (q4 == 0) {
 #pragma unroll
                     for (int m = 0; m < MOT_MAX_EXPERTS; ++m)
@@ -488,6 +511,7 @@ void k_bf16_fused(Problem p, UnitTab ut) {
             }
             mid_barrier();
             __builtin_amdgcn_sched_barrier(0);
+            if constexpr (MOT_FUSED_L1_PRIO > 0 && do_l1) __builtin_amdgcn_s_setprio(MOT_FUSED_L1_PRIO);
             static_for<0, NM>([&](auto kc) {
                 constexpr int k = decltype(kc)::value;
                 if constexpr (do_l1) {
@@ -522,6 +546,10 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                 }
                 __builtin_amdgcn_sched_barrier(0);
             });
+            if constexpr (MOT_FUSED_L1_PRIO > 0 && do_l1) {
+                __builtin_amdgcn_sched_barrier(0);
+                __builtin_amdgcn_s_setprio(0);
+            }
             if constexpr (do_gelu && MOT_FUSED_A_LAST && !C::SPLIT) {
                 static_for<0, 3>([&](auto stc) {
                     static_for<0, NEA>([&](auto ec) { gelu_elem(ec, stc); });
@@ -581,6 +609,9 @@ void k_bf16_fused(Problem p, UnitTab ut) {
         for (int r = 0; r < W1_RL; ++r) load_w1_round(0, 0, r, ow1[r % NV1]);
         __syncthreads();                                     // barrier A
         __syncthreads();                                     // barrier B
+        // the tile's translator usage, counted by the layer-1 waves' router
+        if (!ROUTED && p.usage && q2 == 0 && lane < E && s_usage[lane])
+            atomicAdd(p.usage + unit * E + lane, s_usage[lane]);
         // accumulators seeded with sum_m g_m b2_m[o] on MFMA: A = gates of a
         // token block (k = translator), B = b2 (k = translator); gates split
         // into bf16 high + residual parts keep ~16 mantissa bits.
@@ -659,7 +690,7 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                 if constexpr (NV > 0) {
                     static_for<0, NV>([&](auto rc) {
                         constexpr int r = decltype(rc)::value;
-                        if constexpr ((r * NM) / NV == k) {
+                        if constexpr ((MOT_FUSED_LOAD_SPREAD ? (r * NM) / NV : r) == k) {
                             if constexpr (r < W1_RL) {
                                 if constexpr (do_w1) load_w1_round(c_w1, (c + 1) & 1, r, ow1[r % NV1]);
                             } else {

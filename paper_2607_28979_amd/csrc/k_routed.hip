@@ -7,7 +7,8 @@
 // ascending order within each translator), the tile table of the fused
 // kernel (tiles of tile_rows assignments, never straddling two translators)
 // and, for top_k > 1, each (token, k)'s assignment index.  No atomics: the
-// result is the same on every run.
+// result is the same on every run.  The translator totals are also added to
+// the optional usage counts.
 //
 // k_routed_combine (top_k > 1): out[token] = sum over k of the fp32
 // per-assignment rows, in k order, rounded once to bf16 and stored in the
@@ -27,7 +28,10 @@ __global__ __launch_bounds__(kPlanThreads) void k_route_plan(Problem p, UnitTab 
     __shared__ int32_t s_wave[MOT_MAX_EXPERTS][kPlanThreads / 64];
     __shared__ int32_t s_eoff[MOT_MAX_EXPERTS + 1], s_toff[MOT_MAX_EXPERTS + 1];
 
-    const int gs = unit_gslot(ut.code[blockIdx.x]);
+    const uint32_t code = ut.code[blockIdx.x];
+    const int gs = unit_gslot(code);
+    // translator usage of this unit (the totals of the counting sort)
+    uint32_t* usage = p.usage ? p.usage + ((size_t)unit_j(code) * p.streams + unit_x(code)) * p.E : nullptr;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int N = p.n_tok, K = p.top_k, E = p.E, BM = p.rt.tile_rows;
     const size_t NK = (size_t)N * K;
@@ -81,6 +85,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_route_plan(Problem p, UnitTab 
         int a = 0, tl = 0;
         for (int m = 0; m < E; ++m) {
             const int tot = s_run[m][0];
+            if (usage && tot) atomicAdd(usage + m, (uint32_t)tot);
             s_eoff[m] = a;
             s_toff[m] = tl;
             a += tot;

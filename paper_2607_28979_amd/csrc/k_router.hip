@@ -85,6 +85,9 @@ __global__ __launch_bounds__(256) void k_router(Problem p, UnitTab ut) {
     }
     for (int grp = 0; grp < kGroups; ++grp) {
     const int tok = (blockIdx.x * kGroups + grp) * kTokPerBlock + threadIdx.x / kLanesPerTok;
+    // the gate rows of the last partial pass are still written by lanes q == 0
+    // of valid tokens only; the usage count needs every lane of the wave
+    const bool owner = tok < p.n_tok && q == 0;
     const int E = p.E, d_in = p.d_in;
     const size_t unit = (size_t)j * p.streams + x;
 
@@ -135,7 +138,8 @@ __global__ __launch_bounds__(256) void k_router(Problem p, UnitTab ut) {
             acc[m] = v;
         }
     }
-    if (tok >= p.n_tok || q != 0) continue;
+    // every lane runs the softmax and the selection (lanes without a token
+    // work on zeros and write nothing), so the wave can count selections
     float mx = -INFINITY;
 #pragma unroll
     for (int m = 0; m < MOT_MAX_EXPERTS; ++m) {
@@ -156,16 +160,45 @@ __global__ __launch_bounds__(256) void k_router(Problem p, UnitTab ut) {
 #pragma unroll
     for (int m = 0; m < MOT_MAX_EXPERTS; ++m) acc[m] = m < E ? acc[m] * inv : 0.f;
     if constexpr (LISTS) {
+        // the routed path counts usage in its plan kernel
+        if (!owner) continue;
         const size_t base = ((size_t)gs * p.n_tok + tok) * p.top_k;
         topk_list(acc, E, p.top_k, p.rt.sel + base, p.rt.gk + base);
         continue;
     }
-    topk_renormalise(acc, E, p.top_k);
+    const uint32_t taken = topk_renormalise(acc, E, p.top_k);
+    if (p.usage) count_usage(p.usage + unit * E, E, taken, owner);
+    if (!owner) continue;
     float* g = p.gates + ((size_t)gs * p.n_tok_pad + tok) * E;
 #pragma unroll
     for (int m = 0; m < MOT_MAX_EXPERTS; ++m)
         if (m < E) g[m] = acc[m];
     }
+}
+
+// Translator usage statistics (paper Sec. 4, "MoT Architecture Ablation"),
+// one thread per row of counts I[E]: CV^2 = population variance over the
+// squared mean, entropy = -sum p ln p with p = I / sum I (0 ln 0 = 0), in
+// double; NaN for a row of zeros.
+__global__ __launch_bounds__(256) void k_usage_stats(const uint32_t* counts, int n, int E, double* cv2,
+                                                     double* entropy) {
+    const int r = blockIdx.x * 256 + threadIdx.x;
+    if (r >= n) return;
+    const uint32_t* c = counts + (size_t)r * E;
+    double total = 0.0;
+    for (int m = 0; m < E; ++m) total += (double)c[m];
+    const double mean = total / E;
+    double var = 0.0;
+    for (int m = 0; m < E; ++m) var += ((double)c[m] - mean) * ((double)c[m] - mean);
+    var /= E;
+    cv2[r] = var / (mean * mean);
+    double h = 0.0;
+    for (int m = 0; m < E; ++m) {
+        if (c[m] == 0) continue;
+        const double q = (double)c[m] / total;
+        h -= q * log(q);
+    }
+    entropy[r] = total > 0.0 ? h : __builtin_nan("");
 }
 
 constexpr size_t kWrLdsMax = 64 * 1024;   // router rows staged in LDS up to this size
@@ -190,6 +223,14 @@ hipError_t launch_router(const Problem& p, const UnitTab& ut, bool bf16, hipStre
 
 hipError_t launch_router_lists(const Problem& p, const UnitTab& ut, hipStream_t stream) {
     return launch_k<true, true>(p, ut, stream);
+}
+
+hipError_t launch_usage_stats(const uint32_t* counts, int n, int E, double* cv2, double* entropy,
+                              hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_usage_stats, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, counts, n, E, cv2,
+                       entropy);
+    return hipGetLastError();
 }
 
 }  // namespace mot

@@ -108,6 +108,7 @@ Problem base_problem(const mot_shapes* s) {
     p.n_tok_pad = (int32_t)round_up((size_t)p.n_tok, 128);
     p.src_layout = s->src_layout; p.dst_layout = s->dst_layout; p.act = s->act;
     p.streams = s->streams == 1 ? 1 : 2;
+    p.usage = s->usage;
     return p;
 }
 
@@ -275,6 +276,8 @@ mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* la
         dst_v = nullptr;
     }
     const size_t es = s->dtype == MOT_BF16 ? 2 : 4;
+    if (s->usage && (reinterpret_cast<uintptr_t>(s->usage) & 3))
+        return fail(MOT_ERR_MISALIGNED, "usage %p is not 4-byte aligned", (void*)s->usage);
     const void* bias_ptrs[] = {tw->b1, tw->b2, rw->b};
     for (const void* q : bias_ptrs)
         if (q && !aligned16(q))   // the fused kernel reads b1 in 16-byte pieces
@@ -290,6 +293,10 @@ mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* la
         (two && (overlaps(dst_k, dst_bytes, dst_v, dst_bytes) || overlaps(dst_k, dst_bytes, src_v, src_bytes) ||
                  overlaps(dst_v, dst_bytes, src_k, src_bytes) || overlaps(dst_v, dst_bytes, src_v, src_bytes))))
         return fail(MOT_ERR_BAD_SHAPE, "destination caches overlap each other or the source caches");
+    const size_t usage_bytes = (size_t)s->L_tgt * (two ? 2 : 1) * s->E * 4;
+    if (s->usage && (overlaps(s->usage, usage_bytes, dst_k, dst_bytes) ||
+                     (two && overlaps(s->usage, usage_bytes, dst_v, dst_bytes))))
+        return fail(MOT_ERR_BAD_SHAPE, "usage overlaps a destination cache");
 
     // workspace
     int group = default_group(pl);
@@ -365,6 +372,24 @@ mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* la
             }
         }
     }
+    if (e != hipSuccess) return fail(MOT_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
+    return MOT_OK;
+}
+
+mot_status mot_usage_stats(const uint32_t* counts, int32_t n, int32_t E, double* cv2, double* entropy,
+                           hipStream_t stream) {
+    g_err[0] = 0;
+    if (n < 0 || E < 1 || E > MOT_MAX_EXPERTS)
+        return fail(MOT_ERR_BAD_SHAPE, "n=%d E=%d: need n >= 0 and 1 <= E <= %d", n, E, MOT_MAX_EXPERTS);
+    if (n == 0) return MOT_OK;
+    if (!counts || !cv2 || !entropy) return fail(MOT_ERR_NULL_ARG, "counts, cv2 and entropy are required");
+    if ((reinterpret_cast<uintptr_t>(counts) & 3) || (reinterpret_cast<uintptr_t>(cv2) & 7) ||
+        (reinterpret_cast<uintptr_t>(entropy) & 7))
+        return fail(MOT_ERR_MISALIGNED, "counts must be 4-byte, cv2 and entropy 8-byte aligned");
+    const size_t cb = (size_t)n * E * 4, ob = (size_t)n * 8;
+    if (overlaps(counts, cb, cv2, ob) || overlaps(counts, cb, entropy, ob) || overlaps(cv2, ob, entropy, ob))
+        return fail(MOT_ERR_BAD_SHAPE, "counts, cv2 and entropy overlap");
+    hipError_t e = launch_usage_stats(counts, n, E, cv2, entropy, stream);
     if (e != hipSuccess) return fail(MOT_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
     return MOT_OK;
 }
@@ -493,15 +518,32 @@ mot_status mot_replay_attention(const void* q, const void* k, const void* v, con
     p.q = q; p.k = k; p.v = v; p.idx = idx; p.o = o; p.vt = nullptr;
     p.B = s->B; p.T = s->T; p.H_q = s->H_q; p.H_kv = s->H_kv; p.D = s->D; p.S = idx ? s->S : 0;
     p.kv_layout = s->kv_layout;
-    if (!idx) {   // the full causal path stages V transposed through the library's buffer
-        void* ws = nullptr;
-        st = owned_workspace(replay_vt_bytes(s->B, s->T, s->H_kv, s->D), &ws);
-        if (st != MOT_OK) return st;
+    if (!idx) {   // the full causal path stages V transposed through scratch
+        const size_t need = replay_vt_bytes(s->B, s->T, s->H_kv, s->D);
+        void* ws = s->workspace;
+        if (ws) {
+            if (!aligned16(ws)) return fail(MOT_ERR_MISALIGNED, "workspace %p is not 16-byte aligned", ws);
+            if (s->workspace_bytes < need)
+                return fail(MOT_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes, need %zu", s->workspace_bytes,
+                            need);
+            if (overlaps(ws, need, q, qo) || overlaps(ws, need, k, kv) || overlaps(ws, need, v, kv) ||
+                overlaps(ws, need, o, qo))
+                return fail(MOT_ERR_BAD_SHAPE, "workspace overlaps q, k, v or o");
+        } else {
+            st = owned_workspace(need, &ws);
+            if (st != MOT_OK) return st;
+        }
         p.vt = reinterpret_cast<uint16_t*>(ws);
     }
     hipError_t e = launch_replay_attention(p, stream);
     if (e != hipSuccess) return fail(MOT_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
     return MOT_OK;
+}
+
+size_t mot_replay_workspace_bytes(const mot_replay_shapes* s, int with_sets) {
+    g_err[0] = 0;
+    if (check_replay(s, with_sets != 0) != MOT_OK) return SIZE_MAX;
+    return with_sets ? 0 : replay_vt_bytes(s->B, s->T, s->H_kv, s->D);
 }
 
 size_t mot_backbone_param_count(const mot_shapes* s, const mot_backbone_dims* bd) {
@@ -510,10 +552,30 @@ size_t mot_backbone_param_count(const mot_shapes* s, const mot_backbone_dims* bd
     return backbone_offsets((size_t)s->H_src * s->D_src, bd->d_h, bd->d_ff, (size_t)s->H_tgt * s->D_tgt).total;
 }
 
-mot_status mot_backbone_translate(const void* src_k, const void* src_v, const int32_t* layer_map, const void* params,
-                                  const mot_router_weights* rw, void* dst_k, void* dst_v, const mot_shapes* s,
-                                  const mot_backbone_dims* bd, hipStream_t stream) {
-    g_err[0] = 0;
+namespace {
+// Workspace of the backbone call: gates of every unit, then one unit's
+// activation rows (LayerNorm outputs, z, Q, K, V, attention, h1, FFN, h2, the
+// fp32 mixture), then the attention's transposed V.
+struct BackboneScratch {
+    size_t at[14];
+    size_t at_vt;
+    size_t total;
+};
+BackboneScratch backbone_scratch(const mot_shapes* s, const mot_backbone_dims* bd, int n_units) {
+    const size_t n = (size_t)s->B * s->T, d_in = (size_t)s->H_src * s->D_src, d_out = (size_t)s->H_tgt * s->D_tgt;
+    const size_t d_h = bd->d_h, d_ff = bd->d_ff;
+    const size_t row_b[14] = {d_in * 2, d_h * 2, d_h * 2, d_h * 2, d_h * 2, d_h * 2, d_h * 2,
+                              d_h * 2,  d_h * 2, d_h * 2, d_ff * 2, d_h * 2, d_h * 2, d_out * 4};
+    BackboneScratch b;
+    size_t need = round_up((size_t)n_units * round_up(n, 128) * s->E * 4, kAlign);
+    for (int k = 0; k < 14; ++k) { b.at[k] = need; need += round_up(n * row_b[k], kAlign); }
+    b.at_vt = need;
+    need += round_up(replay_vt_bytes(s->B, s->T, bd->n_heads, bd->d_h / bd->n_heads), kAlign);
+    b.total = need;
+    return b;
+}
+
+mot_status check_backbone(const mot_shapes* s, const mot_backbone_dims* bd) {
     mot_status st = check_shapes(s);
     if (st != MOT_OK) return st;
     if (!bd) return fail(MOT_ERR_NULL_ARG, "backbone dims are NULL");
@@ -531,6 +593,25 @@ mot_status mot_backbone_translate(const void* src_k, const void* src_v, const in
         return fail(MOT_ERR_UNSUPPORTED, "backbone sizes: d_in, d_h multiples of 64 up to 4096, d_ff a multiple of "
                     "64, d_out of 8, head width d_h / n_heads 64 or 128 (got d_in=%d d_h=%d n_heads=%d d_ff=%d "
                     "d_out=%d)", d_in, d_h, nh, d_ff, d_out);
+    return MOT_OK;
+}
+}  // namespace
+
+size_t mot_backbone_workspace_bytes(const mot_shapes* s, const mot_backbone_dims* bd) {
+    g_err[0] = 0;
+    if (check_backbone(s, bd) != MOT_OK) return SIZE_MAX;
+    if ((int64_t)s->B * s->T == 0) return 0;
+    return backbone_scratch(s, bd, 2 * s->L_tgt).total;
+}
+
+mot_status mot_backbone_translate(const void* src_k, const void* src_v, const int32_t* layer_map, const void* params,
+                                  const mot_router_weights* rw, void* dst_k, void* dst_v, const mot_shapes* s,
+                                  const mot_backbone_dims* bd, hipStream_t stream) {
+    g_err[0] = 0;
+    mot_status st = check_backbone(s, bd);
+    if (st != MOT_OK) return st;
+    const int d_in = s->H_src * s->D_src, d_out = s->H_tgt * s->D_tgt, d_h = bd->d_h, nh = bd->n_heads,
+              d_ff = bd->d_ff;
     if ((int64_t)s->B * s->T == 0) return MOT_OK;
     if (!src_k || !src_v || !layer_map || !params || !rw || !rw->w || !dst_k || !dst_v)
         return fail(MOT_ERR_NULL_ARG, "a required argument is NULL");
@@ -541,6 +622,8 @@ mot_status mot_backbone_translate(const void* src_k, const void* src_v, const in
     for (const void* q : dev_ptrs)
         if (!aligned16(q)) return fail(MOT_ERR_MISALIGNED, "device pointer %p is not 16-byte aligned", q);
     if (rw->b && (reinterpret_cast<uintptr_t>(rw->b) & 1)) return fail(MOT_ERR_MISALIGNED, "router bias misaligned");
+    if (s->usage && (reinterpret_cast<uintptr_t>(s->usage) & 3))
+        return fail(MOT_ERR_MISALIGNED, "usage %p is not 4-byte aligned", (void*)s->usage);
     const size_t n = (size_t)s->B * s->T;
     const size_t dst_bytes = (size_t)s->L_tgt * n * d_out * 2, src_bytes = (size_t)s->L_src * n * d_in * 2;
     if (overlaps(dst_k, dst_bytes, dst_v, dst_bytes) || overlaps(dst_k, dst_bytes, src_k, src_bytes) ||
@@ -557,19 +640,24 @@ mot_status mot_backbone_translate(const void* src_k, const void* src_v, const in
             for (int x = 0; x < 2; ++x) { ut.code[nu] = unit_code(j, x, layer_map[j], nu); ++nu; }
     ut.n = nu;
     if (nu == 0) return MOT_OK;
-    // workspace: gates, then one unit's activations
-    const size_t gates_b = round_up((size_t)nu * p.n_tok_pad * s->E * 4, kAlign);
-    const size_t row_b[] = {(size_t)d_in * 2, (size_t)d_h * 2, (size_t)d_h * 2, (size_t)d_h * 2, (size_t)d_h * 2,
-                            (size_t)d_h * 2, (size_t)d_h * 2, (size_t)d_h * 2, (size_t)d_h * 2, (size_t)d_h * 2,
-                            (size_t)d_ff * 2, (size_t)d_h * 2, (size_t)d_h * 2, (size_t)d_out * 4};
-    constexpr int NB = sizeof(row_b) / sizeof(row_b[0]);
-    size_t need = gates_b, at[NB];
-    for (int k = 0; k < NB; ++k) { at[k] = need; need += round_up(n * row_b[k], kAlign); }
-    const size_t at_vt = need;   // V transposed for the attention
-    need += round_up(replay_vt_bytes(s->B, s->T, nh, d_h / nh), kAlign);
-    void* ws = nullptr;
-    st = owned_workspace(need, &ws);
-    if (st != MOT_OK) return st;
+    // workspace: gates, then one unit's activations, then V transposed
+    const BackboneScratch sc = backbone_scratch(s, bd, nu);
+    const size_t* at = sc.at;
+    const size_t at_vt = sc.at_vt;
+    void* ws = s->workspace;
+    if (ws) {
+        const size_t need_all = backbone_scratch(s, bd, 2 * s->L_tgt).total;
+        if (!aligned16(ws)) return fail(MOT_ERR_MISALIGNED, "workspace %p is not 16-byte aligned", ws);
+        if (s->workspace_bytes < sc.total)
+            return fail(MOT_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes, need %zu (%zu for every layer mapped)",
+                        s->workspace_bytes, sc.total, need_all);
+        if (overlaps(ws, sc.total, dst_k, dst_bytes) || overlaps(ws, sc.total, dst_v, dst_bytes) ||
+            overlaps(ws, sc.total, src_k, src_bytes) || overlaps(ws, sc.total, src_v, src_bytes))
+            return fail(MOT_ERR_BAD_SHAPE, "workspace overlaps a source or destination cache");
+    } else {
+        st = owned_workspace(sc.total, &ws);
+        if (st != MOT_OK) return st;
+    }
     char* w8 = reinterpret_cast<char*>(ws);
     uint16_t* xn = reinterpret_cast<uint16_t*>(w8 + at[0]);
     uint16_t* z = reinterpret_cast<uint16_t*>(w8 + at[1]);

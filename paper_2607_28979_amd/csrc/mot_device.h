@@ -46,10 +46,10 @@ __device__ __forceinline__ f32x4 mfma_16x16x32(u32x4 a, u32x4 b, f32x4 c) {
 // over the selected set; the others become zero).  K rounds each take the
 // largest score not yet taken; the scan is ascending with a strict '>', so
 // ties go to the lower index.  K >= E keeps every score unchanged (the dense
-// mixture).
+// mixture).  Returns the selected set as a bit mask (bit m = translator m).
 template <int EMAX>
-__device__ __forceinline__ void topk_renormalise(float (&g)[EMAX], int E, int K) {
-    if (K >= E) return;
+__device__ __forceinline__ uint32_t topk_renormalise(float (&g)[EMAX], int E, int K) {
+    if (K >= E) return E >= 32 ? 0xFFFFFFFFu : (1u << E) - 1u;
     uint32_t taken = 0;
     float sum = 0.f;
     for (int k = 0; k < K; ++k) {
@@ -68,6 +68,18 @@ __device__ __forceinline__ void topk_renormalise(float (&g)[EMAX], int E, int K)
     const float inv = 1.0f / sum;
 #pragma unroll
     for (int m = 0; m < EMAX; ++m) g[m] = ((taken >> m) & 1u) ? g[m] * inv : 0.f;
+    return taken;
+}
+
+// Translator usage: add, for every translator m < E, the number of lanes of
+// the wave whose selected set `taken` holds m (lanes with valid == false
+// add nothing) to usage[m].  Called by every lane of the wave.
+__device__ __forceinline__ void count_usage(uint32_t* usage, int E, uint32_t taken, bool valid) {
+    const int lane = threadIdx.x & 63;
+    for (int m = 0; m < E; ++m) {
+        const unsigned long long b = __ballot(valid && ((taken >> m) & 1u));
+        if (lane == 0 && b) atomicAdd(usage + m, (uint32_t)__popcll(b));
+    }
 }
 
 // The same Top-K as topk_renormalise, emitted as a list: sel[k], gk[k] for

@@ -58,6 +58,7 @@ struct Problem {
     int32_t d_in, d_out, n_tok, n_tok_pad;   // n_tok_pad: n_tok rounded up to 128
     int32_t src_layout, dst_layout, act;
     int32_t streams;      // 2: keys and values; 1: one activation stream (src[0] -> dst[0])
+    uint32_t* usage;      // [L_tgt][streams][E] selection counts to add to, or null
     float* gates;         // workspace: [n_units_total][n_tok_pad][E] fp32
     void* hbuf;           // workspace: [group][n_tok_pad][E*hidden] (layout per path)
     Routing rt;           // routed path only
@@ -153,6 +154,8 @@ hipError_t launch_bf16_fused(const Problem& p, const UnitTab& ut, hipStream_t st
 // combine of the top_k per-assignment rows of every token.
 int fused_tile_rows(const Problem& p);
 hipError_t launch_router_lists(const Problem& p, const UnitTab& ut, hipStream_t stream);
+hipError_t launch_usage_stats(const uint32_t* counts, int n, int E, double* cv2, double* entropy,
+                              hipStream_t stream);
 hipError_t launch_route_plan(const Problem& p, const UnitTab& ut, hipStream_t stream);
 hipError_t launch_bf16_fused_routed(const Problem& p, const UnitTab& ut, hipStream_t stream);
 hipError_t launch_routed_combine(const Problem& p, const UnitTab& ut, hipStream_t stream);

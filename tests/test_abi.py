@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert mb.abi_version() == 4
+    assert mb.abi_version() == 5
 
 
 def test_status_strings(lib):
@@ -346,3 +346,43 @@ def test_replay_set_sizes_and_swizzle(lib, tmp_path):
     for S in (96, 160, 192, 224):
         sc = S // 8
         assert any(sorted(c ^ (d & (sc - 1)) for c in range(sc)) != list(range(sc)) for d in range(64))
+
+
+def test_workspace_size_queries(lib):
+    """mot_replay_workspace_bytes: the V staging of the full causal path
+    (B * H_kv * D * T rounded up to 64, bf16), 0 with key sets, SIZE_MAX for
+    unsupported shapes; mot_backbone_workspace_bytes is positive for valid
+    backbone shapes and SIZE_MAX otherwise."""
+    assert mb.replay_workspace_bytes(2, 100, 8, 2, 128) == 2 * 2 * 128 * 128 * 2
+    assert mb.replay_workspace_bytes(1, 64, 4, 4, 64, S=32, with_sets=True) == 0
+    with pytest.raises(mb.MotError):
+        mb.replay_workspace_bytes(1, 64, 4, 4, 96)
+    s = _shapes(H_tgt=2, D_tgt=64, T=70)
+    n = mb.backbone_workspace_bytes(s, 128, 2, 256)
+    assert n > 70 * (64 * 2 + 128 * 2 * 9 + 256 * 2 + 128 * 4)   # B = 1: every activation row once
+    with pytest.raises(mb.MotError):
+        mb.backbone_workspace_bytes(s, 96, 2, 256)
+
+
+def test_usage_argument_checks(lib):
+    """mot_usage_stats rejects E outside 1..MOT_MAX_EXPERTS, NULL and
+    misaligned buffers before any launch; n = 0 is a no-op.  mot_translate
+    rejects a usage array that is not 4-byte aligned or overlaps a
+    destination cache."""
+    L = mb.load_library()
+    c8, d8 = FAKE, FAKE + (1 << 30)
+    assert mb.STATUS[L.mot_usage_stats(None, 0, 4, None, None, None)] == "MOT_OK"
+    for n, E, a, b, c, code in ((3, 0, c8, d8, d8 + 64, "MOT_ERR_BAD_SHAPE"),
+                                (3, 17, c8, d8, d8 + 64, "MOT_ERR_BAD_SHAPE"),
+                                (3, 4, None, d8, d8 + 64, "MOT_ERR_NULL_ARG"),
+                                (3, 4, c8 + 2, d8, d8 + 64, "MOT_ERR_MISALIGNED"),
+                                (3, 4, c8, d8 + 4, d8 + 64, "MOT_ERR_MISALIGNED"),
+                                (3, 4, c8, d8, d8 + 8, "MOT_ERR_BAD_SHAPE")):
+        assert mb.STATUS[L.mot_usage_stats(a, n, E, b, c, None)] == code, (n, E, code)
+    s = _shapes(top_k=2)
+    lm = np.array([0, 1], np.int32)
+    for usage, code in ((FAKE + (7 << 30) + 2, "MOT_ERR_MISALIGNED"), (FAKE + (5 << 30), "MOT_ERR_BAD_SHAPE")):
+        with pytest.raises(mb.MotError) as e:
+            mb.translate_raw(FAKE, FAKE + (1 << 30), lm, FAKE + (2 << 30), None, FAKE + (3 << 30), None,
+                             FAKE + (4 << 30), None, FAKE + (5 << 30), FAKE + (6 << 30), s, usage=usage)
+        assert e.value.name == code

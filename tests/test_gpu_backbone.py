@@ -35,14 +35,14 @@ CASES = [  # workload, d_h, n_heads, d_ff
 ]
 
 
-def _run(w, d_h, nh, d_ff, lm, params, inp):
+def _run(w, d_h, nh, d_ff, lm, params, inp, workspace=None):
     import torch
     dev = {n: to_dev(getattr(inp, n), "bf16") for n in ("src_k", "src_v", "wr", "br")}
     pr = to_dev(params, "bf16")
     dk = torch.full(dst_shape(w), SENTINEL, dtype=torch.bfloat16, device="cuda")
     dv = torch.full(dst_shape(w), SENTINEL, dtype=torch.bfloat16, device="cuda")
     mb.backbone_translate(dev["src_k"], dev["src_v"], lm, pr, dev["wr"], dev["br"], dk, dv,
-                          mb.Shapes.from_workload(w), d_h, nh, d_ff)
+                          mb.Shapes.from_workload(w), d_h, nh, d_ff, workspace=workspace)
     torch.cuda.synchronize()
     return (dk.float().cpu().numpy().astype(np.float64), dv.float().cpu().numpy().astype(np.float64))
 
@@ -74,3 +74,23 @@ def test_backbone_parity(case, oracle_built):
     # every row runs a chain of seven bf16 stages (three LayerNorms, attention),
     # so single rows get twice the unit bar, as replay positions do
     assert worst_row <= 2 * TOL["bf16"]
+
+
+def test_backbone_caller_workspace_equals_owned():
+    """A caller-owned workspace of mot_backbone_workspace_bytes gives the
+    same bits as the library's own buffer; a smaller one is refused before
+    anything runs (the destination keeps its sentinel)."""
+    import torch
+    w, d_h, nh, d_ff = CASES[0]
+    inp = generate(w)
+    params = backbone_params(w, d_h, d_ff, seed=w.seed)
+    lm = np.arange(w.L_tgt, dtype=np.int32)
+    need = mb.backbone_workspace_bytes(mb.Shapes.from_workload(w), d_h, nh, d_ff)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    ws.fill_(0xA5)
+    a = _run(w, d_h, nh, d_ff, lm, params, inp)
+    b = _run(w, d_h, nh, d_ff, lm, params, inp, workspace=ws)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    with pytest.raises(mb.MotError) as e:
+        _run(w, d_h, nh, d_ff, lm, params, inp, workspace=ws[: need - 256])
+    assert e.value.name == "MOT_ERR_WORKSPACE_TOO_SMALL"

@@ -193,3 +193,28 @@ def test_replay_layer_full_size_sampled(oracle_built):
     want_c = oracle_replay_attention_rows(q, k, v, None, rows_c)
     for i, (b, u) in enumerate(rows_c):
         assert rel_frob(got_c[b, u], want_c[i]) <= TOL["bf16"], u
+
+
+def test_causal_caller_workspace_equals_owned(oracle_built):
+    """The full causal path with a caller-owned workspace (the V staging of
+    mot_replay_workspace_bytes) gives the same bits as with the library's
+    own buffer, and a smaller workspace is refused before any launch."""
+    import torch
+    B, T, Hq, Hkv, D = 2, 333, 8, 2, 128
+    q, k, v = replay_inputs(B, T, Hq, Hkv, D, seed=5, kv_layout=0)
+    dq, dk, dv = (to_dev(a, "bf16") for a in (q, k, v))
+    need = mb.replay_workspace_bytes(B, T, Hq, Hkv, D)
+    assert need == B * Hkv * D * ((T + 63) // 64 * 64) * 2
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    ws.fill_(0x5A)
+    outs = []
+    for wsp in (None, ws):
+        o = torch.zeros((B, T, Hq, D), dtype=torch.bfloat16, device="cuda")
+        mb.replay_attention(dq, dk, dv, None, o, B, T, Hq, Hkv, D, workspace=wsp)
+        torch.cuda.synchronize()
+        outs.append(o.cpu())
+    assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
+    o = torch.zeros((B, T, Hq, D), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(mb.MotError) as e:
+        mb.replay_attention(dq, dk, dv, None, o, B, T, Hq, Hkv, D, workspace=ws[: need - 16])
+    assert e.value.name == "MOT_ERR_WORKSPACE_TOO_SMALL"

@@ -1,0 +1,168 @@
+"""GPU parity of the translator-usage side output (paper Sec. 4, paragraph
+"MoT Architecture Ablation": I_m = the cumulative Top-K selection count of
+translator m; CV^2 and entropy of the counts) on every kernel path.
+
+The counts are integers decided by floating point (the Top-K selection).
+Rows whose K-th and (K+1)-th scores are more than 1e-3 apart have one valid
+set, and there the counts must agree exactly.  A near-tie row may take any of
+its admissible sets (the GPU scores are fp32, the oracle's double), so the
+GPU counts must equal the oracle counts plus, for some choice among those
+sets, the change each near-tie row's choice makes."""
+import numpy as np
+import pytest
+
+from paper_2607_28979_amd import binding as mb
+from paper_2607_28979_amd.configs import WORKLOADS, small_variant
+from paper_2607_28979_amd.inputs import generate
+
+from helpers import admissible_sets, oracle_dims, to_dev, topk_margin, unit_logits, dst_shape
+
+pytestmark = pytest.mark.gpu
+
+
+def _lm(w):
+    if w.layer_map == "identity":
+        return np.arange(w.L_tgt, dtype=np.int32) % w.L_src
+    return mb.depth_ratio_map(w.L_src, w.L_tgt)
+
+
+def _gpu_counts(w, inp, lm, algo, init, calls=1):
+    import torch
+    tdt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    d = {n: to_dev(getattr(inp, n), w.dtype) for n in ("src_k", "src_v", "w1", "b1", "w2", "b2", "wr", "br")}
+    dk = torch.zeros(dst_shape(w), dtype=tdt, device="cuda")
+    dv = torch.zeros(dst_shape(w), dtype=tdt, device="cuda")
+    usage = torch.from_numpy(init.astype(np.int32)).cuda()
+    shapes = mb.Shapes.from_workload(w, algo=algo)
+    for _ in range(calls):
+        mb.translate(d["src_k"], d["src_v"], lm, d["w1"], d["b1"], d["w2"], d["b2"], d["wr"], d["br"], dk, dv,
+                     shapes, usage=usage)
+    torch.cuda.synchronize()
+    return usage.cpu().numpy().astype(np.int64)
+
+
+def _check_counts(w, inp, lm, got):
+    """got: [L_tgt][2][E] counts of one call.  Exact on clear rows; near-tie
+    rows may move a count between the translators of their admissible sets."""
+    from oracle import oracle_rows, oracle_usage
+    want = oracle_usage(oracle_dims(w), inp.src_k, inp.src_v, lm, inp.wr, inp.br)
+    K, n_tie_all = w.top_k or w.E, 0
+    for j in range(w.L_tgt):
+        for x in range(2):
+            if lm[j] < 0:
+                assert (got[j, x] == 0).all()
+                continue
+            assert got[j, x].sum() == K * w.n_tok
+            lg = unit_logits(w, inp, lm, j, x)
+            ties = np.nonzero(topk_margin(lg, K) < 1e-3)[0]
+            n_tie_all += len(ties)
+            if len(ties) == 0:
+                assert np.array_equal(got[j, x], want[j, x]), (j, x, got[j, x], want[j, x])
+                continue
+            # the oracle's own set of each near-tie row, then the reachable changes
+            _, gates = oracle_rows(oracle_dims(w), inp.src_k, inp.src_v, lm, inp.w1, inp.b1, inp.w2, inp.b2,
+                                   inp.wr, inp.br, units=[(j, x)], rows=ties, want_gates=True)
+            reach = {tuple([0] * w.E)}
+            for r, row in enumerate(ties):
+                own = np.zeros(w.E, np.int64)
+                own[gates[0, r] > 0] = 1
+                steps = []
+                for s in admissible_sets(lg[row], K):
+                    alt = np.zeros(w.E, np.int64)
+                    alt[list(s)] = 1
+                    steps.append(alt - own)
+                reach = {tuple(np.array(v) + st) for v in reach for st in steps}
+                assert len(reach) < 200000
+            assert tuple(got[j, x] - want[j, x]) in reach, (j, x, got[j, x], want[j, x], len(ties))
+    return n_tie_all
+
+
+SMALL = [
+    small_variant(WORKLOADS[0], L_src=3, L_tgt=3),                     # fp32, E = 2
+    small_variant(WORKLOADS[1], L_src=2, L_tgt=3, B=2, T=150),         # E = 4, fused shape 128 -> 128
+    small_variant(WORKLOADS[2], L_src=3, L_tgt=4, B=1, T=200),         # E = 4, two-GEMM only
+    small_variant(WORKLOADS[3], L_src=2, L_tgt=2, B=1, T=300),         # E = 8, the headline shape
+]
+CASES = []
+for w in SMALL:
+    paths = ([mb.ALGO_AUTO] if w.dtype == "f32" else
+             [mb.ALGO_FUSED, mb.ALGO_ROUTED, mb.ALGO_UNFUSED] if w.d_in in (128, 256, 512) and w.d_out in (128, 256, 512)
+             else [mb.ALGO_UNFUSED])
+    for k in sorted({1, 2, w.E}):
+        for a in paths:
+            if not (a == mb.ALGO_ROUTED and k == w.E):
+                CASES.append((w, k, a))
+
+
+@pytest.mark.parametrize("w,k,algo", CASES, ids=["%s-top%d-algo%d" % (w.name, k, a) for w, k, a in CASES])
+def test_usage_counts(w, k, algo, oracle_built):
+    """Counts of one call against the oracle, and accumulation: a second call
+    adds the same counts, and rows of unmapped layers keep their contents."""
+    w = w.with_(top_k=k)
+    print("case", w.name, "top_k", k, "algo", algo, flush=True)
+    inp = generate(w)
+    lm = _lm(w).copy()
+    if w.L_tgt >= 3:
+        lm[1] = -1
+    rng = np.random.default_rng(7)
+    init = rng.integers(0, 1000, (w.L_tgt, 2, w.E))
+    got2 = _gpu_counts(w, inp, lm, algo, init, calls=2) - init
+    one = got2 // 2
+    assert np.array_equal(got2, 2 * one)
+    n_tie = _check_counts(w, inp, lm, one)
+    print("  counts exact on clear rows; %d near-tie rows within their admissible sets" % n_tie, flush=True)
+
+
+def test_usage_counts_full_size_routed(oracle_built):
+    """The routed Top-1 launch of `bench.py --top-k 1` on the Qwen2.5-1.5B ->
+    7B caches at full size (32768 tokens, 56 units): every count within the
+    near-tie slack of the oracle's, exact where a unit has no near-tie row."""
+    from oracle import oracle_usage
+    w = WORKLOADS[3].with_(top_k=1)
+    print("case", w.name, "top_k 1 full size routed", flush=True)
+    inp = generate(w)
+    lm = _lm(w)
+    got = _gpu_counts(w, inp, lm, mb.ALGO_AUTO, np.zeros((w.L_tgt, 2, w.E), np.int64))
+    want = oracle_usage(oracle_dims(w), inp.src_k, inp.src_v, lm, inp.wr, inp.br)
+    exact = 0
+    for j in range(w.L_tgt):
+        for x in range(2):
+            lg = unit_logits(w, inp, lm, j, x)
+            ties = np.nonzero(topk_margin(lg, 1) < 1e-3)[0]
+            slack = np.zeros(w.E, np.int64)
+            for row in ties:
+                for s in admissible_sets(lg[row], 1):
+                    slack[list(s)] += 1
+            assert got[j, x].sum() == w.n_tok
+            assert (np.abs(got[j, x] - want[j, x]) <= slack).all(), (j, x)
+            exact += int(len(ties) == 0 and np.array_equal(got[j, x], want[j, x]))
+    print("  %d of 56 units without near-tie rows, all exact" % exact, flush=True)
+
+
+def test_usage_stats_kernel(oracle_built):
+    """mot_usage_stats against the oracle's statistics, to double rounding:
+    random counts, balanced rows (CV^2 = 0, entropy ln E), one-hot rows
+    (CV^2 = E - 1, entropy 0) and a row of zeros (NaN)."""
+    import torch
+    from oracle import oracle_usage_stats
+    rng = np.random.default_rng(11)
+    for E in (1, 2, 4, 8, 16):
+        c = rng.integers(0, 50000, (37, E))
+        c[0] = 1234
+        c[1] = 0
+        c[1, E - 1] = 99
+        c[2] = 0
+        counts = torch.from_numpy(c.astype(np.int32)).cuda()
+        cv2 = torch.empty(37, dtype=torch.float64, device="cuda")
+        ent = torch.empty(37, dtype=torch.float64, device="cuda")
+        mb.usage_stats(counts, cv2, ent)
+        torch.cuda.synchronize()
+        cv2, ent = cv2.cpu().numpy(), ent.cpu().numpy()
+        for r in range(37):
+            wc, we = oracle_usage_stats(c[r])
+            if r == 2:
+                assert np.isnan(cv2[r]) and np.isnan(ent[r])
+                continue
+            assert abs(cv2[r] - wc) <= 1e-12 * max(1.0, wc) and abs(ent[r] - we) <= 1e-12, (E, r)
+        assert cv2[0] == 0.0 and abs(ent[0] - np.log(E)) < 1e-12
+        assert abs(cv2[1] - (E - 1)) < 1e-12 and ent[1] == 0.0

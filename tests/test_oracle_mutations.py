@@ -14,6 +14,7 @@ SRC = os.path.join(ROOT, "oracle", "mot_oracle.c")
 
 PINS = "tests/test_oracle_pins.py"
 HAND = "tests/test_oracle_handworked.py"
+USAGE = "tests/test_oracle_usage.py"
 
 # (name, original text, planted text, pins that must catch it); the original
 # text must occur in the source, and its first occurrence is replaced
@@ -41,6 +42,13 @@ MUTATIONS = [
      "            for (int32_t c = 0; c < d_in; ++c) acc += (double)w1[c] * z[c];",
      "const float* w1 = w->w1 + em * Hd * d_in + k;\n            double acc = 0.0;\n"
      "            for (int32_t c = 0; c < d_in; ++c) acc += (double)w1[(size_t)c * Hd] * z[c];", [PINS]),
+    ("usage CV^2 with the sample variance", "    var /= E;\n", "    var /= (E - 1);\n", [USAGE]),
+    ("usage entropy in bits", "h -= p * log(p);", "h -= p * log2(p);", [USAGE]),
+    ("usage counts ties to the higher index", "if (!sel[m] && (best < 0 || g[m] > g[best])) best = m;\n"
+     "                        sel[best] = 1;\n                    }\n                    for (int32_t m = 0; m < E; ++m) counts",
+     "if (!sel[m] && (best < 0 || g[m] >= g[best])) best = m;\n"
+     "                        sel[best] = 1;\n                    }\n                    for (int32_t m = 0; m < E; ++m) counts",
+     [USAGE]),
 ]
 
 
