@@ -278,6 +278,23 @@ typedef struct {
     size_t workspace_bytes;
 } mot_replay_shapes;
 
+/*
+ * mot_replay_attention for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same operation, arguments and checks, but the full causal
+ * path (idx = NULL) stages V in a static 32 MiB array that the library holds
+ * on each device it runs on until the process ends, instead of a workspace
+ * or a library-allocated buffer; it calls no hipMalloc, hipFree or
+ * allocating routine.  shapes->workspace and workspace_bytes are ignored.
+ * Shapes whose staged V (mot_replay_workspace_bytes) exceeds 32 MiB return
+ * MOT_ERR_WORKSPACE_TOO_SMALL before anything is launched.  All calls on one
+ * device share that array (its contents after a call are unspecified): calls
+ * that overlap in time on one device race.  With key sets (idx != NULL) no
+ * scratch is used.
+ */
+mot_status mot_replay_attention_noalloc(const void* q, const void* k, const void* v, const int32_t* idx, void* o,
+                                        const mot_replay_shapes* shapes, hipStream_t stream);
+
 /* Scratch bytes mot_replay_attention needs for `shapes` with idx = NULL (V
  * staged transposed: B * H_kv * D * T rounded up to 64, bf16); 0 with key
  * sets; SIZE_MAX for invalid or unsupported shapes. */

@@ -27,7 +27,8 @@ STATUS = {0: "MOT_OK", 1: "MOT_ERR_NULL_ARG", 2: "MOT_ERR_BAD_SHAPE", 3: "MOT_ER
 EXPORTED = ("mot_translate", "mot_workspace_bytes", "mot_depth_ratio_map", "mot_status_string",
             "mot_last_error", "mot_abi_version", "mot_restore_kv", "mot_topS_select",
             "mot_replay_attention", "mot_backbone_param_count", "mot_backbone_translate",
-            "mot_usage_stats", "mot_replay_workspace_bytes", "mot_backbone_workspace_bytes")
+            "mot_usage_stats", "mot_replay_workspace_bytes", "mot_backbone_workspace_bytes",
+            "mot_replay_attention_noalloc")
 
 
 class MotError(RuntimeError):
@@ -169,9 +170,9 @@ def load_library():
         lib.mot_usage_stats.restype = ctypes.c_int
         lib.mot_usage_stats.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                         ctypes.c_void_p, ctypes.c_void_p]
-        lib.mot_replay_attention.restype = ctypes.c_int
-        lib.mot_replay_attention.argtypes = [ctypes.c_void_p] * 5 + [ctypes.POINTER(_ReplayShapes),
-                                                                     ctypes.c_void_p]
+        for fn in (lib.mot_replay_attention, lib.mot_replay_attention_noalloc):
+            fn.restype = ctypes.c_int
+            fn.argtypes = [ctypes.c_void_p] * 5 + [ctypes.POINTER(_ReplayShapes), ctypes.c_void_p]
         _lib = lib
     return _lib
 
@@ -327,6 +328,23 @@ def replay_attention(q, k, v, idx, o, B: int, T: int, H_q: int, H_kv: int, D: in
                       workspace.numel() * workspace.element_size() if workspace is not None else 0)
     _check(lib.mot_replay_attention(_ptr(q), _ptr(k), _ptr(v), _ptr(idx), _ptr(o), ctypes.byref(c),
                                     torch.cuda.current_stream().cuda_stream))
+
+
+def replay_attention_noalloc(q, k, v, idx, o, B: int, T: int, H_q: int, H_kv: int, D: int, S: int = 0,
+                             kv_layout: int = LAYOUT_BTHD) -> None:
+    """mot_replay_attention_noalloc on the current torch stream: the same
+    operation as replay_attention, with the full causal path's staging in the
+    library's static per-device scratch (no allocation)."""
+    import torch
+    lib = load_library()
+    for name, t in (("q", q), ("k", k), ("v", v), ("o", o)):
+        if t.dtype != torch.bfloat16 or not t.is_contiguous():
+            raise MotError(2, "%s must be a contiguous bfloat16 tensor" % name)
+    if idx is not None and (idx.dtype != torch.int32 or not idx.is_contiguous()):
+        raise MotError(2, "idx must be a contiguous int32 tensor")
+    c = _ReplayShapes(B, T, H_q, H_kv, D, S if idx is not None else 0, kv_layout)
+    _check(lib.mot_replay_attention_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(idx), _ptr(o), ctypes.byref(c),
+                                            torch.cuda.current_stream().cuda_stream))
 
 
 def backbone_param_count(shapes: Shapes, d_h: int, n_heads: int, d_ff: int) -> int:

@@ -500,9 +500,55 @@ mot_status mot_topS_select(const float* A, int32_t* idx, const mot_replay_shapes
     return MOT_OK;
 }
 
+namespace {
+// Scratch of mot_replay_attention_noalloc: the full causal path's V staging
+// in a file-scope device array, so that entry point allocates nothing.
+// Every device that runs the library holds its own copy until the process
+// ends; host code reaches it only through the address hipGetSymbolAddress
+// returns for the current device (the array's name is a host stand-in).
+constexpr size_t kNoAllocScratchBytes = size_t(32) << 20;
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64];
+
+// Device address of `scratch` on the current device, looked up on the first
+// call per device (with that device current) and kept.
+mot_status noalloc_scratch(void** out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return fail(MOT_ERR_HIP, "hipGetDevice failed");
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr)
+            return fail(MOT_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return MOT_OK;
+}
+
+enum class ReplayScratch { Caller, Static };
+
+mot_status replay_attention_impl(const void* q, const void* k, const void* v, const int32_t* idx, void* o,
+                                 const mot_replay_shapes* s, hipStream_t stream, ReplayScratch mode);
+}  // namespace
+
 mot_status mot_replay_attention(const void* q, const void* k, const void* v, const int32_t* idx, void* o,
                                 const mot_replay_shapes* s, hipStream_t stream) {
     g_err[0] = 0;
+    return replay_attention_impl(q, k, v, idx, o, s, stream, ReplayScratch::Caller);
+}
+
+mot_status mot_replay_attention_noalloc(const void* q, const void* k, const void* v, const int32_t* idx, void* o,
+                                        const mot_replay_shapes* s, hipStream_t stream) {
+    g_err[0] = 0;
+    return replay_attention_impl(q, k, v, idx, o, s, stream, ReplayScratch::Static);
+}
+
+namespace {
+mot_status replay_attention_impl(const void* q, const void* k, const void* v, const int32_t* idx, void* o,
+                                 const mot_replay_shapes* s, hipStream_t stream, ReplayScratch mode) {
     mot_status st = check_replay(s, idx != nullptr);
     if (st != MOT_OK) return st;
     if ((int64_t)s->B * s->T == 0) return MOT_OK;
@@ -520,8 +566,16 @@ mot_status mot_replay_attention(const void* q, const void* k, const void* v, con
     p.kv_layout = s->kv_layout;
     if (!idx) {   // the full causal path stages V transposed through scratch
         const size_t need = replay_vt_bytes(s->B, s->T, s->H_kv, s->D);
-        void* ws = s->workspace;
-        if (ws) {
+        void* ws = mode == ReplayScratch::Caller ? s->workspace : nullptr;
+        if (mode == ReplayScratch::Static) {
+            // every position of the staged V is written before it is read
+            // (zero past T), so nothing has to be cleared between calls
+            if (need > kNoAllocScratchBytes)
+                return fail(MOT_ERR_WORKSPACE_TOO_SMALL, "the staged V needs %zu bytes; the static scratch holds %zu",
+                            need, kNoAllocScratchBytes);
+            st = noalloc_scratch(&ws);
+            if (st != MOT_OK) return st;
+        } else if (ws) {
             if (!aligned16(ws)) return fail(MOT_ERR_MISALIGNED, "workspace %p is not 16-byte aligned", ws);
             if (s->workspace_bytes < need)
                 return fail(MOT_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes, need %zu", s->workspace_bytes,
@@ -539,6 +593,7 @@ mot_status mot_replay_attention(const void* q, const void* k, const void* v, con
     if (e != hipSuccess) return fail(MOT_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
     return MOT_OK;
 }
+}  // namespace
 
 size_t mot_replay_workspace_bytes(const mot_replay_shapes* s, int with_sets) {
     g_err[0] = 0;

@@ -386,3 +386,18 @@ def test_usage_argument_checks(lib):
             mb.translate_raw(FAKE, FAKE + (1 << 30), lm, FAKE + (2 << 30), None, FAKE + (3 << 30), None,
                              FAKE + (4 << 30), None, FAKE + (5 << 30), FAKE + (6 << 30), s, usage=usage)
         assert e.value.name == code
+
+
+def test_noalloc_replay_rejects_oversized_staging(lib):
+    """mot_replay_attention_noalloc refuses a full causal call whose staged V
+    exceeds its 32 MiB static scratch (1 x 65536 positions x 4 KV heads of 128
+    = 64 MiB) with MOT_ERR_WORKSPACE_TOO_SMALL, before touching the device;
+    it applies the same argument checks as mot_replay_attention."""
+    L = mb.load_library()
+    big = mb._ReplayShapes(1, 65536, 8, 4, 128, 0, 0)
+    st = L.mot_replay_attention_noalloc(FAKE, FAKE + (1 << 34), FAKE + (2 << 34), None, FAKE + (3 << 34),
+                                        ctypes.byref(big), None)
+    assert mb.STATUS[st] == "MOT_ERR_WORKSPACE_TOO_SMALL", mb.load_library().mot_last_error()
+    bad = mb._ReplayShapes(1, 64, 8, 4, 96, 0, 0)
+    assert mb.STATUS[L.mot_replay_attention_noalloc(FAKE, FAKE, FAKE, None, FAKE, ctypes.byref(bad), None)] == \
+        "MOT_ERR_UNSUPPORTED"
