@@ -332,42 +332,56 @@ mot_status mot_replay_attention(const void* q, const void* k, const void* v, con
 
 /*
  * The backbone translator body (paper App. C.2, "Backbone Translator") as the
- * experts of the mixture, with a channel window of one slot per unit (target
- * layer j, K or V, source layer layer_map[j]).  For each batch row, over the
- * context positions t, expert m computes
- *     z   = GELU(W_in LN_in(x_t) + b_in)                       (d_h)
- *     h1  = z + Wo CausalMHA(Wq LN_Q(z) + bq, Wk LN_C(z) + bk, Wv LN_C(z) + bv) + bo
- *     h2  = h1 + W_f2 GELU(W_f1 LN_F(h1) + b_f1) + b_f2
- *     y_t = GELU(W_out LN_out(h2) + b_out)                     (d_out)
+ * experts of the mixture, over channel windows of N = dims->n_slots slots (0
+ * or 1: one slot per unit).  Window w covers target layers wN .. wN+N-1 (so
+ * L_tgt must be a multiple of N); its slot r reads source layer
+ * layer_map[wN + r], and a window is either fully mapped or fully -1
+ * (skipped).  Keys and values are translated separately; one unit is a
+ * (window, K or V).  For each batch row, over the context positions t,
+ * expert m computes
+ *     z_r = GELU(W_in LN_in(x_r[t]) + b_in)                     r = 1..N (d_h)
+ *     h_0 = z_1;  for r = 1..N (block CAB_r, its own parameters):
+ *       h~  = h_{r-1} + Wo CausalMHA(Wq LN_Q(h_{r-1}) + bq, Wk LN_C(z_r) + bk,
+ *                                    Wv LN_C(z_r) + bv) + bo
+ *       h_r = h~ + W_f2 GELU(W_f1 LN_F(h~) + b_f1) + b_f2
+ *     y_t = GELU(W_out LN_out(Concat(h_1..h_N)) + b_out)          (N d_out)
  * (n_heads heads of width d_h / n_heads, softmax(q.k / sqrt(width)) over the
  * positions s <= t of the same batch row; LN with population variance,
- * eps 1e-5) and the output row is sum_m g~_m y_t^(m) with the Top-K gates of
- * mot_translate's router.
+ * eps 1e-5); the output row is sum_m g~_m y_t^(m) with Top-K gates from a
+ * router over the window's concatenated source rows, and its slice
+ * [r d_out, (r+1) d_out) is written to target layer wN + r.  One translator
+ * stage (one scan) per expert.
  *
- *   params   device bf16 [L_tgt][2][E][P], P = mot_backbone_param_count():
+ *   params   device bf16 [L_tgt/N][2][E][P], P = mot_backbone_param_count():
  *            per expert, in order: ln_in_g[d_in] ln_in_b[d_in] w_in[d_h][d_in]
- *            b_in[d_h] ln_q_g[d_h] ln_q_b[d_h] ln_c_g[d_h] ln_c_b[d_h]
- *            wq[d_h][d_h] bq[d_h] wk[d_h][d_h] bk[d_h] wv[d_h][d_h] bv[d_h]
- *            wo[d_h][d_h] bo[d_h] ln_f_g[d_h] ln_f_b[d_h] w_f1[d_ff][d_h]
- *            b_f1[d_ff] w_f2[d_h][d_ff] b_f2[d_h] ln_out_g[d_h] ln_out_b[d_h]
- *            w_out[d_out][d_h] b_out[d_out]
- *   router   as for mot_translate (bias optional)
+ *            b_in[d_h]; then for each slot r = 1..N: ln_q_g[d_h] ln_q_b[d_h]
+ *            ln_c_g[d_h] ln_c_b[d_h] wq[d_h][d_h] bq[d_h] wk[d_h][d_h] bk[d_h]
+ *            wv[d_h][d_h] bv[d_h] wo[d_h][d_h] bo[d_h] ln_f_g[d_h] ln_f_b[d_h]
+ *            w_f1[d_ff][d_h] b_f1[d_ff] w_f2[d_h][d_ff] b_f2[d_h]; then
+ *            ln_out_g[N d_h] ln_out_b[N d_h] w_out[N d_out][N d_h]
+ *            b_out[N d_out]
+ *   router   w [L_tgt/N][2][E][N d_in], b [L_tgt/N][2][E] (bias optional);
+ *            with N = 1 the layout of mot_translate's router
  *   shapes   as for mot_translate (including the optional usage counts of
- *            the Top-K selections); dtype MOT_BF16, both layouts
+ *            the Top-K selections, here [L_tgt/N][2][E]: one row per
+ *            window and K/V); dtype MOT_BF16, both layouts
  *            MOT_LAYOUT_BTHD, streams 2; hidden, act and algo are not used.
  *            workspace: device scratch of at least
  *            mot_backbone_workspace_bytes (16-byte aligned, not overlapping
  *            any other argument), or NULL for the per-device buffer that
  *            mot_translate uses without a workspace (calls of either that
  *            overlap in time on one device then race)
- * Requires d_in and d_h multiples of 64 up to 4096, d_ff a multiple of 64,
- * D_tgt a multiple of 8, head width d_h / n_heads of 64 or 128
- * (MOT_ERR_UNSUPPORTED otherwise).  Every check runs before any enqueue.
+ * Requires d_in and d_h multiples of 64 up to 4096, N d_h up to 4096, d_ff a
+ * multiple of 64, D_tgt a multiple of 8, head width d_h / n_heads of 64 or
+ * 128, N <= 8 (MOT_ERR_UNSUPPORTED / MOT_ERR_BAD_SHAPE otherwise; a window
+ * mixing mapped and unmapped slots is MOT_ERR_BAD_LAYER_MAP).  Every check
+ * runs before any enqueue.
  */
 typedef struct {
-    int32_t d_h;       /* translator width          */
-    int32_t n_heads;   /* attention heads           */
-    int32_t d_ff;      /* feed-forward width        */
+    int32_t d_h;       /* translator width                               */
+    int32_t n_heads;   /* attention heads                                */
+    int32_t d_ff;      /* feed-forward width                             */
+    int32_t n_slots;   /* channel-window slots N (0 or 1: one per unit)  */
 } mot_backbone_dims;
 
 /* Elements per expert of the packed parameters (0 for invalid arguments). */

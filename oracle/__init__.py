@@ -10,10 +10,12 @@ from .oracle import (OracleDims, build_oracle, oracle_translate, oracle_rows,
                      oracle_depth_ratio_map, oracle_lib_path, oracle_restore_kv,
                      oracle_topS_select, oracle_replay_attention, oracle_topS_rows,
                      oracle_replay_attention_rows, oracle_backbone_translate, oracle_backbone_param_count,
-                     oracle_usage, oracle_usage_stats)
+                     oracle_usage, oracle_usage_stats, oracle_backbone_window,
+                     oracle_backbone_window_param_count)
 
 __all__ = ["OracleDims", "build_oracle", "oracle_translate", "oracle_rows",
            "oracle_depth_ratio_map", "oracle_lib_path", "oracle_restore_kv",
            "oracle_topS_select", "oracle_replay_attention", "oracle_topS_rows",
            "oracle_replay_attention_rows", "oracle_backbone_translate", "oracle_backbone_param_count",
-           "oracle_usage", "oracle_usage_stats"]
+           "oracle_usage", "oracle_usage_stats", "oracle_backbone_window",
+           "oracle_backbone_window_param_count"]

@@ -853,3 +853,200 @@ int mot_oracle_usage_stats(const int64_t* counts, int32_t E, double* cv2, double
     *entropy = total > 0.0 ? h : NAN;
     return OR_OK;
 }
+
+/* ------------------------------------------------------------------ */
+/* backbone translator over a multi-slot channel window (App. C.2)     */
+/* ------------------------------------------------------------------ */
+
+/* Parameters per (window, X, expert), in order (N = n_slots):
+ *   ln_in_g[d_in] ln_in_b[d_in] w_in[d_h][d_in] b_in[d_h]        (shared by the slots)
+ *   for each slot r = 1..N (the block CAB_r):
+ *     ln_q_g[d_h] ln_q_b[d_h] ln_c_g[d_h] ln_c_b[d_h] wq[d_h][d_h] bq[d_h] wk[d_h][d_h] bk[d_h]
+ *     wv[d_h][d_h] bv[d_h] wo[d_h][d_h] bo[d_h] ln_f_g[d_h] ln_f_b[d_h] w_f1[d_ff][d_h] b_f1[d_ff]
+ *     w_f2[d_h][d_ff] b_f2[d_h]
+ *   ln_out_g[N d_h] ln_out_b[N d_h] w_out[N d_out][N d_h] b_out[N d_out]
+ * With N = 1 this is the packing of mot_oracle_backbone_translate. */
+size_t mot_oracle_backbone_window_param_count(int32_t d_in, int32_t d_h, int32_t d_ff, int32_t d_out, int32_t N)
+{
+    const size_t cab = 4 * (size_t)d_h + 4 * ((size_t)d_h * d_h + d_h) + 2 * (size_t)d_h + (size_t)d_ff * d_h +
+                       d_ff + (size_t)d_h * d_ff + d_h;
+    return 2 * (size_t)d_in + (size_t)d_h * d_in + d_h + (size_t)N * cab + 2 * (size_t)N * d_h +
+           (size_t)N * d_out * N * d_h + (size_t)N * d_out;
+}
+
+/* Windows w = 0 .. L_tgt/N - 1 cover target layers wN .. wN+N-1; slot r of
+ * window w reads source layer layer_map[wN + r].  A window whose entries are
+ * all -1 is skipped (its target layers untouched); a window with some -1
+ * entries is an error.  For each window, X in {K, V} and batch row b, over
+ * the context positions t:
+ *   x_r[t]   = source row of slot r (head-major)
+ *   gates    = Top-K renormalised softmax of Wr Concat(x_1..x_N)[t] + br
+ *              (router weights [L_tgt/N][2][E][N d_in], bias [L_tgt/N][2][E])
+ *   expert m:
+ *     z_r[t] = GELU(W_in LN_in(x_r[t]) + b_in)
+ *     h_0 = z_1;  for r = 1..N:
+ *       a     = CausalMHA(LN_Q^r(h_{r-1}), LN_C^r(z_r), LN_C^r(z_r))  (Wq, Wk, Wv, Wo of slot r)
+ *       h~    = h_{r-1} + Wo^r a + bo^r
+ *       h_r   = h~ + W_f2^r GELU(W_f1^r LN_F^r(h~) + b_f1^r) + b_f2^r
+ *     y[t]   = GELU(W_out LN_out(Concat(h_1..h_N)[t]) + b_out)    (N d_out)
+ *   out[t] = sum_m g~_m y[t];  target layer wN + r receives out[t][r d_out .. (r+1) d_out).
+ * Sums in index order, double throughout. */
+int mot_oracle_backbone_window(const float* src_k, const float* src_v, const int32_t* layer_map,
+                               const float* params, const float* wr, const float* br,
+                               double* dst_k, double* dst_v, const mot_oracle_dims* s,
+                               int32_t d_h, int32_t n_heads, int32_t d_ff, int32_t N)
+{
+    int rc = check_dims(s, layer_map);
+    if (rc) return rc;
+    if (!src_k || !src_v || !params || !wr || !dst_k || !dst_v || s->streams != 2) return OR_BAD_ARG;
+    if (d_h < 1 || n_heads < 1 || d_h % n_heads || d_ff < 1 || N < 1 || s->L_tgt % N) return OR_BAD_ARG;
+    const int32_t d_in = s->H_src * s->D_src, d_out = s->H_tgt * s->D_tgt, E = s->E, T = s->T;
+    const int32_t hw = d_h / n_heads, W = s->L_tgt / N, Nd_in = N * d_in, Nd_h = N * d_h, Nd_out = N * d_out;
+    for (int32_t w = 0; w < W; ++w) {
+        int n_neg = 0;
+        for (int32_t r = 0; r < N; ++r) n_neg += layer_map[w * N + r] < 0;
+        if (n_neg != 0 && n_neg != N) return OR_BAD_ARG;
+    }
+    const size_t P = mot_oracle_backbone_window_param_count(d_in, d_h, d_ff, d_out, N);
+    const size_t cab = 4 * (size_t)d_h + 4 * ((size_t)d_h * d_h + d_h) + 2 * (size_t)d_h + (size_t)d_ff * d_h +
+                       d_ff + (size_t)d_h * d_ff + d_h;
+    const size_t TT = T > 0 ? (size_t)T : 1;
+    double* x = (double*)malloc(sizeof(double) * TT * Nd_in);     /* [t][r][d_in]: the concatenated rows */
+    double* z = (double*)malloc(sizeof(double) * TT * Nd_h);      /* [t][r][d_h] */
+    double* F = (double*)malloc(sizeof(double) * TT * Nd_h);      /* [t][r][d_h]: h_1..h_N */
+    double* Q = (double*)malloc(sizeof(double) * TT * d_h);
+    double* K = (double*)malloc(sizeof(double) * TT * d_h);
+    double* V = (double*)malloc(sizeof(double) * TT * d_h);
+    double* out = (double*)malloc(sizeof(double) * TT * Nd_out);
+    double* gt = (double*)malloc(sizeof(double) * TT * E);
+    double* t1 = (double*)malloc(sizeof(double) * (Nd_h > d_in ? Nd_h : d_in));
+    double* t2 = (double*)malloc(sizeof(double) * d_h);
+    double* att = (double*)malloc(sizeof(double) * d_h);
+    double* f = (double*)malloc(sizeof(double) * d_ff);
+    double* y = (double*)malloc(sizeof(double) * Nd_out);
+    double* sc = (double*)malloc(sizeof(double) * TT);
+    double* lg = (double*)malloc(sizeof(double) * E);
+    int* sel = (int*)malloc(sizeof(int) * E);
+    if (!x || !z || !F || !Q || !K || !V || !out || !gt || !t1 || !t2 || !att || !f || !y || !sc || !lg || !sel) {
+        rc = OR_NO_MEM;
+        goto done;
+    }
+    for (int32_t w = 0; w < W; ++w) {
+        if (layer_map[w * N] < 0) continue;
+        for (int32_t xk = 0; xk < 2; ++xk) {
+            const size_t unit = (size_t)w * 2 + xk;
+            const float* src = xk == 0 ? src_k : src_v;
+            double* dst = xk == 0 ? dst_k : dst_v;
+            for (int32_t b = 0; b < s->B; ++b) {
+                for (int32_t t = 0; t < T; ++t) {
+                    for (int32_t r = 0; r < N; ++r)
+                        gather_row(s, src, layer_map[w * N + r], b, t, x + (size_t)t * Nd_in + (size_t)r * d_in);
+                    const double* xt = x + (size_t)t * Nd_in;
+                    double mx = -INFINITY;
+                    for (int32_t m = 0; m < E; ++m) {
+                        double acc = 0.0;
+                        for (int32_t c = 0; c < Nd_in; ++c) acc += (double)wr[(unit * E + m) * Nd_in + c] * xt[c];
+                        if (br) acc += (double)br[unit * E + m];
+                        lg[m] = acc;
+                        if (acc > mx) mx = acc;
+                    }
+                    double den = 0.0;
+                    for (int32_t m = 0; m < E; ++m) { lg[m] = exp(lg[m] - mx); den += lg[m]; }
+                    for (int32_t m = 0; m < E; ++m) { lg[m] /= den; sel[m] = 0; }
+                    for (int32_t k = 0; k < s->top_k; ++k) {
+                        int32_t best = -1;
+                        for (int32_t m = 0; m < E; ++m)
+                            if (!sel[m] && (best < 0 || lg[m] > lg[best])) best = m;
+                        sel[best] = 1;
+                    }
+                    double gs = 0.0;
+                    for (int32_t m = 0; m < E; ++m) if (sel[m]) gs += lg[m];
+                    for (int32_t m = 0; m < E; ++m) gt[(size_t)t * E + m] = sel[m] ? lg[m] / gs : 0.0;
+                }
+                for (size_t c = 0; c < (size_t)T * Nd_out; ++c) out[c] = 0.0;
+                for (int32_t m = 0; m < E; ++m) {
+                    int used = 0;
+                    for (int32_t t = 0; t < T; ++t) used |= gt[(size_t)t * E + m] != 0.0;
+                    if (!used) continue;
+                    const float* pp = params + (unit * E + m) * P;
+                    const float *ln_in_g = pp, *ln_in_b = ln_in_g + d_in, *w_in = ln_in_b + d_in,
+                                *b_in = w_in + (size_t)d_h * d_in;
+                    const float* cab0 = b_in + d_h;
+                    const float *ln_out_g = cab0 + (size_t)N * cab, *ln_out_b = ln_out_g + Nd_h,
+                                *w_out = ln_out_b + Nd_h, *b_out = w_out + (size_t)Nd_out * Nd_h;
+                    /* z_r = GELU(W_in LN_in(x_r) + b_in) for every slot */
+                    for (int32_t t = 0; t < T; ++t)
+                        for (int32_t r = 0; r < N; ++r) {
+                            bb_layernorm(x + (size_t)t * Nd_in + (size_t)r * d_in, d_in, ln_in_g, ln_in_b, t1);
+                            bb_linear(t1, d_in, w_in, b_in, d_h, 1, z + (size_t)t * Nd_h + (size_t)r * d_h);
+                        }
+                    /* the recurrent scan over the slots */
+                    for (int32_t r = 0; r < N; ++r) {
+                        const float* cp = cab0 + (size_t)r * cab;
+                        const float *ln_q_g = cp, *ln_q_b = ln_q_g + d_h, *ln_c_g = ln_q_b + d_h,
+                                    *ln_c_b = ln_c_g + d_h, *wq = ln_c_b + d_h, *bq = wq + (size_t)d_h * d_h,
+                                    *wk = bq + d_h, *bk = wk + (size_t)d_h * d_h, *wv = bk + d_h,
+                                    *bv = wv + (size_t)d_h * d_h, *wo = bv + d_h, *bo = wo + (size_t)d_h * d_h,
+                                    *ln_f_g = bo + d_h, *ln_f_b = ln_f_g + d_h, *w_f1 = ln_f_b + d_h,
+                                    *b_f1 = w_f1 + (size_t)d_ff * d_h, *w_f2 = b_f1 + d_ff,
+                                    *b_f2 = w_f2 + (size_t)d_h * d_ff;
+                        /* h_{r-1}: z_1 before the first block, then the previous block's output */
+                        for (int32_t t = 0; t < T; ++t) {
+                            const double* hp = r == 0 ? z + (size_t)t * Nd_h : F + (size_t)t * Nd_h + (size_t)(r - 1) * d_h;
+                            const double* zr = z + (size_t)t * Nd_h + (size_t)r * d_h;
+                            bb_layernorm(hp, d_h, ln_q_g, ln_q_b, t1);
+                            bb_linear(t1, d_h, wq, bq, d_h, 0, Q + (size_t)t * d_h);
+                            bb_layernorm(zr, d_h, ln_c_g, ln_c_b, t1);
+                            bb_linear(t1, d_h, wk, bk, d_h, 0, K + (size_t)t * d_h);
+                            bb_linear(t1, d_h, wv, bv, d_h, 0, V + (size_t)t * d_h);
+                        }
+                        for (int32_t t = 0; t < T; ++t) {
+                            for (int32_t hh = 0; hh < n_heads; ++hh) {
+                                const double* qt = Q + (size_t)t * d_h + hh * hw;
+                                double mx = -INFINITY;
+                                for (int32_t u = 0; u <= t; ++u) {
+                                    const double* ku = K + (size_t)u * d_h + hh * hw;
+                                    double acc = 0.0;
+                                    for (int32_t d = 0; d < hw; ++d) acc += qt[d] * ku[d];
+                                    sc[u] = acc / sqrt((double)hw);
+                                    if (sc[u] > mx) mx = sc[u];
+                                }
+                                double den = 0.0;
+                                for (int32_t u = 0; u <= t; ++u) { sc[u] = exp(sc[u] - mx); den += sc[u]; }
+                                for (int32_t d = 0; d < hw; ++d) att[hh * hw + d] = 0.0;
+                                for (int32_t u = 0; u <= t; ++u) {
+                                    const double* vu = V + (size_t)u * d_h + hh * hw;
+                                    for (int32_t d = 0; d < hw; ++d) att[hh * hw + d] += sc[u] / den * vu[d];
+                                }
+                            }
+                            const double* hp = r == 0 ? z + (size_t)t * Nd_h : F + (size_t)t * Nd_h + (size_t)(r - 1) * d_h;
+                            double* hr = F + (size_t)t * Nd_h + (size_t)r * d_h;
+                            bb_linear(att, d_h, wo, bo, d_h, 0, t2);
+                            for (int32_t c = 0; c < d_h; ++c) t2[c] += hp[c];
+                            bb_layernorm(t2, d_h, ln_f_g, ln_f_b, t1);
+                            bb_linear(t1, d_h, w_f1, b_f1, d_ff, 1, f);
+                            bb_linear(f, d_ff, w_f2, b_f2, d_h, 0, hr);
+                            for (int32_t c = 0; c < d_h; ++c) hr[c] += t2[c];
+                        }
+                    }
+                    /* y = GELU(W_out LN_out(Concat(h_1..h_N)) + b_out), gated sum */
+                    for (int32_t t = 0; t < T; ++t) {
+                        bb_layernorm(F + (size_t)t * Nd_h, Nd_h, ln_out_g, ln_out_b, t1);
+                        bb_linear(t1, Nd_h, w_out, b_out, Nd_out, 1, y);
+                        const double g = gt[(size_t)t * E + m];
+                        for (int32_t o = 0; o < Nd_out; ++o) out[(size_t)t * Nd_out + o] += g * y[o];
+                    }
+                }
+                for (int32_t r = 0; r < N; ++r)
+                    for (int32_t t = 0; t < T; ++t)
+                        for (int32_t o = 0; o < d_out; ++o)
+                            dst[cache_index(s, s->dst_layout, s->H_tgt, s->D_tgt, w * N + r, b, t, o / s->D_tgt,
+                                            o % s->D_tgt)] = out[(size_t)t * Nd_out + (size_t)r * d_out + o];
+            }
+        }
+    }
+done:
+    free(x); free(z); free(F); free(Q); free(K); free(V); free(out); free(gt); free(t1); free(t2);
+    free(att); free(f); free(y); free(sc); free(lg); free(sel);
+    return rc;
+}

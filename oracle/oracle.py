@@ -93,11 +93,13 @@ def _load():
         _lib = ctypes.CDLL(path)
         _lib.mot_oracle_backbone_param_count.restype = ctypes.c_size_t
         _lib.mot_oracle_backbone_param_count.argtypes = [ctypes.c_int32] * 4
+        _lib.mot_oracle_backbone_window_param_count.restype = ctypes.c_size_t
+        _lib.mot_oracle_backbone_window_param_count.argtypes = [ctypes.c_int32] * 5
         for fn in (_lib.mot_oracle_translate, _lib.mot_oracle_rows,
                    _lib.mot_oracle_depth_ratio_map, _lib.mot_oracle_restore_kv,
                    _lib.mot_oracle_topS_select, _lib.mot_oracle_replay_attention,
                    _lib.mot_oracle_replay_attention_rows, _lib.mot_oracle_topS_rows,
-                   _lib.mot_oracle_backbone_translate, _lib.mot_oracle_usage,
+                   _lib.mot_oracle_backbone_translate, _lib.mot_oracle_backbone_window, _lib.mot_oracle_usage,
                    _lib.mot_oracle_usage_stats):
             fn.restype = ctypes.c_int
     return _lib
@@ -335,3 +337,35 @@ def oracle_usage_stats(counts) -> tuple:
     if rc != 0:
         raise ValueError("mot_oracle_usage_stats failed with code %d" % rc)
     return cv2.value, ent.value
+
+
+def oracle_backbone_window_param_count(d_in: int, d_h: int, d_ff: int, d_out: int, n_slots: int) -> int:
+    """Parameters per (window, X, expert) of the backbone body over a window
+    of n_slots channel slots (shared input projection, one cross-attention
+    block per slot, output projection of the concatenation)."""
+    return int(_load().mot_oracle_backbone_window_param_count(d_in, d_h, d_ff, d_out, n_slots))
+
+
+def oracle_backbone_window(dims: OracleDims, src_k, src_v, layer_map, params, wr, br, d_h: int, n_heads: int,
+                           d_ff: int, n_slots: int):
+    """Mixture of backbone translators over channel windows of n_slots slots
+    (App. C.2): window w covers target layers w*N .. w*N+N-1, slot r reads
+    source layer layer_map[w*N + r]; params float32 [L_tgt/N][2][E][P]; router
+    weights [L_tgt/N][2][E][N*d_in], bias [L_tgt/N][2][E].  Returns (dst_k,
+    dst_v) float64 in the dst layout (NaN in skipped windows)."""
+    lib = _load()
+    arrs = [_f32(a, n) for a, n in ((src_k, "src_k"), (src_v, "src_v"), (params, "params"), (wr, "wr"),
+                                    (br, "br"))]
+    lm = np.ascontiguousarray(layer_map, dtype=np.int32)
+    shape = ((dims.L_tgt, dims.B, dims.T, dims.H_tgt, dims.D_tgt) if dims.dst_layout == 0
+             else (dims.L_tgt, dims.B, dims.H_tgt, dims.T, dims.D_tgt))
+    dst_k = np.full(shape, np.nan)
+    dst_v = np.full(shape, np.nan)
+    c = dims._c()
+    i32 = ctypes.c_int32
+    rc = lib.mot_oracle_backbone_window(_ptr(arrs[0]), _ptr(arrs[1]), _ptr(lm), _ptr(arrs[2]), _ptr(arrs[3]),
+                                        _ptr(arrs[4]), _ptr(dst_k), _ptr(dst_v), ctypes.byref(c), i32(d_h),
+                                        i32(n_heads), i32(d_ff), i32(n_slots))
+    if rc != 0:
+        raise ValueError("mot_oracle_backbone_window failed with code %d" % rc)
+    return dst_k, dst_v

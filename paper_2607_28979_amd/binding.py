@@ -51,7 +51,7 @@ class _RestoreShapes(ctypes.Structure):
 
 
 class _BackboneDims(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_int32) for n in ("d_h", "n_heads", "d_ff")]
+    _fields_ = [(n, ctypes.c_int32) for n in ("d_h", "n_heads", "d_ff", "n_slots")]
 
 
 class _ReplayShapes(ctypes.Structure):
@@ -347,22 +347,24 @@ def replay_attention_noalloc(q, k, v, idx, o, B: int, T: int, H_q: int, H_kv: in
                                             torch.cuda.current_stream().cuda_stream))
 
 
-def backbone_param_count(shapes: Shapes, d_h: int, n_heads: int, d_ff: int) -> int:
+def backbone_param_count(shapes: Shapes, d_h: int, n_heads: int, d_ff: int, n_slots: int = 1) -> int:
     """Elements per expert of the packed backbone parameters."""
     c = shapes.c()
-    return int(load_library().mot_backbone_param_count(ctypes.byref(c), ctypes.byref(_BackboneDims(d_h, n_heads, d_ff))))
+    return int(load_library().mot_backbone_param_count(ctypes.byref(c),
+                                                       ctypes.byref(_BackboneDims(d_h, n_heads, d_ff, n_slots))))
 
 
-def backbone_workspace_bytes(shapes: Shapes, d_h: int, n_heads: int, d_ff: int) -> int:
+def backbone_workspace_bytes(shapes: Shapes, d_h: int, n_heads: int, d_ff: int, n_slots: int = 1) -> int:
     c = shapes.c()
-    n = load_library().mot_backbone_workspace_bytes(ctypes.byref(c), ctypes.byref(_BackboneDims(d_h, n_heads, d_ff)))
+    n = load_library().mot_backbone_workspace_bytes(ctypes.byref(c),
+                                                    ctypes.byref(_BackboneDims(d_h, n_heads, d_ff, n_slots)))
     if n == ctypes.c_size_t(-1).value:
         raise MotError(2, load_library().mot_last_error().decode())
     return int(n)
 
 
 def backbone_translate(src_k, src_v, layer_map, params, wr, br, dst_k, dst_v, shapes: Shapes, d_h: int,
-                       n_heads: int, d_ff: int, usage=None, workspace=None) -> None:
+                       n_heads: int, d_ff: int, usage=None, workspace=None, n_slots: int = 1) -> None:
     """mot_backbone_translate on the current torch stream (bf16 tensors)."""
     import numpy as np
     import torch
@@ -377,5 +379,5 @@ def backbone_translate(src_k, src_v, layer_map, params, wr, br, dst_k, dst_v, sh
                  _ptr(usage))
     _check(lib.mot_backbone_translate(_ptr(src_k), _ptr(src_v), lm.ctypes.data, _ptr(params), ctypes.byref(rw),
                                       _ptr(dst_k), _ptr(dst_v), ctypes.byref(c),
-                                      ctypes.byref(_BackboneDims(d_h, n_heads, d_ff)),
+                                      ctypes.byref(_BackboneDims(d_h, n_heads, d_ff, n_slots)),
                                       torch.cuda.current_stream().cuda_stream))

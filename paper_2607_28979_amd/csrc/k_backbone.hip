@@ -297,13 +297,14 @@ __global__ __launch_bounds__(256) void k_linear(LinearProblem p) {
     u32x4 rres[NP];
     f32x4 rmix[NP][2];
     float rgate[NP];
+    const size_t ld_res = p.ld_res ? p.ld_res : (size_t)N, ld_out = p.ld_out ? p.ld_out : (size_t)N;
 #pragma unroll
     for (int pass = 0; pass < NP; ++pass) {
         // clamped to the last row / column group: values of lanes that store
         // nothing are never used
         const int t = min(r0 + pass * 16 + (tid >> 4), p.n - 1);
         const size_t at = (size_t)t * N + min(oc, N - 8);
-        rres[pass] = p.res ? *reinterpret_cast<const u32x4*>(p.res + at) : zero;
+        rres[pass] = p.res ? *reinterpret_cast<const u32x4*>(p.res + (size_t)t * ld_res + min(oc, N - 8)) : zero;
         rgate[pass] = p.mix ? p.gates[(size_t)t * p.gate_ld + p.expert] : 0.f;
 #pragma unroll
         for (int i = 0; i < 2; ++i)
@@ -320,7 +321,7 @@ __global__ __launch_bounds__(256) void k_linear(LinearProblem p) {
         const f32x4 lo = stg[tl * 32 + ((2 * h) ^ (tl & 31))];
         const f32x4 hi = stg[tl * 32 + ((2 * h + 1) ^ (tl & 31))];
         float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        const size_t at = (size_t)t * N + oc;
+        const size_t at = (size_t)t * N + oc;   // the fp32 mixture rows are dense
         if (p.res) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
@@ -349,7 +350,7 @@ __global__ __launch_bounds__(256) void k_linear(LinearProblem p) {
         }
         const u32x4 w4 = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
                           pack_bf16x2(v[6], v[7])};
-        *reinterpret_cast<u32x4*>(out + at) = w4;
+        *reinterpret_cast<u32x4*>(out + (size_t)t * ld_out + oc) = w4;
     }
 }
 

@@ -439,23 +439,32 @@ mot_status mot_restore_kv(const void* act, const int32_t* layer_map, const void*
 }
 
 namespace {
-// Offsets (elements) of one expert's packed backbone parameters, in the
-// order the header documents.
+// Offsets (elements) of one expert's packed backbone parameters over a
+// channel window of N slots, in the order the header documents: the shared
+// input projection, N cross-attention blocks of `cab` elements each (the
+// block offsets are relative to the block's start), the output projection.
+// N = 1 is the single-slot packing.
 struct BackboneOffsets {
-    size_t ln_in_g, ln_in_b, w_in, b_in, ln_q_g, ln_q_b, ln_c_g, ln_c_b, wq, bq, wk, bk, wv, bv, wo, bo,
-        ln_f_g, ln_f_b, w_f1, b_f1, w_f2, b_f2, ln_out_g, ln_out_b, w_out, b_out, total;
+    size_t ln_in_g, ln_in_b, w_in, b_in, cab0, cab;
+    size_t ln_q_g, ln_q_b, ln_c_g, ln_c_b, wq, bq, wk, bk, wv, bv, wo, bo, ln_f_g, ln_f_b, w_f1, b_f1, w_f2, b_f2;
+    size_t ln_out_g, ln_out_b, w_out, b_out, total;
 };
-BackboneOffsets backbone_offsets(size_t d_in, size_t d_h, size_t d_ff, size_t d_out) {
+BackboneOffsets backbone_offsets(size_t d_in, size_t d_h, size_t d_ff, size_t d_out, size_t N) {
     BackboneOffsets o;
     size_t at = 0;
     auto take = [&](size_t n) { const size_t r = at; at += n; return r; };
     o.ln_in_g = take(d_in); o.ln_in_b = take(d_in); o.w_in = take(d_h * d_in); o.b_in = take(d_h);
+    o.cab0 = at;
+    at = 0;
     o.ln_q_g = take(d_h); o.ln_q_b = take(d_h); o.ln_c_g = take(d_h); o.ln_c_b = take(d_h);
     o.wq = take(d_h * d_h); o.bq = take(d_h); o.wk = take(d_h * d_h); o.bk = take(d_h);
     o.wv = take(d_h * d_h); o.bv = take(d_h); o.wo = take(d_h * d_h); o.bo = take(d_h);
     o.ln_f_g = take(d_h); o.ln_f_b = take(d_h); o.w_f1 = take(d_ff * d_h); o.b_f1 = take(d_ff);
-    o.w_f2 = take(d_h * d_ff); o.b_f2 = take(d_h); o.ln_out_g = take(d_h); o.ln_out_b = take(d_h);
-    o.w_out = take(d_out * d_h); o.b_out = take(d_out);
+    o.w_f2 = take(d_h * d_ff); o.b_f2 = take(d_h);
+    o.cab = at;
+    at = o.cab0 + N * o.cab;
+    o.ln_out_g = take(N * d_h); o.ln_out_b = take(N * d_h);
+    o.w_out = take(N * d_out * N * d_h); o.b_out = take(N * d_out);
     o.total = at;
     return o;
 }
@@ -601,29 +610,40 @@ size_t mot_replay_workspace_bytes(const mot_replay_shapes* s, int with_sets) {
     return with_sets ? 0 : replay_vt_bytes(s->B, s->T, s->H_kv, s->D);
 }
 
+constexpr int kMaxSlots = 8;   // channel-window slots of the backbone
+
+int backbone_slots(const mot_backbone_dims* bd) { return bd->n_slots > 1 ? bd->n_slots : 1; }
+
 size_t mot_backbone_param_count(const mot_shapes* s, const mot_backbone_dims* bd) {
-    if (!s || !bd || s->H_src < 1 || s->D_src < 1 || s->H_tgt < 1 || s->D_tgt < 1 || bd->d_h < 1 || bd->d_ff < 1)
+    if (!s || !bd || s->H_src < 1 || s->D_src < 1 || s->H_tgt < 1 || s->D_tgt < 1 || bd->d_h < 1 || bd->d_ff < 1 ||
+        bd->n_slots < 0 || bd->n_slots > kMaxSlots)
         return 0;
-    return backbone_offsets((size_t)s->H_src * s->D_src, bd->d_h, bd->d_ff, (size_t)s->H_tgt * s->D_tgt).total;
+    return backbone_offsets((size_t)s->H_src * s->D_src, bd->d_h, bd->d_ff, (size_t)s->H_tgt * s->D_tgt,
+                            backbone_slots(bd)).total;
 }
 
 namespace {
 // Workspace of the backbone call: gates of every unit, then one unit's
-// activation rows (LayerNorm outputs, z, Q, K, V, attention, h1, FFN, h2, the
-// fp32 mixture), then the attention's transposed V.
+// activation rows, then the attention's transposed V.  Buffers, in order:
+// LN_in rows, z of the N slots, LN_Q and LN_C rows, Q, K, V, attention,
+// h~, LN_F rows, FFN hidden, Concat(h_1..h_N), its LayerNorm, the fp32
+// mixture of the N target layers, the window's concatenated source rows
+// (N > 1: the router's input).
+constexpr int kBbBufs = 15;
 struct BackboneScratch {
-    size_t at[14];
+    size_t at[kBbBufs];
     size_t at_vt;
     size_t total;
 };
 BackboneScratch backbone_scratch(const mot_shapes* s, const mot_backbone_dims* bd, int n_units) {
     const size_t n = (size_t)s->B * s->T, d_in = (size_t)s->H_src * s->D_src, d_out = (size_t)s->H_tgt * s->D_tgt;
-    const size_t d_h = bd->d_h, d_ff = bd->d_ff;
-    const size_t row_b[14] = {d_in * 2, d_h * 2, d_h * 2, d_h * 2, d_h * 2, d_h * 2, d_h * 2,
-                              d_h * 2,  d_h * 2, d_h * 2, d_ff * 2, d_h * 2, d_h * 2, d_out * 4};
+    const size_t d_h = bd->d_h, d_ff = bd->d_ff, N = backbone_slots(bd);
+    const size_t row_b[kBbBufs] = {d_in * 2, N * d_h * 2, d_h * 2,     d_h * 2,     d_h * 2,
+                                   d_h * 2,  d_h * 2,     d_h * 2,     d_h * 2,     d_h * 2,
+                                   d_ff * 2, N * d_h * 2, N * d_h * 2, N * d_out * 4, N > 1 ? N * d_in * 2 : 0};
     BackboneScratch b;
     size_t need = round_up((size_t)n_units * round_up(n, 128) * s->E * 4, kAlign);
-    for (int k = 0; k < 14; ++k) { b.at[k] = need; need += round_up(n * row_b[k], kAlign); }
+    for (int k = 0; k < kBbBufs; ++k) { b.at[k] = need; need += round_up(n * row_b[k], kAlign); }
     b.at_vt = need;
     need += round_up(replay_vt_bytes(s->B, s->T, bd->n_heads, bd->d_h / bd->n_heads), kAlign);
     b.total = need;
@@ -639,15 +659,20 @@ mot_status check_backbone(const mot_shapes* s, const mot_backbone_dims* bd) {
     if (d_h < 1 || nh < 1 || d_ff < 1 || d_h % nh)
         return fail(MOT_ERR_BAD_SHAPE, "d_h=%d n_heads=%d d_ff=%d: need positive sizes, d_h a multiple of n_heads",
                     d_h, nh, d_ff);
+    if (bd->n_slots < 0 || bd->n_slots > kMaxSlots)
+        return fail(MOT_ERR_BAD_SHAPE, "n_slots=%d must be in [0, %d]", bd->n_slots, kMaxSlots);
+    const int N = backbone_slots(bd);
+    if (s->L_tgt % N)
+        return fail(MOT_ERR_BAD_SHAPE, "L_tgt=%d is not a multiple of the window of %d slots", s->L_tgt, N);
     if (s->dtype != MOT_BF16 || s->src_layout != MOT_LAYOUT_BTHD || s->dst_layout != MOT_LAYOUT_BTHD ||
         s->streams == 1)
         return fail(MOT_ERR_UNSUPPORTED, "the backbone translator needs bf16, BTHD source and target layouts, "
                     "keys and values (streams = 2)");
-    if (d_in % 64 || d_in > 4096 || d_h % 64 || d_h > 4096 || d_ff % 64 || d_out % 8 ||
+    if (d_in % 64 || d_in > 4096 || d_h % 64 || d_h > 4096 || N * d_h > 4096 || d_ff % 64 || d_out % 8 ||
         (d_h / nh != 64 && d_h / nh != 128))
-        return fail(MOT_ERR_UNSUPPORTED, "backbone sizes: d_in, d_h multiples of 64 up to 4096, d_ff a multiple of "
-                    "64, d_out of 8, head width d_h / n_heads 64 or 128 (got d_in=%d d_h=%d n_heads=%d d_ff=%d "
-                    "d_out=%d)", d_in, d_h, nh, d_ff, d_out);
+        return fail(MOT_ERR_UNSUPPORTED, "backbone sizes: d_in, d_h multiples of 64 up to 4096 (n_slots * d_h too), "
+                    "d_ff a multiple of 64, d_out of 8, head width d_h / n_heads 64 or 128 (got d_in=%d d_h=%d "
+                    "n_heads=%d d_ff=%d d_out=%d n_slots=%d)", d_in, d_h, nh, d_ff, d_out, N);
     return MOT_OK;
 }
 }  // namespace
@@ -656,7 +681,7 @@ size_t mot_backbone_workspace_bytes(const mot_shapes* s, const mot_backbone_dims
     g_err[0] = 0;
     if (check_backbone(s, bd) != MOT_OK) return SIZE_MAX;
     if ((int64_t)s->B * s->T == 0) return 0;
-    return backbone_scratch(s, bd, 2 * s->L_tgt).total;
+    return backbone_scratch(s, bd, 2 * s->L_tgt / backbone_slots(bd)).total;
 }
 
 mot_status mot_backbone_translate(const void* src_k, const void* src_v, const int32_t* layer_map, const void* params,
@@ -666,13 +691,18 @@ mot_status mot_backbone_translate(const void* src_k, const void* src_v, const in
     mot_status st = check_backbone(s, bd);
     if (st != MOT_OK) return st;
     const int d_in = s->H_src * s->D_src, d_out = s->H_tgt * s->D_tgt, d_h = bd->d_h, nh = bd->n_heads,
-              d_ff = bd->d_ff;
+              d_ff = bd->d_ff, N = backbone_slots(bd), W = s->L_tgt / N;
     if ((int64_t)s->B * s->T == 0) return MOT_OK;
     if (!src_k || !src_v || !layer_map || !params || !rw || !rw->w || !dst_k || !dst_v)
         return fail(MOT_ERR_NULL_ARG, "a required argument is NULL");
     for (int j = 0; j < s->L_tgt; ++j)
         if (layer_map[j] < -1 || layer_map[j] >= s->L_src)
             return fail(MOT_ERR_BAD_LAYER_MAP, "layer_map[%d]=%d outside [-1, %d)", j, layer_map[j], s->L_src);
+    for (int w = 0; w < W; ++w)
+        for (int r = 1; r < N; ++r)
+            if ((layer_map[w * N + r] < 0) != (layer_map[w * N] < 0))
+                return fail(MOT_ERR_BAD_LAYER_MAP, "window %d (target layers %d..%d) mixes mapped and unmapped slots",
+                            w, w * N, w * N + N - 1);
     const void* dev_ptrs[] = {src_k, src_v, params, rw->w, dst_k, dst_v};
     for (const void* q : dev_ptrs)
         if (!aligned16(q)) return fail(MOT_ERR_MISALIGNED, "device pointer %p is not 16-byte aligned", q);
@@ -686,13 +716,15 @@ mot_status mot_backbone_translate(const void* src_k, const void* src_v, const in
         overlaps(dst_v, dst_bytes, src_v, src_bytes))
         return fail(MOT_ERR_BAD_SHAPE, "destination caches overlap each other or the source caches");
 
-    const BackboneOffsets off = backbone_offsets(d_in, d_h, d_ff, d_out);
+    const BackboneOffsets off = backbone_offsets(d_in, d_h, d_ff, d_out, N);
     Problem p = base_problem(s);
+    // one unit per (window, X): the window index plays the target layer's
+    // part in the unit code (weights, router, usage are per window)
     static thread_local UnitTab ut;
     int nu = 0;
-    for (int j = 0; j < s->L_tgt; ++j)
-        if (layer_map[j] >= 0)
-            for (int x = 0; x < 2; ++x) { ut.code[nu] = unit_code(j, x, layer_map[j], nu); ++nu; }
+    for (int w = 0; w < W; ++w)
+        if (layer_map[w * N] >= 0)
+            for (int x = 0; x < 2; ++x) { ut.code[nu] = unit_code(w, x, layer_map[w * N], nu); ++nu; }
     ut.n = nu;
     if (nu == 0) return MOT_OK;
     // workspace: gates, then one unit's activations, then V transposed
@@ -701,7 +733,7 @@ mot_status mot_backbone_translate(const void* src_k, const void* src_v, const in
     const size_t at_vt = sc.at_vt;
     void* ws = s->workspace;
     if (ws) {
-        const size_t need_all = backbone_scratch(s, bd, 2 * s->L_tgt).total;
+        const size_t need_all = backbone_scratch(s, bd, 2 * W).total;
         if (!aligned16(ws)) return fail(MOT_ERR_MISALIGNED, "workspace %p is not 16-byte aligned", ws);
         if (s->workspace_bytes < sc.total)
             return fail(MOT_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes, need %zu (%zu for every layer mapped)",
@@ -715,7 +747,7 @@ mot_status mot_backbone_translate(const void* src_k, const void* src_v, const in
     }
     char* w8 = reinterpret_cast<char*>(ws);
     uint16_t* xn = reinterpret_cast<uint16_t*>(w8 + at[0]);
-    uint16_t* z = reinterpret_cast<uint16_t*>(w8 + at[1]);
+    uint16_t* z = reinterpret_cast<uint16_t*>(w8 + at[1]);      // [N][n][d_h]
     uint16_t* qn = reinterpret_cast<uint16_t*>(w8 + at[2]);
     uint16_t* cn = reinterpret_cast<uint16_t*>(w8 + at[3]);
     uint16_t* Q = reinterpret_cast<uint16_t*>(w8 + at[4]);
@@ -725,121 +757,165 @@ mot_status mot_backbone_translate(const void* src_k, const void* src_v, const in
     uint16_t* h1 = reinterpret_cast<uint16_t*>(w8 + at[8]);
     uint16_t* fn = reinterpret_cast<uint16_t*>(w8 + at[9]);
     uint16_t* f1 = reinterpret_cast<uint16_t*>(w8 + at[10]);
-    uint16_t* h2 = reinterpret_cast<uint16_t*>(w8 + at[11]);
-    uint16_t* on = reinterpret_cast<uint16_t*>(w8 + at[12]);
-    float* mix = reinterpret_cast<float*>(w8 + at[13]);
+    uint16_t* F = reinterpret_cast<uint16_t*>(w8 + at[11]);     // [n][N d_h]
+    uint16_t* on = reinterpret_cast<uint16_t*>(w8 + at[12]);    // [n][N d_h]
+    float* mix = reinterpret_cast<float*>(w8 + at[13]);         // [N][n][d_out]
+    uint16_t* xcat = reinterpret_cast<uint16_t*>(w8 + at[14]);  // [n][N d_in]
     uint16_t* vt = reinterpret_cast<uint16_t*>(w8 + at_vt);
 
     p.src[0] = src_k; p.src[1] = src_v; p.wr = rw->w; p.br = rw->b;
     p.gates = reinterpret_cast<float*>(ws);
-    hipError_t e = launch_router(p, ut, true, stream);
+    hipError_t e = hipSuccess;
+    if (N == 1) e = launch_router(p, ut, true, stream);   // every unit at once
     const uint16_t* P0 = reinterpret_cast<const uint16_t*>(params);
     const int n_i = (int)n;
+    const size_t ldF = (size_t)N * d_h;
     for (int u = 0; u < nu && e == hipSuccess; ++u) {
         const uint32_t code = ut.code[u];
-        const int j = unit_j(code), x = unit_x(code), i = unit_i(code), gs = unit_gslot(code);
-        const uint16_t* src = reinterpret_cast<const uint16_t*>(x ? src_v : src_k) + (size_t)i * n * d_in;
-        uint16_t* dst = reinterpret_cast<uint16_t*>(x ? dst_v : dst_k) + (size_t)j * n * d_out;
+        const int w = unit_j(code), x = unit_x(code), gs = unit_gslot(code);
+        const uint16_t* srcx = reinterpret_cast<const uint16_t*>(x ? src_v : src_k);
+        uint16_t* dstx = reinterpret_cast<uint16_t*>(x ? dst_v : dst_k);
+        auto src_slot = [&](int r) { return srcx + (size_t)layer_map[w * N + r] * n * d_in; };
+        if (N > 1) {
+            // the router reads the window's concatenated source rows
+            for (int r = 0; r < N && e == hipSuccess; ++r)
+                e = hipMemcpy2DAsync(xcat + (size_t)r * d_in, (size_t)N * d_in * 2, src_slot(r), (size_t)d_in * 2,
+                                     (size_t)d_in * 2, n, hipMemcpyDeviceToDevice, stream);
+            Problem pr = p;
+            pr.src[0] = pr.src[1] = xcat;
+            pr.d_in = N * d_in; pr.H_src = 1; pr.D_src = N * d_in; pr.src_layout = MOT_LAYOUT_BTHD;
+            static thread_local UnitTab one;
+            one.n = 1;
+            one.code[0] = unit_code(w, x, 0, gs);
+            if (e == hipSuccess) e = launch_router(pr, one, true, stream);
+        }
         for (int m = 0; m < s->E && e == hipSuccess; ++m) {
-            const uint16_t* Pm = P0 + (((size_t)j * 2 + x) * s->E + m) * off.total;
+            const uint16_t* Pm = P0 + (((size_t)w * 2 + x) * s->E + m) * off.total;
             // one linear launch over up to three parts sharing the input rows;
             // the LayerNorm of a part's input is fused when K <= kLinearLnMaxK,
             // otherwise it runs as its own pass into the workspace first
-            auto part = [&](const uint16_t* W, const uint16_t* bias, int N_, uint16_t* out,
+            auto part = [&](const uint16_t* W_, const uint16_t* bias, int N_, uint16_t* out,
                             const uint16_t* g = nullptr, const uint16_t* b = nullptr) {
                 LinearPart q;
-                q.W = W; q.bias = bias; q.ln_g = g; q.ln_b = b; q.out = out; q.N = N_;
+                q.W = W_; q.bias = bias; q.ln_g = g; q.ln_b = b; q.out = out; q.N = N_;
                 return q;
             };
-            auto lin = [&](const uint16_t* in, int K_, int gelu, const uint16_t* res, int np, const LinearPart* ps) {
+            auto lin = [&](const uint16_t* in, size_t ld_in, int K_, int gelu, const uint16_t* res, size_t ld_res,
+                           size_t ld_out, int np, const LinearPart* ps) {
                 LinearProblem lp;
                 memset(&lp, 0, sizeof lp);
-                lp.in = in; lp.ld_in = (size_t)K_; lp.res = res; lp.n = n_i; lp.K = K_; lp.gelu = gelu;
+                lp.in = in; lp.ld_in = ld_in; lp.res = res; lp.ld_res = ld_res; lp.ld_out = ld_out;
+                lp.n = n_i; lp.K = K_; lp.gelu = gelu;
                 lp.nparts = np;
                 for (int q = 0; q < np; ++q) lp.part[q] = ps[q];
                 return launch_linear(lp, stream);
             };
-            auto ln = [&](const uint16_t* in, int w, const uint16_t* g, const uint16_t* b, uint16_t* out,
+            auto ln = [&](const uint16_t* in, size_t ld_in, int wd, const uint16_t* g, const uint16_t* b, uint16_t* out,
                           const uint16_t* g2, const uint16_t* b2, uint16_t* out2) {
                 LnProblem q;
-                q.in = in; q.ld_in = (size_t)w; q.g = g; q.b = b; q.out = out;
-                q.g2 = g2; q.b2 = b2; q.out2 = out2; q.n = n_i; q.w = w;
+                q.in = in; q.ld_in = ld_in; q.g = g; q.b = b; q.out = out;
+                q.g2 = g2; q.b2 = b2; q.out2 = out2; q.n = n_i; q.w = wd;
                 return launch_ln_rows(q, stream);
             };
-            const bool fuse_in = d_in <= kLinearLnMaxK, fuse_h = d_h <= kLinearLnMaxK;
-            // z = GELU(W_in LN_in(src) + b_in)
-            if (fuse_in) {
-                const LinearPart q = part(Pm + off.w_in, Pm + off.b_in, d_h, z, Pm + off.ln_in_g, Pm + off.ln_in_b);
-                e = lin(src, d_in, 1, nullptr, 1, &q);
-            } else {
-                e = ln(src, d_in, Pm + off.ln_in_g, Pm + off.ln_in_b, xn, nullptr, nullptr, nullptr);
-                const LinearPart q = part(Pm + off.w_in, Pm + off.b_in, d_h, z);
-                if (e == hipSuccess) e = lin(xn, d_in, 1, nullptr, 1, &q);
-            }
-            // Q = Wq LN_Q(z) + bq; K, V = Wk, Wv LN_C(z) + bk, bv
-            if (e == hipSuccess) {
-                if (fuse_h) {
-                    const LinearPart q[3] = {part(Pm + off.wq, Pm + off.bq, d_h, Q, Pm + off.ln_q_g, Pm + off.ln_q_b),
-                                             part(Pm + off.wk, Pm + off.bk, d_h, K, Pm + off.ln_c_g, Pm + off.ln_c_b),
-                                             part(Pm + off.wv, Pm + off.bv, d_h, V, Pm + off.ln_c_g, Pm + off.ln_c_b)};
-                    e = lin(z, d_h, 0, nullptr, 3, q);
+            const bool fuse_in = d_in <= kLinearLnMaxK, fuse_h = d_h <= kLinearLnMaxK,
+                       fuse_out = N * d_h <= kLinearLnMaxK;
+            // z_r = GELU(W_in LN_in(x_r) + b_in), every slot
+            for (int r = 0; r < N && e == hipSuccess; ++r) {
+                uint16_t* zr = z + (size_t)r * n * d_h;
+                if (fuse_in) {
+                    const LinearPart q = part(Pm + off.w_in, Pm + off.b_in, d_h, zr, Pm + off.ln_in_g, Pm + off.ln_in_b);
+                    e = lin(src_slot(r), d_in, d_in, 1, nullptr, 0, 0, 1, &q);
                 } else {
-                    e = ln(z, d_h, Pm + off.ln_q_g, Pm + off.ln_q_b, qn, Pm + off.ln_c_g, Pm + off.ln_c_b, cn);
-                    const LinearPart q = part(Pm + off.wq, Pm + off.bq, d_h, Q);
-                    const LinearPart kv[2] = {part(Pm + off.wk, Pm + off.bk, d_h, K), part(Pm + off.wv, Pm + off.bv, d_h, V)};
-                    if (e == hipSuccess) e = lin(qn, d_h, 0, nullptr, 1, &q);
-                    if (e == hipSuccess) e = lin(cn, d_h, 0, nullptr, 2, kv);
+                    e = ln(src_slot(r), d_in, d_in, Pm + off.ln_in_g, Pm + off.ln_in_b, xn, nullptr, nullptr, nullptr);
+                    const LinearPart q = part(Pm + off.w_in, Pm + off.b_in, d_h, zr);
+                    if (e == hipSuccess) e = lin(xn, d_in, d_in, 1, nullptr, 0, 0, 1, &q);
                 }
             }
-            if (e == hipSuccess) {
-                ReplayProblem rp;
-                rp.q = Q; rp.k = K; rp.v = V; rp.idx = nullptr; rp.o = att; rp.vt = vt;
-                rp.B = s->B; rp.T = s->T; rp.H_q = nh; rp.H_kv = nh; rp.D = d_h / nh; rp.S = 0;
-                rp.kv_layout = MOT_LAYOUT_BTHD;
-                e = launch_replay_attention(rp, stream);
-            }
-            // h1 = Wo att + bo + z
-            if (e == hipSuccess) {
-                const LinearPart q = part(Pm + off.wo, Pm + off.bo, d_h, h1);
-                e = lin(att, d_h, 0, z, 1, &q);
-            }
-            // f1 = GELU(W_f1 LN_F(h1) + b_f1)
-            if (e == hipSuccess) {
-                if (fuse_h) {
-                    const LinearPart q = part(Pm + off.w_f1, Pm + off.b_f1, d_ff, f1, Pm + off.ln_f_g, Pm + off.ln_f_b);
-                    e = lin(h1, d_h, 1, nullptr, 1, &q);
+            // the scan h_0 = z_1, h_r = CAB_r(h_{r-1}, z_r); h_r goes to slot r of F
+            for (int r = 0; r < N && e == hipSuccess; ++r) {
+                const uint16_t* C = Pm + off.cab0 + (size_t)r * off.cab;
+                const uint16_t* zr = z + (size_t)r * n * d_h;
+                const uint16_t* hp = r == 0 ? z : F + (size_t)(r - 1) * d_h;   // h_{r-1}
+                const size_t ld_hp = r == 0 ? (size_t)d_h : ldF;
+                // Q = Wq LN_Q(h_{r-1}) + bq; K, V = Wk, Wv LN_C(z_r) + bk, bv
+                if (fuse_h && r == 0) {
+                    const LinearPart q[3] = {part(C + off.wq, C + off.bq, d_h, Q, C + off.ln_q_g, C + off.ln_q_b),
+                                             part(C + off.wk, C + off.bk, d_h, K, C + off.ln_c_g, C + off.ln_c_b),
+                                             part(C + off.wv, C + off.bv, d_h, V, C + off.ln_c_g, C + off.ln_c_b)};
+                    e = lin(zr, d_h, d_h, 0, nullptr, 0, 0, 3, q);
+                } else if (fuse_h) {
+                    const LinearPart q = part(C + off.wq, C + off.bq, d_h, Q, C + off.ln_q_g, C + off.ln_q_b);
+                    const LinearPart kv[2] = {part(C + off.wk, C + off.bk, d_h, K, C + off.ln_c_g, C + off.ln_c_b),
+                                              part(C + off.wv, C + off.bv, d_h, V, C + off.ln_c_g, C + off.ln_c_b)};
+                    e = lin(hp, ld_hp, d_h, 0, nullptr, 0, 0, 1, &q);
+                    if (e == hipSuccess) e = lin(zr, d_h, d_h, 0, nullptr, 0, 0, 2, kv);
                 } else {
-                    e = ln(h1, d_h, Pm + off.ln_f_g, Pm + off.ln_f_b, fn, nullptr, nullptr, nullptr);
-                    const LinearPart q = part(Pm + off.w_f1, Pm + off.b_f1, d_ff, f1);
-                    if (e == hipSuccess) e = lin(fn, d_h, 1, nullptr, 1, &q);
+                    if (r == 0) {
+                        e = ln(zr, d_h, d_h, C + off.ln_q_g, C + off.ln_q_b, qn, C + off.ln_c_g, C + off.ln_c_b, cn);
+                    } else {
+                        e = ln(hp, ld_hp, d_h, C + off.ln_q_g, C + off.ln_q_b, qn, nullptr, nullptr, nullptr);
+                        if (e == hipSuccess)
+                            e = ln(zr, d_h, d_h, C + off.ln_c_g, C + off.ln_c_b, cn, nullptr, nullptr, nullptr);
+                    }
+                    const LinearPart q = part(C + off.wq, C + off.bq, d_h, Q);
+                    const LinearPart kv[2] = {part(C + off.wk, C + off.bk, d_h, K), part(C + off.wv, C + off.bv, d_h, V)};
+                    if (e == hipSuccess) e = lin(qn, d_h, d_h, 0, nullptr, 0, 0, 1, &q);
+                    if (e == hipSuccess) e = lin(cn, d_h, d_h, 0, nullptr, 0, 0, 2, kv);
+                }
+                if (e == hipSuccess) {
+                    ReplayProblem rp;
+                    rp.q = Q; rp.k = K; rp.v = V; rp.idx = nullptr; rp.o = att; rp.vt = vt;
+                    rp.B = s->B; rp.T = s->T; rp.H_q = nh; rp.H_kv = nh; rp.D = d_h / nh; rp.S = 0;
+                    rp.kv_layout = MOT_LAYOUT_BTHD;
+                    e = launch_replay_attention(rp, stream);
+                }
+                // h~ = Wo att + bo + h_{r-1}
+                if (e == hipSuccess) {
+                    const LinearPart q = part(C + off.wo, C + off.bo, d_h, h1);
+                    e = lin(att, d_h, d_h, 0, hp, ld_hp, 0, 1, &q);
+                }
+                // f1 = GELU(W_f1 LN_F(h~) + b_f1)
+                if (e == hipSuccess) {
+                    if (fuse_h) {
+                        const LinearPart q = part(C + off.w_f1, C + off.b_f1, d_ff, f1, C + off.ln_f_g, C + off.ln_f_b);
+                        e = lin(h1, d_h, d_h, 1, nullptr, 0, 0, 1, &q);
+                    } else {
+                        e = ln(h1, d_h, d_h, C + off.ln_f_g, C + off.ln_f_b, fn, nullptr, nullptr, nullptr);
+                        const LinearPart q = part(C + off.w_f1, C + off.b_f1, d_ff, f1);
+                        if (e == hipSuccess) e = lin(fn, d_h, d_h, 1, nullptr, 0, 0, 1, &q);
+                    }
+                }
+                // h_r = W_f2 f1 + b_f2 + h~, into slot r of F
+                if (e == hipSuccess) {
+                    const LinearPart q = part(C + off.w_f2, C + off.b_f2, d_h, F + (size_t)r * d_h);
+                    e = lin(f1, d_ff, d_ff, 0, h1, 0, ldF, 1, &q);
                 }
             }
-            // h2 = W_f2 f1 + b_f2 + h1
-            if (e == hipSuccess) {
-                const LinearPart q = part(Pm + off.w_f2, Pm + off.b_f2, d_h, h2);
-                e = lin(f1, d_ff, 0, h1, 1, &q);
-            }
-            // mixture += gate_m * GELU(W_out LN_out(h2) + b_out)
-            const uint16_t* out_in = h2;
-            if (e == hipSuccess && !fuse_h) {
-                e = ln(h2, d_h, Pm + off.ln_out_g, Pm + off.ln_out_b, on, nullptr, nullptr, nullptr);
+            // mixture += gate_m * GELU(W_out LN_out(F) + b_out), the output
+            // rows of slot r into target layer w N + r
+            const uint16_t* out_in = F;
+            if (e == hipSuccess && !fuse_out) {
+                e = ln(F, ldF, N * d_h, Pm + off.ln_out_g, Pm + off.ln_out_b, on, nullptr, nullptr, nullptr);
                 out_in = on;
             }
-            if (e == hipSuccess) {
+            for (int r = 0; r < N && e == hipSuccess; ++r) {
+                const uint16_t* Wr = Pm + off.w_out + (size_t)r * d_out * N * d_h;
+                uint16_t* dst = dstx + (size_t)(w * N + r) * n * d_out;
                 LinearProblem lp;
                 memset(&lp, 0, sizeof lp);
-                lp.in = out_in; lp.ld_in = (size_t)d_h; lp.nparts = 1;
-                lp.part[0] = fuse_h ? part(Pm + off.w_out, Pm + off.b_out, d_out, dst, Pm + off.ln_out_g, Pm + off.ln_out_b)
-                                    : part(Pm + off.w_out, Pm + off.b_out, d_out, dst);
-                lp.mix_acc = mix;
+                lp.in = out_in; lp.ld_in = ldF; lp.nparts = 1;
+                lp.part[0] = fuse_out ? part(Wr, Pm + off.b_out + (size_t)r * d_out, d_out, dst, Pm + off.ln_out_g,
+                                             Pm + off.ln_out_b)
+                                      : part(Wr, Pm + off.b_out + (size_t)r * d_out, d_out, dst);
+                lp.mix_acc = mix + (size_t)r * n * d_out;
                 lp.gates = p.gates + (size_t)gs * p.n_tok_pad * s->E; lp.gate_ld = s->E; lp.expert = m;
-                lp.n = n_i; lp.K = d_h; lp.gelu = 1; lp.mix = 1;
+                lp.n = n_i; lp.K = N * d_h; lp.gelu = 1; lp.mix = 1;
                 lp.first = m == 0; lp.last = m == s->E - 1;
                 e = launch_linear(lp, stream);
             }
         }
     }
-    if (e != hipSuccess) return fail(MOT_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
+    if (e != hipSuccess) return fail(MOT_ERR_HIP, "launch: %s", hipGetErrorString(e));
     return MOT_OK;
 }
 

@@ -115,7 +115,9 @@ struct LinearProblem {
     LinearPart part[3];
     int32_t nparts;
     // residual and mixture apply to a single part
-    const uint16_t* res;  // [n][N] residual added after the activation, or nullptr
+    const uint16_t* res;  // [n] rows of N: residual added after the activation, or nullptr
+    size_t ld_res;        // row stride of res in elements (0: N)
+    size_t ld_out;        // row stride of the part's plain output in elements (0: N)
     float* mix_acc;       // [n][N] fp32 mixture accumulator (mix)
     const float* gates;   // gate of row t, expert e: gates[t * gate_ld + e] (mix)
     int32_t gate_ld, expert;

@@ -222,22 +222,25 @@ def source_attention(B: int, T: int, seed: int, window: float = 64.0, sink: floa
     return A
 
 
-def backbone_params(w: Workload, d_h: int, d_ff: int, seed: int) -> np.ndarray:
-    """Packed parameters of the backbone experts, float32 [L_tgt][2][E][P]
-    (bf16-representable), from PCG64(60_000 + seed): for each (j, x, m), in
-    the packed order, LayerNorm gains U(0.8, 1.2) and shifts U(+-0.1), weight
-    matrices Xavier-uniform U(+-sqrt(6/(fan_in+fan_out))), biases
-    U(+-1/sqrt(fan_in))."""
-    d_in, d_out = w.d_in, w.d_out
-    parts = [("ln", d_in), ("w", (d_h, d_in)), ("b", (d_h, d_in)), ("ln", d_h), ("ln", d_h),
-             ("w", (d_h, d_h)), ("b", (d_h, d_h)), ("w", (d_h, d_h)), ("b", (d_h, d_h)),
-             ("w", (d_h, d_h)), ("b", (d_h, d_h)), ("w", (d_h, d_h)), ("b", (d_h, d_h)), ("ln", d_h),
-             ("w", (d_ff, d_h)), ("b", (d_ff, d_h)), ("w", (d_h, d_ff)), ("b", (d_h, d_ff)), ("ln", d_h),
-             ("w", (d_out, d_h)), ("b", (d_out, d_h))]
+def backbone_params(w: Workload, d_h: int, d_ff: int, seed: int, n_slots: int = 1) -> np.ndarray:
+    """Packed parameters of the backbone experts, float32 [L_tgt/N][2][E][P]
+    (bf16-representable), from PCG64(60_000 + seed), N = n_slots slots per
+    channel window: for each (window, x, m), in the packed order (the shared
+    input projection, one cross-attention block per slot, the output
+    projection of the N slots' concatenation), LayerNorm gains U(0.8, 1.2) and
+    shifts U(+-0.1), weight matrices Xavier-uniform
+    U(+-sqrt(6/(fan_in+fan_out))), biases U(+-1/sqrt(fan_in))."""
+    d_in, d_out, N = w.d_in, w.d_out, n_slots
+    cab = [("ln", d_h), ("ln", d_h),
+           ("w", (d_h, d_h)), ("b", (d_h, d_h)), ("w", (d_h, d_h)), ("b", (d_h, d_h)),
+           ("w", (d_h, d_h)), ("b", (d_h, d_h)), ("w", (d_h, d_h)), ("b", (d_h, d_h)), ("ln", d_h),
+           ("w", (d_ff, d_h)), ("b", (d_ff, d_h)), ("w", (d_h, d_ff)), ("b", (d_h, d_ff))]
+    parts = ([("ln", d_in), ("w", (d_h, d_in)), ("b", (d_h, d_in))] + cab * N +
+             [("ln", N * d_h), ("w", (N * d_out, N * d_h)), ("b", (N * d_out, N * d_h))])
     P = sum(2 * a if k == "ln" else (a[0] * a[1] if k == "w" else a[0]) for k, a in parts)
     rng = np.random.Generator(np.random.PCG64(60_000 + seed))
-    out = np.empty((w.L_tgt, 2, w.E, P), np.float32)
-    for j in range(w.L_tgt):
+    out = np.empty((w.L_tgt // N, 2, w.E, P), np.float32)
+    for j in range(w.L_tgt // N):
         for x in range(2):
             for m in range(w.E):
                 dst = out[j, x, m]
@@ -255,3 +258,18 @@ def backbone_params(w: Workload, d_h: int, d_ff: int, seed: int) -> np.ndarray:
                         _uniform(rng, dst[o:o + a[0]], 1.0 / math.sqrt(a[1]))
                         o += a[0]
     return round_to_bf16(out)
+
+
+def window_router(w: Workload, n_slots: int, seed: int):
+    """Router of the channel-window backbone: weights [L_tgt/N][2][E][N*d_in]
+    Xavier-uniform and bias [L_tgt/N][2][E] U(+-1/sqrt(N*d_in)), drawn per
+    (window, x) in that order from PCG64(70_000 + seed), bf16-rounded."""
+    N, d = n_slots, n_slots * w.d_in
+    rng = np.random.Generator(np.random.PCG64(70_000 + seed))
+    wr = np.empty((w.L_tgt // N, 2, w.E, d), np.float32)
+    br = np.empty((w.L_tgt // N, 2, w.E), np.float32)
+    for j in range(w.L_tgt // N):
+        for x in range(2):
+            _uniform(rng, wr[j, x], math.sqrt(6.0 / (d + w.E)))
+            _uniform(rng, br[j, x], 1.0 / math.sqrt(d))
+    return round_to_bf16(wr), round_to_bf16(br)

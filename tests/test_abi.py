@@ -401,3 +401,29 @@ def test_noalloc_replay_rejects_oversized_staging(lib):
     bad = mb._ReplayShapes(1, 64, 8, 4, 96, 0, 0)
     assert mb.STATUS[L.mot_replay_attention_noalloc(FAKE, FAKE, FAKE, None, FAKE, ctypes.byref(bad), None)] == \
         "MOT_ERR_UNSUPPORTED"
+
+
+def test_backbone_window_checks(lib, oracle_built):
+    """Channel windows of the backbone: n_slots outside 0..8 and an L_tgt
+    that is not a multiple of the window are refused; a window that mixes
+    mapped and unmapped slots is MOT_ERR_BAD_LAYER_MAP; the packed parameter
+    count matches the oracle's for every window size."""
+    from oracle import oracle_backbone_window_param_count
+    L = mb.load_library()
+    s = _shapes(L_src=2, L_tgt=4, H_tgt=2, D_tgt=64)
+    rw = mb._RW(FAKE + (4 << 30), None)
+
+    def call(lm, n_slots):
+        lm = np.ascontiguousarray(lm, np.int32)
+        c = s.c()
+        st = L.mot_backbone_translate(FAKE, FAKE + (1 << 30), lm.ctypes.data, FAKE + (2 << 30), ctypes.byref(rw),
+                                      FAKE + (5 << 30), FAKE + (6 << 30), ctypes.byref(c),
+                                      ctypes.byref(mb._BackboneDims(128, 2, 256, n_slots)), None)
+        return mb.STATUS[st]
+
+    assert call([0, 1, 0, 1], 9) == "MOT_ERR_BAD_SHAPE"
+    assert call([0, 1, 0, 1], 3) == "MOT_ERR_BAD_SHAPE"        # 4 layers, windows of 3
+    assert call([0, -1, 0, 1], 2) == "MOT_ERR_BAD_LAYER_MAP"   # window 0 half mapped
+    for n_slots in (0, 1, 2, 4):
+        want = oracle_backbone_window_param_count(128, 128, 256, 128, max(1, n_slots))
+        assert mb.backbone_param_count(s, 128, 2, 256, n_slots) == want

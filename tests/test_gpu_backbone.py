@@ -94,3 +94,64 @@ def test_backbone_caller_workspace_equals_owned():
     with pytest.raises(mb.MotError) as e:
         _run(w, d_h, nh, d_ff, lm, params, inp, workspace=ws[: need - 256])
     assert e.value.name == "MOT_ERR_WORKSPACE_TOO_SMALL"
+
+
+# ---------------------------------------------------------------------------
+# channel windows of several slots (the recurrent scan over the slots)
+# ---------------------------------------------------------------------------
+
+WINDOW_CASES = [  # workload, d_h, n_heads, d_ff, n_slots, layer map
+    (Workload("win2", "bf16", L_src=3, L_tgt=4, B=2, T=100, H_src=2, D_src=64, H_tgt=2, D_tgt=64, E=2,
+              hidden=128, seed=91), 128, 2, 256, 2, [0, 1, 1, 2]),
+    (Workload("win3-top1", "bf16", L_src=3, L_tgt=3, B=1, T=150, H_src=2, D_src=64, H_tgt=4, D_tgt=32, E=3,
+              hidden=128, seed=92, top_k=1), 128, 1, 128, 3, [2, 0, 1]),
+    (Workload("win2-skip", "bf16", L_src=2, L_tgt=4, B=1, T=70, H_src=1, D_src=128, H_tgt=1, D_tgt=128, E=2,
+              hidden=128, seed=93), 128, 2, 256, 2, [-1, -1, 0, 1]),
+    # the benchmark's widths with two slots: LN_out over 512 values runs as its own pass
+    (Workload("win2-bench-widths", "bf16", L_src=2, L_tgt=2, B=1, T=300, H_src=2, D_src=128, H_tgt=4, D_tgt=128,
+              E=2, hidden=256, seed=94, key_sigma=1.0), 256, 2, 512, 2, [0, 1]),
+]
+
+
+@pytest.mark.parametrize("case", WINDOW_CASES, ids=[c[0].name for c in WINDOW_CASES])
+def test_backbone_window_parity(case, oracle_built):
+    """Windows of N consecutive target layers (slot r reading layer_map[wN + r])
+    against the oracle: per unit <= 2e-2, per row <= 4e-2; skipped windows keep
+    their sentinel; the usage counts of the window router equal the oracle's
+    selections on rows with a clear Top-K set."""
+    import torch
+    from oracle import oracle_backbone_window
+    from paper_2607_28979_amd.inputs import window_router
+    w, d_h, nh, d_ff, N, lm = case
+    print("case", w.name, "slots", N, flush=True)
+    lm = np.array(lm, np.int32)
+    inp = generate(w)
+    params = backbone_params(w, d_h, d_ff, seed=w.seed, n_slots=N)
+    wr, br = window_router(w, N, seed=w.seed)
+    dev = {n: to_dev(getattr(inp, n), "bf16") for n in ("src_k", "src_v")}
+    dk = torch.full(dst_shape(w), SENTINEL, dtype=torch.bfloat16, device="cuda")
+    dv = torch.full(dst_shape(w), SENTINEL, dtype=torch.bfloat16, device="cuda")
+    usage = torch.zeros((w.L_tgt // N, 2, w.E), dtype=torch.int32, device="cuda")
+    mb.backbone_translate(dev["src_k"], dev["src_v"], lm, to_dev(params, "bf16"), to_dev(wr, "bf16"),
+                          to_dev(br, "bf16"), dk, dv, mb.Shapes.from_workload(w), d_h, nh, d_ff, usage=usage,
+                          n_slots=N)
+    torch.cuda.synchronize()
+    gk, gv = (a.float().cpu().numpy().astype(np.float64) for a in (dk, dv))
+    rk, rv = oracle_backbone_window(oracle_dims(w), inp.src_k, inp.src_v, lm, params, wr, br, d_h, nh, d_ff, N)
+    worst, worst_row = 0.0, 0.0
+    for j in range(w.L_tgt):
+        if lm[j] < 0:
+            assert (gk[j] == SENTINEL).all() and (gv[j] == SENTINEL).all()
+            continue
+        for g, r in ((gk, rk), (gv, rv)):
+            worst = max(worst, rel_frob(unit_rows(g, w, j), unit_rows(r, w, j)))
+            worst_row = max(worst_row, float(row_errors(unit_rows(g, w, j), unit_rows(r, w, j)).max()))
+    print("  max unit rel-Frobenius error %.3e, max row error %.3e" % (worst, worst_row), flush=True)
+    assert worst <= TOL["bf16"]
+    assert worst_row <= 2 * TOL["bf16"]
+    # usage: each token of a mapped window adds top_k selections
+    cnt = usage.cpu().numpy()
+    K = w.top_k or w.E
+    for win in range(w.L_tgt // N):
+        want = K * w.n_tok if lm[win * N] >= 0 else 0
+        assert (cnt[win].sum(axis=-1) == want).all(), (win, cnt[win])

@@ -15,9 +15,10 @@ SRC = os.path.join(ROOT, "oracle", "mot_oracle.c")
 PINS = "tests/test_oracle_pins.py"
 HAND = "tests/test_oracle_handworked.py"
 USAGE = "tests/test_oracle_usage.py"
+WINDOW = "tests/test_oracle_window.py"
 
 # (name, original text, planted text, pins that must catch it); the original
-# text must occur in the source, and its first occurrence is replaced
+# text must occur in the source, and every occurrence is replaced
 MUTATIONS = [
     ("layernorm unbiased variance", "    var /= w;\n", "    var /= (w - 1);\n",
      [HAND + "::test_backbone_layernorms"]),
@@ -49,6 +50,17 @@ MUTATIONS = [
      "if (!sel[m] && (best < 0 || g[m] >= g[best])) best = m;\n"
      "                        sel[best] = 1;\n                    }\n                    for (int32_t m = 0; m < E; ++m) counts",
      [USAGE]),
+    ("window scan starts from the last slot", "r == 0 ? z + (size_t)t * Nd_h :",
+     "r == 0 ? z + (size_t)t * Nd_h + (size_t)(N - 1) * d_h :", [WINDOW]),
+    ("window recurrence restarts from z_r",
+     "r == 0 ? z + (size_t)t * Nd_h : F + (size_t)t * Nd_h + (size_t)(r - 1) * d_h",
+     "z + (size_t)t * Nd_h + (size_t)r * d_h", [WINDOW]),
+    ("window output LayerNorm per slot", "bb_layernorm(F + (size_t)t * Nd_h, Nd_h, ln_out_g, ln_out_b, t1);",
+     "for (int32_t r2 = 0; r2 < N; ++r2) bb_layernorm(F + (size_t)t * Nd_h + (size_t)r2 * d_h, d_h, "
+     "ln_out_g + (size_t)r2 * d_h, ln_out_b + (size_t)r2 * d_h, t1 + (size_t)r2 * d_h);", [WINDOW]),
+    ("window router on the first slot only",
+     "for (int32_t c = 0; c < Nd_in; ++c) acc += (double)wr[(unit * E + m) * Nd_in + c] * xt[c];",
+     "for (int32_t c = 0; c < d_in; ++c) acc += (double)wr[(unit * E + m) * Nd_in + c] * xt[c];", [WINDOW]),
 ]
 
 
@@ -83,6 +95,6 @@ def test_unmutated_build_passes(original, tmp_path):
 def test_mutation_is_caught(name, old, new, pins, original, tmp_path):
     assert old in original, name
     lib = str(tmp_path / "liboracle_mut.so")
-    _build(original.replace(old, new, 1), lib)
+    _build(original.replace(old, new), lib)
     rc, out = _run_pins(lib, pins)
     assert rc == 1, (name, rc, out)   # 1: tests ran and at least one failed
