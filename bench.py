@@ -114,6 +114,9 @@ def main():
     ap.add_argument("--backbone", action="store_true",
                     help="time the mixture with the backbone translator body (App. C.2) as its experts "
                          "on the Qwen2.5-1.5B -> 7B cache rows")
+    ap.add_argument("--slots", type=int, default=1,
+                    help="with --backbone: channel-window slots per expert (the recurrent scan over "
+                         "N consecutive target layers' source rows)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain device copy of MIB MiB (a known-size "
                          "reference for the HBM byte counters of a profiler run)")
@@ -545,20 +548,24 @@ def bench_backbone(args):
     import torch
     from paper_2607_28979_amd import binding as mb
     from paper_2607_28979_amd.configs import BACKBONE
-    from paper_2607_28979_amd.inputs import backbone_params, bf16_bits, generate
+    from paper_2607_28979_amd.inputs import backbone_params, bf16_bits, generate, window_router
 
     bw = BACKBONE
     w = bw.kv
+    N = max(1, args.slots)
     torch.cuda.set_device(0)
     t0 = time.time()
     inp = generate(w)
-    params = backbone_params(w, bw.d_h, bw.d_ff, seed=w.seed)
+    params = backbone_params(w, bw.d_h, bw.d_ff, seed=w.seed, n_slots=N)
     log("inputs generated in %.1f s" % (time.time() - t0))
 
     def dev(a):
         return torch.from_numpy(bf16_bits(a).view(np.int16)).cuda().view(torch.bfloat16)
 
     d = {n: dev(getattr(inp, n)) for n in ("src_k", "src_v", "wr", "br")}
+    if N > 1:
+        wr, br = window_router(w, N, seed=w.seed)
+        d["wr"], d["br"] = dev(wr), dev(br)
     pr = dev(params)
     shape = (w.L_tgt, w.B, w.T, w.H_tgt, w.D_tgt)
     dk = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
@@ -568,7 +575,7 @@ def bench_backbone(args):
 
     def step():
         mb.backbone_translate(d["src_k"], d["src_v"], lm, pr, d["wr"], d["br"], dk, dv, shapes, bw.d_h,
-                              bw.n_heads, bw.d_ff)
+                              bw.n_heads, bw.d_ff, n_slots=N)
 
     calibration_copy(args.calibrate_copy)
     for _ in range(args.warmup):
@@ -588,7 +595,7 @@ def bench_backbone(args):
     ms_per_step = wall * 1e3 / args.steps
     call_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
     log("timed %d steps: wall %.3f ms/step, event avg %.3f ms" % (args.steps, ms_per_step, call_ms))
-    flops = bw.flops()
+    flops = bw.flops(N)
     tf = flops / (call_ms / 1e3) / 1e12
     out = {
         "metric": "translated KV tokens/sec (all layers, backbone-translator experts) Qwen2.5-1.5B→7B",
@@ -599,7 +606,8 @@ def bench_backbone(args):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded numpy; shapes of the model pair, random backbone parameters)",
         "config": {"workload": w.name, "L_tgt": w.L_tgt, "B": w.B, "T": w.T, "d_in": w.d_in, "d_out": w.d_out,
-                   "E": w.E, "d_h": bw.d_h, "n_heads": bw.n_heads, "d_ff": bw.d_ff, "parallelism": "single GPU"},
+                   "E": w.E, "d_h": bw.d_h, "n_heads": bw.n_heads, "d_ff": bw.d_ff, "n_slots": N,
+                   "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": "mot_backbone_translate (LayerNorm + linear + causal attention chain)",
                      "achieved": round(tf, 2), "peak": PEAK_TFLOPS["bf16"], "unit": "TFLOP/s",
                      "frac": round(tf / PEAK_TFLOPS["bf16"], 4), "traffic": None, "alg_flops_per_launch": flops},

@@ -178,15 +178,17 @@ class BackboneWorkload:
     n_heads: int
     d_ff: int
 
-    def flops(self) -> float:
-        """Matrix flops of one call: per unit and expert the input, Q, K, V,
-        output, FFN and target projections, and causal attention (scores and
-        values) within each batch row; every expert runs on every token."""
-        w = self.kv
-        per_tok = 2.0 * (w.d_in * self.d_h + 4 * self.d_h * self.d_h + 2 * self.d_h * self.d_ff
-                         + self.d_h * w.d_out)
-        attn = 4.0 * self.d_h * w.B * w.T * (w.T + 1) / 2
-        return w.units() * w.E * (per_tok * w.n_tok + attn)
+    def flops(self, n_slots: int = 1) -> float:
+        """Matrix flops of one call over channel windows of n_slots slots: per
+        (window, K/V) unit and expert, for each slot the input projection, Q,
+        K, V, output and FFN projections and causal attention (scores and
+        values) within each batch row, then the target projection of the
+        slots' concatenation; every expert runs on every token."""
+        w, N = self.kv, n_slots
+        per_tok = 2.0 * (N * (w.d_in * self.d_h + 4 * self.d_h * self.d_h + 2 * self.d_h * self.d_ff)
+                         + (N * self.d_h) * (N * w.d_out))
+        attn = N * 4.0 * self.d_h * w.B * w.T * (w.T + 1) / 2
+        return w.units() // N * w.E * (per_tok * w.n_tok + attn)
 
 
 # Qwen2.5-1.5B -> Qwen2.5-7B cache rows (256 -> 512), B = 8, T = 4096, two

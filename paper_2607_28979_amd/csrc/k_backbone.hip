@@ -38,7 +38,13 @@ __global__ __launch_bounds__(256) void k_ln_rows(LnProblem p) {
     const int row = (blockIdx.x * 4 + (threadIdx.x >> 6)) * RPW + lane / LPR;
     const bool live = row < p.n;
     const int w = p.w;
-    const uint16_t* r = p.in + (size_t)(live ? row : 0) * p.ld_in;
+    const size_t gy = blockIdx.y;
+    const size_t pg = gy * p.p_gs;
+    const uint16_t *pg_g = p.g + pg, *pg_b = p.b + pg;
+    const uint16_t *pg_g2 = p.out2 ? p.g2 + pg : nullptr, *pg_b2 = p.out2 ? p.b2 + pg : nullptr;
+    uint16_t* out = p.out + gy * p.out_gs;
+    uint16_t* out2 = p.out2 ? p.out2 + gy * p.out_gs : nullptr;
+    const uint16_t* r = p.in + gy * p.in_gs + (size_t)(live ? row : 0) * p.ld_in;
     const u32x4 zero = {0u, 0u, 0u, 0u};
     u32x4 q[MAXC];
 #pragma unroll
@@ -50,11 +56,11 @@ __global__ __launch_bounds__(256) void k_ln_rows(LnProblem p) {
     u32x4 gq[MAXC], bq[MAXC], gq2[MAXC], bq2[MAXC];
     if (MAXC == 1) {
         const int e = hl * 8;
-        gq[0] = e < w ? *reinterpret_cast<const u32x4*>(p.g + e) : zero;
-        bq[0] = e < w ? *reinterpret_cast<const u32x4*>(p.b + e) : zero;
-        if (p.out2) {
-            gq2[0] = e < w ? *reinterpret_cast<const u32x4*>(p.g2 + e) : zero;
-            bq2[0] = e < w ? *reinterpret_cast<const u32x4*>(p.b2 + e) : zero;
+        gq[0] = e < w ? *reinterpret_cast<const u32x4*>(pg_g + e) : zero;
+        bq[0] = e < w ? *reinterpret_cast<const u32x4*>(pg_b + e) : zero;
+        if (out2) {
+            gq2[0] = e < w ? *reinterpret_cast<const u32x4*>(pg_g2 + e) : zero;
+            bq2[0] = e < w ? *reinterpret_cast<const u32x4*>(pg_b2 + e) : zero;
         }
     }
     float v[MAXC][8];
@@ -90,8 +96,8 @@ __global__ __launch_bounds__(256) void k_ln_rows(LnProblem p) {
         const int e = (hl + LPR * c) * 8;
         if (e < w) {
             if (MAXC > 1) {
-                gq[c] = *reinterpret_cast<const u32x4*>(p.g + e);
-                bq[c] = *reinterpret_cast<const u32x4*>(p.b + e);
+                gq[c] = *reinterpret_cast<const u32x4*>(pg_g + e);
+                bq[c] = *reinterpret_cast<const u32x4*>(pg_b + e);
             }
             u32x4 o;
 #pragma unroll
@@ -100,11 +106,11 @@ __global__ __launch_bounds__(256) void k_ln_rows(LnProblem p) {
                 const float y1 = (v[c][2 * i + 1] - mean) * inv * bf16_hi(gq[c][i]) + bf16_hi(bq[c][i]);
                 o[i] = pack_bf16x2(y0, y1);
             }
-            *reinterpret_cast<u32x4*>(p.out + (size_t)row * w + e) = o;
-            if (p.out2) {
+            *reinterpret_cast<u32x4*>(out + (size_t)row * w + e) = o;
+            if (out2) {
                 if (MAXC > 1) {
-                    gq2[c] = *reinterpret_cast<const u32x4*>(p.g2 + e);
-                    bq2[c] = *reinterpret_cast<const u32x4*>(p.b2 + e);
+                    gq2[c] = *reinterpret_cast<const u32x4*>(pg_g2 + e);
+                    bq2[c] = *reinterpret_cast<const u32x4*>(pg_b2 + e);
                 }
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
@@ -112,7 +118,7 @@ __global__ __launch_bounds__(256) void k_ln_rows(LnProblem p) {
                     const float y1 = (v[c][2 * i + 1] - mean) * inv * bf16_hi(gq2[c][i]) + bf16_hi(bq2[c][i]);
                     o[i] = pack_bf16x2(y0, y1);
                 }
-                *reinterpret_cast<u32x4*>(p.out2 + (size_t)row * w + e) = o;
+                *reinterpret_cast<u32x4*>(out2 + (size_t)row * w + e) = o;
             }
         }
     }
@@ -143,9 +149,24 @@ __global__ __launch_bounds__(256) void k_linear(LinearProblem p) {
     uint16_t* out = MOT_PART(out);
     const int N = MOT_PART(N);
 #undef MOT_PART
+    // group of a grouped launch
+    const int gz = blockIdx.z;
+    {
+        const size_t wg = (size_t)gz * p.w_gs;
+        W += wg;
+        bias += wg;
+        if (lng) {
+            lng += wg;
+            lnb += wg;
+        }
+        out = p.out_tab[0] ? p.out_tab[gz] : out + (size_t)gz * p.out_gs;
+    }
+    const uint16_t* res = p.res ? p.res + (size_t)gz * p.res_gs : nullptr;
+    float* mix_acc = p.mix ? p.mix_acc + (size_t)gz * p.mix_gs : nullptr;
+    const float* gates = p.mix ? p.gates + (size_t)gz * p.gate_gs : nullptr;
     const int r0 = blockIdx.x * LN_, o0 = y * LM;
     const int K = p.K;
-    const uint16_t* A = p.in;
+    const uint16_t* A = p.in_tab[0] ? p.in_tab[gz / p.tab_div] : p.in + (size_t)gz * p.in_gs;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1, g = lane >> 5, l32 = lane & 31;
     const u32x4 zero = {0u, 0u, 0u, 0u};
@@ -304,11 +325,11 @@ __global__ __launch_bounds__(256) void k_linear(LinearProblem p) {
         // nothing are never used
         const int t = min(r0 + pass * 16 + (tid >> 4), p.n - 1);
         const size_t at = (size_t)t * N + min(oc, N - 8);
-        rres[pass] = p.res ? *reinterpret_cast<const u32x4*>(p.res + (size_t)t * ld_res + min(oc, N - 8)) : zero;
-        rgate[pass] = p.mix ? p.gates[(size_t)t * p.gate_ld + p.expert] : 0.f;
+        rres[pass] = res ? *reinterpret_cast<const u32x4*>(res + (size_t)t * ld_res + min(oc, N - 8)) : zero;
+        rgate[pass] = p.mix ? gates[(size_t)t * p.gate_ld + p.expert] : 0.f;
 #pragma unroll
         for (int i = 0; i < 2; ++i)
-            rmix[pass][i] = p.mix && !p.first ? reinterpret_cast<const f32x4*>(p.mix_acc + at)[i]
+            rmix[pass][i] = p.mix && !p.first ? reinterpret_cast<const f32x4*>(mix_acc + at)[i]
                                               : f32x4{0.f, 0.f, 0.f, 0.f};
     }
     __syncthreads();
@@ -322,7 +343,7 @@ __global__ __launch_bounds__(256) void k_linear(LinearProblem p) {
         const f32x4 hi = stg[tl * 32 + ((2 * h + 1) ^ (tl & 31))];
         float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         const size_t at = (size_t)t * N + oc;   // the fp32 mixture rows are dense
-        if (p.res) {
+        if (res) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 v[2 * i] += bf16_lo(rres[pass][i]);
@@ -337,7 +358,7 @@ __global__ __launch_bounds__(256) void k_linear(LinearProblem p) {
                 m1[i] += rgate[pass] * v[4 + i];
             }
             if (!p.last) {
-                f32x4* accp = reinterpret_cast<f32x4*>(p.mix_acc + at);
+                f32x4* accp = reinterpret_cast<f32x4*>(mix_acc + at);
                 accp[0] = m0;
                 accp[1] = m1;
                 continue;
@@ -358,10 +379,11 @@ __global__ __launch_bounds__(256) void k_linear(LinearProblem p) {
 
 hipError_t launch_ln_rows(const LnProblem& p, hipStream_t stream) {
     if (p.n == 0) return hipSuccess;
+    const unsigned gy = p.groups > 1 ? (unsigned)p.groups : 1u;
     if (p.w <= 256)
-        hipLaunchKernelGGL(k_ln_rows<32>, dim3((p.n + 7) / 8), dim3(256), 0, stream, p);
+        hipLaunchKernelGGL(k_ln_rows<32>, dim3((p.n + 7) / 8, gy), dim3(256), 0, stream, p);
     else
-        hipLaunchKernelGGL(k_ln_rows<64>, dim3((p.n + 3) / 4), dim3(256), 0, stream, p);
+        hipLaunchKernelGGL(k_ln_rows<64>, dim3((p.n + 3) / 4, gy), dim3(256), 0, stream, p);
     return hipGetLastError();
 }
 
@@ -369,7 +391,8 @@ hipError_t launch_linear(const LinearProblem& p, hipStream_t stream) {
     if (p.n == 0) return hipSuccess;
     int tiles = 0;
     for (int q = 0; q < p.nparts; ++q) tiles += (p.part[q].N + LM - 1) / LM;
-    hipLaunchKernelGGL(k_linear, dim3((p.n + LN_ - 1) / LN_, tiles), dim3(256), 0, stream, p);
+    const unsigned gz = p.groups > 1 ? (unsigned)p.groups : 1u;
+    hipLaunchKernelGGL(k_linear, dim3((p.n + LN_ - 1) / LN_, tiles, gz), dim3(256), 0, stream, p);
     return hipGetLastError();
 }
 

@@ -623,31 +623,55 @@ size_t mot_backbone_param_count(const mot_shapes* s, const mot_backbone_dims* bd
 }
 
 namespace {
-// Workspace of the backbone call: gates of every unit, then one unit's
-// activation rows, then the attention's transposed V.  Buffers, in order:
-// LN_in rows, z of the N slots, LN_Q and LN_C rows, Q, K, V, attention,
-// h~, LN_F rows, FFN hidden, Concat(h_1..h_N), its LayerNorm, the fp32
-// mixture of the N target layers, the window's concatenated source rows
+// Workspace of the backbone call: the gates of every unit, then the
+// activations of one batch of ub units, each with its E experts as groups of
+// grouped launches (group g = unit-in-batch * E + expert, every buffer
+// group-major), then the attention's transposed V.  Buffers, in order: LN_in
+// rows [g][n][d_in], z of the N slots [g][N][n][d_h], LN_Q and LN_C rows, Q,
+// K, V, attention, h~, LN_F rows [g][n][d_h], FFN hidden [g][n][d_ff],
+// Concat(h_1..h_N) and its LayerNorm [g][n][N d_h], the fp32 mixture
+// [unit][N][n][d_out], the window's concatenated source rows [unit][n][N d_in]
 // (N > 1: the router's input).
 constexpr int kBbBufs = 15;
+constexpr size_t kBackboneBatchCap = size_t(8) << 30;   // activation bytes per batch of units
 struct BackboneScratch {
-    size_t at[kBbBufs];
+    size_t gates;             // bytes of the gates of every unit
+    size_t at[kBbBufs];       // offsets of the batch buffers
     size_t at_vt;
     size_t total;
 };
-BackboneScratch backbone_scratch(const mot_shapes* s, const mot_backbone_dims* bd, int n_units) {
+// bytes of one unit's share of the batch buffers (its E groups and mixture)
+size_t backbone_unit_bytes(const mot_shapes* s, const mot_backbone_dims* bd) {
     const size_t n = (size_t)s->B * s->T, d_in = (size_t)s->H_src * s->D_src, d_out = (size_t)s->H_tgt * s->D_tgt;
-    const size_t d_h = bd->d_h, d_ff = bd->d_ff, N = backbone_slots(bd);
-    const size_t row_b[kBbBufs] = {d_in * 2, N * d_h * 2, d_h * 2,     d_h * 2,     d_h * 2,
-                                   d_h * 2,  d_h * 2,     d_h * 2,     d_h * 2,     d_h * 2,
-                                   d_ff * 2, N * d_h * 2, N * d_h * 2, N * d_out * 4, N > 1 ? N * d_in * 2 : 0};
+    const size_t d_h = bd->d_h, d_ff = bd->d_ff, N = bd->n_slots > 1 ? bd->n_slots : 1, E = s->E;
+    const size_t per_group = n * 2 * (d_in + N * d_h + 9 * d_h + d_ff + 2 * N * d_h);
+    const size_t vt = replay_vt_bytes(s->B, s->T, bd->n_heads, bd->d_h / bd->n_heads);
+    return E * (per_group + vt) + n * N * d_out * 4 + (N > 1 ? n * N * d_in * 2 : 0) + 16 * kAlign;
+}
+BackboneScratch backbone_scratch(const mot_shapes* s, const mot_backbone_dims* bd, int n_units, int ub) {
+    const size_t n = (size_t)s->B * s->T, d_in = (size_t)s->H_src * s->D_src, d_out = (size_t)s->H_tgt * s->D_tgt;
+    const size_t d_h = bd->d_h, d_ff = bd->d_ff, N = bd->n_slots > 1 ? bd->n_slots : 1;
+    const size_t G = (size_t)ub * s->E;
+    const size_t row_b[kBbBufs] = {G * d_in * 2, G * N * d_h * 2, G * d_h * 2, G * d_h * 2, G * d_h * 2,
+                                   G * d_h * 2,  G * d_h * 2,     G * d_h * 2, G * d_h * 2, G * d_h * 2,
+                                   G * d_ff * 2, G * N * d_h * 2, G * N * d_h * 2,
+                                   (size_t)ub * N * d_out * 4, N > 1 ? (size_t)ub * N * d_in * 2 : 0};
     BackboneScratch b;
-    size_t need = round_up((size_t)n_units * round_up(n, 128) * s->E * 4, kAlign);
+    b.gates = round_up((size_t)n_units * round_up(n, 128) * s->E * 4, kAlign);
+    size_t need = b.gates;
     for (int k = 0; k < kBbBufs; ++k) { b.at[k] = need; need += round_up(n * row_b[k], kAlign); }
     b.at_vt = need;
-    need += round_up(replay_vt_bytes(s->B, s->T, bd->n_heads, bd->d_h / bd->n_heads), kAlign);
+    need += round_up(replay_vt_bytes((int)(s->B * G), s->T, bd->n_heads, bd->d_h / bd->n_heads), kAlign);
     b.total = need;
     return b;
+}
+// units per batch: every unit when they fit the cap, at most kLinearTab
+int backbone_batch(const mot_shapes* s, const mot_backbone_dims* bd, int n_units) {
+    size_t ub = kBackboneBatchCap / backbone_unit_bytes(s, bd);
+    if (ub < 1) ub = 1;
+    if (ub > (size_t)kLinearTab) ub = kLinearTab;
+    if (ub > (size_t)n_units) ub = n_units;
+    return (int)ub;
 }
 
 mot_status check_backbone(const mot_shapes* s, const mot_backbone_dims* bd) {
@@ -681,7 +705,8 @@ size_t mot_backbone_workspace_bytes(const mot_shapes* s, const mot_backbone_dims
     g_err[0] = 0;
     if (check_backbone(s, bd) != MOT_OK) return SIZE_MAX;
     if ((int64_t)s->B * s->T == 0) return 0;
-    return backbone_scratch(s, bd, 2 * s->L_tgt / backbone_slots(bd)).total;
+    const int nu = 2 * s->L_tgt / backbone_slots(bd);
+    return backbone_scratch(s, bd, nu, backbone_batch(s, bd, nu)).total;
 }
 
 mot_status mot_backbone_translate(const void* src_k, const void* src_v, const int32_t* layer_map, const void* params,
@@ -727,17 +752,17 @@ mot_status mot_backbone_translate(const void* src_k, const void* src_v, const in
             for (int x = 0; x < 2; ++x) { ut.code[nu] = unit_code(w, x, layer_map[w * N], nu); ++nu; }
     ut.n = nu;
     if (nu == 0) return MOT_OK;
-    // workspace: gates, then one unit's activations, then V transposed
-    const BackboneScratch sc = backbone_scratch(s, bd, nu);
-    const size_t* at = sc.at;
-    const size_t at_vt = sc.at_vt;
+    // workspace: gates, then one batch of units' activations, then V transposed;
+    // a caller workspace below the default batch's need gets smaller batches
+    int ub = backbone_batch(s, bd, nu);
+    BackboneScratch sc = backbone_scratch(s, bd, nu, ub);
     void* ws = s->workspace;
     if (ws) {
-        const size_t need_all = backbone_scratch(s, bd, 2 * W).total;
         if (!aligned16(ws)) return fail(MOT_ERR_MISALIGNED, "workspace %p is not 16-byte aligned", ws);
+        while (ub > 1 && s->workspace_bytes < sc.total) sc = backbone_scratch(s, bd, nu, --ub);
         if (s->workspace_bytes < sc.total)
-            return fail(MOT_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes, need %zu (%zu for every layer mapped)",
-                        s->workspace_bytes, sc.total, need_all);
+            return fail(MOT_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes, need at least %zu", s->workspace_bytes,
+                        sc.total);
         if (overlaps(ws, sc.total, dst_k, dst_bytes) || overlaps(ws, sc.total, dst_v, dst_bytes) ||
             overlaps(ws, sc.total, src_k, src_bytes) || overlaps(ws, sc.total, src_v, src_bytes))
             return fail(MOT_ERR_BAD_SHAPE, "workspace overlaps a source or destination cache");
@@ -746,174 +771,216 @@ mot_status mot_backbone_translate(const void* src_k, const void* src_v, const in
         if (st != MOT_OK) return st;
     }
     char* w8 = reinterpret_cast<char*>(ws);
-    uint16_t* xn = reinterpret_cast<uint16_t*>(w8 + at[0]);
-    uint16_t* z = reinterpret_cast<uint16_t*>(w8 + at[1]);      // [N][n][d_h]
-    uint16_t* qn = reinterpret_cast<uint16_t*>(w8 + at[2]);
-    uint16_t* cn = reinterpret_cast<uint16_t*>(w8 + at[3]);
-    uint16_t* Q = reinterpret_cast<uint16_t*>(w8 + at[4]);
-    uint16_t* K = reinterpret_cast<uint16_t*>(w8 + at[5]);
-    uint16_t* V = reinterpret_cast<uint16_t*>(w8 + at[6]);
-    uint16_t* att = reinterpret_cast<uint16_t*>(w8 + at[7]);
-    uint16_t* h1 = reinterpret_cast<uint16_t*>(w8 + at[8]);
-    uint16_t* fn = reinterpret_cast<uint16_t*>(w8 + at[9]);
-    uint16_t* f1 = reinterpret_cast<uint16_t*>(w8 + at[10]);
-    uint16_t* F = reinterpret_cast<uint16_t*>(w8 + at[11]);     // [n][N d_h]
-    uint16_t* on = reinterpret_cast<uint16_t*>(w8 + at[12]);    // [n][N d_h]
-    float* mix = reinterpret_cast<float*>(w8 + at[13]);         // [N][n][d_out]
-    uint16_t* xcat = reinterpret_cast<uint16_t*>(w8 + at[14]);  // [n][N d_in]
-    uint16_t* vt = reinterpret_cast<uint16_t*>(w8 + at_vt);
+    auto buf = [&](int k) { return reinterpret_cast<uint16_t*>(w8 + sc.at[k]); };
+    uint16_t *xn = buf(0), *z = buf(1), *qn = buf(2), *cn = buf(3), *Q = buf(4), *K = buf(5), *V = buf(6),
+             *att = buf(7), *h1 = buf(8), *fn = buf(9), *f1 = buf(10), *F = buf(11), *on = buf(12), *xcat = buf(14);
+    float* mix = reinterpret_cast<float*>(w8 + sc.at[13]);   // [unit][N][n][d_out]
+    uint16_t* vt = reinterpret_cast<uint16_t*>(w8 + sc.at_vt);
 
     p.src[0] = src_k; p.src[1] = src_v; p.wr = rw->w; p.br = rw->b;
     p.gates = reinterpret_cast<float*>(ws);
     hipError_t e = hipSuccess;
     if (N == 1) e = launch_router(p, ut, true, stream);   // every unit at once
     const uint16_t* P0 = reinterpret_cast<const uint16_t*>(params);
-    const int n_i = (int)n;
-    const size_t ldF = (size_t)N * d_h;
-    for (int u = 0; u < nu && e == hipSuccess; ++u) {
-        const uint32_t code = ut.code[u];
-        const int w = unit_j(code), x = unit_x(code), gs = unit_gslot(code);
-        const uint16_t* srcx = reinterpret_cast<const uint16_t*>(x ? src_v : src_k);
-        uint16_t* dstx = reinterpret_cast<uint16_t*>(x ? dst_v : dst_k);
-        auto src_slot = [&](int r) { return srcx + (size_t)layer_map[w * N + r] * n * d_in; };
+    const int n_i = (int)n, E = s->E;
+    const size_t ldF = (size_t)N * d_h, P = off.total, nz = n * (size_t)d_h, nF = n * ldF;
+    const bool fuse_in = d_in <= kLinearLnMaxK, fuse_h = d_h <= kLinearLnMaxK, fuse_out = N * d_h <= kLinearLnMaxK;
+    auto pidx = [&](int u) { return unit_j(ut.code[u]) * 2 + unit_x(ut.code[u]); };   // the unit's parameter block
+
+    for (int u0 = 0; u0 < nu && e == hipSuccess;) {
+        // a batch: up to ub units whose parameter blocks are consecutive
+        int nb = 1;
+        while (nb < ub && u0 + nb < nu && pidx(u0 + nb) == pidx(u0) + nb) ++nb;
+        const int G = nb * E;
+        const uint16_t* Pb = P0 + (size_t)pidx(u0) * E * P;   // group g = (u - u0) * E + m at Pb + g * P
+        auto src_slot = [&](int u, int r) {
+            const uint32_t code = ut.code[u];
+            const uint16_t* sx = reinterpret_cast<const uint16_t*>(unit_x(code) ? src_v : src_k);
+            return sx + (size_t)layer_map[unit_j(code) * N + r] * n * d_in;
+        };
         if (N > 1) {
-            // the router reads the window's concatenated source rows
-            for (int r = 0; r < N && e == hipSuccess; ++r)
-                e = hipMemcpy2DAsync(xcat + (size_t)r * d_in, (size_t)N * d_in * 2, src_slot(r), (size_t)d_in * 2,
-                                     (size_t)d_in * 2, n, hipMemcpyDeviceToDevice, stream);
+            // the router reads each window's concatenated source rows
+            static thread_local UnitTab bt;
+            bt.n = nb;
+            for (int u = 0; u < nb && e == hipSuccess; ++u) {
+                const uint32_t code = ut.code[u0 + u];
+                for (int r = 0; r < N && e == hipSuccess; ++r)
+                    e = hipMemcpy2DAsync(xcat + (size_t)u * n * N * d_in + (size_t)r * d_in, (size_t)N * d_in * 2,
+                                         src_slot(u0 + u, r), (size_t)d_in * 2, (size_t)d_in * 2, n,
+                                         hipMemcpyDeviceToDevice, stream);
+                bt.code[u] = unit_code(unit_j(code), unit_x(code), u, unit_gslot(code));
+            }
             Problem pr = p;
             pr.src[0] = pr.src[1] = xcat;
             pr.d_in = N * d_in; pr.H_src = 1; pr.D_src = N * d_in; pr.src_layout = MOT_LAYOUT_BTHD;
-            static thread_local UnitTab one;
-            one.n = 1;
-            one.code[0] = unit_code(w, x, 0, gs);
-            if (e == hipSuccess) e = launch_router(pr, one, true, stream);
+            if (e == hipSuccess) e = launch_router(pr, bt, true, stream);
         }
-        for (int m = 0; m < s->E && e == hipSuccess; ++m) {
-            const uint16_t* Pm = P0 + (((size_t)w * 2 + x) * s->E + m) * off.total;
-            // one linear launch over up to three parts sharing the input rows;
-            // the LayerNorm of a part's input is fused when K <= kLinearLnMaxK,
-            // otherwise it runs as its own pass into the workspace first
-            auto part = [&](const uint16_t* W_, const uint16_t* bias, int N_, uint16_t* out,
-                            const uint16_t* g = nullptr, const uint16_t* b = nullptr) {
-                LinearPart q;
-                q.W = W_; q.bias = bias; q.ln_g = g; q.ln_b = b; q.out = out; q.N = N_;
-                return q;
-            };
-            auto lin = [&](const uint16_t* in, size_t ld_in, int K_, int gelu, const uint16_t* res, size_t ld_res,
-                           size_t ld_out, int np, const LinearPart* ps) {
+        // grouped launches over the batch's G groups (parameters at stride P)
+        auto part = [&](size_t o, int N_, uint16_t* out, size_t ln_g = SIZE_MAX, size_t ln_b = SIZE_MAX) {
+            LinearPart q;
+            q.W = Pb + o; q.bias = nullptr; q.ln_g = ln_g == SIZE_MAX ? nullptr : Pb + ln_g;
+            q.ln_b = ln_b == SIZE_MAX ? nullptr : Pb + ln_b; q.out = out; q.N = N_;
+            return q;
+        };
+        auto lin = [&](const uint16_t* in, size_t ld_in, size_t in_gs, int K_, int gelu, const uint16_t* res,
+                       size_t ld_res, size_t res_gs, size_t ld_out, size_t out_gs, int np, LinearPart* ps,
+                       const size_t* bias_off) {
+            LinearProblem lp;
+            memset(&lp, 0, sizeof lp);
+            lp.in = in; lp.ld_in = ld_in; lp.in_gs = in_gs; lp.res = res; lp.ld_res = ld_res; lp.res_gs = res_gs;
+            lp.ld_out = ld_out; lp.out_gs = out_gs; lp.w_gs = P; lp.groups = G;
+            lp.n = n_i; lp.K = K_; lp.gelu = gelu;
+            lp.nparts = np;
+            for (int q = 0; q < np; ++q) {
+                lp.part[q] = ps[q];
+                lp.part[q].bias = Pb + bias_off[q];
+            }
+            return launch_linear(lp, stream);
+        };
+        // grouped LayerNorm rows (parameters at stride P)
+        auto ln = [&](const uint16_t* in, size_t ld_in, size_t in_gs, int wd, size_t g_off, size_t b_off,
+                      uint16_t* out, size_t out_gs, size_t g2_off, size_t b2_off, uint16_t* out2) {
+            LnProblem q;
+            q.in = in; q.ld_in = ld_in; q.g = Pb + g_off; q.b = Pb + b_off; q.out = out;
+            q.g2 = out2 ? Pb + g2_off : nullptr; q.b2 = out2 ? Pb + b2_off : nullptr; q.out2 = out2;
+            q.n = n_i; q.w = wd; q.groups = G; q.in_gs = in_gs; q.p_gs = P; q.out_gs = out_gs;
+            return launch_ln_rows(q, stream);
+        };
+        // z_r = GELU(W_in LN_in(x_r) + b_in), every slot; the source rows come
+        // from each unit's table entry (groups of one unit share them)
+        for (int r = 0; r < N && e == hipSuccess; ++r) {
+            if (fuse_in) {
                 LinearProblem lp;
                 memset(&lp, 0, sizeof lp);
-                lp.in = in; lp.ld_in = ld_in; lp.res = res; lp.ld_res = ld_res; lp.ld_out = ld_out;
-                lp.n = n_i; lp.K = K_; lp.gelu = gelu;
-                lp.nparts = np;
-                for (int q = 0; q < np; ++q) lp.part[q] = ps[q];
-                return launch_linear(lp, stream);
-            };
-            auto ln = [&](const uint16_t* in, size_t ld_in, int wd, const uint16_t* g, const uint16_t* b, uint16_t* out,
-                          const uint16_t* g2, const uint16_t* b2, uint16_t* out2) {
-                LnProblem q;
-                q.in = in; q.ld_in = ld_in; q.g = g; q.b = b; q.out = out;
-                q.g2 = g2; q.b2 = b2; q.out2 = out2; q.n = n_i; q.w = wd;
-                return launch_ln_rows(q, stream);
-            };
-            const bool fuse_in = d_in <= kLinearLnMaxK, fuse_h = d_h <= kLinearLnMaxK,
-                       fuse_out = N * d_h <= kLinearLnMaxK;
-            // z_r = GELU(W_in LN_in(x_r) + b_in), every slot
-            for (int r = 0; r < N && e == hipSuccess; ++r) {
-                uint16_t* zr = z + (size_t)r * n * d_h;
-                if (fuse_in) {
-                    const LinearPart q = part(Pm + off.w_in, Pm + off.b_in, d_h, zr, Pm + off.ln_in_g, Pm + off.ln_in_b);
-                    e = lin(src_slot(r), d_in, d_in, 1, nullptr, 0, 0, 1, &q);
+                for (int u = 0; u < nb; ++u) lp.in_tab[u] = src_slot(u0 + u, r);
+                lp.tab_div = E;
+                lp.ld_in = d_in; lp.w_gs = P; lp.groups = G;
+                lp.out_gs = N * nz;
+                lp.nparts = 1;
+                lp.part[0] = part(off.w_in, d_h, z + (size_t)r * nz, off.ln_in_g, off.ln_in_b);
+                lp.part[0].bias = Pb + off.b_in;
+                lp.n = n_i; lp.K = d_in; lp.gelu = 1;
+                e = launch_linear(lp, stream);
+            } else {
+                // LN_in per unit (its E experts' parameters as groups), then the projection
+                for (int u = 0; u < nb && e == hipSuccess; ++u) {
+                    LnProblem q;
+                    q.in = src_slot(u0 + u, r); q.ld_in = d_in;
+                    q.g = Pb + (size_t)u * E * P + off.ln_in_g; q.b = Pb + (size_t)u * E * P + off.ln_in_b;
+                    q.g2 = q.b2 = nullptr; q.out2 = nullptr;
+                    q.out = xn + (size_t)u * E * n * d_in;
+                    q.n = n_i; q.w = d_in; q.groups = E; q.in_gs = 0; q.p_gs = P; q.out_gs = n * d_in;
+                    e = launch_ln_rows(q, stream);
+                }
+                LinearPart q = part(off.w_in, d_h, z + (size_t)r * nz);
+                const size_t bo[1] = {off.b_in};
+                if (e == hipSuccess) e = lin(xn, d_in, n * d_in, d_in, 1, nullptr, 0, 0, 0, N * nz, 1, &q, bo);
+            }
+        }
+        // the scan h_0 = z_1, h_r = CAB_r(h_{r-1}, z_r); h_r goes to slot r of F
+        for (int r = 0; r < N && e == hipSuccess; ++r) {
+            const size_t C = off.cab0 + (size_t)r * off.cab;
+            const uint16_t* zr = z + (size_t)r * nz;
+            const uint16_t* hp = r == 0 ? z : F + (size_t)(r - 1) * d_h;   // h_{r-1}
+            const size_t ld_hp = r == 0 ? (size_t)d_h : ldF, hp_gs = r == 0 ? N * nz : nF;
+            // Q = Wq LN_Q(h_{r-1}) + bq; K, V = Wk, Wv LN_C(z_r) + bk, bv
+            if (fuse_h && r == 0) {
+                LinearPart q[3] = {part(C + off.wq, d_h, Q, C + off.ln_q_g, C + off.ln_q_b),
+                                   part(C + off.wk, d_h, K, C + off.ln_c_g, C + off.ln_c_b),
+                                   part(C + off.wv, d_h, V, C + off.ln_c_g, C + off.ln_c_b)};
+                const size_t bo[3] = {C + off.bq, C + off.bk, C + off.bv};
+                e = lin(zr, d_h, N * nz, d_h, 0, nullptr, 0, 0, 0, nz, 3, q, bo);
+            } else if (fuse_h) {
+                LinearPart q = part(C + off.wq, d_h, Q, C + off.ln_q_g, C + off.ln_q_b);
+                LinearPart kv[2] = {part(C + off.wk, d_h, K, C + off.ln_c_g, C + off.ln_c_b),
+                                    part(C + off.wv, d_h, V, C + off.ln_c_g, C + off.ln_c_b)};
+                const size_t bq[1] = {C + off.bq}, bkv[2] = {C + off.bk, C + off.bv};
+                e = lin(hp, ld_hp, hp_gs, d_h, 0, nullptr, 0, 0, 0, nz, 1, &q, bq);
+                if (e == hipSuccess) e = lin(zr, d_h, N * nz, d_h, 0, nullptr, 0, 0, 0, nz, 2, kv, bkv);
+            } else {
+                if (r == 0) {
+                    e = ln(zr, d_h, N * nz, d_h, C + off.ln_q_g, C + off.ln_q_b, qn, nz, C + off.ln_c_g,
+                           C + off.ln_c_b, cn);
                 } else {
-                    e = ln(src_slot(r), d_in, d_in, Pm + off.ln_in_g, Pm + off.ln_in_b, xn, nullptr, nullptr, nullptr);
-                    const LinearPart q = part(Pm + off.w_in, Pm + off.b_in, d_h, zr);
-                    if (e == hipSuccess) e = lin(xn, d_in, d_in, 1, nullptr, 0, 0, 1, &q);
+                    e = ln(hp, ld_hp, hp_gs, d_h, C + off.ln_q_g, C + off.ln_q_b, qn, nz, 0, 0, nullptr);
+                    if (e == hipSuccess)
+                        e = ln(zr, d_h, N * nz, d_h, C + off.ln_c_g, C + off.ln_c_b, cn, nz, 0, 0, nullptr);
                 }
+                LinearPart q = part(C + off.wq, d_h, Q);
+                LinearPart kv[2] = {part(C + off.wk, d_h, K), part(C + off.wv, d_h, V)};
+                const size_t bq[1] = {C + off.bq}, bkv[2] = {C + off.bk, C + off.bv};
+                if (e == hipSuccess) e = lin(qn, d_h, nz, d_h, 0, nullptr, 0, 0, 0, nz, 1, &q, bq);
+                if (e == hipSuccess) e = lin(cn, d_h, nz, d_h, 0, nullptr, 0, 0, 0, nz, 2, kv, bkv);
             }
-            // the scan h_0 = z_1, h_r = CAB_r(h_{r-1}, z_r); h_r goes to slot r of F
-            for (int r = 0; r < N && e == hipSuccess; ++r) {
-                const uint16_t* C = Pm + off.cab0 + (size_t)r * off.cab;
-                const uint16_t* zr = z + (size_t)r * n * d_h;
-                const uint16_t* hp = r == 0 ? z : F + (size_t)(r - 1) * d_h;   // h_{r-1}
-                const size_t ld_hp = r == 0 ? (size_t)d_h : ldF;
-                // Q = Wq LN_Q(h_{r-1}) + bq; K, V = Wk, Wv LN_C(z_r) + bk, bv
-                if (fuse_h && r == 0) {
-                    const LinearPart q[3] = {part(C + off.wq, C + off.bq, d_h, Q, C + off.ln_q_g, C + off.ln_q_b),
-                                             part(C + off.wk, C + off.bk, d_h, K, C + off.ln_c_g, C + off.ln_c_b),
-                                             part(C + off.wv, C + off.bv, d_h, V, C + off.ln_c_g, C + off.ln_c_b)};
-                    e = lin(zr, d_h, d_h, 0, nullptr, 0, 0, 3, q);
-                } else if (fuse_h) {
-                    const LinearPart q = part(C + off.wq, C + off.bq, d_h, Q, C + off.ln_q_g, C + off.ln_q_b);
-                    const LinearPart kv[2] = {part(C + off.wk, C + off.bk, d_h, K, C + off.ln_c_g, C + off.ln_c_b),
-                                              part(C + off.wv, C + off.bv, d_h, V, C + off.ln_c_g, C + off.ln_c_b)};
-                    e = lin(hp, ld_hp, d_h, 0, nullptr, 0, 0, 1, &q);
-                    if (e == hipSuccess) e = lin(zr, d_h, d_h, 0, nullptr, 0, 0, 2, kv);
+            // causal attention of every group at once: (group, batch row) is the batch index
+            if (e == hipSuccess) {
+                ReplayProblem rp;
+                rp.q = Q; rp.k = K; rp.v = V; rp.idx = nullptr; rp.o = att; rp.vt = vt;
+                rp.B = s->B * G; rp.T = s->T; rp.H_q = nh; rp.H_kv = nh; rp.D = d_h / nh; rp.S = 0;
+                rp.kv_layout = MOT_LAYOUT_BTHD;
+                e = launch_replay_attention(rp, stream);
+            }
+            // h~ = Wo att + bo + h_{r-1}
+            if (e == hipSuccess) {
+                LinearPart q = part(C + off.wo, d_h, h1);
+                const size_t bo[1] = {C + off.bo};
+                e = lin(att, d_h, nz, d_h, 0, hp, ld_hp, hp_gs, 0, nz, 1, &q, bo);
+            }
+            // f1 = GELU(W_f1 LN_F(h~) + b_f1)
+            if (e == hipSuccess) {
+                const size_t bo[1] = {C + off.b_f1};
+                if (fuse_h) {
+                    LinearPart q = part(C + off.w_f1, d_ff, f1, C + off.ln_f_g, C + off.ln_f_b);
+                    e = lin(h1, d_h, nz, d_h, 1, nullptr, 0, 0, 0, n * d_ff, 1, &q, bo);
                 } else {
-                    if (r == 0) {
-                        e = ln(zr, d_h, d_h, C + off.ln_q_g, C + off.ln_q_b, qn, C + off.ln_c_g, C + off.ln_c_b, cn);
-                    } else {
-                        e = ln(hp, ld_hp, d_h, C + off.ln_q_g, C + off.ln_q_b, qn, nullptr, nullptr, nullptr);
-                        if (e == hipSuccess)
-                            e = ln(zr, d_h, d_h, C + off.ln_c_g, C + off.ln_c_b, cn, nullptr, nullptr, nullptr);
-                    }
-                    const LinearPart q = part(C + off.wq, C + off.bq, d_h, Q);
-                    const LinearPart kv[2] = {part(C + off.wk, C + off.bk, d_h, K), part(C + off.wv, C + off.bv, d_h, V)};
-                    if (e == hipSuccess) e = lin(qn, d_h, d_h, 0, nullptr, 0, 0, 1, &q);
-                    if (e == hipSuccess) e = lin(cn, d_h, d_h, 0, nullptr, 0, 0, 2, kv);
-                }
-                if (e == hipSuccess) {
-                    ReplayProblem rp;
-                    rp.q = Q; rp.k = K; rp.v = V; rp.idx = nullptr; rp.o = att; rp.vt = vt;
-                    rp.B = s->B; rp.T = s->T; rp.H_q = nh; rp.H_kv = nh; rp.D = d_h / nh; rp.S = 0;
-                    rp.kv_layout = MOT_LAYOUT_BTHD;
-                    e = launch_replay_attention(rp, stream);
-                }
-                // h~ = Wo att + bo + h_{r-1}
-                if (e == hipSuccess) {
-                    const LinearPart q = part(C + off.wo, C + off.bo, d_h, h1);
-                    e = lin(att, d_h, d_h, 0, hp, ld_hp, 0, 1, &q);
-                }
-                // f1 = GELU(W_f1 LN_F(h~) + b_f1)
-                if (e == hipSuccess) {
-                    if (fuse_h) {
-                        const LinearPart q = part(C + off.w_f1, C + off.b_f1, d_ff, f1, C + off.ln_f_g, C + off.ln_f_b);
-                        e = lin(h1, d_h, d_h, 1, nullptr, 0, 0, 1, &q);
-                    } else {
-                        e = ln(h1, d_h, d_h, C + off.ln_f_g, C + off.ln_f_b, fn, nullptr, nullptr, nullptr);
-                        const LinearPart q = part(C + off.w_f1, C + off.b_f1, d_ff, f1);
-                        if (e == hipSuccess) e = lin(fn, d_h, d_h, 1, nullptr, 0, 0, 1, &q);
-                    }
-                }
-                // h_r = W_f2 f1 + b_f2 + h~, into slot r of F
-                if (e == hipSuccess) {
-                    const LinearPart q = part(C + off.w_f2, C + off.b_f2, d_h, F + (size_t)r * d_h);
-                    e = lin(f1, d_ff, d_ff, 0, h1, 0, ldF, 1, &q);
+                    e = ln(h1, d_h, nz, d_h, C + off.ln_f_g, C + off.ln_f_b, fn, nz, 0, 0, nullptr);
+                    LinearPart q = part(C + off.w_f1, d_ff, f1);
+                    if (e == hipSuccess) e = lin(fn, d_h, nz, d_h, 1, nullptr, 0, 0, 0, n * d_ff, 1, &q, bo);
                 }
             }
-            // mixture += gate_m * GELU(W_out LN_out(F) + b_out), the output
-            // rows of slot r into target layer w N + r
-            const uint16_t* out_in = F;
-            if (e == hipSuccess && !fuse_out) {
-                e = ln(F, ldF, N * d_h, Pm + off.ln_out_g, Pm + off.ln_out_b, on, nullptr, nullptr, nullptr);
-                out_in = on;
+            // h_r = W_f2 f1 + b_f2 + h~, into slot r of F
+            if (e == hipSuccess) {
+                LinearPart q = part(C + off.w_f2, d_h, F + (size_t)r * d_h);
+                const size_t bo[1] = {C + off.b_f2};
+                e = lin(f1, d_ff, n * d_ff, d_ff, 0, h1, d_h, nz, ldF, nF, 1, &q, bo);
             }
+        }
+        // mixture += gate_m * GELU(W_out LN_out(F) + b_out): one launch per
+        // expert (in order) and slot over the batch's units, slot r of unit u
+        // into its target layer w N + r
+        const uint16_t* out_in = F;
+        if (e == hipSuccess && !fuse_out) {
+            e = ln(F, ldF, nF, N * d_h, off.ln_out_g, off.ln_out_b, on, nF, 0, 0, nullptr);
+            out_in = on;
+        }
+        for (int m = 0; m < E && e == hipSuccess; ++m) {
             for (int r = 0; r < N && e == hipSuccess; ++r) {
-                const uint16_t* Wr = Pm + off.w_out + (size_t)r * d_out * N * d_h;
-                uint16_t* dst = dstx + (size_t)(w * N + r) * n * d_out;
                 LinearProblem lp;
                 memset(&lp, 0, sizeof lp);
-                lp.in = out_in; lp.ld_in = ldF; lp.nparts = 1;
-                lp.part[0] = fuse_out ? part(Wr, Pm + off.b_out + (size_t)r * d_out, d_out, dst, Pm + off.ln_out_g,
-                                             Pm + off.ln_out_b)
-                                      : part(Wr, Pm + off.b_out + (size_t)r * d_out, d_out, dst);
-                lp.mix_acc = mix + (size_t)r * n * d_out;
-                lp.gates = p.gates + (size_t)gs * p.n_tok_pad * s->E; lp.gate_ld = s->E; lp.expert = m;
+                const uint16_t* Pm = Pb + (size_t)m * P;
+                lp.in = out_in + (size_t)m * nF; lp.ld_in = ldF; lp.in_gs = (size_t)E * nF;
+                lp.w_gs = (size_t)E * P; lp.groups = nb;
+                lp.nparts = 1;
+                lp.part[0].W = Pm + off.w_out + (size_t)r * d_out * N * d_h;
+                lp.part[0].bias = Pm + off.b_out + (size_t)r * d_out;
+                lp.part[0].ln_g = fuse_out ? Pm + off.ln_out_g : nullptr;
+                lp.part[0].ln_b = fuse_out ? Pm + off.ln_out_b : nullptr;
+                lp.part[0].N = d_out;
+                for (int u = 0; u < nb; ++u) {
+                    const uint32_t code = ut.code[u0 + u];
+                    lp.out_tab[u] = reinterpret_cast<uint16_t*>(unit_x(code) ? dst_v : dst_k) +
+                                    (size_t)(unit_j(code) * N + r) * n * d_out;
+                }
+                lp.part[0].out = lp.out_tab[0];
+                lp.mix_acc = mix + (size_t)r * n * d_out; lp.mix_gs = (size_t)N * n * d_out;
+                lp.gates = p.gates + (size_t)unit_gslot(ut.code[u0]) * p.n_tok_pad * E;
+                lp.gate_gs = (size_t)p.n_tok_pad * E; lp.gate_ld = E; lp.expert = m;
                 lp.n = n_i; lp.K = N * d_h; lp.gelu = 1; lp.mix = 1;
-                lp.first = m == 0; lp.last = m == s->E - 1;
+                lp.first = m == 0; lp.last = m == E - 1;
                 e = launch_linear(lp, stream);
             }
         }
+        u0 += nb;
     }
     if (e != hipSuccess) return fail(MOT_ERR_HIP, "launch: %s", hipGetErrorString(e));
     return MOT_OK;

@@ -109,6 +109,12 @@ struct LinearPart {
     int32_t N;
 };
 constexpr int kLinearLnMaxK = 256;
+constexpr int kLinearTab = 64;   // pointer-table entries of a grouped launch
+// Grouped launches: blockIdx.z = group g < groups (0 or 1: one group).  The
+// input rows, W, bias and LayerNorm parameters, output, residual, mixture and
+// gates of group g sit at their pointer plus g times their group stride; a
+// non-null in_tab[0] gives the input rows of group g as in_tab[g / tab_div]
+// instead, a non-null out_tab[0] the output as out_tab[g].
 struct LinearProblem {
     const uint16_t* in;   // [n] rows of K inputs, row stride ld_in elements
     size_t ld_in;
@@ -123,6 +129,10 @@ struct LinearProblem {
     int32_t gate_ld, expert;
     int32_t n, K;
     int32_t gelu, mix, first, last;
+    int32_t groups, tab_div;
+    size_t in_gs, w_gs, out_gs, res_gs, mix_gs, gate_gs;
+    const uint16_t* in_tab[kLinearTab];
+    uint16_t* out_tab[kLinearTab];
 };
 
 // LayerNorm of n bf16 rows of width w (w % 8 == 0, w <= 4096): out = LN(in; g, b)
@@ -133,6 +143,11 @@ struct LnProblem {
     const uint16_t *g, *b, *g2, *b2;   // [w] each
     uint16_t *out, *out2;              // [n][w]
     int32_t n, w;
+    // grouped launches (blockIdx.y = group g < groups; 0 or 1: one): the rows
+    // of group g at in + g * in_gs, its parameters at g, b, g2, b2 + g * p_gs,
+    // its outputs at out, out2 + g * out_gs
+    int32_t groups;
+    size_t in_gs, p_gs, out_gs;
 };
 
 hipError_t launch_ln_rows(const LnProblem& p, hipStream_t stream);

@@ -78,8 +78,9 @@ def test_backbone_parity(case, oracle_built):
 
 def test_backbone_caller_workspace_equals_owned():
     """A caller-owned workspace of mot_backbone_workspace_bytes gives the
-    same bits as the library's own buffer; a smaller one is refused before
-    anything runs (the destination keeps its sentinel)."""
+    same bits as the library's own buffer; a smaller one runs the units in
+    smaller grouped batches, with the same bits; one below a single unit's
+    need is refused before anything runs."""
     import torch
     w, d_h, nh, d_ff = CASES[0]
     inp = generate(w)
@@ -89,10 +90,11 @@ def test_backbone_caller_workspace_equals_owned():
     ws = torch.empty(need, dtype=torch.uint8, device="cuda")
     ws.fill_(0xA5)
     a = _run(w, d_h, nh, d_ff, lm, params, inp)
-    b = _run(w, d_h, nh, d_ff, lm, params, inp, workspace=ws)
-    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    for size in (need, need - 256, need // 3):
+        b = _run(w, d_h, nh, d_ff, lm, params, inp, workspace=ws[:size])
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]), size
     with pytest.raises(mb.MotError) as e:
-        _run(w, d_h, nh, d_ff, lm, params, inp, workspace=ws[: need - 256])
+        _run(w, d_h, nh, d_ff, lm, params, inp, workspace=ws[:4096])
     assert e.value.name == "MOT_ERR_WORKSPACE_TOO_SMALL"
 
 
