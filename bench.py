@@ -30,17 +30,22 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def measured_traffic(kernel_file: str, workload_tag: str):
-    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
-    summary, or None when that summary was taken on a different kernel source
-    (its recorded hash of the kernel's source file no longer matches)."""
+def measured_traffic(kernel_files, prefix: str, workload_tag: str):
+    """HBM bytes per call from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
+    summary `profiles/<prefix>_<workload_tag>_hbm_traffic.md`, or None when
+    that summary is missing or was taken on different kernel sources (its
+    recorded hash of the concatenated source files no longer matches)."""
     import hashlib
-    src = os.path.join(ROOT, "paper_2607_28979_amd", "csrc", kernel_file)
-    prof = os.path.join(ROOT, "profiles", "%s_%s_hbm_traffic.md" % (kernel_file.split(".")[0].replace("_kernel", ""),
-                                                                    workload_tag))
-    if not (os.path.exists(src) and os.path.exists(prof)):
+    if isinstance(kernel_files, str):
+        kernel_files = [kernel_files]
+    srcs = [os.path.join(ROOT, "paper_2607_28979_amd", "csrc", f) for f in kernel_files]
+    prof = os.path.join(ROOT, "profiles", "%s_%s_hbm_traffic.md" % (prefix, workload_tag))
+    if not (all(os.path.exists(s) for s in srcs) and os.path.exists(prof)):
         return None
-    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for s in srcs:
+        h.update(open(s, "rb").read())
+    digest = h.hexdigest()[:16]
     vals = {}
     for line in open(prof):
         if "=" in line and not line.startswith("|"):
@@ -52,6 +57,11 @@ def measured_traffic(kernel_file: str, workload_tag: str):
         return float(vals["traffic_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+# file-name tags of the five model pairs, in workload order
+WORKLOAD_TAGS = ["gpt2-small-opt-125m", "qwen2.5-0.5b-0.5b", "opt-1.3b-qwen2.5-1.5b", "qwen2.5-1.5b-7b",
+                 "qwen2.5-7b-7b-32k"]
 
 
 def host_cpu() -> dict:
@@ -212,8 +222,12 @@ def main():
         "peak": peak,
         "unit": "TFLOP/s",
         "frac": round(achieved_tflops / peak, 4),
-        "traffic": (measured_traffic("k_bf16_fused_kernel.h", "qwen2.5-1.5b-7b")
-                    if fused and args.workload == 3 and not args.top_k else None),
+        "traffic": (None if routed or args.top_k else
+                    measured_traffic("k_bf16_fused_kernel.h", "k_bf16_fused", WORKLOAD_TAGS[args.workload]) if fused
+                    else measured_traffic(["k_router.hip", "k_f32.hip"], "mot_translate_f32",
+                                          WORKLOAD_TAGS[args.workload]) if w.dtype == "f32"
+                    else measured_traffic(["k_router.hip", "k_bf16_unfused.hip", "k_bf16_gemm256.hip"], "mot_translate_two_gemm",
+                                          WORKLOAD_TAGS[args.workload])),
         "alg_flops_per_launch": flops,
         "alg_bytes_per_launch": w.alg_bytes(),
         "hbm_gbs_alg": round(w.alg_bytes() / (avg_call_ms / 1e3) / 1e9, 1),
@@ -491,7 +505,7 @@ def bench_replay(args):
     dom = max(share, key=share.get)
     kname = {"select": "k_topS_select", "sparse": "k_sparse_attn", "causal": "k_causal_attn"}
     roof = dict(rows[dom], kernel=kname[dom],
-                traffic=measured_traffic("k_replay.hip", "qwen2.5-7b-replay-8k") if dom == "sparse" else None)
+                traffic=measured_traffic("k_replay.hip", "k_replay", "qwen2.5-7b-replay-8k") if dom == "sparse" else None)
     cpu = None if args.no_cpu_baseline else cpu_baseline_replay(w, args.cpu_rows)
     out_line = {
         "metric": "replayed context tokens/sec (all target layers, Top-S source-guided sparse attention)",

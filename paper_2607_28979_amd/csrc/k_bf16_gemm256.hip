@@ -1,0 +1,402 @@
+// Two-GEMM bf16 translation path, large-tile form: the same two products as
+// k_bf16_unfused.hip (translator layer 1 with its gated GELU epilogue, then
+// layer 2 whose K axis runs over every expert's hidden units so the gated sum
+// of the mixture, paper Sec. 3 Eq. mot_definition, is reduced inside the
+// accumulator), on 256 x 256 output tiles.
+//
+//   gemm1: Hs[u][t][m*hidden+k] = bf16( g[u][t][m] * GELU((W1_m z_t + b1_m)[k]) )
+//          MFMA A = W1 rows (hidden), B = source rows (tokens)
+//   gemm2: dst[j][t][o] = bf16( sum_kk W2cat[o][kk] Hs[u][t][kk] + sum_m g_m b2_m[o] )
+//          MFMA A = W2cat rows (outputs), B = hidden rows (tokens)
+//
+// One 256-thread workgroup per CU (128 KB of LDS): four waves in a 2 x 2
+// grid, 128 x 128 outputs per wave = 4 x 4 blocks of v_mfma_f32_32x32x16_bf16
+// (256 accumulators per lane, held in the AGPR half of the register file).
+// Per 64-wide K slice a tile moves 64 KB into LDS for 2 * 256 * 256 * 64
+// flops (128 flop/B, twice the 128 x 128 form's), which keeps the L2->CU
+// and LDS rates well under their limits at the matrix cores' rate.
+//
+// Operands go global -> LDS directly (buffer_load_dwordx4 ... lds, 16 bytes
+// per lane, through a buffer descriptor per operand; the MUBUF form rather
+// than global_load_lds, whose FLAT encoding makes the compiler's wait
+// insertion treat every later LDS read as out of order and wait for all of
+// them): a wave's load fills 1 KB of LDS = 8 rows of 8 16-byte chunks, and the lane
+// order within those rows is chosen so that row r stores logical chunk c at
+// physical chunk c ^ ((r >> 1) & 7).  Sixteen lanes of a fragment read (16
+// consecutive rows, one logical chunk) then hit 16 distinct 16-byte bank
+// groups.  Two LDS stages; the loads of slice k+1 are issued before the MFMAs
+// of slice k, and one barrier per slice retires both.
+//
+// Bias terms enter through the accumulators' initial values: gemm1 starts
+// from b1 (each lane's rows are 4 consecutive hidden units), gemm2 from two
+// extra 32x32x16 products B2 . G with the gates split into a bf16 high part
+// and a bf16 residual (K = 16 covers E <= 16 experts).
+#include "mot_device.h"
+#include "mot_internal.h"
+#include "../../include/mot.h"
+
+namespace mot {
+
+namespace {
+
+constexpr int kTile = 256, kBK = 64;
+constexpr int kStage = 2 * kTile * 8;   // 16-byte slots per stage (A then B)
+constexpr int kGroup = 32;              // B tiles per dispatch group
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+// Raw buffer over `bytes` bytes at `base` (reads past the end return 0).
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, size_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0,
+                                             (int)(bytes < 0xFFFFFFFFu ? bytes : 0xFFFFFFFFu), 0x00020000);
+}
+
+__device__ __forceinline__ void load_lds16(rsrc_t r, uint32_t off, u32x4* lds_dst_wave_base) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds_dst_wave_base, 16, off, 0, 0, 0);
+}
+
+// Dispatch order: groups of kGroup consecutive B tiles (tokens), A tiles
+// outer within a group.  Workgroups go round-robin to the 8 XCDs, so an XCD's
+// 32 resident workgroups cover 4 token tiles x 8 A tiles of one group: 12
+// distinct operand tiles per K slice instead of up to 64.
+__device__ __forceinline__ void tile_of(int lin, int nA, int nB, int& a_tile, int& b_tile) {
+    const int grp = lin / (kGroup * nA);
+    const int gsz = min(kGroup, nB - kGroup * grp);
+    const int r = lin - grp * kGroup * nA;
+    b_tile = kGroup * grp + r % gsz;
+    a_tile = r / gsz;
+}
+
+__device__ __forceinline__ uint32_t src_row_bytes(const Problem& p, int tok) {
+    if (p.src_layout == MOT_LAYOUT_BTHD) return (uint32_t)tok * p.d_in * 2;
+    const int b = tok / p.T, t = tok % p.T;
+    return ((uint32_t)b * p.H_src * p.T + t) * p.D_src * 2;
+}
+__device__ __forceinline__ uint32_t src_k_bytes(const Problem& p, int k) {
+    if (p.src_layout == MOT_LAYOUT_BTHD) return (uint32_t)k * 2;
+    return ((uint32_t)(k / p.D_src) * p.T * p.D_src + k % p.D_src) * 2;
+}
+
+// The K loop shared by both products.  rowA/rowB: this lane's 8 + 8 row byte
+// offsets into the operands' buffers (rows 8J + lane/8 of the tile,
+// J = wave*8 + q); kofs(kt, par, &a, &b)
+// gives the byte offsets of logical chunk c of slice kt for the two chunk
+// parities (par = q & 1).  acc holds the initial values on entry.
+//
+// Register double buffering: the fragments of k-step s+1 are read while the
+// 16 MFMAs of step s run.  The slice's barrier sits before the MFMAs of its
+// last k-step (whose fragments are already in registers), and the first
+// fragments of the next slice are read right after it, so the matrix core
+// has queued work across the barrier.
+template <class KOfs>
+__device__ __forceinline__ void k_loop(u32x4* lds, rsrc_t bufA, rsrc_t bufB, const uint32_t (&rowA)[8],
+                                       const uint32_t (&rowB)[8], int nk, KOfs kofs, f32x16 (&acc)[4][4]) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1, g = lane >> 5, l32 = lane & 31;
+    const int sw = (l32 >> 1) & 7;
+
+    auto issue = [&](int kt, int st) {
+        uint32_t oa[2], ob[2];
+        kofs(kt, 0, oa[0], ob[0]);
+        kofs(kt, 1, oa[1], ob[1]);
+        u32x4* base = lds + st * kStage + wave * 8 * 64;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) load_lds16(bufA, rowA[q] + oa[q & 1], base + q * 64);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) load_lds16(bufB, rowB[q] + ob[q & 1], base + kTile * 8 + q * 64);
+    };
+    // fragments of k-step s of stage st: rows wm*128 + i*32 + l32 (A) and
+    // wn*128 + i*32 + l32 (B), logical chunk 2s + g
+    auto read = [&](int st, int s, u32x4 (&a)[4], u32x4 (&b)[4]) {
+        const u32x4* la = lds + st * kStage + (wm * 128 + l32) * 8;
+        const u32x4* lb = lds + st * kStage + kTile * 8 + (wn * 128 + l32) * 8;
+        const int c = (2 * s + g) ^ sw;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            a[i] = la[i * 32 * 8 + c];
+            b[i] = lb[i * 32 * 8 + c];
+        }
+    };
+    auto mma = [&](const u32x4 (&a)[4], const u32x4 (&b)[4]) {
+#pragma unroll
+        for (int bm = 0; bm < 4; ++bm)
+#pragma unroll
+            for (int bn = 0; bn < 4; ++bn) acc[bm][bn] = mfma_32x32x16(a[bm], b[bn], acc[bm][bn]);
+    };
+
+    u32x4 a0[4], b0[4], a1[4], b1[4];
+    issue(0, 0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    read(0, 0, a0, b0);
+    for (int kt = 0; kt < nk; ++kt) {
+        const int st = kt & 1;
+        const bool more = kt + 1 < nk;
+        // sched_barrier fences keep each read group ahead of the MFMAs that
+        // precede its use (the scheduler would otherwise sink the reads next
+        // to their first use and expose the LDS latency)
+        if (more) issue(kt + 1, st ^ 1);
+        read(st, 1, a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(a0, b0);
+        __builtin_amdgcn_sched_barrier(0);
+        read(st, 2, a0, b0);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
+        read(st, 3, a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(a0, b0);
+        __builtin_amdgcn_sched_barrier(0);
+        // every wave's reads of stage st are in registers and its loads of
+        // slice kt+1 have landed: stage st^1 is complete, stage st is free
+        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (more) read(st ^ 1, 0, a0, b0);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// gemm1.  grid: x = (hidden tiles) x (token tiles) in dispatch order, z = unit
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256, 1) void k_bf16_gemm1_256(Problem p, UnitTab ut) {
+    __shared__ u32x4 lds[2 * kStage];
+    const uint32_t code = ut.code[blockIdx.z];
+    const int j = unit_j(code), x = unit_x(code), i = unit_i(code), gs = unit_gslot(code);
+    const int EH = p.E * p.hidden;
+    const int nA = (EH + kTile - 1) / kTile, nB = (p.n_tok + kTile - 1) / kTile;
+    int at, bt;
+    tile_of(blockIdx.x, nA, nB, at, bt);
+    const int hid0 = at * kTile, tok0 = bt * kTile;
+    const size_t unit = (size_t)j * p.streams + x;
+    const rsrc_t bufA = make_rsrc(reinterpret_cast<const char*>(p.w1) + unit * EH * p.d_in * 2,
+                                  (size_t)EH * p.d_in * 2);
+    const rsrc_t bufB = make_rsrc(reinterpret_cast<const char*>(p.src[x]) + (size_t)i * p.n_tok * p.d_in * 2,
+                                  (size_t)p.n_tok * p.d_in * 2);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int L = lane >> 3, pc = lane & 7;
+    const int c0 = pc ^ (L >> 1), c1 = pc ^ (4 + (L >> 1));
+
+    uint32_t rowA[8], rowB[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        const int J = wave * 8 + q;
+        rowA[q] = (uint32_t)min(hid0 + 8 * J + L, EH - 1) * p.d_in * 2;
+        rowB[q] = src_row_bytes(p, min(tok0 + 8 * J + L, p.n_tok - 1));
+    }
+    auto kofs = [&](int kt, int par, uint32_t& oa, uint32_t& ob) {
+        const int k = kt * kBK + 8 * (par ? c1 : c0);
+        oa = (uint32_t)k * 2;
+        ob = (uint32_t)src_k_bytes(p, k);
+    };
+
+    // accumulators start at b1: lane rows of block bm are hidden
+    // hid0 + wm*128 + bm*32 + 8*ii + 4*g + jj
+    const int wm = wave >> 1, wn = wave & 1, g = lane >> 5, l32 = lane & 31;
+    const uint16_t* b1 = p.b1 ? reinterpret_cast<const uint16_t*>(p.b1) + unit * EH : nullptr;
+    f32x16 acc[4][4];
+#pragma unroll
+    for (int bm = 0; bm < 4; ++bm) {
+        const int hb = min(hid0 + wm * 128 + bm * 32, EH - 32);
+        f32x16 init;
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii) {
+            u32x2 w = {0u, 0u};
+            if (b1) w = *reinterpret_cast<const u32x2*>(b1 + hb + 8 * ii + 4 * g);
+            init[4 * ii + 0] = bf16_lo(w[0]);
+            init[4 * ii + 1] = bf16_hi(w[0]);
+            init[4 * ii + 2] = bf16_lo(w[1]);
+            init[4 * ii + 3] = bf16_hi(w[1]);
+        }
+#pragma unroll
+        for (int bn = 0; bn < 4; ++bn) acc[bm][bn] = init;
+    }
+
+    k_loop(lds, bufA, bufB, rowA, rowB, p.d_in / kBK, kofs, acc);
+
+    // epilogue: GELU, * gate, round to bf16, fragment-native hidden store
+    // (16-byte units of 8 hidden values of one token, [t/32][kk/8][t%32])
+    uint16_t* H = reinterpret_cast<uint16_t*>(p.hbuf) + (size_t)blockIdx.z * p.n_tok_pad * EH;
+    const float* G = p.gates + (size_t)gs * p.n_tok_pad * p.E;
+#pragma unroll
+    for (int bm = 0; bm < 4; ++bm) {
+        const int hbase = hid0 + wm * 128 + bm * 32;
+        if (hbase >= EH) continue;
+        const int e = hbase / p.hidden;   // hidden % 64 == 0: one expert per 32 rows
+#pragma unroll
+        for (int bn = 0; bn < 4; ++bn) {
+            const int tc = tok0 + wn * 128 + bn * 32 + l32;
+            if (tc >= p.n_tok_pad) continue;
+            const float gate = tc < p.n_tok ? G[(size_t)tc * p.E + e] : 0.f;
+            uint16_t* hrow = H + ((size_t)(tc >> 5) * (EH >> 3) + (hbase >> 3)) * 256 + (tc & 31) * 8 + 4 * g;
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii) {
+                float v[4];
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const float a = acc[bm][bn][4 * ii + jj];
+                    v[jj] = gate * (p.act == MOT_ACT_GELU ? gelu_tanh(a) : a);
+                }
+                u32x2 w = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+                *reinterpret_cast<u32x2*>(hrow + (size_t)ii * 256) = w;
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// gemm2.  grid: x = (output tiles) x (token tiles) in dispatch order, z = unit
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256, 1) void k_bf16_gemm2_256(Problem p, UnitTab ut) {
+    __shared__ u32x4 lds[2 * kStage];
+    const uint32_t code = ut.code[blockIdx.z];
+    const int j = unit_j(code), x = unit_x(code), gs = unit_gslot(code);
+    const int EH = p.E * p.hidden;
+    const int nA = (p.d_out + kTile - 1) / kTile, nB = (p.n_tok + kTile - 1) / kTile;
+    int at, bt;
+    tile_of(blockIdx.x, nA, nB, at, bt);
+    const int out0 = at * kTile, tok0 = bt * kTile;
+    const size_t unit = (size_t)j * p.streams + x;
+    const rsrc_t bufA = make_rsrc(reinterpret_cast<const char*>(p.w2) + unit * p.E * p.d_out * p.hidden * 2,
+                                  (size_t)p.E * p.d_out * p.hidden * 2);
+    const rsrc_t bufB = make_rsrc(reinterpret_cast<const char*>(p.hbuf) + (size_t)blockIdx.z * p.n_tok_pad * EH * 2,
+                                  (size_t)p.n_tok_pad * EH * 2);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int L = lane >> 3, pc = lane & 7;
+    const int c0 = pc ^ (L >> 1), c1 = pc ^ (4 + (L >> 1));
+
+    uint32_t rowA[8], rowB[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        const int J = wave * 8 + q;
+        const int o = min(out0 + 8 * J + L, p.d_out - 1);
+        const int t = min(tok0 + 8 * J + L, p.n_tok - 1);
+        rowA[q] = (uint32_t)o * p.hidden * 2;
+        rowB[q] = ((uint32_t)(t >> 5) * (EH >> 3) * 256 + (t & 31) * 8) * 2;
+    }
+    auto kofs = [&](int kt, int par, uint32_t& oa, uint32_t& ob) {
+        const int k0 = kt * kBK, m = k0 / p.hidden, c = par ? c1 : c0;
+        oa = ((uint32_t)m * p.d_out * p.hidden + (k0 - m * p.hidden) + 8 * c) * 2;
+        ob = (uint32_t)((k0 >> 3) + c) * 512;
+    };
+
+    // accumulators start at sum_m b2_m[o] g_m[t]: two 32x32x16 products with
+    // A[o][m] = b2_m[o] and B[t][m] = the gate's bf16 high part, then its
+    // bf16 residual (m < E <= 16; k = 8*g .. 8*g+7 in each lane)
+    const int wm = wave >> 1, wn = wave & 1, g = lane >> 5, l32 = lane & 31;
+    const uint16_t* b2 = p.b2 ? reinterpret_cast<const uint16_t*>(p.b2) + unit * p.E * p.d_out : nullptr;
+    const float* G = p.gates + (size_t)gs * p.n_tok_pad * p.E;
+    f32x16 acc[4][4];
+#pragma unroll
+    for (int bm = 0; bm < 4; ++bm)
+#pragma unroll
+        for (int bn = 0; bn < 4; ++bn)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[bm][bn][e] = 0.f;
+    if (b2) {
+        u32x4 ghi[4], glo[4];
+#pragma unroll
+        for (int bn = 0; bn < 4; ++bn) {
+            const int t = tok0 + wn * 128 + bn * 32 + l32;
+            float gv[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int m = 8 * g + e;
+                gv[e] = (m < p.E && t < p.n_tok) ? G[(size_t)t * p.E + m] : 0.f;
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t h = pack_bf16x2(gv[2 * e], gv[2 * e + 1]);
+                ghi[bn][e] = h;
+                glo[bn][e] = pack_bf16x2(gv[2 * e] - bf16_lo(h), gv[2 * e + 1] - bf16_hi(h));
+            }
+        }
+#pragma unroll
+        for (int bm = 0; bm < 4; ++bm) {
+            const int o = min(out0 + wm * 128 + bm * 32 + l32, p.d_out - 1);
+            u32x4 bb;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int m = 8 * g + 2 * e;
+                const uint32_t lo = m < p.E ? b2[(size_t)m * p.d_out + o] : 0u;
+                const uint32_t hi = m + 1 < p.E ? b2[(size_t)(m + 1) * p.d_out + o] : 0u;
+                bb[e] = lo | (hi << 16);
+            }
+#pragma unroll
+            for (int bn = 0; bn < 4; ++bn) {
+                acc[bm][bn] = mfma_32x32x16(bb, ghi[bn], acc[bm][bn]);
+                acc[bm][bn] = mfma_32x32x16(bb, glo[bn], acc[bm][bn]);
+            }
+        }
+    }
+
+    k_loop(lds, bufA, bufB, rowA, rowB, EH / kBK, kofs, acc);
+
+    // epilogue: round to bf16, four consecutive outputs of one token per store
+    uint16_t* dst = reinterpret_cast<uint16_t*>(p.dst[x]) + (size_t)j * p.n_tok * p.d_out;
+#pragma unroll
+    for (int bm = 0; bm < 4; ++bm) {
+        const int obase = out0 + wm * 128 + bm * 32;
+        if (obase >= p.d_out) continue;   // d_out % 32 == 0
+#pragma unroll
+        for (int bn = 0; bn < 4; ++bn) {
+            const int t = tok0 + wn * 128 + bn * 32 + l32;
+            if (t >= p.n_tok) continue;
+            size_t row;
+            int hs = 0;
+            if (p.dst_layout == MOT_LAYOUT_BTHD) {
+                row = (size_t)t * p.d_out;
+            } else {
+                const int b = t / p.T, tt = t % p.T;
+                row = ((size_t)b * p.H_tgt * p.T + tt) * p.D_tgt;
+                hs = p.T * p.D_tgt;
+            }
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii) {
+                const int o = obase + 8 * ii + 4 * g;   // D_tgt % 8 == 0: o .. o+3 in one head
+                const size_t off = p.dst_layout == MOT_LAYOUT_BTHD
+                                       ? row + o
+                                       : row + (size_t)(o / p.D_tgt) * hs + o % p.D_tgt;
+                u32x2 w = {pack_bf16x2(acc[bm][bn][4 * ii], acc[bm][bn][4 * ii + 1]),
+                           pack_bf16x2(acc[bm][bn][4 * ii + 2], acc[bm][bn][4 * ii + 3])};
+                *reinterpret_cast<u32x2*>(dst + off) = w;
+            }
+        }
+    }
+}
+
+}  // namespace
+
+// Large tiles pay when a launch has at least one round of workgroups.
+bool bf16_gemm256_fits(const Problem& p, int n_units) {
+    const int EH = p.E * p.hidden;
+    const long t = (p.n_tok + kTile - 1) / kTile;
+    const long g1 = t * ((EH + kTile - 1) / kTile) * n_units;
+    // every operand region is addressed with 32-bit byte offsets
+    const size_t lim = (size_t)1 << 31;
+    const size_t w1 = (size_t)EH * p.d_in * 2, src = (size_t)p.n_tok * p.d_in * 2;
+    const size_t hb = (size_t)p.n_tok_pad * EH * 2, w2 = (size_t)EH * p.d_out * 2;
+    return p.E <= 16 && g1 >= 128 && w1 < lim && src < lim && hb < lim && w2 < lim;
+}
+
+hipError_t launch_bf16_gemm1_256(const Problem& p, const UnitTab& ut, hipStream_t stream) {
+    if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
+    const int EH = p.E * p.hidden;
+    dim3 grid(((EH + kTile - 1) / kTile) * ((p.n_tok + kTile - 1) / kTile), 1, ut.n);
+    hipLaunchKernelGGL(k_bf16_gemm1_256, grid, dim3(256), 0, stream, p, ut);
+    return hipGetLastError();
+}
+
+hipError_t launch_bf16_gemm2_256(const Problem& p, const UnitTab& ut, hipStream_t stream) {
+    if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
+    dim3 grid(((p.d_out + kTile - 1) / kTile) * ((p.n_tok + kTile - 1) / kTile), 1, ut.n);
+    hipLaunchKernelGGL(k_bf16_gemm2_256, grid, dim3(256), 0, stream, p, ut);
+    return hipGetLastError();
+}
+
+}  // namespace mot

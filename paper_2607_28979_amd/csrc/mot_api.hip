@@ -363,7 +363,10 @@ mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* la
             const int n = pl.n_units - u0 < group ? pl.n_units - u0 : group;
             ut.n = n;
             memcpy(ut.code, pl.codes + u0, sizeof(uint32_t) * n);
-            if (pl.bf16) {
+            if (pl.bf16 && bf16_gemm256_fits(p, n)) {
+                e = launch_bf16_gemm1_256(p, ut, stream);
+                if (e == hipSuccess) e = launch_bf16_gemm2_256(p, ut, stream);
+            } else if (pl.bf16) {
                 e = launch_bf16_gemm1(p, ut, stream);
                 if (e == hipSuccess) e = launch_bf16_gemm2(p, ut, stream);
             } else {

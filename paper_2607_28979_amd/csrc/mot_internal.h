@@ -161,6 +161,11 @@ hipError_t launch_f32_gemm1(const Problem& p, const UnitTab& ut, hipStream_t str
 hipError_t launch_f32_gemm2(const Problem& p, const UnitTab& ut, hipStream_t stream);
 hipError_t launch_bf16_gemm1(const Problem& p, const UnitTab& ut, hipStream_t stream);
 hipError_t launch_bf16_gemm2(const Problem& p, const UnitTab& ut, hipStream_t stream);
+// 256 x 256-tile forms of the same two products (k_bf16_gemm256.hip), used
+// when a launch of n_units units fills at least half a round of the chip
+bool bf16_gemm256_fits(const Problem& p, int n_units);
+hipError_t launch_bf16_gemm1_256(const Problem& p, const UnitTab& ut, hipStream_t stream);
+hipError_t launch_bf16_gemm2_256(const Problem& p, const UnitTab& ut, hipStream_t stream);
 // Fused single-kernel path (router + both layers + mix + store); returns
 // hipErrorNotSupported when the sizes have no fused instantiation.
 bool fused_supported(const Problem& p);
