@@ -132,8 +132,18 @@ __device__ __forceinline__ int w1_perm(int r) {
     return 8 * q + 4 * hh + jj;
 }
 
-__device__ __forceinline__ void load_lds16(const void* gsrc, u32x4* lds_dst_wave_base) {
-    __builtin_amdgcn_global_load_lds(gsrc, (lds_void*)lds_dst_wave_base, 16, 0, 0);
+// Weight loads go straight into LDS through a buffer descriptor
+// (buffer_load_dwordx4 ... lds): 16 bytes per lane at voff (per lane) + soff
+// (wave-uniform).  The MUBUF form, not global_load_lds: a pending FLAT-family
+// load makes the compiler's wait insertion drain every outstanding LDS read
+// (lgkmcnt(0)) before each use of an LDS operand, which defeats the layer-2
+// waves' operand lookahead.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ void load_lds16(rsrc_t r, uint32_t voff, uint32_t soff, u32x4* lds_dst_wave_base) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds_dst_wave_base, 16, voff, soff, 0, 0);
 }
 
 // Per-lane choice between two registers as a bitwise blend, so the compiler
@@ -237,14 +247,16 @@ void k_bf16_fused(Problem p, UnitTab ut) {
     const uint32_t w2_lane = (uint32_t)((t_ld >> 2) * hidden + ((t_ld & 3) ^ ((t_ld >> 4) & 3)) * 8) * 2u;
     // chunk c of W1 (round r) into stage st; the chunk base is wave-uniform,
     // so each load is a scalar base plus a per-lane offset
+    const rsrc_t w1buf = make_rsrc(W1u, (uint32_t)EH * D_IN * 2);
+    const rsrc_t w2buf = make_rsrc(W2u, (uint32_t)EH * D_OUT * 2);
     auto load_w1_round = [&](int c, int st, int r, uint32_t lane_off) {
-        const char* base = reinterpret_cast<const char*>(W1u + (size_t)c * 32 * D_IN + w1_perm(r * RS) * D_IN);
-        load_lds16(base + lane_off, W1s + st * C::W1_CH + r * 64 * NLD + lw * 64);
+        const uint32_t soff = (uint32_t)(c * 32 * D_IN + w1_perm(r * RS) * D_IN) * 2u;
+        load_lds16(w1buf, lane_off, soff, W1s + st * C::W1_CH + r * 64 * NLD + lw * 64);
     };
     // W2 columns [kk, kk+32) of translator m (round r) into stage st
     auto load_w2_round = [&](int m, int kk, int st, int r) {
-        const char* base = reinterpret_cast<const char*>(W2u + ((size_t)m * D_OUT + 16 * NLD * r) * hidden + kk);
-        load_lds16(base + w2_lane, W2s + st * C::W2_CH + r * 64 * NLD + lw * 64);
+        const uint32_t soff = (uint32_t)((m * D_OUT + 16 * NLD * r) * hidden + kk) * 2u;
+        load_lds16(w2buf, w2_lane, soff, W2s + st * C::W2_CH + r * 64 * NLD + lw * 64);
     };
     const int nch = EH / 32;   // >= 2
     // The three roles run the same number of workgroup barriers: two around
