@@ -83,17 +83,19 @@ typedef enum { MOT_ALGO_AUTO = 0, MOT_ALGO_UNFUSED = 1, MOT_ALGO_FUSED = 2, MOT_
  *   src_layout     layout of each source layer: BTHD [B][T][H][D] or BHTD
  *   dst_layout     layout of each target layer, same encoding
  *   act            MOT_ACT_GELU (the method) or MOT_ACT_IDENTITY (tests)
- *   algo           kernel path: MOT_ALGO_AUTO picks (ROUTED when top_k < E and
- *                  the fused kernel fits, else FUSED when it fits, else
- *                  UNFUSED); MOT_ALGO_FUSED = one kernel per token tile over
- *                  every translator (bf16 only; d_in and d_out in
- *                  {128, 256, 512}; no workspace); MOT_ALGO_ROUTED = the same
- *                  shapes, Top-K sparse: a router pass writes each token's
- *                  top_k translators, a per-unit counting sort groups the
- *                  (token, translator) pairs by translator, the fused kernel
- *                  runs each translator only on its tokens, and for top_k > 1
- *                  a combine sums each token's top_k rows (workspace needed);
- *                  MOT_ALGO_UNFUSED = router, then two grouped GEMMs through a
+ *   algo           kernel path: MOT_ALGO_AUTO picks (bf16: ROUTED when
+ *                  top_k < E, else FUSED when the fused kernel fits, else
+ *                  UNFUSED; fp32: UNFUSED); MOT_ALGO_FUSED = one kernel per
+ *                  token tile over every translator (bf16 only; d_in and d_out
+ *                  in {128, 256, 512}; no workspace); MOT_ALGO_ROUTED = Top-K
+ *                  sparse (bf16 only): a router pass writes each token's top_k
+ *                  translators, a per-unit counting sort groups the (token,
+ *                  translator) pairs by translator, each translator runs only
+ *                  on its tokens (the fused kernel over translator tiles where
+ *                  it fits, else the two GEMMs over translator tiles of up to
+ *                  256 pairs), and for top_k > 1 a combine sums each token's
+ *                  top_k rows (workspace needed); MOT_ALGO_UNFUSED = router,
+ *                  then two grouped GEMMs over every translator through a
  *                  hidden-activation workspace.  Requesting an impossible path
  *                  returns MOT_ERR_UNSUPPORTED.  All paths compute the same
  *                  function.

@@ -83,6 +83,9 @@ typedef __attribute__((address_space(3))) void lds_void;
 #endif
 // Wave priority (s_setprio) of the layer-1 waves during their MFMA slots
 // (0: the default priority throughout)
+#ifndef MOT_FUSED_L2_LOOK
+#define MOT_FUSED_L2_LOOK 2   // layer-2 operand reads issued this many MFMA slots ahead
+#endif
 #ifndef MOT_FUSED_L1_PRIO
 #define MOT_FUSED_L1_PRIO 0
 #endif
@@ -680,7 +683,7 @@ void k_bf16_fused(Problem p, UnitTab ut) {
         auto l2_iter = [&](auto l2c, auto w1c, auto w2c, int c, int c_w1, int m_w2, int kk_w2, int st_w2) {
             constexpr bool do_l2 = decltype(l2c)::value, do_w1 = decltype(w1c)::value,
                            do_w2 = decltype(w2c)::value;
-            constexpr int NM = 2 * TB * C::NBW, LOOK = 2;
+            constexpr int NM = 2 * TB * C::NBW, LOOK = MOT_FUSED_L2_LOOK;
             constexpr int NV = W1_RL + W2_RL;
             const u32x4* Hc = Hs + (c & 1) * C::H_CH;          // chunk c-2 shares c's parity
             const u32x4* W2c = W2s + ((c + C::NW2 - 2) % C::NW2) * C::W2_CH;

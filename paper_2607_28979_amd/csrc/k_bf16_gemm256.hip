@@ -161,20 +161,84 @@ __device__ __forceinline__ void k_loop(u32x4* lds, rsrc_t bufA, rsrc_t bufB, con
     }
 }
 
+// Accumulators of block (bm, bn) start at the bias products of a 32-row
+// block of A rows and a 32-column block of B columns: D[r][t] = sum_m
+// bias_m[r] gate_m[t] over m < nm <= 16, as two 32x32x16 MFMAs with the gates
+// split into a bf16 high part and a bf16 residual.  bias(m, r) and gate(m, t)
+// return the values for this lane's row r (m = 8*g .. 8*g+7) and column t.
+template <class BiasF, class GateF>
+__device__ __forceinline__ void seed_bias(f32x16 (&acc)[4][4], int nm, BiasF bias, GateF gate, int row0,
+                                          int col0) {
+    const int lane = threadIdx.x & 63, g = lane >> 5, l32 = lane & 31;
+    u32x4 ghi[4], glo[4];
+#pragma unroll
+    for (int bn = 0; bn < 4; ++bn) {
+        const int t = col0 + bn * 32 + l32;
+        float gv[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) gv[e] = 8 * g + e < nm ? gate(8 * g + e, t) : 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t h = pack_bf16x2(gv[2 * e], gv[2 * e + 1]);
+            ghi[bn][e] = h;
+            glo[bn][e] = pack_bf16x2(gv[2 * e] - bf16_lo(h), gv[2 * e + 1] - bf16_hi(h));
+        }
+    }
+#pragma unroll
+    for (int bm = 0; bm < 4; ++bm) {
+        const int r = row0 + bm * 32 + l32;
+        u32x4 bb;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int m = 8 * g + 2 * e;
+            const uint32_t lo = m < nm ? bias(m, r) : 0u;
+            const uint32_t hi = m + 1 < nm ? bias(m + 1, r) : 0u;
+            bb[e] = lo | (hi << 16);
+        }
+#pragma unroll
+        for (int bn = 0; bn < 4; ++bn) {
+            acc[bm][bn] = mfma_32x32x16(bb, ghi[bn], acc[bm][bn]);
+            acc[bm][bn] = mfma_32x32x16(bb, glo[bn], acc[bm][bn]);
+        }
+    }
+}
+
+// Rows of the routed path's hidden buffer per unit: assignments rounded up to
+// a 32-row fragment group.
+__device__ __forceinline__ size_t routed_hidden_elems(const Problem& p) {
+    return ((size_t)p.n_tok * p.top_k + 31) / 32 * 32 * p.hidden;
+}
+
 // ---------------------------------------------------------------------------
 // gemm1.  grid: x = (hidden tiles) x (token tiles) in dispatch order, z = unit
+// in the launch.  ROUTED: the token tiles are the routing plan's tiles (up to
+// 256 assignments of one translator m); the B rows are gathered by token
+// index, A is W1_m, and the hidden rows are stored in assignment order with
+// the assignment's gate.
 // ---------------------------------------------------------------------------
+template <bool ROUTED>
 __global__ __launch_bounds__(256, 1) void k_bf16_gemm1_256(Problem p, UnitTab ut) {
     __shared__ u32x4 lds[2 * kStage];
     const uint32_t code = ut.code[blockIdx.z];
     const int j = unit_j(code), x = unit_x(code), i = unit_i(code), gs = unit_gslot(code);
-    const int EH = p.E * p.hidden;
-    const int nA = (EH + kTile - 1) / kTile, nB = (p.n_tok + kTile - 1) / kTile;
+    // A rows: E*hidden (dense) or the hidden units of one translator (routed)
+    const int EH = ROUTED ? p.hidden : p.E * p.hidden;
+    const int nA = (EH + kTile - 1) / kTile;
+    const int nB = ROUTED ? p.rt.max_tiles : (p.n_tok + kTile - 1) / kTile;
     int at, bt;
     tile_of(blockIdx.x, nA, nB, at, bt);
+    int m = 0, first = 0, rows = 0;
+    const int32_t* list = nullptr;
+    if constexpr (ROUTED) {
+        if (bt >= p.rt.ntiles[gs]) return;
+        const int4 tl = p.rt.tiles[(size_t)gs * p.rt.max_tiles + bt];
+        m = tl.x; first = tl.y; rows = tl.z;
+        list = p.rt.list + (size_t)gs * p.n_tok * p.top_k;
+    }
     const int hid0 = at * kTile, tok0 = bt * kTile;
     const size_t unit = (size_t)j * p.streams + x;
-    const rsrc_t bufA = make_rsrc(reinterpret_cast<const char*>(p.w1) + unit * EH * p.d_in * 2,
+    const size_t wsel = ROUTED ? unit * p.E + m : unit;   // W1 block: [EH][d_in]
+    const rsrc_t bufA = make_rsrc(reinterpret_cast<const char*>(p.w1) + wsel * EH * p.d_in * 2,
                                   (size_t)EH * p.d_in * 2);
     const rsrc_t bufB = make_rsrc(reinterpret_cast<const char*>(p.src[x]) + (size_t)i * p.n_tok * p.d_in * 2,
                                   (size_t)p.n_tok * p.d_in * 2);
@@ -187,7 +251,8 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm1_256(Problem p, UnitTab ut
     for (int q = 0; q < 8; ++q) {
         const int J = wave * 8 + q;
         rowA[q] = (uint32_t)min(hid0 + 8 * J + L, EH - 1) * p.d_in * 2;
-        rowB[q] = src_row_bytes(p, min(tok0 + 8 * J + L, p.n_tok - 1));
+        const int tok = ROUTED ? list[first + min(8 * J + L, rows - 1)] : min(tok0 + 8 * J + L, p.n_tok - 1);
+        rowB[q] = src_row_bytes(p, tok);
     }
     auto kofs = [&](int kt, int par, uint32_t& oa, uint32_t& ob) {
         const int k = kt * kBK + 8 * (par ? c1 : c0);
@@ -198,7 +263,7 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm1_256(Problem p, UnitTab ut
     // accumulators start at b1: lane rows of block bm are hidden
     // hid0 + wm*128 + bm*32 + 8*ii + 4*g + jj
     const int wm = wave >> 1, wn = wave & 1, g = lane >> 5, l32 = lane & 31;
-    const uint16_t* b1 = p.b1 ? reinterpret_cast<const uint16_t*>(p.b1) + unit * EH : nullptr;
+    const uint16_t* b1 = p.b1 ? reinterpret_cast<const uint16_t*>(p.b1) + wsel * EH : nullptr;
     f32x16 acc[4][4];
 #pragma unroll
     for (int bm = 0; bm < 4; ++bm) {
@@ -220,9 +285,13 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm1_256(Problem p, UnitTab ut
     k_loop(lds, bufA, bufB, rowA, rowB, p.d_in / kBK, kofs, acc);
 
     // epilogue: GELU, * gate, round to bf16, fragment-native hidden store
-    // (16-byte units of 8 hidden values of one token, [t/32][kk/8][t%32])
-    uint16_t* H = reinterpret_cast<uint16_t*>(p.hbuf) + (size_t)blockIdx.z * p.n_tok_pad * EH;
-    const float* G = p.gates + (size_t)gs * p.n_tok_pad * p.E;
+    // (16-byte units of 8 hidden values of one row, [r/32][kk/8][r%32]; rows
+    // are tokens, or assignments on the routed path)
+    uint16_t* H = reinterpret_cast<uint16_t*>(p.hbuf) +
+                  blockIdx.z * (ROUTED ? routed_hidden_elems(p) : (size_t)p.n_tok_pad * EH);
+    const float* G = ROUTED ? p.rt.agate + (size_t)gs * p.n_tok * p.top_k
+                            : p.gates + (size_t)gs * p.n_tok_pad * p.E;
+    const int row_end = ROUTED ? first + rows : p.n_tok_pad;
 #pragma unroll
     for (int bm = 0; bm < 4; ++bm) {
         const int hbase = hid0 + wm * 128 + bm * 32;
@@ -230,9 +299,9 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm1_256(Problem p, UnitTab ut
         const int e = hbase / p.hidden;   // hidden % 64 == 0: one expert per 32 rows
 #pragma unroll
         for (int bn = 0; bn < 4; ++bn) {
-            const int tc = tok0 + wn * 128 + bn * 32 + l32;
-            if (tc >= p.n_tok_pad) continue;
-            const float gate = tc < p.n_tok ? G[(size_t)tc * p.E + e] : 0.f;
+            const int tc = (ROUTED ? first : tok0) + wn * 128 + bn * 32 + l32;
+            if (tc >= row_end) continue;
+            const float gate = ROUTED ? G[tc] : tc < p.n_tok ? G[(size_t)tc * p.E + e] : 0.f;
             uint16_t* hrow = H + ((size_t)(tc >> 5) * (EH >> 3) + (hbase >> 3)) * 256 + (tc & 31) * 8 + 4 * g;
 #pragma unroll
             for (int ii = 0; ii < 4; ++ii) {
@@ -251,21 +320,36 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm1_256(Problem p, UnitTab ut
 
 // ---------------------------------------------------------------------------
 // gemm2.  grid: x = (output tiles) x (token tiles) in dispatch order, z = unit
+// in the launch.  ROUTED: the token tiles are the plan's tiles; A is W2_m
+// (K = hidden), the B rows are the tile's assignments (contiguous in the
+// hidden buffer), the bias is g * b2_m, and the result goes to the token's
+// target row (top_k = 1) or, in fp32, to the assignment's row of the
+// per-assignment buffer that the combine kernel sums (top_k > 1).
 // ---------------------------------------------------------------------------
+template <bool ROUTED>
 __global__ __launch_bounds__(256, 1) void k_bf16_gemm2_256(Problem p, UnitTab ut) {
     __shared__ u32x4 lds[2 * kStage];
     const uint32_t code = ut.code[blockIdx.z];
     const int j = unit_j(code), x = unit_x(code), gs = unit_gslot(code);
-    const int EH = p.E * p.hidden;
-    const int nA = (p.d_out + kTile - 1) / kTile, nB = (p.n_tok + kTile - 1) / kTile;
+    const int EH = ROUTED ? p.hidden : p.E * p.hidden;   // the K axis
+    const int nA = (p.d_out + kTile - 1) / kTile;
+    const int nB = ROUTED ? p.rt.max_tiles : (p.n_tok + kTile - 1) / kTile;
     int at, bt;
     tile_of(blockIdx.x, nA, nB, at, bt);
-    const int out0 = at * kTile, tok0 = bt * kTile;
+    int m = 0, first = 0, rows = 0;
+    if constexpr (ROUTED) {
+        if (bt >= p.rt.ntiles[gs]) return;
+        const int4 tl = p.rt.tiles[(size_t)gs * p.rt.max_tiles + bt];
+        m = tl.x; first = tl.y; rows = tl.z;
+    }
+    const int out0 = at * kTile, tok0 = ROUTED ? first : bt * kTile;
+    const int row_end = ROUTED ? first + rows : p.n_tok;
     const size_t unit = (size_t)j * p.streams + x;
-    const rsrc_t bufA = make_rsrc(reinterpret_cast<const char*>(p.w2) + unit * p.E * p.d_out * p.hidden * 2,
-                                  (size_t)p.E * p.d_out * p.hidden * 2);
-    const rsrc_t bufB = make_rsrc(reinterpret_cast<const char*>(p.hbuf) + (size_t)blockIdx.z * p.n_tok_pad * EH * 2,
-                                  (size_t)p.n_tok_pad * EH * 2);
+    const size_t wsel = ROUTED ? unit * p.E + m : unit;
+    const size_t hstride = ROUTED ? routed_hidden_elems(p) : (size_t)p.n_tok_pad * EH;
+    const rsrc_t bufA = make_rsrc(reinterpret_cast<const char*>(p.w2) + wsel * EH * p.d_out * 2,
+                                  (size_t)EH * p.d_out * 2);
+    const rsrc_t bufB = make_rsrc(reinterpret_cast<const char*>(p.hbuf) + blockIdx.z * hstride * 2, hstride * 2);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int L = lane >> 3, pc = lane & 7;
     const int c0 = pc ^ (L >> 1), c1 = pc ^ (4 + (L >> 1));
@@ -275,22 +359,18 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm2_256(Problem p, UnitTab ut
     for (int q = 0; q < 8; ++q) {
         const int J = wave * 8 + q;
         const int o = min(out0 + 8 * J + L, p.d_out - 1);
-        const int t = min(tok0 + 8 * J + L, p.n_tok - 1);
+        const int t = min(tok0 + 8 * J + L, row_end - 1);
         rowA[q] = (uint32_t)o * p.hidden * 2;
         rowB[q] = ((uint32_t)(t >> 5) * (EH >> 3) * 256 + (t & 31) * 8) * 2;
     }
     auto kofs = [&](int kt, int par, uint32_t& oa, uint32_t& ob) {
-        const int k0 = kt * kBK, m = k0 / p.hidden, c = par ? c1 : c0;
-        oa = ((uint32_t)m * p.d_out * p.hidden + (k0 - m * p.hidden) + 8 * c) * 2;
+        const int k0 = kt * kBK, e = k0 / p.hidden, c = par ? c1 : c0;
+        oa = ((uint32_t)e * p.d_out * p.hidden + (k0 - e * p.hidden) + 8 * c) * 2;
         ob = (uint32_t)((k0 >> 3) + c) * 512;
     };
 
-    // accumulators start at sum_m b2_m[o] g_m[t]: two 32x32x16 products with
-    // A[o][m] = b2_m[o] and B[t][m] = the gate's bf16 high part, then its
-    // bf16 residual (m < E <= 16; k = 8*g .. 8*g+7 in each lane)
-    const int wm = wave >> 1, wn = wave & 1, g = lane >> 5, l32 = lane & 31;
-    const uint16_t* b2 = p.b2 ? reinterpret_cast<const uint16_t*>(p.b2) + unit * p.E * p.d_out : nullptr;
-    const float* G = p.gates + (size_t)gs * p.n_tok_pad * p.E;
+    // accumulators start at sum_e g_e(t) b2_e[o] (routed: g(t) b2_m[o])
+    const int wave_m = wave >> 1, wn = wave & 1, g = lane >> 5, l32 = lane & 31;
     f32x16 acc[4][4];
 #pragma unroll
     for (int bm = 0; bm < 4; ++bm)
@@ -298,55 +378,47 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm2_256(Problem p, UnitTab ut
         for (int bn = 0; bn < 4; ++bn)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[bm][bn][e] = 0.f;
-    if (b2) {
-        u32x4 ghi[4], glo[4];
-#pragma unroll
-        for (int bn = 0; bn < 4; ++bn) {
-            const int t = tok0 + wn * 128 + bn * 32 + l32;
-            float gv[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int m = 8 * g + e;
-                gv[e] = (m < p.E && t < p.n_tok) ? G[(size_t)t * p.E + m] : 0.f;
-            }
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t h = pack_bf16x2(gv[2 * e], gv[2 * e + 1]);
-                ghi[bn][e] = h;
-                glo[bn][e] = pack_bf16x2(gv[2 * e] - bf16_lo(h), gv[2 * e + 1] - bf16_hi(h));
-            }
-        }
-#pragma unroll
-        for (int bm = 0; bm < 4; ++bm) {
-            const int o = min(out0 + wm * 128 + bm * 32 + l32, p.d_out - 1);
-            u32x4 bb;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int m = 8 * g + 2 * e;
-                const uint32_t lo = m < p.E ? b2[(size_t)m * p.d_out + o] : 0u;
-                const uint32_t hi = m + 1 < p.E ? b2[(size_t)(m + 1) * p.d_out + o] : 0u;
-                bb[e] = lo | (hi << 16);
-            }
-#pragma unroll
-            for (int bn = 0; bn < 4; ++bn) {
-                acc[bm][bn] = mfma_32x32x16(bb, ghi[bn], acc[bm][bn]);
-                acc[bm][bn] = mfma_32x32x16(bb, glo[bn], acc[bm][bn]);
-            }
+    if (p.b2) {
+        const uint16_t* b2 = reinterpret_cast<const uint16_t*>(p.b2) + wsel * (ROUTED ? 1 : p.E) * p.d_out;
+        if constexpr (ROUTED) {
+            const float* ag = p.rt.agate + (size_t)gs * p.n_tok * p.top_k;
+            seed_bias(
+                acc, 1, [&](int, int o) -> uint32_t { return b2[min(o, p.d_out - 1)]; },
+                [&](int, int a) -> float { return a < row_end ? ag[a] : 0.f; }, out0 + wave_m * 128,
+                tok0 + wn * 128);
+        } else {
+            const float* G = p.gates + (size_t)gs * p.n_tok_pad * p.E;
+            seed_bias(
+                acc, p.E, [&](int e, int o) -> uint32_t { return b2[(size_t)e * p.d_out + min(o, p.d_out - 1)]; },
+                [&](int e, int t) -> float { return t < p.n_tok ? G[(size_t)t * p.E + e] : 0.f; },
+                out0 + wave_m * 128, tok0 + wn * 128);
         }
     }
 
     k_loop(lds, bufA, bufB, rowA, rowB, EH / kBK, kofs, acc);
 
-    // epilogue: round to bf16, four consecutive outputs of one token per store
+    // epilogue: four consecutive outputs of one row per store
+    const int32_t* list = ROUTED ? p.rt.list + (size_t)gs * p.n_tok * p.top_k : nullptr;
+    float* part = ROUTED && p.top_k > 1 ? p.rt.part + blockIdx.z * (size_t)p.n_tok * p.top_k * p.d_out : nullptr;
     uint16_t* dst = reinterpret_cast<uint16_t*>(p.dst[x]) + (size_t)j * p.n_tok * p.d_out;
 #pragma unroll
     for (int bm = 0; bm < 4; ++bm) {
-        const int obase = out0 + wm * 128 + bm * 32;
+        const int obase = out0 + wave_m * 128 + bm * 32;
         if (obase >= p.d_out) continue;   // d_out % 32 == 0
 #pragma unroll
         for (int bn = 0; bn < 4; ++bn) {
-            const int t = tok0 + wn * 128 + bn * 32 + l32;
-            if (t >= p.n_tok) continue;
+            const int r = tok0 + wn * 128 + bn * 32 + l32;   // token, or assignment
+            if (r >= row_end) continue;
+            if (part) {
+#pragma unroll
+                for (int ii = 0; ii < 4; ++ii) {
+                    const f32x4 v = {acc[bm][bn][4 * ii], acc[bm][bn][4 * ii + 1], acc[bm][bn][4 * ii + 2],
+                                     acc[bm][bn][4 * ii + 3]};
+                    *reinterpret_cast<f32x4*>(part + (size_t)r * p.d_out + obase + 8 * ii + 4 * g) = v;
+                }
+                continue;
+            }
+            const int t = ROUTED ? list[r] : r;
             size_t row;
             int hs = 0;
             if (p.dst_layout == MOT_LAYOUT_BTHD) {
@@ -388,14 +460,40 @@ hipError_t launch_bf16_gemm1_256(const Problem& p, const UnitTab& ut, hipStream_
     if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
     const int EH = p.E * p.hidden;
     dim3 grid(((EH + kTile - 1) / kTile) * ((p.n_tok + kTile - 1) / kTile), 1, ut.n);
-    hipLaunchKernelGGL(k_bf16_gemm1_256, grid, dim3(256), 0, stream, p, ut);
+    hipLaunchKernelGGL(k_bf16_gemm1_256<false>, grid, dim3(256), 0, stream, p, ut);
     return hipGetLastError();
 }
 
 hipError_t launch_bf16_gemm2_256(const Problem& p, const UnitTab& ut, hipStream_t stream) {
     if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
     dim3 grid(((p.d_out + kTile - 1) / kTile) * ((p.n_tok + kTile - 1) / kTile), 1, ut.n);
-    hipLaunchKernelGGL(k_bf16_gemm2_256, grid, dim3(256), 0, stream, p, ut);
+    hipLaunchKernelGGL(k_bf16_gemm2_256<false>, grid, dim3(256), 0, stream, p, ut);
+    return hipGetLastError();
+}
+
+bool bf16_routed_gemm_fits(const Problem& p) {
+    const size_t lim = (size_t)1 << 31;
+    const size_t nk = (size_t)p.n_tok * p.top_k;
+    const size_t w1 = (size_t)p.hidden * p.d_in * 2, src = (size_t)p.n_tok * p.d_in * 2;
+    const size_t hb = (nk + 31) / 32 * 32 * p.hidden * 2, w2 = (size_t)p.hidden * p.d_out * 2;
+    return p.E <= 16 && w1 < lim && src < lim && hb < lim && w2 < lim;
+}
+
+size_t bf16_routed_hidden_bytes(const Problem& p) {
+    return ((size_t)p.n_tok * p.top_k + 31) / 32 * 32 * p.hidden * 2;
+}
+
+hipError_t launch_bf16_gemm1_routed(const Problem& p, const UnitTab& ut, hipStream_t stream) {
+    if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
+    dim3 grid(((p.hidden + kTile - 1) / kTile) * p.rt.max_tiles, 1, ut.n);
+    hipLaunchKernelGGL(k_bf16_gemm1_256<true>, grid, dim3(256), 0, stream, p, ut);
+    return hipGetLastError();
+}
+
+hipError_t launch_bf16_gemm2_routed(const Problem& p, const UnitTab& ut, hipStream_t stream) {
+    if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
+    dim3 grid(((p.d_out + kTile - 1) / kTile) * p.rt.max_tiles, 1, ut.n);
+    hipLaunchKernelGGL(k_bf16_gemm2_256<true>, grid, dim3(256), 0, stream, p, ut);
     return hipGetLastError();
 }
 

@@ -35,6 +35,7 @@ struct Plan {
     bool bf16 = false;
     bool fused = false;
     bool routed = false;       // Top-K sparse path (fused kernel over translator tiles)
+    bool routed2 = false;      // Top-K sparse path on the two-GEMM kernels (shapes the fused kernel lacks)
     int n_units = 0;
     int32_t n_tok = 0, n_tok_pad = 0;
     size_t fixed_bytes = 0;    // workspace for all units of the call
@@ -77,11 +78,18 @@ mot_status check_shapes(const mot_shapes* s) {
         s->algo != MOT_ALGO_ROUTED)
         return fail(MOT_ERR_BAD_SHAPE, "algo=%d is not a mot_algo value", s->algo);
     const int d_in = s->H_src * s->D_src, d_out = s->H_tgt * s->D_tgt;
-    if (s->algo == MOT_ALGO_FUSED || s->algo == MOT_ALGO_ROUTED) {
+    if (s->algo == MOT_ALGO_FUSED) {
         Problem p = base_problem(s);
         if (s->dtype != MOT_BF16 || !fused_supported(p))
             return fail(MOT_ERR_UNSUPPORTED,
                         "the fused kernel needs bf16, d_in and d_out in {128, 256, 512}, hidden %% 32 == 0");
+    }
+    if (s->algo == MOT_ALGO_ROUTED) {
+        Problem p = base_problem(s);
+        if (s->dtype != MOT_BF16 || (!fused_supported(p) && !bf16_routed_gemm_fits(p)))
+            return fail(MOT_ERR_UNSUPPORTED,
+                        "the routed path needs bf16 and either the fused kernel's shapes or operand regions "
+                        "under 2 GiB for the routed two-GEMM kernels");
     }
     if (s->dtype == MOT_BF16) {
         if (s->D_src % 8 || s->D_tgt % 8 || d_in % 64 || s->hidden % 64 || d_out % 32)
@@ -117,7 +125,9 @@ void make_plan(const mot_shapes* s, const int32_t* layer_map, Plan* pl) {
     Problem p = base_problem(s);
     pl->bf16 = s->dtype == MOT_BF16;
     pl->fused = pl->bf16 && s->algo != MOT_ALGO_UNFUSED && fused_supported(p);
-    pl->routed = pl->fused && (s->algo == MOT_ALGO_ROUTED || (s->algo == MOT_ALGO_AUTO && s->top_k < s->E));
+    const bool want_routed = s->algo == MOT_ALGO_ROUTED || (s->algo == MOT_ALGO_AUTO && s->top_k < s->E);
+    pl->routed = pl->fused && want_routed;
+    pl->routed2 = pl->bf16 && !pl->fused && want_routed && bf16_routed_gemm_fits(p);
     pl->n_tok = p.n_tok;
     pl->n_tok_pad = p.n_tok_pad;
     int n = 0;
@@ -133,14 +143,17 @@ void make_plan(const mot_shapes* s, const int32_t* layer_map, Plan* pl) {
     pl->fixed_bytes = 0;
     pl->unit_bytes = 0;
     pl->max_tiles = pl->tile_rows = 0;
-    if (pl->routed) {
+    if (pl->routed || pl->routed2) {
         const size_t nk = (size_t)p.n_tok * p.top_k;
-        pl->tile_rows = fused_tile_rows(p);
+        pl->tile_rows = pl->routed ? fused_tile_rows(p) : 256;
         pl->max_tiles = (int32_t)round_up((nk + pl->tile_rows - 1) / pl->tile_rows + p.E, 8);
         const size_t per = round_up(nk * 4, kAlign);   // one int32 / fp32 per assignment
         pl->fixed_bytes = (size_t)n * (5 * per + round_up((size_t)pl->max_tiles * 16, kAlign)) +
                           round_up((size_t)n * 4, kAlign);
-        if (p.top_k > 1) pl->unit_bytes = round_up(nk * p.d_out * sizeof(float), kAlign);
+        // per unit of a launch group: (two-GEMM) the hidden rows in assignment
+        // order, then (top_k > 1) the fp32 per-assignment output rows
+        if (pl->routed2) pl->unit_bytes = round_up(bf16_routed_hidden_bytes(p), kAlign);
+        if (p.top_k > 1) pl->unit_bytes += round_up(nk * p.d_out * sizeof(float), kAlign);
     } else if (!pl->fused) {
         pl->fixed_bytes = round_up((size_t)n * p.n_tok_pad * p.E * sizeof(float), kAlign);
         pl->unit_bytes = round_up((size_t)p.n_tok_pad * p.E * p.hidden * (pl->bf16 ? 2 : 4), kAlign);
@@ -332,6 +345,14 @@ mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* la
     p.wr = rw->w; p.br = rw->b;
     if (ws && pl.routed) {
         carve_routing(pl, p, ws, &p.rt);
+    } else if (ws && pl.routed2) {
+        carve_routing(pl, p, ws, &p.rt);
+        // after the routing buffers: the group's hidden buffers, then its fp32 rows
+        const size_t hid = round_up(bf16_routed_hidden_bytes(p), kAlign);
+        p.hbuf = reinterpret_cast<char*>(ws) + pl.fixed_bytes;
+        p.rt.part = p.top_k > 1 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + pl.fixed_bytes +
+                                                           (size_t)group * hid)
+                                : nullptr;
     } else if (ws) {
         p.gates = reinterpret_cast<float*>(ws);
         p.hbuf = reinterpret_cast<char*>(ws) + pl.fixed_bytes;
@@ -349,6 +370,19 @@ mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* la
             ut.n = n;
             memcpy(ut.code, pl.codes + u0, sizeof(uint32_t) * n);
             e = launch_bf16_fused_routed(p, ut, stream);
+            if (e == hipSuccess && p.top_k > 1) e = launch_routed_combine(p, ut, stream);
+        }
+    } else if (pl.routed2) {
+        ut.n = pl.n_units;
+        memcpy(ut.code, pl.codes, sizeof(uint32_t) * pl.n_units);
+        e = launch_router_lists(p, ut, stream);
+        if (e == hipSuccess) e = launch_route_plan(p, ut, stream);
+        for (int u0 = 0; e == hipSuccess && u0 < pl.n_units; u0 += group) {
+            const int n = pl.n_units - u0 < group ? pl.n_units - u0 : group;
+            ut.n = n;
+            memcpy(ut.code, pl.codes + u0, sizeof(uint32_t) * n);
+            e = launch_bf16_gemm1_routed(p, ut, stream);
+            if (e == hipSuccess) e = launch_bf16_gemm2_routed(p, ut, stream);
             if (e == hipSuccess && p.top_k > 1) e = launch_routed_combine(p, ut, stream);
         }
     } else if (pl.fused) {

@@ -166,6 +166,13 @@ hipError_t launch_bf16_gemm2(const Problem& p, const UnitTab& ut, hipStream_t st
 bool bf16_gemm256_fits(const Problem& p, int n_units);
 hipError_t launch_bf16_gemm1_256(const Problem& p, const UnitTab& ut, hipStream_t stream);
 hipError_t launch_bf16_gemm2_256(const Problem& p, const UnitTab& ut, hipStream_t stream);
+// Routed (Top-K sparse) two-GEMM path on the same tiles: each plan tile is up
+// to 256 assignments of one translator; the hidden buffer of a unit holds
+// bf16_routed_hidden_bytes(p) in assignment order.
+bool bf16_routed_gemm_fits(const Problem& p);
+size_t bf16_routed_hidden_bytes(const Problem& p);
+hipError_t launch_bf16_gemm1_routed(const Problem& p, const UnitTab& ut, hipStream_t stream);
+hipError_t launch_bf16_gemm2_routed(const Problem& p, const UnitTab& ut, hipStream_t stream);
 // Fused single-kernel path (router + both layers + mix + store); returns
 // hipErrorNotSupported when the sizes have no fused instantiation.
 bool fused_supported(const Problem& p);

@@ -135,3 +135,73 @@ def test_gemm256_matches_fused_kernel():
     f = run_gpu(w, inp, lm, algo=mb.ALGO_FUSED)
     u = run_gpu(w, inp, lm, algo=mb.ALGO_UNFUSED)
     assert max_unit_error(f[0], f[1], u[0], u[1], w, lm) <= 1e-2
+
+
+# ---------------------------------------------------------------------------
+# routed (Top-K sparse) two-GEMM path: each translator runs only on the
+# tokens that selected it, in plan tiles of up to 256 (token, translator)
+# assignments (paper Sec. 3, Definition "Mixture-of-Translators", K < E)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name,k", [("ragged", 1), ("ragged", 2), ("e16", 1), ("e16", 3), ("skip", 1)])
+def test_routed_two_gemm_parity(name, k, oracle_built):
+    """Routed two-GEMM rows against the oracle: the per-row bar everywhere,
+    near-tie rows matched to one of their admissible sets."""
+    w, lm = CASES[name]
+    w = w.with_(top_k=k)
+    print("case", name, "top_k", k, "routed two-GEMM", flush=True)
+    inp = generate(w)
+    gk, gv = run_gpu(w, inp, lm, algo=mb.ALGO_ROUTED)
+    rk, rv = _oracle(w, inp, lm)
+    worst, worst_row, n_tie, n_all = 0.0, 0.0, 0, 0
+    for j in range(w.L_tgt):
+        if lm[j] < 0:
+            from helpers import SENTINEL
+            assert (gk[j] == SENTINEL).all() and (gv[j] == SENTINEL).all()
+            continue
+        for x, (g, r) in enumerate(((gk, rk), (gv, rv))):
+            gr, rr = unit_rows(g, w, j), unit_rows(r, w, j)
+            assert np.isfinite(gr).all()
+            keep, wr_, nt = check_topk_rows(w, inp, lm, j, x, gr, rr)
+            n_tie += nt
+            n_all += keep.size
+            worst_row = max(worst_row, wr_)
+            worst = max(worst, rel_frob(gr[keep], rr[keep]))
+    print("  max unit rel-Frobenius error %.3e, max row error %.3e (%d near-tie rows of %d)"
+          % (worst, worst_row, n_tie, n_all), flush=True)
+    assert worst <= TOL["bf16"] and n_tie <= max(2, n_all // 100)
+
+
+def test_routed_two_gemm_auto_layouts_and_dense_agreement():
+    """AUTO takes the routed path for top_k < E on these shapes (same bits
+    as ALGO_ROUTED); BHTD caches give the BTHD rows permuted, bit for bit;
+    the dense-masked two-GEMM path agrees to bf16 rounding."""
+    w, lm = CASES["ragged"]
+    w = w.with_(top_k=2)
+    print("case ragged top_k 2: AUTO vs ROUTED vs dense-masked, BTHD vs BHTD", flush=True)
+    inp = generate(w)
+    r = run_gpu(w, inp, lm, algo=mb.ALGO_ROUTED)
+    a = run_gpu(w, inp, lm, algo=mb.ALGO_AUTO)
+    assert np.array_equal(r[0], a[0]) and np.array_equal(r[1], a[1])
+    d = run_gpu(w, inp, lm, algo=mb.ALGO_UNFUSED)
+    assert max_unit_error(r[0], r[1], d[0], d[1], w, lm) <= 1e-2
+    wh = w.with_(src_layout=1, dst_layout=1)
+    h = run_gpu(wh, generate(wh), lm, algo=mb.ALGO_ROUTED)
+    assert np.array_equal(h[0], r[0].transpose(0, 1, 3, 2, 4))
+    assert np.array_equal(h[1], r[1].transpose(0, 1, 3, 2, 4))
+
+
+def test_routed_two_gemm_skewed_and_deterministic(oracle_built):
+    """A router bias that sends every token to translator 1 (Top-1): the other
+    translators' assignment lists are empty and their tiles absent; the result
+    equals the oracle and is bit-identical on a second run."""
+    w, lm = CASES["ragged"]
+    w = w.with_(top_k=1)
+    print("case ragged top_k 1, all tokens to translator 1", flush=True)
+    inp = generate(w)
+    inp.br = np.zeros_like(inp.br)
+    inp.br[..., 1] = 50.0
+    a = run_gpu(w, inp, lm, algo=mb.ALGO_ROUTED)
+    b = run_gpu(w, inp, lm, algo=mb.ALGO_ROUTED)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    _check(w, lm, a, _oracle(w, inp, lm))

@@ -59,7 +59,7 @@ def _translate_act(w, inp, lm, algo, top_k=0):
 def _algos(w):
     if w.d_in in (128, 256, 512) and w.d_out in (128, 256, 512):
         return [mb.ALGO_FUSED, mb.ALGO_ROUTED, mb.ALGO_UNFUSED]
-    return [mb.ALGO_UNFUSED]
+    return [mb.ALGO_ROUTED, mb.ALGO_UNFUSED]
 
 
 @pytest.mark.parametrize("w", MOTH, ids=[w.name for w in MOTH])

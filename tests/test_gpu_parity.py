@@ -54,11 +54,13 @@ SMALL = [
 
 
 def _algos(w):
+    """Every kernel path a shape has: bf16 shapes run the routed path either
+    on the fused kernel's translator tiles or on the two-GEMM kernels'."""
     if w.dtype == "f32":
         return [mb.ALGO_AUTO]
     if w.d_in in (128, 256, 512) and w.d_out in (128, 256, 512):
         return [mb.ALGO_FUSED, mb.ALGO_ROUTED, mb.ALGO_UNFUSED]
-    return [mb.ALGO_UNFUSED]
+    return [mb.ALGO_ROUTED, mb.ALGO_UNFUSED]
 
 
 @pytest.mark.parametrize("w", SMALL, ids=[w.name for w in SMALL])
@@ -145,7 +147,8 @@ def test_full_size_sampled(w, oracle_built):
     assert np.isfinite(gk).all() and np.isfinite(gv).all()
 
 
-ROUTED_FULL = [(WORKLOADS[3], 1), (WORKLOADS[3], 2), (WORKLOADS[4], 2)]
+ROUTED_FULL = [(WORKLOADS[3], 1), (WORKLOADS[3], 2), (WORKLOADS[4], 2),
+               (WORKLOADS[2], 1), (WORKLOADS[2], 2)]   # the last two: routed two-GEMM kernels
 
 
 @pytest.mark.parametrize("w,k", ROUTED_FULL, ids=["%s-top%d" % (w.name, k) for w, k in ROUTED_FULL])

@@ -87,7 +87,7 @@ CASES = []
 for w in SMALL:
     paths = ([mb.ALGO_AUTO] if w.dtype == "f32" else
              [mb.ALGO_FUSED, mb.ALGO_ROUTED, mb.ALGO_UNFUSED] if w.d_in in (128, 256, 512) and w.d_out in (128, 256, 512)
-             else [mb.ALGO_UNFUSED])
+             else [mb.ALGO_ROUTED, mb.ALGO_UNFUSED])
     for k in sorted({1, 2, w.E}):
         for a in paths:
             if not (a == mb.ALGO_ROUTED and k == w.E):
