@@ -405,6 +405,25 @@ def cpu_baseline_moth(w, inp, lm, proj, rows):
             "seconds": round(dt, 2)}
 
 
+def pair_gathered_rows(idx, T: int) -> float:
+    """Key rows the two-position sparse kernel gathers per KV head for one
+    launch: for each pair (u, u+1) of every batch row, the size of the union
+    of their (ascending) sets when it is at most 192, else both sets."""
+    import torch
+    B, _, S = idx.shape
+    tp = T // 2 * 2
+    a = idx[:, 0:tp:2].long()
+    b = idx[:, 1:tp:2].long()
+    na = (a >= 0).sum(-1)
+    nb = (b >= 0).sum(-1)
+    common = ((a.unsqueeze(-1) == b.unsqueeze(-2)) & (a.unsqueeze(-1) >= 0)).sum((-1, -2))
+    union = na + nb - common
+    rows = torch.where(union <= 192, union, na + nb).sum().item()
+    if T % 2:
+        rows += (idx[:, T - 1] >= 0).sum().item()
+    return float(rows)
+
+
 def bench_replay(args):
     """Context replay (App. C.4): one step = for every target layer, either
     the full causal attention (bottom L_full layers) or mot_topS_select on
@@ -482,7 +501,17 @@ def bench_replay(args):
     sel_bytes = 4.0 * w.B * w.T * (w.T + 1) / 2 + 4.0 * n_tok * w.S        # causal half of A once, idx
     # sparse attention: q and o once, idx once, the layer's K and V once; the
     # selected K and V rows it gathers per (query, KV head) are reported beside
-    sp_gather = 2.0 * 2 * w.D * w.H_kv * w.B * sum(min(u + 1, w.S) for u in range(w.T))
+    sp_gather_sets = 2.0 * 2 * w.D * w.H_kv * w.B * sum(min(u + 1, w.S) for u in range(w.T))
+    sp_gather = sp_gather_sets
+    if w.D in (64, 128) and w.S <= 128 and 2 * (w.H_q // w.H_kv) <= 16:   # the library's rule for that kernel
+        # the two-position kernel gathers the union of a pair's sets once (or
+        # both sets when the union exceeds its 192-key limit): count the rows
+        # on this run's own sets, averaged over the sparse layers
+        rows_all = 0.0
+        for l in range(w.L_full, w.L_tgt):
+            mb.topS_select(maps[int(pi[l])], idx, w.B, w.T, w.S)
+            rows_all += pair_gathered_rows(idx, w.T)
+        sp_gather = 2.0 * 2 * w.D * w.H_kv * rows_all / (w.L_tgt - w.L_full)
     sp_bytes = 2.0 * 2 * n_tok * w.H_q * w.D + 4.0 * n_tok * w.S + 2.0 * 2 * n_tok * w.H_kv * w.D
     peak_bf16 = PEAK_TFLOPS["bf16"]
     rows = {
@@ -491,6 +520,7 @@ def bench_replay(args):
         "sparse": {"bound": "hbm", "achieved": sp_bytes / (avg["sparse"] / 1e3) / 1e9, "peak": PEAK_HBM_GBS,
                    "unit": "GB/s", "alg_bytes_per_launch": sp_bytes, "ms": avg["sparse"],
                    "gathered_bytes_per_launch": sp_gather,
+                   "gathered_bytes_per_launch_one_set_per_position": sp_gather_sets,
                    "gather_gbs": round(sp_gather / (avg["sparse"] / 1e3) / 1e9, 1),
                    "tflops": round(sp_flops / (avg["sparse"] / 1e3) / 1e12, 2)},
         "causal": {"bound": "mfma", "achieved": ca_flops / (avg["causal"] / 1e3) / 1e12, "peak": peak_bf16,

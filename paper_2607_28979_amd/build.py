@@ -21,7 +21,7 @@ LIB = os.path.join(CSRC, "libmot.so")
 # (source, object name, preprocessor definitions); the fused kernel's
 # instantiation file is compiled once per (d_in, d_out) so they build in parallel
 SOURCES = [(f, os.path.splitext(f)[0], {}) for f in
-           ("mot_api.hip", "k_router.hip", "k_routed.hip", "k_f32.hip", "k_bf16_unfused.hip", "k_bf16_gemm256.hip",
+           ("mot_api.hip", "k_router.hip", "k_routed.hip", "k_f32.hip", "k_f32_mfma.hip", "k_bf16_unfused.hip", "k_bf16_gemm256.hip",
             "k_bf16_fused.hip", "k_project.hip", "k_replay.hip", "k_backbone.hip")]
 SOURCES += [("k_bf16_fused_inst.hip", "k_bf16_fused_%d_%d" % (a, b),
              {"MOT_FUSED_D_IN": a, "MOT_FUSED_D_OUT": b})

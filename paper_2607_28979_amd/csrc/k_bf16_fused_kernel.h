@@ -48,7 +48,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 #endif
 // The same count for the 12-wave form (two layer-2 waves per SIMD)
 #ifndef MOT_FUSED_PHASE_A12
-#define MOT_FUSED_PHASE_A12 14
+#define MOT_FUSED_PHASE_A12 16
 #endif
 #ifndef MOT_FUSED_A_LAST
 #define MOT_FUSED_A_LAST 0

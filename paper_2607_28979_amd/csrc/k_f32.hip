@@ -1,7 +1,7 @@
-// fp32 translation path: two LDS-tiled GEMMs on the vector ALUs.  Built
-// without packed fp32 instructions, the vector ALUs peak at half of MI355X's
-// 157.3 TFLOP/s fp32 figure (one FMA per lane and cycle); the small fp32
-// workloads this path serves are bound by launch latency and weight reads.
+// fp32 translation path for shapes the matrix-core form (k_f32_mfma.hip)
+// does not take (hidden not a multiple of 64): two LDS-tiled GEMMs on the
+// vector ALUs.  Built without packed fp32 instructions, the vector ALUs peak
+// at half of MI355X's 157.3 TFLOP/s fp32 figure (one FMA per lane and cycle).
 //
 //   gemm1: Hs[u][t][m*hidden+k] = g[u][t][m] * GELU(W1_m z_t + b1_m)[k]
 //   gemm2: dst[j][t][o]         = sum_{m,k} Hs[u][t][m*hidden+k] W2_m[o][k]

@@ -369,6 +369,248 @@ __global__ __launch_bounds__(256) void k_sparse_attn(ReplayProblem p) {
     }
 }
 
+// Two neighbouring positions per workgroup (grouped-query heads G <= 8, sets
+// of up to 128 keys): u0 = 2 * item and u0 + 1 attend over the union of
+// their two sets, each key gathered once, with a per-position membership
+// mask.  The 2G query heads of the pair are the B columns of the score
+// product (16 columns), so the two positions share every gathered K and V row
+// and every MFMA.  Column c < 2G is position pp = c / G, head c % G.
+//
+// The union: when both sets are ascending with their -1 padding at the end
+// (what the Top-S selection writes), it is set 0 followed by the keys of set 1
+// that set 0 lacks (binary search), and a key of set 0 belongs to position 1
+// if set 1 holds it.  When the union exceeds kPairKeys keys, or a set is not
+// ascending (unordered, duplicates), the workgroup makes two passes instead,
+// one per position over that position's set as listed, and stores only that
+// position's columns.  A position attends to the entries of its bit that lie
+// in 0 .. u0 + pp.
+//
+// grid (xcd_grid(ceil(T / 2)), B), 256 threads
+constexpr int kPairKeys = 192;   // largest union one pass takes (register arrays and LDS are sized for it)
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void k_sparse_attn_pair(ReplayProblem p) {
+    constexpr int SMAX = 128, UMAX = kPairKeys, DC = D / 8;
+    __shared__ u32x4 s_lds[(D * UMAX + 16 * UMAX) / 8];
+    __shared__ float red[128];
+    __shared__ int s_set[2][SMAX];
+    __shared__ int s_keys[UMAX];
+    __shared__ int s_mask[UMAX];
+    __shared__ int s_cnt[2];
+    const int npair = (p.T + 1) / 2;
+    const int item = xcd_item(blockIdx.x, npair), b = blockIdx.y;
+    if (item >= npair) return;   // uniform over the workgroup
+    const int u0 = 2 * item;
+    const bool has1 = u0 + 1 < p.T;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, q4 = lane >> 4;
+    const int S = p.S, G = p.H_q / p.H_kv;
+    const uint16_t* Q = reinterpret_cast<const uint16_t*>(p.q);
+    const uint16_t* K = reinterpret_cast<const uint16_t*>(p.k);
+    const uint16_t* V = reinterpret_cast<const uint16_t*>(p.v);
+    uint16_t* O = reinterpret_cast<uint16_t*>(p.o);
+    const float sl2 = kLog2e / sqrtf((float)D);
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+
+    // ---- the two sets, then their union with membership bits
+    if (tid < 2 * S) {
+        const int pp = tid / S, e = tid % S;
+        s_set[pp][e] = pp == 0 || has1 ? p.idx[((size_t)b * p.T + u0 + pp) * S + e] : -1;
+    }
+    __syncthreads();
+    bool bad = false;
+    if (tid < 2 * S) {
+        const int pp = tid / S, e = tid % S, v = s_set[pp][e], nx = e + 1 < S ? s_set[pp][e + 1] : -1;
+        bad = (v < 0 && nx >= 0) || (v >= 0 && nx >= 0 && nx <= v) || v < -1;
+    }
+    const bool ordered = !__syncthreads_or(bad);
+    // nonnegative prefix lengths of the two sets
+    const int n0 = __syncthreads_count(tid < S && s_set[0][tid] >= 0);
+    const int n1 = __syncthreads_count(tid < S && s_set[1][tid] >= 0);
+    // union (one pass) when ordered and small enough; ext = set 1's extra keys
+    bool extra = false;
+    int v1 = -1;
+    if (ordered && tid < S) {
+        auto find = [&](const int* set, int n, int v) {
+            int lo = 0, hi = n;   // first index with set[i] >= v
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (set[mid] < v) lo = mid + 1;
+                else hi = mid;
+            }
+            return lo < n && set[lo] == v;
+        };
+        v1 = s_set[1][tid];
+        extra = tid < n1 && !find(s_set[0], n0, v1);
+        if (tid < n0) {
+            const int v0 = s_set[0][tid];
+            s_keys[tid] = v0;
+            s_mask[tid] = 1 | (find(s_set[1], n1, v0) ? 2 : 0);
+        }
+    }
+    const unsigned long long bal = __ballot(extra);
+    if (lane == 0 && w < 2) s_cnt[w] = __popcll(bal);
+    __syncthreads();
+    const int n_union = n0 + s_cnt[0] + s_cnt[1];
+    const bool one_pass = ordered && n_union <= UMAX;
+    if (one_pass && extra) {
+        const int pos = n0 + (w == 1 ? s_cnt[0] : 0) + __popcll(bal & ((1ull << lane) - 1ull));
+        s_keys[pos] = v1;
+        s_mask[pos] = 2;
+    }
+    // B column of this lane: position pp, head hh (kv head kvh*G + hh)
+    const int pp = l16 / G, hh = l16 - pp * G;
+    const bool col_ok = l16 < 2 * G && (pp == 0 || has1);
+    for (int pass = 0; pass < (one_pass ? 1 : (has1 ? 2 : 1)); ++pass) {
+    // keys of this pass: the union, or set `pass` as listed
+    int U;
+    if (one_pass) {
+        U = n_union;
+    } else {
+        __syncthreads();   // the previous pass has finished with s_keys
+        if (tid < S) {
+            s_keys[tid] = s_set[pass][tid];
+            s_mask[tid] = 1 << pass;
+        }
+        U = S;
+    }
+    // the positions whose columns this pass stores
+    const int store_mask = one_pass ? 3 : 1 << pass;
+    const int UP = U < 32 ? 32 : (U + 31) / 32 * 32;   // rounded up to whole 32-key steps
+    for (int e = U + tid; e < UP; e += 256) {
+        s_keys[e] = -1;
+        s_mask[e] = 0;
+    }
+    __syncthreads();
+
+    const int SC = UP / 8, KB = UP / 16;
+    const int swm = replay_swizzle_mask(SC);
+    u32x4* Vt = s_lds;                      // row d: SC chunks, chunk c at (c ^ (d & swm))
+    u32x4* Pl = s_lds + D * SC;             // row = B column
+    // a key is gathered when some position may attend it
+    auto gather_ok = [&](int kv) { return kv >= 0 && kv <= u0 + (has1 ? 1 : 0); };
+    constexpr int MAXR = replay_sparse_v_items(D, UMAX);
+    constexpr int MAXB = replay_sparse_key_blocks(UMAX);
+
+    for (int kvh = 0; kvh < p.H_kv; ++kvh) {
+        u32x4 va[MAXR], vc[MAXR];
+#pragma unroll
+        for (int r = 0; r < MAXR; ++r) {
+            const int it = tid + 256 * r;
+            va[r] = zero;
+            vc[r] = zero;
+            if (it < (UP / 2) * DC) {
+                const int pr = it % (UP / 2), dc = it / (UP / 2), k0 = 2 * pr;
+                const int v0 = s_keys[k0], v1 = s_keys[k0 + 1];
+                if (gather_ok(v0)) va[r] = *reinterpret_cast<const u32x4*>(V + kv_row(p, b, v0, kvh) + 8 * dc);
+                if (gather_ok(v1)) vc[r] = *reinterpret_cast<const u32x4*>(V + kv_row(p, b, v1, kvh) + 8 * dc);
+            }
+        }
+        u32x4 ka[MAXB][D / 32];
+#pragma unroll
+        for (int i = 0; i < MAXB; ++i) {
+            const int kb = w + 4 * i;
+            const int kr = kb < KB ? s_keys[kb * 16 + l16] : -1;
+            const uint16_t* krow = K + (gather_ok(kr) ? kv_row(p, b, kr, kvh) : 0);
+#pragma unroll
+            for (int ks = 0; ks < D / 32; ++ks)
+                ka[i][ks] = gather_ok(kr) ? *reinterpret_cast<const u32x4*>(krow + 32 * ks + 8 * q4) : zero;
+        }
+        const size_t qrow = (((size_t)b * p.T + u0 + pp) * p.H_q + kvh * G + hh) * D;
+        u32x4 qop[D / 32];
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks)
+            qop[ks] = col_ok ? *reinterpret_cast<const u32x4*>(Q + qrow + 32 * ks + 8 * q4) : zero;
+        // V^T of the union into LDS
+        uint32_t* Vw = reinterpret_cast<uint32_t*>(Vt);
+#pragma unroll
+        for (int r = 0; r < MAXR; ++r) {
+            const int it = tid + 256 * r;
+            if (it < (UP / 2) * DC) {
+                const int pr = it % (UP / 2), dc = it / (UP / 2), k0 = 2 * pr;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const int d = 8 * dc + i;
+                    Vw[(d * SC + ((k0 >> 3) ^ (d & swm))) * 4 + ((k0 & 7) >> 1)] = pair_word(va[r], vc[r], i);
+                }
+            }
+        }
+        // scores^T[key][column], masked per column to its position's entries
+        f32x4 sc[MAXB];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < MAXB; ++i) {
+            const int kb = w + 4 * i;
+            sc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (kb < KB) {
+#pragma unroll
+                for (int ks = 0; ks < D / 32; ++ks) sc[i] = mfma_16x16x32(ka[i][ks], qop[ks], sc[i]);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int e = kb * 16 + 4 * q4 + j, kv = s_keys[e];
+                    const bool ok = col_ok && kv >= 0 && kv <= u0 + pp && ((s_mask[e] >> pp) & 1);
+                    sc[i][j] = ok ? sc[i][j] : -INFINITY;
+                    mx = fmaxf(mx, sc[i][j]);
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) sc[i][j] = -INFINITY;
+            }
+        }
+        // softmax over the union, per column (lane column l16)
+        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        if (q4 == 0) red[w * 16 + l16] = mx;
+        __syncthreads();
+        mx = fmaxf(fmaxf(red[l16], red[16 + l16]), fmaxf(red[32 + l16], red[48 + l16]));
+        float sum = 0.f;
+#pragma unroll
+        for (int i = 0; i < MAXB; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float e = sc[i][j] == -INFINITY ? 0.f : exp2f((sc[i][j] - mx) * sl2);
+                sc[i][j] = e;
+                sum += e;
+            }
+        sum += __shfl_xor(sum, 16, 64);
+        sum += __shfl_xor(sum, 32, 64);
+        __syncthreads();   // every wave has read the maxima
+        if (q4 == 0) red[w * 16 + l16] = sum;
+        __syncthreads();
+        sum = red[l16] + red[16 + l16] + red[32 + l16] + red[48 + l16];
+        const float inv = sum > 0.f ? 1.0f / sum : 0.f;
+        uint32_t* Pw = reinterpret_cast<uint32_t*>(Pl);
+#pragma unroll
+        for (int i = 0; i < MAXB; ++i) {
+            const int kb = w + 4 * i;
+            if (kb < KB) {
+                const int ch = (2 * kb + (q4 >> 1)) ^ (l16 & swm);
+                const int base = (l16 * SC + ch) * 4 + 2 * (q4 & 1);
+                Pw[base] = pack_bf16x2(sc[i][0] * inv, sc[i][1] * inv);
+                Pw[base + 1] = pack_bf16x2(sc[i][2] * inv, sc[i][3] * inv);
+            }
+        }
+        __syncthreads();
+        // O^T[d][column] = V_union^T . P^T, d blocks db = w, w+4, ...
+#pragma unroll
+        for (int i = 0; i < D / 64; ++i) {
+            const int db = w + 4 * i;
+            const int dr = 16 * db + l16;
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            for (int ks = 0; ks < UP / 32; ++ks) {
+                const u32x4 a = Vt[dr * SC + ((4 * ks + q4) ^ (dr & swm))];
+                const u32x4 bb = Pl[l16 * SC + ((4 * ks + q4) ^ (l16 & swm))];
+                acc = mfma_16x16x32(a, bb, acc);
+            }
+            if (col_ok && ((store_mask >> pp) & 1)) {
+                const u32x2 o2 = {pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3])};
+                *reinterpret_cast<u32x2*>(O + qrow + 16 * db + 4 * q4) = o2;
+            }
+        }
+        __syncthreads();   // V^T and P are rewritten for the next KV head
+    }
+    }   // pass
+}
+
 // V transposed for the causal kernel: vt[b][kvh][d][t] (t < replay_tpad(T),
 // zero past T).  grid (replay_tpad(T) / 64, H_kv, B), 256 threads: one
 // 64-key chunk through LDS (rows padded by 8 elements against bank conflicts).
@@ -581,6 +823,12 @@ hipError_t launch_replay_attention(const ReplayProblem& p, hipStream_t stream) {
         // the caller's check admits only these sizes; the register arrays of
         // the instantiation below cover every admitted S
         if (!replay_sparse_supported(p.D, p.S)) return hipErrorInvalidValue;
+        if (replay_sparse_pair_supported(p.D, p.S, p.H_q / p.H_kv)) {
+            const dim3 pgrid(xcd_grid((p.T + 1) / 2), p.B);
+            if (p.D == 128) hipLaunchKernelGGL(k_sparse_attn_pair<128>, pgrid, dim3(256), 0, stream, p);
+            else hipLaunchKernelGGL(k_sparse_attn_pair<64>, pgrid, dim3(256), 0, stream, p);
+            return hipGetLastError();
+        }
         const dim3 grid(xcd_grid(p.T), p.B);
         const size_t lds = replay_sparse_lds_bytes(p.D, p.S);
         // register arrays sized for S <= 128, or for the largest S the LDS allows

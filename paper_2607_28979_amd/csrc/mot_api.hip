@@ -389,6 +389,14 @@ mot_status mot_translate(const void* src_k, const void* src_v, const int32_t* la
         ut.n = pl.n_units;
         memcpy(ut.code, pl.codes, sizeof(uint32_t) * pl.n_units);
         e = launch_bf16_fused(p, ut, stream);
+    } else if (!pl.bf16 && f32_mfma_fits(p)) {
+        for (int u0 = 0; e == hipSuccess && u0 < pl.n_units; u0 += group) {
+            const int n = pl.n_units - u0 < group ? pl.n_units - u0 : group;
+            ut.n = n;
+            memcpy(ut.code, pl.codes + u0, sizeof(uint32_t) * n);
+            e = launch_f32_mfma_gemm1(p, ut, stream);
+            if (e == hipSuccess) e = launch_f32_mfma_gemm2(p, ut, stream);
+        }
     } else {
         ut.n = pl.n_units;
         memcpy(ut.code, pl.codes, sizeof(uint32_t) * pl.n_units);

@@ -159,6 +159,11 @@ hipError_t launch_replay_attention(const ReplayProblem& p, hipStream_t stream);
 hipError_t launch_router(const Problem& p, const UnitTab& ut, bool bf16, hipStream_t stream);
 hipError_t launch_f32_gemm1(const Problem& p, const UnitTab& ut, hipStream_t stream);
 hipError_t launch_f32_gemm2(const Problem& p, const UnitTab& ut, hipStream_t stream);
+// fp32 on the matrix cores (k_f32_mfma.hip): the router runs inside layer 1,
+// which also writes p.gates; used when f32_mfma_fits
+bool f32_mfma_fits(const Problem& p);
+hipError_t launch_f32_mfma_gemm1(const Problem& p, const UnitTab& ut, hipStream_t stream);
+hipError_t launch_f32_mfma_gemm2(const Problem& p, const UnitTab& ut, hipStream_t stream);
 hipError_t launch_bf16_gemm1(const Problem& p, const UnitTab& ut, hipStream_t stream);
 hipError_t launch_bf16_gemm2(const Problem& p, const UnitTab& ut, hipStream_t stream);
 // 256 x 256-tile forms of the same two products (k_bf16_gemm256.hip), used

@@ -44,4 +44,11 @@ constexpr int replay_sparse_instance(int D, int S) { return S <= 128 ? 128 : rep
 constexpr int replay_sparse_v_items(int D, int smax) { return ((smax / 2) * (D / 8) + 255) / 256; }
 constexpr int replay_sparse_key_blocks(int smax) { return (smax / 16 + 3) / 4; }
 
+// The two-position form of the sparse kernel: the union of two sets of up to
+// 128 keys, with the 2G query heads of the pair as the 16 columns of the
+// score product.
+constexpr bool replay_sparse_pair_supported(int D, int S, int G) {
+    return replay_sparse_supported(D, S) && S <= 128 && G >= 1 && 2 * G <= 16;
+}
+
 }  // namespace mot

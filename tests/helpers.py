@@ -142,18 +142,20 @@ def admissible_sets(logit_row: np.ndarray, K: int, rel: float = 1e-3):
 def forced_set_router_bias(inp: Inputs, logit_row: np.ndarray, j: int, x: int, chosen, K: int,
                            rel: float = 1e-3, delta: float = 1e-4) -> np.ndarray:
     """A copy of the router bias that makes one row select `chosen` without
-    ambiguity: within the boundary group, chosen translators get the group's
-    largest logit + delta, the others its smallest - delta (the row's gates
-    move by well under 1 %, far inside the bf16 bar)."""
+    ambiguity: the chosen translators keep their logits, and the others of
+    the boundary group are moved to delta below the lowest chosen one.  The
+    renormalised gates of the chosen set depend only on the chosen logits, so
+    the forced row is the mixture over `chosen` with the row's own gates."""
     g = np.exp(logit_row - logit_row.max())
     g /= g.sum()
     gk = -np.sort(-g)[K - 1]
     group = [m for m in range(g.size) if abs(g[m] - gk) <= rel * gk]
-    top, bot = max(logit_row[group]), min(logit_row[group])
+    inside = [m for m in group if m in chosen]
+    floor = min(logit_row[inside]) if inside else max(logit_row[group])
     br = inp.br.copy()
     for m in group:
-        target = top + delta if m in chosen else bot - delta
-        br[j, x, m] = np.float32(float(br[j, x, m]) + (target - logit_row[m]))
+        if m not in chosen:
+            br[j, x, m] = np.float32(float(br[j, x, m]) + (floor - delta - logit_row[m]))
     return br
 
 

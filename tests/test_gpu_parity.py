@@ -217,6 +217,29 @@ def test_identity_translator_bit_exact(dtype, algo):
             assert np.array_equal(unit_rows(g, w, j), src[lm[j]].reshape(w.n_tok, w.d_in))
 
 
+@pytest.mark.parametrize("hidden,top_k", [(96, 0), (96, 2), (128, 2)])
+def test_f32_both_kernel_forms(hidden, top_k, oracle_built):
+    """fp32 with hidden = 96 runs the vector-ALU kernels (hidden not a
+    multiple of 64), hidden = 128 the matrix-core kernels with the router
+    inside layer 1; both against the oracle at the fp32 bar, with a ragged
+    token count (130 = 2 x 64 + 2), Top-K and an unmapped layer."""
+    w = _tiny("f32", B=2, T=65, H_src=4, D_src=48, H_tgt=3, D_tgt=64, E=3, hidden=hidden, top_k=top_k)
+    inp = generate(w)
+    lm = np.array([2, -1, 0, 1], np.int32)
+    print("case fp32 hidden", hidden, "top_k", top_k, flush=True)
+    gk, gv = run_gpu(w, inp, lm, algo=mb.ALGO_AUTO)
+    rk, rv = _oracle_full(w, inp, lm)
+    assert (gk[1] == SENTINEL).all() and (gv[1] == SENTINEL).all()
+    worst = 0.0
+    for j in (0, 2, 3):
+        for x, (g, r) in enumerate(((gk, rk), (gv, rv))):
+            gr, rr = unit_rows(g, w, j), unit_rows(r, w, j)
+            keep, wr_, _ = check_topk_rows(w, inp, lm, j, x, gr, rr) if top_k else (np.arange(w.n_tok), 0.0, 0)
+            worst = max(worst, rel_frob(gr[keep], rr[keep]), float(row_errors(gr[keep], rr[keep]).max()))
+    print("  max unit / row error %.3e" % worst, flush=True)
+    assert worst <= TOL["f32"]
+
+
 @pytest.mark.parametrize("algo", [mb.ALGO_FUSED, mb.ALGO_UNFUSED])
 def test_one_hot_and_uniform_gates(algo, oracle_built):
     w = _tiny(L_src=1, L_tgt=1)

@@ -98,6 +98,9 @@ ATTN = [  # B, T, H_q, H_kv, D, S, kv_layout
     # LDS swizzle is needed): 12 and 28 chunks
     (1, 240, 6, 2, 64, 96, 0),
     (1, 300, 4, 1, 64, 224, 1),
+    # an odd context: the last position of the two-position kernel is alone
+    (1, 201, 8, 2, 128, 64, 0),
+    (2, 99, 16, 2, 64, 128, 1),       # 8 query heads per KV head: the pair fills all 16 columns
 ]
 
 
@@ -117,6 +120,34 @@ def test_sparse_attention_parity(case, oracle_built):
     # per position too: no row may be off even when the total is fine
     worst = max(rel_frob(got[b, u], want[b, u]) for b in range(B) for u in range(T))
     assert worst <= 2 * TOL["bf16"], worst
+
+
+@pytest.mark.parametrize("order", ["ascending", "shuffled", "duplicates"])
+def test_sparse_pair_union_and_two_pass(order, oracle_built):
+    """The two-position kernel on random sets (neighbouring positions share
+    few keys, so most pairs' unions exceed its 192-key limit and it runs one
+    pass per position), on shuffled sets and on sets with a repeated entry
+    (both taken as listed, one pass per position), for an odd context:
+    every position against the oracle, which attends each listed entry."""
+    from oracle import oracle_replay_attention
+    B, T, Hq, Hkv, D, S = 1, 401, 14, 2, 128, 128
+    print("case pair kernel", order, flush=True)
+    q, k, v = replay_inputs(B, T, Hq, Hkv, D, seed=17)
+    rng = np.random.default_rng(17)
+    idx = np.full((B, T, S), -1, np.int32)
+    for u in range(T):
+        n = min(u + 1, S)
+        sel = rng.choice(u + 1, size=n, replace=False)
+        if order == "ascending":
+            sel = np.sort(sel)
+        if order == "duplicates" and n >= 2:
+            sel[-1] = sel[0]
+        idx[0, u, :n] = sel
+    got = _gpu_attention(q, k, v, idx)
+    want = oracle_replay_attention(q, k, v, idx)
+    worst = max(rel_frob(got[0, u], want[0, u]) for u in range(T))
+    print("  worst position rel-Frobenius %.3e" % worst, flush=True)
+    assert rel_frob(got, want) <= TOL["bf16"] and worst <= 2 * TOL["bf16"], worst
 
 
 def test_sparse_attention_padding_and_invalid_entries(oracle_built):
