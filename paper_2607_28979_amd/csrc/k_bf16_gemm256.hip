@@ -39,9 +39,25 @@ namespace mot {
 
 namespace {
 
-constexpr int kTile = 256, kBK = 64;
-constexpr int kStage = 2 * kTile * 8;   // 16-byte slots per stage (A then B)
+#ifndef MOT_G256_BK
+#define MOT_G256_BK 64   // K slice per LDS stage: 64 (two stages) or 32 (four stages)
+#endif
+
+constexpr int kTile = 256;
 constexpr int kGroup = 32;              // B tiles per dispatch group
+
+// LDS geometry of a K slice of BK columns: rows of CPR 16-byte chunks, a
+// wave's 1 KB load fills RPI rows, NI loads per operand and wave, NST stages
+// of STAGE slots (A rows then B rows) in 128 KB, NSUB k-steps of 16.
+// Logical chunk c of row r sits at c ^ swz(r): 16 consecutive rows of one
+// logical chunk fill 16 distinct 16-byte bank groups.
+template <int BK>
+struct Geo {
+    static constexpr int CPR = BK / 8, RPI = 64 / CPR, NI = kTile / RPI / 4;
+    static constexpr int NST = BK == 64 ? 2 : 4, STAGE = 2 * kTile * CPR, NSUB = BK / 16;
+    __device__ static int swz(int r) { return CPR == 8 ? (r >> 1) & 7 : (r >> 2) & 3; }
+};
+static_assert(Geo<64>::NST * Geo<64>::STAGE == 8192 && Geo<32>::NST * Geo<32>::STAGE == 8192, "128 KB of LDS");
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -79,44 +95,51 @@ __device__ __forceinline__ uint32_t src_k_bytes(const Problem& p, int k) {
     return ((uint32_t)(k / p.D_src) * p.T * p.D_src + k % p.D_src) * 2;
 }
 
-// The K loop shared by both products.  rowA/rowB: this lane's 8 + 8 row byte
-// offsets into the operands' buffers (rows 8J + lane/8 of the tile,
-// J = wave*8 + q); kofs(kt, par, &a, &b)
-// gives the byte offsets of logical chunk c of slice kt for the two chunk
-// parities (par = q & 1).  acc holds the initial values on entry.
+// s_waitcnt immediate (gfx9 encoding): vector-memory count n, LDS/scalar
+// count 0, export count left at its maximum
+constexpr int waitcnt_vm_lgkm0(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
+
+// The K loop shared by both products.  rowA/rowB: this lane's NI + NI row
+// byte offsets into the operands' buffers (rows RPI*J + lane/CPR of the
+// tile, J = wave*NI + q); kofs(kt, c, &a, &b) gives the byte offsets of
+// logical chunk c of slice kt.  acc holds the initial values on entry.
 //
 // Register double buffering: the fragments of k-step s+1 are read while the
 // 16 MFMAs of step s run.  The slice's barrier sits before the MFMAs of its
 // last k-step (whose fragments are already in registers), and the first
 // fragments of the next slice are read right after it, so the matrix core
-// has queued work across the barrier.
-template <class KOfs>
-__device__ __forceinline__ void k_loop(u32x4* lds, rsrc_t bufA, rsrc_t bufB, const uint32_t (&rowA)[8],
-                                       const uint32_t (&rowB)[8], int nk, KOfs kofs, f32x16 (&acc)[4][4]) {
+// has queued work across the barrier.  Slice kt+NST-1 is loaded while slice
+// kt is computed.
+template <int BK, class KOfs>
+__device__ __forceinline__ void k_loop(u32x4* lds, rsrc_t bufA, rsrc_t bufB, const uint32_t (&rowA)[Geo<BK>::NI],
+                                       const uint32_t (&rowB)[Geo<BK>::NI], int nk, KOfs kofs, f32x16 (&acc)[4][4]) {
+    using Gm = Geo<BK>;
+    constexpr int CPR = Gm::CPR, NI = Gm::NI, NST = Gm::NST, NSUB = Gm::NSUB;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1, g = lane >> 5, l32 = lane & 31;
-    const int sw = (l32 >> 1) & 7;
+    const int sw = Gm::swz(l32);
+    const int L = lane / CPR, pc = lane % CPR;
 
     auto issue = [&](int kt, int st) {
-        uint32_t oa[2], ob[2];
-        kofs(kt, 0, oa[0], ob[0]);
-        kofs(kt, 1, oa[1], ob[1]);
-        u32x4* base = lds + st * kStage + wave * 8 * 64;
+        u32x4* base = lds + st * Gm::STAGE + wave * NI * 64;
 #pragma unroll
-        for (int q = 0; q < 8; ++q) load_lds16(bufA, rowA[q] + oa[q & 1], base + q * 64);
-#pragma unroll
-        for (int q = 0; q < 8; ++q) load_lds16(bufB, rowB[q] + ob[q & 1], base + kTile * 8 + q * 64);
+        for (int q = 0; q < NI; ++q) {
+            uint32_t oa, ob;
+            kofs(kt, pc ^ Gm::swz(Gm::RPI * q + L), oa, ob);   // the wave's row offset keeps swz
+            load_lds16(bufA, rowA[q] + oa, base + q * 64);
+            load_lds16(bufB, rowB[q] + ob, base + kTile * CPR + q * 64);
+        }
     };
     // fragments of k-step s of stage st: rows wm*128 + i*32 + l32 (A) and
     // wn*128 + i*32 + l32 (B), logical chunk 2s + g
     auto read = [&](int st, int s, u32x4 (&a)[4], u32x4 (&b)[4]) {
-        const u32x4* la = lds + st * kStage + (wm * 128 + l32) * 8;
-        const u32x4* lb = lds + st * kStage + kTile * 8 + (wn * 128 + l32) * 8;
+        const u32x4* la = lds + st * Gm::STAGE + (wm * 128 + l32) * CPR;
+        const u32x4* lb = lds + st * Gm::STAGE + kTile * CPR + (wn * 128 + l32) * CPR;
         const int c = (2 * s + g) ^ sw;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            a[i] = la[i * 32 * 8 + c];
-            b[i] = lb[i * 32 * 8 + c];
+            a[i] = la[i * 32 * CPR + c];
+            b[i] = lb[i * 32 * CPR + c];
         }
     };
     auto mma = [&](const u32x4 (&a)[4], const u32x4 (&b)[4]) {
@@ -126,35 +149,66 @@ __device__ __forceinline__ void k_loop(u32x4* lds, rsrc_t bufA, rsrc_t bufB, con
             for (int bn = 0; bn < 4; ++bn) acc[bm][bn] = mfma_32x32x16(a[bm], b[bn], acc[bm][bn]);
     };
 
+    // workgroup barrier after an explicit wait: __syncthreads() would add its
+    // own fence, which waits for every load in flight (vmcnt(0)) and so for
+    // the later slices' loads too.  The waits are s_waitcnt instructions the
+    // compiler sees (it then adds no LDS waits of its own after the barrier).
+    auto barrier = [&]() {
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
     u32x4 a0[4], b0[4], a1[4], b1[4];
-    issue(0, 0);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
+    if constexpr (NST == 2) {
+        issue(0, 0);
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+    } else {
+        // slices 0..2 in flight, wait for slice 0 (2 * NI loads per slice)
+        issue(0, 0);
+        if (nk > 1) issue(1, 1);
+        if (nk > 2) issue(2, 2);
+        if (nk > 2) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(4 * NI));
+        else if (nk > 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(2 * NI));
+        else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+    }
+    barrier();
     read(0, 0, a0, b0);
     for (int kt = 0; kt < nk; ++kt) {
-        const int st = kt & 1;
+        const int st = kt % NST;
         const bool more = kt + 1 < nk;
         // sched_barrier fences keep each read group ahead of the MFMAs that
         // precede its use (the scheduler would otherwise sink the reads next
         // to their first use and expose the LDS latency)
-        if (more) issue(kt + 1, st ^ 1);
-        read(st, 1, a1, b1);
-        __builtin_amdgcn_sched_barrier(0);
-        mma(a0, b0);
-        __builtin_amdgcn_sched_barrier(0);
-        read(st, 2, a0, b0);
-        __builtin_amdgcn_sched_barrier(0);
-        mma(a1, b1);
-        __builtin_amdgcn_sched_barrier(0);
-        read(st, 3, a1, b1);
-        __builtin_amdgcn_sched_barrier(0);
-        mma(a0, b0);
+        if (kt + NST - 1 < nk) issue(kt + NST - 1, (kt + NST - 1) % NST);
+        if constexpr (NSUB == 4) {
+            read(st, 1, a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(a0, b0);
+            __builtin_amdgcn_sched_barrier(0);
+            read(st, 2, a0, b0);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
+            read(st, 3, a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(a0, b0);
+        } else {
+            read(st, 1, a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(a0, b0);
+        }
         __builtin_amdgcn_sched_barrier(0);
         // every wave's reads of stage st are in registers and its loads of
-        // slice kt+1 have landed: stage st^1 is complete, stage st is free
-        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
-        __syncthreads();
-        if (more) read(st ^ 1, 0, a0, b0);
+        // slice kt+1 have landed (slices up to kt+NST-1 may stay in flight):
+        // stage (kt+1) % NST is complete, stage st is free
+        if constexpr (NST == 2) {
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+        } else {
+            if (kt + 3 < nk) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(4 * NI));
+            else if (kt + 2 < nk) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(2 * NI));
+            else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+        }
+        barrier();
+        if (more) read((kt + 1) % NST, 0, a0, b0);
         __builtin_amdgcn_sched_barrier(0);
         mma(a1, b1);
         __builtin_amdgcn_sched_barrier(0);
@@ -216,9 +270,10 @@ __device__ __forceinline__ size_t routed_hidden_elems(const Problem& p) {
 // index, A is W1_m, and the hidden rows are stored in assignment order with
 // the assignment's gate.
 // ---------------------------------------------------------------------------
-template <bool ROUTED>
+template <bool ROUTED, int BK>
 __global__ __launch_bounds__(256, 1) void k_bf16_gemm1_256(Problem p, UnitTab ut) {
-    __shared__ u32x4 lds[2 * kStage];
+    using Gm = Geo<BK>;
+    __shared__ u32x4 lds[Gm::NST * Gm::STAGE];
     const uint32_t code = ut.code[blockIdx.z];
     const int j = unit_j(code), x = unit_x(code), i = unit_i(code), gs = unit_gslot(code);
     // A rows: E*hidden (dense) or the hidden units of one translator (routed)
@@ -243,19 +298,18 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm1_256(Problem p, UnitTab ut
     const rsrc_t bufB = make_rsrc(reinterpret_cast<const char*>(p.src[x]) + (size_t)i * p.n_tok * p.d_in * 2,
                                   (size_t)p.n_tok * p.d_in * 2);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int L = lane >> 3, pc = lane & 7;
-    const int c0 = pc ^ (L >> 1), c1 = pc ^ (4 + (L >> 1));
+    const int L = lane / Gm::CPR;
 
-    uint32_t rowA[8], rowB[8];
+    uint32_t rowA[Gm::NI], rowB[Gm::NI];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        const int J = wave * 8 + q;
-        rowA[q] = (uint32_t)min(hid0 + 8 * J + L, EH - 1) * p.d_in * 2;
-        const int tok = ROUTED ? list[first + min(8 * J + L, rows - 1)] : min(tok0 + 8 * J + L, p.n_tok - 1);
+    for (int q = 0; q < Gm::NI; ++q) {
+        const int r = Gm::RPI * (wave * Gm::NI + q) + L;
+        rowA[q] = (uint32_t)min(hid0 + r, EH - 1) * p.d_in * 2;
+        const int tok = ROUTED ? list[first + min(r, rows - 1)] : min(tok0 + r, p.n_tok - 1);
         rowB[q] = src_row_bytes(p, tok);
     }
-    auto kofs = [&](int kt, int par, uint32_t& oa, uint32_t& ob) {
-        const int k = kt * kBK + 8 * (par ? c1 : c0);
+    auto kofs = [&](int kt, int c, uint32_t& oa, uint32_t& ob) {
+        const int k = kt * BK + 8 * c;
         oa = (uint32_t)k * 2;
         ob = (uint32_t)src_k_bytes(p, k);
     };
@@ -282,7 +336,7 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm1_256(Problem p, UnitTab ut
         for (int bn = 0; bn < 4; ++bn) acc[bm][bn] = init;
     }
 
-    k_loop(lds, bufA, bufB, rowA, rowB, p.d_in / kBK, kofs, acc);
+    k_loop<BK>(lds, bufA, bufB, rowA, rowB, p.d_in / BK, kofs, acc);
 
     // epilogue: GELU, * gate, round to bf16, fragment-native hidden store
     // (16-byte units of 8 hidden values of one row, [r/32][kk/8][r%32]; rows
@@ -326,9 +380,10 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm1_256(Problem p, UnitTab ut
 // target row (top_k = 1) or, in fp32, to the assignment's row of the
 // per-assignment buffer that the combine kernel sums (top_k > 1).
 // ---------------------------------------------------------------------------
-template <bool ROUTED>
+template <bool ROUTED, int BK>
 __global__ __launch_bounds__(256, 1) void k_bf16_gemm2_256(Problem p, UnitTab ut) {
-    __shared__ u32x4 lds[2 * kStage];
+    using Gm = Geo<BK>;
+    __shared__ u32x4 lds[Gm::NST * Gm::STAGE];
     const uint32_t code = ut.code[blockIdx.z];
     const int j = unit_j(code), x = unit_x(code), gs = unit_gslot(code);
     const int EH = ROUTED ? p.hidden : p.E * p.hidden;   // the K axis
@@ -351,20 +406,19 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm2_256(Problem p, UnitTab ut
                                   (size_t)EH * p.d_out * 2);
     const rsrc_t bufB = make_rsrc(reinterpret_cast<const char*>(p.hbuf) + blockIdx.z * hstride * 2, hstride * 2);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int L = lane >> 3, pc = lane & 7;
-    const int c0 = pc ^ (L >> 1), c1 = pc ^ (4 + (L >> 1));
+    const int L = lane / Gm::CPR;
 
-    uint32_t rowA[8], rowB[8];
+    uint32_t rowA[Gm::NI], rowB[Gm::NI];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        const int J = wave * 8 + q;
-        const int o = min(out0 + 8 * J + L, p.d_out - 1);
-        const int t = min(tok0 + 8 * J + L, row_end - 1);
+    for (int q = 0; q < Gm::NI; ++q) {
+        const int r = Gm::RPI * (wave * Gm::NI + q) + L;
+        const int o = min(out0 + r, p.d_out - 1);
+        const int t = min(tok0 + r, row_end - 1);
         rowA[q] = (uint32_t)o * p.hidden * 2;
         rowB[q] = ((uint32_t)(t >> 5) * (EH >> 3) * 256 + (t & 31) * 8) * 2;
     }
-    auto kofs = [&](int kt, int par, uint32_t& oa, uint32_t& ob) {
-        const int k0 = kt * kBK, e = k0 / p.hidden, c = par ? c1 : c0;
+    auto kofs = [&](int kt, int c, uint32_t& oa, uint32_t& ob) {
+        const int k0 = kt * BK, e = k0 / p.hidden;
         oa = ((uint32_t)e * p.d_out * p.hidden + (k0 - e * p.hidden) + 8 * c) * 2;
         ob = (uint32_t)((k0 >> 3) + c) * 512;
     };
@@ -395,7 +449,7 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm2_256(Problem p, UnitTab ut
         }
     }
 
-    k_loop(lds, bufA, bufB, rowA, rowB, EH / kBK, kofs, acc);
+    k_loop<BK>(lds, bufA, bufB, rowA, rowB, EH / BK, kofs, acc);
 
     // epilogue: four consecutive outputs of one row per store
     const int32_t* list = ROUTED ? p.rt.list + (size_t)gs * p.n_tok * p.top_k : nullptr;
@@ -460,14 +514,14 @@ hipError_t launch_bf16_gemm1_256(const Problem& p, const UnitTab& ut, hipStream_
     if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
     const int EH = p.E * p.hidden;
     dim3 grid(((EH + kTile - 1) / kTile) * ((p.n_tok + kTile - 1) / kTile), 1, ut.n);
-    hipLaunchKernelGGL(k_bf16_gemm1_256<false>, grid, dim3(256), 0, stream, p, ut);
+    hipLaunchKernelGGL((k_bf16_gemm1_256<false, MOT_G256_BK>), grid, dim3(256), 0, stream, p, ut);
     return hipGetLastError();
 }
 
 hipError_t launch_bf16_gemm2_256(const Problem& p, const UnitTab& ut, hipStream_t stream) {
     if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
     dim3 grid(((p.d_out + kTile - 1) / kTile) * ((p.n_tok + kTile - 1) / kTile), 1, ut.n);
-    hipLaunchKernelGGL(k_bf16_gemm2_256<false>, grid, dim3(256), 0, stream, p, ut);
+    hipLaunchKernelGGL((k_bf16_gemm2_256<false, MOT_G256_BK>), grid, dim3(256), 0, stream, p, ut);
     return hipGetLastError();
 }
 
@@ -486,14 +540,14 @@ size_t bf16_routed_hidden_bytes(const Problem& p) {
 hipError_t launch_bf16_gemm1_routed(const Problem& p, const UnitTab& ut, hipStream_t stream) {
     if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
     dim3 grid(((p.hidden + kTile - 1) / kTile) * p.rt.max_tiles, 1, ut.n);
-    hipLaunchKernelGGL(k_bf16_gemm1_256<true>, grid, dim3(256), 0, stream, p, ut);
+    hipLaunchKernelGGL((k_bf16_gemm1_256<true, MOT_G256_BK>), grid, dim3(256), 0, stream, p, ut);
     return hipGetLastError();
 }
 
 hipError_t launch_bf16_gemm2_routed(const Problem& p, const UnitTab& ut, hipStream_t stream) {
     if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
     dim3 grid(((p.d_out + kTile - 1) / kTile) * p.rt.max_tiles, 1, ut.n);
-    hipLaunchKernelGGL(k_bf16_gemm2_256<true>, grid, dim3(256), 0, stream, p, ut);
+    hipLaunchKernelGGL((k_bf16_gemm2_256<true, MOT_G256_BK>), grid, dim3(256), 0, stream, p, ut);
     return hipGetLastError();
 }
 
