@@ -327,7 +327,9 @@ mot_status mot_topS_select(const float* A, int32_t* idx, const mot_replay_shapes
  * such calls and those of mot_translate or mot_backbone_translate without
  * workspaces that overlap in time on one device race; calls with their own
  * workspaces do not).  A workspace below the need returns
- * MOT_ERR_WORKSPACE_TOO_SMALL; it must not overlap q, k, v or o.
+ * MOT_ERR_WORKSPACE_TOO_SMALL; it must not overlap q, k, v or o.  With idx
+ * NULL, (T + 64) * row stride * 2 bytes must stay under 2^31 (row stride:
+ * H_kv * D in BTHD, D in BHTD), else MOT_ERR_UNSUPPORTED.
  */
 mot_status mot_replay_attention(const void* q, const void* k, const void* v, const int32_t* idx, void* o,
                                 const mot_replay_shapes* shapes, hipStream_t stream);
@@ -375,9 +377,9 @@ mot_status mot_replay_attention(const void* q, const void* k, const void* v, con
  *            overlap in time on one device then race)
  * Requires d_in and d_h multiples of 64 up to 4096, N d_h up to 4096, d_ff a
  * multiple of 64, D_tgt a multiple of 8, head width d_h / n_heads of 64 or
- * 128, N <= 8 (MOT_ERR_UNSUPPORTED / MOT_ERR_BAD_SHAPE otherwise; a window
- * mixing mapped and unmapped slots is MOT_ERR_BAD_LAYER_MAP).  Every check
- * runs before any enqueue.
+ * 128, N <= 8, (T + 64) d_h 2 < 2^31 (MOT_ERR_UNSUPPORTED / MOT_ERR_BAD_SHAPE
+ * otherwise; a window mixing mapped and unmapped slots is
+ * MOT_ERR_BAD_LAYER_MAP).  Every check runs before any enqueue.
  */
 typedef struct {
     int32_t d_h;       /* translator width                               */

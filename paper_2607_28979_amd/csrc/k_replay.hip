@@ -13,9 +13,9 @@
 //   the gathered key rows loaded straight into A operands, a softmax over the
 //   set, and O^T = V_sel^T . P^T with V_sel staged transposed in LDS.
 // * k_causal_attn: the full causal attention of the bottom layers, tiled
-//   (64 query positions of one head, two tiles per workgroup paired short
-//   with long, 64-key chunks staged in LDS with the next chunk prefetched
-//   into registers, online softmax).
+//   (128 query positions of one head, two tiles per workgroup paired short
+//   with long, 64-key chunks of K and V^T loaded straight into LDS one chunk
+//   ahead, online softmax, v_mfma_f32_32x32x16_bf16).
 // Scores, softmax and accumulation are fp32; Q, K, V, O are bf16.
 #include "mot_device.h"
 #include "mot_internal.h"
@@ -26,6 +26,20 @@ namespace mot {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+// Raw buffer over `bytes` bytes at `base` (reads past the end return 0).
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, size_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0,
+                                             (int)(bytes < 0xFFFFFFFFu ? bytes : 0xFFFFFFFFu), 0x00020000);
+}
+
+// 16 bytes per lane from the buffer straight into this wave's 1 KB of LDS
+__device__ __forceinline__ void load_lds16(rsrc_t r, uint32_t off, u32x4* lds_dst_wave_base) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds_dst_wave_base, 16, off, 0, 0, 0);
+}
 
 // Monotone map float -> uint32 (a < b  <=>  key(a) < key(b) for non-NaN).
 __device__ __forceinline__ uint32_t order_key(float a) {
@@ -629,120 +643,147 @@ __global__ __launch_bounds__(256) void k_transpose_v(ReplayProblem p) {
     __syncthreads();
     const int64_t tpad = replay_tpad(p.T);
     uint16_t* out = p.vt + ((size_t)b * p.H_kv + kvh) * D * tpad + t0;
+    // chunk c of a row holds keys 16 (c / 2) + 4 (c % 2) + {0..3} and the
+    // same + 8: the order in which a 32x32 score block's accumulators hold
+    // them, so the causal kernel's P . V operands pair up without a shuffle
     for (int it = tid; it < D * 8; it += 256) {
-        const int d = it >> 3, c = it & 7;
+        const int d = it >> 3, c = it & 7, k0 = 16 * (c >> 1) + 4 * (c & 1);
         u32x4 w;
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-            w[j] = (uint32_t)tl[8 * c + 2 * j][d] | ((uint32_t)tl[8 * c + 2 * j + 1][d] << 16);
+        for (int j = 0; j < 4; ++j) {
+            const int k = k0 + (j < 2 ? 2 * j : 8 + 2 * (j - 2));
+            w[j] = (uint32_t)tl[k][d] | ((uint32_t)tl[k + 1][d] << 16);
+        }
         *reinterpret_cast<u32x4*>(out + (size_t)d * tpad + 8 * c) = w;
     }
 }
 
-// grid xcd_grid(npairs * H_q * B) with npairs = ceil(ceil(T/64) / 2), items
+// grid xcd_grid(npairs * H_q * B) with npairs = ceil(ceil(T/128) / 2), items
 // ordered (pair, head, batch row) pair fastest; 256 threads: query positions
-// u0 + 16w + l16 of head hq for two query tiles (a short and a long one);
-// 64-key chunks up to the tile's last position.  LDS: K chunk
-// [64][D], V^T chunk [D][64], P per wave [16][64] (bf16).
+// u0 + 32w + l32 of head hq for two query tiles of 128 (a short and a long
+// one); 64-key chunks up to the tile's last position.
+//
+// Per wave and chunk, on v_mfma_f32_32x32x16_bf16: scores^T[key][position]
+// for two 32-key blocks (A = K rows from LDS, B = the wave's 32 query rows,
+// held in registers), an online softmax per position (column), and
+// O^T[d][position] += V^T . P^T with A = V^T rows from LDS and B = the
+// probabilities straight from the score accumulators: a lane's accumulator
+// holds keys 8i + 4g + {0..3} of its position, and the staged V^T rows keep
+// each 16-key group in the matching order (keys 0-3, 8-11, 4-7, 12-15), so k
+// step s of the product takes accumulator elements 8 (s % 2) .. +7 of block
+// s / 2 as its B operand.  LDS: K chunk [64][D], V^T chunk [D][64] (bf16).
 template <int D>
-__global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
+__device__ __forceinline__ int causal_kswz(int r) {   // K rows: D/8 chunks
+    return D == 128 ? (r & 15) : ((r >> 1) & 7);
+}
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void k_causal_attn(ReplayProblem p) {
     constexpr int DC = D / 8;
-    constexpr int KSW = (DC < 16 ? DC : 16) - 1;
-    __shared__ u32x4 Kl[64 * DC];          // row key: chunk c at (c ^ (key & KSW))
-    __shared__ u32x4 Vt[D * 8];            // row d: 8 chunks of 8 keys, chunk c at (c ^ (d & 7))
-    __shared__ u32x4 Pl[4][16 * 8];        // per wave, row = position: chunk c at (c ^ (pos & 7))
+    constexpr int KS = 64 * DC, VS = D * 8;   // 16-byte slots of a K chunk and a V^T chunk
+    // two stages, each: K chunk rows (key: chunk c at c ^ causal_kswz(key)),
+    // then V^T rows (d: chunk c at c ^ ((d >> 1) & 7)); filled straight from
+    // global memory (buffer loads into LDS) one chunk ahead
+    __shared__ u32x4 lds[2 * (KS + VS)];
     // workgroup x runs query tile x and tile ntiles-1-x: every workgroup
     // walks about the same number of key chunks
-    const int ntiles = (p.T + 63) / 64, npairs = (ntiles + 1) / 2;
+    const int ntiles = (p.T + 127) / 128, npairs = (ntiles + 1) / 2;
     const int item = xcd_item(blockIdx.x, npairs * p.H_q * p.B);
     if (item >= npairs * p.H_q * p.B) return;   // uniform over the workgroup
     const int px = item % npairs, hq = (item / npairs) % p.H_q, b = item / (npairs * p.H_q);
-    for (int pass = 0; pass < 2; ++pass) {
-    const int tile = pass == 0 ? px : ntiles - 1 - px;
-    if (pass == 1 && tile <= px) break;   // uniform over the workgroup
-    const int u0 = tile * 64;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l16 = lane & 15, q4 = lane >> 4;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, l32 = lane & 31, g = lane >> 5;
     const int G = p.H_q / p.H_kv, kvh = hq / G;
-    const int u = u0 + 16 * w + l16;       // this lane's query column
     const uint16_t* Q = reinterpret_cast<const uint16_t*>(p.q);
-    const uint16_t* K = reinterpret_cast<const uint16_t*>(p.k);
     uint16_t* O = reinterpret_cast<uint16_t*>(p.o);
     const float sl2 = kLog2e / sqrtf((float)D);
     const u32x4 zero = {0u, 0u, 0u, 0u};
-    u32x4 qop[D / 32];
-#pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks)
-        qop[ks] = u < p.T ? *reinterpret_cast<const u32x4*>(Q + (((size_t)b * p.T + u) * p.H_q + hq) * D + 32 * ks + 8 * q4)
-                          : zero;
-    f32x4 acc[D / 16];
-#pragma unroll
-    for (int db = 0; db < D / 16; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float m = -INFINITY, l = 0.f;
-    const int last = (u0 + 63 < p.T ? u0 + 63 : p.T - 1);
-    // the next chunk's K rows and V^T rows are fetched into registers while
-    // the current one is computed: K items (key, d chunk), V^T items (d, 8-key
-    // chunk) from the transposed copy, whose keys past T are zero
-    constexpr int NKI = 64 * DC / 256, NVI = D * 8 / 256;
-    u32x4 kreg[NKI], vreg[NVI];
     const int64_t tpad = replay_tpad(p.T);
-    const uint16_t* VT = p.vt + ((size_t)b * p.H_kv + kvh) * D * tpad;
-    // key t of this batch row and KV head sits at row0 + t * ts in either
-    // layout; per chunk the base is scalar and each item adds a 32-bit offset
-    // (H_kv * D < 2^20 is checked on the host)
+    // key t of this batch row and KV head sits at row t * ts of the K buffer;
+    // the host admits only shapes whose byte offsets (up to (T + 64) * ts * 2)
+    // fit in 31 bits; rows past T lie past the descriptor's range and read as zero
     const uint32_t ts = p.kv_layout == MOT_LAYOUT_BTHD ? (uint32_t)(p.H_kv * D) : (uint32_t)D;
-    const size_t row0 = kv_row(p, b, 0, kvh);
-    auto fetch = [&](int kc0) {
-        const uint16_t* Kc = K + row0 + (size_t)kc0 * ts;
+    const rsrc_t kbuf = make_rsrc(reinterpret_cast<const uint16_t*>(p.k) + kv_row(p, b, 0, kvh),
+                                  ((size_t)(p.T - 1) * ts + D) * 2);
+    const rsrc_t vbuf = make_rsrc(p.vt + ((size_t)b * p.H_kv + kvh) * D * tpad, (size_t)D * tpad * 2);
+    // this lane's part of the chunk loads: wave load q fills slots
+    // (w * NQ + q) * 64 + lane of the K rows (NQ = KS / 256 loads), then of
+    // the V^T rows
+    constexpr int NQK = KS / 256, NQV = VS / 256;
+    uint32_t koff[NQK], voff[NQV];
 #pragma unroll
-        for (int i = 0; i < NKI; ++i) {
-            const int it = tid + 256 * i, kr = it / DC, c = it % DC;
-            kreg[i] = kc0 + kr < p.T ? *reinterpret_cast<const u32x4*>(Kc + ((uint32_t)kr * ts + 8 * c)) : zero;
-        }
+    for (int q = 0; q < NQK; ++q) {
+        const int slot = (w * NQK + q) * 64 + lane, kr = slot / DC, c = (slot % DC) ^ causal_kswz<D>(kr);
+        koff[q] = ((uint32_t)kr * ts + 8 * c) * 2;
+    }
 #pragma unroll
-        for (int i = 0; i < NVI; ++i) {
-            const int it = tid + 256 * i, d = it >> 3, c = it & 7;
-            vreg[i] = *reinterpret_cast<const u32x4*>(VT + (size_t)d * tpad + kc0 + 8 * c);
-        }
+    for (int q = 0; q < NQV; ++q) {
+        const int slot = (w * NQV + q) * 64 + lane, d = slot >> 3, c = (slot & 7) ^ ((d >> 1) & 7);
+        voff[q] = ((uint32_t)d * tpad + 8 * c) * 2;
+    }
+    auto issue = [&](int kc0, int st) {
+        u32x4* kb = lds + st * (KS + VS) + w * NQK * 64;
+        u32x4* vb = lds + st * (KS + VS) + KS + w * NQV * 64;
+#pragma unroll
+        for (int q = 0; q < NQK; ++q) load_lds16(kbuf, koff[q] + (uint32_t)kc0 * ts * 2, kb + q * 64);
+#pragma unroll
+        for (int q = 0; q < NQV; ++q) load_lds16(vbuf, voff[q] + (uint32_t)kc0 * 2, vb + q * 64);
     };
-    fetch(0);
+    auto barrier = [&]() {
+        __builtin_amdgcn_s_waitcnt(0x70);   // vmcnt(0) lgkmcnt(0)
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
+    for (int pass = 0; pass < 2; ++pass) {
+    const int tile = pass == 0 ? px : ntiles - 1 - px;
+    if (pass == 1 && tile <= px) break;   // uniform over the workgroup
+    const int u0 = tile * 128;
+    const int uw = u0 + 32 * w;            // first position of this wave
+    const int u = uw + l32;                // this lane's query column
+    u32x4 qop[D / 16];                     // k step s: d = 16 s + 8 g .. +7
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks)
+        qop[ks] = u < p.T ? *reinterpret_cast<const u32x4*>(Q + (((size_t)b * p.T + u) * p.H_q + hq) * D + 16 * ks + 8 * g)
+                          : zero;
+    f32x16 acc[D / 32];
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[db][e] = 0.f;
+    float m = -INFINITY, l = 0.f;
+    const int last = (u0 + 127 < p.T ? u0 + 127 : p.T - 1);
+    barrier();   // the previous tile's last chunk is consumed
+    issue(0, 0);
+    barrier();
     for (int kc0 = 0; kc0 <= last; kc0 += 64) {
-        __syncthreads();   // the previous chunk's K and V^T are consumed
-#pragma unroll
-        for (int i = 0; i < NKI; ++i) {
-            const int it = tid + 256 * i, kr = it / DC, c = it % DC;
-            Kl[kr * DC + (c ^ (kr & KSW))] = kreg[i];
-        }
-#pragma unroll
-        for (int i = 0; i < NVI; ++i) {
-            const int it = tid + 256 * i, d = it >> 3, c = it & 7;
-            Vt[d * 8 + (c ^ (d & 7))] = vreg[i];
-        }
-        __syncthreads();
-        if (kc0 + 64 <= last) fetch(kc0 + 64);
-        // scores^T[key][position] for 4 key blocks of 16.  Only the diagonal
-        // chunk (kc0 == u0, which also holds any keys past T) needs the mask:
-        // every key of an earlier chunk precedes every position of the tile.
-        const bool diag = kc0 == u0;
-        f32x4 sc[4];
+        const int st = (kc0 >> 6) & 1;
+        if (kc0 + 64 <= last) issue(kc0 + 64, st ^ 1);
+        const u32x4* Kl = lds + st * (KS + VS);
+        const u32x4* Vt = Kl + KS;
+        // keys after every position of this wave add nothing (uniform)
+        if (kc0 <= uw + 31 && uw < p.T) {
+        // scores^T[key][position], two blocks of 32 keys; only chunks that
+        // reach past the wave's first position need the mask
+        const bool diag = kc0 + 63 > uw;
+        f32x16 sc[2];
         float cm = -INFINITY;
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-            sc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-            const int kr = kb * 16 + l16;
+        for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-            for (int ks = 0; ks < D / 32; ++ks)
-                sc[kb] = mfma_16x16x32(Kl[kr * DC + ((4 * ks + q4) ^ (kr & KSW))], qop[ks], sc[kb]);
+            for (int e = 0; e < 16; ++e) sc[kb][e] = 0.f;
+            const int kr = kb * 32 + l32;
+#pragma unroll
+            for (int ks = 0; ks < D / 16; ++ks)
+                sc[kb] = mfma_32x32x16(Kl[kr * DC + ((2 * ks + g) ^ causal_kswz<D>(kr))], qop[ks], sc[kb]);
             if (diag) {
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int key = kc0 + kb * 16 + 4 * q4 + j;
-                    sc[kb][j] = key <= u ? sc[kb][j] : -INFINITY;
+                for (int e = 0; e < 16; ++e) {
+                    const int key = kc0 + kb * 32 + 8 * (e >> 2) + 4 * g + (e & 3);
+                    sc[kb][e] = key <= u ? sc[kb][e] : -INFINITY;
                 }
             }
 #pragma unroll
-            for (int j = 0; j < 4; ++j) cm = fmaxf(cm, sc[kb][j]);
+            for (int e = 0; e < 16; ++e) cm = fmaxf(cm, sc[kb][e]);
         }
-        cm = fmaxf(cm, __shfl_xor(cm, 16, 64));
         cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
         const float mn = fmaxf(m, cm);   // finite: chunk 0 holds key 0 <= u
         // v_exp_f32 directly: results below 2^-126 flush to 0, far below the
@@ -751,53 +792,50 @@ __global__ __launch_bounds__(256) void k_causal_attn(ReplayProblem p) {
         const float mo = mn * sl2;       // e = 2^(s sl2 - mn sl2)
         float rs = 0.f;
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const float e = __builtin_amdgcn_exp2f(fmaf(sc[kb][j], sl2, -mo));
-                sc[kb][j] = e;
-                rs += e;
+            for (int e = 0; e < 16; ++e) {
+                const float ex = __builtin_amdgcn_exp2f(fmaf(sc[kb][e], sl2, -mo));
+                sc[kb][e] = ex;
+                rs += ex;
             }
-        rs += __shfl_xor(rs, 16, 64);
         rs += __shfl_xor(rs, 32, 64);
         l = l * alpha + rs;
         // alpha is exactly 1 where the running maximum did not move: the
         // accumulators are rescaled only when some position's maximum rose
         if (__builtin_amdgcn_ballot_w64(mn != m)) {
 #pragma unroll
-            for (int db = 0; db < D / 16; ++db)
+            for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[db][j] *= alpha;
+                for (int e = 0; e < 16; ++e) acc[db][e] *= alpha;
         }
         m = mn;
-        uint32_t* Pw = reinterpret_cast<uint32_t*>(Pl[w]);
+        // O^T[d][position] += V^T . P^T, four k steps of 16 keys
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-            const int ch = (2 * kb + (q4 >> 1)) ^ (l16 & 7);
-            const int base = (l16 * 8 + ch) * 4 + 2 * (q4 & 1);
-            Pw[base] = pack_bf16x2(sc[kb][0], sc[kb][1]);
-            Pw[base + 1] = pack_bf16x2(sc[kb][2], sc[kb][3]);
+        for (int ks = 0; ks < 4; ++ks) {
+            const int kb = ks >> 1, e0 = 8 * (ks & 1);
+            const u32x4 pf = {pack_bf16x2(sc[kb][e0], sc[kb][e0 + 1]), pack_bf16x2(sc[kb][e0 + 2], sc[kb][e0 + 3]),
+                              pack_bf16x2(sc[kb][e0 + 4], sc[kb][e0 + 5]), pack_bf16x2(sc[kb][e0 + 6], sc[kb][e0 + 7])};
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db) {
+                const int dr = 32 * db + l32;
+                acc[db] = mfma_32x32x16(Vt[dr * 8 + ((2 * ks + g) ^ ((dr >> 1) & 7))], pf, acc[db]);
+            }
         }
-        wave_lds_sync();
-        // O^T[d][position] += V^T . P^T
-#pragma unroll
-        for (int db = 0; db < D / 16; ++db) {
-            const int dr = 16 * db + l16;
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks)
-                acc[db] = mfma_16x16x32(Vt[dr * 8 + ((4 * ks + q4) ^ (dr & 7))],
-                                        Pl[w][l16 * 8 + ((4 * ks + q4) ^ (l16 & 7))], acc[db]);
         }
-        wave_lds_sync();   // this wave's P row is rewritten next chunk
+        barrier();   // stage st^1 has landed; every wave is done with stage st
     }
+    // lane holds d = 32 db + 8 i + 4 g + {0..3} of position u
     if (u < p.T) {
         const float inv = 1.0f / l;
 #pragma unroll
-        for (int db = 0; db < D / 16; ++db) {
-            const u32x2 o2 = {pack_bf16x2(acc[db][0] * inv, acc[db][1] * inv),
-                              pack_bf16x2(acc[db][2] * inv, acc[db][3] * inv)};
-            *reinterpret_cast<u32x2*>(O + (((size_t)b * p.T + u) * p.H_q + hq) * D + 16 * db + 4 * q4) = o2;
-        }
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const u32x2 o2 = {pack_bf16x2(acc[db][4 * i] * inv, acc[db][4 * i + 1] * inv),
+                                  pack_bf16x2(acc[db][4 * i + 2] * inv, acc[db][4 * i + 3] * inv)};
+                *reinterpret_cast<u32x2*>(O + (((size_t)b * p.T + u) * p.H_q + hq) * D + 32 * db + 8 * i + 4 * g) = o2;
+            }
     }
     }
 }
@@ -842,11 +880,12 @@ hipError_t launch_replay_attention(const ReplayProblem& p, hipStream_t stream) {
             else hipLaunchKernelGGL((k_sparse_attn<64, replay_sparse_smax(64)>), grid, dim3(256), lds, stream, p);
         }
     } else {
-        if (!p.vt) return hipErrorInvalidValue;
+        if (!p.vt || !replay_causal_supported(p.T, p.H_kv, p.D, p.kv_layout == MOT_LAYOUT_BTHD))
+            return hipErrorInvalidValue;
         const dim3 tgrid((unsigned)(replay_tpad(p.T) / 64), p.H_kv, p.B);
         if (p.D == 128) hipLaunchKernelGGL(k_transpose_v<128>, tgrid, dim3(256), 0, stream, p);
         else hipLaunchKernelGGL(k_transpose_v<64>, tgrid, dim3(256), 0, stream, p);
-        const int npairs = ((p.T + 63) / 64 + 1) / 2;
+        const int npairs = ((p.T + 127) / 128 + 1) / 2;
         const dim3 grid(xcd_grid(npairs * p.H_q * p.B));
         if (p.D == 128) hipLaunchKernelGGL(k_causal_attn<128>, grid, dim3(256), 0, stream, p);
         else hipLaunchKernelGGL(k_causal_attn<64>, grid, dim3(256), 0, stream, p);

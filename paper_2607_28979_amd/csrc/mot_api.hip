@@ -533,6 +533,10 @@ mot_status check_replay(const mot_replay_shapes* s, bool need_s) {
     if (need_s && !replay_sparse_supported(s->D, s->S))
         return fail(MOT_ERR_UNSUPPORTED, "S=%d: need a multiple of 32 from 32 to %d for D = %d", s->S,
                     replay_sparse_smax(s->D), s->D);
+    if (!need_s && !replay_causal_supported(s->T, s->H_kv, s->D, s->kv_layout == MOT_LAYOUT_BTHD))
+        return fail(MOT_ERR_UNSUPPORTED, "T=%d: a batch row's K of %lld bytes exceeds the 2 GiB the causal kernel "
+                    "addresses", s->T,
+                    (long long)s->T * (s->kv_layout == MOT_LAYOUT_BTHD ? s->H_kv * s->D : s->D) * 2);
     return MOT_OK;
 }
 }  // namespace
@@ -742,6 +746,9 @@ mot_status check_backbone(const mot_shapes* s, const mot_backbone_dims* bd) {
         return fail(MOT_ERR_UNSUPPORTED, "backbone sizes: d_in, d_h multiples of 64 up to 4096 (n_slots * d_h too), "
                     "d_ff a multiple of 64, d_out of 8, head width d_h / n_heads 64 or 128 (got d_in=%d d_h=%d "
                     "n_heads=%d d_ff=%d d_out=%d n_slots=%d)", d_in, d_h, nh, d_ff, d_out, N);
+    if (!replay_causal_supported(s->T, nh, d_h / nh, true))
+        return fail(MOT_ERR_UNSUPPORTED, "T=%d: a batch row's attention keys (%lld bytes) exceed the 2 GiB the "
+                    "causal kernel addresses", s->T, (long long)s->T * d_h * 2);
     return MOT_OK;
 }
 }  // namespace

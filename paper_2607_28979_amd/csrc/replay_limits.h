@@ -51,4 +51,11 @@ constexpr bool replay_sparse_pair_supported(int D, int S, int G) {
     return replay_sparse_supported(D, S) && S <= 128 && G >= 1 && 2 * G <= 16;
 }
 
+// The full causal kernel addresses a batch row's K (and V^T) through 32-bit
+// byte offsets: rows of `ts` elements (H_kv * D for BTHD, D for BHTD) for
+// T positions must stay under 2 GiB.
+constexpr bool replay_causal_supported(long long T, long long H_kv, int D, bool bthd) {
+    return (T + 64) * (bthd ? H_kv * D : D) * 2 < (1LL << 31);
+}
+
 }  // namespace mot

@@ -357,6 +357,12 @@ def test_workspace_size_queries(lib):
     assert mb.replay_workspace_bytes(1, 64, 4, 4, 64, S=32, with_sets=True) == 0
     with pytest.raises(mb.MotError):
         mb.replay_workspace_bytes(1, 64, 4, 4, 96)
+    # the causal kernel addresses a batch row's K rows with 32-bit byte
+    # offsets: (T + 64) * H_kv * D * 2 < 2^31 in BTHD (here H_kv * D = 256)
+    t_max = (1 << 31) // (256 * 2) - 64 - 1
+    assert mb.replay_workspace_bytes(1, t_max, 4, 2, 128) == 2 * 128 * (-(-t_max // 64) * 64) * 2
+    with pytest.raises(mb.MotError, match="2 GiB"):
+        mb.replay_workspace_bytes(1, t_max + 1, 4, 2, 128)
     s = _shapes(H_tgt=2, D_tgt=64, T=70)
     n = mb.backbone_workspace_bytes(s, 128, 2, 256)
     assert n > 70 * (64 * 2 + 128 * 2 * 9 + 256 * 2 + 128 * 4)   # B = 1: every activation row once

@@ -172,7 +172,10 @@ def test_sparse_attention_padding_and_invalid_entries(oracle_built):
     assert rel_frob(got[0, keep], want[0, keep]) <= TOL["bf16"]
 
 
-@pytest.mark.parametrize("B,T,Hq,Hkv,D,lay", [(1, 200, 4, 2, 128, 0), (2, 130, 6, 1, 64, 1), (1, 64, 2, 2, 128, 0)])
+@pytest.mark.parametrize("B,T,Hq,Hkv,D,lay", [(1, 200, 4, 2, 128, 0), (2, 130, 6, 1, 64, 1), (1, 64, 2, 2, 128, 0),
+                                              # several 128-position tile pairs, a ragged last tile,
+                                              # seven query heads per KV head
+                                              (1, 1000, 14, 2, 128, 1), (2, 333, 4, 4, 64, 0)])
 def test_causal_attention_parity(B, T, Hq, Hkv, D, lay, oracle_built):
     from oracle import oracle_replay_attention
     print("case causal", B, T, Hq, Hkv, D, lay, flush=True)
