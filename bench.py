@@ -503,7 +503,8 @@ def bench_replay(args):
     # selected K and V rows it gathers per (query, KV head) are reported beside
     sp_gather_sets = 2.0 * 2 * w.D * w.H_kv * w.B * sum(min(u + 1, w.S) for u in range(w.T))
     sp_gather = sp_gather_sets
-    if w.D in (64, 128) and w.S <= 128 and 2 * (w.H_q // w.H_kv) <= 16:   # the library's rule for that kernel
+    pair = w.D in (64, 128) and w.S <= 128 and 2 * (w.H_q // w.H_kv) <= 16   # the library's rule for that kernel
+    if pair:
         # the two-position kernel gathers the union of a pair's sets once (or
         # both sets when the union exceeds its 192-key limit): count the rows
         # on this run's own sets, averaged over the sparse layers
@@ -533,7 +534,8 @@ def bench_replay(args):
     share = {"select": avg["select"] * (w.L_tgt - w.L_full), "sparse": avg["sparse"] * (w.L_tgt - w.L_full),
              "causal": avg["causal"] * w.L_full}
     dom = max(share, key=share.get)
-    kname = {"select": "k_topS_select", "sparse": "k_sparse_attn", "causal": "k_causal_attn"}
+    kname = {"select": "k_topS_select", "sparse": "k_sparse_attn_pair" if pair else "k_sparse_attn",
+             "causal": "k_causal_attn"}
     roof = dict(rows[dom], kernel=kname[dom],
                 traffic=measured_traffic("k_replay.hip", "k_replay", "qwen2.5-7b-replay-8k") if dom == "sparse" else None)
     cpu = None if args.no_cpu_baseline else cpu_baseline_replay(w, args.cpu_rows)
