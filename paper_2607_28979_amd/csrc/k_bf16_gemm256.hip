@@ -12,20 +12,28 @@
 // One 256-thread workgroup per CU (128 KB of LDS): four waves in a 2 x 2
 // grid, 128 x 128 outputs per wave = 4 x 4 blocks of v_mfma_f32_32x32x16_bf16
 // (256 accumulators per lane, held in the AGPR half of the register file).
-// Per 64-wide K slice a tile moves 64 KB into LDS for 2 * 256 * 256 * 64
-// flops (128 flop/B, twice the 128 x 128 form's), which keeps the L2->CU
-// and LDS rates well under their limits at the matrix cores' rate.
+// Per 32-wide K slice a tile moves 32 KB into LDS for 2 * 256 * 256 * 32
+// flops (128 flop/B, twice the 128 x 128 form's).
 //
 // Operands go global -> LDS directly (buffer_load_dwordx4 ... lds, 16 bytes
 // per lane, through a buffer descriptor per operand; the MUBUF form rather
 // than global_load_lds, whose FLAT encoding makes the compiler's wait
 // insertion treat every later LDS read as out of order and wait for all of
-// them): a wave's load fills 1 KB of LDS = 8 rows of 8 16-byte chunks, and the lane
-// order within those rows is chosen so that row r stores logical chunk c at
-// physical chunk c ^ ((r >> 1) & 7).  Sixteen lanes of a fragment read (16
-// consecutive rows, one logical chunk) then hit 16 distinct 16-byte bank
-// groups.  Two LDS stages; the loads of slice k+1 are issued before the MFMAs
-// of slice k, and one barrier per slice retires both.
+// them): a wave's load fills 1 KB of LDS = 16 rows of four 16-byte chunks,
+// and the lane order within those rows is chosen so that row r stores
+// logical chunk c at physical chunk c ^ ((r >> 2) & 3).  Sixteen lanes of a
+// fragment read (16 consecutive rows, one logical chunk) then hit 16
+// distinct 16-byte bank groups.
+//
+// Five LDS stages (all 160 KB): the loads of slice k+4 are trickled over the
+// MFMAs of slice k, one 1 KB load after every four MFMAs.  A wave that issues
+// several loads back to back cannot issue its next MFMA until the memory
+// pipeline has accepted them, so loads bunched at the start of a slice stall
+// the matrix core although they complete asynchronously; one load per four
+// MFMAs (32 B per clock per CU, about half of what the path sustains) does
+// not.  Every load is a per-lane offset computed once plus the slice's
+// uniform offset in a scalar register, so the loop does almost no vector
+// address arithmetic.  One barrier per slice.
 //
 // Bias terms enter through the accumulators' initial values: gemm1 starts
 // from b1 (each lane's rows are 4 consecutive hidden units), gemm2 from two
@@ -39,25 +47,18 @@ namespace mot {
 
 namespace {
 
-#ifndef MOT_G256_BK
-#define MOT_G256_BK 64   // K slice per LDS stage: 64 (two stages) or 32 (four stages)
-#endif
-
 constexpr int kTile = 256;
 constexpr int kGroup = 32;              // B tiles per dispatch group
 
-// LDS geometry of a K slice of BK columns: rows of CPR 16-byte chunks, a
-// wave's 1 KB load fills RPI rows, NI loads per operand and wave, NST stages
-// of STAGE slots (A rows then B rows) in 128 KB, NSUB k-steps of 16.
-// Logical chunk c of row r sits at c ^ swz(r): 16 consecutive rows of one
-// logical chunk fill 16 distinct 16-byte bank groups.
-template <int BK>
-struct Geo {
-    static constexpr int CPR = BK / 8, RPI = 64 / CPR, NI = kTile / RPI / 4;
-    static constexpr int NST = BK == 64 ? 2 : 4, STAGE = 2 * kTile * CPR, NSUB = BK / 16;
-    __device__ static int swz(int r) { return CPR == 8 ? (r >> 1) & 7 : (r >> 2) & 3; }
-};
-static_assert(Geo<64>::NST * Geo<64>::STAGE == 8192 && Geo<32>::NST * Geo<32>::STAGE == 8192, "128 KB of LDS");
+// LDS geometry of a 32-wide K slice: rows of four 16-byte chunks, a wave's
+// 1 KB load fills 16 rows, kNI loads per operand and wave, kNST stages of
+// kStage slots (A rows then B rows).  Logical chunk c of row r sits at
+// c ^ swz(r): 16 consecutive rows of one logical chunk fill 16 distinct
+// 16-byte bank groups.
+constexpr int kBK = 32, kCPR = kBK / 8, kRPI = 64 / kCPR, kNI = kTile / kRPI / 4;
+constexpr int kNST = 5, kStage = 2 * kTile * kCPR;
+static_assert(kNST * kStage * 16 == 160 * 1024, "160 KB of LDS");
+__device__ __forceinline__ int swz(int r) { return (r >> 2) & 3; }
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -67,10 +68,6 @@ typedef __amdgpu_buffer_rsrc_t rsrc_t;
 __device__ __forceinline__ rsrc_t make_rsrc(const void* base, size_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0,
                                              (int)(bytes < 0xFFFFFFFFu ? bytes : 0xFFFFFFFFu), 0x00020000);
-}
-
-__device__ __forceinline__ void load_lds16(rsrc_t r, uint32_t off, u32x4* lds_dst_wave_base) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds_dst_wave_base, 16, off, 0, 0, 0);
 }
 
 // Dispatch order: groups of kGroup consecutive B tiles (tokens), A tiles
@@ -99,56 +96,61 @@ __device__ __forceinline__ uint32_t src_k_bytes(const Problem& p, int k) {
 // count 0, export count left at its maximum
 constexpr int waitcnt_vm_lgkm0(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
 
-// The K loop shared by both products.  rowA/rowB: this lane's NI + NI row
-// byte offsets into the operands' buffers (rows RPI*J + lane/CPR of the
-// tile, J = wave*NI + q); kofs(kt, c, &a, &b) gives the byte offsets of
-// logical chunk c of slice kt.  acc holds the initial values on entry.
+// The K loop shared by both products.  voA / voB: this lane's byte offsets
+// into the operands' buffers for its rows of each of its kNI loads per
+// operand (rows kRPI*J + lane/kCPR of the tile, J = wave*kNI + q), including
+// the column offset of its chunk wherever that offset is the same in every
+// slice; slice(kt, sa, sb, vb) gives slice kt's uniform byte offsets sa, sb
+// and a per-lane term vb added to voB (zero where B's column offset is
+// uniform).  acc holds the initial values on entry.
 //
-// Register double buffering: the fragments of k-step s+1 are read while the
-// 16 MFMAs of step s run.  The slice's barrier sits before the MFMAs of its
-// last k-step (whose fragments are already in registers), and the first
-// fragments of the next slice are read right after it, so the matrix core
-// has queued work across the barrier.  Slice kt+NST-1 is loaded while slice
-// kt is computed.
-template <int BK, class KOfs>
-__device__ __forceinline__ void k_loop(u32x4* lds, rsrc_t bufA, rsrc_t bufB, const uint32_t (&rowA)[Geo<BK>::NI],
-                                       const uint32_t (&rowB)[Geo<BK>::NI], int nk, KOfs kofs, f32x16 (&acc)[4][4]) {
-    using Gm = Geo<BK>;
-    constexpr int CPR = Gm::CPR, NI = Gm::NI, NST = Gm::NST, NSUB = Gm::NSUB;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// Register double buffering: the fragments of k-step 1 are read while the
+// 16 MFMAs of k-step 0 run; the slice's barrier sits before the MFMAs of
+// k-step 1 (whose fragments are already in registers), and the next slice's
+// first fragments are read right after it, so the matrix core has queued
+// work across the barrier.  Slice indices past the end are clamped (a
+// redundant reload into a stage that is no longer read), so every barrier
+// waits for the same count.
+template <class Slice>
+__device__ __forceinline__ void k_loop(u32x4* lds, rsrc_t bufA, rsrc_t bufB, const uint32_t (&voA)[kNI],
+                                       const uint32_t (&voB)[kNI], int nk, Slice slice, f32x16 (&acc)[4][4]) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1, g = lane >> 5, l32 = lane & 31;
-    const int sw = Gm::swz(l32);
-    const int L = lane / CPR, pc = lane % CPR;
-
-    auto issue = [&](int kt, int st) {
-        u32x4* base = lds + st * Gm::STAGE + wave * NI * 64;
-#pragma unroll
-        for (int q = 0; q < NI; ++q) {
-            uint32_t oa, ob;
-            kofs(kt, pc ^ Gm::swz(Gm::RPI * q + L), oa, ob);   // the wave's row offset keeps swz
-            load_lds16(bufA, rowA[q] + oa, base + q * 64);
-            load_lds16(bufB, rowB[q] + ob, base + kTile * CPR + q * 64);
-        }
+    const int sw = swz(l32);
+    u32x4* const wbase = lds + wave * kNI * 64;
+    // load l of the 2 kNI per wave and slice: q-pair l / 2, operand A (even) or B (odd)
+    auto ld1 = [&](int st, uint32_t sa, uint32_t sb, uint32_t vb, int l) {
+        const int q = l >> 1;
+        u32x4* dst = wbase + st * kStage + ((l & 1) ? kTile * kCPR : 0) + q * 64;
+        if (l & 1) __builtin_amdgcn_raw_ptr_buffer_load_lds(bufB, (lds_void*)dst, 16, voB[q] + vb, sb, 0, 0);
+        else __builtin_amdgcn_raw_ptr_buffer_load_lds(bufA, (lds_void*)dst, 16, voA[q], sa, 0, 0);
     };
     // fragments of k-step s of stage st: rows wm*128 + i*32 + l32 (A) and
     // wn*128 + i*32 + l32 (B), logical chunk 2s + g
     auto read = [&](int st, int s, u32x4 (&a)[4], u32x4 (&b)[4]) {
-        const u32x4* la = lds + st * Gm::STAGE + (wm * 128 + l32) * CPR;
-        const u32x4* lb = lds + st * Gm::STAGE + kTile * CPR + (wn * 128 + l32) * CPR;
+        const u32x4* la = lds + st * kStage + (wm * 128 + l32) * kCPR;
+        const u32x4* lb = lds + st * kStage + kTile * kCPR + (wn * 128 + l32) * kCPR;
         const int c = (2 * s + g) ^ sw;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            a[i] = la[i * 32 * CPR + c];
-            b[i] = lb[i * 32 * CPR + c];
+            a[i] = la[i * 32 * kCPR + c];
+            b[i] = lb[i * 32 * kCPR + c];
         }
     };
-    auto mma = [&](const u32x4 (&a)[4], const u32x4 (&b)[4]) {
+    // the 16 MFMAs of a k-step with loads 4h .. 4h+3 of slice kt+4, one after
+    // every four (sched_barrier fences keep that order, and keep each read
+    // group ahead of the MFMAs that precede its use)
+    auto mma_ld = [&](const u32x4 (&a)[4], const u32x4 (&b)[4], int st, uint32_t sa, uint32_t sb, uint32_t vb,
+                      int h) {
 #pragma unroll
-        for (int bm = 0; bm < 4; ++bm)
+        for (int bm = 0; bm < 4; ++bm) {
 #pragma unroll
             for (int bn = 0; bn < 4; ++bn) acc[bm][bn] = mfma_32x32x16(a[bm], b[bn], acc[bm][bn]);
+            ld1(st, sa, sb, vb, 4 * h + bm);
+            __builtin_amdgcn_sched_barrier(0);
+        }
     };
-
     // workgroup barrier after an explicit wait: __syncthreads() would add its
     // own fence, which waits for every load in flight (vmcnt(0)) and so for
     // the later slices' loads too.  The waits are s_waitcnt instructions the
@@ -157,62 +159,41 @@ __device__ __forceinline__ void k_loop(u32x4* lds, rsrc_t bufA, rsrc_t bufB, con
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
     };
-    u32x4 a0[4], b0[4], a1[4], b1[4];
-    if constexpr (NST == 2) {
-        issue(0, 0);
-        __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
-    } else {
-        // slices 0..2 in flight, wait for slice 0 (2 * NI loads per slice)
-        issue(0, 0);
-        if (nk > 1) issue(1, 1);
-        if (nk > 2) issue(2, 2);
-        if (nk > 2) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(4 * NI));
-        else if (nk > 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(2 * NI));
-        else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+    // slices 0..3 in flight, wait for slice 0
+#pragma unroll
+    for (int s0 = 0; s0 < kNST - 1; ++s0) {
+        uint32_t sa, sb, vb;
+        slice(s0 < nk ? s0 : nk - 1, sa, sb, vb);
+#pragma unroll
+        for (int l = 0; l < 2 * kNI; ++l) ld1(s0, sa, sb, vb, l);
     }
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0((kNST - 2) * 2 * kNI));
     barrier();
+    u32x4 a0[4], b0[4], a1[4], b1[4];
     read(0, 0, a0, b0);
+    int st = 0, stl = kNST - 1;   // stages of slices kt and kt + 4
     for (int kt = 0; kt < nk; ++kt) {
-        const int st = kt % NST;
-        const bool more = kt + 1 < nk;
-        // sched_barrier fences keep each read group ahead of the MFMAs that
-        // precede its use (the scheduler would otherwise sink the reads next
-        // to their first use and expose the LDS latency)
-        if (kt + NST - 1 < nk) issue(kt + NST - 1, (kt + NST - 1) % NST);
-        if constexpr (NSUB == 4) {
-            read(st, 1, a1, b1);
-            __builtin_amdgcn_sched_barrier(0);
-            mma(a0, b0);
-            __builtin_amdgcn_sched_barrier(0);
-            read(st, 2, a0, b0);
-            __builtin_amdgcn_sched_barrier(0);
-            mma(a1, b1);
-            __builtin_amdgcn_sched_barrier(0);
-            read(st, 3, a1, b1);
-            __builtin_amdgcn_sched_barrier(0);
-            mma(a0, b0);
-        } else {
-            read(st, 1, a1, b1);
-            __builtin_amdgcn_sched_barrier(0);
-            mma(a0, b0);
-        }
+        const int kl = kt + kNST - 1;
+        uint32_t sa, sb, vb;
+        slice(kl < nk ? kl : nk - 1, sa, sb, vb);
+        read(st, 1, a1, b1);
         __builtin_amdgcn_sched_barrier(0);
-        // every wave's reads of stage st are in registers and its loads of
-        // slice kt+1 have landed (slices up to kt+NST-1 may stay in flight):
-        // stage (kt+1) % NST is complete, stage st is free
-        if constexpr (NST == 2) {
-            __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
-        } else {
-            if (kt + 3 < nk) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(4 * NI));
-            else if (kt + 2 < nk) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(2 * NI));
-            else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
-        }
+        mma_ld(a0, b0, stl, sa, sb, vb, 0);
+        // every wave's reads of stage st are in registers and slice kt+1 has
+        // landed: slices kt+2, kt+3 and the four loads of slice kt+4 issued
+        // above may stay in flight
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0((kNST - 3) * 2 * kNI + kNI));
         barrier();
-        if (more) read((kt + 1) % NST, 0, a0, b0);
+        const int st1 = st + 1 == kNST ? 0 : st + 1;
+        if (kt + 1 < nk) read(st1, 0, a0, b0);
         __builtin_amdgcn_sched_barrier(0);
-        mma(a1, b1);
+        mma_ld(a1, b1, stl, sa, sb, vb, 1);
         __builtin_amdgcn_sched_barrier(0);
+        st = st1;
+        stl = stl + 1 == kNST ? 0 : stl + 1;
     }
+    // the clamped reloads of the last slices are still in flight
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
 }
 
 // Accumulators of block (bm, bn) start at the bias products of a 32-row
@@ -270,10 +251,9 @@ __device__ __forceinline__ size_t routed_hidden_elems(const Problem& p) {
 // index, A is W1_m, and the hidden rows are stored in assignment order with
 // the assignment's gate.
 // ---------------------------------------------------------------------------
-template <bool ROUTED, int BK>
+template <bool ROUTED>
 __global__ __launch_bounds__(256, 1) void k_bf16_gemm1_256(Problem p, UnitTab ut) {
-    using Gm = Geo<BK>;
-    __shared__ u32x4 lds[Gm::NST * Gm::STAGE];
+    __shared__ u32x4 lds[kNST * kStage];
     const uint32_t code = ut.code[blockIdx.z];
     const int j = unit_j(code), x = unit_x(code), i = unit_i(code), gs = unit_gslot(code);
     // A rows: E*hidden (dense) or the hidden units of one translator (routed)
@@ -298,20 +278,25 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm1_256(Problem p, UnitTab ut
     const rsrc_t bufB = make_rsrc(reinterpret_cast<const char*>(p.src[x]) + (size_t)i * p.n_tok * p.d_in * 2,
                                   (size_t)p.n_tok * p.d_in * 2);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int L = lane / Gm::CPR;
+    const int L = lane / kCPR;
+    // this lane's logical chunk: the same in each of its loads (their rows
+    // differ by multiples of 16, which swz ignores)
+    const int c = (lane % kCPR) ^ swz(L);
 
-    uint32_t rowA[Gm::NI], rowB[Gm::NI];
+    uint32_t voA[kNI], voB[kNI];
 #pragma unroll
-    for (int q = 0; q < Gm::NI; ++q) {
-        const int r = Gm::RPI * (wave * Gm::NI + q) + L;
-        rowA[q] = (uint32_t)min(hid0 + r, EH - 1) * p.d_in * 2;
+    for (int q = 0; q < kNI; ++q) {
+        const int r = kRPI * (wave * kNI + q) + L;
+        voA[q] = (uint32_t)min(hid0 + r, EH - 1) * p.d_in * 2 + 16 * c;
         const int tok = ROUTED ? list[first + min(r, rows - 1)] : min(tok0 + r, p.n_tok - 1);
-        rowB[q] = src_row_bytes(p, tok);
+        voB[q] = src_row_bytes(p, tok);
     }
-    auto kofs = [&](int kt, int c, uint32_t& oa, uint32_t& ob) {
-        const int k = kt * BK + 8 * c;
-        oa = (uint32_t)k * 2;
-        ob = (uint32_t)src_k_bytes(p, k);
+    // W1 columns are uniform; a source row's column offset depends on the
+    // layout (BHTD: head-major), so it is a per-lane term, once per slice
+    auto slice = [&](int kt, uint32_t& sa, uint32_t& sb, uint32_t& vb) {
+        sa = (uint32_t)kt * kBK * 2;
+        sb = 0;
+        vb = src_k_bytes(p, kt * kBK + 8 * c);
     };
 
     // accumulators start at b1: lane rows of block bm are hidden
@@ -336,7 +321,7 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm1_256(Problem p, UnitTab ut
         for (int bn = 0; bn < 4; ++bn) acc[bm][bn] = init;
     }
 
-    k_loop<BK>(lds, bufA, bufB, rowA, rowB, p.d_in / BK, kofs, acc);
+    k_loop(lds, bufA, bufB, voA, voB, p.d_in / kBK, slice, acc);
 
     // epilogue: GELU, * gate, round to bf16, fragment-native hidden store
     // (16-byte units of 8 hidden values of one row, [r/32][kk/8][r%32]; rows
@@ -380,10 +365,9 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm1_256(Problem p, UnitTab ut
 // target row (top_k = 1) or, in fp32, to the assignment's row of the
 // per-assignment buffer that the combine kernel sums (top_k > 1).
 // ---------------------------------------------------------------------------
-template <bool ROUTED, int BK>
+template <bool ROUTED>
 __global__ __launch_bounds__(256, 1) void k_bf16_gemm2_256(Problem p, UnitTab ut) {
-    using Gm = Geo<BK>;
-    __shared__ u32x4 lds[Gm::NST * Gm::STAGE];
+    __shared__ u32x4 lds[kNST * kStage];
     const uint32_t code = ut.code[blockIdx.z];
     const int j = unit_j(code), x = unit_x(code), gs = unit_gslot(code);
     const int EH = ROUTED ? p.hidden : p.E * p.hidden;   // the K axis
@@ -406,21 +390,26 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm2_256(Problem p, UnitTab ut
                                   (size_t)EH * p.d_out * 2);
     const rsrc_t bufB = make_rsrc(reinterpret_cast<const char*>(p.hbuf) + blockIdx.z * hstride * 2, hstride * 2);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int L = lane / Gm::CPR;
+    const int L = lane / kCPR;
+    const int c = (lane % kCPR) ^ swz(L);   // this lane's logical chunk, the same in each load
 
-    uint32_t rowA[Gm::NI], rowB[Gm::NI];
+    uint32_t voA[kNI], voB[kNI];
 #pragma unroll
-    for (int q = 0; q < Gm::NI; ++q) {
-        const int r = Gm::RPI * (wave * Gm::NI + q) + L;
+    for (int q = 0; q < kNI; ++q) {
+        const int r = kRPI * (wave * kNI + q) + L;
         const int o = min(out0 + r, p.d_out - 1);
         const int t = min(tok0 + r, row_end - 1);
-        rowA[q] = (uint32_t)o * p.hidden * 2;
-        rowB[q] = ((uint32_t)(t >> 5) * (EH >> 3) * 256 + (t & 31) * 8) * 2;
+        voA[q] = (uint32_t)o * p.hidden * 2 + 16 * c;
+        voB[q] = ((uint32_t)(t >> 5) * (EH >> 3) * 256 + (t & 31) * 8) * 2 + 512 * c;
     }
-    auto kofs = [&](int kt, int c, uint32_t& oa, uint32_t& ob) {
-        const int k0 = kt * BK, e = k0 / p.hidden;
-        oa = ((uint32_t)e * p.d_out * p.hidden + (k0 - e * p.hidden) + 8 * c) * 2;
-        ob = (uint32_t)((k0 >> 3) + c) * 512;
+    // W2cat is [E][d_out][hidden]: slice kt lies in expert k0 / hidden (hidden
+    // is a multiple of 64); the hidden buffer's 16-byte units of a slice are
+    // [t/32][k/8][t%32], so both column offsets are uniform
+    auto slice = [&](int kt, uint32_t& sa, uint32_t& sb, uint32_t& vb) {
+        const int k0 = kt * kBK, e = k0 / p.hidden;
+        sa = ((uint32_t)e * p.d_out * p.hidden + (k0 - e * p.hidden)) * 2;
+        sb = (uint32_t)(k0 >> 3) * 512;
+        vb = 0;
     };
 
     // accumulators start at sum_e g_e(t) b2_e[o] (routed: g(t) b2_m[o])
@@ -449,7 +438,7 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm2_256(Problem p, UnitTab ut
         }
     }
 
-    k_loop<BK>(lds, bufA, bufB, rowA, rowB, EH / BK, kofs, acc);
+    k_loop(lds, bufA, bufB, voA, voB, EH / kBK, slice, acc);
 
     // epilogue: four consecutive outputs of one row per store
     const int32_t* list = ROUTED ? p.rt.list + (size_t)gs * p.n_tok * p.top_k : nullptr;
@@ -514,14 +503,14 @@ hipError_t launch_bf16_gemm1_256(const Problem& p, const UnitTab& ut, hipStream_
     if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
     const int EH = p.E * p.hidden;
     dim3 grid(((EH + kTile - 1) / kTile) * ((p.n_tok + kTile - 1) / kTile), 1, ut.n);
-    hipLaunchKernelGGL((k_bf16_gemm1_256<false, MOT_G256_BK>), grid, dim3(256), 0, stream, p, ut);
+    hipLaunchKernelGGL(k_bf16_gemm1_256<false>, grid, dim3(256), 0, stream, p, ut);
     return hipGetLastError();
 }
 
 hipError_t launch_bf16_gemm2_256(const Problem& p, const UnitTab& ut, hipStream_t stream) {
     if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
     dim3 grid(((p.d_out + kTile - 1) / kTile) * ((p.n_tok + kTile - 1) / kTile), 1, ut.n);
-    hipLaunchKernelGGL((k_bf16_gemm2_256<false, MOT_G256_BK>), grid, dim3(256), 0, stream, p, ut);
+    hipLaunchKernelGGL(k_bf16_gemm2_256<false>, grid, dim3(256), 0, stream, p, ut);
     return hipGetLastError();
 }
 
@@ -540,14 +529,14 @@ size_t bf16_routed_hidden_bytes(const Problem& p) {
 hipError_t launch_bf16_gemm1_routed(const Problem& p, const UnitTab& ut, hipStream_t stream) {
     if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
     dim3 grid(((p.hidden + kTile - 1) / kTile) * p.rt.max_tiles, 1, ut.n);
-    hipLaunchKernelGGL((k_bf16_gemm1_256<true, MOT_G256_BK>), grid, dim3(256), 0, stream, p, ut);
+    hipLaunchKernelGGL(k_bf16_gemm1_256<true>, grid, dim3(256), 0, stream, p, ut);
     return hipGetLastError();
 }
 
 hipError_t launch_bf16_gemm2_routed(const Problem& p, const UnitTab& ut, hipStream_t stream) {
     if (ut.n == 0 || p.n_tok == 0) return hipSuccess;
     dim3 grid(((p.d_out + kTile - 1) / kTile) * p.rt.max_tiles, 1, ut.n);
-    hipLaunchKernelGGL((k_bf16_gemm2_256<true, MOT_G256_BK>), grid, dim3(256), 0, stream, p, ut);
+    hipLaunchKernelGGL(k_bf16_gemm2_256<true>, grid, dim3(256), 0, stream, p, ut);
     return hipGetLastError();
 }
 
