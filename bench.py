@@ -208,15 +208,21 @@ def main():
     value = n_tok / (ms_per_step / 1e3)
     flops = w.gemm_flops()
     fusable = w.dtype == "bf16" and w.d_in in (128, 256, 512) and w.d_out in (128, 256, 512)
-    routed = args.algo == 3 or (args.algo == 0 and fusable and 0 < w.top_k < w.E)
+    # the library's rule: Top-K with K < E takes the routed path on bf16 (the
+    # fused kernel's routed mode on its shapes, the routed large-tile GEMMs
+    # elsewhere)
+    routed = w.dtype == "bf16" and (args.algo == 3 or (args.algo == 0 and 0 < w.top_k < w.E))
     fused = not routed and (args.algo == 2 or (args.algo == 0 and fusable))
+    # the library's rule for the fp32 matrix-core kernels (else router + vector-ALU GEMMs)
+    f32_mfma = w.dtype == "f32" and w.hidden % 64 == 0 and w.d_in % 16 == 0 and w.d_out % 4 == 0
     achieved_tflops = flops / (avg_call_ms / 1e3) / 1e12
     peak = PEAK_TFLOPS[w.dtype]
     roofline = {
         "bound": "mfma",
-        "kernel": ("k_bf16_fused" if fused else
-                   "mot_translate routed (router lists + plan + k_bf16_fused tiles%s)"
-                   % (" + combine" if w.top_k > 1 else "") if routed
+        "kernel": ("k_bf16_fused" if fused else "k_f32_mfma_gemm1 + k_f32_mfma_gemm2" if f32_mfma else
+                   "mot_translate routed (router lists + plan + %s%s)"
+                   % ("k_bf16_fused tiles" if fusable else "routed large-tile GEMMs",
+                      " + combine" if w.top_k > 1 else "") if routed
                    else "mot_translate (router + gemm1 + gemm2)"),
         "achieved": round(achieved_tflops, 2),
         "peak": peak,
@@ -224,8 +230,8 @@ def main():
         "frac": round(achieved_tflops / peak, 4),
         "traffic": (None if routed or args.top_k else
                     measured_traffic("k_bf16_fused_kernel.h", "k_bf16_fused", WORKLOAD_TAGS[args.workload]) if fused
-                    else measured_traffic(["k_router.hip", "k_f32.hip"], "mot_translate_f32",
-                                          WORKLOAD_TAGS[args.workload]) if w.dtype == "f32"
+                    else measured_traffic(["k_f32_mfma.hip"] if f32_mfma else ["k_router.hip", "k_f32.hip"],
+                                          "mot_translate_f32", WORKLOAD_TAGS[args.workload]) if w.dtype == "f32"
                     else measured_traffic(["k_router.hip", "k_bf16_unfused.hip", "k_bf16_gemm256.hip"], "mot_translate_two_gemm",
                                           WORKLOAD_TAGS[args.workload])),
         "alg_flops_per_launch": flops,
