@@ -4,9 +4,12 @@
 // * k_topS_select: for each query position u, the S key positions v <= u
 //   with the largest head-averaged source attention A[b][u][v] (ties to the
 //   lower position), in ascending position order, padded with -1.  Radix
-//   select over order-preserving 32-bit keys: four 8-bit histogram passes
-//   find the S-th largest key, then one ordered pass keeps every larger key
-//   and the lowest-positioned equal ones.
+//   select over order-preserving 32-bit keys: a 1024-bin histogram of the
+//   top 10 bits finds the bin holding the S-th largest key; that bin's keys
+//   (a few dozen on attention rows) are ranked against each other for the
+//   exact key, or, past 256 of them, 8-bit radix passes over the lower bits
+//   finish the search; then one ordered pass keeps every larger key and the
+//   lowest-positioned equal ones.
 // * k_sparse_attn: attention of every query head of (b, u) over its key set
 //   (grouped-query: query head h reads KV head h / G).  Per KV head the
 //   workgroup computes scores^T = K_sel . Q^T on v_mfma_f32_16x16x32_bf16 with
@@ -47,13 +50,19 @@ __device__ __forceinline__ uint32_t order_key(float a) {
     return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
+constexpr int kSelBits = 10, kSelBins = 1 << kSelBits;   // first radix digit
+constexpr int kSelCand = 256;                              // boundary-bin keys ranked directly
+static_assert(kSelBins == 4 * 256, "four first-digit bins per thread");
+
 // grid (T, B), 256 threads; CACHE: the row's keys live in dynamic LDS (T words)
 // ahead of the per-chunk counts
 template <bool CACHE>
 __global__ __launch_bounds__(256) void k_topS_select(const float* A, int32_t* idx, int T, int S) {
     extern __shared__ uint32_t s_key[];
-    __shared__ uint32_t hist[256];
-    __shared__ uint32_t s_sel[3];
+    __shared__ uint32_t hist[kSelBins];
+    __shared__ uint32_t s_cand[kSelCand];
+    __shared__ uint32_t s_sel[3], s_wsum[4];
+    __shared__ int s_cnt;
     const int u = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
     const int n = u + 1;
     int32_t* out = idx + ((size_t)b * T + u) * S;
@@ -84,61 +93,144 @@ __global__ __launch_bounds__(256) void k_topS_select(const float* A, int32_t* id
         }
         __syncthreads();
     }
+    // first digit: the top kSelBits bits (sign, exponent and one mantissa bit)
+    constexpr int sh1 = 32 - kSelBits;
     auto key_at = [&](int v) -> uint32_t {
         if constexpr (CACHE) return s_key[v];
         else return order_key(row[v]);
     };
-    uint32_t prefix = 0, mask = 0;
-    int rem = S;   // keys still to choose among those matching the prefix
-    for (int shift = 24; shift >= 0; shift -= 8) {
-        hist[tid] = 0;
-        __syncthreads();
-        for (int v = tid; v < n; v += 256) {
-            const uint32_t k = key_at(v);
-            if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+    // 1024 bins: an attention row's keys crowd into a few exponents, and with
+    // an 8-bit first digit the boundary bin held ~70 keys and needed another
+    // full radix pass; with 10 bits it holds a few dozen, ranked directly.
+    if (tid < 64) s_cnt = 0;
+#pragma unroll
+    for (int i = 0; i < kSelBins / 256; ++i) hist[tid + 256 * i] = 0;
+    __syncthreads();
+    for (int v = tid; v < n; v += 256) atomicAdd(&hist[key_at(v) >> sh1], 1u);
+    __syncthreads();
+    {
+        // thread t holds bins 4t .. 4t+3: suffix sums over the threads (within
+        // each wave by shuffles, then the higher waves' totals) find the bin
+        // holding the S-th largest key
+        const int lane = tid & 63, wv = tid >> 6;
+        const uint32_t h0 = hist[4 * tid], h1 = hist[4 * tid + 1], h2 = hist[4 * tid + 2], h3 = hist[4 * tid + 3];
+        const uint32_t c = h0 + h1 + h2 + h3;
+        uint32_t suf = c;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const uint32_t t = __shfl_down(suf, off, 64);
+            if (lane + off < 64) suf += t;
         }
+        if (lane == 0) s_wsum[wv] = suf;
         __syncthreads();
-        if (tid < 64) {
-            // lane l holds bins 4l .. 4l+3; suffix sums over lanes find the
-            // bin holding the rem-th largest remaining key
-            const uint32_t h0 = hist[4 * tid], h1 = hist[4 * tid + 1], h2 = hist[4 * tid + 2],
-                           h3 = hist[4 * tid + 3];
-            const uint32_t c = h0 + h1 + h2 + h3;
-            uint32_t suf = c;
+        for (int q = wv + 1; q < 4; ++q) suf += s_wsum[q];
+        if (suf >= (uint32_t)S && suf - c < (uint32_t)S) {
+            uint32_t cum = suf - c;   // keys in bins above 4t+3
+            const uint32_t hb[4] = {h0, h1, h2, h3};
+            int d = 4 * tid;
+            uint32_t cnt = h0;
 #pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const uint32_t t = __shfl_down(suf, off, 64);
-                if (tid + off < 64) suf += t;
-            }
-            const unsigned long long bal = __ballot(suf >= (uint32_t)rem);   // lanes 0 .. L
-            const int L = 63 - __clzll(bal);
-            if (tid == L) {
-                uint32_t cum = suf - c;   // keys in bins above 4L+3
-                int d = 4 * L;
-                uint32_t cnt = h0;
-                const uint32_t hb[4] = {h0, h1, h2, h3};
-#pragma unroll
-                for (int q = 3; q >= 0; --q) {
-                    if (cum + hb[q] >= (uint32_t)rem) {
-                        d = 4 * L + q;
-                        cnt = hb[q];
-                        break;
-                    }
-                    cum += hb[q];
+            for (int q = 3; q >= 0; --q) {
+                if (cum + hb[q] >= (uint32_t)S) {
+                    d = 4 * tid + q;
+                    cnt = hb[q];
+                    break;
                 }
-                s_sel[0] = (uint32_t)d;
-                s_sel[1] = cum;
-                s_sel[2] = cnt;
+                cum += hb[q];
+            }
+            s_sel[0] = (uint32_t)d;
+            s_sel[1] = cum;
+            s_sel[2] = cnt;
+        }
+    }
+    __syncthreads();
+    const uint32_t d1 = s_sel[0], cnt1 = s_sel[2];
+    int rem = S - (int)s_sel[1];   // keys still to choose in the boundary bin
+    uint32_t prefix = d1 << sh1, mask = ~0u << sh1;
+    if (cnt1 != (uint32_t)rem) {   // uniform: not every key of the boundary bin is taken
+        if (cnt1 <= (uint32_t)kSelCand) {
+            // the boundary bin's keys, ranked against each other: the rem-th
+            // largest is the S-th largest of the row, and the keys equal to it
+            // that are taken are the first ones in position order
+            for (int v = tid; v < n; v += 256) {
+                const uint32_t k = key_at(v);
+                if ((k >> sh1) == d1) s_cand[atomicAdd(&s_cnt, 1)] = k;
+            }
+            __syncthreads();
+            if (tid < (int)cnt1) {
+                const uint32_t ki = s_cand[tid];
+                int gt = 0, eq = 0;
+                for (int j = 0; j < (int)cnt1; ++j) {
+                    const uint32_t kj = s_cand[j];
+                    gt += kj > ki;
+                    eq += kj == ki;
+                }
+                if (gt < rem && rem <= gt + eq) {   // every such thread writes the same pair
+                    s_sel[0] = ki;
+                    s_sel[1] = (uint32_t)(rem - gt);
+                }
+            }
+            __syncthreads();
+            prefix = s_sel[0];
+            mask = ~0u;
+            rem = (int)s_sel[1];
+        } else {
+            // many keys share the digit: 8-bit radix passes over the bits
+            // below it (a last digit that overlaps resolved bits is harmless:
+            // the prefix filter fixes them)
+            for (int sh = sh1; sh > 0;) {
+                sh = sh > 8 ? sh - 8 : 0;
+                const int shift = sh;
+                hist[tid] = 0;
+                __syncthreads();
+                for (int v = tid; v < n; v += 256) {
+                    const uint32_t k = key_at(v);
+                    if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+                }
+                __syncthreads();
+                if (tid < 64) {
+                    // lane l holds bins 4l .. 4l+3; suffix sums over lanes find the
+                    // bin holding the rem-th largest remaining key
+                    const uint32_t h0 = hist[4 * tid], h1 = hist[4 * tid + 1], h2 = hist[4 * tid + 2],
+                                   h3 = hist[4 * tid + 3];
+                    const uint32_t c = h0 + h1 + h2 + h3;
+                    uint32_t suf = c;
+#pragma unroll
+                    for (int off = 1; off < 64; off <<= 1) {
+                        const uint32_t t = __shfl_down(suf, off, 64);
+                        if (tid + off < 64) suf += t;
+                    }
+                    const unsigned long long bal = __ballot(suf >= (uint32_t)rem);   // lanes 0 .. L
+                    const int L = 63 - __clzll(bal);
+                    if (tid == L) {
+                        uint32_t cum = suf - c;   // keys in bins above 4L+3
+                        int d = 4 * L;
+                        uint32_t cnt = h0;
+                        const uint32_t hb[4] = {h0, h1, h2, h3};
+#pragma unroll
+                        for (int q = 3; q >= 0; --q) {
+                            if (cum + hb[q] >= (uint32_t)rem) {
+                                d = 4 * L + q;
+                                cnt = hb[q];
+                                break;
+                            }
+                            cum += hb[q];
+                        }
+                        s_sel[0] = (uint32_t)d;
+                        s_sel[1] = cum;
+                        s_sel[2] = cnt;
+                    }
+                }
+                __syncthreads();
+                const uint32_t d = s_sel[0], cnt = s_sel[2];
+                rem -= (int)s_sel[1];
+                prefix |= d << shift;
+                mask |= 255u << shift;
+                __syncthreads();
+                // every key of the boundary bin is taken: the digits below decide nothing
+                if (cnt == (uint32_t)rem) break;
             }
         }
-        __syncthreads();
-        const uint32_t d = s_sel[0], cnt = s_sel[2];
-        rem -= (int)s_sel[1];
-        prefix |= d << shift;
-        mask |= 255u << shift;
-        __syncthreads();
-        // every key of the boundary bin is taken: the digits below decide nothing
-        if (cnt == (uint32_t)rem) break;
     }
     // prefix is the S-th largest key on the resolved digits (k & mask): take
     // every key larger under the mask and the first rem equal ones in

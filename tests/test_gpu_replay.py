@@ -64,6 +64,22 @@ def test_topS_select_bit_exact(B, T, S, oracle_built):
     assert np.array_equal(got, want), int((got != want).sum())
 
 
+@pytest.mark.parametrize("values", [(0.25,), (0.25, 0.5), (0.3, 0.3000001, 0.7)])
+def test_topS_select_heavy_ties(values, oracle_built):
+    """Maps of one to three distinct values: the boundary bin of the first
+    radix digit holds more than 256 keys on the long rows (the kernel's radix
+    fallback) and fewer on the short ones (its direct ranking); the sets
+    follow the lower-position rule."""
+    from oracle import oracle_topS_select
+    B, T, S = 2, 700, 128
+    print("case select heavy ties", values, flush=True)
+    rng = np.random.default_rng(len(values))
+    A = np.asarray(values, np.float32)[rng.integers(0, len(values), (B, T, T))]
+    got = _gpu_select(A, S).cpu().numpy()
+    want = oracle_topS_select(A, S)
+    assert np.array_equal(got, want), int((got != want).sum())
+
+
 def test_topS_select_structured_map(oracle_built):
     from oracle import oracle_topS_select
     A = source_attention(2, 600, seed=1)
