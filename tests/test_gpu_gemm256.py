@@ -63,6 +63,10 @@ CASES = {
     "e16": (_w(E=16, hidden=64, H_src=8, H_tgt=2, D_tgt=128, T=1300, seed=22), np.array([2, 0, 1, 1], np.int32)),
     # an unmapped layer, d_out 512 = two output tiles
     "skip": (_w(H_tgt=4, D_tgt=128, E=2, hidden=1024, T=700, seed=23), np.array([1, -1, 0, 2], np.int32)),
+    # d_in = E * hidden = 64: two 32-wide K slices per product, fewer than the
+    # slices the pipeline keeps in flight (the prologue reloads the last one)
+    "short_k": (_w(L_src=2, L_tgt=3, H_src=1, D_src=64, H_tgt=1, D_tgt=64, E=1, hidden=64, B=4, T=4100, seed=25),
+                np.array([1, 0, 1], np.int32)),
 }
 
 
