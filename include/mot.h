@@ -96,7 +96,9 @@ typedef enum { MOT_ALGO_AUTO = 0, MOT_ALGO_UNFUSED = 1, MOT_ALGO_FUSED = 2, MOT_
  *                  256 pairs), and for top_k > 1 a combine sums each token's
  *                  top_k rows (workspace needed); MOT_ALGO_UNFUSED = router,
  *                  then two grouped GEMMs over every translator through a
- *                  hidden-activation workspace.  Requesting an impossible path
+ *                  hidden-activation workspace (the fp32 matrix-core GEMMs,
+ *                  used when hidden % 64 == 0, compute the router inside the
+ *                  first one).  Requesting an impossible path
  *                  returns MOT_ERR_UNSUPPORTED.  All paths compute the same
  *                  function.
  *   streams        2 (or 0): keys and values, each with its own translators;
