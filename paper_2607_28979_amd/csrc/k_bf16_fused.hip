@@ -35,7 +35,7 @@ hipError_t launch_shape(const Problem& p, const UnitTab& ut, bool routed, hipStr
 bool fused_supported(const Problem& p) {
     const bool din = p.d_in == 128 || p.d_in == 256 || p.d_in == 512;
     const bool dout = p.d_out == 128 || p.d_out == 256 || p.d_out == 512;
-    return din && dout && p.hidden % 32 == 0 && p.E * p.hidden >= 64 && p.E <= MOT_MAX_EXPERTS;
+    return din && dout && p.hidden % 64 == 0 && p.E * p.hidden >= 64 && p.E <= MOT_MAX_EXPERTS;
 }
 
 int fused_tile_rows(const Problem& p) {

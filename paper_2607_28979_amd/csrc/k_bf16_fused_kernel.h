@@ -149,6 +149,9 @@ __device__ __forceinline__ void load_lds16(rsrc_t r, uint32_t voff, uint32_t sof
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds_dst_wave_base, 16, voff, soff, 0, 0);
 }
 
+// 16 zero bytes: the layer-1 bias source when a call has no bias
+static __device__ __align__(16) const u32x4 kZero16 = {0u, 0u, 0u, 0u};
+
 // Per-lane choice between two registers as a bitwise blend, so the compiler
 // cannot fold it into a dynamically indexed (scratch) array access.
 __device__ __forceinline__ float pick(uint32_t mask, float a, float b) {
@@ -226,9 +229,11 @@ void k_bf16_fused(Problem p, UnitTab ut) {
 
     const uint16_t* W1u = reinterpret_cast<const uint16_t*>(p.w1) + um * hidden * D_IN;
     const uint16_t* W2u = reinterpret_cast<const uint16_t*>(p.w2) + um * D_OUT * hidden;
-    // layer-1 bias: without one, read W1 instead and mask the bits to zero
-    const uint16_t* b1u = p.b1 ? reinterpret_cast<const uint16_t*>(p.b1) + um * hidden : W1u;
-    const uint32_t b1_mask = p.b1 ? 0xFFFFFFFFu : 0u;
+    // layer-1 bias: without one, every lane reads the same 16 zero bytes
+    // (chunk and lane strides 0), so no mask is needed at the use
+    const uint16_t* b1u = p.b1 ? reinterpret_cast<const uint16_t*>(p.b1) + um * hidden
+                               : reinterpret_cast<const uint16_t*>(&kZero16);
+    const int b1_cstride = p.b1 ? 32 : 0;
     const uint16_t* b2u = p.b2 ? reinterpret_cast<const uint16_t*>(p.b2) + um * D_OUT : nullptr;
     const uint16_t* Wru = reinterpret_cast<const uint16_t*>(p.wr) + unit * E * D_IN;
 
@@ -418,12 +423,12 @@ void k_bf16_fused(Problem p, UnitTab ut) {
         const float* Gw = Gs + w * (MOT_MAX_EXPERTS * 32);
         // layer-1 biases enter as the accumulators' initial values: this lane's
         // rows 4*q4 + j of row half hh are hidden 8*q4 + 4*hh + j of the chunk
-        // (w1_perm), i.e. the 16 bytes at hidden 8*q4 of the chunk's b1.  Raw
-        // loads one chunk ahead; the mask (no bias) is applied only at the use
-        // in the next iteration, so nothing waits on these loads mid-iteration.
+        // (w1_perm), i.e. the 16 bytes at hidden 8*q4 of the chunk's b1, loaded
+        // one chunk ahead so nothing waits on these loads mid-iteration.
+        const int b1_lane = p.b1 ? 8 * q4 : 0;
         auto load_b1 = [&](int c, u32x4& bv) {
             typedef const __attribute__((address_space(1))) u32x4* gu128;
-            bv = *(gu128)(b1u + c * 32 + 8 * q4);
+            bv = *(gu128)(b1u + c * b1_cstride + b1_lane);
         };
         // W1 operand of (k-step s, row half hh) sits at W1c[abase[s & 3] +
         // hh*16*CPR1 + 16*(s >> 2)]: the swizzled chunk (4s + q4) ^ l16 splits
@@ -441,16 +446,26 @@ void k_bf16_fused(Problem p, UnitTab ut) {
         // operand reads run LOOK slots ahead.
         constexpr int NEA0 = C::L2W == 8 ? MOT_FUSED_PHASE_A12 : MOT_FUSED_PHASE_A;
         constexpr int NEA = NEA0 < 16 - C::NOFF ? NEA0 : 16 - C::NOFF;
-        auto l1_iter = [&](auto l1c, auto gc, int c, int m, const u32x4& bv,
+        auto l1_iter = [&](auto l1c, auto gc, auto pc, int c, int m, const u32x4& bv,
                            const f32x4 (&sp)[2][2], u32x4& bnext, int c_next,
                            f32x4 (&s)[2][2]) {
             constexpr bool do_l1 = decltype(l1c)::value, do_gelu = decltype(gc)::value;
+            // parity of c: a constant (0 or 1), which makes the LDS stage
+            // offsets immediates, or -1 for the parity of the run-time c
+            constexpr int P0 = decltype(pc)::value;
+            const int P = P0 >= 0 ? P0 : (c & 1);
             constexpr int NEAx = C::SPLIT ? 16 : NEA;
             constexpr int NM = 4 * KS2, LOOK = 4, GD = 3, NEB = 16 - C::NOFF - NEAx;
             static_assert(NEB >= 0, "phase split");
-            const u32x4* W1c = W1s + (c & 1) * C::W1_CH;
-            u32x4* Hw = Hs + ((c - 1) & 1) * C::H_CH + w * 128;
-            const float hg0 = 0.5f * Gw[m * 32 + l16], hg1 = 0.5f * Gw[m * 32 + 16 + l16];
+            const u32x4* W1c = W1s + P * C::W1_CH;
+            u32x4* Hw = Hs + (P ^ 1) * C::H_CH + w * 128;
+            // gates of the two token halves; the GELU stages take 1/g, kept
+            // finite: for a zero gate (a translator outside the Top-K) it is
+            // FLT_MAX, and the element's value is then 0, or below 1e-36 where
+            // e underflows (x above ~5)
+            const float gv0 = Gw[m * 32 + l16], gv1 = Gw[m * 32 + 16 + l16];
+            const float cg0 = fminf(__builtin_amdgcn_rcpf(gv0), 3.4028235e38f),
+                        cg1 = fminf(__builtin_amdgcn_rcpf(gv1), 3.4028235e38f);
             if constexpr (do_l1) load_b1(c_next, bnext);
             u32x4 a1[KS2][2];
             float h[2][2][4], gx[16], gt[16], gq[16];
@@ -470,19 +485,19 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                         gx[e] = sp[hh][th][jj];
                         gelu_stage1(gx[e], gt[e]);
                     } else if constexpr (st == 1) {
-                        gelu_stage2(gt[e], gq[e]);
+                        gelu_stage2_gated(gt[e], th ? cg1 : cg0, gq[e]);
                     } else {
-                        h[hh][th][jj] = gelu_stage3(gx[e], gq[e], th ? hg1 : hg0);
+                        h[hh][th][jj] = gx[e] * gq[e];
                     }
                 } else if constexpr (st == 0) {
-                    h[hh][th][jj] = 2.0f * (th ? hg1 : hg0) * sp[hh][th][jj];
+                    h[hh][th][jj] = (th ? gv1 : gv0) * sp[hh][th][jj];
                 }
             };
             // bias of rows 4*q4 + j of row half hh (zero without a bias)
             f32x4 binit[2];
 #pragma unroll
             for (int hh = 0; hh < 2; ++hh) {
-                const uint32_t w0 = bv[2 * hh] & b1_mask, w1 = bv[2 * hh + 1] & b1_mask;
+                const uint32_t w0 = bv[2 * hh], w1 = bv[2 * hh + 1];
                 binit[hh] = f32x4{bf16_lo(w0), bf16_hi(w0), bf16_lo(w1), bf16_hi(w1)};
             }
             // the GELU results of chunk c-1 into this wave's hidden tile
@@ -547,15 +562,15 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                                 gelu_stage1(v, gt[e]);
                                 asm volatile("" : "+v"(gt[e]));
                             } else if constexpr (k == g0 + GD) {
-                                gelu_stage2(gt[e], gq[e]);
+                                gelu_stage2_gated(gt[e], th ? cg1 : cg0, gq[e]);
                                 asm volatile("" : "+v"(gq[e]));
                             } else if constexpr (k == g0 + 2 * GD) {
-                                h[hh][th][jj] = gelu_stage3(gx[e], gq[e], th ? hg1 : hg0);
+                                h[hh][th][jj] = gx[e] * gq[e];
                             }
                         } else if constexpr (k == g0) {
                             float v = sp[hh][th][jj];
                             asm volatile("" : "+v"(v));
-                            h[hh][th][jj] = 2.0f * (th ? hg1 : hg0) * v;
+                            h[hh][th][jj] = (th ? gv1 : gv0) * v;
                         }
                     });
                 }
@@ -576,7 +591,7 @@ void k_bf16_fused(Problem p, UnitTab ut) {
                 constexpr int TH_OFF = 2 - C::NOFF / 4;
 #pragma unroll
                 for (int th = TH_OFF; th < 2; ++th)
-                    Xs[(c & 1) * C::X_CH + (w * (C::NOFF / 4) + th - TH_OFF) * 64 + lane] =
+                    Xs[P * C::X_CH + (w * (C::NOFF / 4) + th - TH_OFF) * 64 + lane] =
                         __builtin_bit_cast(u32x4, s[1][th]);
             }
         };
@@ -601,19 +616,50 @@ void k_bf16_fused(Problem p, UnitTab ut) {
         const std::integral_constant<bool, true> yes{};
         const std::integral_constant<bool, false> no{};
         // c = 0: layer 1 only; 1 .. nch-1: layer 1 and GELU; nch: GELU only;
-        // nch+1: barrier only (layer 2 of the last chunk runs on other waves)
-        sync_stage();
-        l1_iter(yes, no, 0, m1, bcur, s_prev, bnext, 1, s_new);
-        rotate();
-        for (int c = 1; c < nch; ++c) {
+        // nch+1: barrier only (layer 2 of the last chunk runs on other waves).
+        // nch is even (hidden % 64 == 0): after c = 0 the odd/even pairs
+        // alternate the bias and accumulator registers, and c = nch - 1 (odd)
+        // and c = nch close the walk.
+        const std::integral_constant<int, 0> even{};
+        const std::integral_constant<int, 1> odd{};
+        if constexpr (C::L2W == 8) {
+            // 12-wave form: one loop body, stage offsets from the parity of c
+            // (the odd/even pairs below measured 1.3 % slower at 256 -> 512)
             sync_stage();
-            l1_iter(yes, yes, c, m1, bcur, s_prev, bnext, c + 1 < nch ? c + 1 : nch - 1, s_new);
+            l1_iter(yes, no, even, 0, m1, bcur, s_prev, bnext, 1, s_new);
             rotate();
+            for (int c = 1; c < nch; ++c) {
+                sync_stage();
+                l1_iter(yes, yes, std::integral_constant<int, -1>{}, c, m1, bcur, s_prev, bnext,
+                        c + 1 < nch ? c + 1 : nch - 1, s_new);
+                rotate();
+                advance();
+            }
+            sync_stage();
+            l1_iter(no, yes, even, nch, m1, bcur, s_prev, bnext, nch - 1, s_new);
+            sync_stage();
+        } else {
+            // 8-wave forms: odd/even pairs with the stage offsets as immediates
+            // (2 % faster at 512 -> 512 than the single body)
+            sync_stage();
+            l1_iter(yes, no, even, 0, m1, bcur, s_prev, bnext, 1, s_new);
+            rotate();
+            int c = 1;
+            for (; c + 1 < nch; c += 2) {
+                sync_stage();
+                l1_iter(yes, yes, odd, c, m1, bcur, s_prev, bnext, c + 1, s_new);
+                advance();
+                sync_stage();
+                l1_iter(yes, yes, even, c + 1, m1, bnext, s_new, bcur, c + 2 < nch ? c + 2 : nch - 1, s_prev);
+                advance();
+            }
+            sync_stage();
+            l1_iter(yes, yes, odd, c, m1, bcur, s_prev, bnext, nch - 1, s_new);
             advance();
+            sync_stage();
+            l1_iter(no, yes, even, nch, m1, bnext, s_new, bcur, nch - 1, s_prev);
+            sync_stage();
         }
-        sync_stage();
-        l1_iter(no, yes, nch, m1, bcur, s_prev, bnext, nch - 1, s_new);
-        sync_stage();
         mid_barrier();   // the layer-2 waves' last iteration
     } else if (is_l2) {
         // ---------------------------------------------------------- layer 2

@@ -140,16 +140,15 @@ __device__ __forceinline__ float gelu_tanh(float x) {
     return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
-// The same function as gelu_half_scaled, split into three dependent stages
-// so a software pipeline can overlap the chains of several elements.
+// The same function with the gate g folded in, in three dependent stages so
+// a software pipeline can overlap the chains of several elements: stage 1
+// gives e, stage 2 gives r = g / (1 + e) as the reciprocal of cg (1 + e) with
+// cg = 1/g (kept finite), and stage 3 is the product g GELU(x) = x r.
 __device__ __forceinline__ void gelu_stage1(float x, float& e) {
     e = __builtin_amdgcn_exp2f(x * fmaf(x * x, MOT_GELU_K3, MOT_GELU_K1));
 }
-__device__ __forceinline__ void gelu_stage2(float e, float& r) {
-    r = __builtin_amdgcn_rcpf(fmaf(e, 0.5f, 0.5f));   // 2 / (1 + e)
-}
-__device__ __forceinline__ float gelu_stage3(float x, float r, float hg) {
-    return (hg * x) * r;
+__device__ __forceinline__ void gelu_stage2_gated(float e, float cg, float& r) {
+    r = __builtin_amdgcn_rcpf(fmaf(e, cg, cg));
 }
 
 }  // namespace mot
