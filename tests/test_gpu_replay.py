@@ -80,6 +80,19 @@ def test_topS_select_heavy_ties(values, oracle_built):
     assert np.array_equal(got, want), int((got != want).sum())
 
 
+@pytest.mark.parametrize("T", [2500, 2133])
+def test_topS_select_every_row_of_long_maps(T, oracle_built):
+    """Every row of maps of a few thousand positions (key caches of 10 and
+    8.5 KB; T = 2133 takes the unaligned key fill), against the oracle."""
+    from oracle import oracle_topS_select
+    print("case select long map T", T, flush=True)
+    rng = np.random.default_rng(T)
+    A = (np.round(rng.random((1, T, T)) * 64) / 64).astype(np.float32)
+    got = _gpu_select(A, 128).cpu().numpy()
+    want = oracle_topS_select(A, 128)
+    assert np.array_equal(got, want), int((got != want).sum())
+
+
 def test_topS_select_structured_map(oracle_built):
     from oracle import oracle_topS_select
     A = source_attention(2, 600, seed=1)
