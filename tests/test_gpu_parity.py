@@ -333,6 +333,37 @@ def test_empty_input_is_noop():
     assert gk.size == 0 and gv.size == 0
 
 
+SHORT_WALKS = [(di, do, E, h) for di, do in ((128, 128), (512, 512), (256, 512), (512, 256))
+               for E, h in ((1, 64), (1, 128), (3, 64))]
+
+
+@pytest.mark.parametrize("d_in,d_out,E,hidden", SHORT_WALKS,
+                         ids=["%dx%d-E%d-h%d" % c for c in SHORT_WALKS])
+def test_fused_short_walks(d_in, d_out, E, hidden, oracle_built):
+    """The fused kernel's shortest walks over E*hidden: 2, 4 and 6 chunks of
+    32, in the 8-wave forms (odd/even iteration pairs, the last odd iteration
+    alone) and the 12-wave form, dense and (E = 3, Top-2) on the routed tiles,
+    whose walk is one translator's hidden."""
+    from paper_2607_28979_amd.configs import Workload
+    w = Workload("short", "bf16", L_src=1, L_tgt=1, B=1, T=200, H_src=d_in // 128, D_src=128,
+                 H_tgt=d_out // 128, D_tgt=128, E=E, hidden=hidden, seed=d_in + d_out + E + hidden)
+    lm = np.zeros(1, np.int32)
+    cases = [(w, mb.ALGO_FUSED)] + ([(w.with_(top_k=2), mb.ALGO_ROUTED)] if E == 3 else [])
+    for wk, algo in cases:
+        print("case short walk", d_in, d_out, E, hidden, "algo", algo, "top_k", wk.top_k, flush=True)
+        inp = generate(wk)
+        gk, gv = run_gpu(wk, inp, lm, algo=algo)
+        rk, rv = _oracle_full(wk, inp, lm)
+        if wk.top_k:
+            for x, (g, r) in enumerate(((gk, rk), (gv, rv))):
+                gr, rr = unit_rows(g, wk, 0), unit_rows(r, wk, 0)
+                keep, _, _ = check_topk_rows(wk, inp, lm, 0, x, gr, rr)
+                assert rel_frob(gr[keep], rr[keep]) <= TOL["bf16"]
+        else:
+            assert max_unit_error(gk, gv, rk, rv, wk, lm) <= TOL["bf16"]
+            assert _max_row_error(gk, gv, rk, rv, wk, lm) <= ROW_TOL["bf16"]
+
+
 def test_fused_and_unfused_agree():
     w = _tiny(B=1, T=333, H_src=4, D_src=64, H_tgt=4, D_tgt=128, E=8, hidden=256)
     inp = generate(w)
