@@ -364,6 +364,31 @@ def test_fused_short_walks(d_in, d_out, E, hidden, oracle_built):
             assert _max_row_error(gk, gv, rk, rv, wk, lm) <= ROW_TOL["bf16"]
 
 
+@pytest.mark.parametrize("algo", [mb.ALGO_FUSED, mb.ALGO_ROUTED, mb.ALGO_UNFUSED])
+def test_gelu_without_biases(algo, oracle_built):
+    """No biases at all (b1, b2 and the router's NULL) with the GELU: the
+    fused kernel then reads one 16-byte zero constant as every layer-1 bias."""
+    w = _tiny(B=1, T=190, E=3, hidden=128)
+    if algo == mb.ALGO_ROUTED:
+        w = w.with_(top_k=2)
+    inp = generate(w)
+    for b in (inp.b1, inp.b2, inp.br):   # zero biases for the oracle and the Top-K row checks;
+        b[...] = 0                       # the library gets NULL pointers
+    lm = np.array([0, 2, 1, 1], np.int32)
+    print("case no biases, GELU, algo", algo, flush=True)
+    gk, gv = run_gpu(w, inp, lm, algo=algo, with_bias=False)
+    rk, rv = _oracle_full(w, inp, lm)
+    if w.top_k:
+        for j in range(w.L_tgt):
+            for x, (g, r) in enumerate(((gk, rk), (gv, rv))):
+                gr, rr = unit_rows(g, w, j), unit_rows(r, w, j)
+                keep, _, _ = check_topk_rows(w, inp, lm, j, x, gr, rr)
+                assert rel_frob(gr[keep], rr[keep]) <= TOL["bf16"]
+    else:
+        assert max_unit_error(gk, gv, rk, rv, w, lm) <= TOL["bf16"]
+        assert _max_row_error(gk, gv, rk, rv, w, lm) <= ROW_TOL["bf16"]
+
+
 def test_fused_and_unfused_agree():
     w = _tiny(B=1, T=333, H_src=4, D_src=64, H_tgt=4, D_tgt=128, E=8, hidden=256)
     inp = generate(w)
