@@ -485,6 +485,90 @@ __global__ __launch_bounds__(256, 1) void k_bf16_gemm2_256(Problem p, UnitTab ut
     }
 }
 
+// ---------------------------------------------------------------------------
+// MoT-h restoration (paper App. C.5) on the same tiles: per layer l,
+// out[t][o] = sum_k a[l][t][k] W[o][k] + b[o] with W^K rows (o < d_kv) and
+// W^V rows side by side.  d_kv % 256 == 0, so an output tile lies in one of
+// the two projections.  grid: x = (output tiles) x (token tiles) in dispatch
+// order, z = position in the layer list.  MFMA A = projection rows, B =
+// activation rows; each lane's four consecutive outputs of one token go to
+// the key or value cache as one 8-byte store in the target layout.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256, 1) void k_bf16_project_256(ProjProblem p) {
+    __shared__ u32x4 lds[kNST * kStage];
+    const int l = p.layers[blockIdx.z];
+    const int d_kv = p.d_kv, d_act = p.d_act;
+    int at, bt;
+    tile_of(blockIdx.x, 2 * d_kv / kTile, (p.n_tok + kTile - 1) / kTile, at, bt);
+    const int out0 = at * kTile, tok0 = bt * kTile;
+    const bool isv = out0 >= d_kv;
+    const int ok0 = isv ? out0 - d_kv : out0;   // first row of the tile in its projection
+    const uint16_t* W = reinterpret_cast<const uint16_t*>(isv ? p.wv : p.wk) + (size_t)l * d_kv * d_act;
+    const uint16_t* bias = reinterpret_cast<const uint16_t*>(isv ? p.bv : p.bk);
+    if (bias) bias += (size_t)l * d_kv;
+    const rsrc_t bufA = make_rsrc(W, (size_t)d_kv * d_act * 2);
+    const rsrc_t bufB = make_rsrc(reinterpret_cast<const uint16_t*>(p.act) + (size_t)l * p.n_tok * d_act,
+                                  (size_t)p.n_tok * d_act * 2);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int L = lane / kCPR;
+    const int c = (lane % kCPR) ^ swz(L);   // this lane's logical chunk, the same in each load
+    uint32_t voA[kNI], voB[kNI];
+#pragma unroll
+    for (int q = 0; q < kNI; ++q) {
+        const int r = kRPI * (wave * kNI + q) + L;
+        voA[q] = (uint32_t)(ok0 + r) * d_act * 2 + 16 * c;
+        voB[q] = (uint32_t)min(tok0 + r, p.n_tok - 1) * d_act * 2 + 16 * c;
+    }
+    auto slice = [&](int kt, uint32_t& sa, uint32_t& sb, uint32_t& vb) {
+        sa = (uint32_t)kt * kBK * 2;
+        sb = sa;
+        vb = 0;
+    };
+    // accumulators start at the bias: lane rows of block bm are outputs
+    // ok0 + wm*128 + bm*32 + 8*ii + 4*g + jj of the projection
+    const int wm = wave >> 1, wn = wave & 1, g = lane >> 5, l32 = lane & 31;
+    f32x16 acc[4][4];
+#pragma unroll
+    for (int bm = 0; bm < 4; ++bm) {
+        f32x16 init;
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii) {
+            u32x2 w = {0u, 0u};
+            if (bias) w = *reinterpret_cast<const u32x2*>(bias + ok0 + wm * 128 + bm * 32 + 8 * ii + 4 * g);
+            init[4 * ii + 0] = bf16_lo(w[0]);
+            init[4 * ii + 1] = bf16_hi(w[0]);
+            init[4 * ii + 2] = bf16_lo(w[1]);
+            init[4 * ii + 3] = bf16_hi(w[1]);
+        }
+#pragma unroll
+        for (int bn = 0; bn < 4; ++bn) acc[bm][bn] = init;
+    }
+
+    k_loop(lds, bufA, bufB, voA, voB, d_act / kBK, slice, acc);
+
+    uint16_t* dst = reinterpret_cast<uint16_t*>(isv ? p.dst_v : p.dst_k) + (size_t)l * p.n_tok * d_kv;
+#pragma unroll
+    for (int bn = 0; bn < 4; ++bn) {
+        const int tc = tok0 + wn * 128 + bn * 32 + l32;
+        if (tc >= p.n_tok) continue;
+        const int b = tc / p.T, t = tc % p.T;
+#pragma unroll
+        for (int bm = 0; bm < 4; ++bm) {
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii) {
+                const int ok = ok0 + wm * 128 + bm * 32 + 8 * ii + 4 * g;   // four outputs of one head
+                const int hh = ok / p.D_tgt, dd = ok % p.D_tgt;
+                const size_t off = p.dst_layout == MOT_LAYOUT_BTHD
+                                       ? (size_t)tc * d_kv + ok
+                                       : (((size_t)b * p.H_tgt + hh) * p.T + t) * p.D_tgt + dd;
+                const u32x2 w = {pack_bf16x2(acc[bm][bn][4 * ii], acc[bm][bn][4 * ii + 1]),
+                                 pack_bf16x2(acc[bm][bn][4 * ii + 2], acc[bm][bn][4 * ii + 3])};
+                *reinterpret_cast<u32x2*>(dst + off) = w;
+            }
+        }
+    }
+}
+
 }  // namespace
 
 // Large tiles pay when a launch has at least one round of workgroups.
@@ -520,6 +604,22 @@ bool bf16_routed_gemm_fits(const Problem& p) {
     const size_t w1 = (size_t)p.hidden * p.d_in * 2, src = (size_t)p.n_tok * p.d_in * 2;
     const size_t hb = (nk + 31) / 32 * 32 * p.hidden * 2, w2 = (size_t)p.hidden * p.d_out * 2;
     return p.E <= 16 && w1 < lim && src < lim && hb < lim && w2 < lim;
+}
+
+bool bf16_project_256_fits(const ProjProblem& p, int n_layers) {
+    const size_t lim = (size_t)1 << 31;
+    const long wgs = (long)(2 * p.d_kv / kTile) * ((p.n_tok + kTile - 1) / kTile) * n_layers;
+    // the biases are read four at a time (8 bytes); the API guarantees 2-byte alignment only
+    const bool bias8 = (reinterpret_cast<uintptr_t>(p.bk) & 7) == 0 && (reinterpret_cast<uintptr_t>(p.bv) & 7) == 0;
+    return p.d_kv % kTile == 0 && p.d_act % kBK == 0 && p.D_tgt % 4 == 0 && wgs >= 128 && bias8 &&
+           (size_t)p.n_tok * p.d_act * 2 < lim && (size_t)p.d_kv * p.d_act * 2 < lim;
+}
+
+hipError_t launch_bf16_project_256(const ProjProblem& p, int n_layers, hipStream_t stream) {
+    if (n_layers == 0 || p.n_tok == 0) return hipSuccess;
+    const dim3 grid((2 * p.d_kv / kTile) * ((p.n_tok + kTile - 1) / kTile), 1, n_layers);
+    hipLaunchKernelGGL(k_bf16_project_256, grid, dim3(256), 0, stream, p);
+    return hipGetLastError();
 }
 
 size_t bf16_routed_hidden_bytes(const Problem& p) {

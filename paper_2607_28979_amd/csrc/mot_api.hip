@@ -478,7 +478,8 @@ mot_status mot_restore_kv(const void* act, const int32_t* layer_map, const void*
     int n = 0;
     for (int l = 0; l < s->L; ++l)
         if (!layer_map || layer_map[l] >= 0) p.layers[n++] = l;
-    hipError_t e = launch_bf16_project(p, n, stream);
+    hipError_t e = bf16_project_256_fits(p, n) ? launch_bf16_project_256(p, n, stream)
+                                               : launch_bf16_project(p, n, stream);
     if (e != hipSuccess) return fail(MOT_ERR_HIP, "kernel launch: %s", hipGetErrorString(e));
     return MOT_OK;
 }

@@ -77,6 +77,10 @@ struct ProjProblem {
     int32_t layers[kMaxUnits];   // layers to restore, in launch order
 };
 hipError_t launch_bf16_project(const ProjProblem& p, int n_layers, hipStream_t stream);
+// The same on 256 x 256 tiles (k_bf16_gemm256.hip) when d_kv % 256 == 0 and
+// the launch fills at least half a round of the chip
+bool bf16_project_256_fits(const ProjProblem& p, int n_layers);
+hipError_t launch_bf16_project_256(const ProjProblem& p, int n_layers, hipStream_t stream);
 
 // Context replay attention (Top-S sparse, or full causal when idx == nullptr).
 struct ReplayProblem {

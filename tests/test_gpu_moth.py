@@ -101,6 +101,9 @@ RESTORE = [  # (L, B, T, d_act, H_tgt, D_tgt, layout, bias)
     (2, 1, 200, 192, 5, 40, 0, True),       # d_kv = 200: ragged output tile
     (2, 3, 70, 256, 5, 40, 1, False),
     (1, 1, 129, 1536, 4, 128, 0, True),     # Qwen2.5-7B K/V width from a 1536-wide activation
+    # launches of >= 128 workgroups with d_kv % 256 == 0: the 256 x 256-tile kernel, ragged token tiles
+    (4, 2, 2100, 512, 4, 128, 0, True),
+    (5, 1, 5000, 384, 2, 128, 1, False),
 ]
 
 
@@ -128,11 +131,12 @@ def test_restore_parity(case, oracle_built):
         assert ek <= TOL["bf16"] and ev <= TOL["bf16"], (case, l, ek, ev)
 
 
-@pytest.mark.parametrize("layout", [0, 1])
-def test_restore_identity_is_exact(layout):
+@pytest.mark.parametrize("layout,T,D", [(0, 190, 64), (1, 190, 64), (0, 8200, 128), (1, 8200, 128)])
+def test_restore_identity_is_exact(layout, T, D):
     """W^K = W^V = I, no bias: each output is one exact product plus zeros,
-    so K and V are the bf16 activation cut into heads, bit for bit."""
-    L, B, T, H, D = 2, 1, 190, 2, 64
+    so K and V are the bf16 activation cut into heads, bit for bit (T = 8200
+    with two heads of 128: the 256 x 256-tile kernel)."""
+    L, B, H = 2, 1, 2
     act = activations(L, B, T, H * D, seed=3)
     eye = np.broadcast_to(np.eye(H * D, dtype=np.float32), (L, H * D, H * D)).copy()
     gk, gv = _restore_gpu(act, None, eye, None, eye, None, L, B, T, H, D, layout)
